@@ -1,0 +1,278 @@
+/*
+ * flowmoe.h -- C ABI of the MoE-layer hot path (FlowMoE, arXiv 2510.00207).
+ *
+ * One MoE layer (Sec. 2.1): a linear gate with top-k softmax selection, the
+ * capacity-bounded dispatch into the expert-major all-to-all send layout
+ * G(I') (E x C x M, or its packed form), one two-layer FFN per expert, and the
+ * weighted combine back to T x M; plus the backward of each step, and the
+ * R-chunk two-stream schedule of Sec. 3.2 (Eqs. 3-6).
+ *
+ * Conventions for every call
+ *  - All tensor pointers are DEVICE pointers owned by the caller, row-major
+ *    and contiguous. The library never allocates or frees device memory and
+ *    never synchronises the device: work is enqueued on the stream(s) given.
+ *  - "layer dtype" tensors are float (FLOWMOE_F32) or bf16 bit patterns
+ *    (FLOWMOE_BF16, passed as uint16_t). Gate logits, gate weights, their
+ *    gradients and all weight gradients are always float. Accumulation is
+ *    always in float; bf16 results are rounded to nearest-even.
+ *  - Arguments are validated on the host before anything is enqueued; on a
+ *    non-OK status nothing was enqueued and flowmoe_last_error() (per host
+ *    thread) describes the problem. Launch failures return FLOWMOE_ERR_HIP.
+ *    Faults inside kernels surface at the caller's next synchronisation.
+ *  - Inputs must be finite; NaN/Inf inputs give unspecified results.
+ *  - Outputs are overwritten unless an `accumulate` flag is set.
+ *  - Results are deterministic: no floating-point atomics anywhere.
+ *  - Shapes: T tokens per call (one chunk), M model width, H expert hidden
+ *    width, E experts (1..64), k experts per token (1..min(E, 8)), C the
+ *    per-expert capacity (>= 0). M and H must be multiples of 8.
+ *
+ * Row buffers (x_disp, y_disp, dy_disp, dx_disp, h_save, a_save) hold
+ * flowmoe_rows_capacity(shape) rows: min(T*k, E*C) for the packed layout,
+ * E*C for the padded one. Expert e owns rows [offsets[e], offsets[e] +
+ * counts[e]). In the padded layout, rows between counts[e] and C are written
+ * as zeros by every producer; in the packed layout rows at or past
+ * offsets[E] are left untouched.
+ */
+#ifndef FLOWMOE_H
+#define FLOWMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FLOWMOE_OK = 0,
+  FLOWMOE_ERR_INVALID = 1,     /* bad argument or shape */
+  FLOWMOE_ERR_UNSUPPORTED = 2, /* valid, but not implemented (e.g. E > 64) */
+  FLOWMOE_ERR_HIP = 3,         /* a HIP runtime call failed */
+  FLOWMOE_ERR_WORKSPACE = 4    /* workspace missing or too small */
+} flowmoe_status_t;
+
+enum { FLOWMOE_F32 = 0, FLOWMOE_BF16 = 1 };      /* layer dtype */
+enum { FLOWMOE_GELU = 0, FLOWMOE_SWIGLU = 1 };   /* expert activation */
+enum { FLOWMOE_PACKED = 0, FLOWMOE_PADDED = 1 }; /* dispatch layout */
+
+/* Shape of one layer call (one chunk of T tokens). */
+typedef struct {
+  int32_t T, M, H, E, k, C;
+  int32_t dtype;  /* FLOWMOE_F32 | FLOWMOE_BF16 */
+  int32_t act;    /* FLOWMOE_GELU | FLOWMOE_SWIGLU */
+  int32_t layout; /* FLOWMOE_PACKED | FLOWMOE_PADDED */
+} flowmoe_shape_t;
+
+/* Workspace kinds for flowmoe_workspace_bytes(). */
+enum {
+  FLOWMOE_WS_DISPATCH = 0,
+  FLOWMOE_WS_FFN_BWD = 1,
+  FLOWMOE_WS_GATE_BWD = 2,
+  FLOWMOE_WS_LAYER_BWD = 3
+};
+
+/* ---- utilities ---------------------------------------------------------- */
+
+/* Library version string, e.g. "flowmoe 0.1.0 gfx950". */
+const char* flowmoe_version(void);
+
+/* Message of the last non-OK status returned on this host thread ("" if none). */
+const char* flowmoe_last_error(void);
+
+/* Expert capacity C = ceil(f * k * T / E) (Sec. 2.1, C = f*k*B*N/E), with a
+ * relative slack of 1e-9 so that products that are integers in decimal
+ * arithmetic (e.g. f = 1.1) are not rounded up by binary rounding error.
+ * Returns -1 for T < 0, E < 1, k < 1 or f <= 0. */
+int32_t flowmoe_capacity(int32_t T, int32_t E, int32_t k, double f);
+
+/* Rows of the dispatched buffers for `shape`: E*C (padded) or
+ * min(T*k, E*C) (packed). Returns -1 for an invalid shape. */
+int64_t flowmoe_rows_capacity(const flowmoe_shape_t* shape);
+
+/* Bytes of scratch the call of the given kind needs (0 = none). */
+size_t flowmoe_workspace_bytes(const flowmoe_shape_t* shape, int32_t kind);
+
+/* ---- forward (Sec. 2.1; one chunk's AT_r gating, D_r, E_r, C_r) ---------- */
+
+/* Gate: logits = x W_g (+ bias), the linear M x E gate of Sec. 4.2, then per
+ * token the k largest logits in descending order (ties to the lower expert
+ * index, -0.0 == +0.0) and their weights, the softmax over the k selected
+ * logits (the softmax of Sec. 2.1 renormalised over the selection).
+ *   x        T x M  layer dtype
+ *   w_gate   M x E  layer dtype
+ *   bias     E      float, nullable (constant per-expert logit offset)
+ *   logits   T x E  float (out)
+ *   topk_idx T x k  int32 (out)
+ *   topk_w   T x k  float (out) */
+flowmoe_status_t flowmoe_gate_topk(const flowmoe_shape_t* shape, const void* x,
+                                   const void* w_gate, const float* bias, float* logits,
+                                   int32_t* topk_idx, float* topk_w, hipStream_t stream);
+
+/* The selection and weights of flowmoe_gate_topk from given float logits
+ * (T x E); the same device routine. */
+flowmoe_status_t flowmoe_route(const flowmoe_shape_t* shape, const float* logits,
+                               int32_t* topk_idx, float* topk_w, hipStream_t stream);
+
+/* Dispatch (D_r): capacity-bounded positions and the token permutation into
+ * the expert-major send layout G(I') of Sec. 2.1. Assignments are ranked
+ * every first choice before any second choice, ascending token within a
+ * rank; assignment (t, j) is kept iff fewer than C earlier assignments chose
+ * the same expert. Then x_disp[slot[t][j]] = x[t] for every kept one.
+ *   topk_idx T x k int32 (in); an id outside [0, E) is treated as dropped
+ *   x        T x M layer dtype (in)
+ *   counts   E     int32 (out) kept rows per expert, min(demand, C)
+ *   offsets  E+1   int32 (out) first row of each expert: prefix sums of
+ *                  counts (packed) or e*C (padded); offsets[E] = end
+ *   slot     T x k int32 (out) row of assignment (t, j), or -1 if dropped
+ *   row_src  rows  int32 (out) t*k + j for the assignment in each row, -1
+ *                  for an empty row (rows = flowmoe_rows_capacity)
+ *   load     E     int32 (out, nullable) demand per expert before the drop
+ *   x_disp   rows x M layer dtype (out)
+ *   ws       workspace of flowmoe_workspace_bytes(shape, FLOWMOE_WS_DISPATCH) */
+flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* topk_idx,
+                                  const void* x, int32_t* counts, int32_t* offsets,
+                                  int32_t* slot, int32_t* row_src, int32_t* load,
+                                  void* x_disp, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Expert FFN (E_r), Sec. 2.1's two feed-forward layers M x H then H x M, on
+ * each expert's rows, as one grouped GEMM per layer:
+ *   GELU:   h = X W1_e,              a = gelu(h) (exact erf form)
+ *   SwiGLU: h1 = X W1_e, h3 = X W3_e, a = silu(h1) * h3
+ *   y_disp = a W2_e.
+ *   w1, w3   E x M x H layer dtype (w3 used only for SwiGLU, else nullable)
+ *   w2       E x H x M layer dtype
+ *   h_save   rows x H (GELU) or rows x 2H ([h1 | h3], SwiGLU) (out)
+ *   a_save   rows x H (out)  -- both kept for the backward
+ *   y_disp   rows x M (out) */
+flowmoe_status_t flowmoe_expert_ffn(const flowmoe_shape_t* shape, const void* x_disp,
+                                    const int32_t* counts, const int32_t* offsets,
+                                    const void* w1, const void* w3, const void* w2,
+                                    void* h_save, void* a_save, void* y_disp,
+                                    hipStream_t stream);
+
+/* Combine (C_r): y[t] = sum over kept j of topk_w[t][j] * y_disp[slot[t][j]],
+ * zero when no assignment of t is kept (Sec. 2.1). y is T x M layer dtype. */
+flowmoe_status_t flowmoe_combine(const flowmoe_shape_t* shape, const void* y_disp,
+                                 const int32_t* slot, const float* topk_w, void* y,
+                                 hipStream_t stream);
+
+/* ---- backward (reverse order, Eqs. 5-6) ----------------------------------- */
+
+/* Combine backward: dy_disp[slot] = topk_w * dy[t] and
+ * d_topk_w[t][j] = <dy[t], y_disp[slot[t][j]]> (0 for dropped assignments).
+ * counts/offsets give the padded rows to zero. */
+flowmoe_status_t flowmoe_combine_bwd(const flowmoe_shape_t* shape, const void* dy,
+                                     const void* y_disp, const int32_t* slot,
+                                     const float* topk_w, const int32_t* counts,
+                                     const int32_t* offsets, void* dy_disp, float* d_topk_w,
+                                     hipStream_t stream);
+
+/* Expert FFN backward: dA = dY W2_e^T, dW2_e = A^T dY; through the
+ * activation (GELU: dH = dA * gelu'(h); SwiGLU: dH1 = dA * h3 * silu'(h1),
+ * dH3 = dA * silu(h1)); dW1_e = X^T dH1, dW3_e = X^T dH3,
+ * dX = dH1 W1_e^T (+ dH3 W3_e^T).
+ *   dw1, dw3 E x M x H float; dw2 E x H x M float. With accumulate != 0 the
+ *   weight gradients are added to (sum over chunks, App. H), else written.
+ *   dx_disp rows x M layer dtype (out).
+ *   ws: flowmoe_workspace_bytes(shape, FLOWMOE_WS_FFN_BWD) bytes. */
+flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void* dy_disp,
+                                        const void* x_disp, const void* h_save,
+                                        const void* a_save, const int32_t* counts,
+                                        const int32_t* offsets, const void* w1,
+                                        const void* w3, const void* w2, void* dx_disp,
+                                        float* dw1, float* dw3, float* dw2, int32_t accumulate,
+                                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Dispatch backward: dx[t] = sum over kept j of dx_disp[slot[t][j]]
+ * (zero for a token with no kept assignment). dx is T x M layer dtype. */
+flowmoe_status_t flowmoe_dispatch_bwd(const flowmoe_shape_t* shape, const void* dx_disp,
+                                      const int32_t* slot, void* dx, hipStream_t stream);
+
+/* Gate backward: the softmax-over-selection Jacobian
+ * d_logits[t][S_j] = w_j * (dw_j - sum_j' w_j' dw_j'), zero off the
+ * selection; dw_gate = x^T d_logits (M x E float); dbias = column sums of
+ * d_logits (E float, nullable). If dx is given, dx += d_logits W_g^T
+ * (T x M layer dtype, read-modify-write). accumulate != 0 adds dw_gate and
+ * dbias to the existing values (sum over chunks).
+ *   ws: flowmoe_workspace_bytes(shape, FLOWMOE_WS_GATE_BWD) bytes. */
+flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void* x,
+                                       const void* w_gate, const int32_t* topk_idx,
+                                       const float* topk_w, const float* d_topk_w,
+                                       float* d_logits, float* dw_gate, float* dbias, void* dx,
+                                       int32_t accumulate, void* ws, size_t ws_bytes,
+                                       hipStream_t stream);
+
+/* ---- the R-chunk two-stream layer (Sec. 3.2, Eqs. 3-6) -------------------- */
+
+/* Buffers of a whole layer over R chunks of shape->T tokens each. Per-token
+ * tensors cover all R*T tokens; per-chunk tensors are R consecutive blocks
+ * (routing indices inside a block are chunk-local). rows = rows_capacity. */
+typedef struct {
+  /* parameters */
+  const void* w_gate; /* M x E */
+  const float* bias;  /* E, nullable */
+  const void* w1;     /* E x M x H */
+  const void* w3;     /* E x M x H, SwiGLU only */
+  const void* w2;     /* E x H x M */
+  /* forward */
+  const void* x;      /* RT x M */
+  float* logits;      /* RT x E */
+  int32_t* topk_idx;  /* RT x k */
+  float* topk_w;      /* RT x k */
+  int32_t* counts;    /* R x E */
+  int32_t* offsets;   /* R x (E+1) */
+  int32_t* slot;      /* RT x k */
+  int32_t* row_src;   /* R x rows */
+  int32_t* load;      /* R x E, nullable */
+  void* x_disp;       /* R x rows x M */
+  void* h_save;       /* R x rows x H (x2 for SwiGLU) */
+  void* a_save;       /* R x rows x H */
+  void* y_disp;       /* R x rows x M */
+  void* y;            /* RT x M */
+  /* backward */
+  const void* dy;     /* RT x M */
+  void* dy_disp;      /* R x rows x M */
+  float* d_topk_w;    /* RT x k */
+  void* dx_disp;      /* R x rows x M */
+  void* dx;           /* RT x M */
+  float* d_logits;    /* RT x E */
+  float* dw_gate;     /* M x E, summed over chunks */
+  float* dbias;       /* E, nullable */
+  float* dw1;         /* E x M x H, summed over chunks */
+  float* dw3;         /* E x M x H, SwiGLU only */
+  float* dw2;         /* E x H x M */
+  /* scratch */
+  void* ws;           /* flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD) */
+  size_t ws_bytes;
+} flowmoe_layer_bufs_t;
+
+/* Forward of R chunks. Compute stream gets AT_1..AT_R (gating) then
+ * E_1..E_R (experts) (Eq. 3); comm stream gets D_1..D_R then C_1..C_R
+ * (Eq. 4); events make D_r wait for AT_r, E_r for D_r and C_r for E_r.
+ * The call first makes s_comm wait for work already on s_compute and ends by
+ * making s_compute wait for s_comm, so to the caller it is one operation on
+ * s_compute. s_comm may equal s_compute (serial schedule, same results).
+ * trace (nullable): 8*R events, recorded at start/end of each task, at index
+ * 2*(task*R + r) (+1 for the end), task 0 = gate, 1 = dispatch,
+ * 2 = experts, 3 = combine. The events must be created by the caller. */
+flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
+                                   const flowmoe_layer_bufs_t* bufs, hipStream_t s_compute,
+                                   hipStream_t s_comm, hipEvent_t* trace);
+
+/* Backward of R chunks: comm stream gets C_R..C_1 (combine backward) then
+ * D_R..D_1 (dispatch backward) (Eq. 6); compute stream gets E_R..E_1 then
+ * AT_R..AT_1 (Eq. 5), with E_r after C_r, D_r after E_r, AT_r after D_r
+ * (constraints 6b-6d). Weight gradients are summed over chunks in that order.
+ * trace (nullable): 8*R events as for the forward, task 0 = combine bwd,
+ * 1 = experts bwd, 2 = dispatch bwd, 3 = gate bwd. */
+flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
+                                   const flowmoe_layer_bufs_t* bufs, hipStream_t s_compute,
+                                   hipStream_t s_comm, hipEvent_t* trace);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLOWMOE_H */

@@ -1,0 +1,576 @@
+// C ABI front end of libflowmoe: argument validation, status codes, workspace
+// queries, and the R-chunk two-stream layer schedule (Sec. 3.2, Eqs. 3-6).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <mutex>
+#include <vector>
+
+#include "common.hpp"
+
+using namespace flowmoe;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+flowmoe_status_t fail(flowmoe_status_t st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+flowmoe_status_t ok() {
+  g_err[0] = '\0';
+  return FLOWMOE_OK;
+}
+
+flowmoe_status_t hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(FLOWMOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+long rows_of(const flowmoe_shape_t* s) {
+  const long ec = (long)s->E * s->C;
+  if (s->layout == FLOWMOE_PADDED) return ec;
+  const long tk = (long)s->T * s->k;
+  return tk < ec ? tk : ec;
+}
+
+enum { NEED_H = 1, NEED_C = 2 };
+
+// Validate a shape; fills `out`. Returns OK or the failing status.
+flowmoe_status_t check_shape(const flowmoe_shape_t* s, int need, Shape* out) {
+  if (s == nullptr) return fail(FLOWMOE_ERR_INVALID, "shape is null");
+  if (s->dtype != FLOWMOE_F32 && s->dtype != FLOWMOE_BF16)
+    return fail(FLOWMOE_ERR_INVALID, "dtype %d is not FLOWMOE_F32 or FLOWMOE_BF16", s->dtype);
+  if (s->act != FLOWMOE_GELU && s->act != FLOWMOE_SWIGLU)
+    return fail(FLOWMOE_ERR_INVALID, "act %d is not FLOWMOE_GELU or FLOWMOE_SWIGLU", s->act);
+  if (s->layout != FLOWMOE_PACKED && s->layout != FLOWMOE_PADDED)
+    return fail(FLOWMOE_ERR_INVALID, "layout %d is not FLOWMOE_PACKED or FLOWMOE_PADDED", s->layout);
+  if (s->T < 0) return fail(FLOWMOE_ERR_INVALID, "T = %d < 0", s->T);
+  if (s->M < 8 || s->M % 8) return fail(FLOWMOE_ERR_INVALID, "M = %d must be a positive multiple of 8", s->M);
+  if (s->E < 1) return fail(FLOWMOE_ERR_INVALID, "E = %d < 1", s->E);
+  if (s->E > kMaxE) return fail(FLOWMOE_ERR_UNSUPPORTED, "E = %d > %d", s->E, kMaxE);
+  if (s->k < 1 || s->k > s->E) return fail(FLOWMOE_ERR_INVALID, "k = %d not in [1, E = %d]", s->k, s->E);
+  if (s->k > kMaxK) return fail(FLOWMOE_ERR_UNSUPPORTED, "k = %d > %d", s->k, kMaxK);
+  if ((need & NEED_H) && (s->H < 8 || s->H % 8))
+    return fail(FLOWMOE_ERR_INVALID, "H = %d must be a positive multiple of 8", s->H);
+  if ((need & NEED_C) && s->C < 0) return fail(FLOWMOE_ERR_INVALID, "C = %d < 0", s->C);
+  const long tk = (long)s->T * s->k;
+  if (tk > (1L << 30)) return fail(FLOWMOE_ERR_UNSUPPORTED, "T*k = %ld too large", tk);
+  if ((need & NEED_C) && (long)s->E * s->C > (1L << 30))
+    return fail(FLOWMOE_ERR_UNSUPPORTED, "E*C too large");
+  const long rows = (need & NEED_C) ? rows_of(s) : 0;
+  const long width = (need & NEED_H) ? 2L * (s->H > s->M ? s->H : s->M) : s->M;
+  if (rows * width > (1L << 40) || (long)s->T * s->M > (1L << 40))
+    return fail(FLOWMOE_ERR_UNSUPPORTED, "tensor too large");
+  if (out) {
+    out->T = s->T; out->M = s->M; out->H = s->H; out->E = s->E; out->k = s->k;
+    out->C = s->C; out->dtype = s->dtype; out->act = s->act; out->layout = s->layout;
+    out->rows = rows;
+  }
+  return FLOWMOE_OK;
+}
+
+#define REQUIRE(p, name) \
+  if ((p) == nullptr) return fail(FLOWMOE_ERR_INVALID, "%s is null", name)
+
+flowmoe_status_t check_ws(void* ws, size_t have, size_t need, const char* call) {
+  if (need == 0) return FLOWMOE_OK;
+  if (ws == nullptr || have < need)
+    return fail(FLOWMOE_ERR_WORKSPACE, "%s needs %zu workspace bytes, got %zu%s", call, need,
+                ws == nullptr ? (size_t)0 : have, ws == nullptr ? " (null)" : "");
+  return FLOWMOE_OK;
+}
+
+// per-thread, per-device pool of events for cross-stream ordering
+struct EventPool {
+  int device = -1;
+  std::vector<hipEvent_t> ev;
+};
+thread_local std::vector<EventPool> g_pools;
+
+hipError_t get_events(int n, hipEvent_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  EventPool* pool = nullptr;
+  for (auto& p : g_pools)
+    if (p.device == dev) pool = &p;
+  if (pool == nullptr) {
+    g_pools.push_back(EventPool());
+    pool = &g_pools.back();
+    pool->device = dev;
+  }
+  while ((int)pool->ev.size() < n) {
+    hipEvent_t h;
+    e = hipEventCreateWithFlags(&h, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+    pool->ev.push_back(h);
+  }
+  *out = pool->ev.data();
+  return hipSuccess;
+}
+
+inline const char* cptr(const void* p, long off) { return static_cast<const char*>(p) + off; }
+inline char* mptr(void* p, long off) { return p == nullptr ? nullptr : static_cast<char*>(p) + off; }
+
+}  // namespace
+
+extern "C" {
+
+const char* flowmoe_version(void) { return "flowmoe 0.1.0 gfx950"; }
+
+const char* flowmoe_last_error(void) { return g_err; }
+
+int32_t flowmoe_capacity(int32_t T, int32_t E, int32_t k, double f) {
+  if (T < 0 || E < 1 || k < 1 || !(f > 0.0)) return -1;
+  const double v = f * (double)k * (double)T / (double)E;
+  const double c = ceil(v - 1e-9 * (v > 1.0 ? v : 1.0));
+  if (c > 2147483647.0) return -1;
+  return c < 0 ? 0 : (int32_t)c;
+}
+
+int64_t flowmoe_rows_capacity(const flowmoe_shape_t* shape) {
+  Shape s;
+  if (check_shape(shape, NEED_C, &s) != FLOWMOE_OK) return -1;
+  return s.rows;
+}
+
+size_t flowmoe_workspace_bytes(const flowmoe_shape_t* shape, int32_t kind) {
+  Shape s;
+  if (check_shape(shape, NEED_H | NEED_C, &s) != FLOWMOE_OK) {
+    if (check_shape(shape, 0, &s) != FLOWMOE_OK) return 0;
+  }
+  switch (kind) {
+    case FLOWMOE_WS_DISPATCH: return 0;
+    case FLOWMOE_WS_FFN_BWD: return ffn_bwd_ws_bytes(s);
+    case FLOWMOE_WS_GATE_BWD: return gate_bwd_ws_bytes(s);
+    case FLOWMOE_WS_LAYER_BWD: {
+      const size_t a = ffn_bwd_ws_bytes(s), b = gate_bwd_ws_bytes(s);
+      return a > b ? a : b;
+    }
+    default: return 0;
+  }
+}
+
+flowmoe_status_t flowmoe_gate_topk(const flowmoe_shape_t* shape, const void* x,
+                                   const void* w_gate, const float* bias, float* logits,
+                                   int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, 0, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(w_gate, "w_gate");
+  if (s.T > 0) {
+    REQUIRE(x, "x");
+    REQUIRE(logits, "logits");
+    REQUIRE(topk_idx, "topk_idx");
+    REQUIRE(topk_w, "topk_w");
+  }
+  return hip_status(launch_gate_topk(s, x, w_gate, bias, logits, topk_idx, topk_w, stream),
+                    "flowmoe_gate_topk");
+}
+
+flowmoe_status_t flowmoe_route(const flowmoe_shape_t* shape, const float* logits,
+                               int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, 0, &s);
+  if (st != FLOWMOE_OK) return st;
+  if (s.T > 0) {
+    REQUIRE(logits, "logits");
+    REQUIRE(topk_idx, "topk_idx");
+    REQUIRE(topk_w, "topk_w");
+  }
+  return hip_status(launch_route(s, logits, topk_idx, topk_w, stream), "flowmoe_route");
+}
+
+flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* topk_idx,
+                                  const void* x, int32_t* counts, int32_t* offsets,
+                                  int32_t* slot, int32_t* row_src, int32_t* load, void* x_disp,
+                                  void* ws, size_t ws_bytes, hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, NEED_C, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(counts, "counts");
+  REQUIRE(offsets, "offsets");
+  if (s.T > 0) {
+    REQUIRE(topk_idx, "topk_idx");
+    REQUIRE(x, "x");
+    REQUIRE(slot, "slot");
+  }
+  if (s.rows > 0) {
+    REQUIRE(row_src, "row_src");
+    REQUIRE(x_disp, "x_disp");
+  }
+  (void)ws; (void)ws_bytes;
+  return hip_status(launch_dispatch(s, topk_idx, x, counts, offsets, slot, row_src, load, x_disp,
+                                    stream),
+                    "flowmoe_dispatch");
+}
+
+flowmoe_status_t flowmoe_expert_ffn(const flowmoe_shape_t* shape, const void* x_disp,
+                                    const int32_t* counts, const int32_t* offsets,
+                                    const void* w1, const void* w3, const void* w2,
+                                    void* h_save, void* a_save, void* y_disp,
+                                    hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, NEED_H | NEED_C, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(counts, "counts");
+  REQUIRE(offsets, "offsets");
+  REQUIRE(w1, "w1");
+  REQUIRE(w2, "w2");
+  if (s.act == FLOWMOE_SWIGLU) REQUIRE(w3, "w3");
+  if (s.rows > 0) {
+    REQUIRE(x_disp, "x_disp");
+    REQUIRE(h_save, "h_save");
+    REQUIRE(a_save, "a_save");
+    REQUIRE(y_disp, "y_disp");
+  }
+  return hip_status(launch_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save,
+                                      y_disp, stream),
+                    "flowmoe_expert_ffn");
+}
+
+flowmoe_status_t flowmoe_combine(const flowmoe_shape_t* shape, const void* y_disp,
+                                 const int32_t* slot, const float* topk_w, void* y,
+                                 hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, NEED_C, &s);
+  if (st != FLOWMOE_OK) return st;
+  if (s.T > 0) {
+    REQUIRE(slot, "slot");
+    REQUIRE(topk_w, "topk_w");
+    REQUIRE(y, "y");
+    if (s.rows > 0) REQUIRE(y_disp, "y_disp");
+  }
+  return hip_status(launch_combine(s, y_disp, slot, topk_w, y, stream), "flowmoe_combine");
+}
+
+flowmoe_status_t flowmoe_combine_bwd(const flowmoe_shape_t* shape, const void* dy,
+                                     const void* y_disp, const int32_t* slot,
+                                     const float* topk_w, const int32_t* counts,
+                                     const int32_t* offsets, void* dy_disp, float* d_topk_w,
+                                     hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, NEED_C, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(counts, "counts");
+  if (s.T > 0) {
+    REQUIRE(dy, "dy");
+    REQUIRE(slot, "slot");
+    REQUIRE(topk_w, "topk_w");
+    REQUIRE(d_topk_w, "d_topk_w");
+  }
+  if (s.rows > 0) {
+    REQUIRE(y_disp, "y_disp");
+    REQUIRE(dy_disp, "dy_disp");
+  }
+  return hip_status(launch_combine_bwd(s, dy, y_disp, slot, topk_w, counts, offsets, dy_disp,
+                                       d_topk_w, stream),
+                    "flowmoe_combine_bwd");
+}
+
+flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void* dy_disp,
+                                        const void* x_disp, const void* h_save,
+                                        const void* a_save, const int32_t* counts,
+                                        const int32_t* offsets, const void* w1,
+                                        const void* w3, const void* w2, void* dx_disp,
+                                        float* dw1, float* dw3, float* dw2, int32_t accumulate,
+                                        void* ws, size_t ws_bytes, hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, NEED_H | NEED_C, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(counts, "counts");
+  REQUIRE(offsets, "offsets");
+  REQUIRE(w1, "w1");
+  REQUIRE(w2, "w2");
+  REQUIRE(dw1, "dw1");
+  REQUIRE(dw2, "dw2");
+  if (s.act == FLOWMOE_SWIGLU) {
+    REQUIRE(w3, "w3");
+    REQUIRE(dw3, "dw3");
+  }
+  if (s.rows > 0) {
+    REQUIRE(dy_disp, "dy_disp");
+    REQUIRE(x_disp, "x_disp");
+    REQUIRE(h_save, "h_save");
+    REQUIRE(a_save, "a_save");
+    REQUIRE(dx_disp, "dx_disp");
+  }
+  st = check_ws(ws, ws_bytes, ffn_bwd_ws_bytes(s), "flowmoe_expert_ffn_bwd");
+  if (st != FLOWMOE_OK) return st;
+  return hip_status(launch_expert_ffn_bwd(s, dy_disp, x_disp, h_save, a_save, counts, offsets, w1,
+                                          w3, w2, dx_disp, dw1, dw3, dw2, accumulate != 0, ws,
+                                          stream),
+                    "flowmoe_expert_ffn_bwd");
+}
+
+flowmoe_status_t flowmoe_dispatch_bwd(const flowmoe_shape_t* shape, const void* dx_disp,
+                                      const int32_t* slot, void* dx, hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, NEED_C, &s);
+  if (st != FLOWMOE_OK) return st;
+  if (s.T > 0) {
+    REQUIRE(slot, "slot");
+    REQUIRE(dx, "dx");
+    if (s.rows > 0) REQUIRE(dx_disp, "dx_disp");
+  }
+  return hip_status(launch_dispatch_bwd(s, dx_disp, slot, dx, stream), "flowmoe_dispatch_bwd");
+}
+
+flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void* x,
+                                       const void* w_gate, const int32_t* topk_idx,
+                                       const float* topk_w, const float* d_topk_w,
+                                       float* d_logits, float* dw_gate, float* dbias, void* dx,
+                                       int32_t accumulate, void* ws, size_t ws_bytes,
+                                       hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, 0, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(w_gate, "w_gate");
+  REQUIRE(dw_gate, "dw_gate");
+  if (s.T > 0) {
+    REQUIRE(x, "x");
+    REQUIRE(topk_idx, "topk_idx");
+    REQUIRE(topk_w, "topk_w");
+    REQUIRE(d_topk_w, "d_topk_w");
+    REQUIRE(d_logits, "d_logits");
+  }
+  st = check_ws(ws, ws_bytes, gate_bwd_ws_bytes(s), "flowmoe_gate_topk_bwd");
+  if (st != FLOWMOE_OK) return st;
+  return hip_status(launch_gate_bwd(s, x, w_gate, topk_idx, topk_w, d_topk_w, d_logits, dw_gate,
+                                    dbias, dx, accumulate != 0, ws, stream),
+                    "flowmoe_gate_topk_bwd");
+}
+
+// ---------------------------------------------------------------------------
+// R-chunk layer
+// ---------------------------------------------------------------------------
+namespace {
+
+struct Chunk {
+  const char *x, *dy;
+  float *logits, *w, *dw, *dl;
+  int32_t *idx, *counts, *offsets, *slot, *row_src, *load;
+  char *x_disp, *h_save, *a_save, *y_disp, *y, *dy_disp, *dx_disp, *dx;
+};
+
+Chunk chunk_of(const Shape& s, const flowmoe_layer_bufs_t* b, int r) {
+  const long es = (long)esize(s.dtype);
+  const long T = s.T, M = s.M, E = s.E, k = s.k, rows = s.rows;
+  const long HW = (s.act == FLOWMOE_SWIGLU) ? 2L * s.H : s.H;
+  Chunk c;
+  c.x = b->x ? cptr(b->x, r * T * M * es) : nullptr;
+  c.dy = b->dy ? cptr(b->dy, r * T * M * es) : nullptr;
+  c.logits = b->logits ? b->logits + r * T * E : nullptr;
+  c.w = b->topk_w ? b->topk_w + r * T * k : nullptr;
+  c.dw = b->d_topk_w ? b->d_topk_w + r * T * k : nullptr;
+  c.dl = b->d_logits ? b->d_logits + r * T * E : nullptr;
+  c.idx = b->topk_idx ? b->topk_idx + r * T * k : nullptr;
+  c.counts = b->counts ? b->counts + r * E : nullptr;
+  c.offsets = b->offsets ? b->offsets + r * (E + 1) : nullptr;
+  c.slot = b->slot ? b->slot + r * T * k : nullptr;
+  c.row_src = b->row_src ? b->row_src + r * rows : nullptr;
+  c.load = b->load ? b->load + r * E : nullptr;
+  c.x_disp = mptr(b->x_disp, r * rows * M * es);
+  c.h_save = mptr(b->h_save, r * rows * HW * es);
+  c.a_save = mptr(b->a_save, r * rows * (long)s.H * es);
+  c.y_disp = mptr(b->y_disp, r * rows * M * es);
+  c.y = mptr(b->y, r * T * M * es);
+  c.dy_disp = mptr(b->dy_disp, r * rows * M * es);
+  c.dx_disp = mptr(b->dx_disp, r * rows * M * es);
+  c.dx = mptr(b->dx, r * T * M * es);
+  return c;
+}
+
+struct Sched {
+  hipStream_t sc, sm;
+  bool two;
+  hipEvent_t* trace;
+  int R;
+  hipError_t err = hipSuccess;
+  void mark(int task, int r, int end, hipStream_t st) {
+    if (trace != nullptr && err == hipSuccess)
+      err = hipEventRecord(trace[2 * (task * R + r) + end], st);
+  }
+  void signal(hipEvent_t ev, hipStream_t st) {
+    if (two && err == hipSuccess) err = hipEventRecord(ev, st);
+  }
+  void wait(hipStream_t st, hipEvent_t ev) {
+    if (two && err == hipSuccess) err = hipStreamWaitEvent(st, ev, 0);
+  }
+  void run(hipError_t e) {
+    if (err == hipSuccess) err = e;
+  }
+};
+
+flowmoe_status_t check_layer(const flowmoe_shape_t* shape, int32_t R, const flowmoe_layer_bufs_t* b,
+                             Shape* s) {
+  flowmoe_status_t st = check_shape(shape, NEED_H | NEED_C, s);
+  if (st != FLOWMOE_OK) return st;
+  if (b == nullptr) return fail(FLOWMOE_ERR_INVALID, "bufs is null");
+  if (R < 1) return fail(FLOWMOE_ERR_INVALID, "R = %d < 1", R);
+  if ((long)R * s->T > (1L << 30)) return fail(FLOWMOE_ERR_UNSUPPORTED, "R*T too large");
+  return FLOWMOE_OK;
+}
+
+}  // namespace
+
+flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
+                                   const flowmoe_layer_bufs_t* b, hipStream_t s_compute,
+                                   hipStream_t s_comm, hipEvent_t* trace) {
+  Shape s;
+  flowmoe_status_t st = check_layer(shape, R, b, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(b->w_gate, "bufs->w_gate");
+  REQUIRE(b->w1, "bufs->w1");
+  REQUIRE(b->w2, "bufs->w2");
+  REQUIRE(b->counts, "bufs->counts");
+  REQUIRE(b->offsets, "bufs->offsets");
+  if (s.act == FLOWMOE_SWIGLU) REQUIRE(b->w3, "bufs->w3");
+  if (s.T > 0) {
+    REQUIRE(b->x, "bufs->x"); REQUIRE(b->logits, "bufs->logits");
+    REQUIRE(b->topk_idx, "bufs->topk_idx"); REQUIRE(b->topk_w, "bufs->topk_w");
+    REQUIRE(b->slot, "bufs->slot"); REQUIRE(b->y, "bufs->y");
+  }
+  if (s.rows > 0) {
+    REQUIRE(b->row_src, "bufs->row_src"); REQUIRE(b->x_disp, "bufs->x_disp");
+    REQUIRE(b->h_save, "bufs->h_save"); REQUIRE(b->a_save, "bufs->a_save");
+    REQUIRE(b->y_disp, "bufs->y_disp");
+  }
+  Sched sc{s_compute, s_comm, s_comm != s_compute, trace, R};
+  hipEvent_t* ev = nullptr;
+  sc.run(get_events(3 * R + 2, &ev));
+  if (sc.err != hipSuccess) return hip_status(sc.err, "flowmoe_layer_fwd events");
+  hipEvent_t *evG = ev, *evD = ev + R, *evF = ev + 2 * R, evStart = ev[3 * R], evEnd = ev[3 * R + 1];
+  sc.signal(evStart, s_compute);
+  sc.wait(s_comm, evStart);
+  // AT_1..AT_R on the compute stream (gating part of AT_r)
+  for (int r = 0; r < R; ++r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.mark(0, r, 0, s_compute);
+    sc.run(launch_gate_topk(s, c.x, b->w_gate, b->bias, c.logits, c.idx, c.w, s_compute));
+    sc.mark(0, r, 1, s_compute);
+    sc.signal(evG[r], s_compute);
+  }
+  // D_1..D_R on the comm stream
+  for (int r = 0; r < R; ++r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.wait(s_comm, evG[r]);
+    sc.mark(1, r, 0, s_comm);
+    sc.run(launch_dispatch(s, c.idx, c.x, c.counts, c.offsets, c.slot, c.row_src, c.load, c.x_disp,
+                           s_comm));
+    sc.mark(1, r, 1, s_comm);
+    sc.signal(evD[r], s_comm);
+  }
+  // E_1..E_R on the compute stream
+  for (int r = 0; r < R; ++r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.wait(s_compute, evD[r]);
+    sc.mark(2, r, 0, s_compute);
+    sc.run(launch_expert_ffn(s, c.x_disp, c.counts, c.offsets, b->w1, b->w3, b->w2, c.h_save,
+                             c.a_save, c.y_disp, s_compute));
+    sc.mark(2, r, 1, s_compute);
+    sc.signal(evF[r], s_compute);
+  }
+  // C_1..C_R on the comm stream
+  for (int r = 0; r < R; ++r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.wait(s_comm, evF[r]);
+    sc.mark(3, r, 0, s_comm);
+    sc.run(launch_combine(s, c.y_disp, c.slot, c.w, c.y, s_comm));
+    sc.mark(3, r, 1, s_comm);
+  }
+  sc.signal(evEnd, s_comm);
+  sc.wait(s_compute, evEnd);
+  return hip_status(sc.err, "flowmoe_layer_fwd");
+}
+
+flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
+                                   const flowmoe_layer_bufs_t* b, hipStream_t s_compute,
+                                   hipStream_t s_comm, hipEvent_t* trace) {
+  Shape s;
+  flowmoe_status_t st = check_layer(shape, R, b, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE(b->w_gate, "bufs->w_gate");
+  REQUIRE(b->w1, "bufs->w1");
+  REQUIRE(b->w2, "bufs->w2");
+  REQUIRE(b->counts, "bufs->counts");
+  REQUIRE(b->offsets, "bufs->offsets");
+  REQUIRE(b->dw_gate, "bufs->dw_gate");
+  REQUIRE(b->dw1, "bufs->dw1");
+  REQUIRE(b->dw2, "bufs->dw2");
+  if (s.act == FLOWMOE_SWIGLU) {
+    REQUIRE(b->w3, "bufs->w3");
+    REQUIRE(b->dw3, "bufs->dw3");
+  }
+  if (s.T > 0) {
+    REQUIRE(b->x, "bufs->x"); REQUIRE(b->dy, "bufs->dy"); REQUIRE(b->topk_idx, "bufs->topk_idx");
+    REQUIRE(b->topk_w, "bufs->topk_w"); REQUIRE(b->slot, "bufs->slot");
+    REQUIRE(b->d_topk_w, "bufs->d_topk_w"); REQUIRE(b->d_logits, "bufs->d_logits");
+    REQUIRE(b->dx, "bufs->dx");
+  }
+  if (s.rows > 0) {
+    REQUIRE(b->x_disp, "bufs->x_disp"); REQUIRE(b->h_save, "bufs->h_save");
+    REQUIRE(b->a_save, "bufs->a_save"); REQUIRE(b->y_disp, "bufs->y_disp");
+    REQUIRE(b->dy_disp, "bufs->dy_disp"); REQUIRE(b->dx_disp, "bufs->dx_disp");
+  }
+  const size_t need = flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
+  st = check_ws(b->ws, b->ws_bytes, need, "flowmoe_layer_bwd");
+  if (st != FLOWMOE_OK) return st;
+  Sched sc{s_compute, s_comm, s_comm != s_compute, trace, R};
+  hipEvent_t* ev = nullptr;
+  sc.run(get_events(3 * R + 2, &ev));
+  if (sc.err != hipSuccess) return hip_status(sc.err, "flowmoe_layer_bwd events");
+  hipEvent_t *evC = ev, *evE = ev + R, *evD = ev + 2 * R, evStart = ev[3 * R], evEnd = ev[3 * R + 1];
+  sc.signal(evStart, s_compute);
+  sc.wait(s_comm, evStart);
+  // C_R..C_1 (combine backward) on the comm stream
+  for (int r = R - 1; r >= 0; --r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.mark(0, r, 0, s_comm);
+    sc.run(launch_combine_bwd(s, c.dy, c.y_disp, c.slot, c.w, c.counts, c.offsets, c.dy_disp, c.dw,
+                              s_comm));
+    sc.mark(0, r, 1, s_comm);
+    sc.signal(evC[r], s_comm);
+  }
+  // E_R..E_1 on the compute stream; weight gradients summed in that order
+  for (int r = R - 1; r >= 0; --r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.wait(s_compute, evC[r]);
+    sc.mark(1, r, 0, s_compute);
+    sc.run(launch_expert_ffn_bwd(s, c.dy_disp, c.x_disp, c.h_save, c.a_save, c.counts, c.offsets,
+                                 b->w1, b->w3, b->w2, c.dx_disp, b->dw1, b->dw3, b->dw2,
+                                 r != R - 1, b->ws, s_compute));
+    sc.mark(1, r, 1, s_compute);
+    sc.signal(evE[r], s_compute);
+  }
+  // D_R..D_1 (dispatch backward) on the comm stream
+  for (int r = R - 1; r >= 0; --r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.wait(s_comm, evE[r]);
+    sc.mark(2, r, 0, s_comm);
+    sc.run(launch_dispatch_bwd(s, c.dx_disp, c.slot, c.dx, s_comm));
+    sc.mark(2, r, 1, s_comm);
+    sc.signal(evD[r], s_comm);
+  }
+  // AT_R..AT_1 (gate backward, adds its share into dx) on the compute stream
+  for (int r = R - 1; r >= 0; --r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.wait(s_compute, evD[r]);
+    sc.mark(3, r, 0, s_compute);
+    sc.run(launch_gate_bwd(s, c.x, b->w_gate, c.idx, c.w, c.dw, c.dl, b->dw_gate, b->dbias, c.dx,
+                           r != R - 1, b->ws, s_compute));
+    sc.mark(3, r, 1, s_compute);
+  }
+  sc.signal(evEnd, s_comm);
+  sc.wait(s_compute, evEnd);
+  return hip_status(sc.err, "flowmoe_layer_bwd");
+}
+
+}  // extern "C"

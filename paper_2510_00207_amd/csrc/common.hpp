@@ -1,0 +1,120 @@
+// Shared device helpers and the internal launch interface of libflowmoe.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "flowmoe.h"
+
+namespace flowmoe {
+
+// ---------------------------------------------------------------------------
+// scalar element access for the two layer dtypes
+// ---------------------------------------------------------------------------
+typedef uint16_t bf16_t;  // bf16 bit pattern
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// round to nearest, ties to even (inputs finite)
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static __device__ __forceinline__ float load(const float* p) { return *p; }
+  static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
+};
+template <> struct Elem<bf16_t> {
+  static __device__ __forceinline__ float load(const bf16_t* p) { return bf16_to_f32(*p); }
+  static __device__ __forceinline__ void store(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+// 8 consecutive elements as float, from a 16-byte (bf16) or 2x16-byte (f32) load
+__device__ __forceinline__ void load8(const bf16_t* p, float v[8]) {
+  uint4 q = *reinterpret_cast<const uint4*>(p);
+  uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, float v[8]) {
+  float4 a = *reinterpret_cast<const float4*>(p);
+  float4 b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float v[8]) {
+  uint4 q;
+  q.x = pack_bf16x2(v[0], v[1]);
+  q.y = pack_bf16x2(v[2], v[3]);
+  q.z = pack_bf16x2(v[4], v[5]);
+  q.w = pack_bf16x2(v[6], v[7]);
+  *reinterpret_cast<uint4*>(p) = q;
+}
+__device__ __forceinline__ void store8(float* p, const float v[8]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+// activations (fp32); erff/expf are the device math library's
+__device__ __forceinline__ float gelu_f(float z) { return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f)); }
+__device__ __forceinline__ float gelu_grad_f(float z) {
+  return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) + z * 0.39894228040143268f * expf(-0.5f * z * z);
+}
+__device__ __forceinline__ float sigmoid_f(float z) { return 1.0f / (1.0f + expf(-z)); }
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+struct Shape {
+  int T, M, H, E, k, C, dtype, act, layout;
+  long rows;  // rows capacity of the dispatched buffers
+};
+
+constexpr int kMaxE = 64;
+constexpr int kMaxK = 8;
+
+// internal launchers (return hipSuccess or the launch error)
+hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, const float* bias,
+                            float* logits, int32_t* idx, float* w, hipStream_t st);
+hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float* w, hipStream_t st);
+hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, int32_t* counts,
+                           int32_t* offsets, int32_t* slot, int32_t* row_src, int32_t* load,
+                           void* x_disp, hipStream_t st);
+hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slot, const float* w,
+                          void* y, hipStream_t st);
+hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp,
+                              const int32_t* slot, const float* w, const int32_t* counts,
+                              const int32_t* offsets, void* dy_disp, float* dw, hipStream_t st);
+hipError_t launch_dispatch_bwd(const Shape& s, const void* dx_disp, const int32_t* slot, void* dx,
+                               hipStream_t st);
+size_t gate_bwd_ws_bytes(const Shape& s);
+hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const int32_t* idx,
+                           const float* w, const float* dw, float* d_logits, float* dw_gate,
+                           float* dbias, void* dx, int accumulate, void* ws, hipStream_t st);
+size_t ffn_bwd_ws_bytes(const Shape& s);
+hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* counts,
+                             const int32_t* offsets, const void* w1, const void* w3,
+                             const void* w2, void* h_save, void* a_save, void* y_disp,
+                             hipStream_t st);
+hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void* x_disp,
+                                 const void* h_save, const void* a_save, const int32_t* counts,
+                                 const int32_t* offsets, const void* w1, const void* w3,
+                                 const void* w2, void* dx_disp, float* dw1, float* dw3,
+                                 float* dw2, int accumulate, void* ws, hipStream_t st);
+
+inline size_t esize(int dtype) { return dtype == FLOWMOE_BF16 ? 2 : 4; }
+inline size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
+
+}  // namespace flowmoe

@@ -17,3 +17,13 @@ def pytest_configure(config):
 def rng():
     import numpy as np
     return np.random.Generator(np.random.PCG64(12345))
+
+
+@pytest.fixture(scope="session")
+def flowmoe_lib():
+    """The built libflowmoe (built in-tree first if it is missing)."""
+    from paper_2510_00207_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2510_00207_amd import build
+        build.build(verbose=False)
+    return _lib.load()

@@ -1,0 +1,77 @@
+"""Shared helpers for the GPU parity tests (imported by tests/test_gpu_*.py)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from moe_inputs import as_f64, make_inputs, to_torch
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}  # max relative error: max|g - r| / max|r|
+
+
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def max_rel_err(got, ref) -> float:
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    den = float(np.max(np.abs(ref))) if ref.size else 0.0
+    num = float(np.max(np.abs(got - ref))) if ref.size else 0.0
+    if den == 0.0:
+        return num
+    return num / den
+
+
+def assert_close(got, ref, dtype: str, what: str, tol: float | None = None):
+    t = TOL[dtype] if tol is None else tol
+    err = max_rel_err(got, ref)
+    assert err <= t, f"{what}: max rel err {err:.3e} > {t:.1e}"
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    """Device tensor -> float64 numpy (bf16 widened exactly)."""
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        t = t.float()
+    if t.dtype in (torch.int32, torch.int64):
+        return t.numpy().astype(np.int64)
+    return t.numpy().astype(np.float64)
+
+
+def load_layer(layer, inp):
+    """Copy generator inputs (storage form) into a MoELayer's tensors."""
+    d = layer.x.device
+    layer.x.copy_(to_torch(inp["x"], d))
+    layer.w_gate.copy_(to_torch(inp["w_gate"], d))
+    if inp.get("bias") is not None:
+        layer.bias.copy_(torch.from_numpy(inp["bias"]).to(d))
+    layer.w1.copy_(to_torch(inp["w1"], d))
+    if inp.get("w3") is not None:
+        layer.w3.copy_(to_torch(inp["w3"], d))
+    layer.w2.copy_(to_torch(inp["w2"], d))
+    if inp.get("dy") is not None:
+        layer.dy.copy_(to_torch(inp["dy"], d))
+
+
+def f64_inputs(inp):
+    return {k: (None if v is None else (v.astype(np.float64) if k == "bias" else as_f64(v)))
+            for k, v in inp.items()}
+
+
+def oracle_for_layer(layer_inp64, cfg, R, layout, gpu_logits):
+    """Oracle of the whole layer with routing taken from the GPU logits."""
+    return oracle.layer_fwd_bwd(layer_inp64, k=cfg.k, f=cfg.f, act=cfg.act, R=R, layout=layout,
+                                logits_for_routing=gpu_logits)
+
+
+__all__ = ["TOL", "need_gpu", "dev", "max_rel_err", "assert_close", "host", "load_layer",
+           "f64_inputs", "oracle_for_layer", "make_inputs"]

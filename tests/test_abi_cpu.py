@@ -1,0 +1,134 @@
+"""Host-side checks of the C ABI: every declared symbol is exported, host
+utilities agree with the oracle's definitions, and argument validation
+rejects bad calls before anything is enqueued (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2510_00207_amd import _lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "flowmoe.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(flowmoe_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_symbols_exported(flowmoe_lib):
+    names = declared_functions()
+    assert len(names) >= 16
+    raw = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+    assert L.flowmoe_version().startswith("flowmoe")
+
+
+def test_capacity_matches_oracle(flowmoe_lib):
+    for f in (0.5, 1.0, 1.1, 1.2, 1.25, 1.5, 2.0):
+        for T in (1, 7, 100, 500, 4096, 16384):
+            for E in (1, 3, 8, 10, 64):
+                for k in (1, 2, 6):
+                    assert L.flowmoe_capacity(T, E, k, f) == oracle.capacity(T, E, k, f), (T, E, k, f)
+    assert L.flowmoe_capacity(4096, 8, 2, 1.2) == 1229
+    assert L.flowmoe_capacity(-1, 8, 2, 1.2) == -1
+    assert L.flowmoe_capacity(8, 0, 2, 1.2) == -1
+    assert L.flowmoe_capacity(8, 8, 2, 0.0) == -1
+
+
+def test_rows_capacity(flowmoe_lib):
+    for layout in ("packed", "padded"):
+        for (T, E, k, C) in [(256, 4, 2, 160), (4096, 8, 2, 1229), (8192, 16, 1, 512), (10, 4, 2, 0)]:
+            s = L.make_shape(T, 64, 64, E, k, C, L.BF16, L.GELU, L.PADDED if layout == "padded" else L.PACKED)
+            assert L.flowmoe_rows_capacity(s) == oracle.rows_capacity(T, E, k, C, layout)
+
+
+def test_workspace_sizes(flowmoe_lib):
+    s = L.make_shape(4096, 1024, 4096, 8, 2, 1229, L.BF16, L.GELU, L.PACKED)
+    assert L.flowmoe_workspace_bytes(s, L.WS_DISPATCH) == 0
+    assert L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD) >= 8192 * 4096 * 2
+    assert L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD) >= 1024 * 8 * 4
+    assert L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD) == max(
+        L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD), L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD))
+    sw = L.make_shape(4096, 1024, 4096, 8, 2, 1229, L.BF16, L.SWIGLU, L.PACKED)
+    assert L.flowmoe_workspace_bytes(sw, L.WS_FFN_BWD) >= 8192 * 8192 * 2
+
+
+FAKE = 0x10000  # never dereferenced: every case below fails validation first
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("E", 0, L.ERR_INVALID), ("E", 65, L.ERR_UNSUPPORTED), ("k", 0, L.ERR_INVALID),
+    ("k", 9, L.ERR_INVALID), ("M", 12, L.ERR_INVALID), ("M", 0, L.ERR_INVALID),
+    ("T", -1, L.ERR_INVALID), ("dtype", 7, L.ERR_INVALID), ("act", 3, L.ERR_INVALID),
+    ("layout", 2, L.ERR_INVALID),
+])
+def test_gate_validation(flowmoe_lib, field, value, status):
+    s = L.make_shape(16, 64, 64, 4, 2, 8, L.BF16)
+    setattr(s, field, value)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_gate_topk(s, FAKE, FAKE, None, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == status
+    assert L.flowmoe_last_error()
+
+
+def test_k_above_8_unsupported(flowmoe_lib):
+    s = L.make_shape(16, 64, 64, 16, 9, 8, L.BF16)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_route(s, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == L.ERR_UNSUPPORTED
+
+
+def test_null_pointers_rejected(flowmoe_lib):
+    s = L.make_shape(16, 64, 64, 4, 2, 8, L.BF16)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_gate_topk(s, None, FAKE, None, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "x" in str(ei.value)
+    with pytest.raises(L.FlowMoEError):
+        L.flowmoe_dispatch(s, FAKE, FAKE, None, FAKE, FAKE, FAKE, None, FAKE, stream=0)
+    with pytest.raises(L.FlowMoEError):
+        L.flowmoe_combine(s, FAKE, None, FAKE, FAKE, stream=0)
+    sw = L.make_shape(16, 64, 64, 4, 2, 8, L.BF16, L.SWIGLU)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_expert_ffn(sw, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert "w3" in str(ei.value)
+
+
+def test_h_and_c_validation(flowmoe_lib):
+    s = L.make_shape(16, 64, 60, 4, 2, 8, L.BF16)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_expert_ffn(s, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "H" in str(ei.value)
+    s = L.make_shape(16, 64, 64, 4, 2, -1, L.BF16)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_dispatch(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID
+
+
+def test_workspace_checked_before_launch(flowmoe_lib):
+    s = L.make_shape(16, 64, 64, 4, 2, 8, L.BF16)
+    need = L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD)
+    assert need > 0
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_expert_ffn_bwd(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                                 None, FAKE, 0, None, 0, stream=0)
+    assert ei.value.status == L.ERR_WORKSPACE
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_gate_topk_bwd(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, FAKE, 1,
+                                stream=0)
+    assert ei.value.status == L.ERR_WORKSPACE
+
+
+def test_layer_validation(flowmoe_lib):
+    s = L.make_shape(16, 64, 64, 4, 2, 8, L.BF16)
+    b = L.LayerBufs()
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_layer_fwd(s, 0, b, s_compute=0, s_comm=0)
+    assert ei.value.status == L.ERR_INVALID
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_layer_fwd(s, 1, b, s_compute=0, s_comm=0)
+    assert "w_gate" in str(ei.value)

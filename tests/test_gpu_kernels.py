@@ -1,0 +1,243 @@
+"""Per-call parity of the C ABI entry points against the oracle step they
+implement, including edge cases: ties and signed zeros in the gate, T = 1,
+E = 1, k = E, C = 0, C >= T*k, heavy drops, multi-tile scans."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import assert_close, dev, host, need_gpu
+from moe_inputs import as_f64, get_config, make_inputs, to_torch
+from paper_2510_00207_amd import _lib as L
+
+pytestmark = pytest.mark.gpu
+
+
+def _shape(T, M, H, E, k, C, dtype="bf16", act="gelu", layout="packed"):
+    return L.make_shape(T, M, H, E, k, C, L.BF16 if dtype == "bf16" else L.F32,
+                        L.SWIGLU if act == "swiglu" else L.GELU,
+                        L.PADDED if layout == "padded" else L.PACKED)
+
+
+@pytest.mark.parametrize("E,k", [(1, 1), (3, 2), (4, 4), (8, 2), (16, 1), (33, 5), (64, 6), (64, 8)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gate_topk(E, k, dtype):
+    need_gpu()
+    cfg = get_config("balanced", T=300, M=136, H=8, E=E, k=k, dtype=dtype, seed=E * 10 + k)
+    inp = make_inputs(cfg, with_dy=False, x_zero_rows=[0, 7])
+    d = dev()
+    x, wg = to_torch(inp["x"], d), to_torch(inp["w_gate"], d)
+    bias = torch.linspace(-0.3, 0.3, E, device=d, dtype=torch.float32)
+    logits = torch.empty(cfg.T, E, device=d)
+    idx = torch.empty(cfg.T, k, dtype=torch.int32, device=d)
+    w = torch.empty(cfg.T, k, device=d)
+    s = _shape(cfg.T, cfg.M, 8, E, k, 0, dtype)
+    L.flowmoe_gate_topk(s, x, wg, bias, logits, idx, w)
+    torch.cuda.synchronize()
+    own = oracle.gate_logits(as_f64(inp["x"]), as_f64(inp["w_gate"]), host(bias))
+    gl = host(logits)
+    assert np.max(np.abs(gl - own)) <= 1e-4 * np.max(np.abs(own))
+    ref_i, ref_w = oracle.topk_select(gl, k)
+    assert np.array_equal(host(idx), ref_i)
+    np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
+    # zero tokens: logits equal the bias, selection by bias then index
+    assert np.allclose(gl[0], host(bias))
+
+
+def test_route_ties_and_signed_zeros():
+    need_gpu()
+    rng = np.random.default_rng(7)
+    d = dev()
+    for E in (2, 5, 8, 17, 64):
+        for k in sorted({1, min(E, 3), min(E, 8)}):
+            T = 257
+            L_ = (rng.integers(-3, 4, size=(T, E)) * 0.25).astype(np.float32)
+            z = L_ == 0
+            L_[z] = rng.choice(np.array([0.0, -0.0], np.float32), size=int(z.sum()))
+            L_[5, :] = 1.0                      # all equal
+            L_[6, :] = -0.0
+            lt = torch.from_numpy(L_).to(d)
+            idx = torch.empty(T, k, dtype=torch.int32, device=d)
+            w = torch.empty(T, k, device=d)
+            L.flowmoe_route(_shape(T, 8, 8, E, k, 0, "f32"), lt, idx, w)
+            torch.cuda.synchronize()
+            ref_i, ref_w = oracle.topk_select(L_.astype(np.float64), k)
+            assert np.array_equal(host(idx), ref_i), (E, k)
+            np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
+            assert list(host(idx)[5]) == list(range(k))
+
+
+def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t):
+    d = dev()
+    s = _shape(T, M, 8, E, k, C, "bf16" if x_t.dtype == torch.bfloat16 else "f32", layout=layout)
+    rows = L.flowmoe_rows_capacity(s)
+    counts = torch.full((E,), -7, dtype=torch.int32, device=d)
+    offsets = torch.full((E + 1,), -7, dtype=torch.int32, device=d)
+    slot = torch.full((max(T * k, 1),), -7, dtype=torch.int32, device=d)
+    row_src = torch.full((max(rows, 1),), -7, dtype=torch.int32, device=d)
+    load = torch.full((E,), -7, dtype=torch.int32, device=d)
+    x_disp = torch.full((max(rows, 1), M), 3.0, dtype=x_t.dtype, device=d)
+    idx_t = torch.from_numpy(idx_np.astype(np.int32)).to(d)
+    L.flowmoe_dispatch(s, idx_t, x_t, counts, offsets, slot, row_src, load, x_disp)
+    torch.cuda.synchronize()
+    return dict(counts=host(counts), offsets=host(offsets), slot=host(slot[:T * k]).reshape(T, k),
+                row_src=host(row_src[:rows]), load=host(load), x_disp=x_disp[:rows], rows=rows)
+
+
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+@pytest.mark.parametrize("T,E,k,cf", [
+    (1, 1, 1, 1.0), (1, 4, 2, 1.0), (37, 1, 1, 1.0), (100, 4, 4, 1.0), (300, 8, 2, 1.2),
+    (1000, 16, 1, 1.0), (2048, 64, 6, 1.5), (777, 7, 3, 0.3), (5000, 8, 2, 1.25),
+])
+def test_dispatch(T, E, k, cf, layout):
+    need_gpu()
+    rng = np.random.default_rng(T + E)
+    M = 72
+    # skewed logits so that some experts overflow
+    lg = rng.standard_normal((T, E)) + np.log(np.arange(1, E + 1))[::-1] * 0.7
+    idx, _ = oracle.topk_select(lg, k)
+    x = rng.standard_normal((T, M)).astype(np.float32)
+    x_t = torch.from_numpy(x).to(dev()).to(torch.bfloat16)
+    xb = host(x_t)
+    for C in sorted({0, 1, oracle.capacity(T, E, k, cf), T * k}):
+        g = _run_dispatch(T, M, E, k, C, layout, idx, x_t)
+        ref = oracle.route(idx, E, C, layout)
+        assert np.array_equal(g["counts"], ref["counts"]), C
+        assert np.array_equal(g["offsets"], ref["offsets"]), C
+        assert np.array_equal(g["slot"], ref["slot"]), C
+        assert np.array_equal(g["load"], ref["demand"]), C
+        live = ref["rows"] if layout == "padded" else int(ref["offsets"][-1])
+        assert np.array_equal(g["row_src"][:live], ref["row_src"][:live]), C
+        xd = oracle.dispatch(xb, ref["row_src"], k)
+        assert np.array_equal(host(g["x_disp"][:live]), xd[:live]), C
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+def test_expert_ffn_fwd_bwd(dtype, act, layout):
+    need_gpu()
+    rng = np.random.default_rng(3)
+    E, k, M, H = 6, 1, 200, 264
+    # per-expert counts spanning empty, tiny, tile-exact and ragged groups
+    cnt = np.array([0, 1, 127, 128, 129, 300])
+    C = 300
+    T = int(cnt.sum())
+    idx = np.repeat(np.arange(E), cnt)[:, None]
+    rt = oracle.route(idx, E, C, layout)
+    cfg = get_config("balanced", T=T, M=M, H=H, E=E, k=1, dtype=dtype, act=act, seed=11)
+    inp = make_inputs(cfg)
+    d = dev()
+    xb = as_f64(inp["x"])
+    x_disp64 = oracle.dispatch(xb, rt["row_src"], 1)
+    rows = rt["rows"]
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x_disp = torch.from_numpy(x_disp64).to(d).to(td)
+    counts = torch.from_numpy(rt["counts"].astype(np.int32)).to(d)
+    offsets = torch.from_numpy(rt["offsets"].astype(np.int32)).to(d)
+    w1 = to_torch(inp["w1"], d)
+    w3 = to_torch(inp["w3"], d) if act == "swiglu" else None
+    w2 = to_torch(inp["w2"], d)
+    HW = 2 * H if act == "swiglu" else H
+    h_save = torch.full((rows, HW), 5.0, dtype=td, device=d)
+    a_save = torch.full((rows, H), 5.0, dtype=td, device=d)
+    y_disp = torch.full((rows, M), 5.0, dtype=td, device=d)
+    s = _shape(T, M, H, E, 1, C, dtype, act, layout)
+    assert L.flowmoe_rows_capacity(s) == rows
+    L.flowmoe_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save, y_disp)
+    w64 = {kk: (None if inp[kk] is None else as_f64(inp[kk])) for kk in ("w1", "w3", "w2")}
+    ref = oracle.expert_ffn(x_disp64, rt["counts"], rt["offsets"], w64["w1"], w64["w3"], w64["w2"], act)
+    # backward with a seeded upstream gradient on the live rows
+    dy64 = rng.standard_normal((rows, M))
+    live = np.zeros(rows, bool)
+    for e in range(E):
+        live[rt["offsets"][e]:rt["offsets"][e] + rt["counts"][e]] = True
+    dy64[~live] = 0
+    dy_t = torch.from_numpy(dy64).to(d).to(td)
+    dy64 = host(dy_t)
+    dx_disp = torch.full((rows, M), 5.0, dtype=td, device=d)
+    dw1 = torch.full((E, M, H), 9.0, device=d)
+    dw3 = torch.full((E, M, H), 9.0, device=d) if act == "swiglu" else None
+    dw2 = torch.full((E, H, M), 9.0, device=d)
+    nws = L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD)
+    ws = torch.empty(nws, dtype=torch.uint8, device=d)
+    L.flowmoe_expert_ffn_bwd(s, dy_t, x_disp, h_save, a_save, counts, offsets, w1, w3, w2, dx_disp,
+                             dw1, dw3, dw2, 0, ws, nws)
+    # accumulate = 1 adds a second identical gradient
+    dw2b = dw2.clone()
+    torch.cuda.synchronize()
+    rdx, rdw1, rdw3, rdw2 = oracle.expert_ffn_bwd(dy64, x_disp64, ref, rt["counts"], rt["offsets"],
+                                                  w64["w1"], w64["w3"], w64["w2"], act)
+    nl = rows if layout == "padded" else int(rt["offsets"][-1])
+    hw = ref["h1"] if act == "gelu" else np.concatenate([ref["h1"], ref["h3"]], axis=1)
+    assert_close(host(h_save)[:nl], hw[:nl], dtype, "h_save")
+    assert_close(host(a_save)[:nl], ref["a"][:nl], dtype, "a_save")
+    assert_close(host(y_disp)[:nl], ref["y_disp"][:nl], dtype, "y_disp")
+    if layout == "padded":  # rows past each expert's count are zero
+        assert not host(y_disp)[~live].any() and not host(h_save)[~live].any()
+    assert_close(host(dx_disp)[:nl], rdx[:nl], dtype, "dx_disp")
+    assert_close(host(dw1), rdw1, dtype, "dw1")
+    assert_close(host(dw2), rdw2, dtype, "dw2")
+    if act == "swiglu":
+        assert_close(host(dw3), rdw3, dtype, "dw3")
+    L.flowmoe_expert_ffn_bwd(s, dy_t, x_disp, h_save, a_save, counts, offsets, w1, w3, w2, dx_disp,
+                             dw1, dw3, dw2, 1, ws, nws)
+    torch.cuda.synchronize()
+    assert torch.equal(dw2, 2 * dw2b)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+def test_combine_and_backward_steps(dtype, layout):
+    need_gpu()
+    rng = np.random.default_rng(5)
+    T, M, E, k = 333, 136, 8, 3
+    lg = rng.standard_normal((T, E))
+    idx, w = oracle.topk_select(lg, k)
+    C = oracle.capacity(T, E, k, 0.9)
+    rt = oracle.route(idx, E, C, layout)
+    rows = rt["rows"]
+    d = dev()
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    rnd = lambda *s: host(torch.from_numpy(rng.standard_normal(s)).to(d).to(td))
+    y_disp64, dy64, dx_disp64, x64 = rnd(rows, M), rnd(T, M), rnd(rows, M), rnd(T, M)
+    wg64 = host(torch.from_numpy(rng.standard_normal((M, E)) * 0.05).to(d).to(td))
+    t = lambda a, dt=td: torch.from_numpy(np.ascontiguousarray(a)).to(d).to(dt)
+    s = _shape(T, M, 8, E, k, C, dtype, layout=layout)
+    slot = t(rt["slot"], torch.int32)
+    counts = t(rt["counts"], torch.int32)
+    offsets = t(rt["offsets"], torch.int32)
+    w_t = t(w, torch.float32)
+    y = torch.empty(T, M, dtype=td, device=d)
+    L.flowmoe_combine(s, t(y_disp64), slot, w_t, y)
+    dy_disp = torch.full((rows, M), 7.0, dtype=td, device=d)
+    dtw = torch.empty(T, k, device=d)
+    L.flowmoe_combine_bwd(s, t(dy64), t(y_disp64), slot, w_t, counts, offsets, dy_disp, dtw)
+    dx = torch.empty(T, M, dtype=td, device=d)
+    L.flowmoe_dispatch_bwd(s, t(dx_disp64), slot, dx)
+    torch.cuda.synchronize()
+    assert_close(host(y), oracle.combine(y_disp64, rt["slot"], w), dtype, "y")
+    rdy, rdw = oracle.combine_bwd(dy64, y_disp64, rt["slot"], w)
+    live = rows if layout == "padded" else int(rt["offsets"][-1])
+    assert_close(host(dy_disp)[:live], rdy[:live], dtype, "dy_disp")
+    assert_close(host(dtw), rdw, dtype, "d_topk_w")
+    rdx = oracle.dispatch_bwd(dx_disp64, rt["slot"])
+    assert_close(host(dx), rdx, dtype, "dx")
+    # gate backward, with dx accumulation and chunk accumulation of dW_g
+    dlog = torch.empty(T, E, device=d)
+    dwg = torch.full((M, E), 3.0, device=d)
+    db = torch.full((E,), 3.0, device=d)
+    nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
+    ws = torch.empty(nws, dtype=torch.uint8, device=d)
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), t(idx, torch.int32), w_t, dtw, dlog, dwg, db, dx, 0,
+                            ws, nws)
+    torch.cuda.synchronize()
+    g = oracle.gate_bwd(x64, wg64, idx, w, host(dtw))
+    assert_close(host(dlog), g["d_logits"], dtype, "d_logits")
+    assert_close(host(dwg), g["dw_gate"], dtype, "dw_gate")
+    assert_close(host(db), g["dbias"], dtype, "dbias")
+    assert_close(host(dx), rdx + g["dx_gate"], dtype, "dx + gate")
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), t(idx, torch.int32), w_t, dtw, dlog, dwg, db, None, 1,
+                            ws, nws)
+    torch.cuda.synchronize()
+    assert_close(host(dwg), 2 * g["dw_gate"], dtype, "dw_gate accumulated")

@@ -1,0 +1,115 @@
+"""Whole-layer parity: flowmoe_layer_fwd / flowmoe_layer_bwd (R chunks, two
+streams) against the fp64 oracle, on seeded inputs spanning several tiles with
+ragged tails. Routing (indices, counts, offsets, slots, permutation) must be
+bit-exact against the oracle run on the GPU's fp32 logits; floating-point
+outputs within 1e-4 (fp32) / 2e-2 (bf16) max relative error."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import (assert_close, dev, f64_inputs, host, load_layer, need_gpu,
+                         oracle_for_layer)
+from moe_inputs import get_config, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+# reduced versions of the five workloads (same E, k, f, act, dtype, R), sized
+# for the oracle; H and M are chosen to leave ragged GEMM tiles
+CASES = {
+    "tiny": get_config("tiny"),
+    "balanced_s": get_config("balanced", T=512, M=256, H=392),
+    "skewed_s": get_config("skewed", T=1024, M=256, H=256),
+    "large_s": get_config("large", T=512, M=512, H=456),
+    "fine_s": get_config("fine", T=1024, M=256, H=176),
+}
+
+
+def run_layer(cfg, layout, R=None, two_streams=True, inp=None):
+    from paper_2510_00207_amd.layer import MoELayer
+    R = cfg.R if R is None else R
+    inp = make_inputs(cfg) if inp is None else inp
+    layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
+                     dtype=cfg.dtype, layout=layout, bias=cfg.zipf_bias, device=dev())
+    load_layer(layer, inp)
+    sc = torch.cuda.current_stream()
+    sm = torch.cuda.Stream() if two_streams else sc
+    layer.forward(sc, sm)
+    layer.backward(sc, sm)
+    torch.cuda.synchronize()
+    return layer, inp
+
+
+def check_against_oracle(cfg, layout, layer, inp, R):
+    i64 = f64_inputs(inp)
+    gl = host(layer.logits)
+    ref = oracle_for_layer(i64, cfg, R, layout, gl)
+    dt = cfg.dtype
+    # gate logits vs the oracle's own fp64 logits
+    own = oracle.gate_logits(i64["x"], i64["w_gate"], i64["bias"])
+    dl = np.max(np.abs(gl - own))
+    assert dl <= 1e-4 * np.max(np.abs(own)), f"logits off by {dl}"
+    # routing is a function of the fp32 logits: bit-exact
+    assert np.array_equal(host(layer.topk_idx), ref["topk_idx"])
+    np.testing.assert_allclose(host(layer.topk_w), ref["topk_w"], rtol=2e-6, atol=2e-7)
+    Tr = cfg.T // R
+    for r, c in enumerate(ref["chunks"]):
+        assert np.array_equal(host(layer.counts[r]), c["counts"]), f"counts chunk {r}"
+        assert np.array_equal(host(layer.offsets[r]), c["offsets"]), f"offsets chunk {r}"
+        assert np.array_equal(host(layer.load[r]), c["demand"]), f"load chunk {r}"
+        assert np.array_equal(host(layer.slot[r * Tr:(r + 1) * Tr]), c["slot"]), f"slot chunk {r}"
+        live = c["rows"] if layout == "padded" else int(c["offsets"][-1])
+        assert np.array_equal(host(layer.row_src[r][:c["rows"]])[:live], c["row_src"][:live])
+        # dispatch is an exact copy
+        assert np.array_equal(host(layer.x_disp[r][:live]), c["x_disp"][:live]), f"x_disp chunk {r}"
+        hw = c["h1"] if cfg.act == "gelu" else np.concatenate([c["h1"], c["h3"]], axis=1)
+        assert_close(host(layer.h_save[r][:live]), hw[:live], dt, f"h_save[{r}]")
+        assert_close(host(layer.a_save[r][:live]), c["a"][:live], dt, f"a_save[{r}]")
+        assert_close(host(layer.y_disp[r][:live]), c["y_disp"][:live], dt, f"y_disp[{r}]")
+        assert_close(host(layer.dy_disp[r][:live]), c["dy_disp"][:live], dt, f"dy_disp[{r}]")
+        assert_close(host(layer.dx_disp[r][:live]), c["dx_disp"][:live], dt, f"dx_disp[{r}]")
+    assert_close(host(layer.y), ref["y"], dt, "y")
+    assert_close(host(layer.d_topk_w), ref["d_topk_w"], dt, "d_topk_w")
+    assert_close(host(layer.d_logits), ref["d_logits"], dt, "d_logits")
+    assert_close(host(layer.dx), ref["dx"], dt, "dx")
+    assert_close(host(layer.dw_gate), ref["dw_gate"], dt, "dw_gate")
+    if cfg.zipf_bias:
+        assert_close(host(layer.dbias), ref["dbias"], dt, "dbias")
+    assert_close(host(layer.dw1), ref["dw1"], dt, "dw1")
+    assert_close(host(layer.dw2), ref["dw2"], dt, "dw2")
+    if cfg.act == "swiglu":
+        assert_close(host(layer.dw3), ref["dw3"], dt, "dw3")
+    return ref
+
+
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+@pytest.mark.parametrize("name", list(CASES))
+def test_layer_parity(name, layout):
+    need_gpu()
+    cfg = CASES[name]
+    print(f"[layer] {name} {layout} R={cfg.R}", flush=True)
+    layer, inp = run_layer(cfg, layout)
+    check_against_oracle(cfg, layout, layer, inp, cfg.R)
+
+
+@pytest.mark.parametrize("R", [1, 2, 4])
+def test_layer_chunks(R):
+    need_gpu()
+    cfg = CASES["balanced_s"]
+    print(f"[layer] chunks R={R}", flush=True)
+    layer, inp = run_layer(cfg, "packed", R=R)
+    check_against_oracle(cfg, "packed", layer, inp, R)
+
+
+def test_two_streams_equal_one_stream_and_deterministic():
+    need_gpu()
+    cfg = CASES["fine_s"]
+    inp = make_inputs(cfg)
+    a, _ = run_layer(cfg, "packed", two_streams=True, inp=inp)
+    b, _ = run_layer(cfg, "packed", two_streams=False, inp=inp)
+    c, _ = run_layer(cfg, "packed", two_streams=True, inp=inp)
+    for name in ("logits", "topk_idx", "topk_w", "slot", "x_disp", "h_save", "a_save", "y_disp", "y",
+                 "dy_disp", "d_topk_w", "dx_disp", "dx", "d_logits", "dw_gate", "dw1", "dw3", "dw2"):
+        ta, tb, tc = getattr(a, name), getattr(b, name), getattr(c, name)
+        assert torch.equal(ta, tb), f"{name}: two streams differ from one"
+        assert torch.equal(ta, tc), f"{name}: not deterministic"
