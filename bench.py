@@ -1,0 +1,204 @@
+"""Benchmark: MoE-layer forward + backward throughput on one MI355X.
+
+One step = one pass of the whole hot path over one batch: gate + top-k,
+capacity-bounded dispatch, grouped-GEMM experts, combine (forward), then
+combine backward, expert backward (dgrad + wgrad), dispatch backward and gate
+backward, through flowmoe_layer_fwd / flowmoe_layer_bwd on two HIP streams.
+
+Workload: the balanced MoE layer, T = 4096 tokens (8 x 512), M = 1024,
+H = 4096, E = 8, top-2, capacity factor 1.2, GELU experts, bf16 storage with
+fp32 accumulation, one chunk (R = 1), packed dispatch layout. Inputs are
+seeded synthetic tensors already resident in HBM.
+
+Prints one JSON line with tokens/s, the grouped-GEMM roofline (algorithmic
+FLOPs per launch over the average launch time, from HIP events recorded
+around every GEMM launch of the timed steps) and the fp64 CPU oracle timed on
+one full step of the same inputs.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+WORKLOAD = "balanced"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=WORKLOAD,
+                    help="balanced (default) | skewed | large | fine | tiny")
+    ap.add_argument("--layout", default="packed")
+    ap.add_argument("--R", type=int, default=None, help="override the chunk count")
+    ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def gemm_flops_per_launch(cfg, kept: int) -> float:
+    """Algorithmic FLOPs of one grouped-GEMM launch: every expert GEMM of the
+    layer multiplies the kept rows by an M x H (or H x M) weight, so each
+    launch does 2 * kept * M * H (SwiGLU's fused W1|W3 launch, its
+    [dW1 | dW3] launch and its K = 2H dgrad launch do twice that)."""
+    return 2.0 * kept * cfg.M * cfg.H
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {a.gpus}); the multi-GPU expert-parallel "
+              "path is not part of this build", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from moe_inputs import get_config, make_inputs, to_torch
+    from paper_2510_00207_amd import _lib as L
+    from paper_2510_00207_amd.hiprt import EventArray
+    from paper_2510_00207_amd.layer import MoELayer
+
+    if not os.path.exists(L.LIB_PATH):
+        from paper_2510_00207_amd import build
+        build.build(verbose=False)
+    L.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+
+    cfg = get_config(a.workload)
+    R = cfg.R if a.R is None else a.R
+    inp = make_inputs(cfg)
+    layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
+                     dtype=cfg.dtype, layout=a.layout, bias=cfg.zipf_bias, device=dev)
+    for name in ("x", "w_gate", "w1", "w3", "w2", "dy"):
+        if inp[name] is not None:
+            getattr(layer, name).copy_(to_torch(inp[name], dev))
+    if cfg.zipf_bias:
+        layer.bias.copy_(torch.from_numpy(inp["bias"]).to(dev))
+    bufs = layer.bufs()
+    sc = torch.cuda.current_stream()
+    sm = sc if a.one_stream else torch.cuda.Stream()
+
+    def step():
+        layer.forward(sc, sm, bufs=bufs)
+        layer.backward(sc, sm, bufs=bufs)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    kept = int(layer.counts.sum().item())
+
+    # timed region: every grouped-GEMM launch bracketed by HIP events on its stream
+    gemm_per_step = 6 * R
+    ev = EventArray(gemm_per_step * a.steps)
+    L.flowmoe_trace_start(ev.ev, ev.kinds, ev.pairs, L.kind_mask(L.K_GEMM))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    n = L.flowmoe_trace_stop()
+    elapsed = t1 - t0
+    gemm_ms = [ev.elapsed_ms(i) for i in range(n)]
+    gemm_kinds = [L.K_NAMES[ev.kinds[i]] for i in range(n)]
+    ev.close()
+
+    # untimed: one traced step over every kernel, for the per-kernel breakdown
+    all_ev = EventArray(256)
+    L.flowmoe_trace_start(all_ev.ev, all_ev.kinds, all_ev.pairs, 0xFFFFFFFF)
+    step()
+    torch.cuda.synchronize()
+    m = L.flowmoe_trace_stop()
+    per_kernel = {}
+    for i in range(m):
+        nm = L.K_NAMES[all_ev.kinds[i]]
+        per_kernel.setdefault(nm, []).append(all_ev.elapsed_ms(i) * 1e3)
+    all_ev.close()
+    breakdown = {k: round(float(sum(v)), 2) for k, v in per_kernel.items()}  # us per step
+
+    ms_per_step = elapsed / a.steps * 1e3
+    tokens_per_s = cfg.T * a.steps / elapsed
+    fl = gemm_flops_per_launch(cfg, kept)
+    mult = {"ffn1": 2.0 if cfg.act == "swiglu" else 1.0, "ffn2": 1.0, "dgrad1": 1.0, "wgrad2": 1.0,
+            "wgrad1": 2.0 if cfg.act == "swiglu" else 1.0,
+            "dgrad2": 2.0 if cfg.act == "swiglu" else 1.0}
+    tot_flops = sum(fl * mult[k] for k in gemm_kinds)
+    tot_s = sum(gemm_ms) / 1e3
+    avg_launch_ms = sum(gemm_ms) / max(1, len(gemm_ms))
+    achieved_tflops = tot_flops / tot_s / 1e12 if tot_s > 0 else 0.0
+
+    cpu = None
+    if not a.no_cpu_baseline:
+        import oracle
+        from moe_inputs import as_f64
+        from threadpoolctl import threadpool_info
+        i64 = {k: (None if v is None else (v.astype(np.float64) if k == "bias" else as_f64(v)))
+               for k, v in inp.items()}
+        # whole fwd+bwd steps of the same inputs, repeated until ~10 s of CPU work
+        reps, c0 = 0, time.perf_counter()
+        while True:
+            oracle.layer_fwd_bwd(i64, k=cfg.k, f=cfg.f, act=cfg.act, R=R, layout=a.layout)
+            reps += 1
+            if time.perf_counter() - c0 >= 10.0 or reps >= 20:
+                break
+        c1 = time.perf_counter()
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()
+                       if p.get("user_api") == "blas"] or [1])
+        cpu = {"value": round(cfg.T * reps / (c1 - c0), 2), "unit": "tokens/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"{reps} full fwd+bwd step(s) of the {cfg.name} workload ({cfg.T} tokens "
+                         f"each), numpy fp64, {c1 - c0:.1f} s"}
+
+    out = {
+        "metric": "MoE-layer fwd+bwd tokens/s on 1 MI355X; grouped-GEMM MFMA util %",
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name} MoE layer: T={cfg.T} M={cfg.M} H={cfg.H} E={cfg.E} "
+                         f"top-{cfg.k} f={cfg.f} {cfg.act} {cfg.dtype}, R={R}, {a.layout}, "
+                         f"{'1' if a.one_stream else '2'} stream(s)"),
+            "T": cfg.T, "M": cfg.M, "H": cfg.H, "E": cfg.E, "k": cfg.k, "f": cfg.f,
+            "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "kept_rows": kept,
+        },
+        "roofline": {
+            "kernel": "grouped GEMM (gemm_bf16_kernel, all 6 launches of a step)",
+            "bound": "mfma",
+            "achieved": round(achieved_tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "flops_per_launch": fl,
+            "avg_launch_us": round(avg_launch_ms * 1e3, 2),
+            "launches": len(gemm_ms),
+        },
+        "gemm_mfma_util_pct": round(100 * achieved_tflops / PEAK_BF16_TFLOPS, 2),
+        "kernel_us_per_step": breakdown,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -204,6 +204,41 @@ flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void*
                                        int32_t accumulate, void* ws, size_t ws_bytes,
                                        hipStream_t stream);
 
+/* ---- kernel tracing ------------------------------------------------------- */
+
+/* Kernel kinds (bit i of a trace mask selects kind i). */
+enum {
+  FLOWMOE_K_GATE = 0,            /* gate GEMV + top-k (flowmoe_gate_topk) */
+  FLOWMOE_K_ROUTE = 1,           /* top-k from logits (flowmoe_route) */
+  FLOWMOE_K_SCAN = 2,            /* capacity-bounded route scan (dispatch) */
+  FLOWMOE_K_GATHER = 3,          /* row gather into x_disp (dispatch) */
+  FLOWMOE_K_FFN1 = 4,            /* grouped GEMM h = X W1 (+ W3), activation epilogue */
+  FLOWMOE_K_FFN2 = 5,            /* grouped GEMM y = a W2 */
+  FLOWMOE_K_SWIGLU_ACT = 6,      /* fp32 SwiGLU activation */
+  FLOWMOE_K_COMBINE = 7,         /* combine, and dispatch backward (gather-sum) */
+  FLOWMOE_K_COMBINE_BWD = 8,     /* combine backward */
+  FLOWMOE_K_DGRAD1 = 9,          /* grouped GEMM dA = dY W2^T, activation' epilogue */
+  FLOWMOE_K_WGRAD2 = 10,         /* grouped GEMM dW2 = A^T dY */
+  FLOWMOE_K_WGRAD1 = 11,         /* grouped GEMM [dW1 | dW3] = X^T dH */
+  FLOWMOE_K_DGRAD2 = 12,         /* grouped GEMM dX = dH W1^T (+ dH3 W3^T) */
+  FLOWMOE_K_GATE_BWD_WT = 13,    /* W_g transpose for the dx term */
+  FLOWMOE_K_GATE_BWD_TOKEN = 14, /* d_logits and dx += d_logits W_g^T */
+  FLOWMOE_K_GATE_BWD_DW = 15,    /* dW_g split-T partials */
+  FLOWMOE_K_GATE_BWD_REDUCE = 16 /* dW_g / db reduction over splits */
+};
+
+/* Start tracing on the calling host thread: every later kernel launch whose
+ * kind bit is set in `mask` records events[2i] on its stream just before the
+ * launch and events[2i+1] just after, with kinds[i] (host memory) set to its
+ * kind, for i = 0, 1, ... until `pairs` pairs are used (later launches are
+ * not traced). Events are created by the caller (timing enabled). Tracing
+ * only records events; it changes no result. */
+flowmoe_status_t flowmoe_trace_start(hipEvent_t* events, int32_t* kinds, int32_t pairs,
+                                     uint32_t mask);
+
+/* Stop tracing; returns the number of pairs recorded since the start. */
+int32_t flowmoe_trace_stop(void);
+
 /* ---- the R-chunk two-stream layer (Sec. 3.2, Eqs. 3-6) -------------------- */
 
 /* Buffers of a whole layer over R chunks of shape->T tokens each. Per-token

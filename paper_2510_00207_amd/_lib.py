@@ -81,6 +81,8 @@ def load():
         "flowmoe_expert_ffn_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
         "flowmoe_dispatch_bwd": ([SP, P, P, P, P], I32),
         "flowmoe_gate_topk_bwd": ([SP, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
+        "flowmoe_trace_start": ([P, P, I32, ctypes.c_uint32], I32),
+        "flowmoe_trace_stop": ([], I32),
         "flowmoe_layer_fwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
         "flowmoe_layer_bwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
     }
@@ -198,6 +200,31 @@ def flowmoe_gate_topk_bwd(shape, x, w_gate, topk_idx, topk_w, d_topk_w, d_logits
                                         ptr(topk_w), ptr(d_topk_w), ptr(d_logits), ptr(dw_gate),
                                         ptr(dbias), ptr(dx), int(accumulate), ptr(ws), ws_bytes,
                                         _stream(stream)))
+
+
+# ---- kernel tracing --------------------------------------------------------------
+K_NAMES = ["gate", "route", "scan", "gather", "ffn1", "ffn2", "swiglu_act", "combine",
+           "combine_bwd", "dgrad1", "wgrad2", "wgrad1", "dgrad2", "gate_bwd_wt", "gate_bwd_token",
+           "gate_bwd_dw", "gate_bwd_reduce"]
+K = {n: i for i, n in enumerate(K_NAMES)}
+K_GEMM = ("ffn1", "ffn2", "dgrad1", "wgrad2", "wgrad1", "dgrad2")
+
+
+def kind_mask(names) -> int:
+    m = 0
+    for n in names:
+        m |= 1 << K[n]
+    return m
+
+
+def flowmoe_trace_start(events, kinds, pairs: int, mask: int):
+    """events: ctypes array of 2*pairs hipEvent_t; kinds: ctypes int32 array."""
+    _check(load().flowmoe_trace_start(ctypes.cast(events, ctypes.c_void_p),
+                                      ctypes.cast(kinds, ctypes.c_void_p), pairs, mask))
+
+
+def flowmoe_trace_stop() -> int:
+    return load().flowmoe_trace_stop()
 
 
 # ---- R-chunk layer ---------------------------------------------------------------

@@ -116,12 +116,59 @@ hipError_t get_events(int n, hipEvent_t** out) {
   return hipSuccess;
 }
 
+struct TraceState {
+  hipEvent_t* ev = nullptr;
+  int32_t* kinds = nullptr;
+  int32_t pairs = 0;
+  int32_t used = 0;
+  uint32_t mask = 0;
+  bool open = false;  // a begin was recorded for the current launch
+};
+thread_local TraceState g_trace;
+
 inline const char* cptr(const void* p, long off) { return static_cast<const char*>(p) + off; }
 inline char* mptr(void* p, long off) { return p == nullptr ? nullptr : static_cast<char*>(p) + off; }
 
 }  // namespace
 
+namespace flowmoe {
+hipError_t trace_mark(int kind, bool end, hipStream_t st) {
+  TraceState& t = g_trace;
+  if (t.ev == nullptr || kind < 0 || kind >= 32 || !((t.mask >> kind) & 1u)) return hipSuccess;
+  if (!end) {
+    if (t.used >= t.pairs) return hipSuccess;
+    t.open = true;
+    t.kinds[t.used] = kind;
+    return hipEventRecord(t.ev[2 * t.used], st);
+  }
+  if (!t.open) return hipSuccess;
+  t.open = false;
+  const hipError_t e = hipEventRecord(t.ev[2 * t.used + 1], st);
+  ++t.used;
+  return e;
+}
+}  // namespace flowmoe
+
 extern "C" {
+
+flowmoe_status_t flowmoe_trace_start(hipEvent_t* events, int32_t* kinds, int32_t pairs,
+                                     uint32_t mask) {
+  if (pairs < 0) return fail(FLOWMOE_ERR_INVALID, "pairs = %d < 0", pairs);
+  if (pairs > 0 && (events == nullptr || kinds == nullptr))
+    return fail(FLOWMOE_ERR_INVALID, "events and kinds must be given");
+  g_trace = TraceState();
+  g_trace.ev = pairs > 0 ? events : nullptr;
+  g_trace.kinds = kinds;
+  g_trace.pairs = pairs;
+  g_trace.mask = mask;
+  return ok();
+}
+
+int32_t flowmoe_trace_stop(void) {
+  const int32_t n = g_trace.used;
+  g_trace = TraceState();
+  return n;
+}
 
 const char* flowmoe_version(void) { return "flowmoe 0.1.0 gfx950"; }
 

@@ -114,6 +114,21 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
                                  const void* w2, void* dx_disp, float* dw1, float* dw3,
                                  float* dw2, int accumulate, void* ws, hipStream_t st);
 
+// Kernel tracing (flowmoe_trace_start): record a begin/end event around a
+// launch when the kind is selected. Defined in abi.hip.
+hipError_t trace_mark(int kind, bool end, hipStream_t st);
+
+// launch `f` bracketed by trace marks of `kind`
+template <class F>
+inline hipError_t traced(int kind, hipStream_t st, F&& f) {
+  hipError_t e = trace_mark(kind, false, st);
+  if (e != hipSuccess) return e;
+  f();
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return trace_mark(kind, true, st);
+}
+
 inline size_t esize(int dtype) { return dtype == FLOWMOE_BF16 ? 2 : 4; }
 inline size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 

@@ -227,29 +227,32 @@ hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, in
                            int32_t* offsets, int32_t* slot, int32_t* row_src, int32_t* load,
                            void* x_disp, hipStream_t st) {
   const int padded = s.layout == FLOWMOE_PADDED;
-  hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(kScanThreads), 0, st, idx, counts, offsets,
-                     slot, row_src, load, s.T, s.k, s.E, s.C, padded, s.rows);
-  hipError_t err = hipGetLastError();
+  hipError_t err = traced(FLOWMOE_K_SCAN, st, [&] {
+    hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(kScanThreads), 0, st, idx, counts, offsets,
+                       slot, row_src, load, s.T, s.k, s.E, s.C, padded, s.rows);
+  });
   if (err != hipSuccess || s.rows == 0) return err;
   const int vecs = (int)((long)s.M * esize(s.dtype) / 16);
   const long blocks = (s.rows + 3) / 4;
-  hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
-                     (const uint4*)x, row_src, offsets, (uint4*)x_disp, s.E, s.k, vecs, s.rows,
-                     padded);
-  return hipGetLastError();
+  return traced(FLOWMOE_K_GATHER, st, [&] {
+    hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const uint4*)x, row_src, offsets, (uint4*)x_disp, s.E, s.k, vecs, s.rows,
+                       padded);
+  });
 }
 
 hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slot, const float* w,
                           void* y, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
   const int blocks = (s.T + 3) / 4;
-  if (s.dtype == FLOWMOE_BF16)
-    hipLaunchKernelGGL(combine_rows_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st,
-                       (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k);
-  else
-    hipLaunchKernelGGL(combine_rows_kernel<float>, dim3(blocks), dim3(256), 0, st,
-                       (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k);
-  return hipGetLastError();
+  return traced(FLOWMOE_K_COMBINE, st, [&] {
+    if (s.dtype == FLOWMOE_BF16)
+      hipLaunchKernelGGL(combine_rows_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st,
+                         (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k);
+    else
+      hipLaunchKernelGGL(combine_rows_kernel<float>, dim3(blocks), dim3(256), 0, st,
+                         (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k);
+  });
 }
 
 hipError_t launch_dispatch_bwd(const Shape& s, const void* dx_disp, const int32_t* slot, void* dx,
@@ -265,15 +268,16 @@ hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp
   const long fill_blocks = (s.layout == FLOWMOE_PADDED) ? ((long)s.E * s.C + 3) / 4 : 0;
   const long blocks = token_blocks + fill_blocks;
   if (blocks == 0) return hipSuccess;
-  if (s.dtype == FLOWMOE_BF16)
-    hipLaunchKernelGGL(combine_bwd_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
-                       (const bf16_t*)dy, (const bf16_t*)y_disp, slot, w, counts,
-                       (bf16_t*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
-  else
-    hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st,
-                       (const float*)dy, (const float*)y_disp, slot, w, counts, (float*)dy_disp,
-                       dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
-  return hipGetLastError();
+  return traced(FLOWMOE_K_COMBINE_BWD, st, [&] {
+    if (s.dtype == FLOWMOE_BF16)
+      hipLaunchKernelGGL(combine_bwd_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
+                         (const bf16_t*)dy, (const bf16_t*)y_disp, slot, w, counts,
+                         (bf16_t*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
+    else
+      hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st,
+                         (const float*)dy, (const float*)y_disp, slot, w, counts,
+                         (float*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
+  });
 }
 
 }  // namespace flowmoe

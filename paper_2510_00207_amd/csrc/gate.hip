@@ -281,15 +281,16 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
   int xchunk = kGateLdsFloats / tpb;
   if (xchunk > 256) xchunk = 256;
   const size_t lds = (size_t)tpb * xchunk * sizeof(float);
-  if (s.dtype == FLOWMOE_BF16)
-    hipLaunchKernelGGL(gate_topk_kernel<bf16_t>, dim3(blocks), dim3(kGateThreads), lds, st,
-                       (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M,
-                       s.E, s.k, EP, TPG, xchunk);
-  else
-    hipLaunchKernelGGL(gate_topk_kernel<float>, dim3(blocks), dim3(kGateThreads), lds, st,
-                       (const float*)x, (const float*)w_gate, bias, logits, idx, w, s.T, s.M, s.E,
-                       s.k, EP, TPG, xchunk);
-  return hipGetLastError();
+  return traced(FLOWMOE_K_GATE, st, [&] {
+    if (s.dtype == FLOWMOE_BF16)
+      hipLaunchKernelGGL(gate_topk_kernel<bf16_t>, dim3(blocks), dim3(kGateThreads), lds, st,
+                         (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M,
+                         s.E, s.k, EP, TPG, xchunk);
+    else
+      hipLaunchKernelGGL(gate_topk_kernel<float>, dim3(blocks), dim3(kGateThreads), lds, st,
+                         (const float*)x, (const float*)w_gate, bias, logits, idx, w, s.T, s.M,
+                         s.E, s.k, EP, TPG, xchunk);
+  });
 }
 
 hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float* w, hipStream_t st) {
@@ -297,9 +298,10 @@ hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float
   const int EP = pow2_at_least(s.E);
   const int per_block = 4 * (64 / EP);
   const int blocks = (s.T + per_block - 1) / per_block;
-  hipLaunchKernelGGL(route_kernel, dim3(blocks), dim3(kGateThreads), 0, st, logits, idx, w, s.T,
-                     s.E, s.k, EP);
-  return hipGetLastError();
+  return traced(FLOWMOE_K_ROUTE, st, [&] {
+    hipLaunchKernelGGL(route_kernel, dim3(blocks), dim3(kGateThreads), 0, st, logits, idx, w, s.T,
+                       s.E, s.k, EP);
+  });
 }
 
 size_t gate_bwd_ws_bytes(const Shape& s) {
@@ -316,26 +318,34 @@ hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, co
                                       align256((size_t)s.M * s.E * sizeof(float)));
   const bool bf = s.dtype == FLOWMOE_BF16;
   const int S = gate_splits(s);
+  hipError_t e = hipSuccess;
   if (s.T > 0) {
     if (dx != nullptr) {
       const int nb = (int)(((long)s.M * s.E + 255) / 256);
-      if (bf)
-        hipLaunchKernelGGL(transpose_wg_kernel<bf16_t>, dim3(nb), dim3(256), 0, st,
-                           (const bf16_t*)w_gate, wgt, s.M, s.E);
-      else
-        hipLaunchKernelGGL(transpose_wg_kernel<float>, dim3(nb), dim3(256), 0, st,
-                           (const float*)w_gate, wgt, s.M, s.E);
+      e = traced(FLOWMOE_K_GATE_BWD_WT, st, [&] {
+        if (bf)
+          hipLaunchKernelGGL(transpose_wg_kernel<bf16_t>, dim3(nb), dim3(256), 0, st,
+                             (const bf16_t*)w_gate, wgt, s.M, s.E);
+        else
+          hipLaunchKernelGGL(transpose_wg_kernel<float>, dim3(nb), dim3(256), 0, st,
+                             (const float*)w_gate, wgt, s.M, s.E);
+      });
+      if (e != hipSuccess) return e;
     }
     const int tb = (s.T + 3) / 4;
-    if (bf)
-      hipLaunchKernelGGL(gate_bwd_token_kernel<bf16_t>, dim3(tb), dim3(256), 0, st, idx, w, dw,
-                         wgt, d_logits, (bf16_t*)dx, s.T, s.M, s.E, s.k);
-    else
-      hipLaunchKernelGGL(gate_bwd_token_kernel<float>, dim3(tb), dim3(256), 0, st, idx, w, dw, wgt,
-                         d_logits, (float*)dx, s.T, s.M, s.E, s.k);
+    e = traced(FLOWMOE_K_GATE_BWD_TOKEN, st, [&] {
+      if (bf)
+        hipLaunchKernelGGL(gate_bwd_token_kernel<bf16_t>, dim3(tb), dim3(256), 0, st, idx, w, dw,
+                           wgt, d_logits, (bf16_t*)dx, s.T, s.M, s.E, s.k);
+      else
+        hipLaunchKernelGGL(gate_bwd_token_kernel<float>, dim3(tb), dim3(256), 0, st, idx, w, dw,
+                           wgt, d_logits, (float*)dx, s.T, s.M, s.E, s.k);
+    });
+    if (e != hipSuccess) return e;
     const int tps = (s.T + S - 1) / S;
     dim3 grid((s.M + 1 + 255) / 256, S);
     const int EP = pow2_at_least(s.E);
+    e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
 #define FLOWMOE_DW_LAUNCH(EPV)                                                                   \
   if (bf)                                                                                        \
     hipLaunchKernelGGL((gate_bwd_dw_partial_kernel<bf16_t, EPV>), grid, dim3(256), 0, st,        \
@@ -343,28 +353,29 @@ hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, co
   else                                                                                           \
     hipLaunchKernelGGL((gate_bwd_dw_partial_kernel<float, EPV>), grid, dim3(256), 0, st,         \
                        (const float*)x, d_logits, P, s.T, s.M, s.E, tps);
-    if (EP <= 8) {
-      FLOWMOE_DW_LAUNCH(8)
-    } else if (EP <= 16) {
-      FLOWMOE_DW_LAUNCH(16)
-    } else if (EP <= 32) {
-      FLOWMOE_DW_LAUNCH(32)
-    } else {
-      FLOWMOE_DW_LAUNCH(64)
-    }
+      if (EP <= 8) {
+        FLOWMOE_DW_LAUNCH(8)
+      } else if (EP <= 16) {
+        FLOWMOE_DW_LAUNCH(16)
+      } else if (EP <= 32) {
+        FLOWMOE_DW_LAUNCH(32)
+      } else {
+        FLOWMOE_DW_LAUNCH(64)
+      }
 #undef FLOWMOE_DW_LAUNCH
+    });
+    if (e != hipSuccess) return e;
   }
   const long n = (long)(s.M + 1) * s.E;
   const int nb = (int)((n + 255) / 256);
-  if (s.T > 0) {
+  if (s.T == 0 && accumulate) return hipSuccess;
+  // with no tokens the gradient is zero: a reduce over zero splits writes it
+  const int splits = s.T > 0 ? S : 0;
+  const int acc = s.T > 0 ? accumulate : 0;
+  return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
     hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nb), dim3(256), 0, st, P, dw_gate, dbias,
-                       s.M, s.E, S, accumulate);
-  } else if (!accumulate) {
-    // no tokens: the gradient is zero (reduce over zero splits)
-    hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nb), dim3(256), 0, st, P, dw_gate, dbias,
-                       s.M, s.E, 0, 0);
-  }
-  return hipGetLastError();
+                       s.M, s.E, splits, acc);
+  });
 }
 
 }  // namespace flowmoe

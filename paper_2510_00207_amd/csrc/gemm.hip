@@ -544,7 +544,7 @@ GemmParams base_params(const Shape& s, const int32_t* counts, const int32_t* off
 }
 
 template <int MODE, bool A_KC, bool B_KC, int EPI, int BM, int BN>
-hipError_t run_bf16(const Shape& s, GemmParams p, hipStream_t st) {
+hipError_t run_bf16(int kind, const Shape& s, GemmParams p, hipStream_t st) {
   long blocks;
   if (MODE == MODE_ROWS) {
     const int ncols = (EPI == EPI_SWIGLU_FWD) ? BN / 2 : BN;
@@ -554,13 +554,14 @@ hipError_t run_bf16(const Shape& s, GemmParams p, hipStream_t st) {
     blocks = (long)s.E * ((p.Mdim + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   }
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<MODE, A_KC, B_KC, EPI, BM, BN>), dim3((unsigned)blocks),
-                     dim3(kThreads), 0, st, p);
-  return hipGetLastError();
+  return traced(kind, st, [&] {
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, A_KC, B_KC, EPI, BM, BN>), dim3((unsigned)blocks),
+                       dim3(kThreads), 0, st, p);
+  });
 }
 
 template <int MODE, bool B_KC, int EPI>
-hipError_t run_f32(const Shape& s, GemmParams p, hipStream_t st) {
+hipError_t run_f32(int kind, const Shape& s, GemmParams p, hipStream_t st) {
   long blocks;
   if (MODE == MODE_ROWS) {
     p.mt_bound = rows_tiles_bound(s, 64);
@@ -569,8 +570,10 @@ hipError_t run_f32(const Shape& s, GemmParams p, hipStream_t st) {
     blocks = (long)s.E * ((p.Mdim + 63) / 64) * ((p.N + 63) / 64);
   }
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_f32_kernel<MODE, B_KC, EPI>), dim3((unsigned)blocks), dim3(256), 0, st, p);
-  return hipGetLastError();
+  return traced(kind, st, [&] {
+    hipLaunchKernelGGL((gemm_f32_kernel<MODE, B_KC, EPI>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       p);
+  });
 }
 
 #define FLOWMOE_TRY(x)                 \
@@ -609,22 +612,23 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
   p.ldc1 = H;
   if (s.dtype == FLOWMOE_BF16) {
     if (swiglu)
-      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, false, EPI_SWIGLU_FWD, 128, 128>(s, p, st)));
+      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, false, EPI_SWIGLU_FWD, 128, 128>(FLOWMOE_K_FFN1, s, p, st)));
     else
-      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, false, EPI_GELU_FWD, 128, 128>(s, p, st)));
+      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, false, EPI_GELU_FWD, 128, 128>(FLOWMOE_K_FFN1, s, p, st)));
   } else {
     if (swiglu) {
       p.B1 = nullptr;
-      FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_STORE>(s, p, st)));
+      FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN1, s, p, st)));
       p.B0 = w3;
       p.coloff = H;
-      FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_STORE>(s, p, st)));
-      hipLaunchKernelGGL(swiglu_act_f32_kernel, dim3(1024), dim3(256), 0, st,
-                         (const float*)h_save, (float*)a_save, offsets, s.E, s.rows,
-                         s.layout == FLOWMOE_PADDED, H);
-      FLOWMOE_TRY(hipGetLastError());
+      FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN1, s, p, st)));
+      FLOWMOE_TRY(traced(FLOWMOE_K_SWIGLU_ACT, st, [&] {
+        hipLaunchKernelGGL(swiglu_act_f32_kernel, dim3(1024), dim3(256), 0, st,
+                           (const float*)h_save, (float*)a_save, offsets, s.E, s.rows,
+                           s.layout == FLOWMOE_PADDED, H);
+      }));
     } else {
-      FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_GELU_FWD>(s, p, st)));
+      FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_GELU_FWD>(FLOWMOE_K_FFN1, s, p, st)));
     }
   }
   // layer 2: y = a W2
@@ -639,8 +643,8 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
   q.C0 = y_disp;
   q.ldc = M;
   if (s.dtype == FLOWMOE_BF16)
-    return run_bf16<MODE_ROWS, true, false, EPI_STORE, 128, 128>(s, q, st);
-  return run_f32<MODE_ROWS, false, EPI_STORE>(s, q, st);
+    return run_bf16<MODE_ROWS, true, false, EPI_STORE, 128, 128>(FLOWMOE_K_FFN2, s, q, st);
+  return run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN2, s, q, st);
 }
 
 hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void* x_disp,
@@ -669,14 +673,14 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.ldaux = HW;
     if (bf) {
       if (swiglu)
-        FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_SWIGLU_BWD, 128, 128>(s, p, st)));
+        FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_SWIGLU_BWD, 128, 128>(FLOWMOE_K_DGRAD1, s, p, st)));
       else
-        FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_GELU_BWD, 128, 128>(s, p, st)));
+        FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_GELU_BWD, 128, 128>(FLOWMOE_K_DGRAD1, s, p, st)));
     } else {
       if (swiglu)
-        FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_SWIGLU_BWD>(s, p, st)));
+        FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_SWIGLU_BWD>(FLOWMOE_K_DGRAD1, s, p, st)));
       else
-        FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_GELU_BWD>(s, p, st)));
+        FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_GELU_BWD>(FLOWMOE_K_DGRAD1, s, p, st)));
     }
   }
   // 2. dW2 = A^T dY  (H x M per expert)
@@ -693,9 +697,9 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.c_estride = (long)H * M;
     p.accumulate = accumulate;
     if (bf)
-      FLOWMOE_TRY((run_bf16<MODE_KSUM, false, false, EPI_WGRAD, 128, 128>(s, p, st)));
+      FLOWMOE_TRY((run_bf16<MODE_KSUM, false, false, EPI_WGRAD, 128, 128>(FLOWMOE_K_WGRAD2, s, p, st)));
     else
-      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(s, p, st)));
+      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD2, s, p, st)));
   }
   // 3. [dW1 | dW3] = X^T [dH1 | dH3]  (M x H per expert, each)
   {
@@ -713,9 +717,9 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.c_estride = (long)M * H;
     p.accumulate = accumulate;
     if (bf)
-      FLOWMOE_TRY((run_bf16<MODE_KSUM, false, false, EPI_WGRAD, 128, 128>(s, p, st)));
+      FLOWMOE_TRY((run_bf16<MODE_KSUM, false, false, EPI_WGRAD, 128, 128>(FLOWMOE_K_WGRAD1, s, p, st)));
     else
-      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(s, p, st)));
+      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
   }
   // 4. dX = dH1 W1^T (+ dH3 W3^T)
   if (s.rows > 0) {
@@ -732,9 +736,9 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.C0 = dx_disp;
     p.ldc = M;
     if (bf)
-      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_STORE, 128, 128>(s, p, st)));
+      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_STORE, 128, 128>(FLOWMOE_K_DGRAD2, s, p, st)));
     else
-      FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_STORE>(s, p, st)));
+      FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_STORE>(FLOWMOE_K_DGRAD2, s, p, st)));
   }
   return hipSuccess;
 }
