@@ -17,15 +17,16 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// round to nearest, ties to even (inputs finite)
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// round to nearest, ties to even (v_cvt_pk_bf16_f32; inputs finite)
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<bf16_t>(u >> 16);
+  return __builtin_bit_cast(bf16_t, (__bf16)f);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 template <typename T> struct Elem;
@@ -67,12 +68,31 @@ __device__ __forceinline__ void store8(float* p, const float v[8]) {
   *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
 }
 
-// activations (fp32); erff/expf are the device math library's
-__device__ __forceinline__ float gelu_f(float z) { return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f)); }
-__device__ __forceinline__ float gelu_grad_f(float z) {
-  return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) + z * 0.39894228040143268f * expf(-0.5f * z * z);
+// activations (fp32). erf follows Abramowitz & Stegun 7.1.26,
+// erf(x) = 1 - (a1 t + ... + a5 t^5) exp(-x^2), t = 1 / (1 + p x), x >= 0,
+// absolute error <= 1.5e-7; its exp(-x^2) term is also phi(z) * sqrt(2 pi)
+// for x = z / sqrt(2), which the GELU derivative reuses.
+struct ErfParts {
+  float erf;   // erf(z / sqrt(2))
+  float gexp;  // exp(-z^2 / 2)
+};
+__device__ __forceinline__ ErfParts erf_parts(float z) {
+  const float x = fabsf(z) * 0.70710678118654752f;
+  const float t = __frcp_rn(1.0f + 0.3275911f * x);
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float g = __expf(-x * x);
+  const float ea = 1.0f - poly * g;
+  return ErfParts{z < 0.0f ? -ea : ea, g};
 }
-__device__ __forceinline__ float sigmoid_f(float z) { return 1.0f / (1.0f + expf(-z)); }
+// gelu(z) = z * Phi(z), Phi(z) = (1 + erf(z / sqrt(2))) / 2
+__device__ __forceinline__ float gelu_f(float z) { return 0.5f * z * (1.0f + erf_parts(z).erf); }
+// gelu'(z) = Phi(z) + z * phi(z)
+__device__ __forceinline__ float gelu_grad_f(float z) {
+  const ErfParts e = erf_parts(z);
+  return 0.5f * (1.0f + e.erf) + z * 0.39894228040143268f * e.gexp;
+}
+__device__ __forceinline__ float sigmoid_f(float z) { return __frcp_rn(1.0f + __expf(-z)); }
 
 // ---------------------------------------------------------------------------
 // host side

@@ -133,6 +133,97 @@ __global__ __launch_bounds__(kGateThreads) void gate_topk_kernel(
   }
 }
 
+// bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16): a block of 4 waves owns 64
+// tokens, each wave 16 of them, against all experts padded to 16-column
+// blocks. x rows feed the A operand straight from global memory (16 bytes of
+// one row per lane); W_g chunks of kGateKC rows are staged in LDS transposed
+// (expert-major, K-contiguous) for the B operand. The logits tile goes
+// through LDS to the wavefront top-k.
+constexpr int kGateKC = 128;          // K rows of W_g staged per step
+constexpr int kGateTok = 64;          // tokens per block
+constexpr int kGateWtStride = kGateKC + 8;  // bf16 elements per staged expert row
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg, const float* __restrict__ bias,
+    float* __restrict__ logits, int32_t* __restrict__ idx, float* __restrict__ w, int T, int M,
+    int E, int k, int EP) {
+  __shared__ __attribute__((aligned(16))) bf16_t wt[kMaxE * kGateWtStride];
+  __shared__ float lg[kGateTok][kMaxE + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int NB = (E + 15) >> 4;  // 16-expert column blocks
+  const int t0 = blockIdx.x * kGateTok + wave * 16;
+  const int arow = t0 + (lane & 15);          // token whose A row this lane feeds
+  const int kq = (lane >> 4) * 8;             // k offset of this lane inside a 32-step
+  const bool arow_ok = arow < T;
+  const bf16_t* xrow = x + (long)(arow_ok ? arow : 0) * M;
+  floatx4_t acc[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) acc[nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = 0; k0 < M; k0 += kGateKC) {
+    // A fragments of this chunk, issued before the staging barrier
+    uint4 av[kGateKC / 32];
+#pragma unroll
+    for (int s = 0; s < kGateKC / 32; ++s) {
+      const int kk = k0 + s * 32 + kq;
+      av[s] = (arow_ok && kk < M) ? *reinterpret_cast<const uint4*>(xrow + kk) : make_uint4(0, 0, 0, 0);
+    }
+    __syncthreads();  // previous chunk's readers of wt are done
+    const int rows = min(kGateKC, M - k0);
+    for (int q = tid; q < kGateKC * NB * 16; q += 256) {
+      const int kk = q / (NB * 16), e = q % (NB * 16);
+      const bf16_t v = (kk < rows && e < E) ? wg[(long)(k0 + kk) * E + e] : (bf16_t)0;
+      wt[e * kGateWtStride + kk] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < kGateKC / 32; ++s) {
+      const bf16x8_t a = __builtin_bit_cast(bf16x8_t, av[s]);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        if (nb < NB) {
+          const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(
+              &wt[(nb * 16 + (lane & 15)) * kGateWtStride + s * 32 + kq]);
+          acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[nb], 0, 0, 0);
+        }
+      }
+    }
+  }
+  // acc[nb][r]: token (lane/16)*4 + r of this wave, expert nb*16 + lane%16
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    if (nb < NB) {
+      const int e = nb * 16 + (lane & 15);
+      const float b = (bias != nullptr && e < E) ? bias[e] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int tt = wave * 16 + (lane >> 4) * 4 + r;
+        const float l = acc[nb][r] + b;
+        if (e < E) {
+          lg[tt][e] = l;
+          const int t = blockIdx.x * kGateTok + tt;
+          if (t < T) logits[(long)t * E + e] = l;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // top-k: segments of EP lanes, one token per segment per round
+  const int G = 64 / EP;
+  const int seg = lane / EP, e = lane % EP;
+  const bool evalid = e < E;
+  for (int i = seg; i < 16; i += G) {
+    const int tt = wave * 16 + i;
+    const int t = blockIdx.x * kGateTok + tt;
+    if (t >= T) break;  // uniform across the segment
+    const float l = evalid ? lg[tt][e] : 0.f;
+    topk_write(l, e, evalid, EP, k, idx + (long)t * k, w + (long)t * k);
+  }
+}
+
 __global__ __launch_bounds__(kGateThreads) void route_kernel(const float* __restrict__ logits,
                                                              int32_t* __restrict__ idx,
                                                              float* __restrict__ w, int T, int E,
@@ -274,6 +365,13 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
                             float* logits, int32_t* idx, float* w, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
   const int EP = pow2_at_least(s.E);
+  if (s.dtype == FLOWMOE_BF16) {
+    const int blocks = (s.T + kGateTok - 1) / kGateTok;
+    return traced(FLOWMOE_K_GATE, st, [&] {
+      hipLaunchKernelGGL(gate_topk_mfma_kernel, dim3(blocks), dim3(256), 0, st, (const bf16_t*)x,
+                         (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M, s.E, s.k, EP);
+    });
+  }
   const int G = 64 / EP;
   const int TPG = G >= 8 ? 1 : 8 / G;
   const int tpb = 4 * G * TPG;
@@ -282,14 +380,9 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
   if (xchunk > 256) xchunk = 256;
   const size_t lds = (size_t)tpb * xchunk * sizeof(float);
   return traced(FLOWMOE_K_GATE, st, [&] {
-    if (s.dtype == FLOWMOE_BF16)
-      hipLaunchKernelGGL(gate_topk_kernel<bf16_t>, dim3(blocks), dim3(kGateThreads), lds, st,
-                         (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M,
-                         s.E, s.k, EP, TPG, xchunk);
-    else
-      hipLaunchKernelGGL(gate_topk_kernel<float>, dim3(blocks), dim3(kGateThreads), lds, st,
-                         (const float*)x, (const float*)w_gate, bias, logits, idx, w, s.T, s.M,
-                         s.E, s.k, EP, TPG, xchunk);
+    hipLaunchKernelGGL(gate_topk_kernel<float>, dim3(blocks), dim3(kGateThreads), lds, st,
+                       (const float*)x, (const float*)w_gate, bias, logits, idx, w, s.T, s.M,
+                       s.E, s.k, EP, TPG, xchunk);
   });
 }
 

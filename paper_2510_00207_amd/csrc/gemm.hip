@@ -51,6 +51,7 @@ struct GemmParams {
   int E;
   int padC;          // padded layout: every expert spans C rows (0 = packed)
   int mt_bound;      // ROWS: row tiles per column tile in the grid
+  int ntiles;        // ROWS: column tiles
   void* C0;
   void* C1;
   long ldc, ldc1;
@@ -67,10 +68,13 @@ struct GemmParams {
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------
 constexpr int BK = 64;
-constexpr int kThreads = 256;
 
+// LDS tile layout: 128-byte rows (64 bf16 of K), 16-byte chunks XOR-swizzled
+// by (row / 2) % 8. A ds_read_b128 is serviced 16 lanes per cycle over 64
+// banks; the 16 consecutive rows it touches then fall into 16 distinct
+// 16-byte bank slots.
 __device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * 128 + (((chunk ^ (row & 7)) & 7) << 4);
+  return row * 128 + (((chunk ^ (row >> 1)) & 7) << 4);
 }
 
 // pack 16-bit column `col` of two 8 x bf16 rows into one dword (lo = r0)
@@ -81,75 +85,89 @@ __device__ __forceinline__ uint32_t pick2(const uint4& r0, const uint4& r1, int 
   return (col & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
 }
 
-// K-contiguous tile loader: ROWSxBK tile, 16-byte chunks, NP chunks/thread.
-template <int ROWS>
+// K-contiguous tile loader: ROWS x BK tile in 16-byte chunks. Thread t owns
+// chunk c = t % 8 of rows r0 + p * NT/8 (r0 = t / 8), p < NP. Rows at or past
+// `lim` and chunks at or past K load zeros. Chunks at k >= ksplit come from
+// the second source at k - ksplit.
+template <int ROWS, int NT>
 struct KcLoader {
-  static constexpr int NP = ROWS * 8 / kThreads;
-  const bf16_t* p0[NP];  // row starts (k = 0)
-  const bf16_t* p1[NP];  // second source (k >= ksplit)
-  bool ok[NP];
+  static constexpr int NP = ROWS * 8 / NT;
+  static constexpr int RSTEP = NT / 8;  // rows between a thread's chunks
+  const bf16_t* base0;  // row r0, k = 0
+  const bf16_t* base1;  // second source, row r0, k = 0
+  long rstride;         // elements between rows r0 + p*RSTEP and r0 + (p+1)*RSTEP
+  int lim, r0, c;
   uint4 v[NP];
-  int c;  // chunk of this thread
+  __device__ __forceinline__ void init(const bf16_t* b0, const bf16_t* b1, long ld, int limit) {
+    r0 = threadIdx.x >> 3;
+    c = threadIdx.x & 7;
+    base0 = b0 + (long)r0 * ld;
+    base1 = b1 + (long)r0 * ld;
+    rstride = (long)RSTEP * ld;
+    lim = limit;
+  }
   __device__ __forceinline__ void load(int k0, int K, int ksplit) {
     const int k = k0 + c * 8;
+    const bool second = k >= ksplit;
+    const bf16_t* b = second ? base1 + (k - ksplit) : base0 + k;
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
-      if (ok[p] && k < K) {
-        const bf16_t* src = (k < ksplit) ? (p0[p] + k) : (p1[p] + (k - ksplit));
-        v[p] = *reinterpret_cast<const uint4*>(src);
-      } else {
+      if (r0 + p * RSTEP < lim && k < K)
+        v[p] = *reinterpret_cast<const uint4*>(b + p * rstride);
+      else
         v[p] = make_uint4(0, 0, 0, 0);
-      }
     }
   }
   __device__ __forceinline__ void store(char* lds) const {
-    const int r0 = threadIdx.x >> 3;
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const int row = r0 + p * (kThreads / 8);
-      *reinterpret_cast<uint4*>(lds + lds_off(row, c)) = v[p];
-    }
+    for (int p = 0; p < NP; ++p)
+      *reinterpret_cast<uint4*>(lds + lds_off(r0 + p * RSTEP, c)) = v[p];
   }
 };
 
-// MN-contiguous tile loader: element (row i, k) at col_ptr + k*ld, where each
-// thread owns one group of 8 rows (g) and KT consecutive k (kg).
-template <int ROWS>
+// MN-contiguous tile loader: element (row i, k) at col + k*ld, where each
+// thread owns one group of 8 rows (g) and KT consecutive k (kg); the KT x 8
+// block is transposed in registers before the LDS write.
+template <int ROWS, int NT>
 struct MncLoader {
-  static constexpr int KT = ROWS * BK / (8 * kThreads);  // 4 for 128 rows, 8 for 256
+  static constexpr int KT = ROWS * BK / (8 * NT);  // k rows per thread: 4 or 8
   static constexpr int KG = BK / KT;                    // k groups per tile
-  const bf16_t* col;  // pointer to (k = 0, first row of my group)
+  const bf16_t* col;  // (k = 0, first row of my group)
   long ld;
   bool ok;
   int kg, g;
   uint4 v[KT];
   __device__ __forceinline__ void load(int k0, int Klim) {
+    const bf16_t* b = col + (long)(k0 + kg * KT) * ld;
 #pragma unroll
     for (int j = 0; j < KT; ++j) {
       const int k = k0 + kg * KT + j;
       if (ok && k < Klim)
-        v[j] = *reinterpret_cast<const uint4*>(col + (long)k * ld);
+        v[j] = *reinterpret_cast<const uint4*>(b + (long)j * ld);
       else
         v[j] = make_uint4(0, 0, 0, 0);
     }
   }
+  // Threads of odd groups store their rows in the order 1,0,3,2,..., so one
+  // store instruction writes rows of both parities (both halves of the banks).
   __device__ __forceinline__ void store(char* lds) const {
+    const bool odd = g & 1;
 #pragma unroll
     for (int ii = 0; ii < 8; ++ii) {
-      const int row = g * 8 + ii;
+      const int row = g * 8 + (ii ^ (int)odd);
       if constexpr (KT == 8) {
-        uint4 o;
-        o.x = pick2(v[0], v[1], ii);
-        o.y = pick2(v[2], v[3], ii);
-        o.z = pick2(v[4], v[5], ii);
-        o.w = pick2(v[6], v[7], ii);
-        *reinterpret_cast<uint4*>(lds + lds_off(row, kg)) = o;
+        uint4 a, b;  // column ii and column ii ^ 1 of the 8 x 8 block
+        a.x = pick2(v[0], v[1], ii);      b.x = pick2(v[0], v[1], ii ^ 1);
+        a.y = pick2(v[2], v[3], ii);      b.y = pick2(v[2], v[3], ii ^ 1);
+        a.z = pick2(v[4], v[5], ii);      b.z = pick2(v[4], v[5], ii ^ 1);
+        a.w = pick2(v[6], v[7], ii);      b.w = pick2(v[6], v[7], ii ^ 1);
+        *reinterpret_cast<uint4*>(lds + lds_off(row, kg)) = odd ? b : a;
       } else {
-        uint2 o;
-        o.x = pick2(v[0], v[1], ii);
-        o.y = pick2(v[2], v[3], ii);
+        uint2 a, b;
+        a.x = pick2(v[0], v[1], ii);      b.x = pick2(v[0], v[1], ii ^ 1);
+        a.y = pick2(v[2], v[3], ii);      b.y = pick2(v[2], v[3], ii ^ 1);
         const int kin = kg * KT;  // element offset of my k group in the tile
-        *reinterpret_cast<uint2*>(lds + lds_off(row, kin >> 3) + ((kin & 7) << 1)) = o;
+        *reinterpret_cast<uint2*>(lds + lds_off(row, kin >> 3) + ((kin & 7) << 1)) = odd ? b : a;
       }
     }
   }
@@ -157,21 +175,192 @@ struct MncLoader {
 
 __device__ __forceinline__ float silu_f(float z) { return z * sigmoid_f(z); }
 
-template <int MODE, bool A_KC, bool B_KC, int EPI, int BM, int BN>
-__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p) {
-  constexpr int WM = BM / 2, WN = BN / 2;
+// Blocks are dispatched round-robin over the 8 XCDs (each with its own L2);
+// renumber them so that every XCD works on one contiguous range of tiles.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+  const int q = nblocks >> 3, rem = nblocks & 7;
+  const int x = bid & 7, i = bid >> 3;
+  return x * q + (x < rem ? x : rem) + i;
+}
+
+// Epilogue shared by the bf16 kernels: the block's accumulators (each wave
+// WM x WN, acc[i][j][4*g + q] = C[row wm*WM + i*32 + lane%32]
+// [col wn*WN + j*32 + 8*g + 4*(lane/32) + q]) to global memory. Row mode
+// stages through LDS (smem must be free; at least (NT/64)*64*WN floats).
+template <int MODE, int EPI, int BM, int BN, int NT>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& p,
+                                              floatx16 (&acc)[BM / 64][BN / (NT / 128) / 32],
+                                              char* smem, int e, int mt, int n0, int row0,
+                                              int rows_e, int cnt_e) {
+  constexpr int WGN = NT / 128;
+  constexpr int WM = BM / 2, WN = BN / WGN;
   constexpr int FM = WM / 32, FN = WN / 32;
-  static_assert(EPI != EPI_SWIGLU_FWD || FN == 2, "dual forward needs 64-column wave tiles");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  // acc[i][j][4*g + q] is C[row wm*WM + i*32 + lane%32]
+  //                        [col wn*WN + j*32 + 8*g + 4*(lane/32) + q], q = 0..3
+  const int lrow = lane & 31, lcol = 4 * (lane >> 5);
+  if constexpr (MODE == MODE_ROWS) {
+    // The wave's 128 x WN tile goes out 64 rows at a time through its own LDS
+    // region (fp32, 16-byte chunks XOR-swizzled by row), then each lane
+    // writes 8 consecutive outputs of one row: full 128-byte lines.
+    // The main loop ended with a barrier, so the tile buffers are free.
+    static_assert(FM % 2 == 0, "staged epilogue works on 64-row halves");
+    constexpr int SCH = WN / 4;  // 16-byte chunks per staged row
+    static_assert((NT / 64) * 64 * WN * 4 <= 2 * (BM + BN) * 128, "stage does not fit");
+    float* stage = reinterpret_cast<float*>(smem) + wave * 64 * WN;
+    bf16_t* C0 = static_cast<bf16_t*>(p.C0);
+    bf16_t* C1 = static_cast<bf16_t*>(p.C1);
+    const bf16_t* aux = static_cast<const bf16_t*>(p.aux);
+    auto sidx = [&](int r, int c4) { return r * WN + ((c4 ^ (r & (SCH - 1))) << 2); };
+#pragma unroll
+    for (int hf = 0; hf < FM / 2; ++hf) {
+#pragma unroll
+      for (int i2 = 0; i2 < 2; ++i2)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq) {
+            const int r = i2 * 32 + lrow, c4 = (j * 32 + 8 * gq + lcol) >> 2;
+            const floatx16& a = acc[hf * 2 + i2][j];
+            *reinterpret_cast<float4*>(stage + sidx(r, c4)) =
+                make_float4(a[4 * gq], a[4 * gq + 1], a[4 * gq + 2], a[4 * gq + 3]);
+          }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      auto read8 = [&](int r, int c8, float v[8]) {
+        const float4 lo = *reinterpret_cast<const float4*>(stage + sidx(r, 2 * c8));
+        const float4 hi = *reinterpret_cast<const float4*>(stage + sidx(r, 2 * c8 + 1));
+        v[0] = lo.x; v[1] = lo.y; v[2] = lo.z; v[3] = lo.w;
+        v[4] = hi.x; v[5] = hi.y; v[6] = hi.z; v[7] = hi.w;
+      };
+      if constexpr (EPI == EPI_SWIGLU_FWD) {
+        // column pairs (W1, W3) of 32 each: WN/2 distinct outputs per row
+        constexpr int G8 = WN / 16;        // 8-column groups of distinct outputs per row
+        constexpr int PER = 64 * G8 / 64;  // items per lane
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+          const int item = it * 64 + lane;
+          const int rr = item / G8, c8 = item % G8;  // c8: 8-group among the distinct columns
+          const int jp = c8 >> 2, cin = (c8 & 3) * 8;  // pair and offset inside its 32
+          const int ti = wm * WM + hf * 64 + rr;
+          const int li = mt * BM + ti;
+          const int n = n0 + wn * (WN / 2) + jp * 32 + cin;
+          if (li >= rows_e || n >= p.N) continue;
+          const bool data = li < cnt_e;
+          float h1[8], h3[8], a[8];
+          read8(rr, (jp * 64 + cin) >> 3, h1);
+          read8(rr, (jp * 64 + 32 + cin) >> 3, h3);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            if (!data) h1[q] = h3[q] = 0.f;
+            a[q] = silu_f(h1[q]) * h3[q];
+          }
+          const long g = row0 + ti;
+          store8(C0 + g * p.ldc + n, h1);
+          store8(C0 + g * p.ldc + p.Hh + n, h3);
+          store8(C1 + g * p.ldc1 + n, a);
+        }
+      } else {
+        constexpr int G8 = WN / 8;
+        constexpr int PER = 64 * G8 / 64;
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+          const int item = it * 64 + lane;
+          const int rr = item / G8, c8 = item % G8;
+          const int ti = wm * WM + hf * 64 + rr;
+          const int li = mt * BM + ti;
+          const int n = n0 + wn * WN + c8 * 8;
+          if (li >= rows_e || n >= p.N) continue;
+          const bool data = li < cnt_e;
+          float v[8];
+          read8(rr, c8, v);
+          if (!data) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] = 0.f;
+          }
+          const long g = row0 + ti;
+          if constexpr (EPI == EPI_STORE) {
+            store8(C0 + g * p.ldc + n, v);
+          } else if constexpr (EPI == EPI_GELU_FWD) {
+            float a[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) a[q] = gelu_f(v[q]);
+            store8(C0 + g * p.ldc + n, v);
+            store8(C1 + g * p.ldc1 + n, a);
+          } else if constexpr (EPI == EPI_GELU_BWD) {
+            float h[8];
+            load8(aux + g * p.ldaux + n, h);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] *= gelu_grad_f(h[q]);
+            store8(C0 + g * p.ldc + n, v);
+          } else if constexpr (EPI == EPI_SWIGLU_BWD) {
+            float h1[8], h3[8], d3[8];
+            load8(aux + g * p.ldaux + n, h1);
+            load8(aux + g * p.ldaux + p.Hh + n, h3);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              const float sg = sigmoid_f(h1[q]);
+              d3[q] = v[q] * h1[q] * sg;
+              v[q] = v[q] * h3[q] * sg * (1.f + h1[q] * (1.f - sg));
+            }
+            store8(C0 + g * p.ldc + n, v);
+            store8(C0 + g * p.ldc + p.Hh + n, d3);
+          }
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+  } else {  // KSUM wgrad, fp32 out
+    float* C0 = static_cast<float*>(p.C0);
+    float* C1 = static_cast<float*>(p.C1);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int m = mt * BM + wm * WM + i * 32 + lrow;
+      if (m >= p.Mdim) continue;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          const int n = n0 + wn * WN + j * 32 + 8 * gq + lcol;
+          if (n >= p.N) continue;
+          float* dst = (n < p.nsplit) ? C0 + (long)e * p.c_estride + (long)m * p.ldc + n
+                                      : C1 + (long)e * p.c_estride + (long)m * p.ldc + (n - p.nsplit);
+          float4 v = make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2],
+                                 acc[i][j][4 * gq + 3]);
+          if (p.accumulate) {
+            const float4 o = *reinterpret_cast<const float4*>(dst);
+            v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+          }
+          *reinterpret_cast<float4*>(dst) = v;
+        }
+      }
+    }
+  }
+}
+
+template <int MODE, bool A_KC, bool B_KC, int EPI, int BM, int BN, int NT>
+__global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
+  constexpr int WGN = NT / 128;  // waves along N (two along M)
+  constexpr int WM = BM / 2, WN = BN / WGN;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  static_assert(EPI != EPI_SWIGLU_FWD || (FN % 2) == 0, "dual forward needs W1/W3 column pairs");
   __shared__ __attribute__((aligned(16))) char smem[2 * (BM + BN) * 128];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int vbid = xcd_remap(blockIdx.x, gridDim.x);
 
   // ---- which tile --------------------------------------------------------
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
   if constexpr (MODE == MODE_ROWS) {
-    nt = blockIdx.x / p.mt_bound;
-    const int ml = blockIdx.x % p.mt_bound;
+    // column tiles fastest: concurrent blocks share the A rows of one tile
+    const int ntn = p.ntiles;
+    nt = vbid % ntn;
+    const int ml = vbid / ntn;
     int acc_t = 0;
     mt = -1;
     for (e = 0; e < p.E; ++e) {
@@ -190,8 +379,8 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p) {
     row0 = p.offsets[e] + mt * BM;  // first global row of this tile
   } else {
     const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
-    e = blockIdx.x / (mtn * ntn);
-    const int rem = blockIdx.x % (mtn * ntn);
+    e = vbid / (mtn * ntn);
+    const int rem = vbid % (mtn * ntn);
     mt = rem / ntn;
     nt = rem % ntn;
     cnt_e = p.counts[e];
@@ -207,47 +396,34 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p) {
   int Kred;  // reduction length
   if constexpr (MODE == MODE_ROWS) Kred = p.K; else Kred = cnt_e;
 
-  KcLoader<BM> la;
-  MncLoader<BM> lam;
+  KcLoader<BM, NT> la;
+  MncLoader<BM, NT> lam;
   if constexpr (A_KC) {  // ROWS: A rows are the expert's rows
-    la.c = tid & 7;
-#pragma unroll
-    for (int q = 0; q < KcLoader<BM>::NP; ++q) {
-      const int i = (tid >> 3) + q * (kThreads / 8);
-      const int li = mt * BM + i;
-      la.ok[q] = li < cnt_e;
-      la.p0[q] = A + (long)(row0 + i) * p.lda;
-      la.p1[q] = la.p0[q];
-    }
+    const bf16_t* a0 = A + (long)row0 * p.lda;
+    la.init(a0, a0, p.lda, cnt_e - mt * BM);
   } else {  // KSUM: A[i][k] = A[(row0 + k) * lda + m0 + i]
-    lam.kg = tid % MncLoader<BM>::KG;
-    lam.g = tid / MncLoader<BM>::KG;
+    lam.kg = tid % MncLoader<BM, NT>::KG;
+    lam.g = tid / MncLoader<BM, NT>::KG;
     const int i0 = mt * BM + lam.g * 8;
     lam.ok = i0 < p.Mdim;
     lam.ld = p.lda;
     lam.col = A + (long)row0 * p.lda + i0;
   }
-  KcLoader<BN> lb;
-  MncLoader<BN> lbm;
+  KcLoader<BN, NT> lb;
+  MncLoader<BN, NT> lbm;
   if constexpr (B_KC) {  // ROWS dgrad: B[k][n] at B + e*estride + n*ldb + k
-    lb.c = tid & 7;
-#pragma unroll
-    for (int q = 0; q < KcLoader<BN>::NP; ++q) {
-      const int i = (tid >> 3) + q * (kThreads / 8);
-      const int n = n0 + i;
-      lb.ok[q] = n < p.N;
-      lb.p0[q] = B0 + (long)e * p.b_estride + (long)n * p.ldb;
-      lb.p1[q] = (B1 != nullptr) ? B1 + (long)e * p.b_estride + (long)n * p.ldb : lb.p0[q];
-    }
+    const bf16_t* b0 = B0 + (long)e * p.b_estride + (long)n0 * p.ldb;
+    const bf16_t* b1 = (B1 != nullptr) ? B1 + (long)e * p.b_estride + (long)n0 * p.ldb : b0;
+    lb.init(b0, b1, p.ldb, p.N - n0);
   } else {
-    lbm.kg = tid % MncLoader<BN>::KG;
-    lbm.g = tid / MncLoader<BN>::KG;
+    lbm.kg = tid % MncLoader<BN, NT>::KG;
+    lbm.g = tid / MncLoader<BN, NT>::KG;
     lbm.ld = p.ldb;
     if constexpr (MODE == MODE_ROWS) {
       const bf16_t* base = B0;
       int n = n0 + lbm.g * 8;
       if constexpr (EPI == EPI_SWIGLU_FWD) {
-        const int cc = lbm.g * 8;  // tile column
+        const int cc = lbm.g * 8;  // tile column: 32-column blocks alternate W1 / W3
         base = ((cc >> 5) & 1) ? B1 : B0;
         n = n0 + (cc >> 6) * 32 + (cc & 31);
       }
@@ -290,98 +466,325 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p) {
     if (more) load_tiles((kt + 1) * BK);
     const char* a_s = smem + (kt & 1) * (BM + BN) * 128;
     const char* b_s = a_s + BM * 128;
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
+    // fragments of step kk+1 are read while the MFMAs of step kk run
+    bf16x8 af[2][FM], bfr[2][FN];
+    auto read_frags = [&](int kk, int set) {
       const int ch = kk * 2 + (lane >> 5);
-      bf16x8 af[FM], bfr[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(a_s + lds_off(wm * WM + i * 32 + (lane & 31), ch));
+        af[set][i] = *reinterpret_cast<const bf16x8*>(a_s + lds_off(wm * WM + i * 32 + (lane & 31), ch));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(b_s + lds_off(wn * WN + j * 32 + (lane & 31), ch));
+        bfr[set][j] = *reinterpret_cast<const bf16x8*>(b_s + lds_off(wn * WN + j * 32 + (lane & 31), ch));
+    };
+    read_frags(0, 0);
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      if (kk + 1 < BK / 16) read_frags(kk + 1, (kk + 1) & 1);
+      // B as the first operand: the result tile is C^T, so each lane ends up
+      // with 4 consecutive output columns of one row
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i],
+                                                              acc[i][j], 0, 0, 0);
     }
     if (more) store_tiles((kt + 1) & 1);
     __syncthreads();
   }
 
-  // ---- epilogue ------------------------------------------------------------
-  // acc[i][j][r] holds row  wm*WM + i*32 + 8*(r/4) + 4*(lane/32) + r%4,
-  //                   col  wn*WN + j*32 + lane%32
-  const int lcol = lane & 31, lhalf = lane >> 5;
+  gemm_epilogue<MODE, EPI, BM, BN, NT>(p, acc, smem, e, mt, n0, row0, rows_e, cnt_e);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 kernel with direct-to-LDS operand streaming
+// ---------------------------------------------------------------------------
+// 256 x 256 block tile, 512 threads (2 x 4 waves of 128 x 64), BK = 32, a
+// ring of 4 LDS stages (32 KB each: A then B). Operands go global -> LDS with
+// bounds-checked buffer_load_dwordx4 ... lds (no staging registers; reads
+// past a buffer's range return zeros, which masks ragged expert rows and the
+// ragged reduction of the weight gradients). Each wave load fills one 1 KB
+// block of LDS in lane order; the source chunk of each lane is chosen so the
+// block holds the swizzled layout:
+//   K-contiguous operand: [256 rows][32 k] (64 B rows), chunk c of row r at
+//     physical chunk c ^ ((r / 4) % 4); fragments via ds_read_b128.
+//   M/N-contiguous operand: panels of [32 k][PW cols] (PW*2 B rows), 16-byte
+//     chunk m of row k at m ^ (4 * (k % 4)); fragments via two
+//     ds_read_b64_tr_b16, which hand lane l' of each 16-lane group element
+//     l' % 4 of lane 4q + l'/4 in slot q: lanes aimed at rows k0 + s/4,
+//     columns c0 + 4 (s % 4) receive the K-contiguous 4-vectors the MFMA wants.
+// Requires the reduction length of the row mode to be a multiple of 32.
+constexpr int DBK = 32;
+constexpr int DSTAGES = 4;
+constexpr int DSTAGE_BYTES = 32768;
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor (stride 0, byte offsets) whose range check covers
+// `bytes` from `base`: loads past it return zeros.
+__device__ __forceinline__ u32x4 make_rsrc(const void* base, long bytes) {
+  const unsigned long a = reinterpret_cast<unsigned long>(base);
+  const unsigned n = bytes <= 0 ? 0u : (bytes > 0x7FFFFFFFL ? 0x7FFFFFFFu : (unsigned)bytes);
+  u32x4 d;
+  d.x = __builtin_amdgcn_readfirstlane((unsigned)a);
+  d.y = __builtin_amdgcn_readfirstlane((unsigned)(a >> 32) & 0xFFFFu);
+  d.z = __builtin_amdgcn_readfirstlane(n);
+  d.w = 0x00020000u;
+  return d;
+}
+
+// One wave: 64 x 16 bytes from the buffer (per-lane byte offset voff) into
+// the 1 KB LDS block at lds_block, lane-ordered. Issued as inline assembly so
+// that the compiler does not pair it with the LDS reads of other stages: the
+// kernel orders them itself with s_waitcnt vmcnt and barriers.
+__device__ __forceinline__ void dma16(u32x4 d, char* lds_block, unsigned voff) {
+  const unsigned m0v =
+      __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_void_t*)lds_block);
+  unsigned saved;  // m0 is reserved: keep the compiler's value intact
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(d), "s"(m0v)
+      : "memory");
+}
+
+// wait until at most n vector-memory operations of this wave are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ int kc_off(int row, int chunk) {
+  return row * 64 + (((chunk ^ (row >> 2)) & 3) << 4);
+}
+
+// K-contiguous fragment: row `row`, k16 step kk
+__device__ __forceinline__ bf16x8 frag_kc(const char* region, int row, int kk, int lane) {
+  return *reinterpret_cast<const bf16x8*>(region + kc_off(row, kk * 2 + (lane >> 5)));
+}
+
+// M/N-contiguous fragment of 32 columns starting at tile column cb
+template <int PW>
+__device__ __forceinline__ bf16x8 frag_mnc(const char* region, int cb, int kk, int lane) {
+  const int G = lane >> 4, sl = lane & 15;
+  const int col = cb + (G & 1) * 16 + 4 * (sl & 3);
+  const int pc = col % PW;
+  const char* pb = region + (col / PW) * (DBK * PW * 2);
+  v4i16 h[2];
+#pragma unroll
+  for (int ins = 0; ins < 2; ++ins) {
+    const int k = kk * 16 + (G >> 1) * 8 + 4 * ins + (sl >> 2);
+    const char* a = pb + k * (PW * 2) + ((((pc >> 3) ^ ((k & 3) << 2))) << 4) + ((pc & 7) << 1);
+    h[ins] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)a);
+  }
+  const v4i16 lo = h[0], hi = h[1];
+  const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int MODE, bool A_KC, bool B_KC, int EPI>
+__global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
+  constexpr int BM = 256, BN = 256, NT = 512;
+  constexpr int WGN = 4, WM = 128, WN = 64, FM = 4, FN = 2;
+  constexpr bool DUAL = EPI == EPI_SWIGLU_FWD;
+  constexpr int BPW = DUAL ? 128 : 256;  // B panel width (M/N-contiguous B)
+  __shared__ __attribute__((aligned(1024))) char smem[DSTAGES * DSTAGE_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int vbid = xcd_remap(blockIdx.x, gridDim.x);
+
+  // ---- which tile (same scheme as gemm_bf16_kernel) ----
+  int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
   if constexpr (MODE == MODE_ROWS) {
-    bf16_t* C0 = static_cast<bf16_t*>(p.C0);
-    bf16_t* C1 = static_cast<bf16_t*>(p.C1);
-    const bf16_t* aux = static_cast<const bf16_t*>(p.aux);
+    nt = vbid % p.ntiles;
+    const int ml = vbid / p.ntiles;
+    int acc_t = 0;
+    mt = -1;
+    for (e = 0; e < p.E; ++e) {
+      const int c = p.counts[e];
+      const int r = p.padC ? p.padC : c;
+      const int te = (r + BM - 1) / BM;
+      if (ml < acc_t + te) {
+        mt = ml - acc_t;
+        rows_e = r;
+        cnt_e = c;
+        break;
+      }
+      acc_t += te;
+    }
+    if (mt < 0) return;
+    row0 = p.offsets[e] + mt * BM;
+  } else {
+    const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
+    e = vbid / (mtn * ntn);
+    const int rem = vbid % (mtn * ntn);
+    mt = rem / ntn;
+    nt = rem % ntn;
+    cnt_e = p.counts[e];
+    row0 = p.offsets[e];
+  }
+  constexpr int NCOLS = DUAL ? BN / 2 : BN;
+  const int n0 = nt * NCOLS;
+  const int Kred = (MODE == MODE_ROWS) ? p.K : cnt_e;
+  const int nk = (Kred + DBK - 1) / DBK;
+
+  const bf16_t* A = static_cast<const bf16_t*>(p.A);
+  const bf16_t* B0 = static_cast<const bf16_t*>(p.B0);
+  const bf16_t* B1 = static_cast<const bf16_t*>(p.B1);
+
+  // ---- buffer resources and per-lane source offsets (bytes, k0 = 0) ----
+  // Each thread issues 2 A and 2 B block loads per stage: blocks wave and wave + 8.
+  u32x4 ra, rb0, rb1;
+  unsigned aoff[2], boff[2];
+  int a_kstep, b_kstep;  // byte step per k-tile
+  if constexpr (A_KC) {  // rows of the expert: [rows][K]
+    const long valid = (long)(cnt_e - mt * BM) * p.lda;
+    ra = make_rsrc(A + (long)row0 * p.lda, valid * 2);
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
+    for (int i = 0; i < 2; ++i) {
+      const int b = wave + 8 * i, row = 16 * b + (lane >> 2);
+      const int c = (lane & 3) ^ ((row >> 2) & 3);
+      aoff[i] = (unsigned)(((long)row * p.lda + c * 8) * 2);
+    }
+    a_kstep = DBK * 2;
+  } else {  // KSUM: element (m, r) at A + (row0 + r) * lda + m; one panel of 256
+    const int m0 = mt * BM;
+    ra = make_rsrc(A + (long)row0 * p.lda + m0, ((long)cnt_e * p.lda - m0) * 2);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ti = wm * WM + i * 32 + 8 * (r >> 2) + 4 * lhalf + (r & 3);
-        const int li = mt * BM + ti;  // row within the expert
-        if (li >= rows_e) continue;
-        const bool data = li < cnt_e;
-        const long g = row0 + ti;
-        if constexpr (EPI == EPI_SWIGLU_FWD) {
-          const int n = n0 + wn * 32 + lcol;
-          if (n < p.N) {
-            const float h1 = data ? acc[i][0][r] : 0.f;
-            const float h3 = data ? acc[i][1][r] : 0.f;
-            C0[g * p.ldc + n] = f32_to_bf16(h1);
-            C0[g * p.ldc + p.Hh + n] = f32_to_bf16(h3);
-            C1[g * p.ldc1 + n] = f32_to_bf16(silu_f(h1) * h3);
-          }
-        } else {
+    for (int i = 0; i < 2; ++i) {
+      const int b = wave + 8 * i, kr = 2 * b + (lane >> 5);
+      const int cm = (lane & 31) ^ ((kr & 3) << 2);
+      aoff[i] = (unsigned)(((long)kr * p.lda + cm * 8) * 2);
+    }
+    a_kstep = DBK * p.lda * 2;
+  }
+  if constexpr (B_KC) {  // rows n: [N][K] per expert; k >= ksplit from B1
+    const long valid = (long)(p.N - n0) * p.ldb;
+    rb0 = make_rsrc(B0 + (long)e * p.b_estride + (long)n0 * p.ldb, valid * 2);
+    rb1 = (B1 != nullptr) ? make_rsrc(B1 + (long)e * p.b_estride + (long)n0 * p.ldb, valid * 2) : rb0;
 #pragma unroll
-          for (int j = 0; j < FN; ++j) {
-            const int n = n0 + wn * WN + j * 32 + lcol;
-            if (n >= p.N) continue;
-            const float v = data ? acc[i][j][r] : 0.f;
-            if constexpr (EPI == EPI_STORE) {
-              C0[g * p.ldc + n] = f32_to_bf16(v);
-            } else if constexpr (EPI == EPI_GELU_FWD) {
-              C0[g * p.ldc + n] = f32_to_bf16(v);
-              C1[g * p.ldc1 + n] = f32_to_bf16(gelu_f(v));
-            } else if constexpr (EPI == EPI_GELU_BWD) {
-              const float h = bf16_to_f32(aux[g * p.ldaux + n]);
-              C0[g * p.ldc + n] = f32_to_bf16(v * gelu_grad_f(h));
-            } else if constexpr (EPI == EPI_SWIGLU_BWD) {
-              const float h1 = bf16_to_f32(aux[g * p.ldaux + n]);
-              const float h3 = bf16_to_f32(aux[g * p.ldaux + p.Hh + n]);
-              const float sg = sigmoid_f(h1);
-              C0[g * p.ldc + n] = f32_to_bf16(v * h3 * sg * (1.f + h1 * (1.f - sg)));
-              C0[g * p.ldc + p.Hh + n] = f32_to_bf16(v * h1 * sg);
-            }
-          }
-        }
+    for (int i = 0; i < 2; ++i) {
+      const int b = wave + 8 * i, row = 16 * b + (lane >> 2);
+      const int c = (lane & 3) ^ ((row >> 2) & 3);
+      boff[i] = (unsigned)(((long)row * p.ldb + c * 8) * 2);
+    }
+    b_kstep = DBK * 2;
+  } else if constexpr (MODE == MODE_ROWS) {  // weights [K][N] per expert
+    const long span = (long)p.K * p.ldb;
+    if constexpr (DUAL) {  // panel 0: W1 columns n0.., panel 1: W3 columns n0..
+      rb0 = make_rsrc(B0 + (long)e * p.b_estride + n0, (span - n0) * 2);
+      rb1 = make_rsrc(B1 + (long)e * p.b_estride + n0, (span - n0) * 2);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int b = wave + 8 * i, kr = 4 * (b & 7) + (lane >> 4);
+        const int cm = (lane & 15) ^ ((kr & 3) << 2);
+        boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
+      }
+    } else {
+      rb0 = make_rsrc(B0 + (long)e * p.b_estride + n0, (span - n0) * 2);
+      rb1 = rb0;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int b = wave + 8 * i, kr = 2 * b + (lane >> 5);
+        const int cm = (lane & 31) ^ ((kr & 3) << 2);
+        boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
       }
     }
-  } else {  // KSUM wgrad, fp32 out
-    float* C0 = static_cast<float*>(p.C0);
-    float* C1 = static_cast<float*>(p.C1);
+    b_kstep = DBK * p.ldb * 2;
+  } else {  // KSUM: element (r, n) at B + (row0 + r) * ldb + n
+    rb0 = make_rsrc(B0 + (long)row0 * p.ldb + n0, ((long)cnt_e * p.ldb - n0) * 2);
+    rb1 = rb0;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
+    for (int i = 0; i < 2; ++i) {
+      const int b = wave + 8 * i, kr = 2 * b + (lane >> 5);
+      const int cm = (lane & 31) ^ ((kr & 3) << 2);
+      boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
+    }
+    b_kstep = DBK * p.ldb * 2;
+  }
+
+  auto issue = [&](int kt, int stage) {
+    char* sa = smem + stage * DSTAGE_BYTES;
+    char* sb = sa + DSTAGE_BYTES / 2;
+    const unsigned ka = (unsigned)kt * (unsigned)a_kstep;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = mt * BM + wm * WM + i * 32 + 8 * (r >> 2) + 4 * lhalf + (r & 3);
-        if (m >= p.Mdim) continue;
+    for (int i = 0; i < 2; ++i) dma16(ra, sa + (wave + 8 * i) * 1024, aoff[i] + ka);
+    if constexpr (B_KC) {
+      const int k0 = kt * DBK;
+      const bool second = k0 >= p.ksplit;
+      const unsigned kb = (unsigned)((second ? k0 - p.ksplit : k0) * 2);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int n = n0 + wn * WN + j * 32 + lcol;
-          if (n >= p.N) continue;
-          float* dst = (n < p.nsplit) ? C0 + (long)e * p.c_estride + (long)m * p.ldc + n
-                                      : C1 + (long)e * p.c_estride + (long)m * p.ldc + (n - p.nsplit);
-          const float v = acc[i][j][r];
-          *dst = p.accumulate ? *dst + v : v;
-        }
+      for (int i = 0; i < 2; ++i)
+        dma16(second ? rb1 : rb0, sb + (wave + 8 * i) * 1024, boff[i] + kb);
+    } else {
+      const unsigned kb = (unsigned)kt * (unsigned)b_kstep;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        dma16((DUAL && i == 1) ? rb1 : rb0, sb + (wave + 8 * i) * 1024, boff[i] + kb);
+    }
+  };
+
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+#pragma unroll
+  for (int s = 0; s < DSTAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    // this thread's loads of tile kt are done when at most the loads of the
+    // (up to two) younger tiles are outstanding
+    if (kt + 2 < nk) wait_vmcnt<8>();
+    else if (kt + 1 < nk) wait_vmcnt<4>();
+    else wait_vmcnt<0>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();  // every wave's tile kt is in LDS; stage kt-1 is free
+    asm volatile("" ::: "memory");
+    if (kt + DSTAGES - 1 < nk) issue(kt + DSTAGES - 1, (kt + DSTAGES - 1) % DSTAGES);
+    const char* sa = smem + (kt % DSTAGES) * DSTAGE_BYTES;
+    const char* sb = sa + DSTAGE_BYTES / 2;
+#pragma unroll
+    for (int kk = 0; kk < DBK / 16; ++kk) {
+      bf16x8 af[FM], bfr[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        if constexpr (A_KC)
+          af[i] = frag_kc(sa, wm * WM + i * 32 + (lane & 31), kk, lane);
+        else
+          af[i] = frag_mnc<256>(sa, wm * WM + i * 32, kk, lane);
       }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        if constexpr (B_KC)
+          bfr[j] = frag_kc(sb, wn * WN + j * 32 + (lane & 31), kk, lane);
+        else if constexpr (DUAL)
+          bfr[j] = frag_mnc<BPW>(sb, j * 128 + wn * 32, kk, lane);
+        else
+          bfr[j] = frag_mnc<BPW>(sb, wn * WN + j * 32, kk, lane);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
     }
   }
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();  // all LDS reads done before the epilogue reuses the stages
+  gemm_epilogue<MODE, EPI, BM, BN, NT>(p, acc, smem, e, mt, n0, row0, rows_e, cnt_e);
 }
 
 // ---------------------------------------------------------------------------
@@ -543,21 +946,51 @@ GemmParams base_params(const Shape& s, const int32_t* counts, const int32_t* off
   return p;
 }
 
-template <int MODE, bool A_KC, bool B_KC, int EPI, int BM, int BN>
+template <int MODE, bool A_KC, bool B_KC, int EPI, int BM, int BN, int NT>
 hipError_t run_bf16(int kind, const Shape& s, GemmParams p, hipStream_t st) {
   long blocks;
   if (MODE == MODE_ROWS) {
     const int ncols = (EPI == EPI_SWIGLU_FWD) ? BN / 2 : BN;
     p.mt_bound = rows_tiles_bound(s, BM);
-    blocks = (long)p.mt_bound * ((p.N + ncols - 1) / ncols);
+    p.ntiles = (p.N + ncols - 1) / ncols;
+    blocks = (long)p.mt_bound * p.ntiles;
   } else {
     blocks = (long)s.E * ((p.Mdim + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   }
   if (blocks == 0) return hipSuccess;
   return traced(kind, st, [&] {
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, A_KC, B_KC, EPI, BM, BN>), dim3((unsigned)blocks),
-                       dim3(kThreads), 0, st, p);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, A_KC, B_KC, EPI, BM, BN, NT>),
+                       dim3((unsigned)blocks), dim3(NT), 0, st, p);
   });
+}
+
+template <int MODE, bool A_KC, bool B_KC, int EPI>
+hipError_t run_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
+  long blocks;
+  if (MODE == MODE_ROWS) {
+    const int ncols = (EPI == EPI_SWIGLU_FWD) ? 128 : 256;
+    p.mt_bound = rows_tiles_bound(s, 256);
+    p.ntiles = (p.N + ncols - 1) / ncols;
+    blocks = (long)p.mt_bound * p.ntiles;
+  } else {
+    blocks = (long)s.E * ((p.Mdim + 255) / 256) * ((p.N + 255) / 256);
+  }
+  if (blocks == 0) return hipSuccess;
+  return traced(kind, st, [&] {
+    hipLaunchKernelGGL((gemm_dma_kernel<MODE, A_KC, B_KC, EPI>), dim3((unsigned)blocks), dim3(512),
+                       0, st, p);
+  });
+}
+
+// The streaming kernel needs the row-mode reduction length (and a K split)
+// to be a multiple of its 32-deep k-tile; otherwise the register-staged
+// kernel runs.
+template <int MODE, bool A_KC, bool B_KC, int EPI>
+hipError_t run_gemm_bf16(int kind, const Shape& s, GemmParams p, hipStream_t st) {
+  const bool dma_ok = MODE == MODE_KSUM ||
+                      (p.K % DBK == 0 && (p.ksplit >= p.K || p.ksplit % DBK == 0));
+  if (dma_ok) return run_dma<MODE, A_KC, B_KC, EPI>(kind, s, p, st);
+  return run_bf16<MODE, A_KC, B_KC, EPI, 256, 256, 512>(kind, s, p, st);
 }
 
 template <int MODE, bool B_KC, int EPI>
@@ -612,9 +1045,9 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
   p.ldc1 = H;
   if (s.dtype == FLOWMOE_BF16) {
     if (swiglu)
-      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, false, EPI_SWIGLU_FWD, 128, 128>(FLOWMOE_K_FFN1, s, p, st)));
+      FLOWMOE_TRY((run_gemm_bf16<MODE_ROWS, true, false, EPI_SWIGLU_FWD>(FLOWMOE_K_FFN1, s, p, st)));
     else
-      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, false, EPI_GELU_FWD, 128, 128>(FLOWMOE_K_FFN1, s, p, st)));
+      FLOWMOE_TRY((run_gemm_bf16<MODE_ROWS, true, false, EPI_GELU_FWD>(FLOWMOE_K_FFN1, s, p, st)));
   } else {
     if (swiglu) {
       p.B1 = nullptr;
@@ -643,7 +1076,7 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
   q.C0 = y_disp;
   q.ldc = M;
   if (s.dtype == FLOWMOE_BF16)
-    return run_bf16<MODE_ROWS, true, false, EPI_STORE, 128, 128>(FLOWMOE_K_FFN2, s, q, st);
+    return run_gemm_bf16<MODE_ROWS, true, false, EPI_STORE>(FLOWMOE_K_FFN2, s, q, st);
   return run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN2, s, q, st);
 }
 
@@ -673,9 +1106,9 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.ldaux = HW;
     if (bf) {
       if (swiglu)
-        FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_SWIGLU_BWD, 128, 128>(FLOWMOE_K_DGRAD1, s, p, st)));
+        FLOWMOE_TRY((run_gemm_bf16<MODE_ROWS, true, true, EPI_SWIGLU_BWD>(FLOWMOE_K_DGRAD1, s, p, st)));
       else
-        FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_GELU_BWD, 128, 128>(FLOWMOE_K_DGRAD1, s, p, st)));
+        FLOWMOE_TRY((run_gemm_bf16<MODE_ROWS, true, true, EPI_GELU_BWD>(FLOWMOE_K_DGRAD1, s, p, st)));
     } else {
       if (swiglu)
         FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_SWIGLU_BWD>(FLOWMOE_K_DGRAD1, s, p, st)));
@@ -697,7 +1130,7 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.c_estride = (long)H * M;
     p.accumulate = accumulate;
     if (bf)
-      FLOWMOE_TRY((run_bf16<MODE_KSUM, false, false, EPI_WGRAD, 128, 128>(FLOWMOE_K_WGRAD2, s, p, st)));
+      FLOWMOE_TRY((run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(FLOWMOE_K_WGRAD2, s, p, st)));
     else
       FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD2, s, p, st)));
   }
@@ -717,7 +1150,7 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.c_estride = (long)M * H;
     p.accumulate = accumulate;
     if (bf)
-      FLOWMOE_TRY((run_bf16<MODE_KSUM, false, false, EPI_WGRAD, 128, 128>(FLOWMOE_K_WGRAD1, s, p, st)));
+      FLOWMOE_TRY((run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
     else
       FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
   }
@@ -736,7 +1169,7 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.C0 = dx_disp;
     p.ldc = M;
     if (bf)
-      FLOWMOE_TRY((run_bf16<MODE_ROWS, true, true, EPI_STORE, 128, 128>(FLOWMOE_K_DGRAD2, s, p, st)));
+      FLOWMOE_TRY((run_gemm_bf16<MODE_ROWS, true, true, EPI_STORE>(FLOWMOE_K_DGRAD2, s, p, st)));
     else
       FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_STORE>(FLOWMOE_K_DGRAD2, s, p, st)));
   }

@@ -112,13 +112,17 @@ def test_dispatch(T, E, k, cf, layout):
         assert np.array_equal(host(g["x_disp"][:live]), xd[:live]), C
 
 
+@pytest.mark.parametrize("MH", [(200, 264), (224, 288)], ids=["staged", "streaming"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
-def test_expert_ffn_fwd_bwd(dtype, act, layout):
+def test_expert_ffn_fwd_bwd(dtype, act, layout, MH):
+    """(200, 264): reductions not multiples of 32 (register-staged bf16 GEMM);
+    (224, 288): multiples of 32 (LDS-streaming bf16 GEMM); both ragged."""
     need_gpu()
     rng = np.random.default_rng(3)
-    E, k, M, H = 6, 1, 200, 264
+    E, k = 6, 1
+    M, H = MH
     # per-expert counts spanning empty, tiny, tile-exact and ragged groups
     cnt = np.array([0, 1, 127, 128, 129, 300])
     C = 300
