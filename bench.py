@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--R", type=int, default=None, help="override the chunk count")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="after the timed steps, copy a MIB-sized buffer once: the plain copy "
+                         "kernel of known size that calibrates HBM byte counters")
     return ap.parse_args()
 
 
@@ -139,6 +142,29 @@ def main():
     avg_launch_ms = sum(gemm_ms) / max(1, len(gemm_ms))
     achieved_tflops = tot_flops / tot_s / 1e12 if tot_s > 0 else 0.0
 
+    if a.copy_probe > 0:
+        n = a.copy_probe * 2**20 // 4
+        src = torch.ones(n, device=dev, dtype=torch.float32)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # HBM traffic of the grouped GEMM per launch, from the PMC passes kept
+    # under profiles/ for this workload, if they were taken on this kernel source
+    traffic, traffic_note = None, "no PMC summary for this workload"
+    tpath = os.path.join(ROOT, "profiles", f"gemm_traffic_{cfg.name}.json")
+    if os.path.exists(tpath):
+        from paper_2510_00207_amd.profsum import gemm_source_hash
+        tj = json.load(open(tpath))
+        if tj.get("gemm_source_sha256") == gemm_source_hash():
+            traffic = round(tj["gemm_bytes_per_launch"])
+            traffic_note = (f"HBM bytes per launch (FETCH_SIZE x{tj['fetch_scale']} + WRITE_SIZE "
+                            f"x{tj['write_scale']}, scaled by a {tj['probe_mib']} MiB copy probe)")
+        else:
+            traffic_note = "kernel changed since the PMC summary was taken"
+
     cpu = None
     if not a.no_cpu_baseline:
         import oracle
@@ -182,13 +208,14 @@ def main():
             "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "kept_rows": kept,
         },
         "roofline": {
-            "kernel": "grouped GEMM (gemm_bf16_kernel, all 6 launches of a step)",
+            "kernel": "grouped GEMM (gemm_dma_kernel, all 6 launches of a step)",
             "bound": "mfma",
             "achieved": round(achieved_tflops, 2),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_note": traffic_note,
             "flops_per_launch": fl,
             "avg_launch_us": round(avg_launch_ms * 1e3, 2),
             "launches": len(gemm_ms),

@@ -554,10 +554,12 @@ __device__ __forceinline__ void dma16(u32x4 d, char* lds_block, unsigned voff) {
       : "memory");
 }
 
-// wait until at most n vector-memory operations of this wave are outstanding
+
+// wait until at most n vector-memory operations and no LDS operation of this
+// wave are outstanding
 template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
 __device__ __forceinline__ int kc_off(int row, int chunk) {
@@ -588,12 +590,16 @@ __device__ __forceinline__ bf16x8 frag_mnc(const char* region, int cb, int kk, i
   return __builtin_bit_cast(bf16x8, v);
 }
 
-template <int MODE, bool A_KC, bool B_KC, int EPI>
-__global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
-  constexpr int BM = 256, BN = 256, NT = 512;
-  constexpr int WGN = 4, WM = 128, WN = 64, FM = 4, FN = 2;
+template <int MODE, bool A_KC, bool B_KC, int EPI, int WGN>
+__global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
+  // WGN waves along N, two along M: WGN = 4 -> 8 waves of 128 x 64;
+  // WGN = 2 -> 4 waves of 128 x 128 (half the LDS fragment traffic per MFMA)
+  constexpr int BM = 256, BN = 256, NT = 128 * WGN;
+  constexpr int NW = NT / 64;         // waves
+  constexpr int BPW = 16 / NW;        // 1 KB LDS blocks per operand per wave per stage
+  constexpr int WM = 128, WN = BN / WGN, FM = 4, FN = WN / 32;
   constexpr bool DUAL = EPI == EPI_SWIGLU_FWD;
-  constexpr int BPW = DUAL ? 128 : 256;  // B panel width (M/N-contiguous B)
+  constexpr int PWB = DUAL ? 128 : 256;  // B panel width (M/N-contiguous B)
   __shared__ __attribute__((aligned(1024))) char smem[DSTAGES * DSTAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -640,16 +646,16 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
   const bf16_t* B1 = static_cast<const bf16_t*>(p.B1);
 
   // ---- buffer resources and per-lane source offsets (bytes, k0 = 0) ----
-  // Each thread issues 2 A and 2 B block loads per stage: blocks wave and wave + 8.
+  // Each wave issues BPW A and BPW B block loads per stage: blocks wave + NW*i.
   u32x4 ra, rb0, rb1;
-  unsigned aoff[2], boff[2];
+  unsigned aoff[BPW], boff[BPW];
   int a_kstep, b_kstep;  // byte step per k-tile
   if constexpr (A_KC) {  // rows of the expert: [rows][K]
     const long valid = (long)(cnt_e - mt * BM) * p.lda;
     ra = make_rsrc(A + (long)row0 * p.lda, valid * 2);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int b = wave + 8 * i, row = 16 * b + (lane >> 2);
+    for (int i = 0; i < BPW; ++i) {
+      const int b = wave + NW * i, row = 16 * b + (lane >> 2);
       const int c = (lane & 3) ^ ((row >> 2) & 3);
       aoff[i] = (unsigned)(((long)row * p.lda + c * 8) * 2);
     }
@@ -658,8 +664,8 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     const int m0 = mt * BM;
     ra = make_rsrc(A + (long)row0 * p.lda + m0, ((long)cnt_e * p.lda - m0) * 2);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int b = wave + 8 * i, kr = 2 * b + (lane >> 5);
+    for (int i = 0; i < BPW; ++i) {
+      const int b = wave + NW * i, kr = 2 * b + (lane >> 5);
       const int cm = (lane & 31) ^ ((kr & 3) << 2);
       aoff[i] = (unsigned)(((long)kr * p.lda + cm * 8) * 2);
     }
@@ -670,8 +676,8 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     rb0 = make_rsrc(B0 + (long)e * p.b_estride + (long)n0 * p.ldb, valid * 2);
     rb1 = (B1 != nullptr) ? make_rsrc(B1 + (long)e * p.b_estride + (long)n0 * p.ldb, valid * 2) : rb0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int b = wave + 8 * i, row = 16 * b + (lane >> 2);
+    for (int i = 0; i < BPW; ++i) {
+      const int b = wave + NW * i, row = 16 * b + (lane >> 2);
       const int c = (lane & 3) ^ ((row >> 2) & 3);
       boff[i] = (unsigned)(((long)row * p.ldb + c * 8) * 2);
     }
@@ -682,8 +688,8 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
       rb0 = make_rsrc(B0 + (long)e * p.b_estride + n0, (span - n0) * 2);
       rb1 = make_rsrc(B1 + (long)e * p.b_estride + n0, (span - n0) * 2);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int b = wave + 8 * i, kr = 4 * (b & 7) + (lane >> 4);
+      for (int i = 0; i < BPW; ++i) {
+        const int b = wave + NW * i, kr = 4 * (b & 7) + (lane >> 4);
         const int cm = (lane & 15) ^ ((kr & 3) << 2);
         boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
       }
@@ -691,8 +697,8 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
       rb0 = make_rsrc(B0 + (long)e * p.b_estride + n0, (span - n0) * 2);
       rb1 = rb0;
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int b = wave + 8 * i, kr = 2 * b + (lane >> 5);
+      for (int i = 0; i < BPW; ++i) {
+        const int b = wave + NW * i, kr = 2 * b + (lane >> 5);
         const int cm = (lane & 31) ^ ((kr & 3) << 2);
         boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
       }
@@ -702,8 +708,8 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     rb0 = make_rsrc(B0 + (long)row0 * p.ldb + n0, ((long)cnt_e * p.ldb - n0) * 2);
     rb1 = rb0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int b = wave + 8 * i, kr = 2 * b + (lane >> 5);
+    for (int i = 0; i < BPW; ++i) {
+      const int b = wave + NW * i, kr = 2 * b + (lane >> 5);
       const int cm = (lane & 31) ^ ((kr & 3) << 2);
       boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
     }
@@ -715,19 +721,19 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     char* sb = sa + DSTAGE_BYTES / 2;
     const unsigned ka = (unsigned)kt * (unsigned)a_kstep;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) dma16(ra, sa + (wave + 8 * i) * 1024, aoff[i] + ka);
+    for (int i = 0; i < BPW; ++i) dma16(ra, sa + (wave + NW * i) * 1024, aoff[i] + ka);
     if constexpr (B_KC) {
       const int k0 = kt * DBK;
       const bool second = k0 >= p.ksplit;
       const unsigned kb = (unsigned)((second ? k0 - p.ksplit : k0) * 2);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        dma16(second ? rb1 : rb0, sb + (wave + 8 * i) * 1024, boff[i] + kb);
+      for (int i = 0; i < BPW; ++i)
+        dma16(second ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
     } else {
       const unsigned kb = (unsigned)kt * (unsigned)b_kstep;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        dma16((DUAL && i == 1) ? rb1 : rb0, sb + (wave + 8 * i) * 1024, boff[i] + kb);
+      for (int i = 0; i < BPW; ++i)  // blocks 8..15 (i >= BPW/2, as wave < NW) hold the W3 panel
+        dma16((DUAL && i >= BPW / 2) ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
     }
   };
 
@@ -739,47 +745,99 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-#pragma unroll
-  for (int s = 0; s < DSTAGES - 1; ++s)
-    if (s < nk) issue(s, s);
-
-  for (int kt = 0; kt < nk; ++kt) {
-    // this thread's loads of tile kt are done when at most the loads of the
-    // (up to two) younger tiles are outstanding
-    if (kt + 2 < nk) wait_vmcnt<8>();
-    else if (kt + 1 < nk) wait_vmcnt<4>();
-    else wait_vmcnt<0>();
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();  // every wave's tile kt is in LDS; stage kt-1 is free
-    asm volatile("" ::: "memory");
-    if (kt + DSTAGES - 1 < nk) issue(kt + DSTAGES - 1, (kt + DSTAGES - 1) % DSTAGES);
-    const char* sa = smem + (kt % DSTAGES) * DSTAGE_BYTES;
+  // Fragments of one 16-deep k step; two sets so that the LDS reads of the
+  // next step are in flight while the MFMAs of the current one run.
+  bf16x8 af[2][FM], bfr[2][FN];
+  auto read_frags = [&](int stage, int kk, int set) {
+    const char* sa = smem + stage * DSTAGE_BYTES;
     const char* sb = sa + DSTAGE_BYTES / 2;
 #pragma unroll
-    for (int kk = 0; kk < DBK / 16; ++kk) {
-      bf16x8 af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        if constexpr (A_KC)
-          af[i] = frag_kc(sa, wm * WM + i * 32 + (lane & 31), kk, lane);
-        else
-          af[i] = frag_mnc<256>(sa, wm * WM + i * 32, kk, lane);
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        if constexpr (B_KC)
-          bfr[j] = frag_kc(sb, wn * WN + j * 32 + (lane & 31), kk, lane);
-        else if constexpr (DUAL)
-          bfr[j] = frag_mnc<BPW>(sb, j * 128 + wn * 32, kk, lane);
-        else
-          bfr[j] = frag_mnc<BPW>(sb, wn * WN + j * 32, kk, lane);
-      }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+    for (int i = 0; i < FM; ++i) {
+      if constexpr (A_KC)
+        af[set][i] = frag_kc(sa, wm * WM + i * 32 + (lane & 31), kk, lane);
+      else
+        af[set][i] = frag_mnc<256>(sa, wm * WM + i * 32, kk, lane);
     }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      if constexpr (B_KC)
+        bfr[set][j] = frag_kc(sb, wn * WN + j * 32 + (lane & 31), kk, lane);
+      else if constexpr (DUAL)  // pairs (h1, h3) of 32 columns: W1 panel, W3 panel
+        bfr[set][j] = frag_mnc<PWB>(sb, (j & 1) * 128 + wn * (WN / 2) + (j >> 1) * 32, kk, lane);
+      else
+        bfr[set][j] = frag_mnc<PWB>(sb, wn * WN + j * 32, kk, lane);
+    }
+  };
+  // LDS read instructions per fragment set (ds_read_b128 for a K-contiguous
+  // fragment, two ds_read_b64_tr_b16 for an M/N-contiguous one)
+  constexpr int NRD = FM * (A_KC ? 1 : 2) + FN * (B_KC ? 1 : 2);
+  constexpr int NMF = FM * FN;
+  auto mfmas = [&](int set) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[set][j], af[set][i], acc[i][j], 0, 0, 0);
+  };
+  // interleave the MFMAs of one set with the LDS reads of the other
+  auto interleave = [&]() {
+#pragma unroll
+    for (int q = 0; q < NRD; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
+      __builtin_amdgcn_sched_group_barrier(0x008, (NMF + NRD - 1) / NRD, 0);  // MFMAs
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);  // the rest of the MFMAs
+  };
+
+  // Ring of DSTAGES k-tiles: tile t lives in stage t % DSTAGES. Every wave
+  // loads its share of each tile; a barrier after a wave's own loads of tile
+  // t have landed (s_waitcnt vmcnt) makes the whole tile visible. Tile t's
+  // stage is refilled (tile t + DSTAGES) only after the barrier that follows
+  // every wave's last LDS read of tile t.
+#pragma unroll
+  for (int s = 0; s < DSTAGES; ++s)
+    if (s < nk) issue(s, s);
+
+  // wait until this wave's loads of tile t have landed, given that the loads
+  // of tiles up to min(t + ahead, nk - 1) have been issued
+  auto wait_tile = [&](int t, int ahead) {
+    const int younger = min(ahead, nk - 1 - t);  // tiles issued after t
+    if (younger >= 3) wait_vm_lgkm0<6 * BPW>();
+    else if (younger == 2) wait_vm_lgkm0<4 * BPW>();
+    else if (younger == 1) wait_vm_lgkm0<2 * BPW>();
+    else wait_vm_lgkm0<0>();
+  };
+
+  if (nk > 0) {
+    wait_tile(0, DSTAGES - 1);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    read_frags(0, 0, 0);
+  }
+  // All tiles but the last: the barrier sits between the two k steps, so
+  // each half pairs the MFMAs of one step with the reads of the next.
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const int stage = kt % DSTAGES;
+    read_frags(stage, 1, 1);  // step 1 of tile kt ...
+    mfmas(0);                 // ... while step 0 of tile kt runs
+    interleave();
+    // this wave's reads of tile kt are done (lgkmcnt 0) and its loads of
+    // tile kt + 1 have landed; after the barrier every wave's have
+    wait_tile(kt + 1, DSTAGES - 2);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (kt + DSTAGES < nk) issue(kt + DSTAGES, stage);
+    read_frags((kt + 1) % DSTAGES, 0, 0);  // step 0 of tile kt + 1 ...
+    mfmas(1);                              // ... while step 1 of tile kt runs
+    interleave();
+  }
+  if (nk > 0) {
+    read_frags((nk - 1) % DSTAGES, 1, 1);
+    mfmas(0);
+    interleave();
+    mfmas(1);
   }
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0);
@@ -964,8 +1022,15 @@ hipError_t run_bf16(int kind, const Shape& s, GemmParams p, hipStream_t st) {
   });
 }
 
+// wave layout of the streaming kernel (waves along N): 8 waves of 128 x 64.
+// Measured on the balanced layer, 4 waves of 128 x 128 (one per SIMD) were
+// 10-20% slower: with a single wave per SIMD nothing hides its barrier waits.
+constexpr int kDmaWgnRows = 4;
+constexpr int kDmaWgnKsum = 4;
+
 template <int MODE, bool A_KC, bool B_KC, int EPI>
 hipError_t run_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
+  constexpr int WGN = (MODE == MODE_ROWS) ? kDmaWgnRows : kDmaWgnKsum;
   long blocks;
   if (MODE == MODE_ROWS) {
     const int ncols = (EPI == EPI_SWIGLU_FWD) ? 128 : 256;
@@ -977,8 +1042,8 @@ hipError_t run_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
   }
   if (blocks == 0) return hipSuccess;
   return traced(kind, st, [&] {
-    hipLaunchKernelGGL((gemm_dma_kernel<MODE, A_KC, B_KC, EPI>), dim3((unsigned)blocks), dim3(512),
-                       0, st, p);
+    hipLaunchKernelGGL((gemm_dma_kernel<MODE, A_KC, B_KC, EPI, WGN>), dim3((unsigned)blocks),
+                       dim3(128 * WGN), 0, st, p);
   });
 }
 

@@ -1,0 +1,138 @@
+"""Summaries of rocprofv3 output for the measurements kept under profiles/.
+
+    python -m paper_2510_00207_amd.profsum trace DIR --out FILE.md --command "..."
+        kernel-trace statistics (run_kernel_stats.csv) as a markdown table
+
+    python -m paper_2510_00207_amd.profsum traffic FETCH_DIR WRITE_DIR --probe-mib N
+            --out FILE.json --md FILE.md --command "..."
+        HBM bytes per dispatch from two PMC passes (FETCH_SIZE, then WRITE_SIZE,
+        KiB per dispatch), each scaled by what the same counter reads for the
+        plain copy of N MiB that bench.py --copy-probe N runs last; the grouped
+        GEMM's average over its launches is stored with a hash of the kernel
+        source, so a later kernel change is detected and the figure dropped.
+
+Reads CSV files only; runs nothing on the GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import hashlib
+import json
+import os
+import re
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+GEMM_SOURCES = ("csrc/gemm.hip", "csrc/common.hpp")
+GEMM_KERNEL = "gemm_dma_kernel"
+
+
+def gemm_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in GEMM_SOURCES:
+        with open(os.path.join(PKG, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def short_name(name: str) -> str:
+    name = re.sub(r"^void ", "", name).replace("flowmoe::(anonymous namespace)::", "")
+    return re.sub(r"\((flowmoe|GemmParams|unsigned|int const|float const|HIP_vector).*$", "", name)
+
+
+def cmd_trace(a) -> None:
+    rows = list(csv.DictReader(open(os.path.join(a.dir, "run_kernel_stats.csv"))))
+    lines = [f"# {a.title}", "", "Command (repo root on the GPU box, MI355X):", "",
+             f"    {a.command}", "",
+             "| kernel | calls | avg us | min us | max us | total ms |",
+             "|---|---|---|---|---|---|"]
+    for r in rows:
+        nm = short_name(r["Name"])
+        if nm.startswith("at::") or "rocclr" in nm:
+            continue
+        lines.append(f"| `{nm}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.3f} |")
+    if a.note:
+        lines += ["", a.note]
+    open(a.out, "w").write("\n".join(lines) + "\n")
+
+
+def _pmc(dirname: str, counter: str):
+    """dispatch id -> (short kernel name, counter value in bytes)"""
+    out = {}
+    for r in csv.DictReader(open(os.path.join(dirname, "run_counter_collection.csv"))):
+        if r["Counter_Name"] != counter:
+            continue
+        d = int(r["Dispatch_Id"])
+        nm, v = short_name(r["Kernel_Name"]), float(r["Counter_Value"]) * 1024.0
+        out[d] = (nm, out.get(d, (nm, 0.0))[1] + v)
+    return out
+
+
+def cmd_traffic(a) -> None:
+    fetch, write = _pmc(a.fetch_dir, "FETCH_SIZE"), _pmc(a.write_dir, "WRITE_SIZE")
+    probe = float(a.probe_mib) * 2**20
+
+    def probe_value(tab):  # the copy probe is the last copy kernel of the run
+        copies = [d for d, (nm, _) in tab.items() if "copyBuffer" in nm or "copy" in nm.lower()]
+        return tab[max(copies)][1]
+
+    f_scale, w_scale = probe / probe_value(fetch), probe / probe_value(write)
+    per = collections.defaultdict(lambda: [[], []])
+    for d, (nm, v) in fetch.items():
+        per[nm][0].append(v * f_scale)
+    for d, (nm, v) in write.items():
+        per[nm][1].append(v * w_scale)
+    kernels = {}
+    for nm, (fv, wv) in sorted(per.items()):
+        if nm.startswith("at::") or "rocclr" in nm:
+            continue
+        kernels[nm] = {"dispatches": len(fv), "fetch_bytes": sum(fv) / max(1, len(fv)),
+                       "write_bytes": sum(wv) / max(1, len(wv))}
+    gemm = [(sum(per[nm][0]) + sum(per[nm][1]), len(per[nm][0]))
+            for nm in per if nm.startswith(GEMM_KERNEL)]
+    tot, n = sum(g[0] for g in gemm), sum(g[1] for g in gemm)
+    res = {"gemm_source_sha256": gemm_source_hash(), "command": a.command,
+           "probe_mib": a.probe_mib, "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+           "gemm_bytes_per_launch": tot / max(1, n), "gemm_launches": n, "kernels": kernels}
+    json.dump(res, open(a.out, "w"), indent=1)
+    if a.md:
+        lines = [f"# {a.title}", "", "Commands (repo root on the GPU box, MI355X), one pass per counter:", "",
+                 f"    {a.command}", "",
+                 f"Calibration: the {a.probe_mib} MiB copy probe read FETCH_SIZE x{f_scale:.3f} and "
+                 f"WRITE_SIZE x{w_scale:.3f} of its true bytes; the figures below are scaled by those "
+                 "factors (MiB per dispatch).", "",
+                 "| kernel | dispatches | fetch MiB | write MiB |", "|---|---|---|---|"]
+        for nm, k in kernels.items():
+            lines.append(f"| `{nm}` | {k['dispatches']} | {k['fetch_bytes'] / 2**20:.1f} | "
+                         f"{k['write_bytes'] / 2**20:.1f} |")
+        lines += ["", f"Grouped GEMM ({GEMM_KERNEL}), average over its {n} launches: "
+                      f"{res['gemm_bytes_per_launch'] / 2**20:.1f} MiB of HBM traffic per launch."]
+        open(a.md, "w").write("\n".join(lines) + "\n")
+
+
+def main() -> None:
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    t = sub.add_parser("trace")
+    t.add_argument("dir")
+    t.add_argument("--out", required=True)
+    t.add_argument("--title", default="Kernel trace")
+    t.add_argument("--command", required=True)
+    t.add_argument("--note", default="")
+    p = sub.add_parser("traffic")
+    p.add_argument("fetch_dir")
+    p.add_argument("write_dir")
+    p.add_argument("--probe-mib", type=int, required=True)
+    p.add_argument("--out", required=True)
+    p.add_argument("--md", default="")
+    p.add_argument("--title", default="HBM traffic per dispatch")
+    p.add_argument("--command", required=True)
+    a = ap.parse_args()
+    cmd_trace(a) if a.cmd == "trace" else cmd_traffic(a)
+
+
+if __name__ == "__main__":
+    main()
