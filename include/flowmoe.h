@@ -11,6 +11,9 @@
  *  - All tensor pointers are DEVICE pointers owned by the caller, row-major
  *    and contiguous. The library never allocates or frees device memory and
  *    never synchronises the device: work is enqueued on the stream(s) given.
+ *  - Tensors of the layer dtype (x, W_g, W1, W3, W2, the row buffers, y, dy,
+ *    dx) must be 16-byte aligned (FLOWMOE_ERR_INVALID otherwise): kernels
+ *    move them in 16-byte vectors.
  *  - "layer dtype" tensors are float (FLOWMOE_F32) or bf16 bit patterns
  *    (FLOWMOE_BF16, passed as uint16_t). Gate logits, gate weights, their
  *    gradients and all weight gradients are always float. Accumulation is
@@ -215,15 +218,16 @@ enum {
   FLOWMOE_K_FFN1 = 4,            /* grouped GEMM h = X W1 (+ W3), activation epilogue */
   FLOWMOE_K_FFN2 = 5,            /* grouped GEMM y = a W2 */
   FLOWMOE_K_SWIGLU_ACT = 6,      /* fp32 SwiGLU activation */
-  FLOWMOE_K_COMBINE = 7,         /* combine, and dispatch backward (gather-sum) */
+  FLOWMOE_K_COMBINE = 7,         /* combine, and dispatch backward (gather-sum; in
+                                    flowmoe_layer_bwd fused with dx += d_logits W_g^T) */
   FLOWMOE_K_COMBINE_BWD = 8,     /* combine backward */
   FLOWMOE_K_DGRAD1 = 9,          /* grouped GEMM dA = dY W2^T, activation' epilogue */
   FLOWMOE_K_WGRAD2 = 10,         /* grouped GEMM dW2 = A^T dY */
   FLOWMOE_K_WGRAD1 = 11,         /* grouped GEMM [dW1 | dW3] = X^T dH */
   FLOWMOE_K_DGRAD2 = 12,         /* grouped GEMM dX = dH W1^T (+ dH3 W3^T) */
-  FLOWMOE_K_GATE_BWD_WT = 13,    /* W_g transpose for the dx term */
-  FLOWMOE_K_GATE_BWD_TOKEN = 14, /* d_logits and dx += d_logits W_g^T */
-  FLOWMOE_K_GATE_BWD_DW = 15,    /* dW_g split-T partials */
+  FLOWMOE_K_GATE_BWD_WT = 13,    /* W_g transpose (float, E x M) for the dx term */
+  FLOWMOE_K_GATE_BWD_TOKEN = 14, /* dx += d_logits W_g^T (flowmoe_gate_topk_bwd with dx) */
+  FLOWMOE_K_GATE_BWD_DW = 15,    /* d_logits, and dW_g / db split-T partials */
   FLOWMOE_K_GATE_BWD_REDUCE = 16 /* dW_g / db reduction over splits */
 };
 
@@ -297,11 +301,16 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
                                    hipStream_t s_comm, hipEvent_t* trace);
 
 /* Backward of R chunks: comm stream gets C_R..C_1 (combine backward) then
- * D_R..D_1 (dispatch backward) (Eq. 6); compute stream gets E_R..E_1 then
- * AT_R..AT_1 (Eq. 5), with E_r after C_r, D_r after E_r, AT_r after D_r
- * (constraints 6b-6d). Weight gradients are summed over chunks in that order.
+ * D_R..D_1 (dispatch backward) (Eq. 6); compute stream gets E_R..E_1
+ * (Eq. 5), with E_r after C_r and D_r after E_r (constraints 6b-6c). The
+ * gating part of AT_r splits by what it reads: its parameter gradients
+ * (d_logits, dW_g, db) need only C_r's d_topk_w and x, so AT_R..AT_1's share
+ * runs on the comm stream right after C_1, while the compute stream is busy
+ * with the expert backward; its input gradient dx += d_logits W_g^T is
+ * fused into D_r. Weight gradients are summed over chunks in R..1 order.
  * trace (nullable): 8*R events as for the forward, task 0 = combine bwd,
- * 1 = experts bwd, 2 = dispatch bwd, 3 = gate bwd. */
+ * 1 = experts bwd, 2 = dispatch bwd (+ gate dx term), 3 = gate parameter
+ * gradients. */
 flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
                                    const flowmoe_layer_bufs_t* bufs, hipStream_t s_compute,
                                    hipStream_t s_comm, hipEvent_t* trace);

@@ -79,6 +79,13 @@ flowmoe_status_t check_shape(const flowmoe_shape_t* s, int need, Shape* out) {
 #define REQUIRE(p, name) \
   if ((p) == nullptr) return fail(FLOWMOE_ERR_INVALID, "%s is null", name)
 
+// a tensor of the layer dtype: non-null and 16-byte aligned (kernels move it
+// in 16-byte vectors)
+#define REQUIRE_T(p, name)                                                      \
+  if ((p) == nullptr) return fail(FLOWMOE_ERR_INVALID, "%s is null", name);      \
+  if (reinterpret_cast<uintptr_t>(p) % 16 != 0)                                 \
+    return fail(FLOWMOE_ERR_INVALID, "%s is not 16-byte aligned", name)
+
 flowmoe_status_t check_ws(void* ws, size_t have, size_t need, const char* call) {
   if (need == 0) return FLOWMOE_OK;
   if (ws == nullptr || have < need)
@@ -197,10 +204,8 @@ size_t flowmoe_workspace_bytes(const flowmoe_shape_t* shape, int32_t kind) {
     case FLOWMOE_WS_DISPATCH: return 0;
     case FLOWMOE_WS_FFN_BWD: return ffn_bwd_ws_bytes(s);
     case FLOWMOE_WS_GATE_BWD: return gate_bwd_ws_bytes(s);
-    case FLOWMOE_WS_LAYER_BWD: {
-      const size_t a = ffn_bwd_ws_bytes(s), b = gate_bwd_ws_bytes(s);
-      return a > b ? a : b;
-    }
+    case FLOWMOE_WS_LAYER_BWD:  // disjoint: the gate backward overlaps the expert backward
+      return align256(ffn_bwd_ws_bytes(s)) + gate_bwd_ws_bytes(s);
     default: return 0;
   }
 }
@@ -211,9 +216,9 @@ flowmoe_status_t flowmoe_gate_topk(const flowmoe_shape_t* shape, const void* x,
   Shape s;
   flowmoe_status_t st = check_shape(shape, 0, &s);
   if (st != FLOWMOE_OK) return st;
-  REQUIRE(w_gate, "w_gate");
+  REQUIRE_T(w_gate, "w_gate");
   if (s.T > 0) {
-    REQUIRE(x, "x");
+    REQUIRE_T(x, "x");
     REQUIRE(logits, "logits");
     REQUIRE(topk_idx, "topk_idx");
     REQUIRE(topk_w, "topk_w");
@@ -246,12 +251,12 @@ flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* t
   REQUIRE(offsets, "offsets");
   if (s.T > 0) {
     REQUIRE(topk_idx, "topk_idx");
-    REQUIRE(x, "x");
+    REQUIRE_T(x, "x");
     REQUIRE(slot, "slot");
   }
   if (s.rows > 0) {
     REQUIRE(row_src, "row_src");
-    REQUIRE(x_disp, "x_disp");
+    REQUIRE_T(x_disp, "x_disp");
   }
   (void)ws; (void)ws_bytes;
   return hip_status(launch_dispatch(s, topk_idx, x, counts, offsets, slot, row_src, load, x_disp,
@@ -269,14 +274,14 @@ flowmoe_status_t flowmoe_expert_ffn(const flowmoe_shape_t* shape, const void* x_
   if (st != FLOWMOE_OK) return st;
   REQUIRE(counts, "counts");
   REQUIRE(offsets, "offsets");
-  REQUIRE(w1, "w1");
-  REQUIRE(w2, "w2");
-  if (s.act == FLOWMOE_SWIGLU) REQUIRE(w3, "w3");
+  REQUIRE_T(w1, "w1");
+  REQUIRE_T(w2, "w2");
+  if (s.act == FLOWMOE_SWIGLU) REQUIRE_T(w3, "w3");
   if (s.rows > 0) {
-    REQUIRE(x_disp, "x_disp");
-    REQUIRE(h_save, "h_save");
-    REQUIRE(a_save, "a_save");
-    REQUIRE(y_disp, "y_disp");
+    REQUIRE_T(x_disp, "x_disp");
+    REQUIRE_T(h_save, "h_save");
+    REQUIRE_T(a_save, "a_save");
+    REQUIRE_T(y_disp, "y_disp");
   }
   return hip_status(launch_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save,
                                       y_disp, stream),
@@ -292,8 +297,8 @@ flowmoe_status_t flowmoe_combine(const flowmoe_shape_t* shape, const void* y_dis
   if (s.T > 0) {
     REQUIRE(slot, "slot");
     REQUIRE(topk_w, "topk_w");
-    REQUIRE(y, "y");
-    if (s.rows > 0) REQUIRE(y_disp, "y_disp");
+    REQUIRE_T(y, "y");
+    if (s.rows > 0) REQUIRE_T(y_disp, "y_disp");
   }
   return hip_status(launch_combine(s, y_disp, slot, topk_w, y, stream), "flowmoe_combine");
 }
@@ -308,14 +313,14 @@ flowmoe_status_t flowmoe_combine_bwd(const flowmoe_shape_t* shape, const void* d
   if (st != FLOWMOE_OK) return st;
   REQUIRE(counts, "counts");
   if (s.T > 0) {
-    REQUIRE(dy, "dy");
+    REQUIRE_T(dy, "dy");
     REQUIRE(slot, "slot");
     REQUIRE(topk_w, "topk_w");
     REQUIRE(d_topk_w, "d_topk_w");
   }
   if (s.rows > 0) {
-    REQUIRE(y_disp, "y_disp");
-    REQUIRE(dy_disp, "dy_disp");
+    REQUIRE_T(y_disp, "y_disp");
+    REQUIRE_T(dy_disp, "dy_disp");
   }
   return hip_status(launch_combine_bwd(s, dy, y_disp, slot, topk_w, counts, offsets, dy_disp,
                                        d_topk_w, stream),
@@ -334,20 +339,20 @@ flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void
   if (st != FLOWMOE_OK) return st;
   REQUIRE(counts, "counts");
   REQUIRE(offsets, "offsets");
-  REQUIRE(w1, "w1");
-  REQUIRE(w2, "w2");
+  REQUIRE_T(w1, "w1");
+  REQUIRE_T(w2, "w2");
   REQUIRE(dw1, "dw1");
   REQUIRE(dw2, "dw2");
   if (s.act == FLOWMOE_SWIGLU) {
-    REQUIRE(w3, "w3");
+    REQUIRE_T(w3, "w3");
     REQUIRE(dw3, "dw3");
   }
   if (s.rows > 0) {
-    REQUIRE(dy_disp, "dy_disp");
-    REQUIRE(x_disp, "x_disp");
-    REQUIRE(h_save, "h_save");
-    REQUIRE(a_save, "a_save");
-    REQUIRE(dx_disp, "dx_disp");
+    REQUIRE_T(dy_disp, "dy_disp");
+    REQUIRE_T(x_disp, "x_disp");
+    REQUIRE_T(h_save, "h_save");
+    REQUIRE_T(a_save, "a_save");
+    REQUIRE_T(dx_disp, "dx_disp");
   }
   st = check_ws(ws, ws_bytes, ffn_bwd_ws_bytes(s), "flowmoe_expert_ffn_bwd");
   if (st != FLOWMOE_OK) return st;
@@ -364,8 +369,8 @@ flowmoe_status_t flowmoe_dispatch_bwd(const flowmoe_shape_t* shape, const void* 
   if (st != FLOWMOE_OK) return st;
   if (s.T > 0) {
     REQUIRE(slot, "slot");
-    REQUIRE(dx, "dx");
-    if (s.rows > 0) REQUIRE(dx_disp, "dx_disp");
+    REQUIRE_T(dx, "dx");
+    if (s.rows > 0) REQUIRE_T(dx_disp, "dx_disp");
   }
   return hip_status(launch_dispatch_bwd(s, dx_disp, slot, dx, stream), "flowmoe_dispatch_bwd");
 }
@@ -379,15 +384,17 @@ flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void*
   Shape s;
   flowmoe_status_t st = check_shape(shape, 0, &s);
   if (st != FLOWMOE_OK) return st;
-  REQUIRE(w_gate, "w_gate");
+  REQUIRE_T(w_gate, "w_gate");
   REQUIRE(dw_gate, "dw_gate");
   if (s.T > 0) {
-    REQUIRE(x, "x");
+    REQUIRE_T(x, "x");
     REQUIRE(topk_idx, "topk_idx");
     REQUIRE(topk_w, "topk_w");
     REQUIRE(d_topk_w, "d_topk_w");
     REQUIRE(d_logits, "d_logits");
   }
+  if (dx != nullptr && reinterpret_cast<uintptr_t>(dx) % 16 != 0)
+    return fail(FLOWMOE_ERR_INVALID, "dx is not 16-byte aligned");
   st = check_ws(ws, ws_bytes, gate_bwd_ws_bytes(s), "flowmoe_gate_topk_bwd");
   if (st != FLOWMOE_OK) return st;
   return hip_status(launch_gate_bwd(s, x, w_gate, topk_idx, topk_w, d_topk_w, d_logits, dw_gate,
@@ -474,21 +481,21 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
   Shape s;
   flowmoe_status_t st = check_layer(shape, R, b, &s);
   if (st != FLOWMOE_OK) return st;
-  REQUIRE(b->w_gate, "bufs->w_gate");
-  REQUIRE(b->w1, "bufs->w1");
-  REQUIRE(b->w2, "bufs->w2");
+  REQUIRE_T(b->w_gate, "bufs->w_gate");
+  REQUIRE_T(b->w1, "bufs->w1");
+  REQUIRE_T(b->w2, "bufs->w2");
   REQUIRE(b->counts, "bufs->counts");
   REQUIRE(b->offsets, "bufs->offsets");
-  if (s.act == FLOWMOE_SWIGLU) REQUIRE(b->w3, "bufs->w3");
+  if (s.act == FLOWMOE_SWIGLU) REQUIRE_T(b->w3, "bufs->w3");
   if (s.T > 0) {
-    REQUIRE(b->x, "bufs->x"); REQUIRE(b->logits, "bufs->logits");
+    REQUIRE_T(b->x, "bufs->x"); REQUIRE(b->logits, "bufs->logits");
     REQUIRE(b->topk_idx, "bufs->topk_idx"); REQUIRE(b->topk_w, "bufs->topk_w");
-    REQUIRE(b->slot, "bufs->slot"); REQUIRE(b->y, "bufs->y");
+    REQUIRE(b->slot, "bufs->slot"); REQUIRE_T(b->y, "bufs->y");
   }
   if (s.rows > 0) {
-    REQUIRE(b->row_src, "bufs->row_src"); REQUIRE(b->x_disp, "bufs->x_disp");
-    REQUIRE(b->h_save, "bufs->h_save"); REQUIRE(b->a_save, "bufs->a_save");
-    REQUIRE(b->y_disp, "bufs->y_disp");
+    REQUIRE(b->row_src, "bufs->row_src"); REQUIRE_T(b->x_disp, "bufs->x_disp");
+    REQUIRE_T(b->h_save, "bufs->h_save"); REQUIRE_T(b->a_save, "bufs->a_save");
+    REQUIRE_T(b->y_disp, "bufs->y_disp");
   }
   Sched sc{s_compute, s_comm, s_comm != s_compute, trace, R};
   hipEvent_t* ev = nullptr;
@@ -544,28 +551,28 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
   Shape s;
   flowmoe_status_t st = check_layer(shape, R, b, &s);
   if (st != FLOWMOE_OK) return st;
-  REQUIRE(b->w_gate, "bufs->w_gate");
-  REQUIRE(b->w1, "bufs->w1");
-  REQUIRE(b->w2, "bufs->w2");
+  REQUIRE_T(b->w_gate, "bufs->w_gate");
+  REQUIRE_T(b->w1, "bufs->w1");
+  REQUIRE_T(b->w2, "bufs->w2");
   REQUIRE(b->counts, "bufs->counts");
   REQUIRE(b->offsets, "bufs->offsets");
   REQUIRE(b->dw_gate, "bufs->dw_gate");
   REQUIRE(b->dw1, "bufs->dw1");
   REQUIRE(b->dw2, "bufs->dw2");
   if (s.act == FLOWMOE_SWIGLU) {
-    REQUIRE(b->w3, "bufs->w3");
+    REQUIRE_T(b->w3, "bufs->w3");
     REQUIRE(b->dw3, "bufs->dw3");
   }
   if (s.T > 0) {
-    REQUIRE(b->x, "bufs->x"); REQUIRE(b->dy, "bufs->dy"); REQUIRE(b->topk_idx, "bufs->topk_idx");
+    REQUIRE_T(b->x, "bufs->x"); REQUIRE_T(b->dy, "bufs->dy"); REQUIRE(b->topk_idx, "bufs->topk_idx");
     REQUIRE(b->topk_w, "bufs->topk_w"); REQUIRE(b->slot, "bufs->slot");
     REQUIRE(b->d_topk_w, "bufs->d_topk_w"); REQUIRE(b->d_logits, "bufs->d_logits");
-    REQUIRE(b->dx, "bufs->dx");
+    REQUIRE_T(b->dx, "bufs->dx");
   }
   if (s.rows > 0) {
-    REQUIRE(b->x_disp, "bufs->x_disp"); REQUIRE(b->h_save, "bufs->h_save");
-    REQUIRE(b->a_save, "bufs->a_save"); REQUIRE(b->y_disp, "bufs->y_disp");
-    REQUIRE(b->dy_disp, "bufs->dy_disp"); REQUIRE(b->dx_disp, "bufs->dx_disp");
+    REQUIRE_T(b->x_disp, "bufs->x_disp"); REQUIRE_T(b->h_save, "bufs->h_save");
+    REQUIRE_T(b->a_save, "bufs->a_save"); REQUIRE_T(b->y_disp, "bufs->y_disp");
+    REQUIRE_T(b->dy_disp, "bufs->dy_disp"); REQUIRE_T(b->dx_disp, "bufs->dx_disp");
   }
   const size_t need = flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
   st = check_ws(b->ws, b->ws_bytes, need, "flowmoe_layer_bwd");
@@ -574,9 +581,14 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
   hipEvent_t* ev = nullptr;
   sc.run(get_events(3 * R + 2, &ev));
   if (sc.err != hipSuccess) return hip_status(sc.err, "flowmoe_layer_bwd events");
-  hipEvent_t *evC = ev, *evE = ev + R, *evD = ev + 2 * R, evStart = ev[3 * R], evEnd = ev[3 * R + 1];
+  hipEvent_t *evC = ev, *evE = ev + R, evStart = ev[3 * R], evEnd = ev[3 * R + 1];
   sc.signal(evStart, s_compute);
   sc.wait(s_comm, evStart);
+  // The gate's own gradients (d_logits, dW_g, db) need only the combine
+  // backward's d_topk_w, so they run on the comm stream while the expert
+  // backward occupies the compute stream; its dx term is fused into the
+  // dispatch backward. Workspace: [expert backward | gate partials].
+  void* ws_gate = static_cast<char*>(b->ws) + align256(ffn_bwd_ws_bytes(s));
   // C_R..C_1 (combine backward) on the comm stream
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);
@@ -585,6 +597,16 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
                               s_comm));
     sc.mark(0, r, 1, s_comm);
     sc.signal(evC[r], s_comm);
+  }
+  // gate parameter gradients of AT_R..AT_1, summed over chunks in that order;
+  // W_g^T for the dx term first (the gate workspace keeps it at its front)
+  if (s.T > 0) sc.run(launch_gate_wt(s, b->w_gate, ws_gate, s_comm));
+  for (int r = R - 1; r >= 0; --r) {
+    Chunk c = chunk_of(s, b, r);
+    sc.mark(3, r, 0, s_comm);
+    sc.run(launch_gate_dw(s, c.x, c.idx, c.w, c.dw, c.dl, b->dw_gate, b->dbias, r != R - 1,
+                          ws_gate, s_comm));
+    sc.mark(3, r, 1, s_comm);
   }
   // E_R..E_1 on the compute stream; weight gradients summed in that order
   for (int r = R - 1; r >= 0; --r) {
@@ -597,23 +619,14 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     sc.mark(1, r, 1, s_compute);
     sc.signal(evE[r], s_compute);
   }
-  // D_R..D_1 (dispatch backward) on the comm stream
+  // D_R..D_1 (dispatch backward, plus the gate's dx term) on the comm stream
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);
     sc.wait(s_comm, evE[r]);
     sc.mark(2, r, 0, s_comm);
-    sc.run(launch_dispatch_bwd(s, c.dx_disp, c.slot, c.dx, s_comm));
+    sc.run(launch_dispatch_bwd_gate(s, c.dx_disp, c.slot, c.idx, c.w, c.dw, gate_ws_wgt(ws_gate),
+                                    c.dx, s_comm));
     sc.mark(2, r, 1, s_comm);
-    sc.signal(evD[r], s_comm);
-  }
-  // AT_R..AT_1 (gate backward, adds its share into dx) on the compute stream
-  for (int r = R - 1; r >= 0; --r) {
-    Chunk c = chunk_of(s, b, r);
-    sc.wait(s_compute, evD[r]);
-    sc.mark(3, r, 0, s_compute);
-    sc.run(launch_gate_bwd(s, c.x, b->w_gate, c.idx, c.w, c.dw, c.dl, b->dw_gate, b->dbias, c.dx,
-                           r != R - 1, b->ws, s_compute));
-    sc.mark(3, r, 1, s_compute);
   }
   sc.signal(evEnd, s_comm);
   sc.wait(s_compute, evEnd);

@@ -119,7 +119,19 @@ hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp
                               const int32_t* offsets, void* dy_disp, float* dw, hipStream_t st);
 hipError_t launch_dispatch_bwd(const Shape& s, const void* dx_disp, const int32_t* slot, void* dx,
                                hipStream_t st);
+hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const int32_t* slot,
+                                    const int32_t* idx, const float* w, const float* dw,
+                                    const float* wgt, void* dx, hipStream_t st);
+// gate backward workspace: [W_g^T, float E x M | dW_g partials]
 size_t gate_bwd_ws_bytes(const Shape& s);
+inline const float* gate_ws_wgt(const void* ws) { return static_cast<const float*>(ws); }
+hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, const float* w,
+                          const float* dw, float* d_logits, float* dw_gate, float* dbias,
+                          int accumulate, void* ws, hipStream_t st);
+hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, const float* dw,
+                          const float* wgt, void* dx, hipStream_t st);
+// W_g (M x E, layer dtype) -> W_g^T (E x M, float) at the front of the gate workspace
+hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st);
 hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const int32_t* idx,
                            const float* w, const float* dw, float* d_logits, float* dw_gate,
                            float* dbias, void* dx, int accumulate, void* ws, hipStream_t st);

@@ -2,11 +2,15 @@
 //
 // route_scan: capacity-bounded positions in the priority order "every first
 //   choice, then every second choice, ..., ascending token within a rank",
-//   i.e. a stable counting sort of the sequence s = j*T + t by expert. One
-//   1024-thread workgroup walks the sequence in tiles; inside a wave, lanes
-//   with the same expert are matched with 6 ballots (E <= 64), giving each
-//   lane its rank among equal experts; per-expert wave counts are scanned in
-//   LDS across the 16 waves and carried across tiles.
+//   i.e. a stable counting sort of the sequence s = j*T + t by expert. Block b
+//   owns the 1024 positions [1024 b, 1024 b + 1024) of that sequence. It
+//   counts, per expert, the assignments before its tile and after it (every
+//   block reads all of topk_idx, from L2), so it knows both its tile's base
+//   per expert and the totals (hence counts and offsets) without any
+//   cross-block communication. Counting works on 64-position chunks: 6
+//   ballots on the expert bits tell every lane which lanes share its expert
+//   (its rank) and lane e how many lanes hold expert e. Inside the tile, the
+//   16 waves' counts are scanned per expert with 16-lane shuffles.
 // gather / combine / scatter kernels move whole rows with 16-byte vectors,
 //   one wave per row or token, accumulating in float in a fixed order.
 #include "common.hpp"
@@ -16,93 +20,138 @@ namespace {
 
 constexpr int kScanThreads = 1024;
 constexpr int kScanWaves = kScanThreads / 64;
+constexpr int kScanUnroll = 8;  // chunk loads in flight per lane
+
+// expert of priority position s (j = s / T, t = s % T), or -1
+__device__ __forceinline__ int scan_expert(const int32_t* __restrict__ idx, unsigned s, unsigned n,
+                                           unsigned T, int k, int E) {
+  if (s >= n) return -1;
+  const unsigned j = s / T, t = s - j * T;
+  const int e = idx[(long)t * k + j];
+  return ((unsigned)e < (unsigned)E) ? e : -1;
+}
+
+// ballots over one 64-position chunk: rank of this lane's assignment among
+// lanes with the same expert, and (for lane e) the chunk's count of expert e
+__device__ __forceinline__ void chunk_match(int e, int lane, uint64_t lt_mask, int& rank,
+                                            int& count) {
+  const bool valid = e >= 0;
+  const int ev = valid ? e : 0;
+  const uint64_t vm = __ballot(valid);
+  uint64_t same = vm, mine = vm;
+#pragma unroll
+  for (int b = 0; b < 6; ++b) {
+    const uint64_t m = __ballot(valid && ((ev >> b) & 1));
+    same &= ((ev >> b) & 1) ? m : ~m;
+    mine &= ((lane >> b) & 1) ? m : ~m;
+  }
+  rank = __popcll(same & lt_mask);
+  count = __popcll(mine);
+}
 
 __global__ __launch_bounds__(kScanThreads) void route_scan_kernel(
     const int32_t* __restrict__ idx, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ slot, int32_t* __restrict__ row_src, int32_t* __restrict__ load, int T,
     int k, int E, int C, int padded, long rows) {
-  __shared__ int wcnt[kScanWaves][kMaxE];
-  __shared__ int running[kMaxE];
+  __shared__ int own[kScanWaves][64];   // tile counts per wave, then element bases
+  __shared__ int bef[kScanWaves][64];   // per-wave counts before the tile
+  __shared__ int aft[kScanWaves][64];   // per-wave counts after the tile
+  __shared__ int tot[64];
   __shared__ int offs[kMaxE + 1];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const unsigned n = (unsigned)T * (unsigned)k;  // <= 2^30 (host check)
+  const unsigned tile0 = blockIdx.x * (unsigned)kScanThreads;
 
-  for (long r = tid; r < rows; r += kScanThreads) row_src[r] = -1;
-  if (tid < kMaxE) running[tid] = 0;
-
-  const long n = (long)T * k;
-  // pass 1: positions
-  for (long base = 0; base < n; base += kScanThreads) {
-    __syncthreads();  // previous tile's readers of wcnt are done
-    for (int q = tid; q < kScanWaves * kMaxE; q += kScanThreads) (&wcnt[0][0])[q] = 0;
-    __syncthreads();
-    const long s = base + tid;
-    bool valid = s < n;
-    int t = 0, j = 0, e = 0;
-    if (valid) {
-      j = (int)(s / T);
-      t = (int)(s - (long)j * T);
-      e = idx[(long)t * k + j];
-      if ((unsigned)e >= (unsigned)E) {  // not an expert id: never kept
-        valid = false;
-        e = 0;
-      }
-    }
-    uint64_t same = __ballot(valid);
+  // 1. counts outside the tile: wave w takes chunks c = i * 1024 + 64 w
+  int cb = 0, ca = 0;
+  const unsigned nt = (n + kScanThreads - 1) / kScanThreads;  // tiles
+  for (unsigned i0 = 0; i0 < nt; i0 += kScanUnroll) {
+    int ev[kScanUnroll];
 #pragma unroll
-    for (int b = 0; b < 6; ++b) {
-      const uint64_t m = __ballot(valid && ((e >> b) & 1));
-      same &= ((e >> b) & 1) ? m : ~m;
+    for (int u = 0; u < kScanUnroll; ++u) {
+      const unsigned i = i0 + u;
+      const unsigned s = i * kScanThreads + wave * 64 + lane;
+      ev[u] = (i < nt && i != blockIdx.x) ? scan_expert(idx, s, n, T, k, E) : -1;
     }
-    const int rank = __popcll(same & lt_mask);
-    if (valid && rank == 0) wcnt[wave][e] = __popcll(same);
-    __syncthreads();
-    if (tid < E) {
-      int run = running[tid];
-      for (int w = 0; w < kScanWaves; ++w) {
-        const int c = wcnt[w][tid];
-        wcnt[w][tid] = run;
-        run += c;
-      }
-      running[tid] = run;
-    }
-    __syncthreads();
-    if (valid) slot[(long)t * k + j] = wcnt[wave][e] + rank;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int acc = 0;
-    for (int e = 0; e < E; ++e) {
-      offs[e] = padded ? e * C : acc;
-      acc += min(running[e], C);
-    }
-    offs[E] = padded ? E * C : acc;
-  }
-  __syncthreads();
-  if (tid < E) {
-    counts[tid] = min(running[tid], C);
-    if (load != nullptr) load[tid] = running[tid];
-  }
-  if (tid <= E) offsets[tid] = offs[tid];
-  __threadfence_block();
-  __syncthreads();
-  // pass 2: rows (each thread revisits exactly the elements it wrote)
-  for (long base = 0; base < n; base += kScanThreads) {
-    const long s = base + tid;
-    if (s < n) {
-      const int j = (int)(s / T);
-      const int t = (int)(s - (long)j * T);
-      const long a = (long)t * k + j;
-      const int e = idx[a];
-      const int pos = ((unsigned)e < (unsigned)E) ? slot[a] : C;
-      if (pos < C) {
-        const int r = offs[e] + pos;
-        slot[a] = r;
-        row_src[r] = (int)a;
-      } else {
-        slot[a] = -1;
+#pragma unroll
+    for (int u = 0; u < kScanUnroll; ++u) {
+      const unsigned i = i0 + u;
+      if (i < nt && i != blockIdx.x) {  // uniform
+        int rank, cnt;
+        chunk_match(ev[u], lane, lt_mask, rank, cnt);
+        if (i < blockIdx.x) cb += cnt; else ca += cnt;
       }
     }
+  }
+  // 2. the tile itself
+  const unsigned s = tile0 + tid;
+  const int e = scan_expert(idx, s, n, T, k, E);
+  int rank, cnt;
+  chunk_match(e, lane, lt_mask, rank, cnt);
+  own[wave][lane] = cnt;
+  bef[wave][lane] = cb;
+  aft[wave][lane] = ca;
+  __syncthreads();
+  {
+    // thread (expert ex, wave w): element base = (assignments of ex before
+    // the tile) + (in earlier waves of the tile); totals for the offsets
+    const int ex = tid >> 4, w = tid & 15;
+    const int c = own[w][ex];
+    int inc = c, b4 = bef[w][ex], all = bef[w][ex] + c + aft[w][ex];
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const int o = __shfl_up(inc, off, 16);
+      if (w >= off) inc += o;
+      b4 += __shfl_xor(b4, off, 16);
+      all += __shfl_xor(all, off, 16);
+    }
+    own[w][ex] = b4 + inc - c;
+    if (w == 0) tot[ex] = all;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // offsets: exclusive prefix of min(total, C) over experts (lane = expert)
+    const int kept = (lane < E) ? min(tot[lane], C) : 0;
+    int inc = kept;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int o = __shfl_up(inc, off, 64);
+      if (lane >= off) inc += o;
+    }
+    if (lane < E) offs[lane] = padded ? lane * C : inc - kept;
+    if (lane == E - 1) offs[E] = padded ? E * C : inc;
+    if (blockIdx.x == 0 && lane < E) {
+      counts[lane] = kept;
+      if (load != nullptr) load[lane] = tot[lane];
+    }
+  }
+  __syncthreads();
+  if (blockIdx.x == 0 && tid <= E) offsets[tid] = offs[tid];
+  // 3. slot and row of this block's assignments
+  if (s < n) {
+    const unsigned j = s / (unsigned)T, t = s - j * (unsigned)T;
+    const long a = (long)t * k + j;
+    const int pos = (e >= 0) ? own[wave][e] + rank : C;
+    if (pos < C) {
+      const int r = offs[e] + pos;
+      slot[a] = r;
+      row_src[r] = (int)a;
+    } else {
+      slot[a] = -1;
+    }
+  }
+  // 4. rows that no kept assignment fills: the packed tail, the padded gaps
+  for (long r = (long)blockIdx.x * kScanThreads + tid; r < rows; r += (long)gridDim.x * kScanThreads) {
+    bool empty;
+    if (padded) {
+      const int ee = (int)(r / C);
+      empty = (int)(r - (long)ee * C) >= min(tot[ee], C);
+    } else {
+      empty = r >= offs[E];
+    }
+    if (empty) row_src[r] = -1;
   }
 }
 
@@ -129,13 +178,15 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restric
 }
 
 // y[t] = sum_j w[t][j] * src[slot[t][j]] over kept j (w == nullptr: weight 1).
-// One wave per token, 8 elements per lane step.
-template <typename TE>
-__global__ __launch_bounds__(256) void combine_rows_kernel(const TE* __restrict__ src,
-                                                           const int32_t* __restrict__ slot,
-                                                           const float* __restrict__ w,
-                                                           TE* __restrict__ y, int T, int M,
-                                                           int k) {
+// One wave per token, 8 elements per lane step. GATE (dispatch backward of
+// the layer): also adds the gate's share dl_t W_g^T, with dl_t taken from the
+// selection (gidx), its weights (gw) and their gradients (gdw), and W_g^T
+// given transposed in float (wgt, E x M).
+template <typename TE, bool GATE>
+__global__ __launch_bounds__(256) void combine_rows_kernel(
+    const TE* __restrict__ src, const int32_t* __restrict__ slot, const float* __restrict__ w,
+    TE* __restrict__ y, int T, int M, int k, const int32_t* __restrict__ gidx,
+    const float* __restrict__ gw, const float* __restrict__ gdw, const float* __restrict__ wgt, int E) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = threadIdx.x & 63;
@@ -147,6 +198,23 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(const TE* __restrict_
       sl[j] = slot[(long)t * k + j];
       wt[j] = (w != nullptr) ? w[(long)t * k + j] : 1.0f;
     }
+  }
+  int ge[kMaxK];
+  float gl[kMaxK];
+  if constexpr (GATE) {
+    // dl over the selected experts: w_j (dw_j - sum_j' w_j' dw_j')
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      if (j < k) {
+        ge[j] = gidx[(long)t * k + j];
+        gl[j] = gw[(long)t * k + j];
+        s += gl[j] * gdw[(long)t * k + j];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+      if (j < k) gl[j] = gl[j] * (gdw[(long)t * k + j] - s);
   }
   for (int m = lane * 8; m < M; m += 64 * 8) {
     float acc[8];
@@ -160,6 +228,16 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(const TE* __restrict_
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc[q] += wt[j] * v[q];
       }
+    }
+    if constexpr (GATE) {
+#pragma unroll
+      for (int j = 0; j < kMaxK; ++j)
+        if (j < k) {
+          float g[8];
+          load8(wgt + (long)ge[j] * M + m, g);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[q] += gl[j] * g[q];
+        }
     }
     store8(y + (long)t * M + m, acc);
   }
@@ -227,9 +305,13 @@ hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, in
                            int32_t* offsets, int32_t* slot, int32_t* row_src, int32_t* load,
                            void* x_disp, hipStream_t st) {
   const int padded = s.layout == FLOWMOE_PADDED;
+  const long n = (long)s.T * s.k;
+  const long tiles = (n + kScanThreads - 1) / kScanThreads;
+  const long fill = (s.rows + kScanThreads - 1) / kScanThreads;  // blocks for the row fill
+  const unsigned grid = (unsigned)(tiles > 0 ? tiles : (fill > 0 ? (fill < 64 ? fill : 64) : 1));
   hipError_t err = traced(FLOWMOE_K_SCAN, st, [&] {
-    hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(kScanThreads), 0, st, idx, counts, offsets,
-                       slot, row_src, load, s.T, s.k, s.E, s.C, padded, s.rows);
+    hipLaunchKernelGGL(route_scan_kernel, dim3(grid), dim3(kScanThreads), 0, st, idx, counts,
+                       offsets, slot, row_src, load, s.T, s.k, s.E, s.C, padded, s.rows);
   });
   if (err != hipSuccess || s.rows == 0) return err;
   const int vecs = (int)((long)s.M * esize(s.dtype) / 16);
@@ -247,17 +329,36 @@ hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slo
   const int blocks = (s.T + 3) / 4;
   return traced(FLOWMOE_K_COMBINE, st, [&] {
     if (s.dtype == FLOWMOE_BF16)
-      hipLaunchKernelGGL(combine_rows_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st,
-                         (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k);
+      hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false>), dim3(blocks), dim3(256), 0, st,
+                         (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k, nullptr,
+                         nullptr, nullptr, nullptr, s.E);
     else
-      hipLaunchKernelGGL(combine_rows_kernel<float>, dim3(blocks), dim3(256), 0, st,
-                         (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k);
+      hipLaunchKernelGGL((combine_rows_kernel<float, false>), dim3(blocks), dim3(256), 0, st,
+                         (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k, nullptr,
+                         nullptr, nullptr, nullptr, s.E);
   });
 }
 
 hipError_t launch_dispatch_bwd(const Shape& s, const void* dx_disp, const int32_t* slot, void* dx,
                                hipStream_t st) {
   return launch_combine(s, dx_disp, slot, nullptr, dx, st);
+}
+
+hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const int32_t* slot,
+                                    const int32_t* idx, const float* w, const float* dw,
+                                    const float* wgt, void* dx, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const int blocks = (s.T + 3) / 4;
+  return traced(FLOWMOE_K_COMBINE, st, [&] {
+    if (s.dtype == FLOWMOE_BF16)
+      hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true>), dim3(blocks), dim3(256), 0, st,
+                         (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx, s.T, s.M, s.k, idx, w,
+                         dw, wgt, s.E);
+    else
+      hipLaunchKernelGGL((combine_rows_kernel<float, true>), dim3(blocks), dim3(256), 0, st,
+                         (const float*)dx_disp, slot, nullptr, (float*)dx, s.T, s.M, s.k, idx, w,
+                         dw, wgt, s.E);
+  });
 }
 
 hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp,

@@ -133,93 +133,134 @@ __global__ __launch_bounds__(kGateThreads) void gate_topk_kernel(
   }
 }
 
-// bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16): a block of 4 waves owns 64
-// tokens, each wave 16 of them, against all experts padded to 16-column
-// blocks. x rows feed the A operand straight from global memory (16 bytes of
-// one row per lane); W_g chunks of kGateKC rows are staged in LDS transposed
-// (expert-major, K-contiguous) for the B operand. The logits tile goes
-// through LDS to the wavefront top-k.
-constexpr int kGateKC = 128;          // K rows of W_g staged per step
-constexpr int kGateTok = 64;          // tokens per block
-constexpr int kGateWtStride = kGateKC + 8;  // bf16 elements per staged expert row
+// bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16). A block of 4 waves owns 16
+// tokens; the reduction over M is split between the waves (wave w takes the
+// 32-deep k steps s = w, w + 4, ...), so every wave has its x loads in flight
+// at once: the kernel reads x in about one memory round trip. x rows feed the
+// A operand straight from global memory (16 bytes of one row per lane). W_g
+// rows are copied into LDS in chunks of KC rows (as stored, [k][E], one
+// contiguous range) and each lane gathers its B fragment (8 consecutive k of
+// one expert) with 2-byte LDS reads. The four partial logit tiles are summed
+// in LDS in wave order (deterministic), the bias added, and each token's
+// top-k taken by a segment of EP lanes.
+constexpr int kGateTok = 16;            // tokens per block
+constexpr int kGateWgBytes = 32768;     // LDS for one chunk of W_g rows
+constexpr int kGateBatch = 8;           // x loads in flight per lane
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
+// rows of W_g per LDS chunk: a multiple of 32 (whole k steps)
+__host__ __device__ inline int gate_chunk_rows(int E) {
+  int kc = kGateWgBytes / (2 * E);
+  return kc - kc % 32;
+}
+
+template <int NB>  // 16-expert column blocks (E <= 16 * NB)
 __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg, const float* __restrict__ bias,
     float* __restrict__ logits, int32_t* __restrict__ idx, float* __restrict__ w, int T, int M,
     int E, int k, int EP) {
-  __shared__ __attribute__((aligned(16))) bf16_t wt[kMaxE * kGateWtStride];
-  __shared__ float lg[kGateTok][kMaxE + 1];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int NB = (E + 15) >> 4;  // 16-expert column blocks
-  const int t0 = blockIdx.x * kGateTok + wave * 16;
-  const int arow = t0 + (lane & 15);          // token whose A row this lane feeds
-  const int kq = (lane >> 4) * 8;             // k offset of this lane inside a 32-step
+  __shared__ __attribute__((aligned(16))) bf16_t wgs[kGateWgBytes / 2];
+  __shared__ float part[4][kGateTok][NB * 16 + 1];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int t0 = blockIdx.x * kGateTok;
+  const int arow = t0 + (lane & 15);  // token whose A row this lane feeds
+  const int kq = (lane >> 4) * 8;     // k offset of this lane inside a step
   const bool arow_ok = arow < T;
   const bf16_t* xrow = x + (long)(arow_ok ? arow : 0) * M;
-  floatx4_t acc[4];
-#pragma unroll
-  for (int nb = 0; nb < 4; ++nb) acc[nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  const int KC = gate_chunk_rows(E);
 
-  for (int k0 = 0; k0 < M; k0 += kGateKC) {
-    // A fragments of this chunk, issued before the staging barrier
-    uint4 av[kGateKC / 32];
+  floatx4_t acc[NB];
 #pragma unroll
-    for (int s = 0; s < kGateKC / 32; ++s) {
-      const int kk = k0 + s * 32 + kq;
-      av[s] = (arow_ok && kk < M) ? *reinterpret_cast<const uint4*>(xrow + kk) : make_uint4(0, 0, 0, 0);
-    }
-    __syncthreads();  // previous chunk's readers of wt are done
-    const int rows = min(kGateKC, M - k0);
-    for (int q = tid; q < kGateKC * NB * 16; q += 256) {
-      const int kk = q / (NB * 16), e = q % (NB * 16);
-      const bf16_t v = (kk < rows && e < E) ? wg[(long)(k0 + kk) * E + e] : (bf16_t)0;
-      wt[e * kGateWtStride + kk] = v;
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = 0; k0 < M; k0 += KC) {
+    const int kc = min(KC, M - k0);
+    const int s_end = (k0 + kc + 31) / 32;  // k steps of this chunk: [k0/32, s_end)
+    int s = k0 / 32 + wave;
+    // this wave's first batch of x fragments, issued before the staging barrier
+    uint4 av[kGateBatch];
+    auto load_batch = [&](int s0) {
+#pragma unroll
+      for (int i = 0; i < kGateBatch; ++i) {
+        const int kk = (s0 + 4 * i) * 32 + kq;
+        av[i] = (arow_ok && s0 + 4 * i < s_end && kk < M)
+                    ? *reinterpret_cast<const uint4*>(xrow + kk)
+                    : make_uint4(0, 0, 0, 0);
+      }
+    };
+    load_batch(s);
+    __syncthreads();  // previous chunk's readers of wgs are done
+    {
+      // rows [k0, k0 + kc) of W_g are one contiguous range of kc * E values;
+      // kc and M are multiples of 8, so it is a whole number of 16-byte units
+      const uint4* src = reinterpret_cast<const uint4*>(wg + (long)k0 * E);
+      uint4* dst = reinterpret_cast<uint4*>(wgs);
+      const int n16 = kc * E / 8;  // <= 8 per thread (32 KB)
+      uint4 tmp[kGateWgBytes / 16 / 256];
+#pragma unroll
+      for (int i = 0; i < kGateWgBytes / 16 / 256; ++i)
+        if (tid + 256 * i < n16) tmp[i] = src[tid + 256 * i];
+#pragma unroll
+      for (int i = 0; i < kGateWgBytes / 16 / 256; ++i)
+        if (tid + 256 * i < n16) dst[tid + 256 * i] = tmp[i];
     }
     __syncthreads();
+    for (; s < s_end; s += 4 * kGateBatch) {
 #pragma unroll
-    for (int s = 0; s < kGateKC / 32; ++s) {
-      const bf16x8_t a = __builtin_bit_cast(bf16x8_t, av[s]);
+      for (int i = 0; i < kGateBatch; ++i) {
+        const int si = s + 4 * i;
+        if (si < s_end) {
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, av[i]);
+          const int r0 = si * 32 - k0 + kq;  // first W_g row of this lane's fragment
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        if (nb < NB) {
-          const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(
-              &wt[(nb * 16 + (lane & 15)) * kGateWtStride + s * 32 + kq]);
-          acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[nb], 0, 0, 0);
+          for (int nb = 0; nb < NB; ++nb) {
+            const int e = nb * 16 + (lane & 15);
+            uint32_t u[4] = {0u, 0u, 0u, 0u};
+            if (e < E) {
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int ra = r0 + 2 * q, rb = ra + 1;
+                const uint32_t lo = (ra < kc) ? wgs[ra * E + e] : 0u;
+                const uint32_t hi = (rb < kc) ? wgs[rb * E + e] : 0u;
+                u[q] = lo | (hi << 16);
+              }
+            }
+            const bf16x8_t b = __builtin_bit_cast(bf16x8_t, make_uint4(u[0], u[1], u[2], u[3]));
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[nb], 0, 0, 0);
+          }
         }
       }
+      if (s + 4 * kGateBatch < s_end) load_batch(s + 4 * kGateBatch);
     }
   }
-  // acc[nb][r]: token (lane/16)*4 + r of this wave, expert nb*16 + lane%16
+  // acc[nb][r]: token (lane / 16) * 4 + r, expert nb * 16 + lane % 16
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
-    if (nb < NB) {
-      const int e = nb * 16 + (lane & 15);
-      const float b = (bias != nullptr && e < E) ? bias[e] : 0.f;
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int tt = wave * 16 + (lane >> 4) * 4 + r;
-        const float l = acc[nb][r] + b;
-        if (e < E) {
-          lg[tt][e] = l;
-          const int t = blockIdx.x * kGateTok + tt;
-          if (t < T) logits[(long)t * E + e] = l;
-        }
-      }
-    }
+    for (int r = 0; r < 4; ++r) part[wave][(lane >> 4) * 4 + r][nb * 16 + (lane & 15)] = acc[nb][r];
+  __syncthreads();
+  // sum the four partial tiles in wave order; bias; logits out
+  for (int q = tid; q < kGateTok * E; q += 256) {
+    const int tt = q / E, e = q % E;
+    float l = part[0][tt][e] + part[1][tt][e];
+    l += part[2][tt][e];
+    l += part[3][tt][e];
+    if (bias != nullptr) l += bias[e];
+    part[0][tt][e] = l;
+    if (t0 + tt < T) logits[(long)(t0 + tt) * E + e] = l;
   }
   __syncthreads();
   // top-k: segments of EP lanes, one token per segment per round
   const int G = 64 / EP;
   const int seg = lane / EP, e = lane % EP;
   const bool evalid = e < E;
-  for (int i = seg; i < 16; i += G) {
-    const int tt = wave * 16 + i;
-    const int t = blockIdx.x * kGateTok + tt;
+  for (int i = wave * G + seg; i < kGateTok; i += 4 * G) {
+    const int t = t0 + i;
     if (t >= T) break;  // uniform across the segment
-    const float l = evalid ? lg[tt][e] : 0.f;
+    const float l = evalid ? part[0][i][e] : 0.f;
     topk_write(l, e, evalid, EP, k, idx + (long)t * k, w + (long)t * k);
   }
 }
@@ -239,122 +280,191 @@ __global__ __launch_bounds__(kGateThreads) void route_kernel(const float* __rest
 }
 
 // ---- backward ---------------------------------------------------------------
+//
+// dl_{t, S_t[j]} = w_j (dw_j - sum_j' w_j' dw_j') and 0 off S_t (the Jacobian
+// of the softmax over the k selected logits); dW_g = x^T dl, db = sum_t dl_t,
+// dx_t += dl_t W_g^T.
 
-// W_g (M x E, layer dtype) -> W_g^T (E x M, float) in the workspace
-template <typename TIn>
-__global__ void transpose_wg_kernel(const TIn* __restrict__ wg, float* __restrict__ wgt, int M,
-                                    int E) {
-  const long n = (long)M * E;
-  for (long q = blockIdx.x * (long)blockDim.x + threadIdx.x; q < n; q += (long)gridDim.x * blockDim.x) {
-    const int e = (int)(q / M), m = (int)(q % M);
-    wgt[q] = Elem<TIn>::load(wg + (size_t)m * E + e);
-  }
-}
-
-// One wave per token: d_logits row, and optionally dx[t] += dl W_g^T.
-template <typename TIn>
-__global__ __launch_bounds__(256) void gate_bwd_token_kernel(
-    const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
-    const float* __restrict__ wgt, float* __restrict__ d_logits, TIn* __restrict__ dx, int T,
-    int M, int E, int k) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
-  float wj[kMaxK], dl[kMaxK];
-  int ij[kMaxK];
+// dl of one token for its k selected experts
+__device__ __forceinline__ void token_dl(const int32_t* __restrict__ idx, const float* __restrict__ w,
+                                         const float* __restrict__ dw, long t, int k,
+                                         int (&ij)[kMaxK], float (&dl)[kMaxK]) {
+  float wj[kMaxK], dwj[kMaxK];
   float s = 0.f;
 #pragma unroll
   for (int j = 0; j < kMaxK; ++j) {
     if (j < k) {
-      wj[j] = w[(size_t)t * k + j];
-      ij[j] = idx[(size_t)t * k + j];
-      s += wj[j] * dw[(size_t)t * k + j];
+      ij[j] = idx[t * k + j];
+      wj[j] = w[t * k + j];
+      dwj[j] = dw[t * k + j];
+      s += wj[j] * dwj[j];
+    } else {
+      ij[j] = -1;
     }
   }
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j)
-    if (j < k) dl[j] = wj[j] * (dw[(size_t)t * k + j] - s);
-  for (int e = lane; e < E; e += 64) {
-    float v = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j)
-      if (j < k && ij[j] == e) v = dl[j];
-    d_logits[(size_t)t * E + e] = v;
+  for (int j = 0; j < kMaxK; ++j) dl[j] = (j < k) ? wj[j] * (dwj[j] - s) : 0.f;
+}
+
+// W_g (M x E, layer dtype) -> W_g^T (E x M, float), so that the dx term reads
+// 8 consecutive m of one expert as two 16-byte vectors
+template <typename TIn>
+__global__ __launch_bounds__(256) void transpose_wg_kernel(const TIn* __restrict__ wg,
+                                                           float* __restrict__ wgt, int M, int E) {
+  const long n = (long)M * E;
+  for (long q = blockIdx.x * 256L + threadIdx.x; q < n; q += (long)gridDim.x * 256) {
+    const int e = (int)(q / M), m = (int)(q % M);
+    wgt[q] = Elem<TIn>::load(wg + (long)m * E + e);
   }
-  if (dx == nullptr) return;
-  // M is a multiple of 8 (checked on the host)
-  TIn* row = dx + (size_t)t * M;
-  for (int m = lane * 8; m < M; m += 64 * 8) {
+}
+
+// dx[t] += dl_t W_g^T, one wave per token
+template <typename TIn>
+__global__ __launch_bounds__(256) void gate_bwd_dx_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
+    const float* __restrict__ wgt, TIn* __restrict__ dx, int T, int M, int k) {
+  const int lane = threadIdx.x & 63;
+  const long t = blockIdx.x * 4L + (threadIdx.x >> 6);
+  if (t >= T) return;
+  int ij[kMaxK];
+  float dl[kMaxK];
+  token_dl(idx, w, dw, t, k, ij, dl);
+  TIn* row = dx + t * M;
+  for (int m = lane * 8; m < M; m += 64 * 8) {  // M is a multiple of 8
     float v[8];
     load8(row + m, v);
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j) {
       if (j < k) {
-        const float* wr = wgt + (size_t)ij[j] * M + m;
+        float g[8];
+        load8(wgt + (long)ij[j] * M + m, g);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) v[q] += dl[j] * wr[q];
+        for (int q = 0; q < 8; ++q) v[q] += dl[j] * g[q];
       }
     }
     store8(row + m, v);
   }
 }
 
-// dW_g partials: block (m-tile of 256 rows of x^T plus the bias row, split s).
-// Row m == M is the bias row (x = 1). P[s][m][e], m in [0, M].
-template <typename TIn, int EP>
-__global__ __launch_bounds__(256) void gate_bwd_dw_partial_kernel(
-    const TIn* __restrict__ x, const float* __restrict__ d_logits, float* __restrict__ P, int T,
-    int M, int E, int tokens_per_split) {
-  __shared__ float dls[64][EP];
-  const int m = blockIdx.x * 256 + threadIdx.x;
+// dW_g partials. Block (m tile of 64 columns of x, token split s); thread
+// (mg: 8 consecutive m, eg: 8 consecutive experts, tl: token lane) holds an
+// 8 x 8 tile and walks the split's tokens t = tl, tl + TL, ...; the TL lanes
+// are summed in LDS in lane order. P[s][m][e] for m < M; Pb[s][e] = sum of dl
+// (the bias row) from the blocks of m tile 0, which also write d_logits.
+template <typename TIn, int EG>
+__global__ __launch_bounds__(256) void gate_bwd_dw_kernel(
+    const TIn* __restrict__ x, const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const float* __restrict__ dw, float* __restrict__ d_logits, float* __restrict__ P,
+    float* __restrict__ Pb, int T, int M, int E, int k, int tokens_per_split) {
+  constexpr int TL = 32 / EG;
+  constexpr int NE = 8 * EG;  // experts covered by the block
+  __shared__ float red[TL][64 + 1][NE];
+  const int tid = threadIdx.x;
+  const int mg = tid & 7, eg = (tid >> 3) % EG, tl = tid / (8 * EG);
+  const int m0 = blockIdx.x * 64 + mg * 8;
+  const int e0 = eg * 8;
   const int s = blockIdx.y;
-  const int tb = s * tokens_per_split, te = min(T, tb + tokens_per_split);
-  float acc[EP];
+  const long tb = (long)s * tokens_per_split;
+  const long te = min((long)T, tb + tokens_per_split);
+  const bool first_tile = blockIdx.x == 0;
+  float acc[8][8], accb[8];
 #pragma unroll
-  for (int e = 0; e < EP; ++e) acc[e] = 0.f;
-  for (int c0 = tb; c0 < te; c0 += 64) {
-    const int n = min(64, te - c0);
-    __syncthreads();
-    for (int q = threadIdx.x; q < 64 * EP; q += 256) {
-      int tt = q / EP, e = q % EP;
-      dls[tt][e] = (tt < n && e < E) ? d_logits[(size_t)(c0 + tt) * E + e] : 0.f;
-    }
-    __syncthreads();
-    if (m <= M) {
-      for (int tt = 0; tt < n; ++tt) {
-        const float xv = (m < M) ? Elem<TIn>::load(x + (size_t)(c0 + tt) * M + m) : 1.0f;
+  for (int i = 0; i < 8; ++i) {
+    accb[i] = 0.f;
 #pragma unroll
-        for (int e = 0; e < EP; ++e) acc[e] += xv * dls[tt][e];
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
+  }
+  // tokens in batches of 4: every load of a batch is in flight together
+  constexpr int TB = 4;
+  for (long t0 = tb + tl; t0 < te; t0 += TB * TL) {
+    float xv[TB][8], d[TB][8];
+#pragma unroll
+    for (int u = 0; u < TB; ++u) {
+      const long t = t0 + u * TL;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) xv[u][q] = d[u][q] = 0.f;
+      if (t < te) {
+        int ij[kMaxK];
+        float dlk[kMaxK];
+        token_dl(idx, w, dw, t, k, ij, dlk);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+#pragma unroll
+          for (int j = 0; j < kMaxK; ++j)
+            if (ij[j] == e0 + q) d[u][q] = dlk[j];
+        if (m0 < M) load8(x + t * M + m0, xv[u]);
       }
     }
+#pragma unroll
+    for (int u = 0; u < TB; ++u) {
+      const long t = t0 + u * TL;
+      if (t >= te) break;
+      if (first_tile && mg == 0) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          if (e0 + q < E) d_logits[t * E + e0 + q] = d[u][q];
+          accb[q] += d[u][q];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[i][q] += xv[u][i] * d[u][q];
+    }
   }
-  if (m <= M) {
-    float* out = P + ((size_t)s * (M + 1) + m) * E;
-    for (int e = 0; e < E; ++e) out[e] = acc[e];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) red[tl][mg * 8 + i][e0 + q] = acc[i][q];
+  if (first_tile && mg == 0) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) red[tl][64][e0 + q] = accb[q];
   }
-}
-
-__global__ void gate_bwd_dw_reduce_kernel(const float* __restrict__ P, float* __restrict__ dw_gate,
-                                          float* __restrict__ dbias, int M, int E, int S,
-                                          int accumulate) {
-  const long n = (long)(M + 1) * E;
-  for (long q = blockIdx.x * (long)blockDim.x + threadIdx.x; q < n; q += (long)gridDim.x * blockDim.x) {
+  __syncthreads();
+  const int rows = first_tile ? 65 : 64;
+  for (int q = tid; q < rows * NE; q += 256) {
+    const int mm = q / NE, e = q % NE;
+    if (e >= E) continue;
     float v = 0.f;
-    for (int s = 0; s < S; ++s) v += P[(size_t)s * n + q];
-    const int m = (int)(q / E);
-    if (m < M) {
-      dw_gate[q] = accumulate ? dw_gate[q] + v : v;
-    } else if (dbias != nullptr) {
-      const int e = (int)(q % E);
-      dbias[e] = accumulate ? dbias[e] + v : v;
+    for (int l = 0; l < TL; ++l) v += red[l][mm][e];
+    if (mm == 64) {
+      Pb[(long)s * E + e] = v;
+    } else {
+      const int m = blockIdx.x * 64 + mm;
+      if (m < M) P[((long)s * M + m) * E + e] = v;
     }
   }
 }
 
+// dW_g[m][e] = sum over splits of P (split order), db likewise
+__global__ __launch_bounds__(256) void gate_bwd_dw_reduce_kernel(
+    const float* __restrict__ P, const float* __restrict__ Pb, float* __restrict__ dw_gate,
+    float* __restrict__ dbias, int M, int E, int S, int accumulate) {
+  const long n = (long)M * E;
+  const long q = blockIdx.x * 256L + threadIdx.x;
+  if (q >= n + E) return;
+  if (q < n) {
+    float v = 0.f;
+#pragma unroll 8
+    for (int s = 0; s < S; ++s) v += P[(long)s * n + q];
+    dw_gate[q] = accumulate ? dw_gate[q] + v : v;
+  } else if (q < n + E && dbias != nullptr) {
+    const int e = (int)(q - n);
+    float v = 0.f;
+    for (int s = 0; s < S; ++s) v += Pb[(long)s * E + e];
+    dbias[e] = accumulate ? dbias[e] + v : v;
+  }
+}
+
+int gate_eg(int E) { return E <= 8 ? 1 : E <= 16 ? 2 : E <= 32 ? 4 : 8; }
+
+// token splits: about two blocks per CU over the m tiles, at least one token
+// per token lane
 int gate_splits(const Shape& s) {
-  // enough blocks to fill the chip, at least 64 tokens per split
-  int by_tokens = (s.T + 63) / 64;
-  int sp = 64;
+  const int mtiles = (s.M + 63) / 64;
+  const int tl = 32 / gate_eg(s.E);
+  int sp = (512 + mtiles - 1) / mtiles;
+  const int by_tokens = (s.T + tl - 1) / tl;
   if (sp > by_tokens) sp = by_tokens;
   return sp < 1 ? 1 : sp;
 }
@@ -367,9 +477,17 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
   const int EP = pow2_at_least(s.E);
   if (s.dtype == FLOWMOE_BF16) {
     const int blocks = (s.T + kGateTok - 1) / kGateTok;
+    const int NB = (s.E + 15) / 16;
     return traced(FLOWMOE_K_GATE, st, [&] {
-      hipLaunchKernelGGL(gate_topk_mfma_kernel, dim3(blocks), dim3(256), 0, st, (const bf16_t*)x,
-                         (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M, s.E, s.k, EP);
+#define FLOWMOE_GATE_LAUNCH(NBV)                                                                  \
+  hipLaunchKernelGGL(gate_topk_mfma_kernel<NBV>, dim3(blocks), dim3(256), 0, st,                  \
+                     (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M, s.E, \
+                     s.k, EP)
+      if (NB == 1) FLOWMOE_GATE_LAUNCH(1);
+      else if (NB == 2) FLOWMOE_GATE_LAUNCH(2);
+      else if (NB == 3) FLOWMOE_GATE_LAUNCH(3);
+      else FLOWMOE_GATE_LAUNCH(4);
+#undef FLOWMOE_GATE_LAUNCH
     });
   }
   const int G = 64 / EP;
@@ -397,78 +515,96 @@ hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float
   });
 }
 
+// workspace: [W_g^T (E x M float) | P (S x M x E) | Pb (S x E)]
+size_t gate_wt_bytes(const Shape& s) { return align256((size_t)s.M * s.E * sizeof(float)); }
+
 size_t gate_bwd_ws_bytes(const Shape& s) {
-  const size_t wgt = align256((size_t)s.M * s.E * sizeof(float));
-  const size_t part = align256((size_t)gate_splits(s) * (s.M + 1) * s.E * sizeof(float));
-  return wgt + part;
+  const int S = gate_splits(s);
+  return gate_wt_bytes(s) + align256((size_t)S * s.M * s.E * sizeof(float)) +
+         align256((size_t)S * s.E * sizeof(float));
 }
 
-hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const int32_t* idx,
-                           const float* w, const float* dw, float* d_logits, float* dw_gate,
-                           float* dbias, void* dx, int accumulate, void* ws, hipStream_t st) {
+hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st) {
   float* wgt = static_cast<float*>(ws);
-  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                      align256((size_t)s.M * s.E * sizeof(float)));
-  const bool bf = s.dtype == FLOWMOE_BF16;
+  const long n = (long)s.M * s.E;
+  const int nb = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+  return traced(FLOWMOE_K_GATE_BWD_WT, st, [&] {
+    if (s.dtype == FLOWMOE_BF16)
+      hipLaunchKernelGGL(transpose_wg_kernel<bf16_t>, dim3(nb), dim3(256), 0, st,
+                         (const bf16_t*)w_gate, wgt, s.M, s.E);
+    else
+      hipLaunchKernelGGL(transpose_wg_kernel<float>, dim3(nb), dim3(256), 0, st,
+                         (const float*)w_gate, wgt, s.M, s.E);
+  });
+}
+
+hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, const float* dw,
+                          const float* wgt, void* dx, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const int tb = (s.T + 3) / 4;
+  return traced(FLOWMOE_K_GATE_BWD_TOKEN, st, [&] {
+    if (s.dtype == FLOWMOE_BF16)
+      hipLaunchKernelGGL(gate_bwd_dx_kernel<bf16_t>, dim3(tb), dim3(256), 0, st, idx, w, dw, wgt,
+                         (bf16_t*)dx, s.T, s.M, s.k);
+    else
+      hipLaunchKernelGGL(gate_bwd_dx_kernel<float>, dim3(tb), dim3(256), 0, st, idx, w, dw, wgt,
+                         (float*)dx, s.T, s.M, s.k);
+  });
+}
+
+hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, const float* w,
+                          const float* dw, float* d_logits, float* dw_gate, float* dbias,
+                          int accumulate, void* ws, hipStream_t st) {
   const int S = gate_splits(s);
-  hipError_t e = hipSuccess;
+  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + gate_wt_bytes(s));
+  float* Pb = reinterpret_cast<float*>(reinterpret_cast<char*>(P) +
+                                       align256((size_t)S * s.M * s.E * sizeof(float)));
+  const bool bf = s.dtype == FLOWMOE_BF16;
   if (s.T > 0) {
-    if (dx != nullptr) {
-      const int nb = (int)(((long)s.M * s.E + 255) / 256);
-      e = traced(FLOWMOE_K_GATE_BWD_WT, st, [&] {
-        if (bf)
-          hipLaunchKernelGGL(transpose_wg_kernel<bf16_t>, dim3(nb), dim3(256), 0, st,
-                             (const bf16_t*)w_gate, wgt, s.M, s.E);
-        else
-          hipLaunchKernelGGL(transpose_wg_kernel<float>, dim3(nb), dim3(256), 0, st,
-                             (const float*)w_gate, wgt, s.M, s.E);
-      });
-      if (e != hipSuccess) return e;
-    }
-    const int tb = (s.T + 3) / 4;
-    e = traced(FLOWMOE_K_GATE_BWD_TOKEN, st, [&] {
-      if (bf)
-        hipLaunchKernelGGL(gate_bwd_token_kernel<bf16_t>, dim3(tb), dim3(256), 0, st, idx, w, dw,
-                           wgt, d_logits, (bf16_t*)dx, s.T, s.M, s.E, s.k);
-      else
-        hipLaunchKernelGGL(gate_bwd_token_kernel<float>, dim3(tb), dim3(256), 0, st, idx, w, dw,
-                           wgt, d_logits, (float*)dx, s.T, s.M, s.E, s.k);
-    });
-    if (e != hipSuccess) return e;
     const int tps = (s.T + S - 1) / S;
-    dim3 grid((s.M + 1 + 255) / 256, S);
-    const int EP = pow2_at_least(s.E);
-    e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
-#define FLOWMOE_DW_LAUNCH(EPV)                                                                   \
+    const dim3 grid((s.M + 63) / 64, S);
+    const int EG = gate_eg(s.E);
+    hipError_t e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
+#define FLOWMOE_DW_LAUNCH(EGV)                                                                   \
   if (bf)                                                                                        \
-    hipLaunchKernelGGL((gate_bwd_dw_partial_kernel<bf16_t, EPV>), grid, dim3(256), 0, st,        \
-                       (const bf16_t*)x, d_logits, P, s.T, s.M, s.E, tps);                       \
+    hipLaunchKernelGGL((gate_bwd_dw_kernel<bf16_t, EGV>), grid, dim3(256), 0, st,                \
+                       (const bf16_t*)x, idx, w, dw, d_logits, P, Pb, s.T, s.M, s.E, s.k, tps);  \
   else                                                                                           \
-    hipLaunchKernelGGL((gate_bwd_dw_partial_kernel<float, EPV>), grid, dim3(256), 0, st,         \
-                       (const float*)x, d_logits, P, s.T, s.M, s.E, tps);
-      if (EP <= 8) {
-        FLOWMOE_DW_LAUNCH(8)
-      } else if (EP <= 16) {
-        FLOWMOE_DW_LAUNCH(16)
-      } else if (EP <= 32) {
-        FLOWMOE_DW_LAUNCH(32)
+    hipLaunchKernelGGL((gate_bwd_dw_kernel<float, EGV>), grid, dim3(256), 0, st,                 \
+                       (const float*)x, idx, w, dw, d_logits, P, Pb, s.T, s.M, s.E, s.k, tps);
+      if (EG == 1) {
+        FLOWMOE_DW_LAUNCH(1)
+      } else if (EG == 2) {
+        FLOWMOE_DW_LAUNCH(2)
+      } else if (EG == 4) {
+        FLOWMOE_DW_LAUNCH(4)
       } else {
-        FLOWMOE_DW_LAUNCH(64)
+        FLOWMOE_DW_LAUNCH(8)
       }
 #undef FLOWMOE_DW_LAUNCH
     });
     if (e != hipSuccess) return e;
   }
-  const long n = (long)(s.M + 1) * s.E;
-  const int nb = (int)((n + 255) / 256);
   if (s.T == 0 && accumulate) return hipSuccess;
   // with no tokens the gradient is zero: a reduce over zero splits writes it
   const int splits = s.T > 0 ? S : 0;
   const int acc = s.T > 0 ? accumulate : 0;
+  const long n = (long)s.M * s.E + s.E;
+  const int nb = (int)((n + 255) / 256);
   return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
-    hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nb), dim3(256), 0, st, P, dw_gate, dbias,
-                       s.M, s.E, splits, acc);
+    hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nb), dim3(256), 0, st, P, Pb, dw_gate,
+                       dbias, s.M, s.E, splits, acc);
   });
+}
+
+hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const int32_t* idx,
+                           const float* w, const float* dw, float* d_logits, float* dw_gate,
+                           float* dbias, void* dx, int accumulate, void* ws, hipStream_t st) {
+  hipError_t e = launch_gate_dw(s, x, idx, w, dw, d_logits, dw_gate, dbias, accumulate, ws, st);
+  if (e != hipSuccess || dx == nullptr || s.T == 0) return e;
+  e = launch_gate_wt(s, w_gate, ws, st);
+  if (e != hipSuccess) return e;
+  return launch_gate_dx(s, idx, w, dw, gate_ws_wgt(ws), dx, st);
 }
 
 }  // namespace flowmoe

@@ -52,8 +52,9 @@ def test_workspace_sizes(flowmoe_lib):
     assert L.flowmoe_workspace_bytes(s, L.WS_DISPATCH) == 0
     assert L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD) >= 8192 * 4096 * 2
     assert L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD) >= 1024 * 8 * 4
-    assert L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD) == max(
-        L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD), L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD))
+    # the layer's gate and expert backward run concurrently: disjoint regions
+    assert L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD) >= (
+        L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD) + L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD))
     sw = L.make_shape(4096, 1024, 4096, 8, 2, 1229, L.BF16, L.SWIGLU, L.PACKED)
     assert L.flowmoe_workspace_bytes(sw, L.WS_FFN_BWD) >= 8192 * 8192 * 2
 
@@ -132,3 +133,20 @@ def test_layer_validation(flowmoe_lib):
     with pytest.raises(L.FlowMoEError) as ei:
         L.flowmoe_layer_fwd(s, 1, b, s_compute=0, s_comm=0)
     assert "w_gate" in str(ei.value)
+
+
+def test_misaligned_tensors_rejected(flowmoe_lib):
+    # layer-dtype tensors are moved in 16-byte vectors: a misaligned one is an
+    # argument error, caught before anything is enqueued
+    s = L.make_shape(16, 64, 64, 4, 2, 8, L.BF16)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_gate_topk(s, FAKE + 8, FAKE, None, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "aligned" in str(ei.value)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_gate_topk(s, FAKE, FAKE + 2, None, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "w_gate" in str(ei.value)
+    need = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_gate_topk_bwd(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE + 4, 0, FAKE,
+                                need, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "dx" in str(ei.value)

@@ -44,6 +44,28 @@ def test_gate_topk(E, k, dtype):
     assert np.allclose(gl[0], host(bias))
 
 
+@pytest.mark.parametrize("T,M,E,k", [(77, 520, 64, 6), (130, 1000, 33, 3), (40, 4104, 8, 2)])
+def test_gate_topk_chunked_weights(T, M, E, k):
+    """W_g taller than one LDS chunk of the bf16 gate (32 KB of rows: 256 rows
+    at E = 64, 496 at E = 33, 2048 at E = 8), with a ragged last chunk."""
+    need_gpu()
+    cfg = get_config("balanced", T=T, M=M, H=8, E=E, k=k, dtype="bf16", seed=M + E)
+    inp = make_inputs(cfg, with_dy=False)
+    d = dev()
+    x, wg = to_torch(inp["x"], d), to_torch(inp["w_gate"], d)
+    logits = torch.empty(T, E, device=d)
+    idx = torch.empty(T, k, dtype=torch.int32, device=d)
+    w = torch.empty(T, k, device=d)
+    L.flowmoe_gate_topk(_shape(T, M, 8, E, k, 0), x, wg, None, logits, idx, w)
+    torch.cuda.synchronize()
+    own = oracle.gate_logits(as_f64(inp["x"]), as_f64(inp["w_gate"]), None)
+    gl = host(logits)
+    assert np.max(np.abs(gl - own)) <= 1e-4 * np.max(np.abs(own))
+    ref_i, ref_w = oracle.topk_select(gl, k)
+    assert np.array_equal(host(idx), ref_i)
+    np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
+
+
 def test_route_ties_and_signed_zeros():
     need_gpu()
     rng = np.random.default_rng(7)
@@ -88,6 +110,7 @@ def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t):
 @pytest.mark.parametrize("T,E,k,cf", [
     (1, 1, 1, 1.0), (1, 4, 2, 1.0), (37, 1, 1, 1.0), (100, 4, 4, 1.0), (300, 8, 2, 1.2),
     (1000, 16, 1, 1.0), (2048, 64, 6, 1.5), (777, 7, 3, 0.3), (5000, 8, 2, 1.25),
+    (13000, 4, 4, 1.1),  # T*k = 52000: more assignments than the scan stages in LDS
 ])
 def test_dispatch(T, E, k, cf, layout):
     need_gpu()
