@@ -517,6 +517,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
 // Requires the reduction length of the row mode to be a multiple of 32.
 constexpr int DBK = 32;
 constexpr int DSTAGES = 4;
+constexpr int kRowGroup = 4;  // row tiles per group of the row-mode tile order
 constexpr int DSTAGE_BYTES = 32768;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -545,6 +546,11 @@ __device__ __forceinline__ u32x4 make_rsrc(const void* base, long bytes) {
 __device__ __forceinline__ void dma16(u32x4 d, char* lds_block, unsigned voff) {
   const unsigned m0v =
       __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_void_t*)lds_block);
+  // the descriptor is wave-uniform; say so, so that it sits in scalar registers
+  d.x = __builtin_amdgcn_readfirstlane(d.x);
+  d.y = __builtin_amdgcn_readfirstlane(d.y);
+  d.z = __builtin_amdgcn_readfirstlane(d.z);
+  d.w = __builtin_amdgcn_readfirstlane(d.w);
   unsigned saved;  // m0 is reserved: keep the compiler's value intact
   asm volatile(
       "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\t"
@@ -606,11 +612,16 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
   const int wm = wave / WGN, wn = wave % WGN;
   const int vbid = xcd_remap(blockIdx.x, gridDim.x);
 
-  // ---- which tile (same scheme as gemm_bf16_kernel) ----
+  // ---- which tile ----
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
   if constexpr (MODE == MODE_ROWS) {
-    nt = vbid % p.ntiles;
-    const int ml = vbid / p.ntiles;
+    // Grouped order: consecutive blocks (one XCD's share, running together)
+    // walk kRowGroup row tiles x the column tiles, row tiles fastest
+    const int gsz = kRowGroup * p.ntiles;
+    const int g = vbid / gsz, r = vbid - g * gsz;
+    const int gm = min(kRowGroup, p.mt_bound - g * kRowGroup);  // row tiles in this group
+    nt = r / gm;
+    const int ml = g * kRowGroup + (r - nt * gm);
     int acc_t = 0;
     mt = -1;
     for (e = 0; e < p.E; ++e) {
@@ -716,25 +727,31 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
     b_kstep = DBK * p.ldb * 2;
   }
 
-  auto issue = [&](int kt, int stage) {
+  // Loads of k-tile kt into stage `stage`, in two parts: part q takes this
+  // wave's blocks i in [q * BPW / 2, (q + 1) * BPW / 2) of both operands.
+  auto issue_part = [&](int kt, int stage, int q) {
     char* sa = smem + stage * DSTAGE_BYTES;
     char* sb = sa + DSTAGE_BYTES / 2;
     const unsigned ka = (unsigned)kt * (unsigned)a_kstep;
+    constexpr int H = BPW / 2;
 #pragma unroll
-    for (int i = 0; i < BPW; ++i) dma16(ra, sa + (wave + NW * i) * 1024, aoff[i] + ka);
-    if constexpr (B_KC) {
-      const int k0 = kt * DBK;
-      const bool second = k0 >= p.ksplit;
-      const unsigned kb = (unsigned)((second ? k0 - p.ksplit : k0) * 2);
-#pragma unroll
-      for (int i = 0; i < BPW; ++i)
+    for (int i = q * H; i < (q + 1) * H; ++i) {
+      dma16(ra, sa + (wave + NW * i) * 1024, aoff[i] + ka);
+      if constexpr (B_KC) {
+        const int k0 = kt * DBK;
+        const bool second = k0 >= p.ksplit;
+        const unsigned kb = (unsigned)((second ? k0 - p.ksplit : k0) * 2);
         dma16(second ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
-    } else {
-      const unsigned kb = (unsigned)kt * (unsigned)b_kstep;
-#pragma unroll
-      for (int i = 0; i < BPW; ++i)  // blocks 8..15 (i >= BPW/2, as wave < NW) hold the W3 panel
+      } else {
+        const unsigned kb = (unsigned)kt * (unsigned)b_kstep;
+        // blocks 8..15 (i >= BPW/2, as wave < NW) hold the W3 panel
         dma16((DUAL && i >= BPW / 2) ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
+      }
     }
+  };
+  auto issue = [&](int kt, int stage) {
+    issue_part(kt, stage, 0);
+    issue_part(kt, stage, 1);
   };
 
   floatx16 acc[FM][FN];
@@ -772,13 +789,14 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
   // fragment, two ds_read_b64_tr_b16 for an M/N-contiguous one)
   constexpr int NRD = FM * (A_KC ? 1 : 2) + FN * (B_KC ? 1 : 2);
   constexpr int NMF = FM * FN;
-  auto mfmas = [&](int set) {
+  auto mfma_rows = [&](int set, int i0, int i1) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = i0; i < i1; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[set][j], af[set][i], acc[i][j], 0, 0, 0);
   };
+  auto mfmas = [&](int set) { mfma_rows(set, 0, FM); };
   // interleave the MFMAs of one set with the LDS reads of the other
   auto interleave = [&]() {
 #pragma unroll
@@ -787,6 +805,25 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
       __builtin_amdgcn_sched_group_barrier(0x008, (NMF + NRD - 1) / NRD, 0);  // MFMAs
     }
     __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);  // the rest of the MFMAs
+  };
+  // One half k-step: the LDS reads of the next set interleaved with the
+  // first half of this set's MFMAs, then one part of a k-tile's loads (if
+  // any) between the two halves of the MFMAs, so that the memory pipe takes
+  // the loads a few at a time while the matrix pipe stays busy. The
+  // scheduling barriers keep the inline-asm loads where they are.
+  auto half_step = [&](int set, auto&& reads, auto&& loads) {
+    reads();
+    mfma_rows(set, 0, FM / 2);
+#pragma unroll
+    for (int q = 0; q < NRD; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, (NMF / 2 + NRD - 1) / NRD, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NMF / 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    loads();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_rows(set, FM / 2, FM);
   };
 
   // Ring of DSTAGES k-tiles: tile t lives in stage t % DSTAGES. Every wave
@@ -817,21 +854,32 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
   }
   // All tiles but the last: the barrier sits between the two k steps, so
   // each half pairs the MFMAs of one step with the reads of the next.
+  // The loads of tile kt + DSTAGES go out in two parts: the first in the
+  // second half of iteration kt (its stage was freed by that iteration's
+  // barrier), the second in the first half of iteration kt + 1, both before
+  // the wait that needs them (iteration kt + DSTAGES - 1).
   for (int kt = 0; kt + 1 < nk; ++kt) {
     const int stage = kt % DSTAGES;
-    read_frags(stage, 1, 1);  // step 1 of tile kt ...
-    mfmas(0);                 // ... while step 0 of tile kt runs
-    interleave();
+    // step 1 of tile kt is read while step 0 runs; second part of tile kt + 3
+    half_step(
+        0, [&] { read_frags(stage, 1, 1); },
+        [&] {
+          const int tl = kt + DSTAGES - 1;
+          if (tl >= DSTAGES && tl < nk) issue_part(tl, tl % DSTAGES, 1);
+        });
     // this wave's reads of tile kt are done (lgkmcnt 0) and its loads of
     // tile kt + 1 have landed; after the barrier every wave's have
     wait_tile(kt + 1, DSTAGES - 2);
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (kt + DSTAGES < nk) issue(kt + DSTAGES, stage);
-    read_frags((kt + 1) % DSTAGES, 0, 0);  // step 0 of tile kt + 1 ...
-    mfmas(1);                              // ... while step 1 of tile kt runs
-    interleave();
+    // step 0 of tile kt + 1 is read while step 1 of tile kt runs; first part
+    // of tile kt + 4 into the stage tile kt leaves
+    half_step(
+        1, [&] { read_frags((kt + 1) % DSTAGES, 0, 0); },
+        [&] {
+          if (kt + DSTAGES < nk) issue_part(kt + DSTAGES, stage, 0);
+        });
   }
   if (nk > 0) {
     read_frags((nk - 1) % DSTAGES, 1, 1);
