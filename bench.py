@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--R", type=int, default=None, help="override the chunk count")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-memory-bound", action="store_true",
+                    help="skip the per-call timing of the memory-bound steps")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy a MIB-sized buffer once: the plain copy "
                          "kernel of known size that calibrates HBM byte counters")
@@ -55,6 +57,56 @@ def gemm_flops_per_launch(cfg, kept: int) -> float:
     launch does 2 * kept * M * H (SwiGLU's fused W1|W3 launch, its
     [dW1 | dW3] launch and its K = 2H dgrad launch do twice that)."""
     return 2.0 * kept * cfg.M * cfg.H
+
+
+def memory_bound(L, layer, cfg, torch, reps: int = 20):
+    """Achieved bandwidth of the memory-bound steps of chunk 0: each C-ABI call
+    repeated `reps` times back to back on one stream (inputs warm: after the
+    timed steps, and small enough here to stay in the 256 MB Infinity Cache),
+    against the algorithmic bytes of the step (kept rows A of the chunk):
+      gate T*M*b; dispatch (scan + gather) (T + A)*M*b; combine (A + T)*M*b;
+      combine bwd (T + 2A)*M*b; dispatch bwd (A + T)*M*b; gate bwd T*M*b."""
+    s = layer.shape
+    T, M, E, k = s.T, s.M, s.E, s.k
+    b = 2 if layer.dt == L.BF16 else 4
+    A = int(layer.counts[0].sum().item())
+    st = torch.cuda.current_stream()
+    x, y, dy, dx = layer.x[:T], layer.y[:T], layer.dy[:T], layer.dx[:T]
+    lg, idx, w = layer.logits[:T], layer.topk_idx[:T], layer.topk_w[:T]
+    dw, dl, slot = layer.d_topk_w[:T], layer.d_logits[:T], layer.slot[:T]
+    cnt, off, rs, ld = layer.counts[0], layer.offsets[0], layer.row_src[0], layer.load[0]
+    xd, yd, dyd, dxd = layer.x_disp[0], layer.y_disp[0], layer.dy_disp[0], layer.dx_disp[0]
+    steps = {
+        "gate": (lambda: L.flowmoe_gate_topk(s, x, layer.w_gate, layer.bias, lg, idx, w, stream=st),
+                 T * M * b),
+        "dispatch (scan + gather)": (
+            lambda: L.flowmoe_dispatch(s, idx, x, cnt, off, slot, rs, ld, xd, stream=st),
+            (T + A) * M * b),
+        "combine": (lambda: L.flowmoe_combine(s, yd, slot, w, y, stream=st), (A + T) * M * b),
+        "combine bwd": (lambda: L.flowmoe_combine_bwd(s, dy, yd, slot, w, cnt, off, dyd, dw,
+                                                      stream=st), (T + 2 * A) * M * b),
+        "dispatch bwd": (lambda: L.flowmoe_dispatch_bwd(s, dxd, slot, dx, stream=st),
+                         (A + T) * M * b),
+        "gate bwd (d_logits, dW_g)": (
+            lambda: L.flowmoe_gate_topk_bwd(s, x, layer.w_gate, idx, w, dw, dl, layer.dw_gate,
+                                            layer.dbias, None, 0, layer.ws, layer.ws_bytes,
+                                            stream=st), T * M * b),
+    }
+    out = {}
+    for name, (fn, nbytes) in steps.items():
+        fn()
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
+            fn()
+        e1.record(st)
+        e1.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        gbs = nbytes / (us * 1e-6) / 1e9
+        out[name] = {"bytes": nbytes, "us": round(us, 2), "GBps": round(gbs, 1),
+                     "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return out
 
 
 def main():
@@ -102,16 +154,23 @@ def main():
     torch.cuda.synchronize()
     kept = int(layer.counts.sum().item())
 
-    # timed region: every grouped-GEMM launch bracketed by HIP events on its stream
+    # timed region: every grouped-GEMM launch bracketed by HIP events on its
+    # stream; an event on the compute stream after every step for the step
+    # time distribution
     gemm_per_step = 6 * R
     ev = EventArray(gemm_per_step * a.steps)
+    step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
     L.flowmoe_trace_start(ev.ev, ev.kinds, ev.pairs, L.kind_mask(L.K_GEMM))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(a.steps):
+    step_ev[0].record(sc)
+    for i in range(a.steps):
         step()
+        step_ev[i + 1].record(sc)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    step_ms = sorted(step_ev[i].elapsed_time(step_ev[i + 1]) for i in range(a.steps))
+    q = lambda f: float(np.percentile(step_ms, f))
     n = L.flowmoe_trace_stop()
     elapsed = t1 - t0
     gemm_ms = [ev.elapsed_ms(i) for i in range(n)]
@@ -133,7 +192,9 @@ def main():
 
     ms_per_step = elapsed / a.steps * 1e3
     tokens_per_s = cfg.T * a.steps / elapsed
-    fl = gemm_flops_per_launch(cfg, kept)
+    # each launch covers one chunk: average FLOPs per launch use kept / R rows
+    # (exact for the sum, as every chunk's six launches appear once per step)
+    fl = gemm_flops_per_launch(cfg, kept / R)
     mult = {"ffn1": 2.0 if cfg.act == "swiglu" else 1.0, "ffn2": 1.0, "dgrad1": 1.0, "wgrad2": 1.0,
             "wgrad1": 2.0 if cfg.act == "swiglu" else 1.0,
             "dgrad2": 2.0 if cfg.act == "swiglu" else 1.0}
@@ -141,6 +202,8 @@ def main():
     tot_s = sum(gemm_ms) / 1e3
     avg_launch_ms = sum(gemm_ms) / max(1, len(gemm_ms))
     achieved_tflops = tot_flops / tot_s / 1e12 if tot_s > 0 else 0.0
+
+    mem = None if a.no_memory_bound else memory_bound(L, layer, cfg, torch)
 
     if a.copy_probe > 0:
         n = a.copy_probe * 2**20 // 4
@@ -221,6 +284,9 @@ def main():
             "launches": len(gemm_ms),
         },
         "gemm_mfma_util_pct": round(100 * achieved_tflops / PEAK_BF16_TFLOPS, 2),
+        "step_ms_median": round(q(50), 4),
+        "step_ms_iqr": [round(q(25), 4), round(q(75), 4)],
+        "memory_bound": mem,
         "kernel_us_per_step": breakdown,
         "cpu_baseline": cpu,
     }
