@@ -266,7 +266,7 @@ def main():
         "config": {
             "workload": (f"{cfg.name} MoE layer: T={cfg.T} M={cfg.M} H={cfg.H} E={cfg.E} "
                          f"top-{cfg.k} f={cfg.f} {cfg.act} {cfg.dtype}, R={R}, {a.layout}, "
-                         f"{'1' if a.one_stream else '2'} stream(s)"),
+                         f"{'1' if (a.one_stream or R == 1) else '2'} stream(s)"),
             "T": cfg.T, "M": cfg.M, "H": cfg.H, "E": cfg.E, "k": cfg.k, "f": cfg.f,
             "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "kept_rows": kept,
         },

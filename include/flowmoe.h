@@ -292,7 +292,8 @@ typedef struct {
  * (Eq. 4); events make D_r wait for AT_r, E_r for D_r and C_r for E_r.
  * The call first makes s_comm wait for work already on s_compute and ends by
  * making s_compute wait for s_comm, so to the caller it is one operation on
- * s_compute. s_comm may equal s_compute (serial schedule, same results).
+ * s_compute. s_comm may equal s_compute (serial schedule, same results); with
+ * R = 1 there is nothing to overlap and everything runs on s_compute.
  * trace (nullable): 8*R events, recorded at start/end of each task, at index
  * 2*(task*R + r) (+1 for the end), task 0 = gate, 1 = dispatch,
  * 2 = experts, 3 = combine. The events must be created by the caller. */

@@ -497,6 +497,9 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
     REQUIRE_T(b->h_save, "bufs->h_save"); REQUIRE_T(b->a_save, "bufs->a_save");
     REQUIRE_T(b->y_disp, "bufs->y_disp");
   }
+  // With one chunk there is no overlap to gain and each cross-stream event
+  // wait costs several microseconds: one chunk runs on s_compute only.
+  if (R == 1) s_comm = s_compute;
   Sched sc{s_compute, s_comm, s_comm != s_compute, trace, R};
   hipEvent_t* ev = nullptr;
   sc.run(get_events(3 * R + 2, &ev));
@@ -577,6 +580,9 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
   const size_t need = flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
   st = check_ws(b->ws, b->ws_bytes, need, "flowmoe_layer_bwd");
   if (st != FLOWMOE_OK) return st;
+  // With one chunk there is no overlap to gain and each cross-stream event
+  // wait costs several microseconds: one chunk runs on s_compute only.
+  if (R == 1) s_comm = s_compute;
   Sched sc{s_compute, s_comm, s_comm != s_compute, trace, R};
   hipEvent_t* ev = nullptr;
   sc.run(get_events(3 * R + 2, &ev));
