@@ -185,8 +185,8 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
 
 // Epilogue shared by the bf16 kernels: the block's accumulators (each wave
 // WM x WN, acc[i][j][4*g + q] = C[row wm*WM + i*32 + lane%32]
-// [col wn*WN + j*32 + 8*g + 4*(lane/32) + q]) to global memory. Row mode
-// stages through LDS (smem must be free; at least (NT/64)*64*WN floats).
+// [col wn*WN + j*32 + 8*g + 4*(lane/32) + q]) to global memory, staged
+// through LDS (smem must be free; at least (NT/64)*64*WN floats).
 template <int MODE, int EPI, int BM, int BN, int NT>
 __device__ __forceinline__ void gemm_epilogue(const GemmParams& p,
                                               floatx16 (&acc)[BM / 64][BN / (NT / 128) / 32],
@@ -200,10 +200,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p,
   // acc[i][j][4*g + q] is C[row wm*WM + i*32 + lane%32]
   //                        [col wn*WN + j*32 + 8*g + 4*(lane/32) + q], q = 0..3
   const int lrow = lane & 31, lcol = 4 * (lane >> 5);
-  if constexpr (MODE == MODE_ROWS) {
+  {
     // The wave's 128 x WN tile goes out 64 rows at a time through its own LDS
     // region (fp32, 16-byte chunks XOR-swizzled by row), then each lane
-    // writes 8 consecutive outputs of one row: full 128-byte lines.
+    // writes 8 consecutive outputs of one row: full 128-byte lines (bf16
+    // rows of the dispatched buffers, or fp32 rows of the weight gradients).
     // The main loop ended with a barrier, so the tile buffers are free.
     static_assert(FM % 2 == 0, "staged epilogue works on 64-row halves");
     constexpr int SCH = WN / 4;  // 16-byte chunks per staged row
@@ -262,6 +263,30 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p,
           store8(C0 + g * p.ldc + p.Hh + n, h3);
           store8(C1 + g * p.ldc1 + n, a);
         }
+      } else if constexpr (MODE == MODE_KSUM) {  // fp32 weight gradient, C0 | C1 split at nsplit
+        constexpr int G8 = WN / 8;
+        constexpr int PER = 64 * G8 / 64;
+        float* D0 = static_cast<float*>(p.C0);
+        float* D1 = static_cast<float*>(p.C1);
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+          const int item = it * 64 + lane;
+          const int rr = item / G8, c8 = item % G8;
+          const int m = mt * BM + wm * WM + hf * 64 + rr;
+          const int n = n0 + wn * WN + c8 * 8;
+          if (m >= p.Mdim || n >= p.N) continue;  // N and nsplit are multiples of 8
+          float v[8];
+          read8(rr, c8, v);
+          float* dst = (n < p.nsplit) ? D0 + (long)e * p.c_estride + (long)m * p.ldc + n
+                                      : D1 + (long)e * p.c_estride + (long)m * p.ldc + (n - p.nsplit);
+          if (p.accumulate) {
+            float o[8];
+            load8(dst, o);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] += o[q];
+          }
+          store8(dst, v);
+        }
       } else {
         constexpr int G8 = WN / 8;
         constexpr int PER = 64 * G8 / 64;
@@ -313,31 +338,6 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p,
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    }
-  } else {  // KSUM wgrad, fp32 out
-    float* C0 = static_cast<float*>(p.C0);
-    float* C1 = static_cast<float*>(p.C1);
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int m = mt * BM + wm * WM + i * 32 + lrow;
-      if (m >= p.Mdim) continue;
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-#pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-          const int n = n0 + wn * WN + j * 32 + 8 * gq + lcol;
-          if (n >= p.N) continue;
-          float* dst = (n < p.nsplit) ? C0 + (long)e * p.c_estride + (long)m * p.ldc + n
-                                      : C1 + (long)e * p.c_estride + (long)m * p.ldc + (n - p.nsplit);
-          float4 v = make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2],
-                                 acc[i][j][4 * gq + 3]);
-          if (p.accumulate) {
-            const float4 o = *reinterpret_cast<const float4*>(dst);
-            v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
-          }
-          *reinterpret_cast<float4*>(dst) = v;
-        }
-      }
     }
   }
 }
