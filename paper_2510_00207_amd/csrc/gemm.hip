@@ -518,6 +518,73 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
 constexpr int DBK = 32;
 constexpr int DSTAGES = 4;
 constexpr int kRowGroup = 4;  // row tiles per group of the row-mode tile order
+
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+
+// Row-mode tile of the streaming kernel for block `bid`. The row tiles fall
+// in two classes: heavy ones (at least half a tile of live rows) and light
+// ones (an expert's short last tile, or padding only). Every XCD (blocks are
+// dispatched round-robin over the 8 XCDs) takes an equal share of each class
+// and runs its heavy tiles first, so that the light tiles make up the last,
+// partial round on every XCD instead of a full-cost round on some. Inside a
+// class, consecutive tiles walk kRowGroup row tiles x the column tiles, row
+// tiles fastest, so that the blocks running together on one XCD share A rows
+// and B columns through its L2. Returns false for a block with no tile.
+template <int BM>
+__device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, int& e, int& mt,
+                                                  int& nt, int& rows_e, int& cnt_e) {
+  int HR = 0, LR = 0;  // heavy / light row tiles
+  for (int x = 0; x < p.E; ++x) {
+    const int c = p.counts[x], r = p.padC ? p.padC : c;
+    const int te = (r + BM - 1) / BM;
+    const int he = min(te, (c + BM / 2) / BM);
+    HR += he;
+    LR += te - he;
+  }
+  const int x = bid & 7, i = bid >> 3;
+  const int H = HR * p.ntiles, L = LR * p.ntiles;
+  const int hx = (H >> 3) + (x < (H & 7)), lx = (L >> 3) + (x < (L & 7));
+  bool heavy;
+  int idx, nrows;
+  if (i < hx) {
+    heavy = true;
+    idx = x * (H >> 3) + min(x, H & 7) + i;
+    nrows = HR;
+  } else if (i < hx + lx) {
+    heavy = false;
+    idx = x * (L >> 3) + min(x, L & 7) + (i - hx);
+    nrows = LR;
+  } else {
+    return false;
+  }
+  const int gsz = kRowGroup * p.ntiles;
+  const int g = idx / gsz, rg = idx - g * gsz;
+  const int gm = min(kRowGroup, nrows - g * kRowGroup);  // row tiles in this group
+  nt = rg / gm;
+  const int ml = g * kRowGroup + (rg - nt * gm);
+  int acc_t = 0;
+  for (e = 0; e < p.E; ++e) {
+    const int c = p.counts[e], r = p.padC ? p.padC : c;
+    const int te = (r + BM - 1) / BM;
+    const int he = min(te, (c + BM / 2) / BM);
+    const int ce = heavy ? he : te - he;
+    if (ml < acc_t + ce) {
+      mt = (heavy ? 0 : he) + (ml - acc_t);
+      rows_e = r;
+      cnt_e = c;
+      return true;
+    }
+    acc_t += ce;
+  }
+  return false;
+}
+
+// grid of the streaming kernel in row mode: ceil(tiles / 8) + 1 blocks per
+// XCD cover any split of the tile bound into the two classes
+__host__ __device__ constexpr long row_mode_blocks(long tile_bound) { return 8 * ((tile_bound + 7) / 8 + 1); }
 constexpr int DSTAGE_BYTES = 32768;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -615,28 +682,7 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
   // ---- which tile ----
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
   if constexpr (MODE == MODE_ROWS) {
-    // Grouped order: consecutive blocks (one XCD's share, running together)
-    // walk kRowGroup row tiles x the column tiles, row tiles fastest
-    const int gsz = kRowGroup * p.ntiles;
-    const int g = vbid / gsz, r = vbid - g * gsz;
-    const int gm = min(kRowGroup, p.mt_bound - g * kRowGroup);  // row tiles in this group
-    nt = r / gm;
-    const int ml = g * kRowGroup + (r - nt * gm);
-    int acc_t = 0;
-    mt = -1;
-    for (e = 0; e < p.E; ++e) {
-      const int c = p.counts[e];
-      const int r = p.padC ? p.padC : c;
-      const int te = (r + BM - 1) / BM;
-      if (ml < acc_t + te) {
-        mt = ml - acc_t;
-        rows_e = r;
-        cnt_e = c;
-        break;
-      }
-      acc_t += te;
-    }
-    if (mt < 0) return;
+    if (!row_tile_of_block<BM>(p, blockIdx.x, e, mt, nt, rows_e, cnt_e)) return;
     row0 = p.offsets[e] + mt * BM;
   } else {
     const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
@@ -650,7 +696,8 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
   constexpr int NCOLS = DUAL ? BN / 2 : BN;
   const int n0 = nt * NCOLS;
   const int Kred = (MODE == MODE_ROWS) ? p.K : cnt_e;
-  const int nk = (Kred + DBK - 1) / DBK;
+  // a padding-only tile (padded layout) has nothing to reduce: zeros
+  const int nk = (MODE == MODE_ROWS && cnt_e <= mt * BM) ? 0 : (Kred + DBK - 1) / DBK;
 
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
   const bf16_t* B0 = static_cast<const bf16_t*>(p.B0);
@@ -762,70 +809,6 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Fragments of one 16-deep k step; two sets so that the LDS reads of the
-  // next step are in flight while the MFMAs of the current one run.
-  bf16x8 af[2][FM], bfr[2][FN];
-  auto read_frags = [&](int stage, int kk, int set) {
-    const char* sa = smem + stage * DSTAGE_BYTES;
-    const char* sb = sa + DSTAGE_BYTES / 2;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      if constexpr (A_KC)
-        af[set][i] = frag_kc(sa, wm * WM + i * 32 + (lane & 31), kk, lane);
-      else
-        af[set][i] = frag_mnc<256>(sa, wm * WM + i * 32, kk, lane);
-    }
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      if constexpr (B_KC)
-        bfr[set][j] = frag_kc(sb, wn * WN + j * 32 + (lane & 31), kk, lane);
-      else if constexpr (DUAL)  // pairs (h1, h3) of 32 columns: W1 panel, W3 panel
-        bfr[set][j] = frag_mnc<PWB>(sb, (j & 1) * 128 + wn * (WN / 2) + (j >> 1) * 32, kk, lane);
-      else
-        bfr[set][j] = frag_mnc<PWB>(sb, wn * WN + j * 32, kk, lane);
-    }
-  };
-  // LDS read instructions per fragment set (ds_read_b128 for a K-contiguous
-  // fragment, two ds_read_b64_tr_b16 for an M/N-contiguous one)
-  constexpr int NRD = FM * (A_KC ? 1 : 2) + FN * (B_KC ? 1 : 2);
-  constexpr int NMF = FM * FN;
-  auto mfma_rows = [&](int set, int i0, int i1) {
-#pragma unroll
-    for (int i = i0; i < i1; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[set][j], af[set][i], acc[i][j], 0, 0, 0);
-  };
-  auto mfmas = [&](int set) { mfma_rows(set, 0, FM); };
-  // interleave the MFMAs of one set with the LDS reads of the other
-  auto interleave = [&]() {
-#pragma unroll
-    for (int q = 0; q < NRD; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
-      __builtin_amdgcn_sched_group_barrier(0x008, (NMF + NRD - 1) / NRD, 0);  // MFMAs
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);  // the rest of the MFMAs
-  };
-  // One half k-step: the LDS reads of the next set interleaved with the
-  // first half of this set's MFMAs, then one part of a k-tile's loads (if
-  // any) between the two halves of the MFMAs, so that the memory pipe takes
-  // the loads a few at a time while the matrix pipe stays busy. The
-  // scheduling barriers keep the inline-asm loads where they are.
-  auto half_step = [&](int set, auto&& reads, auto&& loads) {
-    reads();
-    mfma_rows(set, 0, FM / 2);
-#pragma unroll
-    for (int q = 0; q < NRD; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, (NMF / 2 + NRD - 1) / NRD, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, NMF / 2, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    loads();
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_rows(set, FM / 2, FM);
-  };
-
   // Ring of DSTAGES k-tiles: tile t lives in stage t % DSTAGES. Every wave
   // loads its share of each tile; a barrier after a wave's own loads of tile
   // t have landed (s_waitcnt vmcnt) makes the whole tile visible. Tile t's
@@ -844,49 +827,127 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
     else if (younger == 1) wait_vm_lgkm0<2 * BPW>();
     else wait_vm_lgkm0<0>();
   };
+  auto barrier = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
 
-  if (nk > 0) {
-    wait_tile(0, DSTAGES - 1);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    read_frags(0, 0, 0);
-  }
-  // All tiles but the last: the barrier sits between the two k steps, so
-  // each half pairs the MFMAs of one step with the reads of the next.
-  // The loads of tile kt + DSTAGES go out in two parts: the first in the
-  // second half of iteration kt (its stage was freed by that iteration's
-  // barrier), the second in the first half of iteration kt + 1, both before
-  // the wait that needs them (iteration kt + DSTAGES - 1).
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    const int stage = kt % DSTAGES;
-    // step 1 of tile kt is read while step 0 runs; second part of tile kt + 3
-    half_step(
-        0, [&] { read_frags(stage, 1, 1); },
-        [&] {
-          const int tl = kt + DSTAGES - 1;
-          if (tl >= DSTAGES && tl < nk) issue_part(tl, tl % DSTAGES, 1);
-        });
-    // this wave's reads of tile kt are done (lgkmcnt 0) and its loads of
-    // tile kt + 1 have landed; after the barrier every wave's have
-    wait_tile(kt + 1, DSTAGES - 2);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    // step 0 of tile kt + 1 is read while step 1 of tile kt runs; first part
-    // of tile kt + 4 into the stage tile kt leaves
-    half_step(
-        1, [&] { read_frags((kt + 1) % DSTAGES, 0, 0); },
-        [&] {
-          if (kt + DSTAGES < nk) issue_part(kt + DSTAGES, stage, 0);
-        });
-  }
-  if (nk > 0) {
-    read_frags((nk - 1) % DSTAGES, 1, 1);
-    mfmas(0);
-    interleave();
-    mfmas(1);
-  }
+  // The k loop for a wave whose first FML 32-row fragments hold live rows
+  // (FML = FM for every wave of a tile with 256 live rows; the short last
+  // tile of an expert skips the MFMAs and A reads of rows past its count).
+  auto k_loop = [&](auto fml_c) {
+    constexpr int FML = decltype(fml_c)::value;
+    // Fragments of one 16-deep k step; two sets so that the LDS reads of the
+    // next step are in flight while the MFMAs of the current one run.
+    bf16x8 af[2][FM], bfr[2][FN];
+    auto read_frags = [&](int stage, int kk, int set) {
+      if constexpr (FML > 0) {
+        const char* sa = smem + stage * DSTAGE_BYTES;
+        const char* sb = sa + DSTAGE_BYTES / 2;
+#pragma unroll
+        for (int i = 0; i < FML; ++i) {
+          if constexpr (A_KC)
+            af[set][i] = frag_kc(sa, wm * WM + i * 32 + (lane & 31), kk, lane);
+          else
+            af[set][i] = frag_mnc<256>(sa, wm * WM + i * 32, kk, lane);
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          if constexpr (B_KC)
+            bfr[set][j] = frag_kc(sb, wn * WN + j * 32 + (lane & 31), kk, lane);
+          else if constexpr (DUAL)  // pairs (h1, h3) of 32 columns: W1 panel, W3 panel
+            bfr[set][j] = frag_mnc<PWB>(sb, (j & 1) * 128 + wn * (WN / 2) + (j >> 1) * 32, kk, lane);
+          else
+            bfr[set][j] = frag_mnc<PWB>(sb, wn * WN + j * 32, kk, lane);
+        }
+      }
+    };
+    // LDS read instructions per fragment set (ds_read_b128 for a K-contiguous
+    // fragment, two ds_read_b64_tr_b16 for an M/N-contiguous one)
+    constexpr int NRD = FML == 0 ? 0 : FML * (A_KC ? 1 : 2) + FN * (B_KC ? 1 : 2);
+    constexpr int NMF = FML * FN;
+    auto mfma_rows = [&](int set, int i0, int i1) {
+#pragma unroll
+      for (int i = i0; i < i1; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[set][j], af[set][i], acc[i][j], 0, 0, 0);
+    };
+    // One half k-step: the LDS reads of the next set interleaved with the
+    // first half of this set's MFMAs, then one part of a k-tile's loads (if
+    // any) between the two halves of the MFMAs, so that the memory pipe takes
+    // the loads a few at a time while the matrix pipe stays busy. The
+    // scheduling barriers keep the inline-asm loads where they are.
+    auto half_step = [&](int set, auto&& reads, auto&& loads) {
+      reads();
+      mfma_rows(set, 0, FML / 2);
+      if constexpr (NRD > 0) {
+#pragma unroll
+        for (int q = 0; q < NRD; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, (NMF / 2 + NRD - 1) / NRD, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NMF / 2, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      loads();
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_rows(set, FML / 2, FML);
+    };
+
+    if (nk > 0) {
+      wait_tile(0, DSTAGES - 1);
+      barrier();
+      read_frags(0, 0, 0);
+    }
+    // All tiles but the last: the barrier sits between the two k steps, so
+    // each half pairs the MFMAs of one step with the reads of the next.
+    // The loads of tile kt + DSTAGES go out in two parts: the first in the
+    // second half of iteration kt (its stage was freed by that iteration's
+    // barrier), the second in the first half of iteration kt + 1, both before
+    // the wait that needs them (iteration kt + DSTAGES - 1).
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+      const int stage = kt % DSTAGES;
+      // step 1 of tile kt is read while step 0 runs; second part of tile kt + 3
+      half_step(
+          0, [&] { read_frags(stage, 1, 1); },
+          [&] {
+            const int tl = kt + DSTAGES - 1;
+            if (tl >= DSTAGES && tl < nk) issue_part(tl, tl % DSTAGES, 1);
+          });
+      // this wave's reads of tile kt are done (lgkmcnt 0) and its loads of
+      // tile kt + 1 have landed; after the barrier every wave's have
+      wait_tile(kt + 1, DSTAGES - 2);
+      barrier();
+      // step 0 of tile kt + 1 is read while step 1 of tile kt runs; first part
+      // of tile kt + 4 into the stage tile kt leaves
+      half_step(
+          1, [&] { read_frags((kt + 1) % DSTAGES, 0, 0); },
+          [&] {
+            if (kt + DSTAGES < nk) issue_part(kt + DSTAGES, stage, 0);
+          });
+    }
+    if (nk > 0) {
+      read_frags((nk - 1) % DSTAGES, 1, 1);
+      mfma_rows(0, 0, FML);
+      if constexpr (NRD > 0) {
+#pragma unroll
+        for (int q = 0; q < NRD; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
+          __builtin_amdgcn_sched_group_barrier(0x008, (NMF + NRD - 1) / NRD, 0);  // MFMAs
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);  // the rest of the MFMAs
+      }
+      mfma_rows(1, 0, FML);
+    }
+  };
+  // live 32-row fragments of this wave (wave-uniform)
+  const int live = (MODE == MODE_ROWS) ? min(BM, max(0, cnt_e - mt * BM)) : BM;
+  const int fml = __builtin_amdgcn_readfirstlane(min(FM, max(0, (live - wm * WM + 31) / 32)));
+  if (fml > FM / 2) k_loop(IntC<FM>{});
+  else if (fml > 0) k_loop(IntC<FM / 2>{});
+  else k_loop(IntC<0>{});
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();  // all LDS reads done before the epilogue reuses the stages
@@ -1084,7 +1145,7 @@ hipError_t run_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
     const int ncols = (EPI == EPI_SWIGLU_FWD) ? 128 : 256;
     p.mt_bound = rows_tiles_bound(s, 256);
     p.ntiles = (p.N + ncols - 1) / ncols;
-    blocks = (long)p.mt_bound * p.ntiles;
+    blocks = (s.rows == 0 || p.N == 0) ? 0 : row_mode_blocks((long)p.mt_bound * p.ntiles);
   } else {
     blocks = (long)s.E * ((p.Mdim + 255) / 256) * ((p.N + 255) / 256);
   }
