@@ -243,6 +243,20 @@ flowmoe_status_t flowmoe_trace_start(hipEvent_t* events, int32_t* kinds, int32_t
 /* Stop tracing; returns the number of pairs recorded since the start. */
 int32_t flowmoe_trace_stop(void);
 
+/* ---- grouped-GEMM tile shape ------------------------------------------------ */
+
+/* Output tile shapes of the bf16 grouped GEMM (expert FFN forward and
+ * backward). AUTO, the default: 256 x 256 tiles (one block per compute unit)
+ * unless a launch would have at most 1.25 x 256 of them, then 256 x 128
+ * tiles (up to two blocks per compute unit). WIDE and NARROW force one
+ * shape (the SwiGLU forward always takes 256 x 256). Both shapes accumulate
+ * every output in the same k order: results are bit-identical. */
+enum { FLOWMOE_TILES_AUTO = 0, FLOWMOE_TILES_WIDE = 1, FLOWMOE_TILES_NARROW = 2 };
+
+/* Set the tile shape for launches enqueued after the call, process-wide
+ * (for tests and tuning). FLOWMOE_ERR_INVALID for another value. */
+flowmoe_status_t flowmoe_set_gemm_tiles(int32_t tiles);
+
 /* ---- the R-chunk two-stream layer (Sec. 3.2, Eqs. 3-6) -------------------- */
 
 /* Buffers of a whole layer over R chunks of shape->T tokens each. Per-token

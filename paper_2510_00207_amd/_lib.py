@@ -83,6 +83,7 @@ def load():
         "flowmoe_gate_topk_bwd": ([SP, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
         "flowmoe_trace_start": ([P, P, I32, ctypes.c_uint32], I32),
         "flowmoe_trace_stop": ([], I32),
+        "flowmoe_set_gemm_tiles": ([I32], I32),
         "flowmoe_layer_fwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
         "flowmoe_layer_bwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
     }
@@ -225,6 +226,15 @@ def flowmoe_trace_start(events, kinds, pairs: int, mask: int):
 
 def flowmoe_trace_stop() -> int:
     return load().flowmoe_trace_stop()
+
+
+TILES = {"auto": 0, "wide": 1, "narrow": 2}
+
+
+def flowmoe_set_gemm_tiles(tiles: str | int) -> None:
+    """Grouped-GEMM tile shape for later launches: "auto", "wide" (256 x 256)
+    or "narrow" (256 x 128), or the FLOWMOE_TILES_* value."""
+    _check(load().flowmoe_set_gemm_tiles(TILES[tiles] if isinstance(tiles, str) else tiles))
 
 
 # ---- R-chunk layer ---------------------------------------------------------------

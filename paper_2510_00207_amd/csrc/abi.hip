@@ -177,6 +177,13 @@ int32_t flowmoe_trace_stop(void) {
   return n;
 }
 
+flowmoe_status_t flowmoe_set_gemm_tiles(int32_t tiles) {
+  if (tiles != FLOWMOE_TILES_AUTO && tiles != FLOWMOE_TILES_WIDE && tiles != FLOWMOE_TILES_NARROW)
+    return fail(FLOWMOE_ERR_INVALID, "tiles = %d is not a FLOWMOE_TILES_* value", tiles);
+  set_gemm_tiles(tiles);
+  return ok();
+}
+
 const char* flowmoe_version(void) { return "flowmoe 0.1.0 gfx950"; }
 
 const char* flowmoe_last_error(void) { return g_err; }

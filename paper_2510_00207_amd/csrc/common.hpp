@@ -136,6 +136,7 @@ hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, co
                            const float* w, const float* dw, float* d_logits, float* dw_gate,
                            float* dbias, void* dx, int accumulate, void* ws, hipStream_t st);
 size_t ffn_bwd_ws_bytes(const Shape& s);
+void set_gemm_tiles(int tiles);  // FLOWMOE_TILES_*, validated by the caller
 hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* counts,
                              const int32_t* offsets, const void* w1, const void* w3,
                              const void* w2, void* h_save, void* a_save, void* y_disp,

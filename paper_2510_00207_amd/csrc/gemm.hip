@@ -19,6 +19,8 @@
 // same modes and epilogues.
 #include <math.h>
 
+#include <atomic>
+
 #include "common.hpp"
 
 namespace flowmoe {
@@ -183,32 +185,28 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return x * q + (x < rem ? x : rem) + i;
 }
 
-// Epilogue shared by the bf16 kernels: the block's accumulators (each wave
-// WM x WN, acc[i][j][4*g + q] = C[row wm*WM + i*32 + lane%32]
+// Epilogue shared by the bf16 kernels: the accumulators of wave (wm, wn)
+// of the tile (each WM x WN, acc[i][j][4*g + q] = C[row wm*WM + i*32 + lane%32]
 // [col wn*WN + j*32 + 8*g + 4*(lane/32) + q]) to global memory, staged
-// through LDS (smem must be free; at least (NT/64)*64*WN floats).
-template <int MODE, int EPI, int BM, int BN, int NT>
-__device__ __forceinline__ void gemm_epilogue(const GemmParams& p,
-                                              floatx16 (&acc)[BM / 64][BN / (NT / 128) / 32],
+// through LDS (smem: SMEM free bytes, at least (NT/64)*64*WN floats).
+template <int MODE, int EPI, int BM, int BN, int NT, int SMEM, int WM, int WN>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&acc)[WM / 32][WN / 32],
                                               char* smem, int e, int mt, int n0, int row0,
-                                              int rows_e, int cnt_e) {
-  constexpr int WGN = NT / 128;
-  constexpr int WM = BM / 2, WN = BN / WGN;
+                                              int rows_e, int cnt_e, int wm, int wn) {
   constexpr int FM = WM / 32, FN = WN / 32;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
   // acc[i][j][4*g + q] is C[row wm*WM + i*32 + lane%32]
   //                        [col wn*WN + j*32 + 8*g + 4*(lane/32) + q], q = 0..3
   const int lrow = lane & 31, lcol = 4 * (lane >> 5);
   {
-    // The wave's 128 x WN tile goes out 64 rows at a time through its own LDS
+    // The wave's WM x WN tile goes out 64 rows at a time through its own LDS
     // region (fp32, 16-byte chunks XOR-swizzled by row), then each lane
     // writes 8 consecutive outputs of one row: full 128-byte lines (bf16
     // rows of the dispatched buffers, or fp32 rows of the weight gradients).
     // The main loop ended with a barrier, so the tile buffers are free.
     static_assert(FM % 2 == 0, "staged epilogue works on 64-row halves");
     constexpr int SCH = WN / 4;  // 16-byte chunks per staged row
-    static_assert((NT / 64) * 64 * WN * 4 <= 2 * (BM + BN) * 128, "stage does not fit");
+    static_assert((NT / 64) * 64 * WN * 4 <= SMEM, "stage does not fit");
     float* stage = reinterpret_cast<float*>(smem) + wave * 64 * WN;
     bf16_t* C0 = static_cast<bf16_t*>(p.C0);
     bf16_t* C1 = static_cast<bf16_t*>(p.C1);
@@ -494,7 +492,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
     __syncthreads();
   }
 
-  gemm_epilogue<MODE, EPI, BM, BN, NT>(p, acc, smem, e, mt, n0, row0, rows_e, cnt_e);
+  gemm_epilogue<MODE, EPI, BM, BN, NT, (int)sizeof(smem), WM, WN>(p, acc, smem, e, mt, n0, row0, rows_e,
+                                                                   cnt_e, wm, wn);
 }
 
 // ---------------------------------------------------------------------------
@@ -516,7 +515,6 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
 //     columns c0 + 4 (s % 4) receive the K-contiguous 4-vectors the MFMA wants.
 // Requires the reduction length of the row mode to be a multiple of 32.
 constexpr int DBK = 32;
-constexpr int DSTAGES = 4;
 constexpr int kRowGroup = 4;  // row tiles per group of the row-mode tile order
 
 template <int V>
@@ -585,7 +583,6 @@ __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, 
 // grid of the streaming kernel in row mode: ceil(tiles / 8) + 1 blocks per
 // XCD cover any split of the tile bound into the two classes
 __host__ __device__ constexpr long row_mode_blocks(long tile_bound) { return 8 * ((tile_bound + 7) / 8 + 1); }
-constexpr int DSTAGE_BYTES = 32768;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
@@ -663,17 +660,26 @@ __device__ __forceinline__ bf16x8 frag_mnc(const char* region, int cb, int kk, i
   return __builtin_bit_cast(bf16x8, v);
 }
 
-template <int MODE, bool A_KC, bool B_KC, int EPI, int WGN>
-__global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
-  // WGN waves along N, two along M: WGN = 4 -> 8 waves of 128 x 64;
-  // WGN = 2 -> 4 waves of 128 x 128 (half the LDS fragment traffic per MFMA)
-  constexpr int BM = 256, BN = 256, NT = 128 * WGN;
-  constexpr int NW = NT / 64;         // waves
-  constexpr int BPW = 16 / NW;        // 1 KB LDS blocks per operand per wave per stage
-  constexpr int WM = 128, WN = BN / WGN, FM = 4, FN = WN / 32;
+template <int MODE, bool A_KC, bool B_KC, int EPI, bool NARROW>
+__global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmParams p) {
+  // Waves of 128 x 64 accumulators, two along M:
+  //   wide:   256 x 256 tiles, 8 waves, 4 stages of the k-tile ring (128 KB
+  //           of LDS, one block per CU);
+  //   narrow: 256 x 128 tiles, 4 waves, 3 stages (72 KB, up to two blocks per
+  //           CU), for launches whose wide tiles would leave CUs idle.
+  constexpr int BM = 256, BN = NARROW ? 128 : 256, NT = NARROW ? 256 : 512;
+  constexpr int WGM = 2, WGN = NARROW ? 2 : 4;
+  constexpr int NW = NT / 64;          // waves
+  constexpr int NST = NARROW ? 3 : 4;  // stages of the k-tile ring
+  constexpr int A_BYTES = BM * DBK * 2, STB = A_BYTES + BN * DBK * 2;  // bytes per stage
+  constexpr int BPA = (BM / 16) / NW, BPB = (BN / 16) / NW;  // 1 KB blocks per wave per stage
+  constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
   constexpr bool DUAL = EPI == EPI_SWIGLU_FWD;
-  constexpr int PWB = DUAL ? 128 : 256;  // B panel width (M/N-contiguous B)
-  __shared__ __attribute__((aligned(1024))) char smem[DSTAGES * DSTAGE_BYTES];
+  static_assert(!DUAL || !NARROW, "the dual forward pairs 128-column W1 and W3 panels");
+  constexpr int PWB = DUAL ? 128 : BN;  // B panel width (M/N-contiguous B)
+  // the k-tile ring, reused by the epilogue's staging (64 fp32 rows per wave)
+  constexpr int SMEM = NST * STB > NW * 64 * WN * 4 ? NST * STB : NW * 64 * WN * 4;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
@@ -704,15 +710,22 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
   const bf16_t* B1 = static_cast<const bf16_t*>(p.B1);
 
   // ---- buffer resources and per-lane source offsets (bytes, k0 = 0) ----
-  // Each wave issues BPW A and BPW B block loads per stage: blocks wave + NW*i.
+  // Each wave issues BPA A and BPB B block loads per stage: blocks wave + NW*i.
+  // An M/N-contiguous panel of PW columns holds 64 / (PW / 8) k-rows per
+  // block, 16-byte chunks XOR-swizzled by k-row.
+  auto mnc_off = [&](int b, int pw, long ld) {
+    const int cpr = pw / 8, kr = (64 / cpr) * b + lane / cpr;
+    const int cm = (lane % cpr) ^ ((kr & 3) << 2);
+    return (unsigned)(((long)kr * ld + cm * 8) * 2);
+  };
   u32x4 ra, rb0, rb1;
-  unsigned aoff[BPW], boff[BPW];
+  unsigned aoff[BPA], boff[BPB];
   int a_kstep, b_kstep;  // byte step per k-tile
   if constexpr (A_KC) {  // rows of the expert: [rows][K]
     const long valid = (long)(cnt_e - mt * BM) * p.lda;
     ra = make_rsrc(A + (long)row0 * p.lda, valid * 2);
 #pragma unroll
-    for (int i = 0; i < BPW; ++i) {
+    for (int i = 0; i < BPA; ++i) {
       const int b = wave + NW * i, row = 16 * b + (lane >> 2);
       const int c = (lane & 3) ^ ((row >> 2) & 3);
       aoff[i] = (unsigned)(((long)row * p.lda + c * 8) * 2);
@@ -722,11 +735,7 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
     const int m0 = mt * BM;
     ra = make_rsrc(A + (long)row0 * p.lda + m0, ((long)cnt_e * p.lda - m0) * 2);
 #pragma unroll
-    for (int i = 0; i < BPW; ++i) {
-      const int b = wave + NW * i, kr = 2 * b + (lane >> 5);
-      const int cm = (lane & 31) ^ ((kr & 3) << 2);
-      aoff[i] = (unsigned)(((long)kr * p.lda + cm * 8) * 2);
-    }
+    for (int i = 0; i < BPA; ++i) aoff[i] = mnc_off(wave + NW * i, 256, p.lda);
     a_kstep = DBK * p.lda * 2;
   }
   if constexpr (B_KC) {  // rows n: [N][K] per expert; k >= ksplit from B1
@@ -734,7 +743,7 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
     rb0 = make_rsrc(B0 + (long)e * p.b_estride + (long)n0 * p.ldb, valid * 2);
     rb1 = (B1 != nullptr) ? make_rsrc(B1 + (long)e * p.b_estride + (long)n0 * p.ldb, valid * 2) : rb0;
 #pragma unroll
-    for (int i = 0; i < BPW; ++i) {
+    for (int i = 0; i < BPB; ++i) {
       const int b = wave + NW * i, row = 16 * b + (lane >> 2);
       const int c = (lane & 3) ^ ((row >> 2) & 3);
       boff[i] = (unsigned)(((long)row * p.ldb + c * 8) * 2);
@@ -746,44 +755,33 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
       rb0 = make_rsrc(B0 + (long)e * p.b_estride + n0, (span - n0) * 2);
       rb1 = make_rsrc(B1 + (long)e * p.b_estride + n0, (span - n0) * 2);
 #pragma unroll
-      for (int i = 0; i < BPW; ++i) {
-        const int b = wave + NW * i, kr = 4 * (b & 7) + (lane >> 4);
-        const int cm = (lane & 15) ^ ((kr & 3) << 2);
-        boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
-      }
+      for (int i = 0; i < BPB; ++i) boff[i] = mnc_off((wave + NW * i) & 7, 128, p.ldb);
     } else {
       rb0 = make_rsrc(B0 + (long)e * p.b_estride + n0, (span - n0) * 2);
       rb1 = rb0;
 #pragma unroll
-      for (int i = 0; i < BPW; ++i) {
-        const int b = wave + NW * i, kr = 2 * b + (lane >> 5);
-        const int cm = (lane & 31) ^ ((kr & 3) << 2);
-        boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
-      }
+      for (int i = 0; i < BPB; ++i) boff[i] = mnc_off(wave + NW * i, BN, p.ldb);
     }
     b_kstep = DBK * p.ldb * 2;
   } else {  // KSUM: element (r, n) at B + (row0 + r) * ldb + n
     rb0 = make_rsrc(B0 + (long)row0 * p.ldb + n0, ((long)cnt_e * p.ldb - n0) * 2);
     rb1 = rb0;
 #pragma unroll
-    for (int i = 0; i < BPW; ++i) {
-      const int b = wave + NW * i, kr = 2 * b + (lane >> 5);
-      const int cm = (lane & 31) ^ ((kr & 3) << 2);
-      boff[i] = (unsigned)(((long)kr * p.ldb + cm * 8) * 2);
-    }
+    for (int i = 0; i < BPB; ++i) boff[i] = mnc_off(wave + NW * i, BN, p.ldb);
     b_kstep = DBK * p.ldb * 2;
   }
 
-  // Loads of k-tile kt into stage `stage`, in two parts: part q takes this
-  // wave's blocks i in [q * BPW / 2, (q + 1) * BPW / 2) of both operands.
+  // Loads of k-tile kt into stage `stage`, in two parts: part 0 takes this
+  // wave's first ceil(n / 2) of its n blocks of each operand, part 1 the rest.
   auto issue_part = [&](int kt, int stage, int q) {
-    char* sa = smem + stage * DSTAGE_BYTES;
-    char* sb = sa + DSTAGE_BYTES / 2;
+    char* sa = smem + stage * STB;
+    char* sb = sa + A_BYTES;
     const unsigned ka = (unsigned)kt * (unsigned)a_kstep;
-    constexpr int H = BPW / 2;
+    constexpr int HA = (BPA + 1) / 2, HB = (BPB + 1) / 2;
 #pragma unroll
-    for (int i = q * H; i < (q + 1) * H; ++i) {
-      dma16(ra, sa + (wave + NW * i) * 1024, aoff[i] + ka);
+    for (int i = q ? HA : 0; i < (q ? BPA : HA); ++i) dma16(ra, sa + (wave + NW * i) * 1024, aoff[i] + ka);
+#pragma unroll
+    for (int i = q ? HB : 0; i < (q ? BPB : HB); ++i) {
       if constexpr (B_KC) {
         const int k0 = kt * DBK;
         const bool second = k0 >= p.ksplit;
@@ -791,8 +789,8 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
         dma16(second ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
       } else {
         const unsigned kb = (unsigned)kt * (unsigned)b_kstep;
-        // blocks 8..15 (i >= BPW/2, as wave < NW) hold the W3 panel
-        dma16((DUAL && i >= BPW / 2) ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
+        // blocks 8..15 (i >= 1, as wave < NW = 8 in the wide tile) hold the W3 panel
+        dma16((DUAL && i >= 1) ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
       }
     }
   };
@@ -809,22 +807,23 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Ring of DSTAGES k-tiles: tile t lives in stage t % DSTAGES. Every wave
-  // loads its share of each tile; a barrier after a wave's own loads of tile
-  // t have landed (s_waitcnt vmcnt) makes the whole tile visible. Tile t's
-  // stage is refilled (tile t + DSTAGES) only after the barrier that follows
-  // every wave's last LDS read of tile t.
+  // Ring of NST k-tiles: tile t lives in stage t % NST. Every wave loads its
+  // share of each tile; a barrier after a wave's own loads of tile t have
+  // landed (s_waitcnt vmcnt) makes the whole tile visible. Tile t's stage is
+  // refilled (tile t + NST) only after the barrier that follows every wave's
+  // last LDS read of tile t.
 #pragma unroll
-  for (int s = 0; s < DSTAGES; ++s)
+  for (int s = 0; s < NST; ++s)
     if (s < nk) issue(s, s);
 
   // wait until this wave's loads of tile t have landed, given that the loads
   // of tiles up to min(t + ahead, nk - 1) have been issued
+  constexpr int LPT = BPA + BPB;  // loads per wave per k-tile
   auto wait_tile = [&](int t, int ahead) {
     const int younger = min(ahead, nk - 1 - t);  // tiles issued after t
-    if (younger >= 3) wait_vm_lgkm0<6 * BPW>();
-    else if (younger == 2) wait_vm_lgkm0<4 * BPW>();
-    else if (younger == 1) wait_vm_lgkm0<2 * BPW>();
+    if (younger >= 3) wait_vm_lgkm0<3 * LPT>();
+    else if (younger == 2) wait_vm_lgkm0<2 * LPT>();
+    else if (younger == 1) wait_vm_lgkm0<LPT>();
     else wait_vm_lgkm0<0>();
   };
   auto barrier = [] {
@@ -843,8 +842,8 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
     bf16x8 af[2][FM], bfr[2][FN];
     auto read_frags = [&](int stage, int kk, int set) {
       if constexpr (FML > 0) {
-        const char* sa = smem + stage * DSTAGE_BYTES;
-        const char* sb = sa + DSTAGE_BYTES / 2;
+        const char* sa = smem + stage * STB;
+        const char* sb = sa + A_BYTES;
 #pragma unroll
         for (int i = 0; i < FML; ++i) {
           if constexpr (A_KC)
@@ -897,39 +896,39 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
     };
 
     if (nk > 0) {
-      wait_tile(0, DSTAGES - 1);
+      wait_tile(0, NST - 1);
       barrier();
       read_frags(0, 0, 0);
     }
     // All tiles but the last: the barrier sits between the two k steps, so
     // each half pairs the MFMAs of one step with the reads of the next.
-    // The loads of tile kt + DSTAGES go out in two parts: the first in the
+    // The loads of tile kt + NST go out in two parts: the first in the
     // second half of iteration kt (its stage was freed by that iteration's
     // barrier), the second in the first half of iteration kt + 1, both before
-    // the wait that needs them (iteration kt + DSTAGES - 1).
+    // the wait that needs them (iteration kt + NST - 1).
     for (int kt = 0; kt + 1 < nk; ++kt) {
-      const int stage = kt % DSTAGES;
-      // step 1 of tile kt is read while step 0 runs; second part of tile kt + 3
+      const int stage = kt % NST;
+      // step 1 of tile kt is read while step 0 runs; second part of tile kt + NST - 1
       half_step(
           0, [&] { read_frags(stage, 1, 1); },
           [&] {
-            const int tl = kt + DSTAGES - 1;
-            if (tl >= DSTAGES && tl < nk) issue_part(tl, tl % DSTAGES, 1);
+            const int tl = kt + NST - 1;
+            if (tl >= NST && tl < nk) issue_part(tl, tl % NST, 1);
           });
       // this wave's reads of tile kt are done (lgkmcnt 0) and its loads of
       // tile kt + 1 have landed; after the barrier every wave's have
-      wait_tile(kt + 1, DSTAGES - 2);
+      wait_tile(kt + 1, NST - 2);
       barrier();
       // step 0 of tile kt + 1 is read while step 1 of tile kt runs; first part
-      // of tile kt + 4 into the stage tile kt leaves
+      // of tile kt + NST into the stage tile kt leaves
       half_step(
-          1, [&] { read_frags((kt + 1) % DSTAGES, 0, 0); },
+          1, [&] { read_frags((kt + 1) % NST, 0, 0); },
           [&] {
-            if (kt + DSTAGES < nk) issue_part(kt + DSTAGES, stage, 0);
+            if (kt + NST < nk) issue_part(kt + NST, stage, 0);
           });
     }
     if (nk > 0) {
-      read_frags((nk - 1) % DSTAGES, 1, 1);
+      read_frags((nk - 1) % NST, 1, 1);
       mfma_rows(0, 0, FML);
       if constexpr (NRD > 0) {
 #pragma unroll
@@ -951,7 +950,8 @@ __global__ __launch_bounds__(128 * WGN) void gemm_dma_kernel(GemmParams p) {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();  // all LDS reads done before the epilogue reuses the stages
-  gemm_epilogue<MODE, EPI, BM, BN, NT>(p, acc, smem, e, mt, n0, row0, rows_e, cnt_e);
+  gemm_epilogue<MODE, EPI, BM, BN, NT, SMEM, WM, WN>(p, acc, smem, e, mt, n0, row0, rows_e, cnt_e, wm,
+                                                     wn);
 }
 
 // ---------------------------------------------------------------------------
@@ -1131,29 +1131,44 @@ hipError_t run_bf16(int kind, const Shape& s, GemmParams p, hipStream_t st) {
   });
 }
 
-// wave layout of the streaming kernel (waves along N): 8 waves of 128 x 64.
-// Measured on the balanced layer, 4 waves of 128 x 128 (one per SIMD) were
-// 10-20% slower: with a single wave per SIMD nothing hides its barrier waits.
-constexpr int kDmaWgnRows = 4;
-constexpr int kDmaWgnKsum = 4;
+// Tile shape of the streaming kernel: 256 x 256 unless those tiles would
+// cover the launch in at most 1.25 rounds of the CUs, then 256 x 128.
+constexpr int kCUs = 256;
+std::atomic<int> g_tiles{FLOWMOE_TILES_AUTO};
 
-template <int MODE, bool A_KC, bool B_KC, int EPI>
-hipError_t run_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
-  constexpr int WGN = (MODE == MODE_ROWS) ? kDmaWgnRows : kDmaWgnKsum;
+template <int MODE, bool A_KC, bool B_KC, int EPI, bool NARROW>
+hipError_t launch_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
+  constexpr int BN = NARROW ? 128 : 256;
   long blocks;
   if (MODE == MODE_ROWS) {
-    const int ncols = (EPI == EPI_SWIGLU_FWD) ? 128 : 256;
+    const int ncols = (EPI == EPI_SWIGLU_FWD) ? 128 : BN;
     p.mt_bound = rows_tiles_bound(s, 256);
     p.ntiles = (p.N + ncols - 1) / ncols;
     blocks = (s.rows == 0 || p.N == 0) ? 0 : row_mode_blocks((long)p.mt_bound * p.ntiles);
   } else {
-    blocks = (long)s.E * ((p.Mdim + 255) / 256) * ((p.N + 255) / 256);
+    blocks = (long)s.E * ((p.Mdim + 255) / 256) * ((p.N + BN - 1) / BN);
   }
   if (blocks == 0) return hipSuccess;
   return traced(kind, st, [&] {
-    hipLaunchKernelGGL((gemm_dma_kernel<MODE, A_KC, B_KC, EPI, WGN>), dim3((unsigned)blocks),
-                       dim3(128 * WGN), 0, st, p);
+    hipLaunchKernelGGL((gemm_dma_kernel<MODE, A_KC, B_KC, EPI, NARROW>), dim3((unsigned)blocks),
+                       dim3(NARROW ? 256 : 512), 0, st, p);
   });
+}
+
+template <int MODE, bool A_KC, bool B_KC, int EPI>
+hipError_t run_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
+  if constexpr (EPI == EPI_SWIGLU_FWD) {
+    return launch_dma<MODE, A_KC, B_KC, EPI, false>(kind, s, p, st);
+  } else {
+    // wide tiles the launch would have (row mode: the live rows' tiles)
+    const long rt = (MODE == MODE_ROWS) ? (s.rows + 255) / 256 : (long)s.E * ((p.Mdim + 255) / 256);
+    const long wide = rt * ((p.N + 255) / 256);
+    const int tiles = g_tiles.load(std::memory_order_relaxed);
+    const bool narrow = tiles == FLOWMOE_TILES_NARROW ||
+                        (tiles == FLOWMOE_TILES_AUTO && wide <= kCUs + kCUs / 4);
+    if (narrow) return launch_dma<MODE, A_KC, B_KC, EPI, true>(kind, s, p, st);
+    return launch_dma<MODE, A_KC, B_KC, EPI, false>(kind, s, p, st);
+  }
 }
 
 // The streaming kernel needs the row-mode reduction length (and a K split)
@@ -1190,6 +1205,8 @@ hipError_t run_f32(int kind, const Shape& s, GemmParams p, hipStream_t st) {
   } while (0)
 
 }  // namespace
+
+void set_gemm_tiles(int tiles) { g_tiles.store(tiles, std::memory_order_relaxed); }
 
 size_t ffn_bwd_ws_bytes(const Shape& s) {
   const int hw = (s.act == FLOWMOE_SWIGLU) ? 2 * s.H : s.H;

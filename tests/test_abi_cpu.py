@@ -150,3 +150,12 @@ def test_misaligned_tensors_rejected(flowmoe_lib):
         L.flowmoe_gate_topk_bwd(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE + 4, 0, FAKE,
                                 need, stream=0)
     assert ei.value.status == L.ERR_INVALID and "dx" in str(ei.value)
+
+
+def test_gemm_tiles_setting(flowmoe_lib):
+    for t in ("wide", "narrow", "auto"):
+        L.flowmoe_set_gemm_tiles(t)
+    raw = ctypes.CDLL(L.LIB_PATH)
+    raw.flowmoe_set_gemm_tiles.argtypes = [ctypes.c_int32]
+    assert raw.flowmoe_set_gemm_tiles(3) == L.ERR_INVALID
+    assert raw.flowmoe_set_gemm_tiles(-1) == L.ERR_INVALID

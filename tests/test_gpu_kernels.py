@@ -135,17 +135,28 @@ def test_dispatch(T, E, k, cf, layout):
         assert np.array_equal(host(g["x_disp"][:live]), xd[:live]), C
 
 
-@pytest.mark.parametrize("MH", [(200, 264), (224, 288)], ids=["staged", "streaming"])
+@pytest.fixture
+def gemm_tiles():
+    """Set the grouped-GEMM tile shape for one test; back to "auto" after it."""
+    yield L.flowmoe_set_gemm_tiles
+    L.flowmoe_set_gemm_tiles("auto")
+
+
+@pytest.mark.parametrize("MHT", [(200, 264, "auto"), (224, 288, "wide"), (224, 288, "narrow")],
+                         ids=["staged", "streaming-wide", "streaming-narrow"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
-def test_expert_ffn_fwd_bwd(dtype, act, layout, MH):
+def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, gemm_tiles):
     """(200, 264): reductions not multiples of 32 (register-staged bf16 GEMM);
-    (224, 288): multiples of 32 (LDS-streaming bf16 GEMM); both ragged."""
+    (224, 288): multiples of 32 (LDS-streaming bf16 GEMM, 256 x 256 and
+    256 x 128 tiles); all ragged. The counts give row tiles of every class:
+    empty, a few rows, under and over half a tile, full."""
     need_gpu()
     rng = np.random.default_rng(3)
     E, k = 6, 1
-    M, H = MH
+    M, H, tiles = MHT
+    gemm_tiles(tiles)
     # per-expert counts spanning empty, tiny, tile-exact and ragged groups
     cnt = np.array([0, 1, 127, 128, 129, 300])
     C = 300
@@ -211,6 +222,69 @@ def test_expert_ffn_fwd_bwd(dtype, act, layout, MH):
                              dw1, dw3, dw2, 1, ws, nws)
     torch.cuda.synchronize()
     assert torch.equal(dw2, 2 * dw2b)
+
+
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+def test_gemm_tile_shapes_agree(act, layout, gemm_tiles):
+    """256 x 256 and 256 x 128 tiles over several row and column tiles with
+    ragged edges and light last row tiles: both match the oracle, and as
+    both accumulate every output in the same k order, their outputs are
+    bit-identical."""
+    need_gpu()
+    rng = np.random.default_rng(21)
+    E, M, H = 4, 512, 800
+    cnt = np.array([700, 513, 0, 260])
+    C = 720
+    T = int(cnt.sum())
+    idx = np.repeat(np.arange(E), cnt)[:, None]
+    rt = oracle.route(idx, E, C, layout)
+    rows = rt["rows"]
+    d = dev()
+    bf = torch.bfloat16
+    rnd = lambda *sh, sc=1.0: (torch.from_numpy(rng.standard_normal(sh) * sc).to(d).to(bf))
+    x_disp, dy = rnd(rows, M), rnd(rows, M)
+    live = torch.zeros(rows, dtype=torch.bool)
+    for e in range(E):
+        live[rt["offsets"][e]:rt["offsets"][e] + rt["counts"][e]] = True
+    dy[~live.to(d)] = 0  # upstream gradient only on the live rows
+    w1, w2 = rnd(E, M, H, sc=0.05), rnd(E, H, M, sc=0.05)
+    w3 = rnd(E, M, H, sc=0.05) if act == "swiglu" else None
+    counts = torch.from_numpy(rt["counts"].astype(np.int32)).to(d)
+    offsets = torch.from_numpy(rt["offsets"].astype(np.int32)).to(d)
+    s = _shape(T, M, H, E, 1, C, "bf16", act, layout)
+    HW = 2 * H if act == "swiglu" else H
+    nws = L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD)
+    out = {}
+    for tiles in ("wide", "narrow"):
+        gemm_tiles(tiles)
+        h = torch.full((rows, HW), 5.0, dtype=bf, device=d)
+        a = torch.full((rows, H), 5.0, dtype=bf, device=d)
+        y = torch.full((rows, M), 5.0, dtype=bf, device=d)
+        L.flowmoe_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h, a, y)
+        dx = torch.full((rows, M), 5.0, dtype=bf, device=d)
+        dw1 = torch.full((E, M, H), 9.0, device=d)
+        dw3 = torch.full((E, M, H), 9.0, device=d) if act == "swiglu" else None
+        dw2 = torch.full((E, H, M), 9.0, device=d)
+        ws = torch.empty(nws, dtype=torch.uint8, device=d)
+        L.flowmoe_expert_ffn_bwd(s, dy, x_disp, h, a, counts, offsets, w1, w3, w2, dx, dw1, dw3, dw2,
+                                 0, ws, nws)
+        torch.cuda.synchronize()
+        out[tiles] = [t for t in (h, a, y, dx, dw1, dw3, dw2) if t is not None]
+        if tiles == "wide":
+            x64, dy64 = host(x_disp), host(dy)
+            w64 = [None if w is None else host(w) for w in (w1, w3, w2)]
+            ref = oracle.expert_ffn(x64, rt["counts"], rt["offsets"], *w64, act)
+            rdx, rdw1, rdw3, rdw2 = oracle.expert_ffn_bwd(dy64, x64, ref, rt["counts"], rt["offsets"],
+                                                          *w64, act)
+        nl = rows if layout == "padded" else int(rt["offsets"][-1])
+        assert_close(host(y)[:nl], ref["y_disp"][:nl], "bf16", f"{tiles} y")
+        assert_close(host(dx)[:nl], rdx[:nl], "bf16", f"{tiles} dx")
+        assert_close(host(dw1), rdw1, "bf16", f"{tiles} dw1")
+        assert_close(host(dw2), rdw2, "bf16", f"{tiles} dw2")
+    names = [n for n in ("h", "a", "y", "dx", "dw1", "dw3", "dw2") if n != "dw3" or act == "swiglu"]
+    for name, p, q in zip(names, out["wide"], out["narrow"]):
+        assert torch.equal(p, q), name
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
