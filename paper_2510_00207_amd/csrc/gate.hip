@@ -78,6 +78,47 @@ __device__ __forceinline__ void topk_write(float logit, int e, bool valid, int E
   }
 }
 
+// Top-k of one token's E logits by one thread: a sorted list of the kMaxK
+// best (value, index) so far, scanned in expert order. A later expert
+// displaces an entry only with a strictly larger value, so equal values keep
+// the lower index, and -0.0 == +0.0 (IEEE compare). Then the softmax over
+// the k selected, shifted by the largest.
+__device__ __forceinline__ void topk_scan(const float* logit, int E, int k, int32_t* idx_out,
+                                          float* w_out) {
+  float tv[kMaxK];
+  int ti[kMaxK];
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    tv[j] = -INFINITY;
+    ti[j] = 1 << 30;
+  }
+  for (int e = 0; e < E; ++e) {
+    const float v = logit[e];
+#pragma unroll
+    for (int j = kMaxK - 1; j >= 0; --j) {
+      const bool here = v > tv[j] || (v == tv[j] && e < ti[j]);
+      const bool above = j > 0 && (v > tv[j - 1] || (v == tv[j - 1] && e < ti[j - 1]));
+      if (here) {
+        tv[j] = above ? tv[j - 1 < 0 ? 0 : j - 1] : v;
+        ti[j] = above ? ti[j - 1 < 0 ? 0 : j - 1] : e;
+      }
+    }
+  }
+  float ex[kMaxK], denom = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    ex[j] = j < k ? expf(tv[j] - tv[0]) : 0.f;
+    denom += ex[j];
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    if (j < k) {
+      idx_out[j] = ti[j];
+      w_out[j] = ex[j] / denom;
+    }
+  }
+}
+
 // Fused gate: per block 4 waves; each wave has G = 64/EP segments, each
 // segment TPG tokens. x rows of the block are staged in LDS as float.
 template <typename TIn>
@@ -133,117 +174,186 @@ __global__ __launch_bounds__(kGateThreads) void gate_topk_kernel(
   }
 }
 
-// bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16). A block of 4 waves owns 16
-// tokens; the reduction over M is split between the waves (wave w takes the
-// 32-deep k steps s = w, w + 4, ...), so every wave has its x loads in flight
-// at once: the kernel reads x in about one memory round trip. x rows feed the
-// A operand straight from global memory (16 bytes of one row per lane). W_g
-// rows are copied into LDS in chunks of KC rows (as stored, [k][E], one
-// contiguous range) and each lane gathers its B fragment (8 consecutive k of
-// one expert) with 2-byte LDS reads. The four partial logit tiles are summed
-// in LDS in wave order (deterministic), the bias added, and each token's
-// top-k taken by a segment of EP lanes.
-constexpr int kGateTok = 16;            // tokens per block
+// bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16). A block of 4 waves owns TGB
+// groups of 16 tokens; the reduction over M is split between the waves (wave
+// w takes the 32-deep k steps s = w, w + 4, ...), so every wave has its x
+// loads in flight at once. x rows feed the A operand straight from global
+// memory (16 bytes of one row per lane). W_g rows are copied into LDS in
+// chunks of KC rows (rows zero past M) and each lane gathers its B fragment
+// (8 consecutive k of one expert) with 2-byte LDS reads, once per k step for
+// all the block's token groups: a chunk staged serves 16 * TGB tokens (W_g
+// is re-read once per block, so wide gates take more token groups per
+// block). The four partial logit tiles are summed in
+// LDS in wave order (deterministic), the bias added, and each token's top-k
+// taken by a segment of EP lanes (E <= 16) or by one thread (wider gates).
+constexpr int kGateTok = 16;            // tokens per group
 constexpr int kGateWgBytes = 32768;     // LDS for one chunk of W_g rows
-constexpr int kGateBatch = 8;           // x loads in flight per lane
+constexpr int kGateBatch = 8;           // x fragments in flight per lane
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
-// rows of W_g per LDS chunk: a multiple of 32 (whole k steps)
-__host__ __device__ inline int gate_chunk_rows(int E) {
-  int kc = kGateWgBytes / (2 * E);
-  return kc - kc % 32;
-}
 
-template <int NB>  // 16-expert column blocks (E <= 16 * NB)
+template <int NB, int TGB>  // 16-expert column blocks (E <= 16 * NB), token groups per block
 __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg, const float* __restrict__ bias,
     float* __restrict__ logits, int32_t* __restrict__ idx, float* __restrict__ w, int T, int M,
     int E, int k, int EP) {
-  __shared__ __attribute__((aligned(16))) bf16_t wgs[kGateWgBytes / 2];
-  __shared__ float part[4][kGateTok][NB * 16 + 1];
+  constexpr int TB = kGateTok * TGB;           // tokens per block
+  constexpr int PW = NB * 16 + 1;              // partial-tile row pitch (floats)
+  constexpr int PART_BYTES = 4 * TB * PW * 4;  // the four waves' partial tiles
+  constexpr int SMEM = PART_BYTES > 2 * kGateWgBytes ? PART_BYTES : 2 * kGateWgBytes;
+  constexpr int BS = kGateBatch / TGB;         // k steps per batch of x loads
+  static_assert(BS >= 1, "token groups per block");
+  // two W_g chunk buffers during the k loop, then the partial tiles
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  bf16_t* wgs = reinterpret_cast<bf16_t*>(smem);
+  float(*part)[TB][PW] = reinterpret_cast<float(*)[TB][PW]>(smem);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int t0 = blockIdx.x * kGateTok;
-  const int arow = t0 + (lane & 15);  // token whose A row this lane feeds
-  const int kq = (lane >> 4) * 8;     // k offset of this lane inside a step
-  const bool arow_ok = arow < T;
-  const bf16_t* xrow = x + (long)(arow_ok ? arow : 0) * M;
-  const int KC = gate_chunk_rows(E);
+  const int t0 = blockIdx.x * TB;
+  const int kq = (lane >> 4) * 8;  // k offset of this lane inside a step
+  const bf16_t* xrow[TGB];
+  bool arow_ok[TGB];
+#pragma unroll
+  for (int g = 0; g < TGB; ++g) {
+    const int arow = t0 + g * kGateTok + (lane & 15);  // token whose A row this lane feeds
+    arow_ok[g] = arow < T;
+    xrow[g] = x + (long)(arow_ok[g] ? arow : 0) * M;
+  }
+  // W_g rows in LDS with a pitch of 16 NB + 8 bf16: a B fragment's eight
+  // rows are immediate offsets from one address, and the lanes of the four
+  // k groups (rows 8 apart) fall on two bank sets instead of one
+  constexpr int PITCH = 16 * NB + 8;
+  constexpr int KC = (kGateWgBytes / (2 * PITCH)) / 32 * 32;  // rows per chunk
+  const int nchunks = (M + KC - 1) / KC;
 
-  floatx4_t acc[NB];
+  floatx4_t acc[TGB][NB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  for (int g = 0; g < TGB; ++g)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[g][nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = 0; k0 < M; k0 += KC) {
-    const int kc = min(KC, M - k0);
-    const int s_end = (k0 + kc + 31) / 32;  // k steps of this chunk: [k0/32, s_end)
-    int s = k0 / 32 + wave;
-    // this wave's first batch of x fragments, issued before the staging barrier
-    uint4 av[kGateBatch];
-    auto load_batch = [&](int s0) {
+  // W_g chunks alternate between two LDS buffers. The loads of chunk c + 1
+  // (its W_g rows into registers, this wave's first batch of x fragments)
+  // are issued as chunk c's multiplies start, so their latency overlaps
+  // them; the W_g rows go to the other buffer after the multiplies, and one
+  // barrier per chunk publishes them. Every load is issued, from a clamped
+  // in-bounds address, and values outside the range are zeroed afterwards:
+  // no branch around a load, so the buffers stay in registers.
+  constexpr int WGV = kGateWgBytes / 16 / 256;  // 16-byte W_g units per thread per chunk
+  constexpr int WGE = kGateWgBytes / 2;         // bf16 per chunk buffer
+  typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+  u32x4_t wtmp[WGV];
+  const bool vec = (E % 8) == 0;  // rows are whole 16-byte units
+  const int UR = E / 8;           // 16-byte units per row
+  auto load_wg = [&](int c) __attribute__((always_inline)) {
+    if (!vec) return;
+    const int k0 = c * KC, kc = min(KC, M - k0);
+    // rows [k0, k0 + kc) of W_g are one contiguous range of kc * E values
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(wg + (long)k0 * E);
+    const int n16 = kc * UR;
 #pragma unroll
-      for (int i = 0; i < kGateBatch; ++i) {
-        const int kk = (s0 + 4 * i) * 32 + kq;
-        av[i] = (arow_ok && s0 + 4 * i < s_end && kk < M)
-                    ? *reinterpret_cast<const uint4*>(xrow + kk)
-                    : make_uint4(0, 0, 0, 0);
-      }
-    };
-    load_batch(s);
-    __syncthreads();  // previous chunk's readers of wgs are done
-    {
-      // rows [k0, k0 + kc) of W_g are one contiguous range of kc * E values;
-      // kc and M are multiples of 8, so it is a whole number of 16-byte units
-      const uint4* src = reinterpret_cast<const uint4*>(wg + (long)k0 * E);
-      uint4* dst = reinterpret_cast<uint4*>(wgs);
-      const int n16 = kc * E / 8;  // <= 8 per thread (32 KB)
-      uint4 tmp[kGateWgBytes / 16 / 256];
-#pragma unroll
-      for (int i = 0; i < kGateWgBytes / 16 / 256; ++i)
-        if (tid + 256 * i < n16) tmp[i] = src[tid + 256 * i];
-#pragma unroll
-      for (int i = 0; i < kGateWgBytes / 16 / 256; ++i)
-        if (tid + 256 * i < n16) dst[tid + 256 * i] = tmp[i];
+    for (int i = 0; i < WGV; ++i) {
+      const int q = tid + 256 * i;
+      const u32x4_t v = src[q < n16 ? q : 0];
+      wtmp[i] = q < n16 ? v : u32x4_t{0u, 0u, 0u, 0u};  // rows past the chunk: zero
     }
-    __syncthreads();
-    for (; s < s_end; s += 4 * kGateBatch) {
+  };
+  auto store_wg = [&](int c, int buf) __attribute__((always_inline)) {
+    bf16_t* dst = wgs + buf * WGE;
+    if (vec) {
 #pragma unroll
-      for (int i = 0; i < kGateBatch; ++i) {
+      for (int i = 0; i < WGV; ++i) {
+        const int q = tid + 256 * i;
+        if (q < KC * UR) {
+          const int r = q / UR, cu = q - r * UR;
+          *reinterpret_cast<u32x4_t*>(dst + r * PITCH + cu * 8) = wtmp[i];
+        }
+      }
+    } else {  // element by element (E not a multiple of 8), rows past the chunk zero
+      const int k0 = c * KC, kc = min(KC, M - k0);
+      for (int q = tid; q < KC * E; q += 256) {
+        const int r = q / E, e = q - r * E;
+        dst[r * PITCH + e] = r < kc ? wg[(long)(k0 + r) * E + e] : (bf16_t)0;
+      }
+    }
+  };
+  uint4 av[BS][TGB], avn[BS][TGB];
+  auto load_x = [&](uint4(&dst)[BS][TGB], int s0, int s_end) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < BS; ++i) {
+      const int kk = (s0 + 4 * i) * 32 + kq;
+      const bool in = s0 + 4 * i < s_end && kk < M;
+#pragma unroll
+      for (int g = 0; g < TGB; ++g) {
+        const uint4 v = *reinterpret_cast<const uint4*>(xrow[g] + (in ? kk : 0));
+        dst[i][g] = (arow_ok[g] && in) ? v : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto chunk_end = [&](int c) { return (c * KC + min(KC, M - c * KC) + 31) / 32; };
+  load_wg(0);
+  load_x(av, wave, chunk_end(0));
+  store_wg(0, 0);
+  __syncthreads();
+  for (int c = 0; c < nchunks; ++c) {
+    const int k0 = c * KC;
+    const int s_end = chunk_end(c);  // k steps of this chunk: [k0/32, s_end)
+    const bf16_t* wb = wgs + (c & 1) * WGE;
+    {  // (the last chunk reloads itself: no branch around the loads)
+      const int cn = c + 1 < nchunks ? c + 1 : c;
+      load_wg(cn);
+      load_x(avn, cn * KC / 32 + wave, chunk_end(cn));
+    }
+    for (int s = k0 / 32 + wave; s < s_end; s += 4 * BS) {
+#pragma unroll
+      for (int i = 0; i < BS; ++i) {
         const int si = s + 4 * i;
         if (si < s_end) {
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, av[i]);
           const int r0 = si * 32 - k0 + kq;  // first W_g row of this lane's fragment
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
             const int e = nb * 16 + (lane & 15);
-            uint32_t u[4] = {0u, 0u, 0u, 0u};
-            if (e < E) {
+            const bf16_t* bp = wb + r0 * PITCH + e;
+            uint32_t u[4];
 #pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                const int ra = r0 + 2 * q, rb = ra + 1;
-                const uint32_t lo = (ra < kc) ? wgs[ra * E + e] : 0u;
-                const uint32_t hi = (rb < kc) ? wgs[rb * E + e] : 0u;
-                u[q] = lo | (hi << 16);
-              }
+            for (int q = 0; q < 4; ++q) {
+              const uint32_t lo = bp[(2 * q) * PITCH], hi = bp[(2 * q + 1) * PITCH];
+              u[q] = e < E ? lo | (hi << 16) : 0u;  // columns past E were never written
             }
             const bf16x8_t b = __builtin_bit_cast(bf16x8_t, make_uint4(u[0], u[1], u[2], u[3]));
-            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[nb], 0, 0, 0);
+#pragma unroll
+            for (int g = 0; g < TGB; ++g)
+              acc[g][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8_t, av[i][g]), b, acc[g][nb], 0, 0, 0);
           }
         }
       }
-      if (s + 4 * kGateBatch < s_end) load_batch(s + 4 * kGateBatch);
+      if (s + 4 * BS < s_end) load_x(av, s + 4 * BS, s_end);
     }
+    // buffer (c + 1) & 1 was last read by chunk c - 1, before the barrier
+    // that ended it
+    store_wg(c + 1 < nchunks ? c + 1 : c, (c + 1) & 1);
+#pragma unroll
+    for (int i = 0; i < BS; ++i)
+#pragma unroll
+      for (int g = 0; g < TGB; ++g) av[i][g] = avn[i][g];
+    __syncthreads();
   }
-  // acc[nb][r]: token (lane / 16) * 4 + r, expert nb * 16 + lane % 16
+  // (the loop ended with a barrier: the W_g buffers are dead, their LDS
+  // takes the partial tiles)
+  // acc[g][nb][r]: token g * 16 + (lane / 16) * 4 + r, expert nb * 16 + lane % 16
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+  for (int g = 0; g < TGB; ++g)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) part[wave][(lane >> 4) * 4 + r][nb * 16 + (lane & 15)] = acc[nb][r];
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        part[wave][g * kGateTok + (lane >> 4) * 4 + r][nb * 16 + (lane & 15)] = acc[g][nb][r];
   __syncthreads();
   // sum the four partial tiles in wave order; bias; logits out
-  for (int q = tid; q < kGateTok * E; q += 256) {
+  for (int q = tid; q < TB * E; q += 256) {
     const int tt = q / E, e = q % E;
     float l = part[0][tt][e] + part[1][tt][e];
     l += part[2][tt][e];
@@ -253,16 +363,32 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     if (t0 + tt < T) logits[(long)(t0 + tt) * E + e] = l;
   }
   __syncthreads();
-  // top-k: segments of EP lanes, one token per segment per round
-  const int G = 64 / EP;
-  const int seg = lane / EP, e = lane % EP;
-  const bool evalid = e < E;
-  for (int i = wave * G + seg; i < kGateTok; i += 4 * G) {
-    const int t = t0 + i;
-    if (t >= T) break;  // uniform across the segment
-    const float l = evalid ? part[0][i][e] : 0.f;
-    topk_write(l, e, evalid, EP, k, idx + (long)t * k, w + (long)t * k);
+  if (E > 16) {
+    // top-k: one token per thread, its logits scanned from LDS (the odd row
+    // pitch keeps the threads of a wave on distinct banks)
+    if (tid < TB && t0 + tid < T)
+      topk_scan(part[0][tid], E, k, idx + (long)(t0 + tid) * k, w + (long)(t0 + tid) * k);
+  } else {
+    // top-k: segments of EP <= 16 lanes, one token per segment per round
+    const int G = 64 / EP;
+    const int seg = lane / EP, e = lane % EP;
+    const bool evalid = e < E;
+    for (int i = wave * G + seg; i < TB; i += 4 * G) {
+      const int t = t0 + i;
+      if (t >= T) break;  // uniform across the segment
+      const float l = evalid ? part[0][i][e] : 0.f;
+      topk_write(l, e, evalid, EP, k, idx + (long)t * k, w + (long)t * k);
+    }
   }
+}
+
+// token groups per block: one W_g staging serves more tokens when W_g is
+// wide or the launch has blocks to spare
+inline int gate_groups_per_block(int T, int E) {
+  const int groups = (T + kGateTok - 1) / kGateTok;
+  if (E > 32 || groups >= 4096) return 4;
+  if (E > 16 || groups >= 2048) return 2;
+  return 1;
 }
 
 __global__ __launch_bounds__(kGateThreads) void route_kernel(const float* __restrict__ logits,
@@ -436,27 +562,110 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_kernel(
   }
 }
 
-// dW_g[m][e] = sum over splits of P (split order), db likewise
+// bf16 layers: d_logits of 64 tokens per block, written as float (the
+// output) and as a bf16 pair hi + lo per value (hi = bf16(dl), lo =
+// bf16(dl - hi): about 16 significant bits) in rows [hi(E4) | lo(E4)] for
+// the dW_g GEMM; db partials per block (token order); block 0 also writes
+// the row counts and offsets of the GEMM's token splits.
+constexpr int kDlTok = 64;
+__global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
+    float* __restrict__ d_logits, bf16_t* __restrict__ dlhl, float* __restrict__ Pb,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int T, int E, int E4, int k, int S,
+    int tps) {
+  // dense tile of the block's d_logits rows (odd pitch: column sums and row
+  // writes both spread over the banks)
+  __shared__ float tile[kDlTok][kMaxE + 1];
+  const int tid = threadIdx.x;
+  const long t0 = (long)blockIdx.x * kDlTok;
+  for (int q = tid; q < kDlTok * (kMaxE + 1); q += 256) (&tile[0][0])[q] = 0.f;
+  if (blockIdx.x == 0 && tid < S) {
+    const long r0 = (long)tid * tps;
+    counts[tid] = (int32_t)(r0 < T ? min((long)tps, T - r0) : 0);
+    offsets[tid] = (int32_t)(r0 < T ? r0 : T);
+  }
+  __syncthreads();
+  if (tid < kDlTok && t0 + tid < T) {
+    int ij[kMaxK];
+    float dl[kMaxK];
+    token_dl(idx, w, dw, t0 + tid, k, ij, dl);
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+      if (j < k) tile[tid][ij[j]] = dl[j];  // the k selected experts are distinct
+  }
+  __syncthreads();
+  for (int q = tid; q < kDlTok * E4; q += 256) {
+    const int tt = q / E4, e = q % E4;
+    const long t = t0 + tt;
+    if (t >= T) break;
+    const float v = tile[tt][e];
+    if (e < E) d_logits[t * E + e] = v;
+    const bf16_t hi = f32_to_bf16(v);
+    dlhl[t * 2 * E4 + e] = hi;
+    dlhl[t * 2 * E4 + E4 + e] = f32_to_bf16(v - bf16_to_f32(hi));
+  }
+  if (tid < E) {
+    float v = 0.f;
+    for (int tt = 0; tt < kDlTok; ++tt) v += tile[tt][tid];  // rows past T are zero
+    Pb[(long)blockIdx.x * E + tid] = v;
+  }
+}
+
+// dW_g[m][e] = sum over splits of P[s][m][e] (split order; rows of pitch
+// ldp), plus the same sum over column lo_off + e when lo_off >= 0 (the lo
+// halves of the bf16 path); db = sum over the SB rows of Pb
 __global__ __launch_bounds__(256) void gate_bwd_dw_reduce_kernel(
     const float* __restrict__ P, const float* __restrict__ Pb, float* __restrict__ dw_gate,
-    float* __restrict__ dbias, int M, int E, int S, int accumulate) {
+    float* __restrict__ dbias, int M, int E, int S, int ldp, int lo_off, int SB, int accumulate) {
   const long n = (long)M * E;
   const long q = blockIdx.x * 256L + threadIdx.x;
   if (q >= n + E) return;
   if (q < n) {
+    const long m = q / E, e = q % E;
+    const long stride = (long)M * ldp;
+    const float* p = P + m * ldp + e;
     float v = 0.f;
 #pragma unroll 8
-    for (int s = 0; s < S; ++s) v += P[(long)s * n + q];
+    for (int s = 0; s < S; ++s) v += p[s * stride];
+    if (lo_off >= 0) {
+      float vl = 0.f;
+#pragma unroll 8
+      for (int s = 0; s < S; ++s) vl += p[s * stride + lo_off];
+      v += vl;
+    }
     dw_gate[q] = accumulate ? dw_gate[q] + v : v;
   } else if (q < n + E && dbias != nullptr) {
     const int e = (int)(q - n);
     float v = 0.f;
-    for (int s = 0; s < S; ++s) v += Pb[(long)s * E + e];
+    for (int s = 0; s < SB; ++s) v += Pb[(long)s * E + e];
     dbias[e] = accumulate ? dbias[e] + v : v;
   }
 }
 
 int gate_eg(int E) { return E <= 8 ? 1 : E <= 16 ? 2 : E <= 32 ? 4 : 8; }
+
+// bf16 path: the GEMM's column count (hi and lo halves of E rounded up to 4)
+int gate_dw_cols(int E) { return 2 * ((E + 3) / 4 * 4); }
+
+// bf16 gates with E <= 16 over at most 8 M elements of x take the
+// register-tile kernel (one launch and a reduce; at these sizes launch
+// latency dominates); the others d_logits, then dW_g as a GEMM
+bool gate_dw_on_gemm(const Shape& s) {
+  return s.dtype == FLOWMOE_BF16 && (s.E > 16 || (long)s.T * s.M > (8L << 20));
+}
+
+// GEMM path: token splits of the dW_g GEMM (its pseudo-experts): about 256
+// blocks of 256 x 128 tiles, at least 128 tokens per split, at most 16 MB
+// of fp32 partials
+int gate_dw_splits(const Shape& s) {
+  const long mt = (s.M + 255) / 256, nt = (gate_dw_cols(s.E) + 127) / 128;
+  long sp = 256 / (mt * nt);
+  const long by_tokens = s.T / 128, by_bytes = (16L << 20) / ((long)s.M * gate_dw_cols(s.E) * 4);
+  if (sp > by_tokens) sp = by_tokens;
+  if (sp > by_bytes) sp = by_bytes;
+  if (sp > 64) sp = 64;
+  return sp < 1 ? 1 : (int)sp;
+}
 
 // token splits: about two blocks per CU over the m tiles, at least one token
 // per token lane
@@ -476,17 +685,23 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
   if (s.T == 0) return hipSuccess;
   const int EP = pow2_at_least(s.E);
   if (s.dtype == FLOWMOE_BF16) {
-    const int blocks = (s.T + kGateTok - 1) / kGateTok;
     const int NB = (s.E + 15) / 16;
+    const int TGB = gate_groups_per_block(s.T, s.E);
+    const int blocks = (s.T + kGateTok * TGB - 1) / (kGateTok * TGB);
     return traced(FLOWMOE_K_GATE, st, [&] {
-#define FLOWMOE_GATE_LAUNCH(NBV)                                                                  \
-  hipLaunchKernelGGL(gate_topk_mfma_kernel<NBV>, dim3(blocks), dim3(256), 0, st,                  \
+#define FLOWMOE_GATE_LAUNCH(NBV, TGBV)                                                            \
+  hipLaunchKernelGGL((gate_topk_mfma_kernel<NBV, TGBV>), dim3(blocks), dim3(256), 0, st,          \
                      (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M, s.E, \
                      s.k, EP)
-      if (NB == 1) FLOWMOE_GATE_LAUNCH(1);
-      else if (NB == 2) FLOWMOE_GATE_LAUNCH(2);
-      else if (NB == 3) FLOWMOE_GATE_LAUNCH(3);
-      else FLOWMOE_GATE_LAUNCH(4);
+#define FLOWMOE_GATE_NB(TGBV)                  \
+  if (NB == 1) FLOWMOE_GATE_LAUNCH(1, TGBV);   \
+  else if (NB == 2) FLOWMOE_GATE_LAUNCH(2, TGBV); \
+  else if (NB == 3) FLOWMOE_GATE_LAUNCH(3, TGBV); \
+  else FLOWMOE_GATE_LAUNCH(4, TGBV);
+      if (TGB == 1) { FLOWMOE_GATE_NB(1) }
+      else if (TGB == 2) { FLOWMOE_GATE_NB(2) }
+      else { FLOWMOE_GATE_NB(4) }
+#undef FLOWMOE_GATE_NB
 #undef FLOWMOE_GATE_LAUNCH
     });
   }
@@ -515,14 +730,48 @@ hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float
   });
 }
 
-// workspace: [W_g^T (E x M float) | P (S x M x E) | Pb (S x E)]
+// workspace: [W_g^T (E x M float) | P | Pb | GEMM path: dl hi/lo (T x N bf16),
+// split counts and offsets (S int32 each)]; register-tile path: P (S x M x E),
+// Pb (S x E); GEMM path: P (S x M x N, N = gate_dw_cols(E)), Pb (ceil(T/64) x E)
 size_t gate_wt_bytes(const Shape& s) { return align256((size_t)s.M * s.E * sizeof(float)); }
 
-size_t gate_bwd_ws_bytes(const Shape& s) {
-  const int S = gate_splits(s);
-  return gate_wt_bytes(s) + align256((size_t)S * s.M * s.E * sizeof(float)) +
-         align256((size_t)S * s.E * sizeof(float));
+namespace {
+struct GateWs {
+  float* P;
+  float* Pb;
+  bf16_t* dlhl;
+  int32_t* counts;
+  int32_t* offsets;
+  size_t bytes;  // from the start of the workspace
+};
+GateWs gate_ws(const Shape& s, void* ws) {
+  char* base = static_cast<char*>(ws);
+  size_t off = gate_wt_bytes(s);
+  GateWs g = {};
+  auto take = [&](size_t n) {
+    char* p = base ? base + off : nullptr;
+    off += align256(n);
+    return p;
+  };
+  if (gate_dw_on_gemm(s)) {
+    const int S = gate_dw_splits(s), N = gate_dw_cols(s.E);
+    const long nb = (s.T + kDlTok - 1) / kDlTok;
+    g.P = reinterpret_cast<float*>(take((size_t)S * s.M * N * sizeof(float)));
+    g.Pb = reinterpret_cast<float*>(take((size_t)(nb > 0 ? nb : 1) * s.E * sizeof(float)));
+    g.dlhl = reinterpret_cast<bf16_t*>(take((size_t)s.T * N * sizeof(bf16_t)));
+    g.counts = reinterpret_cast<int32_t*>(take((size_t)S * sizeof(int32_t)));
+    g.offsets = reinterpret_cast<int32_t*>(take((size_t)S * sizeof(int32_t)));
+  } else {
+    const int S = gate_splits(s);
+    g.P = reinterpret_cast<float*>(take((size_t)S * s.M * s.E * sizeof(float)));
+    g.Pb = reinterpret_cast<float*>(take((size_t)S * s.E * sizeof(float)));
+  }
+  g.bytes = off;
+  return g;
 }
+}  // namespace
+
+size_t gate_bwd_ws_bytes(const Shape& s) { return gate_ws(s, nullptr).bytes; }
 
 hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st) {
   float* wgt = static_cast<float*>(ws);
@@ -555,45 +804,64 @@ hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, co
 hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, const float* w,
                           const float* dw, float* d_logits, float* dw_gate, float* dbias,
                           int accumulate, void* ws, hipStream_t st) {
-  const int S = gate_splits(s);
-  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + gate_wt_bytes(s));
-  float* Pb = reinterpret_cast<float*>(reinterpret_cast<char*>(P) +
-                                       align256((size_t)S * s.M * s.E * sizeof(float)));
+  const GateWs g = gate_ws(s, ws);
   const bool bf = s.dtype == FLOWMOE_BF16;
-  if (s.T > 0) {
+  const long n = (long)s.M * s.E + s.E;
+  const int nred = (int)((n + 255) / 256);
+  if (s.T == 0) {
+    // with no tokens the gradient is zero: a reduce over zero splits writes it
+    if (accumulate) return hipSuccess;
+    return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
+      hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred), dim3(256), 0, st, g.P, g.Pb,
+                         dw_gate, dbias, s.M, s.E, 0, s.E, -1, 0, 0);
+    });
+  }
+  if (gate_dw_on_gemm(s)) {
+    // d_logits (and its hi/lo copy), then dW_g = x^T [hi | lo] as a weight-
+    // gradient GEMM whose pseudo-experts are the token splits, then the sum
+    // over splits and halves
+    const int S = gate_dw_splits(s), N = gate_dw_cols(s.E);
     const int tps = (s.T + S - 1) / S;
-    const dim3 grid((s.M + 63) / 64, S);
-    const int EG = gate_eg(s.E);
+    const int nb = (s.T + kDlTok - 1) / kDlTok;
     hipError_t e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
-#define FLOWMOE_DW_LAUNCH(EGV)                                                                   \
-  if (bf)                                                                                        \
-    hipLaunchKernelGGL((gate_bwd_dw_kernel<bf16_t, EGV>), grid, dim3(256), 0, st,                \
-                       (const bf16_t*)x, idx, w, dw, d_logits, P, Pb, s.T, s.M, s.E, s.k, tps);  \
-  else                                                                                           \
-    hipLaunchKernelGGL((gate_bwd_dw_kernel<float, EGV>), grid, dim3(256), 0, st,                 \
-                       (const float*)x, idx, w, dw, d_logits, P, Pb, s.T, s.M, s.E, s.k, tps);
-      if (EG == 1) {
-        FLOWMOE_DW_LAUNCH(1)
-      } else if (EG == 2) {
-        FLOWMOE_DW_LAUNCH(2)
-      } else if (EG == 4) {
-        FLOWMOE_DW_LAUNCH(4)
-      } else {
-        FLOWMOE_DW_LAUNCH(8)
-      }
-#undef FLOWMOE_DW_LAUNCH
+      hipLaunchKernelGGL(gate_bwd_dl_kernel, dim3(nb), dim3(256), 0, st, idx, w, dw, d_logits,
+                         g.dlhl, g.Pb, g.counts, g.offsets, s.T, s.E, N / 2, s.k, S, tps);
     });
     if (e != hipSuccess) return e;
+    e = launch_gate_dw_gemm(x, s.M, g.dlhl, N, g.counts, g.offsets, S, g.P, st);
+    if (e != hipSuccess) return e;
+    return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
+      hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred), dim3(256), 0, st, g.P, g.Pb,
+                         dw_gate, dbias, s.M, s.E, S, N, N / 2, nb, accumulate);
+    });
   }
-  if (s.T == 0 && accumulate) return hipSuccess;
-  // with no tokens the gradient is zero: a reduce over zero splits writes it
-  const int splits = s.T > 0 ? S : 0;
-  const int acc = s.T > 0 ? accumulate : 0;
-  const long n = (long)s.M * s.E + s.E;
-  const int nb = (int)((n + 255) / 256);
+  const int S = gate_splits(s);
+  const int tps = (s.T + S - 1) / S;
+  const dim3 grid((s.M + 63) / 64, S);
+  const int EG = gate_eg(s.E);
+  hipError_t e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
+#define FLOWMOE_DW_LAUNCH(EGV)                                                                    \
+  if (bf)                                                                                         \
+    hipLaunchKernelGGL((gate_bwd_dw_kernel<bf16_t, EGV>), grid, dim3(256), 0, st,                 \
+                       (const bf16_t*)x, idx, w, dw, d_logits, g.P, g.Pb, s.T, s.M, s.E, s.k, tps); \
+  else                                                                                            \
+    hipLaunchKernelGGL((gate_bwd_dw_kernel<float, EGV>), grid, dim3(256), 0, st, (const float*)x, \
+                       idx, w, dw, d_logits, g.P, g.Pb, s.T, s.M, s.E, s.k, tps);
+    if (EG == 1) {
+      FLOWMOE_DW_LAUNCH(1)
+    } else if (EG == 2) {
+      FLOWMOE_DW_LAUNCH(2)
+    } else if (EG == 4) {
+      FLOWMOE_DW_LAUNCH(4)
+    } else {
+      FLOWMOE_DW_LAUNCH(8)
+    }
+#undef FLOWMOE_DW_LAUNCH
+  });
+  if (e != hipSuccess) return e;
   return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
-    hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nb), dim3(256), 0, st, P, Pb, dw_gate,
-                       dbias, s.M, s.E, splits, acc);
+    hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred), dim3(256), 0, st, g.P, g.Pb, dw_gate,
+                       dbias, s.M, s.E, S, s.E, -1, S, accumulate);
   });
 }
 

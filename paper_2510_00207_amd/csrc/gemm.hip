@@ -36,7 +36,8 @@ enum {
   EPI_SWIGLU_FWD = 2,  // dual accumulators h1, h3: C0 = [h1 | h3], C1 = silu(h1) h3
   EPI_GELU_BWD = 3,    // C0 = acc * gelu'(aux h)
   EPI_SWIGLU_BWD = 4,  // C0 = [acc h3 silu'(h1) | acc silu(h1)] with aux = [h1 | h3]
-  EPI_WGRAD = 5        // fp32 C0 (cols < nsplit) / C1 (cols >= nsplit), optional +=
+  EPI_WGRAD = 5,       // fp32 C0 (cols < nsplit) / C1 (cols >= nsplit), optional +=
+  EPI_GATE_DW = 6      // as EPI_WGRAD (its own instance: the gate's dW_g partials)
 };
 
 struct GemmParams {
@@ -1207,6 +1208,29 @@ hipError_t run_f32(int kind, const Shape& s, GemmParams p, hipStream_t st) {
 }  // namespace
 
 void set_gemm_tiles(int tiles) { g_tiles.store(tiles, std::memory_order_relaxed); }
+
+hipError_t launch_gate_dw_gemm(const void* x, int M, const void* d, int N, const int32_t* counts,
+                               const int32_t* offsets, int S, float* P, hipStream_t st) {
+  Shape s2 = {};
+  s2.E = S;
+  GemmParams p = {};
+  p.counts = counts;
+  p.offsets = offsets;
+  p.E = S;
+  p.A = x;
+  p.lda = M;
+  p.B0 = d;
+  p.ldb = N;
+  p.Mdim = M;
+  p.N = N;
+  p.C0 = P;
+  p.C1 = P;
+  p.ldc = N;
+  p.c_estride = (long)M * N;
+  p.nsplit = 1 << 30;
+  p.ksplit = 1 << 30;
+  return run_gemm_bf16<MODE_KSUM, false, false, EPI_GATE_DW>(FLOWMOE_K_GATE_BWD_DW, s2, p, st);
+}
 
 size_t ffn_bwd_ws_bytes(const Shape& s) {
   const int hw = (s.act == FLOWMOE_SWIGLU) ? 2 * s.H : s.H;

@@ -19,7 +19,8 @@ def _shape(T, M, H, E, k, C, dtype="bf16", act="gelu", layout="packed"):
                         L.PADDED if layout == "padded" else L.PACKED)
 
 
-@pytest.mark.parametrize("E,k", [(1, 1), (3, 2), (4, 4), (8, 2), (16, 1), (33, 5), (64, 6), (64, 8)])
+@pytest.mark.parametrize("E,k", [(1, 1), (3, 2), (4, 4), (8, 2), (16, 1), (24, 3), (32, 4), (33, 5), (64, 6),
+                                 (64, 8)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_gate_topk(E, k, dtype):
     need_gpu()
@@ -46,8 +47,9 @@ def test_gate_topk(E, k, dtype):
 
 @pytest.mark.parametrize("T,M,E,k", [(77, 520, 64, 6), (130, 1000, 33, 3), (40, 4104, 8, 2)])
 def test_gate_topk_chunked_weights(T, M, E, k):
-    """W_g taller than one LDS chunk of the bf16 gate (32 KB of rows: 256 rows
-    at E = 64, 496 at E = 33, 2048 at E = 8), with a ragged last chunk."""
+    """W_g taller than one LDS chunk of the bf16 gate (32 KB of rows at a pitch
+    of 16 * ceil(E / 16) + 8: 224 rows at E = 64, 288 at E = 33 (copied
+    element by element), 672 at E = 8), with a ragged last chunk."""
     need_gpu()
     cfg = get_config("balanced", T=T, M=M, H=8, E=E, k=k, dtype="bf16", seed=M + E)
     inp = make_inputs(cfg, with_dy=False)
@@ -59,6 +61,29 @@ def test_gate_topk_chunked_weights(T, M, E, k):
     L.flowmoe_gate_topk(_shape(T, M, 8, E, k, 0), x, wg, None, logits, idx, w)
     torch.cuda.synchronize()
     own = oracle.gate_logits(as_f64(inp["x"]), as_f64(inp["w_gate"]), None)
+    gl = host(logits)
+    assert np.max(np.abs(gl - own)) <= 1e-4 * np.max(np.abs(own))
+    ref_i, ref_w = oracle.topk_select(gl, k)
+    assert np.array_equal(host(idx), ref_i)
+    np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
+
+
+@pytest.mark.parametrize("T,M,E,k", [(33000, 64, 8, 2), (65600, 32, 4, 1)])
+def test_gate_topk_many_tokens(T, M, E, k):
+    """Launches with 2 and 4 groups of 16 tokens per block of the bf16 gate
+    (chosen from the token count), ragged in the last block."""
+    need_gpu()
+    cfg = get_config("balanced", T=T, M=M, H=8, E=E, k=k, dtype="bf16", seed=T % 97)
+    inp = make_inputs(cfg, with_dy=False)
+    d = dev()
+    x, wg = to_torch(inp["x"], d), to_torch(inp["w_gate"], d)
+    bias = torch.linspace(-0.1, 0.1, E, device=d, dtype=torch.float32)
+    logits = torch.empty(T, E, device=d)
+    idx = torch.empty(T, k, dtype=torch.int32, device=d)
+    w = torch.empty(T, k, device=d)
+    L.flowmoe_gate_topk(_shape(T, M, 8, E, k, 0), x, wg, bias, logits, idx, w)
+    torch.cuda.synchronize()
+    own = oracle.gate_logits(as_f64(inp["x"]), as_f64(inp["w_gate"]), host(bias))
     gl = host(logits)
     assert np.max(np.abs(gl - own)) <= 1e-4 * np.max(np.abs(own))
     ref_i, ref_w = oracle.topk_select(gl, k)
@@ -285,6 +310,38 @@ def test_gemm_tile_shapes_agree(act, layout, gemm_tiles):
     names = [n for n in ("h", "a", "y", "dx", "dw1", "dw3", "dw2") if n != "dw3" or act == "swiglu"]
     for name, p, q in zip(names, out["wide"], out["narrow"]):
         assert torch.equal(p, q), name
+
+
+@pytest.mark.parametrize("T,M,E,k", [(3000, 520, 64, 6), (2000, 520, 20, 4), (9000, 1000, 3, 2),
+                                     (1000, 264, 3, 2), (777, 1024, 16, 1), (40, 136, 8, 2)])
+def test_gate_bwd_shapes(T, M, E, k):
+    """bf16 gate backward on both dW_g paths: the GEMM (E > 16 or more than 8 M
+    elements of x; several token splits and x column tiles, ragged, E not a
+    multiple of 4) and the register tiles (the rest, down to fewer tokens
+    than one split): d_logits, dW_g and db against the oracle within the
+    fp32 bound (the GEMM multiplies a hi + lo bf16 pair per d_logits value:
+    about 16 significant bits)."""
+    need_gpu()
+    rng = np.random.default_rng(T + M + E)
+    d = dev()
+    x64 = host(torch.from_numpy(rng.standard_normal((T, M))).to(d).to(torch.bfloat16))
+    wg64 = host(torch.from_numpy(rng.standard_normal((M, E)) * 0.05).to(d).to(torch.bfloat16))
+    idx, w = oracle.topk_select(rng.standard_normal((T, E)), k)
+    dtw64 = rng.standard_normal((T, k))
+    t = lambda a, dt=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(d).to(dt)
+    s = _shape(T, M, 8, E, k, 0, "bf16")
+    dlog = torch.empty(T, E, device=d)
+    dwg = torch.full((M, E), 3.0, device=d)
+    db = torch.full((E,), 3.0, device=d)
+    nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
+    ws = torch.empty(nws, dtype=torch.uint8, device=d)
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), t(idx, torch.int32), t(w, torch.float32),
+                            t(dtw64, torch.float32), dlog, dwg, db, None, 0, ws, nws)
+    torch.cuda.synchronize()
+    g = oracle.gate_bwd(x64, wg64, idx, host(t(w, torch.float32)), host(t(dtw64, torch.float32)))
+    assert_close(host(dlog), g["d_logits"], "f32", "d_logits")
+    assert_close(host(dwg), g["dw_gate"], "f32", "dw_gate")
+    assert_close(host(db), g["dbias"], "f32", "dbias")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
