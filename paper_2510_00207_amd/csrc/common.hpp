@@ -68,6 +68,37 @@ __device__ __forceinline__ void store8(float* p, const float v[8]) {
   *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
 }
 
+// 8 consecutive elements in their stored form (bf16: one 16-byte vector;
+// float: two), so that a kernel can issue all its loads before converting
+// any of them (ext-vector types: arrays of them stay in registers)
+typedef unsigned u32x4v_t __attribute__((ext_vector_type(4)));
+struct Raw8b {
+  u32x4v_t a;
+};
+struct Raw8f {
+  u32x4v_t a, b;
+};
+__device__ __forceinline__ Raw8b raw8_load(const bf16_t* p) {
+  return Raw8b{*reinterpret_cast<const u32x4v_t*>(p)};
+}
+__device__ __forceinline__ Raw8f raw8_load(const float* p) {
+  return Raw8f{*reinterpret_cast<const u32x4v_t*>(p), *reinterpret_cast<const u32x4v_t*>(p + 4)};
+}
+__device__ __forceinline__ void raw8_f32(const Raw8b& r, float v[8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(r.a[i] << 16);
+    v[2 * i + 1] = __uint_as_float(r.a[i] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ void raw8_f32(const Raw8f& r, float v[8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[i] = __uint_as_float(r.a[i]);
+    v[4 + i] = __uint_as_float(r.b[i]);
+  }
+}
+
 // activations (fp32). erf follows Abramowitz & Stegun 7.1.26,
 // erf(x) = 1 - (a1 t + ... + a5 t^5) exp(-x^2), t = 1 / (1 + p x), x >= 0,
 // absolute error <= 1.5e-7; its exp(-x^2) term is also phi(z) * sqrt(2 pi)

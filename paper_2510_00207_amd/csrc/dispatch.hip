@@ -18,6 +18,18 @@
 namespace flowmoe {
 namespace {
 
+template <int V>
+struct KConst {
+  static constexpr int value = V;
+};
+// f(KConst<KM>) with KM the smallest of 2, 4, 8 that is >= k
+template <typename F>
+__host__ void with_kmax(int k, F&& f) {
+  if (k <= 2) f(KConst<2>{});
+  else if (k <= 4) f(KConst<4>{});
+  else f(KConst<8>{});
+}
+
 constexpr int kScanThreads = 1024;
 constexpr int kScanWaves = kScanThreads / 64;
 constexpr int kScanUnroll = 8;  // chunk loads in flight per lane
@@ -156,33 +168,46 @@ __global__ __launch_bounds__(kScanThreads) void route_scan_kernel(
 }
 
 // x_disp[r] = x[row_src[r] / k] or zeros; rows [0, offsets[E]) (packed) or
-// all rows (padded). One wave per row.
-__global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restrict__ x,
+// all rows (padded). One wave per row; each lane has 4 loads in flight.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4v_t* __restrict__ x,
                                                           const int32_t* __restrict__ row_src,
                                                           const int32_t* __restrict__ offsets,
-                                                          uint4* __restrict__ x_disp, int E, int k,
+                                                          u32x4v_t* __restrict__ x_disp, int E, int k,
                                                           int vecs, long rows, int padded) {
+  constexpr int U = 4;
   const long r = blockIdx.x * 4L + (threadIdx.x >> 6);
   const long live = padded ? rows : (long)offsets[E];
   if (r >= live) return;
   const int lane = threadIdx.x & 63;
   const int src = row_src[r];
-  uint4* dst = x_disp + r * vecs;
+  u32x4v_t* dst = x_disp + r * vecs;
   if (src >= 0) {
-    const uint4* s = x + (long)(src / k) * vecs;
-    for (int v = lane; v < vecs; v += 64) dst[v] = s[v];
+    const u32x4v_t* s = x + (long)(src / k) * vecs;
+    for (int v0 = lane; v0 < vecs; v0 += 64 * U) {
+      u32x4v_t t[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int v = v0 + 64 * u;
+        t[u] = s[v < vecs ? v : v0];  // (every load issued, from in-bounds addresses)
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (v0 + 64 * u < vecs) dst[v0 + 64 * u] = t[u];
+    }
   } else {
-    const uint4 z = make_uint4(0, 0, 0, 0);
+    const u32x4v_t z = {0u, 0u, 0u, 0u};
     for (int v = lane; v < vecs; v += 64) dst[v] = z;
   }
 }
 
 // y[t] = sum_j w[t][j] * src[slot[t][j]] over kept j (w == nullptr: weight 1).
-// One wave per token, 8 elements per lane step. GATE (dispatch backward of
-// the layer): also adds the gate's share dl_t W_g^T, with dl_t taken from the
-// selection (gidx), its weights (gw) and their gradients (gdw), and W_g^T
-// given transposed in float (wgt, E x M).
-template <typename TE, bool GATE>
+// One wave per token, 8 elements per lane step; the k source rows of U
+// steps are all loaded before any is used (every load issued, from
+// in-bounds addresses), so each lane has k * U loads in flight. GATE
+// (dispatch backward of the layer): also adds the gate's share dl_t W_g^T,
+// with dl_t taken from the selection (gidx), its weights (gw) and their
+// gradients (gdw), and W_g^T given transposed in float (wgt, E x M).
+template <typename TE, bool GATE, int KM>  // KM >= k: size of the per-token arrays
 __global__ __launch_bounds__(256) void combine_rows_kernel(
     const TE* __restrict__ src, const int32_t* __restrict__ slot, const float* __restrict__ w,
     TE* __restrict__ y, int T, int M, int k, const int32_t* __restrict__ gidx,
@@ -190,22 +215,22 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = threadIdx.x & 63;
-  int sl[kMaxK];
-  float wt[kMaxK];
+  int sl[KM];
+  float wt[KM];
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
+  for (int j = 0; j < KM; ++j) {
     if (j < k) {
       sl[j] = slot[(long)t * k + j];
       wt[j] = (w != nullptr) ? w[(long)t * k + j] : 1.0f;
     }
   }
-  int ge[kMaxK];
-  float gl[kMaxK];
+  int ge[KM];
+  float gl[KM];
   if constexpr (GATE) {
     // dl over the selected experts: w_j (dw_j - sum_j' w_j' dw_j')
     float s = 0.f;
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
+    for (int j = 0; j < KM; ++j) {
       if (j < k) {
         ge[j] = gidx[(long)t * k + j];
         gl[j] = gw[(long)t * k + j];
@@ -213,38 +238,52 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
       }
     }
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j)
+    for (int j = 0; j < KM; ++j)
       if (j < k) gl[j] = gl[j] * (gdw[(long)t * k + j] - s);
   }
-  for (int m = lane * 8; m < M; m += 64 * 8) {
-    float acc[8];
+  constexpr int U = sizeof(TE) == 2 ? 2 : 1;
+  for (int m0 = lane * 8; m0 < M; m0 += 64 * 8 * U) {
+    decltype(raw8_load(src)) raw[U][KM];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int u = 0; u < U; ++u) {
+      const int m = m0 + 64 * 8 * u < M ? m0 + 64 * 8 * u : m0;
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-      if (j < k && sl[j] >= 0) {
-        float v[8];
-        load8(src + (long)sl[j] * M + m, v);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) acc[q] += wt[j] * v[q];
-      }
+      for (int j = 0; j < KM; ++j)
+        if (j < k) raw[u][j] = raw8_load(src + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
     }
-    if constexpr (GATE) {
 #pragma unroll
-      for (int j = 0; j < kMaxK; ++j)
-        if (j < k) {
-          float g[8];
-          load8(wgt + (long)ge[j] * M + m, g);
+    for (int u = 0; u < U; ++u) {
+      const int m = m0 + 64 * 8 * u;
+      if (m >= M) break;
+      float acc[8];
 #pragma unroll
-          for (int q = 0; q < 8; ++q) acc[q] += gl[j] * g[q];
+      for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        if (j < k && sl[j] >= 0) {
+          float v[8];
+          raw8_f32(raw[u][j], v);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[q] += wt[j] * v[q];
         }
+      }
+      if constexpr (GATE) {
+#pragma unroll
+        for (int j = 0; j < KM; ++j)
+          if (j < k) {
+            float g[8];
+            load8(wgt + (long)ge[j] * M + m, g);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[q] += gl[j] * g[q];
+          }
+      }
+      store8(y + (long)t * M + m, acc);
     }
-    store8(y + (long)t * M + m, acc);
   }
 }
 
 // combine backward, token part: dy_disp[slot] = w * dy[t], d_w = <dy[t], y_disp[slot]>
-template <typename TE>
+template <typename TE, int KM>  // KM >= k: size of the per-token arrays
 __global__ __launch_bounds__(256) void combine_bwd_kernel(
     const TE* __restrict__ dy, const TE* __restrict__ y_disp, const int32_t* __restrict__ slot,
     const float* __restrict__ w, const int32_t* __restrict__ counts, TE* __restrict__ dy_disp,
@@ -262,35 +301,51 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
   }
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  int sl[kMaxK];
-  float wt[kMaxK], dot[kMaxK];
+  int sl[KM];
+  float wt[KM], dot[KM];
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
+  for (int j = 0; j < KM; ++j) {
     dot[j] = 0.f;
     if (j < k) {
       sl[j] = slot[(long)t * k + j];
       wt[j] = w[(long)t * k + j];
     }
   }
-  for (int m = lane * 8; m < M; m += 64 * 8) {
-    float g[8];
-    load8(dy + (long)t * M + m, g);
+  // dy and the k rows of y_disp of U steps loaded before any is used
+  constexpr int U = sizeof(TE) == 2 ? 2 : 1;
+  for (int m0 = lane * 8; m0 < M; m0 += 64 * 8 * U) {
+    decltype(raw8_load(dy)) graw[U], raw[U][KM];
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-      if (j < k && sl[j] >= 0) {
-        float v[8], o[8];
-        load8(y_disp + (long)sl[j] * M + m, v);
+    for (int u = 0; u < U; ++u) {
+      const int m = m0 + 64 * 8 * u < M ? m0 + 64 * 8 * u : m0;
+      graw[u] = raw8_load(dy + (long)t * M + m);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          dot[j] += g[q] * v[q];
-          o[q] = wt[j] * g[q];
+      for (int j = 0; j < KM; ++j)
+        if (j < k) raw[u][j] = raw8_load(y_disp + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int m = m0 + 64 * 8 * u;
+      if (m >= M) break;
+      float g[8];
+      raw8_f32(graw[u], g);
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        if (j < k && sl[j] >= 0) {
+          float v[8], o[8];
+          raw8_f32(raw[u][j], v);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            dot[j] += g[q] * v[q];
+            o[q] = wt[j] * g[q];
+          }
+          store8(dy_disp + (long)sl[j] * M + m, o);
         }
-        store8(dy_disp + (long)sl[j] * M + m, o);
       }
     }
   }
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
+  for (int j = 0; j < KM; ++j) {
     if (j < k) {
       float d = dot[j];
       for (int off = 32; off > 0; off >>= 1) d += __shfl_xor(d, off, 64);
@@ -318,7 +373,7 @@ hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, in
   const long blocks = (s.rows + 3) / 4;
   return traced(FLOWMOE_K_GATHER, st, [&] {
     hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
-                       (const uint4*)x, row_src, offsets, (uint4*)x_disp, s.E, s.k, vecs, s.rows,
+                       (const u32x4v_t*)x, row_src, offsets, (u32x4v_t*)x_disp, s.E, s.k, vecs, s.rows,
                        padded);
   });
 }
@@ -328,14 +383,17 @@ hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slo
   if (s.T == 0) return hipSuccess;
   const int blocks = (s.T + 3) / 4;
   return traced(FLOWMOE_K_COMBINE, st, [&] {
-    if (s.dtype == FLOWMOE_BF16)
-      hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false>), dim3(blocks), dim3(256), 0, st,
-                         (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k, nullptr,
-                         nullptr, nullptr, nullptr, s.E);
-    else
-      hipLaunchKernelGGL((combine_rows_kernel<float, false>), dim3(blocks), dim3(256), 0, st,
-                         (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k, nullptr,
-                         nullptr, nullptr, nullptr, s.E);
+    with_kmax(s.k, [&](auto kc) {
+      constexpr int KMV = decltype(kc)::value;
+      if (s.dtype == FLOWMOE_BF16)
+        hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV>), dim3(blocks), dim3(256), 0, st,
+                           (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k, nullptr,
+                           nullptr, nullptr, nullptr, s.E);
+      else
+        hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV>), dim3(blocks), dim3(256), 0, st,
+                           (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k, nullptr,
+                           nullptr, nullptr, nullptr, s.E);
+    });
   });
 }
 
@@ -350,14 +408,17 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
   if (s.T == 0) return hipSuccess;
   const int blocks = (s.T + 3) / 4;
   return traced(FLOWMOE_K_COMBINE, st, [&] {
-    if (s.dtype == FLOWMOE_BF16)
-      hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true>), dim3(blocks), dim3(256), 0, st,
-                         (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx, s.T, s.M, s.k, idx, w,
-                         dw, wgt, s.E);
-    else
-      hipLaunchKernelGGL((combine_rows_kernel<float, true>), dim3(blocks), dim3(256), 0, st,
-                         (const float*)dx_disp, slot, nullptr, (float*)dx, s.T, s.M, s.k, idx, w,
-                         dw, wgt, s.E);
+    with_kmax(s.k, [&](auto kc) {
+      constexpr int KMV = decltype(kc)::value;
+      if (s.dtype == FLOWMOE_BF16)
+        hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true, KMV>), dim3(blocks), dim3(256), 0, st,
+                           (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx, s.T, s.M, s.k, idx, w,
+                           dw, wgt, s.E);
+      else
+        hipLaunchKernelGGL((combine_rows_kernel<float, true, KMV>), dim3(blocks), dim3(256), 0, st,
+                           (const float*)dx_disp, slot, nullptr, (float*)dx, s.T, s.M, s.k, idx, w,
+                           dw, wgt, s.E);
+    });
   });
 }
 
@@ -370,14 +431,17 @@ hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp
   const long blocks = token_blocks + fill_blocks;
   if (blocks == 0) return hipSuccess;
   return traced(FLOWMOE_K_COMBINE_BWD, st, [&] {
-    if (s.dtype == FLOWMOE_BF16)
-      hipLaunchKernelGGL(combine_bwd_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
-                         (const bf16_t*)dy, (const bf16_t*)y_disp, slot, w, counts,
-                         (bf16_t*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
-    else
-      hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st,
-                         (const float*)dy, (const float*)y_disp, slot, w, counts,
-                         (float*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
+    with_kmax(s.k, [&](auto kc) {
+      constexpr int KMV = decltype(kc)::value;
+      if (s.dtype == FLOWMOE_BF16)
+        hipLaunchKernelGGL((combine_bwd_kernel<bf16_t, KMV>), dim3((unsigned)blocks), dim3(256), 0, st,
+                           (const bf16_t*)dy, (const bf16_t*)y_disp, slot, w, counts,
+                           (bf16_t*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
+      else
+        hipLaunchKernelGGL((combine_bwd_kernel<float, KMV>), dim3((unsigned)blocks), dim3(256), 0, st,
+                           (const float*)dy, (const float*)y_disp, slot, w, counts,
+                           (float*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
+    });
   });
 }
 
