@@ -115,3 +115,48 @@ def test_two_streams_equal_one_stream_and_deterministic():
         ta, tb, tc = getattr(a, name), getattr(b, name), getattr(c, name)
         assert torch.equal(ta, tb), f"{name}: two streams differ from one"
         assert torch.equal(ta, tc), f"{name}: not deterministic"
+
+
+@pytest.mark.parametrize("name,R", [("balanced_s", 1), ("fine_s", 4)])
+def test_layer_graph_replays_equal_eager(name, R):
+    """A layer fwd+bwd step captured in a HIP graph (R chunks, two streams
+    joined through the layer's events) replays bit-identical to the eager
+    step, replay after replay, with eager work and synchronizations in
+    between (nothing in the captured step is a memset node)."""
+    need_gpu()
+    cfg = CASES[name]
+    inp = make_inputs(cfg)
+    ref, _ = run_layer(cfg, "packed", R=R, inp=inp)
+    from paper_2510_00207_amd.layer import MoELayer
+    layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
+                     dtype=cfg.dtype, layout="packed", bias=cfg.zipf_bias, device=dev())
+    load_layer(layer, inp)
+    bufs = layer.bufs()
+    gs, sm = torch.cuda.Stream(), torch.cuda.Stream()
+    # eager run first (the library's one-time set-up happens outside the capture)
+    layer.forward(gs, sm, bufs=bufs)
+    layer.backward(gs, sm, bufs=bufs)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=gs):
+        layer.forward(gs, sm, bufs=bufs)
+        layer.backward(gs, sm, bufs=bufs)
+    names = ("logits", "topk_idx", "topk_w", "slot", "x_disp", "h_save", "a_save", "y_disp", "y",
+             "dy_disp", "d_topk_w", "dx_disp", "dx", "d_logits", "dw_gate", "dw1", "dw2")
+    # buffers in the dispatched layout: only the live rows of each chunk are
+    # written (the packed tail past offsets[E] is not)
+    disp = ("x_disp", "h_save", "a_save", "y_disp", "dy_disp", "dx_disp")
+    live = [int(v) for v in ref.offsets[:, cfg.E].tolist()]
+    for rep in range(3):
+        for nm in names:  # clobber the outputs eagerly between replays
+            getattr(layer, nm).fill_(7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for nm in names:
+            a, b = getattr(layer, nm), getattr(ref, nm)
+            if nm in disp:
+                for r in range(R):
+                    assert torch.equal(a[r, :live[r]], b[r, :live[r]]), f"replay {rep}: {nm} chunk {r}"
+            else:
+                assert torch.equal(a, b), f"replay {rep}: {nm}"
