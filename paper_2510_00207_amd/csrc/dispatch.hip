@@ -244,12 +244,18 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
   constexpr int U = sizeof(TE) == 2 ? 2 : 1;
   for (int m0 = lane * 8; m0 < M; m0 += 64 * 8 * U) {
     decltype(raw8_load(src)) raw[U][KM];
+    Raw8f graw[GATE ? U : 1][GATE ? KM : 1];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int m = m0 + 64 * 8 * u < M ? m0 + 64 * 8 * u : m0;
 #pragma unroll
       for (int j = 0; j < KM; ++j)
         if (j < k) raw[u][j] = raw8_load(src + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
+      if constexpr (GATE) {
+#pragma unroll
+        for (int j = 0; j < KM; ++j)
+          if (j < k) graw[u][j] = raw8_load(wgt + (long)ge[j] * M + m);
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -272,7 +278,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
         for (int j = 0; j < KM; ++j)
           if (j < k) {
             float g[8];
-            load8(wgt + (long)ge[j] * M + m, g);
+            raw8_f32(graw[u][j], g);
 #pragma unroll
             for (int q = 0; q < 8; ++q) acc[q] += gl[j] * g[q];
           }

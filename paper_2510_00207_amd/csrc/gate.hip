@@ -457,13 +457,19 @@ __global__ __launch_bounds__(256) void gate_bwd_dx_kernel(
   token_dl(idx, w, dw, t, k, ij, dl);
   TIn* row = dx + t * M;
   for (int m = lane * 8; m < M; m += 64 * 8) {  // M is a multiple of 8
+    // this step's dx and W_g^T rows loaded before the add and the store
+    const auto xr = raw8_load(row + m);
+    Raw8f gr[kMaxK];
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+      if (j < k) gr[j] = raw8_load(wgt + (long)ij[j] * M + m);
     float v[8];
-    load8(row + m, v);
+    raw8_f32(xr, v);
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j) {
       if (j < k) {
         float g[8];
-        load8(wgt + (long)ij[j] * M + m, g);
+        raw8_f32(gr[j], g);
 #pragma unroll
         for (int q = 0; q < 8; ++q) v[q] += dl[j] * g[q];
       }

@@ -215,6 +215,25 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
     auto sidx = [&](int r, int c4) { return r * WN + ((c4 ^ (r & (SCH - 1))) << 2); };
 #pragma unroll
     for (int hf = 0; hf < FM / 2; ++hf) {
+      // activation-backward epilogues read the saved pre-activations: all of
+      // this half's loads go out before the staging, and none waits behind
+      // an output store (one memory round trip per half, not one per item)
+      constexpr bool AUXB = MODE == MODE_ROWS && (EPI == EPI_GELU_BWD || EPI == EPI_SWIGLU_BWD);
+      constexpr int AG8 = WN / 8, APER = AUXB ? AG8 : 1;
+      Raw8b hr[APER], h3r[APER];
+      if constexpr (AUXB) {
+#pragma unroll
+        for (int it = 0; it < APER; ++it) {
+          const int item = it * 64 + lane;
+          const int rr = item / AG8, c8 = item % AG8;
+          const int ti = wm * WM + hf * 64 + rr;
+          const int n = n0 + wn * WN + c8 * 8;
+          const bool ok = mt * BM + ti < rows_e && n < p.N;
+          const long off = ok ? (long)(row0 + ti) * p.ldaux + n : 0;  // (clamped: every load issued)
+          hr[it] = raw8_load(aux + off);
+          if constexpr (EPI == EPI_SWIGLU_BWD) h3r[it] = raw8_load(aux + off + (ok ? p.Hh : 0));
+        }
+      }
 #pragma unroll
       for (int i2 = 0; i2 < 2; ++i2)
 #pragma unroll
@@ -265,26 +284,48 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
       } else if constexpr (MODE == MODE_KSUM) {  // fp32 weight gradient, C0 | C1 split at nsplit
         constexpr int G8 = WN / 8;
         constexpr int PER = 64 * G8 / 64;
+        constexpr int PB = PER >= 4 ? 4 : PER;  // items per batch of accumulation loads
         float* D0 = static_cast<float*>(p.C0);
         float* D1 = static_cast<float*>(p.C1);
-#pragma unroll
-        for (int it = 0; it < PER; ++it) {
+        auto dst_of = [&](int it, bool& ok) {
           const int item = it * 64 + lane;
           const int rr = item / G8, c8 = item % G8;
           const int m = mt * BM + wm * WM + hf * 64 + rr;
           const int n = n0 + wn * WN + c8 * 8;
-          if (m >= p.Mdim || n >= p.N) continue;  // N and nsplit are multiples of 8
-          float v[8];
-          read8(rr, c8, v);
-          float* dst = (n < p.nsplit) ? D0 + (long)e * p.c_estride + (long)m * p.ldc + n
-                                      : D1 + (long)e * p.c_estride + (long)m * p.ldc + (n - p.nsplit);
-          if (p.accumulate) {
-            float o[8];
-            load8(dst, o);
+          ok = m < p.Mdim && n < p.N;  // N and nsplit are multiples of 8
+          return (n < p.nsplit) ? D0 + (long)e * p.c_estride + (long)m * p.ldc + n
+                                : D1 + (long)e * p.c_estride + (long)m * p.ldc + (n - p.nsplit);
+        };
 #pragma unroll
-            for (int q = 0; q < 8; ++q) v[q] += o[q];
+        for (int b0 = 0; b0 < PER; b0 += PB) {
+          // accumulation: the batch's old values are all loaded before any
+          // store (from clamped addresses), one memory round trip per batch
+          Raw8f old[PB];
+          if (p.accumulate) {
+#pragma unroll
+            for (int i = 0; i < PB; ++i) {
+              bool ok;
+              float* d = dst_of(b0 + i, ok);
+              old[i] = raw8_load(ok ? d : D0);
+            }
           }
-          store8(dst, v);
+#pragma unroll
+          for (int i = 0; i < PB; ++i) {
+            const int it = b0 + i;
+            bool ok;
+            float* dst = dst_of(it, ok);
+            if (!ok) continue;
+            const int item = it * 64 + lane;
+            float v[8];
+            read8(item / G8, item % G8, v);
+            if (p.accumulate) {
+              float o[8];
+              raw8_f32(old[i], o);
+#pragma unroll
+              for (int q = 0; q < 8; ++q) v[q] += o[q];
+            }
+            store8(dst, v);
+          }
         }
       } else {
         constexpr int G8 = WN / 8;
@@ -315,14 +356,14 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
             store8(C1 + g * p.ldc1 + n, a);
           } else if constexpr (EPI == EPI_GELU_BWD) {
             float h[8];
-            load8(aux + g * p.ldaux + n, h);
+            raw8_f32(hr[it], h);
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[q] *= gelu_grad_f(h[q]);
             store8(C0 + g * p.ldc + n, v);
           } else if constexpr (EPI == EPI_SWIGLU_BWD) {
             float h1[8], h3[8], d3[8];
-            load8(aux + g * p.ldaux + n, h1);
-            load8(aux + g * p.ldaux + p.Hh + n, h3);
+            raw8_f32(hr[it], h1);
+            raw8_f32(h3r[it], h3);
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
               const float sg = sigmoid_f(h1[q]);
