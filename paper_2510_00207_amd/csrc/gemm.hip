@@ -576,11 +576,20 @@ struct IntC {
 template <int BM>
 __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, int& e, int& mt,
                                                   int& nt, int& rows_e, int& cnt_e) {
+  // the experts' counts in one vector load (lane x: expert x, E <= 64), then
+  // walked in scalar registers (no memory round trip per expert)
+  const int lane = threadIdx.x & 63;
+  const int cvec = lane < p.E ? p.counts[lane] : 0;
+  auto tiles = [&](int x, int& c, int& r, int& te, int& he) {
+    c = __builtin_amdgcn_readlane(cvec, x);
+    r = p.padC ? p.padC : c;
+    te = (r + BM - 1) / BM;
+    he = min(te, (c + BM / 2) / BM);
+  };
   int HR = 0, LR = 0;  // heavy / light row tiles
   for (int x = 0; x < p.E; ++x) {
-    const int c = p.counts[x], r = p.padC ? p.padC : c;
-    const int te = (r + BM - 1) / BM;
-    const int he = min(te, (c + BM / 2) / BM);
+    int c, r, te, he;
+    tiles(x, c, r, te, he);
     HR += he;
     LR += te - he;
   }
@@ -607,9 +616,8 @@ __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, 
   const int ml = g * kRowGroup + (rg - nt * gm);
   int acc_t = 0;
   for (e = 0; e < p.E; ++e) {
-    const int c = p.counts[e], r = p.padC ? p.padC : c;
-    const int te = (r + BM - 1) / BM;
-    const int he = min(te, (c + BM / 2) / BM);
+    int c, r, te, he;
+    tiles(e, c, r, te, he);
     const int ce = heavy ? he : te - he;
     if (ml < acc_t + ce) {
       mt = (heavy ? 0 : he) + (ml - acc_t);
