@@ -386,8 +386,8 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
 // wide or the launch has blocks to spare
 inline int gate_groups_per_block(int T, int E) {
   const int groups = (T + kGateTok - 1) / kGateTok;
-  if (E > 32 || groups >= 4096) return 4;
-  if (E > 16 || groups >= 2048) return 2;
+  if (E > 32 || groups >= 1024) return 4;
+  if (E > 16) return 2;
   return 1;
 }
 
