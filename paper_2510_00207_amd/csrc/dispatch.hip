@@ -200,6 +200,55 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4v_t* __rest
   }
 }
 
+// x_disp[slot[t][j]] = x[t] for every kept j: one wave per token, the row read
+// once (4 loads in flight per lane) and written to each of its rows. Padded
+// layout: blocks past the token blocks zero the rows past each expert's
+// count. (Rows of the packed layout past offsets[E] are not written.)
+template <int KM>  // KM >= k
+__global__ __launch_bounds__(256) void scatter_rows_kernel(
+    const u32x4v_t* __restrict__ x, const int32_t* __restrict__ slot,
+    const int32_t* __restrict__ counts, u32x4v_t* __restrict__ x_disp, int T, int k, int vecs,
+    int E, int C, int token_blocks) {
+  constexpr int U = 4;
+  const int lane = threadIdx.x & 63;
+  if ((int)blockIdx.x >= token_blocks) {
+    const long r = ((long)blockIdx.x - token_blocks) * 4 + (threadIdx.x >> 6);
+    if (r >= (long)E * C) return;
+    const int e = (int)(r / C), i = (int)(r % C);
+    if (i < counts[e]) return;
+    const u32x4v_t z = {0u, 0u, 0u, 0u};
+    for (int v = lane; v < vecs; v += 64) x_disp[r * vecs + v] = z;
+    return;
+  }
+  const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  int sl[KM];
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    sl[j] = j < k ? slot[t * k + j] : -1;
+    any |= sl[j] >= 0;
+  }
+  if (!any) return;  // every assignment of the token dropped
+  const u32x4v_t* src = x + t * vecs;
+  for (int v0 = lane; v0 < vecs; v0 += 64 * U) {
+    u32x4v_t q[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + 64 * u;
+      q[u] = src[v < vecs ? v : v0];  // (every load issued, from in-bounds addresses)
+    }
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      if (sl[j] < 0) continue;
+      u32x4v_t* dst = x_disp + (long)sl[j] * vecs;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (v0 + 64 * u < vecs) dst[v0 + 64 * u] = q[u];
+    }
+  }
+}
+
 // y[t] = sum_j w[t][j] * src[slot[t][j]] over kept j (w == nullptr: weight 1).
 // One wave per token, 8 elements per lane step; the k source rows of U
 // steps are all loaded before any is used (every load issued, from
@@ -376,11 +425,26 @@ hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, in
   });
   if (err != hipSuccess || s.rows == 0) return err;
   const int vecs = (int)((long)s.M * esize(s.dtype) / 16);
-  const long blocks = (s.rows + 3) / 4;
+  if (s.k == 1) {  // one row per token: walk the rows
+    const long blocks = (s.rows + 3) / 4;
+    return traced(FLOWMOE_K_GATHER, st, [&] {
+      hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                         (const u32x4v_t*)x, row_src, offsets, (u32x4v_t*)x_disp, s.E, s.k, vecs,
+                         s.rows, padded);
+    });
+  }
+  // k >= 2: walk the tokens, each x row read once for its k rows
+  const int token_blocks = (s.T + 3) / 4;
+  const long fill_blocks = padded ? ((long)s.E * s.C + 3) / 4 : 0;
+  const long blocks = token_blocks + fill_blocks;
+  if (blocks == 0) return hipSuccess;
   return traced(FLOWMOE_K_GATHER, st, [&] {
-    hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
-                       (const u32x4v_t*)x, row_src, offsets, (u32x4v_t*)x_disp, s.E, s.k, vecs, s.rows,
-                       padded);
+    with_kmax(s.k, [&](auto kc) {
+      constexpr int KMV = decltype(kc)::value;
+      hipLaunchKernelGGL((scatter_rows_kernel<KMV>), dim3((unsigned)blocks), dim3(256), 0, st,
+                         (const u32x4v_t*)x, slot, counts, (u32x4v_t*)x_disp, s.T, s.k, vecs, s.E,
+                         s.C, token_blocks);
+    });
   });
 }
 
