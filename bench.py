@@ -80,7 +80,8 @@ def memory_bound(L, layer, cfg, torch, reps: int = 20):
         "gate": (lambda: L.flowmoe_gate_topk(s, x, layer.w_gate, layer.bias, lg, idx, w, stream=st),
                  T * M * b),
         "dispatch (scan + gather)": (
-            lambda: L.flowmoe_dispatch(s, idx, x, cnt, off, slot, rs, ld, xd, stream=st),
+            lambda: L.flowmoe_dispatch(s, idx, x, cnt, off, slot, rs, ld, xd, layer.ws,
+                                       layer.ws_bytes, stream=st),
             (T + A) * M * b),
         "combine": (lambda: L.flowmoe_combine(s, yd, slot, w, y, stream=st), (A + T) * M * b),
         "combine bwd": (lambda: L.flowmoe_combine_bwd(s, dy, yd, slot, w, cnt, off, dyd, dw,

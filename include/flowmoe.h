@@ -133,7 +133,12 @@ flowmoe_status_t flowmoe_route(const flowmoe_shape_t* shape, const float* logits
  *                  for an empty row (rows = flowmoe_rows_capacity)
  *   load     E     int32 (out, nullable) demand per expert before the drop
  *   x_disp   rows x M layer dtype (out)
- *   ws       workspace of flowmoe_workspace_bytes(shape, FLOWMOE_WS_DISPATCH) */
+ *   ws       nullable; flowmoe_workspace_bytes(shape, FLOWMOE_WS_DISPATCH)
+ *            bytes (0 for T*k <= 16384). With it, inputs of more than 16384
+ *            assignments count each 1024-assignment tile's experts once into
+ *            the workspace instead of every tile recounting all others;
+ *            results are identical. Non-null but too small:
+ *            FLOWMOE_ERR_WORKSPACE. */
 flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* topk_idx,
                                   const void* x, int32_t* counts, int32_t* offsets,
                                   int32_t* slot, int32_t* row_src, int32_t* load,
@@ -297,7 +302,9 @@ typedef struct {
   float* dw3;         /* E x M x H, SwiGLU only */
   float* dw2;         /* E x H x M */
   /* scratch */
-  void* ws;           /* flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD) */
+  void* ws;           /* flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
+                         nullable in the forward, which uses it as the
+                         dispatch workspace of each chunk in turn */
   size_t ws_bytes;
 } flowmoe_layer_bufs_t;
 

@@ -208,11 +208,14 @@ size_t flowmoe_workspace_bytes(const flowmoe_shape_t* shape, int32_t kind) {
     if (check_shape(shape, 0, &s) != FLOWMOE_OK) return 0;
   }
   switch (kind) {
-    case FLOWMOE_WS_DISPATCH: return 0;
+    case FLOWMOE_WS_DISPATCH: return dispatch_ws_bytes(s);
     case FLOWMOE_WS_FFN_BWD: return ffn_bwd_ws_bytes(s);
     case FLOWMOE_WS_GATE_BWD: return gate_bwd_ws_bytes(s);
-    case FLOWMOE_WS_LAYER_BWD:  // disjoint: the gate backward overlaps the expert backward
-      return align256(ffn_bwd_ws_bytes(s)) + gate_bwd_ws_bytes(s);
+    case FLOWMOE_WS_LAYER_BWD: {  // disjoint: the gate backward overlaps the expert backward
+      const size_t bwd = align256(ffn_bwd_ws_bytes(s)) + gate_bwd_ws_bytes(s);
+      const size_t fwd = dispatch_ws_bytes(s);  // the forward's dispatch scan
+      return bwd > fwd ? bwd : fwd;
+    }
     default: return 0;
   }
 }
@@ -265,9 +268,12 @@ flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* t
     REQUIRE(row_src, "row_src");
     REQUIRE_T(x_disp, "x_disp");
   }
-  (void)ws; (void)ws_bytes;
+  if (ws != nullptr) {
+    st = check_ws(ws, ws_bytes, dispatch_ws_bytes(s), "flowmoe_dispatch");
+    if (st != FLOWMOE_OK) return st;
+  }
   return hip_status(launch_dispatch(s, topk_idx, x, counts, offsets, slot, row_src, load, x_disp,
-                                    stream),
+                                    ws, stream),
                     "flowmoe_dispatch");
 }
 
@@ -494,6 +500,10 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
   REQUIRE(b->counts, "bufs->counts");
   REQUIRE(b->offsets, "bufs->offsets");
   if (s.act == FLOWMOE_SWIGLU) REQUIRE_T(b->w3, "bufs->w3");
+  if (b->ws != nullptr) {  // optional here: the dispatch scan's tile histograms
+    st = check_ws(b->ws, b->ws_bytes, dispatch_ws_bytes(s), "flowmoe_layer_fwd");
+    if (st != FLOWMOE_OK) return st;
+  }
   if (s.T > 0) {
     REQUIRE_T(b->x, "bufs->x"); REQUIRE(b->logits, "bufs->logits");
     REQUIRE(b->topk_idx, "bufs->topk_idx"); REQUIRE(b->topk_w, "bufs->topk_w");
@@ -528,7 +538,7 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
     sc.wait(s_comm, evG[r]);
     sc.mark(1, r, 0, s_comm);
     sc.run(launch_dispatch(s, c.idx, c.x, c.counts, c.offsets, c.slot, c.row_src, c.load, c.x_disp,
-                           s_comm));
+                           b->ws, s_comm));
     sc.mark(1, r, 1, s_comm);
     sc.signal(evD[r], s_comm);
   }

@@ -140,9 +140,12 @@ constexpr int kMaxK = 8;
 hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, const float* bias,
                             float* logits, int32_t* idx, float* w, hipStream_t st);
 hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float* w, hipStream_t st);
+// dispatch workspace: per-tile expert histograms (0 bytes up to 16 tiles of
+// 1024 assignments); ws may be null, then the scan recounts every tile
+size_t dispatch_ws_bytes(const Shape& s);
 hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, int32_t* counts,
                            int32_t* offsets, int32_t* slot, int32_t* row_src, int32_t* load,
-                           void* x_disp, hipStream_t st);
+                           void* x_disp, void* ws, hipStream_t st);
 hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slot, const float* w,
                           void* y, hipStream_t st);
 hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp,

@@ -11,6 +11,10 @@
 //   ballots on the expert bits tell every lane which lanes share its expert
 //   (its rank) and lane e how many lanes hold expert e. Inside the tile, the
 //   16 waves' counts are scanned per expert with 16-lane shuffles.
+//   With more than 16 tiles that recount grows with the square of the
+//   input, so a first kernel (tile_hist) writes each tile's per-expert
+//   counts to a workspace and the scan sums those E-wide rows instead: the
+//   same integers in the same order, from 1024/E times fewer reads.
 // gather / combine / scatter kernels move whole rows with 16-byte vectors,
 //   one wave per row or token, accumulating in float in a fixed order.
 #include "common.hpp"
@@ -33,6 +37,7 @@ __host__ void with_kmax(int k, F&& f) {
 constexpr int kScanThreads = 1024;
 constexpr int kScanWaves = kScanThreads / 64;
 constexpr int kScanUnroll = 8;  // chunk loads in flight per lane
+constexpr long kScanHistTiles = 16;  // more tiles than this: histogram pass
 
 // expert of priority position s (j = s / T, t = s % T), or -1
 __device__ __forceinline__ int scan_expert(const int32_t* __restrict__ idx, unsigned s, unsigned n,
@@ -61,10 +66,32 @@ __device__ __forceinline__ void chunk_match(int e, int lane, uint64_t lt_mask, i
   count = __popcll(mine);
 }
 
+// hist[b][e] = assignments of expert e among the tile's 1024 positions
+__global__ __launch_bounds__(kScanThreads) void tile_hist_kernel(const int32_t* __restrict__ idx,
+                                                                 int32_t* __restrict__ hist,
+                                                                 int T, int k, int E) {
+  __shared__ int part[kScanWaves][64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const unsigned n = (unsigned)T * (unsigned)k;
+  const int e = scan_expert(idx, blockIdx.x * (unsigned)kScanThreads + tid, n, T, k, E);
+  int rank, cnt;
+  chunk_match(e, lane, lt_mask, rank, cnt);
+  part[wave][lane] = cnt;
+  __syncthreads();
+  if (wave == 0 && lane < E) {
+    int sum = 0;
+#pragma unroll
+    for (int w = 0; w < kScanWaves; ++w) sum += part[w][lane];
+    hist[(long)blockIdx.x * E + lane] = sum;
+  }
+}
+
 __global__ __launch_bounds__(kScanThreads) void route_scan_kernel(
-    const int32_t* __restrict__ idx, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
-    int32_t* __restrict__ slot, int32_t* __restrict__ row_src, int32_t* __restrict__ load, int T,
-    int k, int E, int C, int padded, long rows) {
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ hist,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ slot,
+    int32_t* __restrict__ row_src, int32_t* __restrict__ load, int T, int k, int E, int C,
+    int padded, long rows) {
   __shared__ int own[kScanWaves][64];   // tile counts per wave, then element bases
   __shared__ int bef[kScanWaves][64];   // per-wave counts before the tile
   __shared__ int aft[kScanWaves][64];   // per-wave counts after the tile
@@ -76,10 +103,24 @@ __global__ __launch_bounds__(kScanThreads) void route_scan_kernel(
   const unsigned n = (unsigned)T * (unsigned)k;  // <= 2^30 (host check)
   const unsigned tile0 = blockIdx.x * (unsigned)kScanThreads;
 
-  // 1. counts outside the tile: wave w takes chunks c = i * 1024 + 64 w
+  // 1. counts outside the tile: wave w takes chunks c = i * 1024 + 64 w, or
+  //    with the tile histograms (lane = expert) the tiles i = w mod 16
   int cb = 0, ca = 0;
   const unsigned nt = (n + kScanThreads - 1) / kScanThreads;  // tiles
-  for (unsigned i0 = 0; i0 < nt; i0 += kScanUnroll) {
+  if (hist != nullptr) {
+    for (unsigned i0 = wave; i0 < nt; i0 += kScanWaves * kScanUnroll) {
+      int hv[kScanUnroll];
+#pragma unroll
+      for (int u = 0; u < kScanUnroll; ++u) {
+        const unsigned i = i0 + u * kScanWaves;
+        hv[u] = (i < nt && i != blockIdx.x && lane < E) ? hist[(long)i * E + lane] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < kScanUnroll; ++u) {
+        if (i0 + u * kScanWaves < blockIdx.x) cb += hv[u]; else ca += hv[u];
+      }
+    }
+  } else for (unsigned i0 = 0; i0 < nt; i0 += kScanUnroll) {
     int ev[kScanUnroll];
 #pragma unroll
     for (int u = 0; u < kScanUnroll; ++u) {
@@ -411,17 +452,27 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
 
 }  // namespace
 
+size_t dispatch_ws_bytes(const Shape& s) {
+  const long tiles = ((long)s.T * s.k + kScanThreads - 1) / kScanThreads;
+  return tiles > kScanHistTiles ? align256((size_t)tiles * s.E * sizeof(int32_t)) : 0;
+}
+
 hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, int32_t* counts,
                            int32_t* offsets, int32_t* slot, int32_t* row_src, int32_t* load,
-                           void* x_disp, hipStream_t st) {
+                           void* x_disp, void* ws, hipStream_t st) {
   const int padded = s.layout == FLOWMOE_PADDED;
   const long n = (long)s.T * s.k;
   const long tiles = (n + kScanThreads - 1) / kScanThreads;
   const long fill = (s.rows + kScanThreads - 1) / kScanThreads;  // blocks for the row fill
   const unsigned grid = (unsigned)(tiles > 0 ? tiles : (fill > 0 ? (fill < 64 ? fill : 64) : 1));
+  int32_t* hist = (ws != nullptr && dispatch_ws_bytes(s) > 0) ? (int32_t*)ws : nullptr;
   hipError_t err = traced(FLOWMOE_K_SCAN, st, [&] {
-    hipLaunchKernelGGL(route_scan_kernel, dim3(grid), dim3(kScanThreads), 0, st, idx, counts,
-                       offsets, slot, row_src, load, s.T, s.k, s.E, s.C, padded, s.rows);
+    if (hist != nullptr)
+      hipLaunchKernelGGL(tile_hist_kernel, dim3((unsigned)tiles), dim3(kScanThreads), 0, st, idx,
+                         hist, s.T, s.k, s.E);
+    hipLaunchKernelGGL(route_scan_kernel, dim3(grid), dim3(kScanThreads), 0, st, idx,
+                       (const int32_t*)hist, counts, offsets, slot, row_src, load, s.T, s.k, s.E,
+                       s.C, padded, s.rows);
   });
   if (err != hipSuccess || s.rows == 0) return err;
   const int vecs = (int)((long)s.M * esize(s.dtype) / 16);

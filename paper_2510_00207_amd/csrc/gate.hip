@@ -78,40 +78,82 @@ __device__ __forceinline__ void topk_write(float logit, int e, bool valid, int E
   }
 }
 
-// Top-k of one token's E logits by one thread: a sorted list of the kMaxK
-// best (value, index) so far, scanned in expert order. A later expert
-// displaces an entry only with a strictly larger value, so equal values keep
-// the lower index, and -0.0 == +0.0 (IEEE compare). Then the softmax over
-// the k selected, shifted by the largest.
-__device__ __forceinline__ void topk_scan(const float* logit, int E, int k, int32_t* idx_out,
-                                          float* w_out) {
-  float tv[kMaxK];
-  int ti[kMaxK];
+// Top-k of one token's E logits by P consecutive lanes (P a power of two
+// <= 64). Order: larger value first, equal values by lower index, -0.0 ==
+// +0.0 (IEEE compare); an empty slot is (-inf, 2^30), below every logit.
+// Lane p keeps a sorted list of the KM best of logits p, p + P, ... (an
+// insertion without branches); then log2(P) exchanges with lane p ^ m merge
+// two sorted lists: the better of a[j] and b[KM - 1 - j] for every j gives
+// the KM best of both as a bitonic sequence, which half-cleaners sort. Every
+// lane ends with the same list; lane p == 0 writes the k selected and their
+// softmax, shifted by the largest.
+__device__ __forceinline__ bool key_beats(float v, int i, float tv, int ti) {
+  return (v > tv) | ((v == tv) & (i < ti));
+}
+
+template <int KM>
+__device__ __forceinline__ void topk_insert(float v, int i, float (&tv)[KM], int (&ti)[KM]) {
+  bool b[KM];
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
+  for (int j = 0; j < KM; ++j) b[j] = key_beats(v, i, tv[j], ti[j]);
+#pragma unroll
+  for (int j = KM - 1; j >= 1; --j) {  // b is monotone: b[j - 1] implies b[j]
+    const float nv = b[j - 1] ? tv[j - 1] : v;
+    const int ni = b[j - 1] ? ti[j - 1] : i;
+    tv[j] = b[j] ? nv : tv[j];
+    ti[j] = b[j] ? ni : ti[j];
+  }
+  tv[0] = b[0] ? v : tv[0];
+  ti[0] = b[0] ? i : ti[0];
+}
+
+template <int KM, int P>
+__device__ __forceinline__ void topk_lanes(const float* logit, int E, int k, int p,
+                                           int32_t* idx_out, float* w_out) {
+  float tv[KM];
+  int ti[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
     tv[j] = -INFINITY;
     ti[j] = 1 << 30;
   }
-  for (int e = 0; e < E; ++e) {
-    const float v = logit[e];
+  for (int e = p; e < E; e += P) topk_insert<KM>(logit[e], e, tv, ti);
 #pragma unroll
-    for (int j = kMaxK - 1; j >= 0; --j) {
-      const bool here = v > tv[j] || (v == tv[j] && e < ti[j]);
-      const bool above = j > 0 && (v > tv[j - 1] || (v == tv[j - 1] && e < ti[j - 1]));
-      if (here) {
-        tv[j] = above ? tv[j - 1 < 0 ? 0 : j - 1] : v;
-        ti[j] = above ? ti[j - 1 < 0 ? 0 : j - 1] : e;
-      }
+  for (int m = 1; m < P; m <<= 1) {
+    float ov[KM];
+    int oi[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      ov[j] = __shfl_xor(tv[j], m);
+      oi[j] = __shfl_xor(ti[j], m);
     }
-  }
-  float ex[kMaxK], denom = 0.f;
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
+    for (int j = 0; j < KM; ++j) {
+      const bool mine = key_beats(tv[j], ti[j], ov[KM - 1 - j], oi[KM - 1 - j]);
+      tv[j] = mine ? tv[j] : ov[KM - 1 - j];
+      ti[j] = mine ? ti[j] : oi[KM - 1 - j];
+    }
+#pragma unroll
+    for (int d = KM / 2; d >= 1; d >>= 1)
+#pragma unroll
+      for (int j = 0; j < KM; ++j)
+        if ((j & d) == 0) {
+          const bool keep = key_beats(tv[j], ti[j], tv[j + d], ti[j + d]);
+          const float hv = keep ? tv[j] : tv[j + d], lv = keep ? tv[j + d] : tv[j];
+          const int hi = keep ? ti[j] : ti[j + d], li = keep ? ti[j + d] : ti[j];
+          tv[j] = hv; ti[j] = hi;
+          tv[j + d] = lv; ti[j + d] = li;
+        }
+  }
+  if (p != 0) return;
+  float ex[KM], denom = 0.f;
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
     ex[j] = j < k ? expf(tv[j] - tv[0]) : 0.f;
     denom += ex[j];
   }
 #pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
+  for (int j = 0; j < KM; ++j) {
     if (j < k) {
       idx_out[j] = ti[j];
       w_out[j] = ex[j] / denom;
@@ -364,10 +406,16 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
   }
   __syncthreads();
   if (E > 16) {
-    // top-k: one token per thread, its logits scanned from LDS (the odd row
-    // pitch keeps the threads of a wave on distinct banks)
-    if (tid < TB && t0 + tid < T)
-      topk_scan(part[0][tid], E, k, idx + (long)(t0 + tid) * k, w + (long)(t0 + tid) * k);
+    // top-k: the block's 256 lanes, P per token, logits read from LDS
+    constexpr int P = 256 / TB;
+    const int tt = tid / P, p = tid % P, t = t0 + tt;
+    if (t < T) {  // (whole P-lane groups: T bounds tokens, P divides 64)
+      int32_t* io = idx + (long)t * k;
+      float* wo = w + (long)t * k;
+      if (k <= 2) topk_lanes<2, P>(part[0][tt], E, k, p, io, wo);
+      else if (k <= 4) topk_lanes<4, P>(part[0][tt], E, k, p, io, wo);
+      else topk_lanes<8, P>(part[0][tt], E, k, p, io, wo);
+    }
   } else {
     // top-k: segments of EP <= 16 lanes, one token per segment per round
     const int G = 64 / EP;

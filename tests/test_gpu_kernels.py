@@ -114,7 +114,7 @@ def test_route_ties_and_signed_zeros():
             assert list(host(idx)[5]) == list(range(k))
 
 
-def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t):
+def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t, with_ws=False):
     d = dev()
     s = _shape(T, M, 8, E, k, C, "bf16" if x_t.dtype == torch.bfloat16 else "f32", layout=layout)
     rows = L.flowmoe_rows_capacity(s)
@@ -125,7 +125,12 @@ def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t):
     load = torch.full((E,), -7, dtype=torch.int32, device=d)
     x_disp = torch.full((max(rows, 1), M), 3.0, dtype=x_t.dtype, device=d)
     idx_t = torch.from_numpy(idx_np.astype(np.int32)).to(d)
-    L.flowmoe_dispatch(s, idx_t, x_t, counts, offsets, slot, row_src, load, x_disp)
+    ws, nws = None, 0
+    if with_ws:  # the tile-histogram scan (more than 16 tiles of 1024 assignments)
+        nws = L.flowmoe_workspace_bytes(s, L.WS_DISPATCH)
+        assert (nws > 0) == (T * k > 16 * 1024)
+        ws = torch.full((max(nws, 1),), 0x5A, dtype=torch.uint8, device=d)
+    L.flowmoe_dispatch(s, idx_t, x_t, counts, offsets, slot, row_src, load, x_disp, ws, nws)
     torch.cuda.synchronize()
     return dict(counts=host(counts), offsets=host(offsets), slot=host(slot[:T * k]).reshape(T, k),
                 row_src=host(row_src[:rows]), load=host(load), x_disp=x_disp[:rows], rows=rows)
@@ -136,6 +141,8 @@ def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t):
     (1, 1, 1, 1.0), (1, 4, 2, 1.0), (37, 1, 1, 1.0), (100, 4, 4, 1.0), (300, 8, 2, 1.2),
     (1000, 16, 1, 1.0), (2048, 64, 6, 1.5), (777, 7, 3, 0.3), (5000, 8, 2, 1.25),
     (13000, 4, 4, 1.1),  # T*k = 52000: more assignments than the scan stages in LDS
+    (16384, 8, 1, 1.0), (16385, 8, 1, 1.0),  # 16 tiles; 17 with a one-assignment tail
+    (20000, 64, 2, 1.1), (40000, 16, 3, 0.8),
 ])
 def test_dispatch(T, E, k, cf, layout):
     need_gpu()
@@ -150,6 +157,11 @@ def test_dispatch(T, E, k, cf, layout):
     for C in sorted({0, 1, oracle.capacity(T, E, k, cf), T * k}):
         g = _run_dispatch(T, M, E, k, C, layout, idx, x_t)
         ref = oracle.route(idx, E, C, layout)
+        if T * k > 16 * 1024:  # both scans: the same integers
+            h = _run_dispatch(T, M, E, k, C, layout, idx, x_t, with_ws=True)
+            for key in ("counts", "offsets", "slot", "load", "row_src"):
+                assert np.array_equal(h[key], g[key]), (key, C)
+            assert torch.equal(h["x_disp"], g["x_disp"]), C
         assert np.array_equal(g["counts"], ref["counts"]), C
         assert np.array_equal(g["offsets"], ref["offsets"]), C
         assert np.array_equal(g["slot"], ref["slot"]), C
