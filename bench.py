@@ -59,13 +59,15 @@ def gemm_flops_per_launch(cfg, kept: int) -> float:
     return 2.0 * kept * cfg.M * cfg.H
 
 
-def memory_bound(L, layer, cfg, torch, reps: int = 20):
+def memory_bound(L, layer, cfg, torch, reps: int = 20, flush=None):
     """Achieved bandwidth of the memory-bound steps of chunk 0: each C-ABI call
     repeated `reps` times back to back on one stream (inputs warm: after the
     timed steps, and small enough here to stay in the 256 MB Infinity Cache),
     against the algorithmic bytes of the step (kept rows A of the chunk):
       gate T*M*b; dispatch (scan + gather) (T + A)*M*b; combine (A + T)*M*b;
-      combine bwd (T + 2A)*M*b; dispatch bwd (A + T)*M*b; gate bwd T*M*b."""
+      combine bwd (T + 2A)*M*b; dispatch bwd (A + T)*M*b; gate bwd T*M*b.
+    With a `flush` buffer (int64, >= 512 MiB) each step is also timed with
+    cold caches (the *_flushed figures)."""
     s = layer.shape
     T, M, E, k = s.T, s.M, s.E, s.k
     b = 2 if layer.dt == L.BF16 else 4
@@ -94,6 +96,7 @@ def memory_bound(L, layer, cfg, torch, reps: int = 20):
                                             stream=st), T * M * b),
     }
     out = {}
+    flush_sum = torch.zeros((), dtype=torch.int64, device=x.device)
     for name, (fn, nbytes) in steps.items():
         fn()
         fn()
@@ -107,6 +110,28 @@ def memory_bound(L, layer, cfg, torch, reps: int = 20):
         gbs = nbytes / (us * 1e-6) / 1e9
         out[name] = {"bytes": nbytes, "us": round(us, 2), "GBps": round(gbs, 1),
                      "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        if flush is not None:
+            # cold caches: reading a 512 MiB buffer before every call evicts
+            # the inputs from L2 and the Infinity Cache and leaves only clean
+            # lines behind (a fill would leave dirty lines whose write-back
+            # the measured call would pay for); the call's time is that of
+            # (read + call) minus that of the read alone, both back to back
+            def span(with_call):
+                f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                with torch.cuda.stream(st):
+                    f0.record(st)
+                    for _ in range(reps):
+                        flush_sum.copy_(flush.sum())
+                        if with_call:
+                            fn()
+                    f1.record(st)
+                f1.synchronize()
+                return f0.elapsed_time(f1) / reps * 1e3
+            span(True)
+            cold = span(True) - span(False)
+            cgbs = nbytes / (cold * 1e-6) / 1e9
+            out[name].update({"us_flushed": round(cold, 2), "GBps_flushed": round(cgbs, 1),
+                              "frac_flushed": round(cgbs / PEAK_HBM_GBS, 4)})
     return out
 
 
@@ -218,7 +243,11 @@ def main():
     avg_launch_ms = sum(gemm_ms) / max(1, len(gemm_ms))
     achieved_tflops = tot_flops / tot_s / 1e12 if tot_s > 0 else 0.0
 
-    mem = None if a.no_memory_bound else memory_bound(L, layer, cfg, torch)
+    mem = None
+    if not a.no_memory_bound:
+        flush = torch.ones(64 << 20, dtype=torch.int64, device=dev)  # 512 MiB
+        mem = memory_bound(L, layer, cfg, torch, flush=flush)
+        del flush
 
     if a.copy_probe > 0:
         n = a.copy_probe * 2**20 // 4

@@ -22,143 +22,117 @@ __host__ __device__ inline int pow2_at_least(int e) {
   return p;
 }
 
-// Segmented argmax across EP lanes. Larger value wins; equal values go to the
-// smaller index.
-__device__ __forceinline__ void seg_argmax(float& v, int& i, int EP) {
-  for (int off = EP >> 1; off > 0; off >>= 1) {
-    float ov = __shfl_xor(v, off, 64);
-    int oi = __shfl_xor(i, off, 64);
-    if (ov > v || (ov == v && oi < i)) {
-      v = ov;
-      i = oi;
-    }
-  }
+// Selection key of (logit v, expert e): a larger key comes first in the
+// order (larger value; equal values by the lower index; -0.0 == +0.0). The
+// value's bits map monotonically onto an unsigned word (negative values:
+// every bit flipped; others: the sign bit set), -0.0 taken as +0.0; the low
+// word is 2^32 - 1 - e. Key 0 is below every logit (an empty slot or a lane
+// past E); keys of one token's logits are distinct.
+__device__ __forceinline__ uint64_t sel_key(float v, int e) {
+  uint32_t b = __float_as_uint(v);
+  b = (b == 0x80000000u) ? 0u : b;
+  const uint32_t m = (b & 0x80000000u) ? 0xFFFFFFFFu : 0x80000000u;
+  return ((uint64_t)(b ^ m) << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)e);
+}
+__device__ __forceinline__ float key_value(uint64_t key) {
+  const uint32_t s = (uint32_t)(key >> 32);
+  return __uint_as_float((s & 0x80000000u) ? (s ^ 0x80000000u) : ~s);
+}
+__device__ __forceinline__ int key_index(uint64_t key) {
+  return (int)(0xFFFFFFFFu - (uint32_t)key);
+}
+__device__ __forceinline__ uint64_t shfl_xor_key(uint64_t key, int m) {
+  const uint32_t lo = __shfl_xor((uint32_t)key, m), hi = __shfl_xor((uint32_t)(key >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-// Select the top-k of one token's logits held one per lane (lane expert e,
-// invalid lanes pass valid=false), then write idx/w. All EP lanes of the
-// segment take part; the first k lanes write.
-__device__ __forceinline__ void topk_write(float logit, int e, bool valid, int EP, int k,
-                                           int32_t* idx_out, float* w_out) {
-  float top_v[kMaxK];
-  int top_i[kMaxK];
-  float mine = valid ? logit : -INFINITY;
-  int my_i = valid ? e : (1 << 20) + e;
-#pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
-    if (j < k) {
-      float v = mine;
-      int i = my_i;
-      seg_argmax(v, i, EP);
-      top_v[j] = v;
-      top_i[j] = i;
-      if (i == my_i) {  // this lane was selected: remove it
-        mine = -INFINITY;
-        my_i = (1 << 21) + e;
-      }
-    }
-  }
-  // softmax over the k selected logits, shifted by the largest
-  float denom = 0.f;
-  float ex[kMaxK];
-#pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
-    if (j < k) {
-      ex[j] = expf(top_v[j] - top_v[0]);
-      denom += ex[j];
-    }
-  }
-  const int lane_in_seg = e;
-#pragma unroll
-  for (int j = 0; j < kMaxK; ++j) {
-    if (j < k && lane_in_seg == j) {
-      idx_out[j] = top_i[j];
-      w_out[j] = ex[j] / denom;
-    }
-  }
-}
-
-// Top-k of one token's E logits by P consecutive lanes (P a power of two
-// <= 64). Order: larger value first, equal values by lower index, -0.0 ==
-// +0.0 (IEEE compare); an empty slot is (-inf, 2^30), below every logit.
-// Lane p keeps a sorted list of the KM best of logits p, p + P, ... (an
-// insertion without branches); then log2(P) exchanges with lane p ^ m merge
-// two sorted lists: the better of a[j] and b[KM - 1 - j] for every j gives
-// the KM best of both as a bitonic sequence, which half-cleaners sort. Every
-// lane ends with the same list; lane p == 0 writes the k selected and their
-// softmax, shifted by the largest.
-__device__ __forceinline__ bool key_beats(float v, int i, float tv, int ti) {
-  return (v > tv) | ((v == tv) & (i < ti));
-}
-
+// the k selected (keys in order) -> idx and the softmax over their logits,
+// shifted by the largest; lane `writer` of the group writes
 template <int KM>
-__device__ __forceinline__ void topk_insert(float v, int i, float (&tv)[KM], int (&ti)[KM]) {
-  bool b[KM];
-#pragma unroll
-  for (int j = 0; j < KM; ++j) b[j] = key_beats(v, i, tv[j], ti[j]);
-#pragma unroll
-  for (int j = KM - 1; j >= 1; --j) {  // b is monotone: b[j - 1] implies b[j]
-    const float nv = b[j - 1] ? tv[j - 1] : v;
-    const int ni = b[j - 1] ? ti[j - 1] : i;
-    tv[j] = b[j] ? nv : tv[j];
-    ti[j] = b[j] ? ni : ti[j];
-  }
-  tv[0] = b[0] ? v : tv[0];
-  ti[0] = b[0] ? i : ti[0];
-}
-
-template <int KM, int P>
-__device__ __forceinline__ void topk_lanes(const float* logit, int E, int k, int p,
-                                           int32_t* idx_out, float* w_out) {
-  float tv[KM];
-  int ti[KM];
-#pragma unroll
-  for (int j = 0; j < KM; ++j) {
-    tv[j] = -INFINITY;
-    ti[j] = 1 << 30;
-  }
-  for (int e = p; e < E; e += P) topk_insert<KM>(logit[e], e, tv, ti);
-#pragma unroll
-  for (int m = 1; m < P; m <<= 1) {
-    float ov[KM];
-    int oi[KM];
-#pragma unroll
-    for (int j = 0; j < KM; ++j) {
-      ov[j] = __shfl_xor(tv[j], m);
-      oi[j] = __shfl_xor(ti[j], m);
-    }
-#pragma unroll
-    for (int j = 0; j < KM; ++j) {
-      const bool mine = key_beats(tv[j], ti[j], ov[KM - 1 - j], oi[KM - 1 - j]);
-      tv[j] = mine ? tv[j] : ov[KM - 1 - j];
-      ti[j] = mine ? ti[j] : oi[KM - 1 - j];
-    }
-#pragma unroll
-    for (int d = KM / 2; d >= 1; d >>= 1)
-#pragma unroll
-      for (int j = 0; j < KM; ++j)
-        if ((j & d) == 0) {
-          const bool keep = key_beats(tv[j], ti[j], tv[j + d], ti[j + d]);
-          const float hv = keep ? tv[j] : tv[j + d], lv = keep ? tv[j + d] : tv[j];
-          const int hi = keep ? ti[j] : ti[j + d], li = keep ? ti[j + d] : ti[j];
-          tv[j] = hv; ti[j] = hi;
-          tv[j + d] = lv; ti[j + d] = li;
-        }
-  }
-  if (p != 0) return;
+__device__ __forceinline__ void topk_store(const uint64_t (&top)[KM], int k, int32_t* idx_out,
+                                           float* w_out) {
   float ex[KM], denom = 0.f;
+  const float v0 = key_value(top[0]);
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    ex[j] = j < k ? expf(tv[j] - tv[0]) : 0.f;
+    ex[j] = j < k ? expf(key_value(top[j]) - v0) : 0.f;
     denom += ex[j];
   }
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     if (j < k) {
-      idx_out[j] = ti[j];
+      idx_out[j] = key_index(top[j]);
       w_out[j] = ex[j] / denom;
     }
   }
+}
+
+// Top-k of one token's logits held one per lane by a segment of EP lanes
+// (lane expert e; lanes past E pass valid = false): k rounds of a butterfly
+// maximum of the keys, the winner's lane dropping out. Lane 0 of the
+// segment writes idx/w.
+__device__ __forceinline__ void topk_write(float logit, int e, bool valid, int EP, int k,
+                                           int32_t* idx_out, float* w_out) {
+  uint64_t top[kMaxK];
+  uint64_t mine = valid ? sel_key(logit, e) : 0ull;
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    uint64_t best = mine;
+    if (j < k) {
+      for (int off = EP >> 1; off > 0; off >>= 1) {
+        const uint64_t o = shfl_xor_key(best, off);
+        best = o > best ? o : best;
+      }
+      mine = (best == mine) ? 0ull : mine;
+    }
+    top[j] = best;
+  }
+  if (e == 0) topk_store<kMaxK>(top, k, idx_out, w_out);
+}
+
+// Top-k of one token's E logits by P consecutive lanes (P a power of two
+// <= 64). Lane p keeps the KM largest keys of logits p, p + P, ... in order
+// (an insertion without branches); then log2(P) exchanges with lane p ^ m
+// merge two sorted lists: the larger of a[j] and b[KM - 1 - j] for every j
+// gives the KM largest of both as a bitonic sequence, which half-cleaners
+// sort. Every lane ends with the same list; lane p == 0 writes.
+template <int KM>
+__device__ __forceinline__ void topk_insert(uint64_t key, uint64_t (&tk)[KM]) {
+  bool b[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) b[j] = key > tk[j];
+#pragma unroll
+  for (int j = KM - 1; j >= 1; --j)  // b is monotone: b[j - 1] implies b[j]
+    tk[j] = b[j] ? (b[j - 1] ? tk[j - 1] : key) : tk[j];
+  tk[0] = b[0] ? key : tk[0];
+}
+
+template <int KM, int P>
+__device__ __forceinline__ void topk_lanes(const float* logit, int E, int k, int p,
+                                           int32_t* idx_out, float* w_out) {
+  uint64_t tk[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) tk[j] = 0ull;
+  for (int e = p; e < E; e += P) topk_insert<KM>(sel_key(logit[e], e), tk);
+#pragma unroll
+  for (int m = 1; m < P; m <<= 1) {
+    uint64_t o[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) o[j] = shfl_xor_key(tk[j], m);
+#pragma unroll
+    for (int j = 0; j < KM; ++j) tk[j] = tk[j] > o[KM - 1 - j] ? tk[j] : o[KM - 1 - j];
+#pragma unroll
+    for (int d = KM / 2; d >= 1; d >>= 1)
+#pragma unroll
+      for (int j = 0; j < KM; ++j)
+        if ((j & d) == 0) {
+          const uint64_t hi = tk[j] > tk[j + d] ? tk[j] : tk[j + d];
+          const uint64_t lo = tk[j] > tk[j + d] ? tk[j + d] : tk[j];
+          tk[j] = hi;
+          tk[j + d] = lo;
+        }
+  }
+  if (p == 0) topk_store<KM>(tk, k, idx_out, w_out);
 }
 
 // Fused gate: per block 4 waves; each wave has G = 64/EP segments, each
@@ -217,26 +191,31 @@ __global__ __launch_bounds__(kGateThreads) void gate_topk_kernel(
 }
 
 // bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16). A block of 4 waves owns TGB
-// groups of 16 tokens; the reduction over M is split between the waves (wave
-// w takes the 32-deep k steps s = w, w + 4, ...), so every wave has its x
-// loads in flight at once. x rows feed the A operand straight from global
-// memory (16 bytes of one row per lane). W_g rows are copied into LDS in
-// chunks of KC rows (rows zero past M) and each lane gathers its B fragment
-// (8 consecutive k of one expert) with 2-byte LDS reads, once per k step for
-// all the block's token groups: a chunk staged serves 16 * TGB tokens (W_g
-// is re-read once per block, so wide gates take more token groups per
-// block). The four partial logit tiles are summed in
-// LDS in wave order (deterministic), the bias added, and each token's top-k
-// taken by a segment of EP lanes (E <= 16) or by one thread (wider gates).
-constexpr int kGateTok = 16;            // tokens per group
-constexpr int kGateWgBytes = 32768;     // LDS for one chunk of W_g rows
-constexpr int kGateBatch = 8;           // x fragments in flight per lane
+// groups of 16 tokens; the reduction over M is split between the waves: wave
+// w takes the 32-deep k steps s = w, w + 4, ... and needs only those steps'
+// W_g rows, so each wave streams on its own, with no block barrier until the
+// partial sums meet. Per step a lane loads 16 bytes of x for each token group
+// (8 consecutive k of one token: the A fragment as it lies in memory) and up
+// to NB 16-byte units of the step's 32 W_g rows; a ring of D steps of these
+// loads stays in flight in registers. The W_g rows of the next step go to
+// the wave's own LDS slice (two slices, alternating), from which each lane
+// gathers its B fragments (8 consecutive k of one expert) with 2-byte reads.
+// Every load is issued from a clamped in-bounds address and its value
+// zeroed when out of range (rows past M, tokens past T, steps past the
+// wave's last), so the ring never leaves registers. The four partial logit
+// tiles are summed in LDS in wave order (deterministic), the bias added, and
+// each token's top-k taken by a segment of EP lanes (E <= 16) or by P = 256 /
+// (16 TGB) lanes per token (wider gates).
+constexpr int kGateTok = 16;  // tokens per group
+constexpr int kGateDepth = 4; // k steps of loads in flight per wave
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
 
-template <int NB, int TGB>  // 16-expert column blocks (E <= 16 * NB), token groups per block
+// NB 16-expert column blocks (E <= 16 NB), TGB token groups per block, VEC:
+// E a multiple of 8 (W_g rows are whole 16-byte units)
+template <int NB, int TGB, bool VEC>
 __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg, const float* __restrict__ bias,
     float* __restrict__ logits, int32_t* __restrict__ idx, float* __restrict__ w, int T, int M,
@@ -244,15 +223,21 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
   constexpr int TB = kGateTok * TGB;           // tokens per block
   constexpr int PW = NB * 16 + 1;              // partial-tile row pitch (floats)
   constexpr int PART_BYTES = 4 * TB * PW * 4;  // the four waves' partial tiles
-  constexpr int SMEM = PART_BYTES > 2 * kGateWgBytes ? PART_BYTES : 2 * kGateWgBytes;
-  constexpr int BS = kGateBatch / TGB;         // k steps per batch of x loads
-  static_assert(BS >= 1, "token groups per block");
-  // two W_g chunk buffers during the k loop, then the partial tiles
+  // W_g slice: 32 rows at a pitch of 16 NB + 8 bf16, so a B fragment's eight
+  // rows are immediate offsets from one address and the lanes of the four k
+  // groups (rows 8 apart) fall on two bank sets instead of one
+  constexpr int PITCH = 16 * NB + 8;
+  constexpr int SLICE = 32 * PITCH + 8;  // bf16 per slice (+ a 16-byte slot for unused lanes)
+  constexpr int SLICE_BYTES = 4 * 2 * SLICE * 2;    // two slices per wave
+  constexpr int SMEM = PART_BYTES > SLICE_BYTES ? PART_BYTES : SLICE_BYTES;
+  constexpr int D = kGateDepth;
+  constexpr int WU = NB;  // 16-byte W_g units per lane per step: 32 rows * E / 8 <= 64 NB
+  typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  bf16_t* wgs = reinterpret_cast<bf16_t*>(smem);
   float(*part)[TB][PW] = reinterpret_cast<float(*)[TB][PW]>(smem);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  bf16_t* slices = reinterpret_cast<bf16_t*>(smem) + wave * 2 * SLICE;
   const int t0 = blockIdx.x * TB;
   const int kq = (lane >> 4) * 8;  // k offset of this lane inside a step
   const bf16_t* xrow[TGB];
@@ -263,12 +248,10 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     arow_ok[g] = arow < T;
     xrow[g] = x + (long)(arow_ok[g] ? arow : 0) * M;
   }
-  // W_g rows in LDS with a pitch of 16 NB + 8 bf16: a B fragment's eight
-  // rows are immediate offsets from one address, and the lanes of the four
-  // k groups (rows 8 apart) fall on two bank sets instead of one
-  constexpr int PITCH = 16 * NB + 8;
-  constexpr int KC = (kGateWgBytes / (2 * PITCH)) / 32 * 32;  // rows per chunk
-  const int nchunks = (M + KC - 1) / KC;
+  const int S = (M + 31) / 32;                       // k steps
+  const int nj = S > wave ? (S - wave + 3) / 4 : 0;  // this wave's steps: s = wave + 4 j
+  const int UR = E / 8;                              // 16-byte units per W_g row
+  const int n16 = 32 * UR;                           // units per step
 
   floatx4_t acc[TGB][NB];
 #pragma unroll
@@ -276,115 +259,105 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[g][nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  // W_g chunks alternate between two LDS buffers. The loads of chunk c + 1
-  // (its W_g rows into registers, this wave's first batch of x fragments)
-  // are issued as chunk c's multiplies start, so their latency overlaps
-  // them; the W_g rows go to the other buffer after the multiplies, and one
-  // barrier per chunk publishes them. Every load is issued, from a clamped
-  // in-bounds address, and values outside the range are zeroed afterwards:
-  // no branch around a load, so the buffers stay in registers.
-  constexpr int WGV = kGateWgBytes / 16 / 256;  // 16-byte W_g units per thread per chunk
-  constexpr int WGE = kGateWgBytes / 2;         // bf16 per chunk buffer
-  typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
-  u32x4_t wtmp[WGV];
-  const bool vec = (E % 8) == 0;  // rows are whole 16-byte units
-  const int UR = E / 8;           // 16-byte units per row
-  auto load_wg = [&](int c) __attribute__((always_inline)) {
-    if (!vec) return;
-    const int k0 = c * KC, kc = min(KC, M - k0);
-    // rows [k0, k0 + kc) of W_g are one contiguous range of kc * E values
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(wg + (long)k0 * E);
-    const int n16 = kc * UR;
+  u32x4_t xr[D][TGB], wr[D][WU];
+  // The wave's j-th step is s = wave + 4 ((j + rot) mod nj): blocks start at
+  // different k steps, so they do not all read the same W_g rows at once (on
+  // 16384 tokens at E = 8 that hot spot made the gate 1.5x slower). Steps
+  // past nj are dead.
+  const int rot = nj > 0 ? (int)(blockIdx.x % (unsigned)nj) : 0;
+  auto step_of = [&](int j) {
+    const int jj = j + rot;
+    return wave + 4 * (jj < nj ? jj : jj - nj);
+  };
+  // rows of W_g in the wave's step j: 0 past the last step
+  auto step_rows = [&](int j) { return j < nj ? min(32, M - step_of(j) * 32) : 0; };
+  // loads of step j into ring slot d. No value is masked here (a select
+  // would wait for the load): x of tokens past T only reaches logits that
+  // are not written, x past M meets W_g rows that are zero in LDS, and the
+  // W_g units past the step's rows are zeroed when staged.
+  auto issue = [&](int d, int j) __attribute__((always_inline)) {
+    const int s = step_of(j);
+    const int kk = s * 32 + kq;
+    const int ko = (j < nj && kk < M) ? kk : 0;
 #pragma unroll
-    for (int i = 0; i < WGV; ++i) {
-      const int q = tid + 256 * i;
-      const u32x4_t v = src[q < n16 ? q : 0];
-      wtmp[i] = q < n16 ? v : u32x4_t{0u, 0u, 0u, 0u};  // rows past the chunk: zero
+    for (int g = 0; g < TGB; ++g) xr[d][g] = *reinterpret_cast<const u32x4_t*>(xrow[g] + ko);
+    // rows [32 s, 32 s + 32) of W_g are one contiguous range of 32 E values
+    // (16-byte aligned: 64 E bytes per step)
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(wg + (j < nj ? (long)s * 32 * E : 0));
+    const int units = step_rows(j) * E / 8;  // whole 16-byte units inside W_g
+#pragma unroll
+    for (int u = 0; u < WU; ++u) {
+      const int q = lane + 64 * u;
+      wr[d][u] = src[q < units ? q : 0];
     }
   };
-  auto store_wg = [&](int c, int buf) __attribute__((always_inline)) {
-    bf16_t* dst = wgs + buf * WGE;
-    if (vec) {
+  // W_g rows of step j into slice b (rows past M zero; columns past E are
+  // never read)
+  auto stage = [&](int d, int j, int b) __attribute__((always_inline)) {
+    bf16_t* dst = slices + b * SLICE;
+    if constexpr (VEC) {
+      const int units = step_rows(j) * UR;
 #pragma unroll
-      for (int i = 0; i < WGV; ++i) {
-        const int q = tid + 256 * i;
-        if (q < KC * UR) {
-          const int r = q / UR, cu = q - r * UR;
-          *reinterpret_cast<u32x4_t*>(dst + r * PITCH + cu * 8) = wtmp[i];
-        }
+      for (int u = 0; u < WU; ++u) {
+        const int q = lane + 64 * u;
+        const int r = q / UR, cu = q - r * UR;
+        // (lanes past the slice's units write the spare slot: no branch)
+        *reinterpret_cast<u32x4_t*>(dst + (q < n16 ? r * PITCH + cu * 8 : 32 * PITCH)) =
+            q < units ? wr[d][u] : u32x4_t{0u, 0u, 0u, 0u};
       }
-    } else {  // element by element (E not a multiple of 8), rows past the chunk zero
-      const int k0 = c * KC, kc = min(KC, M - k0);
-      for (int q = tid; q < KC * E; q += 256) {
+    } else {  // element by element (E not a multiple of 8)
+      const int s = step_of(j);
+      for (int q = lane; q < 32 * E; q += 64) {
         const int r = q / E, e = q - r * E;
-        dst[r * PITCH + e] = r < kc ? wg[(long)(k0 + r) * E + e] : (bf16_t)0;
+        const int row = s * 32 + r;
+        dst[r * PITCH + e] = (j < nj && row < M) ? wg[(long)row * E + e] : (bf16_t)0;
       }
     }
   };
-  uint4 av[BS][TGB], avn[BS][TGB];
-  auto load_x = [&](uint4(&dst)[BS][TGB], int s0, int s_end) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < BS; ++i) {
-      const int kk = (s0 + 4 * i) * 32 + kq;
-      const bool in = s0 + 4 * i < s_end && kk < M;
-#pragma unroll
-      for (int g = 0; g < TGB; ++g) {
-        const uint4 v = *reinterpret_cast<const uint4*>(xrow[g] + (in ? kk : 0));
-        dst[i][g] = (arow_ok[g] && in) ? v : make_uint4(0, 0, 0, 0);
-      }
-    }
+  // (the LDS operations of one wave complete in order; the fence keeps the
+  // compiler from moving a slice's reads above other lanes' writes to it,
+  // or its next writes above the reads)
+  auto lds_fence = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   };
-  auto chunk_end = [&](int c) { return (c * KC + min(KC, M - c * KC) + 31) / 32; };
-  load_wg(0);
-  load_x(av, wave, chunk_end(0));
-  store_wg(0, 0);
-  __syncthreads();
-  for (int c = 0; c < nchunks; ++c) {
-    const int k0 = c * KC;
-    const int s_end = chunk_end(c);  // k steps of this chunk: [k0/32, s_end)
-    const bf16_t* wb = wgs + (c & 1) * WGE;
-    {  // (the last chunk reloads itself: no branch around the loads)
-      const int cn = c + 1 < nchunks ? c + 1 : c;
-      load_wg(cn);
-      load_x(avn, cn * KC / 32 + wave, chunk_end(cn));
-    }
-    for (int s = k0 / 32 + wave; s < s_end; s += 4 * BS) {
+
 #pragma unroll
-      for (int i = 0; i < BS; ++i) {
-        const int si = s + 4 * i;
-        if (si < s_end) {
-          const int r0 = si * 32 - k0 + kq;  // first W_g row of this lane's fragment
+  for (int d = 0; d < D; ++d) issue(d, d);
+  stage(0, 0, 0);
+  lds_fence();
+  // (steps past the wave's last, up to a multiple of D, add exact zeros:
+  // their W_g rows are staged as zeros and their x loads read real x)
+  for (int j0 = 0; j0 < nj; j0 += D) {
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const int e = nb * 16 + (lane & 15);
-            const bf16_t* bp = wb + r0 * PITCH + e;
-            uint32_t u[4];
+    for (int d = 0; d < D; ++d) {
+      const int j = j0 + d;
+      {
+        // next step's W_g rows into the other slice
+        stage((d + 1) % D, j + 1, (d + 1) & 1);
+        const bf16_t* sb = slices + (d & 1) * SLICE;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const uint32_t lo = bp[(2 * q) * PITCH], hi = bp[(2 * q + 1) * PITCH];
-              u[q] = e < E ? lo | (hi << 16) : 0u;  // columns past E were never written
-            }
-            const bf16x8_t b = __builtin_bit_cast(bf16x8_t, make_uint4(u[0], u[1], u[2], u[3]));
+        for (int nb = 0; nb < NB; ++nb) {
+          const int e = nb * 16 + (lane & 15);
+          const bf16_t* bp = sb + kq * PITCH + e;
+          uint32_t u[4];
 #pragma unroll
-            for (int g = 0; g < TGB; ++g)
-              acc[g][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  __builtin_bit_cast(bf16x8_t, av[i][g]), b, acc[g][nb], 0, 0, 0);
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t lo = bp[(2 * q) * PITCH], hi = bp[(2 * q + 1) * PITCH];
+            u[q] = e < E ? lo | (hi << 16) : 0u;  // columns past E were never written
           }
+          const bf16x8_t bfr = __builtin_bit_cast(bf16x8_t, make_uint4(u[0], u[1], u[2], u[3]));
+#pragma unroll
+          for (int g = 0; g < TGB; ++g)
+            acc[g][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, xr[d][g]), bfr, acc[g][nb], 0, 0, 0);
         }
+        issue(d, j + D);
+        lds_fence();
       }
-      if (s + 4 * BS < s_end) load_x(av, s + 4 * BS, s_end);
     }
-    // buffer (c + 1) & 1 was last read by chunk c - 1, before the barrier
-    // that ended it
-    store_wg(c + 1 < nchunks ? c + 1 : c, (c + 1) & 1);
-#pragma unroll
-    for (int i = 0; i < BS; ++i)
-#pragma unroll
-      for (int g = 0; g < TGB; ++g) av[i][g] = avn[i][g];
-    __syncthreads();
   }
-  // (the loop ended with a barrier: the W_g buffers are dead, their LDS
-  // takes the partial tiles)
+  // the slices overlap other waves' partial tiles
+  __syncthreads();
   // acc[g][nb][r]: token g * 16 + (lane / 16) * 4 + r, expert nb * 16 + lane % 16
 #pragma unroll
   for (int g = 0; g < TGB; ++g)
@@ -430,12 +403,15 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
   }
 }
 
-// token groups per block: one W_g staging serves more tokens when W_g is
-// wide or the launch has blocks to spare
+// token groups per block: every block reads all of W_g (from L2), so wide
+// gates take as many tokens per block as still leave a block per CU; narrow
+// ones (E <= 16) stop at two groups, leaving two blocks per CU on long
+// inputs, so that one block's top-k overlaps another's loads
 inline int gate_groups_per_block(int T, int E) {
   const int groups = (T + kGateTok - 1) / kGateTok;
-  if (E > 32 || groups >= 1024) return 4;
-  if (E > 16) return 2;
+  if (E <= 16) return groups >= 1024 ? 2 : 1;
+  if (groups >= 1024) return 4;
+  if (groups >= 512) return 2;
   return 1;
 }
 
@@ -743,10 +719,15 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
     const int TGB = gate_groups_per_block(s.T, s.E);
     const int blocks = (s.T + kGateTok * TGB - 1) / (kGateTok * TGB);
     return traced(FLOWMOE_K_GATE, st, [&] {
-#define FLOWMOE_GATE_LAUNCH(NBV, TGBV)                                                            \
-  hipLaunchKernelGGL((gate_topk_mfma_kernel<NBV, TGBV>), dim3(blocks), dim3(256), 0, st,          \
+#define FLOWMOE_GATE_KERNEL(NBV, TGBV, VECV)                                                      \
+  hipLaunchKernelGGL((gate_topk_mfma_kernel<NBV, TGBV, VECV>), dim3(blocks), dim3(256), 0, st,    \
                      (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M, s.E, \
                      s.k, EP)
+#define FLOWMOE_GATE_LAUNCH(NBV, TGBV)                              \
+  do {                                                              \
+    if (s.E % 8 == 0) FLOWMOE_GATE_KERNEL(NBV, TGBV, true);        \
+    else FLOWMOE_GATE_KERNEL(NBV, TGBV, false);                    \
+  } while (0)
 #define FLOWMOE_GATE_NB(TGBV)                  \
   if (NB == 1) FLOWMOE_GATE_LAUNCH(1, TGBV);   \
   else if (NB == 2) FLOWMOE_GATE_LAUNCH(2, TGBV); \
@@ -757,6 +738,7 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
       else { FLOWMOE_GATE_NB(4) }
 #undef FLOWMOE_GATE_NB
 #undef FLOWMOE_GATE_LAUNCH
+#undef FLOWMOE_GATE_KERNEL
     });
   }
   const int G = 64 / EP;
