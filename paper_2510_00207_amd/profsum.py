@@ -11,6 +11,13 @@
         GEMM's average over its launches is stored with a hash of the kernel
         source, so a later kernel change is detected and the figure dropped.
 
+    python -m paper_2510_00207_amd.profsum mfma DIR --out FILE.md --command "..."
+        MFMA busy share of the expert GEMMs from one PMC pass with
+        SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE: GRBM_GUI_ACTIVE is summed
+        over the 8 XCDs, so a dispatch's cycles are GRBM_GUI_ACTIVE / 8 and its
+        MFMA busy share is SQ_VALU_MFMA_BUSY_CYCLES / (cycles * 1024 SIMDs);
+        the clock is cycles / duration.
+
 Reads CSV files only; runs nothing on the GPU.
 """
 from __future__ import annotations
@@ -117,6 +124,42 @@ def cmd_traffic(a) -> None:
         open(a.md, "w").write("\n".join(lines) + "\n")
 
 
+def cmd_mfma(a) -> None:
+    per = collections.defaultdict(dict)
+    for r in csv.DictReader(open(os.path.join(a.dir, "run_counter_collection.csv"))):
+        d = int(r["Dispatch_Id"])
+        c = per[d]
+        c["name"] = short_name(r["Kernel_Name"])
+        c["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        c[r["Counter_Name"]] = c.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    agg = collections.defaultdict(lambda: [0, 0.0, 0.0, 0.0])  # launches, busy, cycles, ns
+    for c in per.values():
+        if not expert_gemm(c["name"]) or "SQ_VALU_MFMA_BUSY_CYCLES" not in c:
+            continue
+        g = agg[c["name"]]
+        g[0] += 1
+        g[1] += c["SQ_VALU_MFMA_BUSY_CYCLES"]
+        g[2] += c["GRBM_GUI_ACTIVE"] / 8.0
+        g[3] += c["ns"]
+    lines = [f"# {a.title}", "", "Command (repo root on the GPU box, MI355X):", "",
+             f"    {a.command}", "",
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cycles x 1024 SIMDs), cycles = "
+             "GRBM_GUI_ACTIVE / 8 (the counter is summed over the 8 XCDs); clock = cycles / "
+             "duration.", "",
+             "| kernel | launches | avg us | clock GHz | MFMA busy |", "|---|---|---|---|---|"]
+    tb = tc = 0.0
+    for nm, (n, busy, cyc, ns) in sorted(agg.items()):
+        tb += busy
+        tc += cyc
+        lines.append(f"| `{nm}` | {n} | {ns / n / 1e3:.1f} | {cyc / ns:.2f} | "
+                     f"{busy / (cyc * 1024):.3f} |")
+    if tc > 0:
+        lines += ["", f"All expert GEMM launches together: MFMA busy {tb / (tc * 1024):.3f}."]
+    if a.note:
+        lines += ["", a.note]
+    open(a.out, "w").write("\n".join(lines) + "\n")
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -134,8 +177,14 @@ def main() -> None:
     p.add_argument("--md", default="")
     p.add_argument("--title", default="HBM traffic per dispatch")
     p.add_argument("--command", required=True)
+    m = sub.add_parser("mfma")
+    m.add_argument("dir")
+    m.add_argument("--out", required=True)
+    m.add_argument("--title", default="MFMA busy share of the expert GEMMs")
+    m.add_argument("--command", required=True)
+    m.add_argument("--note", default="")
     a = ap.parse_args()
-    cmd_trace(a) if a.cmd == "trace" else cmd_traffic(a)
+    {"trace": cmd_trace, "traffic": cmd_traffic, "mfma": cmd_mfma}[a.cmd](a)
 
 
 if __name__ == "__main__":
