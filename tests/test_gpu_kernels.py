@@ -68,10 +68,16 @@ def test_gate_topk_chunked_weights(T, M, E, k):
     np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
 
 
-@pytest.mark.parametrize("T,M,E,k", [(16368, 64, 8, 2), (16400, 64, 8, 2), (65600, 32, 4, 1)])
+@pytest.mark.parametrize("T,M,E,k", [
+    (16368, 64, 8, 2), (16400, 64, 8, 2), (65600, 32, 4, 1),
+    (9000, 96, 64, 6),    # 563 groups: 2 per block, top-k on 8 lanes per token
+    (16400, 128, 20, 3),  # 4 groups per block, two 16-expert blocks, 4 lanes per token
+    (8200, 64, 40, 8),    # k = 8, three 16-expert blocks
+])
 def test_gate_topk_many_tokens(T, M, E, k):
-    """Both sides of the token count (1024 groups of 16) from which the bf16
-    gate takes 4 groups per block, ragged in the last block."""
+    """Token counts around the group thresholds of the bf16 gate (512 and
+    1024 groups of 16 tokens), ragged in the last block, and the wide-gate
+    top-k at each lane count."""
     need_gpu()
     cfg = get_config("balanced", T=T, M=M, H=8, E=E, k=k, dtype="bf16", seed=T % 97)
     inp = make_inputs(cfg, with_dy=False)
@@ -89,6 +95,37 @@ def test_gate_topk_many_tokens(T, M, E, k):
     ref_i, ref_w = oracle.topk_select(gl, k)
     assert np.array_equal(host(idx), ref_i)
     np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
+
+
+@pytest.mark.parametrize("T,E,k", [(600, 12, 4), (600, 40, 5), (9000, 64, 6), (16400, 24, 3)])
+def test_gate_topk_ties(T, E, k):
+    """Equal logits through the bf16 gate itself: W_g's columns repeat with
+    period 8, so experts e and e + 8 get bit-identical logits (each column is
+    reduced in the same order), and some tokens are all zero (every logit
+    equal to zero). The selection must take the lower index of equal logits
+    on every top-k path (segmented lanes for E <= 16, 16/8/4 lanes per token
+    above)."""
+    need_gpu()
+    M = 64
+    rng = np.random.default_rng(E * 1000 + k)
+    d = dev()
+    x = torch.from_numpy(rng.standard_normal((T, M)).astype(np.float32)).to(d).to(torch.bfloat16)
+    x[::7] = 0
+    base = rng.standard_normal((M, 8)).astype(np.float32) * 0.05
+    wg_np = np.stack([base[:, e % 8] for e in range(E)], axis=1)
+    wg = torch.from_numpy(wg_np).to(d).to(torch.bfloat16)
+    logits = torch.empty(T, E, device=d)
+    idx = torch.empty(T, k, dtype=torch.int32, device=d)
+    w = torch.empty(T, k, device=d)
+    L.flowmoe_gate_topk(_shape(T, M, 8, E, k, 0), x, wg, None, logits, idx, w)
+    torch.cuda.synchronize()
+    gl = host(logits)
+    for e in range(8, E):  # the repeated columns really tie
+        assert np.array_equal(gl[:, e], gl[:, e % 8])
+    ref_i, ref_w = oracle.topk_select(gl, k)
+    assert np.array_equal(host(idx), ref_i)
+    np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
+    assert list(host(idx)[0]) == list(range(k))  # token 0 is all zero
 
 
 def test_route_ties_and_signed_zeros():
