@@ -131,6 +131,25 @@ def test_workspace_checked_before_launch(flowmoe_lib):
     assert ei.value.status == L.ERR_WORKSPACE
 
 
+def test_dispatch_workspace_checked(flowmoe_lib):
+    # 18000 assignments: 18 tiles of 1024, so the scan may use 18 x 8 int32
+    # histograms; a workspace that is given must hold them (null: no histograms)
+    s = L.make_shape(9000, 64, 64, 8, 2, 2250, L.BF16)
+    need = L.flowmoe_workspace_bytes(s, L.WS_DISPATCH)
+    assert need == 768
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_dispatch(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, need - 1,
+                           stream=0)
+    assert ei.value.status == L.ERR_WORKSPACE and "flowmoe_dispatch" in str(ei.value)
+    b = L.LayerBufs()
+    for name in L._LAYER_FIELDS:
+        setattr(b, name, FAKE)
+    b.ws_bytes = need - 256
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_layer_fwd(s, 1, b, s_compute=0, s_comm=0)
+    assert ei.value.status == L.ERR_WORKSPACE and "flowmoe_layer_fwd" in str(ei.value)
+
+
 def test_layer_validation(flowmoe_lib):
     s = L.make_shape(16, 64, 64, 4, 2, 8, L.BF16)
     b = L.LayerBufs()
