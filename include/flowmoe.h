@@ -134,7 +134,7 @@ flowmoe_status_t flowmoe_route(const flowmoe_shape_t* shape, const float* logits
  *   load     E     int32 (out, nullable) demand per expert before the drop
  *   x_disp   rows x M layer dtype (out)
  *   ws       nullable; flowmoe_workspace_bytes(shape, FLOWMOE_WS_DISPATCH)
- *            bytes (0 for T*k <= 16384). With it, inputs of more than 16384
+ *            bytes (0 for T*k <= 1024). With it, inputs of more than 1024
  *            assignments count each 1024-assignment tile's experts once into
  *            the workspace instead of every tile recounting all others;
  *            results are identical. Non-null but too small:

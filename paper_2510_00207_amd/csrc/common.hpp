@@ -140,7 +140,7 @@ constexpr int kMaxK = 8;
 hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, const float* bias,
                             float* logits, int32_t* idx, float* w, hipStream_t st);
 hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float* w, hipStream_t st);
-// dispatch workspace: per-tile expert histograms (0 bytes up to 16 tiles of
+// dispatch workspace: per-tile expert histograms (0 bytes for one tile of
 // 1024 assignments); ws may be null, then the scan recounts every tile
 size_t dispatch_ws_bytes(const Shape& s);
 hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, int32_t* counts,

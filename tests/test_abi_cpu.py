@@ -49,9 +49,11 @@ def test_rows_capacity(flowmoe_lib):
 
 def test_workspace_sizes(flowmoe_lib):
     s = L.make_shape(4096, 1024, 4096, 8, 2, 1229, L.BF16, L.GELU, L.PACKED)
-    assert L.flowmoe_workspace_bytes(s, L.WS_DISPATCH) == 0  # 8 tiles of 1024 assignments
-    # over 16 tiles: one E-wide int32 histogram per tile, 256-byte aligned
-    for T, E, k in [(8193, 8, 2), (20000, 64, 2), (49152, 16, 2)]:
+    # one tile of 1024 assignments: no histograms
+    assert L.flowmoe_workspace_bytes(L.make_shape(512, 1024, 4096, 8, 2, 160, L.BF16, L.GELU,
+                                                  L.PACKED), L.WS_DISPATCH) == 0
+    # more tiles: one E-wide int32 histogram per tile, 256-byte aligned
+    for T, E, k in [(513, 8, 2), (4096, 8, 2), (20000, 64, 2), (49152, 16, 2)]:
         sd = L.make_shape(T, 1024, 4096, E, k, 1229, L.BF16, L.GELU, L.PACKED)
         tiles = -(-T * k // 1024)
         want = -(-tiles * E * 4 // 256) * 256

@@ -163,9 +163,9 @@ def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t, with_ws=False):
     x_disp = torch.full((max(rows, 1), M), 3.0, dtype=x_t.dtype, device=d)
     idx_t = torch.from_numpy(idx_np.astype(np.int32)).to(d)
     ws, nws = None, 0
-    if with_ws:  # the tile-histogram scan (more than 16 tiles of 1024 assignments)
+    if with_ws:  # the tile-histogram scan (more than one tile of 1024 assignments)
         nws = L.flowmoe_workspace_bytes(s, L.WS_DISPATCH)
-        assert (nws > 0) == (T * k > 16 * 1024)
+        assert (nws > 0) == (T * k > 1024)
         ws = torch.full((max(nws, 1),), 0x5A, dtype=torch.uint8, device=d)
     L.flowmoe_dispatch(s, idx_t, x_t, counts, offsets, slot, row_src, load, x_disp, ws, nws)
     torch.cuda.synchronize()
@@ -178,7 +178,8 @@ def _run_dispatch(T, M, E, k, C, layout, idx_np, x_t, with_ws=False):
     (1, 1, 1, 1.0), (1, 4, 2, 1.0), (37, 1, 1, 1.0), (100, 4, 4, 1.0), (300, 8, 2, 1.2),
     (1000, 16, 1, 1.0), (2048, 64, 6, 1.5), (777, 7, 3, 0.3), (5000, 8, 2, 1.25),
     (13000, 4, 4, 1.1),  # T*k = 52000: more assignments than the scan stages in LDS
-    (16384, 8, 1, 1.0), (16385, 8, 1, 1.0),  # 16 tiles; 17 with a one-assignment tail
+    (1024, 8, 1, 1.0), (1025, 8, 1, 1.0),  # one tile; two with a one-assignment tail
+    (16384, 8, 1, 1.0), (16385, 8, 1, 1.0),
     (20000, 64, 2, 1.1), (40000, 16, 3, 0.8),
 ])
 def test_dispatch(T, E, k, cf, layout):
@@ -194,7 +195,7 @@ def test_dispatch(T, E, k, cf, layout):
     for C in sorted({0, 1, oracle.capacity(T, E, k, cf), T * k}):
         g = _run_dispatch(T, M, E, k, C, layout, idx, x_t)
         ref = oracle.route(idx, E, C, layout)
-        if T * k > 16 * 1024:  # both scans: the same integers
+        if T * k > 1024:  # both scans: the same integers
             h = _run_dispatch(T, M, E, k, C, layout, idx, x_t, with_ws=True)
             for key in ("counts", "offsets", "slot", "load", "row_src"):
                 assert np.array_equal(h[key], g[key]), (key, C)
