@@ -285,7 +285,7 @@ typedef struct {
   int32_t* row_src;   /* R x rows */
   int32_t* load;      /* R x E, nullable */
   void* x_disp;       /* R x rows x M */
-  void* h_save;       /* R x rows x H (x2 for SwiGLU) */
+  void* h_save;       /* R x rows x H (x2 for SwiGLU); dH after flowmoe_layer_bwd */
   void* a_save;       /* R x rows x H */
   void* y_disp;       /* R x rows x M */
   void* y;            /* RT x M */
@@ -329,10 +329,17 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
  * (d_logits, dW_g, db) need only C_r's d_topk_w and x, so AT_R..AT_1's share
  * runs on the comm stream right after C_1, while the compute stream is busy
  * with the expert backward; its input gradient dx += d_logits W_g^T is
- * fused into D_r. Weight gradients are summed over chunks in R..1 order.
+ * fused into D_r. E_r computes the chunk's hidden-layer gradient dH and dX,
+ * which D_r needs; the expert weight gradients, which no later task of the
+ * layer needs, run once after E_1 as one GEMM per weight whose reduction
+ * runs over the rows of chunks 1..R in that order (the same sums as R
+ * per-chunk GEMMs, without R read-modify-write passes over the fp32
+ * gradients). dW_g and db are summed over chunks in R..1 order.
+ * bufs->h_save is consumed: each chunk's h_save is overwritten with its dH
+ * (rows x H for GELU, rows x 2H = [dH1 | dH3] for SwiGLU).
  * trace (nullable): 8*R events as for the forward, task 0 = combine bwd,
- * 1 = experts bwd, 2 = dispatch bwd (+ gate dx term), 3 = gate parameter
- * gradients. */
+ * 1 = experts bwd (chunk 1's span also covers the weight gradients),
+ * 2 = dispatch bwd (+ gate dx term), 3 = gate parameter gradients. */
 flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
                                    const flowmoe_layer_bufs_t* bufs, hipStream_t s_compute,
                                    hipStream_t s_comm, hipEvent_t* trace);

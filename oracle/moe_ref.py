@@ -194,10 +194,13 @@ def combine_bwd(dy, y_disp, slot, w):
     return dy_disp, dw
 
 
-def expert_ffn_bwd(dy_disp, x_disp, saved, counts, offsets, w1, w3, w2, act):
+def expert_ffn_bwd(dy_disp, x_disp, saved, counts, offsets, w1, w3, w2, act, return_dh=False):
     """Step 10: per expert, dA = dY W2^T, dW2 = A^T dY, then through the
-    activation, dW1 = X^T dH1 (dW3 = X^T dH3) and dX = dH1 W1^T (+ dH3 W3^T)."""
+    activation, dW1 = X^T dH1 (dW3 = X^T dH3) and dX = dH1 W1^T (+ dH3 W3^T).
+    With return_dh, also the hidden-layer gradient per row: dH1 (GELU) or
+    [dH1 | dH3] (SwiGLU), zero outside the experts' rows."""
     E, M, H = w1.shape
+    dh = np.zeros((x_disp.shape[0], H if act == "gelu" else 2 * H))
     dx_disp = np.zeros_like(x_disp)
     dw1 = np.zeros_like(w1)
     dw3 = np.zeros_like(w1) if act == "swiglu" else None
@@ -214,6 +217,7 @@ def expert_ffn_bwd(dy_disp, x_disp, saved, counts, offsets, w1, w3, w2, act):
             dH1 = dA * gelu_grad(h1)
             dw1[e] = X.T @ dH1
             dx_disp[lo:hi] = dH1 @ w1[e].T
+            dh[lo:hi] = dH1
         else:
             h3 = saved["h3"][lo:hi]
             dH1 = dA * h3 * silu_grad(h1)
@@ -221,6 +225,10 @@ def expert_ffn_bwd(dy_disp, x_disp, saved, counts, offsets, w1, w3, w2, act):
             dw1[e] = X.T @ dH1
             dw3[e] = X.T @ dH3
             dx_disp[lo:hi] = dH1 @ w1[e].T + dH3 @ w3[e].T
+            dh[lo:hi, :H] = dH1
+            dh[lo:hi, H:] = dH3
+    if return_dh:
+        return dx_disp, dw1, dw3, dw2, dh
     return dx_disp, dw1, dw3, dw2
 
 
@@ -270,11 +278,11 @@ def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
     if dy is None:
         return out
     dy_disp, dw = combine_bwd(dy, sv["y_disp"], rt["slot"], w)
-    dx_disp, dw1, dw3, dw2 = expert_ffn_bwd(dy_disp, x_disp, sv, rt["counts"], rt["offsets"],
-                                            w1, w3, w2, act)
+    dx_disp, dw1, dw3, dw2, dh = expert_ffn_bwd(dy_disp, x_disp, sv, rt["counts"], rt["offsets"],
+                                                w1, w3, w2, act, return_dh=True)
     dx = dispatch_bwd(dx_disp, rt["slot"])
     g = gate_bwd(x, w_gate, idx, w, dw)
-    out.update(dy_disp=dy_disp, d_topk_w=dw, dx_disp=dx_disp, dw1=dw1, dw3=dw3, dw2=dw2,
+    out.update(dy_disp=dy_disp, d_topk_w=dw, dx_disp=dx_disp, dh=dh, dw1=dw1, dw3=dw3, dw2=dw2,
                d_logits=g["d_logits"], dw_gate=g["dw_gate"], dbias=g["dbias"],
                dx=dx + g["dx_gate"], dx_experts=dx)
     return out

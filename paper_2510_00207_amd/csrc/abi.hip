@@ -211,9 +211,8 @@ size_t flowmoe_workspace_bytes(const flowmoe_shape_t* shape, int32_t kind) {
     case FLOWMOE_WS_DISPATCH: return dispatch_ws_bytes(s);
     case FLOWMOE_WS_FFN_BWD: return ffn_bwd_ws_bytes(s);
     case FLOWMOE_WS_GATE_BWD: return gate_bwd_ws_bytes(s);
-    case FLOWMOE_WS_LAYER_BWD: {  // disjoint: the gate backward overlaps the expert backward
-      const size_t bwd = align256(ffn_bwd_ws_bytes(s)) + gate_bwd_ws_bytes(s);
-      const size_t fwd = dispatch_ws_bytes(s);  // the forward's dispatch scan
+    case FLOWMOE_WS_LAYER_BWD: {  // the backward's gate partials; the forward's scan histograms
+      const size_t bwd = gate_bwd_ws_bytes(s), fwd = dispatch_ws_bytes(s);
       return bwd > fwd ? bwd : fwd;
     }
     default: return 0;
@@ -610,8 +609,9 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
   // The gate's own gradients (d_logits, dW_g, db) need only the combine
   // backward's d_topk_w, so they run on the comm stream while the expert
   // backward occupies the compute stream; its dx term is fused into the
-  // dispatch backward. Workspace: [expert backward | gate partials].
-  void* ws_gate = static_cast<char*>(b->ws) + align256(ffn_bwd_ws_bytes(s));
+  // dispatch backward. The workspace holds the gate's partials (the expert
+  // backward keeps dH in h_save).
+  void* ws_gate = b->ws;
   // C_R..C_1 (combine backward) on the comm stream
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);
@@ -631,17 +631,22 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
                           ws_gate, s_comm));
     sc.mark(3, r, 1, s_comm);
   }
-  // E_R..E_1 on the compute stream; weight gradients summed in that order
+  // E_R..E_1 on the compute stream: each chunk's dH (written over its h_save)
+  // and dX, which D_r waits for; the weight gradients, which nothing in the
+  // layer waits for, once after E_1 over the rows of all chunks (one GEMM per
+  // weight instead of R read-modify-write passes over the fp32 gradients)
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);
     sc.wait(s_compute, evC[r]);
     sc.mark(1, r, 0, s_compute);
-    sc.run(launch_expert_ffn_bwd(s, c.dy_disp, c.x_disp, c.h_save, c.a_save, c.counts, c.offsets,
-                                 b->w1, b->w3, b->w2, c.dx_disp, b->dw1, b->dw3, b->dw2,
-                                 r != R - 1, b->ws, s_compute));
-    sc.mark(1, r, 1, s_compute);
+    sc.run(launch_expert_ffn_dgrad(s, c.dy_disp, c.h_save, c.counts, c.offsets, b->w1, b->w3,
+                                   b->w2, c.h_save, c.dx_disp, s_compute));
     sc.signal(evE[r], s_compute);
+    if (r > 0) sc.mark(1, r, 1, s_compute);
   }
+  sc.run(launch_expert_ffn_wgrad(s, R, b->dy_disp, b->x_disp, b->a_save, b->h_save, b->counts,
+                                 b->offsets, b->dw1, b->dw3, b->dw2, 0, s_compute));
+  sc.mark(1, 0, 1, s_compute);
   // D_R..D_1 (dispatch backward, plus the gate's dx term) on the comm stream
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);

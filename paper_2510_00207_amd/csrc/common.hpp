@@ -180,6 +180,19 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
                              const int32_t* offsets, const void* w1, const void* w3,
                              const void* w2, void* h_save, void* a_save, void* y_disp,
                              hipStream_t st);
+// input side of the expert backward of one chunk: dH (into dh, which may be
+// h_save itself: each element's pre-activation is read before its gradient
+// is written) and dX
+hipError_t launch_expert_ffn_dgrad(const Shape& s, const void* dy_disp, const void* h_save,
+                                   const int32_t* counts, const int32_t* offsets, const void* w1,
+                                   const void* w3, const void* w2, void* dh, void* dx_disp,
+                                   hipStream_t st);
+// weight gradients summed over R chunks (chunk r's rows at r * rows of each
+// row buffer, its counts and offsets at r * E and r * (E + 1)), one GEMM each
+hipError_t launch_expert_ffn_wgrad(const Shape& s, int R, const void* dy_disp, const void* x_disp,
+                                   const void* a_save, const void* dh, const int32_t* counts,
+                                   const int32_t* offsets, float* dw1, float* dw3, float* dw2,
+                                   int accumulate, hipStream_t st);
 hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void* x_disp,
                                  const void* h_save, const void* a_save, const int32_t* counts,
                                  const int32_t* offsets, const void* w1, const void* w3,

@@ -302,7 +302,7 @@ template <typename TE, bool GATE, int KM>  // KM >= k: size of the per-token arr
 __global__ __launch_bounds__(256) void combine_rows_kernel(
     const TE* __restrict__ src, const int32_t* __restrict__ slot, const float* __restrict__ w,
     TE* __restrict__ y, int T, int M, int k, const int32_t* __restrict__ gidx,
-    const float* __restrict__ gw, const float* __restrict__ gdw, const float* __restrict__ wgt, int E) {
+    const float* __restrict__ gw, const float* __restrict__ gdw, const float* __restrict__ wgt) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = threadIdx.x & 63;
@@ -510,11 +510,11 @@ hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slo
       if (s.dtype == FLOWMOE_BF16)
         hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV>), dim3(blocks), dim3(256), 0, st,
                            (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k, nullptr,
-                           nullptr, nullptr, nullptr, s.E);
+                           nullptr, nullptr, nullptr);
       else
         hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV>), dim3(blocks), dim3(256), 0, st,
                            (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k, nullptr,
-                           nullptr, nullptr, nullptr, s.E);
+                           nullptr, nullptr, nullptr);
     });
   });
 }
@@ -535,11 +535,11 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
       if (s.dtype == FLOWMOE_BF16)
         hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true, KMV>), dim3(blocks), dim3(256), 0, st,
                            (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx, s.T, s.M, s.k, idx, w,
-                           dw, wgt, s.E);
+                           dw, wgt);
       else
         hipLaunchKernelGGL((combine_rows_kernel<float, true, KMV>), dim3(blocks), dim3(256), 0, st,
                            (const float*)dx_disp, slot, nullptr, (float*)dx, s.T, s.M, s.k, idx, w,
-                           dw, wgt, s.E);
+                           dw, wgt);
     });
   });
 }

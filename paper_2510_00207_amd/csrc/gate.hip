@@ -1,11 +1,12 @@
 // Gate (the AT_r gating part of Sec. 2.1 / Sec. 4.2): logits = x W_g (+ b),
 // top-k selection with renormalised softmax weights, and the gate backward.
 //
-// Wavefront layout: experts are spread over a segment of EP lanes (EP = next
-// power of two >= E, E <= 64); a 64-wide wave holds 64/EP segments, each
-// working on its own tokens. Top-k is k rounds of a segmented butterfly
-// argmax on (logit, -index), so ties go to the lower expert index and
-// -0.0 == +0.0 (IEEE compare).
+// Selection order: larger logit first, equal logits by the lower expert
+// index, -0.0 == +0.0; every top-k path compares 64-bit keys that encode
+// exactly this order. The fp32 gate and flowmoe_route spread a token's
+// experts over a segment of EP lanes (EP = next power of two >= E, E <= 64;
+// a 64-wide wave holds 64/EP segments) and take k rounds of a segmented
+// butterfly maximum; the bf16 gate selects in its own epilogue.
 #include <math.h>
 
 #include "common.hpp"

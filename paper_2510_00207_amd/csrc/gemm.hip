@@ -65,6 +65,12 @@ struct GemmParams {
   long ldaux;
   int Hh;            // SwiGLU: H (offset of the second half)
   int accumulate;
+  // KSUM: the reduction runs over nseg row segments (the chunks of a layer
+  // call), in segment order; segment g's rows of expert e are those of
+  // counts[g * E + e] and offsets[g * (E + 1) + e] in A + g * a_sstride and
+  // B0 + g * b_sstride (elements)
+  int nseg;
+  long a_sstride, b_sstride;
 };
 
 // ---------------------------------------------------------------------------
@@ -753,7 +759,7 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   const int n0 = nt * NCOLS;
   const int Kred = (MODE == MODE_ROWS) ? p.K : cnt_e;
   // a padding-only tile (padded layout) has nothing to reduce: zeros
-  const int nk = (MODE == MODE_ROWS && cnt_e <= mt * BM) ? 0 : (Kred + DBK - 1) / DBK;
+  int nk = (MODE == MODE_ROWS && cnt_e <= mt * BM) ? 0 : (Kred + DBK - 1) / DBK;
 
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
   const bf16_t* B0 = static_cast<const bf16_t*>(p.B0);
@@ -821,6 +827,22 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
     b_kstep = DBK * p.ldb * 2;
   }
 
+  // KSUM: bind segment g (g >= 1) of the reduction: the expert's rows in the
+  // g-th chunk's buffers (same per-lane offsets and k steps)
+  auto bind_segment = [&](int g) {
+    if constexpr (MODE == MODE_KSUM) {
+      cnt_e = p.counts[g * p.E + e];
+      row0 = p.offsets[g * (p.E + 1) + e];
+      const bf16_t* Ag = A + g * p.a_sstride;
+      const bf16_t* Bg = B0 + g * p.b_sstride;
+      const int m0 = mt * BM;
+      ra = make_rsrc(Ag + (long)row0 * p.lda + m0, ((long)cnt_e * p.lda - m0) * 2);
+      rb0 = make_rsrc(Bg + (long)row0 * p.ldb + n0, ((long)cnt_e * p.ldb - n0) * 2);
+      rb1 = rb0;
+      nk = (cnt_e + DBK - 1) / DBK;
+    }
+  };
+
   // Loads of k-tile kt into stage `stage`, in two parts: part 0 takes this
   // wave's first ceil(n / 2) of its n blocks of each operand, part 1 the rest.
   auto issue_part = [&](int kt, int stage, int q) {
@@ -862,9 +884,11 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   // landed (s_waitcnt vmcnt) makes the whole tile visible. Tile t's stage is
   // refilled (tile t + NST) only after the barrier that follows every wave's
   // last LDS read of tile t.
+  auto prologue = [&] {
 #pragma unroll
-  for (int s = 0; s < NST; ++s)
-    if (s < nk) issue(s, s);
+    for (int s = 0; s < NST; ++s)
+      if (s < nk) issue(s, s);
+  };
 
   // wait until this wave's loads of tile t have landed, given that the loads
   // of tiles up to min(t + ahead, nk - 1) have been issued
@@ -991,12 +1015,28 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
       mfma_rows(1, 0, FML);
     }
   };
-  // live 32-row fragments of this wave (wave-uniform)
-  const int live = (MODE == MODE_ROWS) ? min(BM, max(0, cnt_e - mt * BM)) : BM;
-  const int fml = __builtin_amdgcn_readfirstlane(min(FM, max(0, (live - wm * WM + 31) / 32)));
-  if (fml > FM / 2) k_loop(IntC<FM>{});
-  else if (fml > 0) k_loop(IntC<FM / 2>{});
-  else k_loop(IntC<0>{});
+  if constexpr (MODE == MODE_KSUM) {
+    // every row of a weight-gradient tile is live; segments one after the
+    // other into the same accumulators, the ring drained between them
+    for (int g = 0; g < p.nseg; ++g) {
+      if (g > 0) {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();  // all LDS reads of the last segment done before the refill
+        bind_segment(g);
+      }
+      prologue();
+      k_loop(IntC<FM>{});
+    }
+  } else {
+    prologue();
+    // live 32-row fragments of this wave (wave-uniform)
+    const int live = min(BM, max(0, cnt_e - mt * BM));
+    const int fml = __builtin_amdgcn_readfirstlane(min(FM, max(0, (live - wm * WM + 31) / 32)));
+    if (fml > FM / 2) k_loop(IntC<FM>{});
+    else if (fml > 0) k_loop(IntC<FM / 2>{});
+    else k_loop(IntC<0>{});
+  }
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();  // all LDS reads done before the epilogue reuses the stages
@@ -1046,49 +1086,59 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
   const float* A = static_cast<const float*>(p.A);
   const float* B0 = static_cast<const float*>(p.B0);
   const float* B1 = static_cast<const float*>(p.B1);
-  const int Kred = (MODE == MODE_ROWS) ? p.K : cnt_e;
   const int ty = tid >> 4, tx = tid & 15;
   float acc[4][4] = {};
-  for (int k0 = 0; k0 < Kred; k0 += TK) {
-    for (int q = tid; q < TK * TB; q += 256) {
-      const int kk = q / TB, ii = q % TB;
-      const int k = k0 + kk;
-      float av = 0.f, bv = 0.f;
-      if (k < Kred) {
-        if constexpr (MODE == MODE_ROWS) {
-          if (mt * TB + ii < cnt_e) av = A[(long)(row0 + ii) * p.lda + k];
-        } else {
-          if (mt * TB + ii < p.Mdim) av = A[(long)(row0 + k) * p.lda + mt * TB + ii];
-        }
-        const int n = n0 + ii;
-        if (n < p.N) {
-          if constexpr (MODE == MODE_KSUM) {
-            bv = B0[(long)(row0 + k) * p.ldb + n];
-          } else if constexpr (B_KC) {
-            bv = (k < p.ksplit) ? B0[(long)e * p.b_estride + (long)n * p.ldb + k]
-                                : B1[(long)e * p.b_estride + (long)n * p.ldb + (k - p.ksplit)];
+  // KSUM: segments (chunks) one after the other into the same accumulators
+  const int nseg = (MODE == MODE_KSUM) ? p.nseg : 1;
+  for (int g = 0; g < nseg; ++g) {
+    if (g > 0) {
+      cnt_e = p.counts[g * p.E + e];
+      row0 = p.offsets[g * (p.E + 1) + e];
+      A = static_cast<const float*>(p.A) + g * p.a_sstride;
+      B0 = static_cast<const float*>(p.B0) + g * p.b_sstride;
+    }
+    const int Kred = (MODE == MODE_ROWS) ? p.K : cnt_e;
+    for (int k0 = 0; k0 < Kred; k0 += TK) {
+      for (int q = tid; q < TK * TB; q += 256) {
+        const int kk = q / TB, ii = q % TB;
+        const int k = k0 + kk;
+        float av = 0.f, bv = 0.f;
+        if (k < Kred) {
+          if constexpr (MODE == MODE_ROWS) {
+            if (mt * TB + ii < cnt_e) av = A[(long)(row0 + ii) * p.lda + k];
           } else {
-            bv = B0[(long)e * p.b_estride + (long)k * p.ldb + n];
+            if (mt * TB + ii < p.Mdim) av = A[(long)(row0 + k) * p.lda + mt * TB + ii];
+          }
+          const int n = n0 + ii;
+          if (n < p.N) {
+            if constexpr (MODE == MODE_KSUM) {
+              bv = B0[(long)(row0 + k) * p.ldb + n];
+            } else if constexpr (B_KC) {
+              bv = (k < p.ksplit) ? B0[(long)e * p.b_estride + (long)n * p.ldb + k]
+                                  : B1[(long)e * p.b_estride + (long)n * p.ldb + (k - p.ksplit)];
+            } else {
+              bv = B0[(long)e * p.b_estride + (long)k * p.ldb + n];
+            }
           }
         }
+        As[kk][ii] = av;
+        Bs[kk][ii] = bv;
       }
-      As[kk][ii] = av;
-      Bs[kk][ii] = bv;
+      __syncthreads();
+#pragma unroll
+      for (int kk = 0; kk < TK; ++kk) {
+        float a[4], b[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
+      }
+      __syncthreads();
     }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < TK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
-    }
-    __syncthreads();
   }
   float* C0 = static_cast<float*>(p.C0);
   float* C1 = static_cast<float*>(p.C1);
@@ -1160,6 +1210,7 @@ GemmParams base_params(const Shape& s, const int32_t* counts, const int32_t* off
   p.ksplit = 1 << 30;
   p.nsplit = 1 << 30;
   p.Hh = s.H;
+  p.nseg = 1;
   return p;
 }
 
@@ -1226,6 +1277,7 @@ hipError_t run_dma(int kind, const Shape& s, GemmParams p, hipStream_t st) {
 // kernel runs.
 template <int MODE, bool A_KC, bool B_KC, int EPI>
 hipError_t run_gemm_bf16(int kind, const Shape& s, GemmParams p, hipStream_t st) {
+  if (MODE == MODE_KSUM && p.nseg < 1) return hipErrorInvalidValue;  // (a launcher bug)
   const bool dma_ok = MODE == MODE_KSUM ||
                       (p.K % DBK == 0 && (p.ksplit >= p.K || p.ksplit % DBK == 0));
   if (dma_ok) return run_dma<MODE, A_KC, B_KC, EPI>(kind, s, p, st);
@@ -1234,6 +1286,7 @@ hipError_t run_gemm_bf16(int kind, const Shape& s, GemmParams p, hipStream_t st)
 
 template <int MODE, bool B_KC, int EPI>
 hipError_t run_f32(int kind, const Shape& s, GemmParams p, hipStream_t st) {
+  if (MODE == MODE_KSUM && p.nseg < 1) return hipErrorInvalidValue;  // (a launcher bug)
   long blocks;
   if (MODE == MODE_ROWS) {
     p.mt_bound = rows_tiles_bound(s, 64);
@@ -1278,6 +1331,7 @@ hipError_t launch_gate_dw_gemm(const void* x, int M, const void* d, int N, const
   p.c_estride = (long)M * N;
   p.nsplit = 1 << 30;
   p.ksplit = 1 << 30;
+  p.nseg = 1;
   return run_gemm_bf16<MODE_KSUM, false, false, EPI_GATE_DW>(FLOWMOE_K_GATE_BWD_DW, s2, p, st);
 }
 
@@ -1344,18 +1398,19 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
   return run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN2, s, q, st);
 }
 
-hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void* x_disp,
-                                 const void* h_save, const void* a_save, const int32_t* counts,
-                                 const int32_t* offsets, const void* w1, const void* w3,
-                                 const void* w2, void* dx_disp, float* dw1, float* dw3,
-                                 float* dw2, int accumulate, void* ws, hipStream_t st) {
+hipError_t launch_expert_ffn_dgrad(const Shape& s, const void* dy_disp, const void* h_save,
+                                   const int32_t* counts, const int32_t* offsets, const void* w1,
+                                   const void* w3, const void* w2, void* dh, void* dx_disp,
+                                   hipStream_t st) {
+  if (s.rows == 0) return hipSuccess;
   const bool swiglu = s.act == FLOWMOE_SWIGLU;
   const bool bf = s.dtype == FLOWMOE_BF16;
   const int H = s.H, M = s.M;
   const int HW = swiglu ? 2 * H : H;
-  void* dH = ws;
-  // 1. dA = dY W2^T, through the activation -> dH (rows x HW)
-  if (s.rows > 0) {
+  // 1. dA = dY W2^T, through the activation -> dH (rows x HW); an element's
+  // pre-activation is read by the lane that then writes its gradient, so dh
+  // may be h_save itself
+  {
     GemmParams p = base_params(s, counts, offsets);
     p.A = dy_disp;
     p.lda = M;
@@ -1364,7 +1419,7 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
     p.B0 = w2;  // B[k=m][n=h] = W2[e][h][m]: K-contiguous
     p.ldb = M;
     p.b_estride = (long)H * M;
-    p.C0 = dH;
+    p.C0 = dh;
     p.ldc = HW;
     p.aux = h_save;
     p.ldaux = HW;
@@ -1380,48 +1435,10 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
         FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_GELU_BWD>(FLOWMOE_K_DGRAD1, s, p, st)));
     }
   }
-  // 2. dW2 = A^T dY  (H x M per expert)
+  // 2. dX = dH1 W1^T (+ dH3 W3^T)
   {
     GemmParams p = base_params(s, counts, offsets);
-    p.A = a_save;
-    p.lda = H;
-    p.Mdim = H;
-    p.B0 = dy_disp;
-    p.ldb = M;
-    p.N = M;
-    p.C0 = dw2;
-    p.ldc = M;
-    p.c_estride = (long)H * M;
-    p.accumulate = accumulate;
-    if (bf)
-      FLOWMOE_TRY((run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(FLOWMOE_K_WGRAD2, s, p, st)));
-    else
-      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD2, s, p, st)));
-  }
-  // 3. [dW1 | dW3] = X^T [dH1 | dH3]  (M x H per expert, each)
-  {
-    GemmParams p = base_params(s, counts, offsets);
-    p.A = x_disp;
-    p.lda = M;
-    p.Mdim = M;
-    p.B0 = dH;
-    p.ldb = HW;
-    p.N = HW;
-    p.C0 = dw1;
-    p.C1 = dw3;
-    p.nsplit = H;
-    p.ldc = H;
-    p.c_estride = (long)M * H;
-    p.accumulate = accumulate;
-    if (bf)
-      FLOWMOE_TRY((run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
-    else
-      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
-  }
-  // 4. dX = dH1 W1^T (+ dH3 W3^T)
-  if (s.rows > 0) {
-    GemmParams p = base_params(s, counts, offsets);
-    p.A = dH;
+    p.A = dh;
     p.lda = HW;
     p.K = HW;
     p.N = M;
@@ -1438,6 +1455,74 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
       FLOWMOE_TRY((run_f32<MODE_ROWS, true, EPI_STORE>(FLOWMOE_K_DGRAD2, s, p, st)));
   }
   return hipSuccess;
+}
+
+hipError_t launch_expert_ffn_wgrad(const Shape& s, int R, const void* dy_disp, const void* x_disp,
+                                   const void* a_save, const void* dh, const int32_t* counts,
+                                   const int32_t* offsets, float* dw1, float* dw3, float* dw2,
+                                   int accumulate, hipStream_t st) {
+  const bool swiglu = s.act == FLOWMOE_SWIGLU;
+  const bool bf = s.dtype == FLOWMOE_BF16;
+  const int H = s.H, M = s.M;
+  const int HW = swiglu ? 2 * H : H;
+  const long rows = s.rows;
+  // 1. dW2 = sum over chunks of A^T dY  (H x M per expert)
+  {
+    GemmParams p = base_params(s, counts, offsets);
+    p.A = a_save;
+    p.lda = H;
+    p.Mdim = H;
+    p.B0 = dy_disp;
+    p.ldb = M;
+    p.N = M;
+    p.C0 = dw2;
+    p.ldc = M;
+    p.c_estride = (long)H * M;
+    p.accumulate = accumulate;
+    p.nseg = R;
+    p.a_sstride = rows * H;
+    p.b_sstride = rows * M;
+    if (bf)
+      FLOWMOE_TRY((run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(FLOWMOE_K_WGRAD2, s, p, st)));
+    else
+      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD2, s, p, st)));
+  }
+  // 2. [dW1 | dW3] = sum over chunks of X^T [dH1 | dH3]  (M x H per expert, each)
+  {
+    GemmParams p = base_params(s, counts, offsets);
+    p.A = x_disp;
+    p.lda = M;
+    p.Mdim = M;
+    p.B0 = dh;
+    p.ldb = HW;
+    p.N = HW;
+    p.C0 = dw1;
+    p.C1 = dw3;
+    p.nsplit = H;
+    p.ldc = H;
+    p.c_estride = (long)M * H;
+    p.accumulate = accumulate;
+    p.nseg = R;
+    p.a_sstride = rows * M;
+    p.b_sstride = rows * HW;
+    if (bf)
+      FLOWMOE_TRY((run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
+    else
+      FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void* x_disp,
+                                 const void* h_save, const void* a_save, const int32_t* counts,
+                                 const int32_t* offsets, const void* w1, const void* w3,
+                                 const void* w2, void* dx_disp, float* dw1, float* dw3,
+                                 float* dw2, int accumulate, void* ws, hipStream_t st) {
+  // dH in the workspace (h_save is left as it is)
+  FLOWMOE_TRY(launch_expert_ffn_dgrad(s, dy_disp, h_save, counts, offsets, w1, w3, w2, ws, dx_disp,
+                                      st));
+  return launch_expert_ffn_wgrad(s, 1, dy_disp, x_disp, a_save, ws, counts, offsets, dw1, dw3, dw2,
+                                 accumulate, st);
 }
 
 }  // namespace flowmoe
