@@ -145,7 +145,10 @@ flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* t
                                   void* x_disp, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Expert FFN (E_r), Sec. 2.1's two feed-forward layers M x H then H x M, on
- * each expert's rows, as one grouped GEMM per layer:
+ * each expert's rows (counts and offsets as flowmoe_dispatch writes them;
+ * they are device data, so they are not checked on the host, but a range
+ * they would take past the rows buffers is cut there), as one grouped GEMM
+ * per layer:
  *   GELU:   h = X W1_e,              a = gelu(h) (exact erf form)
  *   SwiGLU: h1 = X W1_e, h3 = X W3_e, a = silu(h1) * h3
  *   y_disp = a W2_e.

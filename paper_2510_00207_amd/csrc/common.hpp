@@ -174,8 +174,9 @@ void set_gemm_tiles(int tiles);  // FLOWMOE_TILES_*, validated by the caller
 // dW_g partials of the bf16 gate backward: P[s] = X_s^T D_s (fp32, M x N)
 // over token split s (rows offsets[s] .. + counts[s] of x (T x M, bf16) and
 // of d (T x N, bf16)), on the grouped GEMM's weight-gradient path
-hipError_t launch_gate_dw_gemm(const void* x, int M, const void* d, int N, const int32_t* counts,
-                               const int32_t* offsets, int S, float* P, hipStream_t st);
+hipError_t launch_gate_dw_gemm(const void* x, int T, int M, const void* d, int N,
+                               const int32_t* counts, const int32_t* offsets, int S, float* P,
+                               hipStream_t st);
 hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* counts,
                              const int32_t* offsets, const void* w1, const void* w3,
                              const void* w2, void* h_save, void* a_save, void* y_disp,

@@ -865,7 +865,7 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, con
                          g.dlhl, g.Pb, g.counts, g.offsets, s.T, s.E, N / 2, s.k, S, tps);
     });
     if (e != hipSuccess) return e;
-    e = launch_gate_dw_gemm(x, s.M, g.dlhl, N, g.counts, g.offsets, S, g.P, st);
+    e = launch_gate_dw_gemm(x, s.T, s.M, g.dlhl, N, g.counts, g.offsets, S, g.P, st);
     if (e != hipSuccess) return e;
     return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
       hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred), dim3(256), 0, st, g.P, g.Pb,

@@ -71,7 +71,17 @@ struct GemmParams {
   // B0 + g * b_sstride (elements)
   int nseg;
   long a_sstride, b_sstride;
+  // rows of each row buffer (of each segment's): an expert's range
+  // [offsets[e], offsets[e] + rows) is cut at it
+  long rows_cap;
 };
+
+// counts and offsets are device data: a range that inconsistent ones would
+// take past the row buffers is cut there, not followed
+__device__ __forceinline__ int clip_rows(long off, int n, long cap) {
+  if (off < 0 || off >= cap || n <= 0) return 0;
+  return (int)min((long)n, cap - off);
+}
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
@@ -422,6 +432,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
       acc_t += te;
     }
     if (mt < 0) return;
+    rows_e = clip_rows(p.offsets[e], rows_e, p.rows_cap);
+    cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
     row0 = p.offsets[e] + mt * BM;  // first global row of this tile
   } else {
     const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
@@ -429,7 +441,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
     const int rem = vbid % (mtn * ntn);
     mt = rem / ntn;
     nt = rem % ntn;
-    cnt_e = p.counts[e];
+    cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
     row0 = p.offsets[e];
   }
   constexpr int NCOLS = (EPI == EPI_SWIGLU_FWD) ? BN / 2 : BN;  // distinct output columns per tile
@@ -745,6 +757,8 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
   if constexpr (MODE == MODE_ROWS) {
     if (!row_tile_of_block<BM>(p, blockIdx.x, e, mt, nt, rows_e, cnt_e)) return;
+    rows_e = clip_rows(p.offsets[e], rows_e, p.rows_cap);
+    cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
     row0 = p.offsets[e] + mt * BM;
   } else {
     const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
@@ -752,7 +766,7 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
     const int rem = vbid % (mtn * ntn);
     mt = rem / ntn;
     nt = rem % ntn;
-    cnt_e = p.counts[e];
+    cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
     row0 = p.offsets[e];
   }
   constexpr int NCOLS = DUAL ? BN / 2 : BN;
@@ -831,8 +845,8 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   // g-th chunk's buffers (same per-lane offsets and k steps)
   auto bind_segment = [&](int g) {
     if constexpr (MODE == MODE_KSUM) {
-      cnt_e = p.counts[g * p.E + e];
       row0 = p.offsets[g * (p.E + 1) + e];
+      cnt_e = clip_rows(row0, p.counts[g * p.E + e], p.rows_cap);
       const bf16_t* Ag = A + g * p.a_sstride;
       const bf16_t* Bg = B0 + g * p.b_sstride;
       const int m0 = mt * BM;
@@ -1072,6 +1086,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
       acc_t += te;
     }
     if (mt < 0) return;
+    rows_e = clip_rows(p.offsets[e], rows_e, p.rows_cap);
+    cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
     row0 = p.offsets[e] + mt * TB;
   } else {
     const int mtn = (p.Mdim + TB - 1) / TB, ntn = (p.N + TB - 1) / TB;
@@ -1079,7 +1095,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
     const int rem = blockIdx.x % (mtn * ntn);
     mt = rem / ntn;
     nt = rem % ntn;
-    cnt_e = p.counts[e];
+    cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
     row0 = p.offsets[e];
   }
   const int n0 = nt * TB;
@@ -1092,8 +1108,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
   const int nseg = (MODE == MODE_KSUM) ? p.nseg : 1;
   for (int g = 0; g < nseg; ++g) {
     if (g > 0) {
-      cnt_e = p.counts[g * p.E + e];
       row0 = p.offsets[g * (p.E + 1) + e];
+      cnt_e = clip_rows(row0, p.counts[g * p.E + e], p.rows_cap);
       A = static_cast<const float*>(p.A) + g * p.a_sstride;
       B0 = static_cast<const float*>(p.B0) + g * p.b_sstride;
     }
@@ -1183,7 +1199,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 __global__ void swiglu_act_f32_kernel(const float* __restrict__ h, float* __restrict__ a,
                                       const int32_t* __restrict__ offsets, int E, long rows,
                                       int padded, int H) {
-  const long live = padded ? rows : (long)offsets[E];
+  const long live = padded ? rows : min((long)offsets[E], rows);  // (cut at the buffers)
   const long n = live * H;
   for (long q = blockIdx.x * (long)blockDim.x + threadIdx.x; q < n; q += (long)gridDim.x * blockDim.x) {
     const long r = q / H;
@@ -1211,6 +1227,7 @@ GemmParams base_params(const Shape& s, const int32_t* counts, const int32_t* off
   p.nsplit = 1 << 30;
   p.Hh = s.H;
   p.nseg = 1;
+  p.rows_cap = s.rows;
   return p;
 }
 
@@ -1311,8 +1328,9 @@ hipError_t run_f32(int kind, const Shape& s, GemmParams p, hipStream_t st) {
 
 void set_gemm_tiles(int tiles) { g_tiles.store(tiles, std::memory_order_relaxed); }
 
-hipError_t launch_gate_dw_gemm(const void* x, int M, const void* d, int N, const int32_t* counts,
-                               const int32_t* offsets, int S, float* P, hipStream_t st) {
+hipError_t launch_gate_dw_gemm(const void* x, int T, int M, const void* d, int N,
+                               const int32_t* counts, const int32_t* offsets, int S, float* P,
+                               hipStream_t st) {
   Shape s2 = {};
   s2.E = S;
   GemmParams p = {};
@@ -1332,6 +1350,7 @@ hipError_t launch_gate_dw_gemm(const void* x, int M, const void* d, int N, const
   p.nsplit = 1 << 30;
   p.ksplit = 1 << 30;
   p.nseg = 1;
+  p.rows_cap = T;
   return run_gemm_bf16<MODE_KSUM, false, false, EPI_GATE_DW>(FLOWMOE_K_GATE_BWD_DW, s2, p, st);
 }
 
