@@ -9,7 +9,9 @@ notes with its reason):
   * gate = linear M x E map (Sec. 4.2), plus an optional constant bias b;
   * top-k selection by descending logit, ties to the lower expert index, with
     IEEE comparison (-0.0 == +0.0); selected weights are the softmax over the
-    k selected logits (= full softmax renormalised over the selection);
+    k selected logits (= full softmax renormalised over the selection), or,
+    in the Switch-style variant (gate="full"), the selected experts' own
+    probabilities under the softmax over all E logits, not renormalised;
   * C = ceil(f*k*T_r/E) in exact arithmetic on the decimal value of f, per
     chunk of T_r = T/R tokens (gating belongs to each chunk's subtask AT_r);
   * capacity priority: every first choice before any second choice, and
@@ -55,11 +57,16 @@ def gate_logits(x, w_gate, bias=None):
     return l
 
 
-def topk_select(logits, k):
+def topk_select(logits, k, gate="renorm"):
     """Steps 2-3: per token, the k experts with the largest logits (ties go to
-    the lower expert index) in descending order, and their gate weights
-    w_j = exp(l_j - l_0) / sum_j' exp(l_j' - l_0) (softmax of Sec. 2.1
-    renormalised over the selected experts)."""
+    the lower expert index) in descending order, and their gate weights:
+    gate="renorm": w_j = exp(l_j - l_0) / sum_j' exp(l_j' - l_0), the softmax
+    of Sec. 2.1 renormalised over the selected experts;
+    gate="full": w_j = exp(l_j - l_0) / sum_e exp(l_e - l_0), the selected
+    experts' probabilities under the softmax over all E logits (l_0 is the
+    largest logit, so both are shifted by the row maximum)."""
+    if gate not in ("renorm", "full"):
+        raise ValueError(gate)
     T, E = logits.shape
     idx = np.zeros((T, k), dtype=np.int64)
     w = np.zeros((T, k), dtype=np.float64)
@@ -69,7 +76,8 @@ def topk_select(logits, k):
         idx[t] = order
         sel = np.array([row[e] for e in order])
         ex = np.exp(sel - sel[0])
-        w[t] = ex / ex.sum()
+        den = ex.sum() if gate == "renorm" else np.exp(row - sel[0]).sum()
+        w[t] = ex / den
     return idx, w
 
 
@@ -243,15 +251,25 @@ def dispatch_bwd(dx_disp, slot):
     return dx
 
 
-def gate_bwd(x, w_gate, topk_idx, w, dw):
-    """Steps 12-13: softmax-over-selection Jacobian
-    dl_{t,S_j} = w_j (dw_j - sum_j' w_j' dw_j'), zero off the selection; then
-    dW_g = x^T dl, db = sum_t dl_t and the gate's share of dx, dl W_g^T."""
+def gate_bwd(x, w_gate, topk_idx, w, dw, logits=None, gate="renorm"):
+    """Steps 12-13: the Jacobian of the gate weights, with s = sum_j w_j dw_j.
+    gate="renorm" (softmax over the selection): dl_{t,S_j} = w_j (dw_j - s),
+    zero off the selection. gate="full" (w_j = p_{S_j}, p the softmax over
+    all E logits, which ``logits`` gives): dl_{t,e} = p_e (dw_j - s) for
+    e = S_j and -p_e s for every other expert. Then dW_g = x^T dl,
+    db = sum_t dl_t and the gate's share of dx, dl W_g^T."""
     T, k = topk_idx.shape
     E = w_gate.shape[1]
     dl = np.zeros((T, E))
     for t in range(T):
         s = float(w[t] @ dw[t])
+        if gate == "full":
+            row = logits[t]
+            p = np.exp(row - row.max())
+            p /= p.sum()
+            dl[t] = -p * s
+        elif gate != "renorm":
+            raise ValueError(gate)
         for j in range(k):
             dl[t, topk_idx[t, j]] = w[t, j] * (dw[t, j] - s)
     return dict(d_logits=dl, dw_gate=x.T @ dl, dbias=dl.sum(axis=0), dx_gate=dl @ w_gate.T)
@@ -261,7 +279,7 @@ def gate_bwd(x, w_gate, topk_idx, w, dw):
 # one chunk, and the chunked layer (Sec. 3.2 partition; App. H accumulation)
 # ---------------------------------------------------------------------------
 def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
-                logits_for_routing=None):
+                logits_for_routing=None, gate="renorm"):
     """Forward and backward of one chunk. ``logits_for_routing`` (the GPU's
     fp32 logits widened to fp64) replaces the oracle's own logits for
     selection and gate weights, so that floating-point parity is measured
@@ -269,7 +287,7 @@ def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
     E = w_gate.shape[1]
     logits = gate_logits(x, w_gate, bias)
     lr = logits if logits_for_routing is None else logits_for_routing
-    idx, w = topk_select(lr, k)
+    idx, w = topk_select(lr, k, gate)
     rt = route(idx, E, C, layout)
     x_disp = dispatch(x, rt["row_src"], k)
     sv = expert_ffn(x_disp, rt["counts"], rt["offsets"], w1, w3, w2, act)
@@ -281,7 +299,7 @@ def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
     dx_disp, dw1, dw3, dw2, dh = expert_ffn_bwd(dy_disp, x_disp, sv, rt["counts"], rt["offsets"],
                                                 w1, w3, w2, act, return_dh=True)
     dx = dispatch_bwd(dx_disp, rt["slot"])
-    g = gate_bwd(x, w_gate, idx, w, dw)
+    g = gate_bwd(x, w_gate, idx, w, dw, lr, gate)
     out.update(dy_disp=dy_disp, d_topk_w=dw, dx_disp=dx_disp, dh=dh, dw1=dw1, dw3=dw3, dw2=dw2,
                d_logits=g["d_logits"], dw_gate=g["dw_gate"], dbias=g["dbias"],
                dx=dx + g["dx_gate"], dx_experts=dx)
@@ -289,7 +307,7 @@ def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
 
 
 def layer_fwd_bwd(inp, k, f, act, R=1, layout=PACKED, logits_for_routing=None,
-                  C=None):
+                  C=None, gate="renorm"):
     """The layer over T tokens split into R equal contiguous chunks, each an
     independent layer call with its own capacity; per-token outputs are
     concatenated and weight gradients summed over chunks. ``inp`` holds
@@ -308,7 +326,7 @@ def layer_fwd_bwd(inp, k, f, act, R=1, layout=PACKED, logits_for_routing=None,
         lr = None if logits_for_routing is None else logits_for_routing[sl]
         dy = None if inp.get("dy") is None else inp["dy"][sl]
         chunks.append(layer_chunk(x[sl], inp["w_gate"], inp.get("bias"), inp["w1"],
-                                  inp.get("w3"), inp["w2"], dy, k, C, act, layout, lr))
+                                  inp.get("w3"), inp["w2"], dy, k, C, act, layout, lr, gate))
     res = dict(C=C, chunks=chunks)
     for key in ("logits", "topk_idx", "topk_w", "y", "dx", "d_topk_w", "d_logits"):
         if key in chunks[0]:

@@ -244,10 +244,12 @@ def test_k_equals_E_is_dense_softmax_mixture(rng, act):
 # ---------------------------------------------------------------------------
 # gradients: independent torch fp64 autograd of a dense masked formulation
 # ---------------------------------------------------------------------------
-def _torch_layer_grads(inp, k, C, act):
+def _torch_layer_grads(inp, k, C, act, gate="renorm"):
     """Dense masked layer in torch fp64: the selection (torch.topk on
     continuous logits) and the keep mask (brute-force position count) are
-    constants; y_t = sum_e keep_te * softmax_S(l_t)_e * FFN_e(x_t)."""
+    constants; y_t = sum_e keep_te * g_te * FFN_e(x_t) with g = softmax_S(l_t)
+    (softmax over the selected logits) or, gate="full", softmax(l_t) over all
+    experts masked to the selection."""
     t64 = lambda a: None if a is None else torch.tensor(a, dtype=torch.float64, requires_grad=True)
     x, wg, w1, w2 = t64(inp["x"]), t64(inp["w_gate"]), t64(inp["w1"]), t64(inp["w2"])
     w3 = t64(inp["w3"])
@@ -263,8 +265,11 @@ def _torch_layer_grads(inp, k, C, act):
             sel_mask[t, sel[t, j]] = 1
             if pos[t, j] < C:
                 keep[t, sel[t, j]] = 1
-    lm = l.masked_fill(sel_mask == 0, float("-inf"))
-    g = torch.softmax(lm, dim=1) * keep
+    if gate == "full":
+        g = torch.softmax(l, dim=1) * sel_mask * keep
+    else:
+        lm = l.masked_fill(sel_mask == 0, float("-inf"))
+        g = torch.softmax(lm, dim=1) * keep
     y = torch.zeros_like(x)
     for e in range(E):
         h1 = x @ w1[e]
@@ -296,14 +301,15 @@ def _small_inputs(rng, T, M, H, E, act, bias=True):
     )
 
 
+@pytest.mark.parametrize("gate", ["renorm", "full"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
 @pytest.mark.parametrize("f", [0.5, 1.0, 4.0])
-def test_layer_grads_match_torch_autograd(rng, act, layout, f):
+def test_layer_grads_match_torch_autograd(rng, act, layout, f, gate):
     T, M, H, E, k = 24, 8, 12, 4, 2
     inp = _small_inputs(rng, T, M, H, E, act)
-    out = oracle.layer_fwd_bwd(inp, k=k, f=f, act=act, layout=layout)
-    ref = _torch_layer_grads(inp, k, out["C"], act)
+    out = oracle.layer_fwd_bwd(inp, k=k, f=f, act=act, layout=layout, gate=gate)
+    ref = _torch_layer_grads(inp, k, out["C"], act, gate)
     for key in ref:
         np.testing.assert_allclose(out[key], ref[key], rtol=1e-11, atol=1e-12, err_msg=key)
 
@@ -318,18 +324,19 @@ def test_zero_capacity_leaves_only_gate_path(rng):
     assert not out["dx"].any() and not out["dw_gate"].any()
 
 
+@pytest.mark.parametrize("gate", ["renorm", "full"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
-def test_layer_finite_differences(rng, act):
+def test_layer_finite_differences(rng, act, gate):
     T, M, H, E, k = 10, 6, 5, 3, 2
     inp = _small_inputs(rng, T, M, H, E, act)
-    out = oracle.layer_fwd_bwd(inp, k=k, f=1.0, act=act)
+    out = oracle.layer_fwd_bwd(inp, k=k, f=1.0, act=act, gate=gate)
     # routing must be locally constant for the check to hold
     l = out["logits"]
     srt = np.sort(l, axis=1)
     assert np.min(srt[:, -k] - srt[:, -k - 1]) > 1e-3
 
     def loss(mod):
-        o = oracle.layer_fwd_bwd(mod, k=k, f=1.0, act=act, C=out["C"])
+        o = oracle.layer_fwd_bwd(mod, k=k, f=1.0, act=act, C=out["C"], gate=gate)
         return float((o["y"] * inp["dy"]).sum())
 
     h = 1e-6
@@ -344,6 +351,50 @@ def test_layer_finite_differences(rng, act):
             minus[name] = a.copy(); minus[name][ix] -= h
             fd = (loss(plus) - loss(minus)) / (2 * h)
             assert abs(fd - out[gname[name]][ix]) <= 1e-6 * max(1.0, abs(fd)), (name, ix)
+
+
+def test_full_softmax_gate_closed_forms(rng):
+    """gate="full": the selected experts' probabilities under the softmax over
+    all experts. k = E reduces to the renormalised gate; k = 1 gives the
+    largest probability 1 / sum_e exp(l_e - l_max); the weights of k < E
+    experts sum to less than one."""
+    L_ = rng.standard_normal((40, 6))
+    i_full, w_full = oracle.topk_select(L_, 6, "full")
+    i_ren, w_ren = oracle.topk_select(L_, 6)
+    assert np.array_equal(i_full, i_ren)
+    np.testing.assert_allclose(w_full, w_ren, rtol=1e-14)
+    np.testing.assert_allclose(w_full, np.take_along_axis(softmax(L_, axis=1), i_full, 1), rtol=1e-14)
+    _, w1 = oracle.topk_select(L_, 1, "full")
+    np.testing.assert_allclose(w1[:, 0], softmax(L_, axis=1).max(axis=1), rtol=1e-14)
+    _, w3 = oracle.topk_select(L_, 3, "full")
+    assert np.all(w3.sum(axis=1) < 1.0)
+    assert np.all(np.diff(w3, axis=1) <= 0)
+
+
+@pytest.mark.parametrize("gate", ["renorm", "full"])
+def test_gate_jacobian_rows_sum_to_zero(rng, gate):
+    """The gate weights are softmax probabilities (of the selection or of all
+    experts), so shifting every logit of a token changes nothing: each row of
+    d_logits sums to zero."""
+    T, M, E, k = 30, 5, 7, 3
+    x, wg = rng.standard_normal((T, M)), rng.standard_normal((M, E))
+    L_ = x @ wg
+    idx, w = oracle.topk_select(L_, k, gate)
+    dw = rng.standard_normal((T, k))
+    g = oracle.gate_bwd(x, wg, idx, w, dw, L_, gate)
+    np.testing.assert_allclose(g["d_logits"].sum(axis=1), 0.0, atol=1e-14)
+    if gate == "full":  # every expert of every token has a gradient
+        assert np.all(g["d_logits"] != 0.0)
+
+
+def test_top1_full_softmax_gate_has_gradient(rng):
+    """Unlike the renormalised top-1 gate (weight 1, no gradient), the
+    Switch-style gate keeps the router trainable: d_logits = p (dw [e = S] - s)."""
+    T, M, H, E = 20, 8, 6, 4
+    inp = _small_inputs(rng, T, M, H, E, "gelu")
+    out = oracle.layer_fwd_bwd(inp, k=1, f=1.0, act="gelu", gate="full")
+    assert np.all(out["topk_w"] < 1.0)
+    assert out["d_logits"].any() and out["dw_gate"].any()
 
 
 def test_top1_gate_has_no_gradient(rng):
