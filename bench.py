@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--workload", default=WORKLOAD,
                     help="balanced (default) | skewed | large | fine | tiny")
     ap.add_argument("--layout", default="packed")
+    ap.add_argument("--gate", default="renorm", choices=("renorm", "full"),
+                    help="gate weights: softmax over the k selected (renorm) or the selected "
+                         "experts' full-softmax probabilities (full, Switch-style)")
     ap.add_argument("--R", type=int, default=None, help="override the chunk count")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -91,7 +94,7 @@ def memory_bound(L, layer, cfg, torch, reps: int = 20, flush=None):
         "dispatch bwd": (lambda: L.flowmoe_dispatch_bwd(s, dxd, slot, dx, stream=st),
                          (A + T) * M * b),
         "gate bwd (d_logits, dW_g)": (
-            lambda: L.flowmoe_gate_topk_bwd(s, x, layer.w_gate, idx, w, dw, dl, layer.dw_gate,
+            lambda: L.flowmoe_gate_topk_bwd(s, x, layer.w_gate, lg, idx, w, dw, dl, layer.dw_gate,
                                             layer.dbias, None, 0, layer.ws, layer.ws_bytes,
                                             stream=st), T * M * b),
     }
@@ -157,11 +160,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
 
-    cfg = get_config(a.workload)
+    cfg = get_config(a.workload, gate=a.gate)
     R = cfg.R if a.R is None else a.R
     inp = make_inputs(cfg)
     layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
-                     dtype=cfg.dtype, layout=a.layout, bias=cfg.zipf_bias, device=dev)
+                     dtype=cfg.dtype, layout=a.layout, bias=cfg.zipf_bias, gate=cfg.gate,
+                     device=dev)
     for name in ("x", "w_gate", "w1", "w3", "w2", "dy"):
         if inp[name] is not None:
             getattr(layer, name).copy_(to_torch(inp[name], dev))
@@ -310,9 +314,11 @@ def main():
         "config": {
             "workload": (f"{cfg.name} MoE layer: T={cfg.T} M={cfg.M} H={cfg.H} E={cfg.E} "
                          f"top-{cfg.k} f={cfg.f} {cfg.act} {cfg.dtype}, R={R}, {a.layout}, "
-                         f"{'1' if (a.one_stream or R == 1) else '2'} stream(s)"),
+                         f"{'1' if (a.one_stream or R == 1) else '2'} stream(s)"
+                         f"{', full-softmax gate' if cfg.gate == 'full' else ''}"),
             "T": cfg.T, "M": cfg.M, "H": cfg.H, "E": cfg.E, "k": cfg.k, "f": cfg.f,
-            "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "kept_rows": kept,
+            "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "gate": cfg.gate,
+            "kept_rows": kept,
         },
         "roofline": {
             "kernel": "grouped GEMM (gemm_dma_kernel, all 6 launches of a step)",

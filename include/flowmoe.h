@@ -59,6 +59,13 @@ typedef enum {
 enum { FLOWMOE_F32 = 0, FLOWMOE_BF16 = 1 };      /* layer dtype */
 enum { FLOWMOE_GELU = 0, FLOWMOE_SWIGLU = 1 };   /* expert activation */
 enum { FLOWMOE_PACKED = 0, FLOWMOE_PADDED = 1 }; /* dispatch layout */
+/* Gate weights of the k selected experts (Sec. 2.1's softmax gate):
+ * RENORM: the softmax over the k selected logits (the full softmax
+ *         renormalised over the selection; k = 1 gives weight 1);
+ * FULL:   the selected experts' own probabilities under the softmax over all
+ *         E logits, not renormalised (Switch-style: a top-1 router keeps a
+ *         gradient); bf16 layers only. */
+enum { FLOWMOE_GATE_RENORM = 0, FLOWMOE_GATE_FULL = 1 };
 
 /* Shape of one layer call (one chunk of T tokens). */
 typedef struct {
@@ -66,6 +73,7 @@ typedef struct {
   int32_t dtype;  /* FLOWMOE_F32 | FLOWMOE_BF16 */
   int32_t act;    /* FLOWMOE_GELU | FLOWMOE_SWIGLU */
   int32_t layout; /* FLOWMOE_PACKED | FLOWMOE_PADDED */
+  int32_t gate;   /* FLOWMOE_GATE_RENORM (0) | FLOWMOE_GATE_FULL */
 } flowmoe_shape_t;
 
 /* Workspace kinds for flowmoe_workspace_bytes(). */
@@ -101,8 +109,10 @@ size_t flowmoe_workspace_bytes(const flowmoe_shape_t* shape, int32_t kind);
 
 /* Gate: logits = x W_g (+ bias), the linear M x E gate of Sec. 4.2, then per
  * token the k largest logits in descending order (ties to the lower expert
- * index, -0.0 == +0.0) and their weights, the softmax over the k selected
- * logits (the softmax of Sec. 2.1 renormalised over the selection).
+ * index, -0.0 == +0.0) and their weights: the softmax over the k selected
+ * logits (FLOWMOE_GATE_RENORM: the softmax of Sec. 2.1 renormalised over the
+ * selection) or the selected experts' probabilities under the softmax over
+ * all E logits (FLOWMOE_GATE_FULL).
  *   x        T x M  layer dtype
  *   w_gate   M x E  layer dtype
  *   bias     E      float, nullable (constant per-expert logit offset)
@@ -201,19 +211,22 @@ flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void
 flowmoe_status_t flowmoe_dispatch_bwd(const flowmoe_shape_t* shape, const void* dx_disp,
                                       const int32_t* slot, void* dx, hipStream_t stream);
 
-/* Gate backward: the softmax-over-selection Jacobian
- * d_logits[t][S_j] = w_j * (dw_j - sum_j' w_j' dw_j'), zero off the
- * selection; dw_gate = x^T d_logits (M x E float); dbias = column sums of
- * d_logits (E float, nullable). If dx is given, dx += d_logits W_g^T
- * (T x M layer dtype, read-modify-write). accumulate != 0 adds dw_gate and
- * dbias to the existing values (sum over chunks).
+/* Gate backward: the Jacobian of the gate weights, with
+ * s = sum_j w_j dw_j: FLOWMOE_GATE_RENORM d_logits[t][S_j] = w_j (dw_j - s),
+ * zero off the selection; FLOWMOE_GATE_FULL d_logits[t][e] = -p_e s for
+ * every expert (p the softmax of the token's logits, which `logits` gives:
+ * T x E float, required in that mode, unused otherwise), except
+ * w_j (dw_j - s) at e = S_j. dw_gate = x^T d_logits (M x E float);
+ * dbias = column sums of d_logits (E float, nullable). If dx is given,
+ * dx += d_logits W_g^T (T x M layer dtype, read-modify-write). accumulate
+ * != 0 adds dw_gate and dbias to the existing values (sum over chunks).
  *   ws: flowmoe_workspace_bytes(shape, FLOWMOE_WS_GATE_BWD) bytes. */
 flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void* x,
-                                       const void* w_gate, const int32_t* topk_idx,
-                                       const float* topk_w, const float* d_topk_w,
-                                       float* d_logits, float* dw_gate, float* dbias, void* dx,
-                                       int32_t accumulate, void* ws, size_t ws_bytes,
-                                       hipStream_t stream);
+                                       const void* w_gate, const float* logits,
+                                       const int32_t* topk_idx, const float* topk_w,
+                                       const float* d_topk_w, float* d_logits, float* dw_gate,
+                                       float* dbias, void* dx, int32_t accumulate, void* ws,
+                                       size_t ws_bytes, hipStream_t stream);
 
 /* ---- kernel tracing ------------------------------------------------------- */
 

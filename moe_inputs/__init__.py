@@ -64,6 +64,7 @@ class MoEConfig:
     R: int = 1      # token chunks (pipelining degree)
     zipf_bias: bool = False
     seed: int = 0
+    gate: str = "renorm"  # gate weights: "renorm" (softmax over the selection) | "full"
 
     def replace(self, **kw) -> "MoEConfig":
         return dataclasses.replace(self, **kw)

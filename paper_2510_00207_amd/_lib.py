@@ -18,6 +18,7 @@ OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 GELU, SWIGLU = 0, 1
 PACKED, PADDED = 0, 1
+GATE_RENORM, GATE_FULL = 0, 1
 WS_DISPATCH, WS_FFN_BWD, WS_GATE_BWD, WS_LAYER_BWD = 0, 1, 2, 3
 
 _STATUS = {1: "FLOWMOE_ERR_INVALID", 2: "FLOWMOE_ERR_UNSUPPORTED", 3: "FLOWMOE_ERR_HIP",
@@ -31,7 +32,8 @@ class FlowMoEError(RuntimeError):
 
 
 class Shape(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("T", "M", "H", "E", "k", "C", "dtype", "act", "layout")]
+    _fields_ = [(n, ctypes.c_int32)
+                for n in ("T", "M", "H", "E", "k", "C", "dtype", "act", "layout", "gate")]
 
 
 _VP = ctypes.c_void_p
@@ -80,7 +82,7 @@ def load():
         "flowmoe_combine_bwd": ([SP, P, P, P, P, P, P, P, P, P], I32),
         "flowmoe_expert_ffn_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
         "flowmoe_dispatch_bwd": ([SP, P, P, P, P], I32),
-        "flowmoe_gate_topk_bwd": ([SP, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
+        "flowmoe_gate_topk_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
         "flowmoe_trace_start": ([P, P, I32, ctypes.c_uint32], I32),
         "flowmoe_trace_stop": ([], I32),
         "flowmoe_set_gemm_tiles": ([I32], I32),
@@ -118,8 +120,8 @@ def _check(status: int) -> None:
         raise FlowMoEError(status, load().flowmoe_last_error().decode())
 
 
-def make_shape(T, M, H, E, k, C, dtype=BF16, act=GELU, layout=PACKED) -> Shape:
-    return Shape(T, M, H, E, k, C, dtype, act, layout)
+def make_shape(T, M, H, E, k, C, dtype=BF16, act=GELU, layout=PACKED, gate=GATE_RENORM) -> Shape:
+    return Shape(T, M, H, E, k, C, dtype, act, layout, gate)
 
 
 # ---- utilities ---------------------------------------------------------------
@@ -195,12 +197,12 @@ def flowmoe_dispatch_bwd(shape, dx_disp, slot, dx, stream=None):
                                        _stream(stream)))
 
 
-def flowmoe_gate_topk_bwd(shape, x, w_gate, topk_idx, topk_w, d_topk_w, d_logits, dw_gate, dbias,
-                          dx, accumulate, ws, ws_bytes, stream=None):
-    _check(load().flowmoe_gate_topk_bwd(ctypes.byref(shape), ptr(x), ptr(w_gate), ptr(topk_idx),
-                                        ptr(topk_w), ptr(d_topk_w), ptr(d_logits), ptr(dw_gate),
-                                        ptr(dbias), ptr(dx), int(accumulate), ptr(ws), ws_bytes,
-                                        _stream(stream)))
+def flowmoe_gate_topk_bwd(shape, x, w_gate, logits, topk_idx, topk_w, d_topk_w, d_logits, dw_gate,
+                          dbias, dx, accumulate, ws, ws_bytes, stream=None):
+    _check(load().flowmoe_gate_topk_bwd(ctypes.byref(shape), ptr(x), ptr(w_gate), ptr(logits),
+                                        ptr(topk_idx), ptr(topk_w), ptr(d_topk_w), ptr(d_logits),
+                                        ptr(dw_gate), ptr(dbias), ptr(dx), int(accumulate), ptr(ws),
+                                        ws_bytes, _stream(stream)))
 
 
 # ---- kernel tracing --------------------------------------------------------------

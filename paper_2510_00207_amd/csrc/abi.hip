@@ -51,6 +51,11 @@ flowmoe_status_t check_shape(const flowmoe_shape_t* s, int need, Shape* out) {
     return fail(FLOWMOE_ERR_INVALID, "act %d is not FLOWMOE_GELU or FLOWMOE_SWIGLU", s->act);
   if (s->layout != FLOWMOE_PACKED && s->layout != FLOWMOE_PADDED)
     return fail(FLOWMOE_ERR_INVALID, "layout %d is not FLOWMOE_PACKED or FLOWMOE_PADDED", s->layout);
+  if (s->gate != FLOWMOE_GATE_RENORM && s->gate != FLOWMOE_GATE_FULL)
+    return fail(FLOWMOE_ERR_INVALID, "gate %d is not FLOWMOE_GATE_RENORM or FLOWMOE_GATE_FULL",
+                s->gate);
+  if (s->gate == FLOWMOE_GATE_FULL && s->dtype != FLOWMOE_BF16)
+    return fail(FLOWMOE_ERR_UNSUPPORTED, "FLOWMOE_GATE_FULL needs FLOWMOE_BF16 layers");
   if (s->T < 0) return fail(FLOWMOE_ERR_INVALID, "T = %d < 0", s->T);
   if (s->M < 8 || s->M % 8) return fail(FLOWMOE_ERR_INVALID, "M = %d must be a positive multiple of 8", s->M);
   if (s->E < 1) return fail(FLOWMOE_ERR_INVALID, "E = %d < 1", s->E);
@@ -71,6 +76,7 @@ flowmoe_status_t check_shape(const flowmoe_shape_t* s, int need, Shape* out) {
   if (out) {
     out->T = s->T; out->M = s->M; out->H = s->H; out->E = s->E; out->k = s->k;
     out->C = s->C; out->dtype = s->dtype; out->act = s->act; out->layout = s->layout;
+    out->gate = s->gate;
     out->rows = rows;
   }
   return FLOWMOE_OK;
@@ -388,8 +394,9 @@ flowmoe_status_t flowmoe_dispatch_bwd(const flowmoe_shape_t* shape, const void* 
 }
 
 flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void* x,
-                                       const void* w_gate, const int32_t* topk_idx,
-                                       const float* topk_w, const float* d_topk_w,
+                                       const void* w_gate, const float* logits,
+                                       const int32_t* topk_idx, const float* topk_w,
+                                       const float* d_topk_w,
                                        float* d_logits, float* dw_gate, float* dbias, void* dx,
                                        int32_t accumulate, void* ws, size_t ws_bytes,
                                        hipStream_t stream) {
@@ -404,13 +411,14 @@ flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void*
     REQUIRE(topk_w, "topk_w");
     REQUIRE(d_topk_w, "d_topk_w");
     REQUIRE(d_logits, "d_logits");
+    if (s.gate == FLOWMOE_GATE_FULL) REQUIRE(logits, "logits");
   }
   if (dx != nullptr && reinterpret_cast<uintptr_t>(dx) % 16 != 0)
     return fail(FLOWMOE_ERR_INVALID, "dx is not 16-byte aligned");
   st = check_ws(ws, ws_bytes, gate_bwd_ws_bytes(s), "flowmoe_gate_topk_bwd");
   if (st != FLOWMOE_OK) return st;
-  return hip_status(launch_gate_bwd(s, x, w_gate, topk_idx, topk_w, d_topk_w, d_logits, dw_gate,
-                                    dbias, dx, accumulate != 0, ws, stream),
+  return hip_status(launch_gate_bwd(s, x, w_gate, logits, topk_idx, topk_w, d_topk_w, d_logits,
+                                    dw_gate, dbias, dx, accumulate != 0, ws, stream),
                     "flowmoe_gate_topk_bwd");
 }
 
@@ -587,6 +595,7 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     REQUIRE(b->topk_w, "bufs->topk_w"); REQUIRE(b->slot, "bufs->slot");
     REQUIRE(b->d_topk_w, "bufs->d_topk_w"); REQUIRE(b->d_logits, "bufs->d_logits");
     REQUIRE_T(b->dx, "bufs->dx");
+    if (s.gate == FLOWMOE_GATE_FULL) REQUIRE(b->logits, "bufs->logits");
   }
   if (s.rows > 0) {
     REQUIRE_T(b->x_disp, "bufs->x_disp"); REQUIRE_T(b->h_save, "bufs->h_save");
@@ -622,13 +631,21 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     sc.signal(evC[r], s_comm);
   }
   // gate parameter gradients of AT_R..AT_1, summed over chunks in that order;
-  // W_g^T for the dx term first (the gate workspace keeps it at its front)
-  if (s.T > 0) sc.run(launch_gate_wt(s, b->w_gate, ws_gate, s_comm));
+  // W_g^T for the dx term first (the gate workspace keeps it at its front).
+  // The full softmax gate's d_logits is dense: its dx term is a GEMM over
+  // all E experts, run per chunk right after that chunk's d_logits (whose
+  // bf16 copy the next chunk's overwrites) and stored into dx, to which D_r
+  // then adds the experts' part
+  const bool full = s.gate == FLOWMOE_GATE_FULL;
+  if (s.T > 0)
+    sc.run(full ? launch_gate_wstack(s, b->w_gate, ws_gate, s_comm)
+                : launch_gate_wt(s, b->w_gate, ws_gate, s_comm));
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);
     sc.mark(3, r, 0, s_comm);
-    sc.run(launch_gate_dw(s, c.x, c.idx, c.w, c.dw, c.dl, b->dw_gate, b->dbias, r != R - 1,
-                          ws_gate, s_comm));
+    sc.run(launch_gate_dw(s, c.x, c.logits, c.idx, c.w, c.dw, c.dl, b->dw_gate, b->dbias,
+                          r != R - 1, ws_gate, s_comm));
+    if (full) sc.run(launch_gate_dx_full(s, ws_gate, c.dx, false, s_comm));
     sc.mark(3, r, 1, s_comm);
   }
   // E_R..E_1 on the compute stream: each chunk's dH (written over its h_save)
@@ -652,8 +669,9 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     Chunk c = chunk_of(s, b, r);
     sc.wait(s_comm, evE[r]);
     sc.mark(2, r, 0, s_comm);
-    sc.run(launch_dispatch_bwd_gate(s, c.dx_disp, c.slot, c.idx, c.w, c.dw, gate_ws_wgt(ws_gate),
-                                    c.dx, s_comm));
+    sc.run(full ? launch_dispatch_bwd_add(s, c.dx_disp, c.slot, c.dx, s_comm)
+                : launch_dispatch_bwd_gate(s, c.dx_disp, c.slot, c.idx, c.w, c.dw,
+                                           gate_ws_wgt(ws_gate), c.dx, s_comm));
     sc.mark(2, r, 1, s_comm);
   }
   sc.signal(evEnd, s_comm);

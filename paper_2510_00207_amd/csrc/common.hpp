@@ -130,6 +130,7 @@ __device__ __forceinline__ float sigmoid_f(float z) { return __frcp_rn(1.0f + __
 // ---------------------------------------------------------------------------
 struct Shape {
   int T, M, H, E, k, C, dtype, act, layout;
+  int gate;   // FLOWMOE_GATE_RENORM | FLOWMOE_GATE_FULL
   long rows;  // rows capacity of the dispatched buffers
 };
 
@@ -153,22 +154,32 @@ hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp
                               const int32_t* offsets, void* dy_disp, float* dw, hipStream_t st);
 hipError_t launch_dispatch_bwd(const Shape& s, const void* dx_disp, const int32_t* slot, void* dx,
                                hipStream_t st);
+// dx += the dispatch backward (the full softmax gate's layer path)
+hipError_t launch_dispatch_bwd_add(const Shape& s, const void* dx_disp, const int32_t* slot,
+                                   void* dx, hipStream_t st);
 hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const int32_t* slot,
                                     const int32_t* idx, const float* w, const float* dw,
                                     const float* wgt, void* dx, hipStream_t st);
 // gate backward workspace: [W_g^T, float E x M | dW_g partials]
 size_t gate_bwd_ws_bytes(const Shape& s);
 inline const float* gate_ws_wgt(const void* ws) { return static_cast<const float*>(ws); }
-hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, const float* w,
-                          const float* dw, float* d_logits, float* dw_gate, float* dbias,
-                          int accumulate, void* ws, hipStream_t st);
+// logits: needed by the full softmax gate (nullable otherwise)
+hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, const int32_t* idx,
+                          const float* w, const float* dw, float* d_logits, float* dw_gate,
+                          float* dbias, int accumulate, void* ws, hipStream_t st);
 hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, const float* dw,
                           const float* wgt, void* dx, hipStream_t st);
 // W_g (M x E, layer dtype) -> W_g^T (E x M, float) at the front of the gate workspace
 hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st);
-hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const int32_t* idx,
-                           const float* w, const float* dw, float* d_logits, float* dw_gate,
-                           float* dbias, void* dx, int accumulate, void* ws, hipStream_t st);
+hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const float* logits,
+                           const int32_t* idx, const float* w, const float* dw, float* d_logits,
+                           float* dw_gate, float* dbias, void* dx, int accumulate, void* ws,
+                           hipStream_t st);
+// full softmax gate: [W_g^T ; W_g^T] (bf16) into the gate workspace, then the
+// dense dx term of the last launch_gate_dw on that workspace, stored into dx
+// (add = false) or added to it
+hipError_t launch_gate_wstack(const Shape& s, const void* w_gate, void* ws, hipStream_t st);
+hipError_t launch_gate_dx_full(const Shape& s, void* ws, void* dx, bool add, hipStream_t st);
 size_t ffn_bwd_ws_bytes(const Shape& s);
 void set_gemm_tiles(int tiles);  // FLOWMOE_TILES_*, validated by the caller
 // dW_g partials of the bf16 gate backward: P[s] = X_s^T D_s (fp32, M x N)
@@ -177,6 +188,11 @@ void set_gemm_tiles(int tiles);  // FLOWMOE_TILES_*, validated by the caller
 hipError_t launch_gate_dw_gemm(const void* x, int T, int M, const void* d, int N,
                                const int32_t* counts, const int32_t* offsets, int S, float* P,
                                hipStream_t st);
+// dx (T x M, bf16) = or += [hi | lo] (T x K) . wstack (K x M): the gate's
+// dense dx term, the token splits as pseudo-experts sharing one B
+hipError_t launch_gate_dx_gemm(const void* dlhl, int T, int K, const void* wstack, int M,
+                               const int32_t* counts, const int32_t* offsets, int S, void* dx,
+                               bool add, hipStream_t st);
 hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* counts,
                              const int32_t* offsets, const void* w1, const void* w3,
                              const void* w2, void* h_save, void* a_save, void* y_disp,

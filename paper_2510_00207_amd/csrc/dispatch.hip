@@ -298,7 +298,8 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(
 // (dispatch backward of the layer): also adds the gate's share dl_t W_g^T,
 // with dl_t taken from the selection (gidx), its weights (gw) and their
 // gradients (gdw), and W_g^T given transposed in float (wgt, E x M).
-template <typename TE, bool GATE, int KM>  // KM >= k: size of the per-token arrays
+// ADD: y[t] += (the sum) instead of =, the old y loaded with the source rows.
+template <typename TE, bool GATE, int KM, bool ADD = false>  // KM >= k: per-token array size
 __global__ __launch_bounds__(256) void combine_rows_kernel(
     const TE* __restrict__ src, const int32_t* __restrict__ slot, const float* __restrict__ w,
     TE* __restrict__ y, int T, int M, int k, const int32_t* __restrict__ gidx,
@@ -335,6 +336,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
   constexpr int U = sizeof(TE) == 2 ? 2 : 1;
   for (int m0 = lane * 8; m0 < M; m0 += 64 * 8 * U) {
     decltype(raw8_load(src)) raw[U][KM];
+    decltype(raw8_load(src)) yold[ADD ? U : 1];
     Raw8f graw[GATE ? U : 1][GATE ? KM : 1];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -347,6 +349,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
         for (int j = 0; j < KM; ++j)
           if (j < k) graw[u][j] = raw8_load(wgt + (long)ge[j] * M + m);
       }
+      if constexpr (ADD) yold[u] = raw8_load(y + (long)t * M + m);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -373,6 +376,12 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
 #pragma unroll
             for (int q = 0; q < 8; ++q) acc[q] += gl[j] * g[q];
           }
+      }
+      if constexpr (ADD) {
+        float o[8];
+        raw8_f32(yold[u], o);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] += o[q];
       }
       store8(y + (long)t * M + m, acc);
     }
@@ -522,6 +531,25 @@ hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slo
 hipError_t launch_dispatch_bwd(const Shape& s, const void* dx_disp, const int32_t* slot, void* dx,
                                hipStream_t st) {
   return launch_combine(s, dx_disp, slot, nullptr, dx, st);
+}
+
+hipError_t launch_dispatch_bwd_add(const Shape& s, const void* dx_disp, const int32_t* slot,
+                                   void* dx, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const int blocks = (s.T + 3) / 4;
+  return traced(FLOWMOE_K_COMBINE, st, [&] {
+    with_kmax(s.k, [&](auto kc) {
+      constexpr int KMV = decltype(kc)::value;
+      if (s.dtype == FLOWMOE_BF16)
+        hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV, true>), dim3(blocks),
+                           dim3(256), 0, st, (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx,
+                           s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+      else
+        hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV, true>), dim3(blocks),
+                           dim3(256), 0, st, (const float*)dx_disp, slot, nullptr, (float*)dx,
+                           s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+    });
+  });
 }
 
 hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const int32_t* slot,

@@ -47,11 +47,13 @@ __device__ __forceinline__ uint64_t shfl_xor_key(uint64_t key, int m) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// the k selected (keys in order) -> idx and the softmax over their logits,
-// shifted by the largest; lane `writer` of the group writes
+// the k selected (keys in order) -> idx and weights exp(l_j - l_0) / Z,
+// shifted by the largest logit l_0: Z = the sum over the selection (zfull <
+// 0: the renormalised gate) or zfull, the sum over all E experts (the full
+// softmax gate)
 template <int KM>
-__device__ __forceinline__ void topk_store(const uint64_t (&top)[KM], int k, int32_t* idx_out,
-                                           float* w_out) {
+__device__ __forceinline__ void topk_store(const uint64_t (&top)[KM], int k, float zfull,
+                                           int32_t* idx_out, float* w_out) {
   float ex[KM], denom = 0.f;
   const float v0 = key_value(top[0]);
 #pragma unroll
@@ -59,6 +61,7 @@ __device__ __forceinline__ void topk_store(const uint64_t (&top)[KM], int k, int
     ex[j] = j < k ? expf(key_value(top[j]) - v0) : 0.f;
     denom += ex[j];
   }
+  if (zfull >= 0.f) denom = zfull;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     if (j < k) {
@@ -70,10 +73,11 @@ __device__ __forceinline__ void topk_store(const uint64_t (&top)[KM], int k, int
 
 // Top-k of one token's logits held one per lane by a segment of EP lanes
 // (lane expert e; lanes past E pass valid = false): k rounds of a butterfly
-// maximum of the keys, the winner's lane dropping out. Lane 0 of the
-// segment writes idx/w.
+// maximum of the keys, the winner's lane dropping out; with `full`, a
+// butterfly sum of exp(l_e - l_0) over the segment for the full softmax.
+// Lane 0 of the segment writes idx/w.
 __device__ __forceinline__ void topk_write(float logit, int e, bool valid, int EP, int k,
-                                           int32_t* idx_out, float* w_out) {
+                                           bool full, int32_t* idx_out, float* w_out) {
   uint64_t top[kMaxK];
   uint64_t mine = valid ? sel_key(logit, e) : 0ull;
 #pragma unroll
@@ -88,7 +92,12 @@ __device__ __forceinline__ void topk_write(float logit, int e, bool valid, int E
     }
     top[j] = best;
   }
-  if (e == 0) topk_store<kMaxK>(top, k, idx_out, w_out);
+  float z = -1.f;
+  if (full) {  // (uniform)
+    z = valid ? expf(logit - key_value(top[0])) : 0.f;
+    for (int off = EP >> 1; off > 0; off >>= 1) z += __shfl_xor(z, off);
+  }
+  if (e == 0) topk_store<kMaxK>(top, k, z, idx_out, w_out);
 }
 
 // Top-k of one token's E logits by P consecutive lanes (P a power of two
@@ -109,7 +118,7 @@ __device__ __forceinline__ void topk_insert(uint64_t key, uint64_t (&tk)[KM]) {
 }
 
 template <int KM, int P>
-__device__ __forceinline__ void topk_lanes(const float* logit, int E, int k, int p,
+__device__ __forceinline__ void topk_lanes(const float* logit, int E, int k, int p, bool full,
                                            int32_t* idx_out, float* w_out) {
   uint64_t tk[KM];
 #pragma unroll
@@ -133,7 +142,15 @@ __device__ __forceinline__ void topk_lanes(const float* logit, int E, int k, int
           tk[j + d] = lo;
         }
   }
-  if (p == 0) topk_store<KM>(tk, k, idx_out, w_out);
+  float z = -1.f;
+  if (full) {  // the full softmax's sum: each lane its logits, then a butterfly
+    const float v0 = key_value(tk[0]);
+    z = 0.f;
+    for (int e = p; e < E; e += P) z += expf(logit[e] - v0);
+#pragma unroll
+    for (int m = 1; m < P; m <<= 1) z += __shfl_xor(z, m);
+  }
+  if (p == 0) topk_store<KM>(tk, k, z, idx_out, w_out);
 }
 
 // Fused gate: per block 4 waves; each wave has G = 64/EP segments, each
@@ -142,7 +159,7 @@ template <typename TIn>
 __global__ __launch_bounds__(kGateThreads) void gate_topk_kernel(
     const TIn* __restrict__ x, const TIn* __restrict__ wg, const float* __restrict__ bias,
     float* __restrict__ logits, int32_t* __restrict__ idx, float* __restrict__ w, int T, int M,
-    int E, int k, int EP, int TPG, int xchunk) {
+    int E, int k, int EP, int TPG, int xchunk, int full) {
   extern __shared__ float xs[];  // [tokens_per_block][xchunk]
   const int G = 64 / EP;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -185,7 +202,7 @@ __global__ __launch_bounds__(kGateThreads) void gate_topk_kernel(
       if (t < T) {  // uniform across the segment
         float l = acc[i] + b;
         if (evalid) logits[(size_t)t * E + e] = l;
-        topk_write(l, e, evalid, EP, k, idx + (size_t)t * k, w + (size_t)t * k);
+        topk_write(l, e, evalid, EP, k, full, idx + (size_t)t * k, w + (size_t)t * k);
       }
     }
   }
@@ -220,7 +237,7 @@ template <int NB, int TGB, bool VEC>
 __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg, const float* __restrict__ bias,
     float* __restrict__ logits, int32_t* __restrict__ idx, float* __restrict__ w, int T, int M,
-    int E, int k, int EP) {
+    int E, int k, int EP, int full) {
   constexpr int TB = kGateTok * TGB;           // tokens per block
   constexpr int PW = NB * 16 + 1;              // partial-tile row pitch (floats)
   constexpr int PART_BYTES = 4 * TB * PW * 4;  // the four waves' partial tiles
@@ -386,9 +403,9 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     if (t < T) {  // (whole P-lane groups: T bounds tokens, P divides 64)
       int32_t* io = idx + (long)t * k;
       float* wo = w + (long)t * k;
-      if (k <= 2) topk_lanes<2, P>(part[0][tt], E, k, p, io, wo);
-      else if (k <= 4) topk_lanes<4, P>(part[0][tt], E, k, p, io, wo);
-      else topk_lanes<8, P>(part[0][tt], E, k, p, io, wo);
+      if (k <= 2) topk_lanes<2, P>(part[0][tt], E, k, p, full, io, wo);
+      else if (k <= 4) topk_lanes<4, P>(part[0][tt], E, k, p, full, io, wo);
+      else topk_lanes<8, P>(part[0][tt], E, k, p, full, io, wo);
     }
   } else {
     // top-k: segments of EP <= 16 lanes, one token per segment per round
@@ -399,7 +416,7 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
       const int t = t0 + i;
       if (t >= T) break;  // uniform across the segment
       const float l = evalid ? part[0][i][e] : 0.f;
-      topk_write(l, e, evalid, EP, k, idx + (long)t * k, w + (long)t * k);
+      topk_write(l, e, evalid, EP, k, full, idx + (long)t * k, w + (long)t * k);
     }
   }
 }
@@ -419,7 +436,7 @@ inline int gate_groups_per_block(int T, int E) {
 __global__ __launch_bounds__(kGateThreads) void route_kernel(const float* __restrict__ logits,
                                                              int32_t* __restrict__ idx,
                                                              float* __restrict__ w, int T, int E,
-                                                             int k, int EP) {
+                                                             int k, int EP, int full) {
   const int G = 64 / EP;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int seg = lane / EP, e = lane % EP;
@@ -427,7 +444,7 @@ __global__ __launch_bounds__(kGateThreads) void route_kernel(const float* __rest
   if (t >= T) return;  // uniform per segment
   const bool evalid = e < E;
   float l = evalid ? logits[(size_t)t * E + e] : 0.f;
-  topk_write(l, e, evalid, EP, k, idx + (size_t)t * k, w + (size_t)t * k);
+  topk_write(l, e, evalid, EP, k, full, idx + (size_t)t * k, w + (size_t)t * k);
 }
 
 // ---- backward ---------------------------------------------------------------
@@ -601,9 +618,9 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_kernel(
 constexpr int kDlTok = 64;
 __global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
-    float* __restrict__ d_logits, bf16_t* __restrict__ dlhl, float* __restrict__ Pb,
-    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int T, int E, int E4, int k, int S,
-    int tps) {
+    const float* __restrict__ logits, float* __restrict__ d_logits, bf16_t* __restrict__ dlhl,
+    float* __restrict__ Pb, int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int T,
+    int E, int E4, int k, int S, int tps, int full) {
   // dense tile of the block's d_logits rows (odd pitch: column sums and row
   // writes both spread over the banks)
   __shared__ float tile[kDlTok][kMaxE + 1];
@@ -617,9 +634,26 @@ __global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
   }
   __syncthreads();
   if (tid < kDlTok && t0 + tid < T) {
+    const long t = t0 + tid;
     int ij[kMaxK];
     float dl[kMaxK];
-    token_dl(idx, w, dw, t0 + tid, k, ij, dl);
+    token_dl(idx, w, dw, t, k, ij, dl);
+    if (full) {
+      // the full softmax gate: every expert gets -p_e s (p the softmax over
+      // all E logits, shifted by their maximum; s = sum_j w_j dw_j), the
+      // selected ones w_j (dw_j - s) next
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < kMaxK; ++j)
+        if (j < k) s += w[t * k + j] * dw[t * k + j];
+      const float* lr = logits + t * E;
+      float vmax = lr[0];
+      for (int e = 1; e < E; ++e) vmax = fmaxf(vmax, lr[e]);
+      float z = 0.f;
+      for (int e = 0; e < E; ++e) z += expf(lr[e] - vmax);
+      const float f = -s / z;
+      for (int e = 0; e < E; ++e) tile[tid][e] = expf(lr[e] - vmax) * f;
+    }
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j)
       if (j < k) tile[tid][ij[j]] = dl[j];  // the k selected experts are distinct
@@ -639,6 +673,19 @@ __global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
     float v = 0.f;
     for (int tt = 0; tt < kDlTok; ++tt) v += tile[tt][tid];  // rows past T are zero
     Pb[(long)blockIdx.x * E + tid] = v;
+  }
+}
+
+// the full softmax gate's dense dx term takes dx += [hi | lo] B with
+// B = [W_g^T ; W_g^T] (2 E4 x M, bf16; rows e >= E of each half zero)
+__global__ __launch_bounds__(256) void gate_wstack_kernel(const bf16_t* __restrict__ wg,
+                                                          bf16_t* __restrict__ wstack, int M,
+                                                          int E, int E4) {
+  const long n = 2L * E4 * M;
+  for (long q = blockIdx.x * 256L + threadIdx.x; q < n; q += (long)gridDim.x * 256) {
+    const long r = q / M, m = q - r * M;
+    const int e = (int)(r % E4);
+    wstack[q] = e < E ? wg[m * E + e] : (bf16_t)0;
   }
 }
 
@@ -682,6 +729,7 @@ int gate_dw_cols(int E) { return 2 * ((E + 3) / 4 * 4); }
 // register-tile kernel (one launch and a reduce; at these sizes launch
 // latency dominates); the others d_logits, then dW_g as a GEMM
 bool gate_dw_on_gemm(const Shape& s) {
+  if (s.gate == FLOWMOE_GATE_FULL) return true;  // (bf16 only: dense d_logits for the dx GEMM)
   return s.dtype == FLOWMOE_BF16 && (s.E > 16 || (long)s.T * s.M > (8L << 20));
 }
 
@@ -715,6 +763,7 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
                             float* logits, int32_t* idx, float* w, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
   const int EP = pow2_at_least(s.E);
+  const int full = s.gate == FLOWMOE_GATE_FULL;
   if (s.dtype == FLOWMOE_BF16) {
     const int NB = (s.E + 15) / 16;
     const int TGB = gate_groups_per_block(s.T, s.E);
@@ -723,7 +772,7 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
 #define FLOWMOE_GATE_KERNEL(NBV, TGBV, VECV)                                                      \
   hipLaunchKernelGGL((gate_topk_mfma_kernel<NBV, TGBV, VECV>), dim3(blocks), dim3(256), 0, st,    \
                      (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M, s.E, \
-                     s.k, EP)
+                     s.k, EP, full)
 #define FLOWMOE_GATE_LAUNCH(NBV, TGBV)                              \
   do {                                                              \
     if (s.E % 8 == 0) FLOWMOE_GATE_KERNEL(NBV, TGBV, true);        \
@@ -752,7 +801,7 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
   return traced(FLOWMOE_K_GATE, st, [&] {
     hipLaunchKernelGGL(gate_topk_kernel<float>, dim3(blocks), dim3(kGateThreads), lds, st,
                        (const float*)x, (const float*)w_gate, bias, logits, idx, w, s.T, s.M,
-                       s.E, s.k, EP, TPG, xchunk);
+                       s.E, s.k, EP, TPG, xchunk, full);
   });
 }
 
@@ -763,7 +812,7 @@ hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float
   const int blocks = (s.T + per_block - 1) / per_block;
   return traced(FLOWMOE_K_ROUTE, st, [&] {
     hipLaunchKernelGGL(route_kernel, dim3(blocks), dim3(kGateThreads), 0, st, logits, idx, w, s.T,
-                       s.E, s.k, EP);
+                       s.E, s.k, EP, (int)(s.gate == FLOWMOE_GATE_FULL));
   });
 }
 
@@ -779,7 +828,8 @@ struct GateWs {
   bf16_t* dlhl;
   int32_t* counts;
   int32_t* offsets;
-  size_t bytes;  // from the start of the workspace
+  bf16_t* wstack;  // full softmax gate: [W_g^T ; W_g^T] (2 E4 x M) for the dx GEMM
+  size_t bytes;    // from the start of the workspace
 };
 GateWs gate_ws(const Shape& s, void* ws) {
   char* base = static_cast<char*>(ws);
@@ -798,6 +848,8 @@ GateWs gate_ws(const Shape& s, void* ws) {
     g.dlhl = reinterpret_cast<bf16_t*>(take((size_t)s.T * N * sizeof(bf16_t)));
     g.counts = reinterpret_cast<int32_t*>(take((size_t)S * sizeof(int32_t)));
     g.offsets = reinterpret_cast<int32_t*>(take((size_t)S * sizeof(int32_t)));
+    if (s.gate == FLOWMOE_GATE_FULL)
+      g.wstack = reinterpret_cast<bf16_t*>(take((size_t)N * s.M * sizeof(bf16_t)));
   } else {
     const int S = gate_splits(s);
     g.P = reinterpret_cast<float*>(take((size_t)S * s.M * s.E * sizeof(float)));
@@ -809,6 +861,24 @@ GateWs gate_ws(const Shape& s, void* ws) {
 }  // namespace
 
 size_t gate_bwd_ws_bytes(const Shape& s) { return gate_ws(s, nullptr).bytes; }
+
+hipError_t launch_gate_wstack(const Shape& s, const void* w_gate, void* ws, hipStream_t st) {
+  const GateWs g = gate_ws(s, ws);
+  const int E4 = gate_dw_cols(s.E) / 2;
+  const long n = 2L * E4 * s.M;
+  const int nb = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+  return traced(FLOWMOE_K_GATE_BWD_WT, st, [&] {
+    hipLaunchKernelGGL(gate_wstack_kernel, dim3(nb), dim3(256), 0, st, (const bf16_t*)w_gate,
+                       g.wstack, s.M, s.E, E4);
+  });
+}
+
+hipError_t launch_gate_dx_full(const Shape& s, void* ws, void* dx, bool add, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const GateWs g = gate_ws(s, ws);
+  return launch_gate_dx_gemm(g.dlhl, s.T, gate_dw_cols(s.E), g.wstack, s.M, g.counts, g.offsets,
+                             gate_dw_splits(s), dx, add, st);
+}
 
 hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st) {
   float* wgt = static_cast<float*>(ws);
@@ -838,9 +908,9 @@ hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, co
   });
 }
 
-hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, const float* w,
-                          const float* dw, float* d_logits, float* dw_gate, float* dbias,
-                          int accumulate, void* ws, hipStream_t st) {
+hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, const int32_t* idx,
+                          const float* w, const float* dw, float* d_logits, float* dw_gate,
+                          float* dbias, int accumulate, void* ws, hipStream_t st) {
   const GateWs g = gate_ws(s, ws);
   const bool bf = s.dtype == FLOWMOE_BF16;
   const long n = (long)s.M * s.E + s.E;
@@ -861,8 +931,9 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, con
     const int tps = (s.T + S - 1) / S;
     const int nb = (s.T + kDlTok - 1) / kDlTok;
     hipError_t e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
-      hipLaunchKernelGGL(gate_bwd_dl_kernel, dim3(nb), dim3(256), 0, st, idx, w, dw, d_logits,
-                         g.dlhl, g.Pb, g.counts, g.offsets, s.T, s.E, N / 2, s.k, S, tps);
+      hipLaunchKernelGGL(gate_bwd_dl_kernel, dim3(nb), dim3(256), 0, st, idx, w, dw, logits,
+                         d_logits, g.dlhl, g.Pb, g.counts, g.offsets, s.T, s.E, N / 2, s.k, S,
+                         tps, (int)(s.gate == FLOWMOE_GATE_FULL));
     });
     if (e != hipSuccess) return e;
     e = launch_gate_dw_gemm(x, s.T, s.M, g.dlhl, N, g.counts, g.offsets, S, g.P, st);
@@ -902,11 +973,18 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const int32_t* idx, con
   });
 }
 
-hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const int32_t* idx,
-                           const float* w, const float* dw, float* d_logits, float* dw_gate,
-                           float* dbias, void* dx, int accumulate, void* ws, hipStream_t st) {
-  hipError_t e = launch_gate_dw(s, x, idx, w, dw, d_logits, dw_gate, dbias, accumulate, ws, st);
+hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const float* logits,
+                           const int32_t* idx, const float* w, const float* dw, float* d_logits,
+                           float* dw_gate, float* dbias, void* dx, int accumulate, void* ws,
+                           hipStream_t st) {
+  hipError_t e = launch_gate_dw(s, x, logits, idx, w, dw, d_logits, dw_gate, dbias, accumulate, ws,
+                                st);
   if (e != hipSuccess || dx == nullptr || s.T == 0) return e;
+  if (s.gate == FLOWMOE_GATE_FULL) {  // dense d_logits: dx += [hi | lo] [W_g^T ; W_g^T]
+    e = launch_gate_wstack(s, w_gate, ws, st);
+    if (e != hipSuccess) return e;
+    return launch_gate_dx_full(s, ws, dx, true, st);
+  }
   e = launch_gate_wt(s, w_gate, ws, st);
   if (e != hipSuccess) return e;
   return launch_gate_dx(s, idx, w, dw, gate_ws_wgt(ws), dx, st);

@@ -37,7 +37,8 @@ enum {
   EPI_GELU_BWD = 3,    // C0 = acc * gelu'(aux h)
   EPI_SWIGLU_BWD = 4,  // C0 = [acc h3 silu'(h1) | acc silu(h1)] with aux = [h1 | h3]
   EPI_WGRAD = 5,       // fp32 C0 (cols < nsplit) / C1 (cols >= nsplit), optional +=
-  EPI_GATE_DW = 6      // as EPI_WGRAD (its own instance: the gate's dW_g partials)
+  EPI_GATE_DW = 6,     // as EPI_WGRAD (its own instance: the gate's dW_g partials)
+  EPI_ADD = 7          // C0 += acc (bf16; aux = C0 itself, prefetched like a pre-activation)
 };
 
 struct GemmParams {
@@ -234,7 +235,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
       // activation-backward epilogues read the saved pre-activations: all of
       // this half's loads go out before the staging, and none waits behind
       // an output store (one memory round trip per half, not one per item)
-      constexpr bool AUXB = MODE == MODE_ROWS && (EPI == EPI_GELU_BWD || EPI == EPI_SWIGLU_BWD);
+      constexpr bool AUXB = MODE == MODE_ROWS &&
+                            (EPI == EPI_GELU_BWD || EPI == EPI_SWIGLU_BWD || EPI == EPI_ADD);
       constexpr int AG8 = WN / 8, APER = AUXB ? AG8 : 1;
       Raw8b hr[APER], h3r[APER];
       if constexpr (AUXB) {
@@ -363,6 +365,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
           }
           const long g = row0 + ti;
           if constexpr (EPI == EPI_STORE) {
+            store8(C0 + g * p.ldc + n, v);
+          } else if constexpr (EPI == EPI_ADD) {
+            float o[8];
+            raw8_f32(hr[it], o);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] += o[q];
             store8(C0 + g * p.ldc + n, v);
           } else if constexpr (EPI == EPI_GELU_FWD) {
             float a[8];
@@ -1352,6 +1360,37 @@ hipError_t launch_gate_dw_gemm(const void* x, int T, int M, const void* d, int N
   p.nseg = 1;
   p.rows_cap = T;
   return run_gemm_bf16<MODE_KSUM, false, false, EPI_GATE_DW>(FLOWMOE_K_GATE_BWD_DW, s2, p, st);
+}
+
+hipError_t launch_gate_dx_gemm(const void* dlhl, int T, int K, const void* wstack, int M,
+                               const int32_t* counts, const int32_t* offsets, int S, void* dx,
+                               bool add, hipStream_t st) {
+  Shape s2 = {};
+  s2.T = T;
+  s2.E = S;
+  s2.rows = T;
+  s2.layout = FLOWMOE_PACKED;
+  GemmParams p = {};
+  p.counts = counts;
+  p.offsets = offsets;
+  p.E = S;
+  p.A = dlhl;
+  p.lda = K;
+  p.K = K;
+  p.B0 = wstack;  // B[k][n] = wstack[k][n] for every token split (b_estride 0)
+  p.ldb = M;
+  p.N = M;
+  p.C0 = dx;
+  p.ldc = M;
+  p.aux = dx;     // (EPI_ADD: the values added to)
+  p.ldaux = M;
+  p.ksplit = 1 << 30;
+  p.nsplit = 1 << 30;
+  p.nseg = 1;
+  p.rows_cap = T;
+  if (add)
+    return run_gemm_bf16<MODE_ROWS, true, false, EPI_ADD>(FLOWMOE_K_GATE_BWD_TOKEN, s2, p, st);
+  return run_gemm_bf16<MODE_ROWS, true, false, EPI_STORE>(FLOWMOE_K_GATE_BWD_TOKEN, s2, p, st);
 }
 
 size_t ffn_bwd_ws_bytes(const Shape& s) {

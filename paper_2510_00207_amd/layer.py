@@ -24,7 +24,7 @@ class MoELayer:
     def __init__(self, *, T_total: int, M: int, H: int, E: int, k: int, R: int = 1,
                  f: float | None = None, C: int | None = None, act: str = "gelu",
                  dtype: str = "bf16", layout: str = "packed", bias: bool = False,
-                 device="cuda"):
+                 gate: str = "renorm", device="cuda"):
         if T_total % R:
             raise ValueError("T_total must be a multiple of R")
         T = T_total // R
@@ -38,7 +38,8 @@ class MoELayer:
         self.dt = L.BF16 if dtype == "bf16" else L.F32
         self.shape = L.make_shape(T, M, H, E, k, C, self.dt,
                                   L.SWIGLU if act == "swiglu" else L.GELU,
-                                  L.PADDED if layout == "padded" else L.PACKED)
+                                  L.PADDED if layout == "padded" else L.PACKED,
+                                  L.GATE_FULL if gate == "full" else L.GATE_RENORM)
         self.rows = L.flowmoe_rows_capacity(self.shape)
         if self.rows < 0:
             raise L.FlowMoEError(L.ERR_INVALID, L.flowmoe_last_error())

@@ -70,7 +70,7 @@ def f64_inputs(inp):
 def oracle_for_layer(layer_inp64, cfg, R, layout, gpu_logits):
     """Oracle of the whole layer with routing taken from the GPU logits."""
     return oracle.layer_fwd_bwd(layer_inp64, k=cfg.k, f=cfg.f, act=cfg.act, R=R, layout=layout,
-                                logits_for_routing=gpu_logits)
+                                logits_for_routing=gpu_logits, gate=cfg.gate)
 
 
 __all__ = ["TOL", "need_gpu", "dev", "max_rel_err", "assert_close", "host", "load_layer",

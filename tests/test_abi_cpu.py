@@ -129,7 +129,7 @@ def test_workspace_checked_before_launch(flowmoe_lib):
                                  None, FAKE, 0, None, 0, stream=0)
     assert ei.value.status == L.ERR_WORKSPACE
     with pytest.raises(L.FlowMoEError) as ei:
-        L.flowmoe_gate_topk_bwd(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, FAKE, 1,
+        L.flowmoe_gate_topk_bwd(s, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, FAKE, 1,
                                 stream=0)
     assert ei.value.status == L.ERR_WORKSPACE
 
@@ -176,7 +176,7 @@ def test_misaligned_tensors_rejected(flowmoe_lib):
     assert ei.value.status == L.ERR_INVALID and "w_gate" in str(ei.value)
     need = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
     with pytest.raises(L.FlowMoEError) as ei:
-        L.flowmoe_gate_topk_bwd(s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE + 4, 0, FAKE,
+        L.flowmoe_gate_topk_bwd(s, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE + 4, 0, FAKE,
                                 need, stream=0)
     assert ei.value.status == L.ERR_INVALID and "dx" in str(ei.value)
 

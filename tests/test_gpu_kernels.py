@@ -13,10 +13,11 @@ from paper_2510_00207_amd import _lib as L
 pytestmark = pytest.mark.gpu
 
 
-def _shape(T, M, H, E, k, C, dtype="bf16", act="gelu", layout="packed"):
+def _shape(T, M, H, E, k, C, dtype="bf16", act="gelu", layout="packed", gate="renorm"):
     return L.make_shape(T, M, H, E, k, C, L.BF16 if dtype == "bf16" else L.F32,
                         L.SWIGLU if act == "swiglu" else L.GELU,
-                        L.PADDED if layout == "padded" else L.PACKED)
+                        L.PADDED if layout == "padded" else L.PACKED,
+                        L.GATE_FULL if gate == "full" else L.GATE_RENORM)
 
 
 @pytest.mark.parametrize("E,k", [(1, 1), (3, 2), (4, 4), (8, 2), (16, 1), (24, 3), (32, 4), (33, 5), (64, 6),
@@ -126,6 +127,93 @@ def test_gate_topk_ties(T, E, k):
     assert np.array_equal(host(idx), ref_i)
     np.testing.assert_allclose(host(w), ref_w, rtol=2e-6, atol=2e-7)
     assert list(host(idx)[0]) == list(range(k))  # token 0 is all zero
+
+
+# the full softmax gate's weights divide by a sum over all E experts in fp32
+FULL_W_TOL = dict(rtol=1e-5, atol=1e-7)
+
+
+@pytest.mark.parametrize("T,M,E,k", [
+    (700, 64, 4, 1), (700, 64, 8, 2), (700, 128, 16, 1), (700, 64, 24, 3), (700, 64, 64, 6),
+    (700, 64, 64, 8), (9000, 96, 64, 6), (16400, 64, 8, 2), (8200, 64, 40, 1),
+])
+def test_gate_topk_full_softmax(T, M, E, k):
+    """FLOWMOE_GATE_FULL: the same selection, weights = the selected experts'
+    probabilities under the softmax over all E logits (every top-k path:
+    segmented lanes for E <= 16, 16/8/4 lanes per token above)."""
+    need_gpu()
+    rng = np.random.default_rng(T + E + k)
+    d = dev()
+    x = torch.from_numpy(rng.standard_normal((T, M)).astype(np.float32)).to(d).to(torch.bfloat16)
+    wg = torch.from_numpy((rng.standard_normal((M, E)) * 0.1).astype(np.float32)).to(d).to(
+        torch.bfloat16)
+    logits = torch.empty(T, E, device=d)
+    idx = torch.empty(T, k, dtype=torch.int32, device=d)
+    w = torch.empty(T, k, device=d)
+    L.flowmoe_gate_topk(_shape(T, M, 8, E, k, 0, gate="full"), x, wg, None, logits, idx, w)
+    torch.cuda.synchronize()
+    gl = host(logits)
+    ref_i, ref_w = oracle.topk_select(gl, k, "full")
+    assert np.array_equal(host(idx), ref_i)
+    np.testing.assert_allclose(host(w), ref_w, **FULL_W_TOL)
+    if k < E:
+        assert np.all(host(w).sum(axis=1) < 1.0)
+
+
+def test_route_full_softmax_ties():
+    need_gpu()
+    rng = np.random.default_rng(11)
+    d = dev()
+    for E in (2, 5, 8, 17, 64):
+        for k in sorted({1, min(E, 3)}):
+            T = 257
+            L_ = (rng.integers(-3, 4, size=(T, E)) * 0.25).astype(np.float32)
+            L_[5, :] = 1.0
+            lt = torch.from_numpy(L_).to(d)
+            idx = torch.empty(T, k, dtype=torch.int32, device=d)
+            w = torch.empty(T, k, device=d)
+            L.flowmoe_route(_shape(T, 8, 8, E, k, 0, gate="full"), lt, idx, w)
+            torch.cuda.synchronize()
+            ref_i, ref_w = oracle.topk_select(L_.astype(np.float64), k, "full")
+            assert np.array_equal(host(idx), ref_i), (E, k)
+            np.testing.assert_allclose(host(w), ref_w, **FULL_W_TOL)
+            np.testing.assert_allclose(host(w)[5], np.full(k, 1.0 / E), rtol=1e-6)
+
+
+@pytest.mark.parametrize("T,M,E,k", [(333, 136, 8, 3), (700, 64, 16, 1), (1000, 256, 64, 6),
+                                     (4100, 128, 24, 2)])
+def test_gate_bwd_full_softmax(T, M, E, k):
+    """FLOWMOE_GATE_FULL backward: dense d_logits (-p_e s off the selection),
+    dW_g and db from them, and dx += d_logits W_g^T over all E experts (a
+    GEMM of the bf16 hi/lo parts of d_logits against the stacked W_g^T)."""
+    need_gpu()
+    rng = np.random.default_rng(T * 3 + E)
+    d = dev()
+    td = torch.bfloat16
+    rnd = lambda *s_, sc=1.0: host(torch.from_numpy(rng.standard_normal(s_) * sc).to(d).to(td))
+    x64, wg64, dx0 = rnd(T, M), rnd(M, E, sc=0.05), rnd(T, M)
+    gl = (x64 @ wg64).astype(np.float32).astype(np.float64)
+    idx, w = oracle.topk_select(gl, k, "full")
+    dtw = rng.standard_normal((T, k)).astype(np.float32)
+    t = lambda a, dt=td: torch.from_numpy(np.ascontiguousarray(a)).to(d).to(dt)
+    s = _shape(T, M, 8, E, k, 0, gate="full")
+    nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
+    ws = torch.empty(nws, dtype=torch.uint8, device=d)
+    dlog = torch.empty(T, E, device=d)
+    dwg = torch.full((M, E), 3.0, device=d)
+    db = torch.full((E,), 3.0, device=d)
+    dx = t(dx0)
+    w32 = w.astype(np.float32)
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), t(gl, torch.float32), t(idx, torch.int32),
+                            t(w32, torch.float32), t(dtw, torch.float32), dlog, dwg, db, dx, 0, ws,
+                            nws)
+    torch.cuda.synchronize()
+    g = oracle.gate_bwd(x64, wg64, idx, w32.astype(np.float64), dtw.astype(np.float64), gl, "full")
+    assert np.all(host(dlog) != 0.0)  # every expert has a gradient
+    assert_close(host(dlog), g["d_logits"], "f32", "d_logits", tol=1e-5)
+    assert_close(host(dwg), g["dw_gate"], "bf16", "dw_gate")
+    assert_close(host(db), g["dbias"], "bf16", "dbias")
+    assert_close(host(dx), dx0 + g["dx_gate"], "bf16", "dx + dense gate term")
 
 
 def test_route_ties_and_signed_zeros():
@@ -385,7 +473,7 @@ def test_gate_bwd_shapes(T, M, E, k):
     db = torch.full((E,), 3.0, device=d)
     nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
     ws = torch.empty(nws, dtype=torch.uint8, device=d)
-    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), t(idx, torch.int32), t(w, torch.float32),
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), None, t(idx, torch.int32), t(w, torch.float32),
                             t(dtw64, torch.float32), dlog, dwg, db, None, 0, ws, nws)
     torch.cuda.synchronize()
     g = oracle.gate_bwd(x64, wg64, idx, host(t(w, torch.float32)), host(t(dtw64, torch.float32)))
@@ -437,15 +525,15 @@ def test_combine_and_backward_steps(dtype, layout):
     db = torch.full((E,), 3.0, device=d)
     nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
     ws = torch.empty(nws, dtype=torch.uint8, device=d)
-    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), t(idx, torch.int32), w_t, dtw, dlog, dwg, db, dx, 0,
-                            ws, nws)
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), None, t(idx, torch.int32), w_t, dtw, dlog, dwg, db,
+                            dx, 0, ws, nws)
     torch.cuda.synchronize()
     g = oracle.gate_bwd(x64, wg64, idx, w, host(dtw))
     assert_close(host(dlog), g["d_logits"], dtype, "d_logits")
     assert_close(host(dwg), g["dw_gate"], dtype, "dw_gate")
     assert_close(host(db), g["dbias"], dtype, "dbias")
     assert_close(host(dx), rdx + g["dx_gate"], dtype, "dx + gate")
-    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), t(idx, torch.int32), w_t, dtw, dlog, dwg, db, None, 1,
-                            ws, nws)
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), None, t(idx, torch.int32), w_t, dtw, dlog, dwg, db,
+                            None, 1, ws, nws)
     torch.cuda.synchronize()
     assert_close(host(dwg), 2 * g["dw_gate"], dtype, "dw_gate accumulated")

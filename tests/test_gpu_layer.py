@@ -32,7 +32,8 @@ def run_layer(cfg, layout, R=None, two_streams=True, inp=None):
     R = cfg.R if R is None else R
     inp = make_inputs(cfg) if inp is None else inp
     layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
-                     dtype=cfg.dtype, layout=layout, bias=cfg.zipf_bias, device=dev())
+                     dtype=cfg.dtype, layout=layout, bias=cfg.zipf_bias, gate=cfg.gate,
+                     device=dev())
     load_layer(layer, inp)
     sc = torch.cuda.current_stream()
     sm = torch.cuda.Stream() if two_streams else sc
@@ -53,7 +54,9 @@ def check_against_oracle(cfg, layout, layer, inp, R):
     assert dl <= 1e-4 * np.max(np.abs(own)), f"logits off by {dl}"
     # routing is a function of the fp32 logits: bit-exact
     assert np.array_equal(host(layer.topk_idx), ref["topk_idx"])
-    np.testing.assert_allclose(host(layer.topk_w), ref["topk_w"], rtol=2e-6, atol=2e-7)
+    # (the full softmax gate divides by a sum over all E experts in fp32)
+    wtol = dict(rtol=1e-5, atol=1e-7) if cfg.gate == "full" else dict(rtol=2e-6, atol=2e-7)
+    np.testing.assert_allclose(host(layer.topk_w), ref["topk_w"], **wtol)
     Tr = cfg.T // R
     for r, c in enumerate(ref["chunks"]):
         assert np.array_equal(host(layer.counts[r]), c["counts"]), f"counts chunk {r}"
@@ -114,6 +117,25 @@ def test_layer_chunks_f32(R, act, layout):
     print(f"[layer] f32 {act} {layout} R={R}", flush=True)
     layer, inp = run_layer(cfg, layout, R=R)
     check_against_oracle(cfg, layout, layer, inp, R)
+
+
+@pytest.mark.parametrize("name,R", [("balanced_s", 1), ("skewed_s", 1), ("fine_s", 4),
+                                    ("large_s", 2)])
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+def test_layer_full_softmax_gate(name, R, layout):
+    """The layer with the Switch-style gate (FLOWMOE_GATE_FULL): the skewed
+    layer is top-1, whose renormalised gate has no gradient; here its router
+    gets one, and every step still matches the oracle."""
+    need_gpu()
+    cfg = CASES[name].replace(gate="full")
+    print(f"[layer] full gate {name} {layout} R={R}", flush=True)
+    layer, inp = run_layer(cfg, layout, R=R)
+    check_against_oracle(cfg, layout, layer, inp, R)
+    # every expert's logit of a token with a kept assignment has a gradient
+    # (a token whose assignments were all dropped has dw = 0, hence none)
+    live = np.any(host(layer.d_topk_w) != 0.0, axis=1)
+    assert live.any() and host(layer.dw_gate).any()
+    assert np.all(host(layer.d_logits)[live] != 0.0)
 
 
 def test_two_streams_equal_one_stream_and_deterministic():
