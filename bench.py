@@ -44,6 +44,8 @@ def parse():
                     help="gate weights: softmax over the k selected (renorm) or the selected "
                          "experts' full-softmax probabilities (full, Switch-style)")
     ap.add_argument("--R", type=int, default=None, help="override the chunk count")
+    for dim, typ in (("T", int), ("M", int), ("H", int), ("E", int), ("k", int), ("f", float)):
+        ap.add_argument(f"--{dim}", type=typ, default=None, help=f"override the workload's {dim}")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-memory-bound", action="store_true",
@@ -160,7 +162,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
 
-    cfg = get_config(a.workload, gate=a.gate)
+    over = {d: getattr(a, d) for d in ("T", "M", "H", "E", "k", "f") if getattr(a, d) is not None}
+    cfg = get_config(a.workload, gate=a.gate, **over)
+    if over:  # another shape: named apart (no counter summary of the workload applies to it)
+        cfg = cfg.replace(name=cfg.name + "(" + " ".join(f"{d}={v}" for d, v in over.items()) + ")")
     R = cfg.R if a.R is None else a.R
     inp = make_inputs(cfg)
     layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
