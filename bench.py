@@ -47,6 +47,8 @@ def parse():
     for dim, typ in (("T", int), ("M", int), ("H", int), ("E", int), ("k", int), ("f", float)):
         ap.add_argument(f"--{dim}", type=typ, default=None, help=f"override the workload's {dim}")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
+    ap.add_argument("--tiles", default="auto", choices=("auto", "wide", "narrow"),
+                    help="grouped-GEMM tile shape")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-memory-bound", action="store_true",
                     help="skip the per-call timing of the memory-bound steps")
@@ -159,6 +161,7 @@ def main():
         from paper_2510_00207_amd import build
         build.build(verbose=False)
     L.load()
+    L.flowmoe_set_gemm_tiles(a.tiles)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
 
@@ -303,6 +306,16 @@ def main():
                "sample": f"{reps} full fwd+bwd step(s) of the {cfg.name} workload ({cfg.T} tokens "
                          f"each), numpy fp64, {c1 - c0:.1f} s"}
 
+    # the library's schedule: one chunk runs its forward on one stream, and its
+    # backward on two only for layers whose expert GEMMs span many rounds
+    if a.one_stream:
+        streams = "1 stream"
+    elif R > 1:
+        streams = "2 streams"
+    elif float(layer.rows) * cfg.M * cfg.H >= 2.5e11:
+        streams = "1 stream forward, 2 backward"
+    else:
+        streams = "1 stream"
     out = {
         "metric": "MoE-layer fwd+bwd tokens/s on 1 MI355X; grouped-GEMM MFMA util %",
         "value": round(tokens_per_s, 1),
@@ -319,10 +332,10 @@ def main():
         "config": {
             "workload": (f"{cfg.name} MoE layer: T={cfg.T} M={cfg.M} H={cfg.H} E={cfg.E} "
                          f"top-{cfg.k} f={cfg.f} {cfg.act} {cfg.dtype}, R={R}, {a.layout}, "
-                         f"{'1' if (a.one_stream or R == 1) else '2'} stream(s)"
+                         f"{streams}"
                          f"{', full-softmax gate' if cfg.gate == 'full' else ''}"),
             "T": cfg.T, "M": cfg.M, "H": cfg.H, "E": cfg.E, "k": cfg.k, "f": cfg.f,
-            "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "gate": cfg.gate,
+            "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "gate": cfg.gate, "tiles": a.tiles,
             "kept_rows": kept,
         },
         "roofline": {

@@ -355,7 +355,10 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
  * (rows x H for GELU, rows x 2H = [dH1 | dH3] for SwiGLU).
  * trace (nullable): 8*R events as for the forward, task 0 = combine bwd,
  * 1 = experts bwd (chunk 1's span also covers the weight gradients),
- * 2 = dispatch bwd (+ gate dx term), 3 = gate parameter gradients. */
+ * 2 = dispatch bwd (+ gate dx term), 3 = gate parameter gradients.
+ * With R = 1 the two streams are used only for large layers (capacity rows
+ * x M x H >= 2.5e11), where the expert GEMMs span many rounds of the compute
+ * units; smaller ones run everything on s_compute. */
 flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
                                    const flowmoe_layer_bufs_t* bufs, hipStream_t s_compute,
                                    hipStream_t s_comm, hipEvent_t* trace);

@@ -159,17 +159,18 @@ hipError_t launch_dispatch_bwd_add(const Shape& s, const void* dx_disp, const in
                                    void* dx, hipStream_t st);
 hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const int32_t* slot,
                                     const int32_t* idx, const float* w, const float* dw,
-                                    const float* wgt, void* dx, hipStream_t st);
-// gate backward workspace: [W_g^T, float E x M | dW_g partials]
+                                    const void* wgt, void* dx, hipStream_t st);
+// gate backward workspace: [W_g^T, E x M in the layer dtype | dW_g partials]
 size_t gate_bwd_ws_bytes(const Shape& s);
-inline const float* gate_ws_wgt(const void* ws) { return static_cast<const float*>(ws); }
+inline const void* gate_ws_wgt(const void* ws) { return ws; }
 // logits: needed by the full softmax gate (nullable otherwise)
 hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, const int32_t* idx,
                           const float* w, const float* dw, float* d_logits, float* dw_gate,
                           float* dbias, int accumulate, void* ws, hipStream_t st);
 hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, const float* dw,
-                          const float* wgt, void* dx, hipStream_t st);
-// W_g (M x E, layer dtype) -> W_g^T (E x M, float) at the front of the gate workspace
+                          const void* wgt, void* dx, hipStream_t st);
+// W_g (M x E) -> W_g^T (E x M, both in the layer dtype: an exact copy) at the
+// front of the gate workspace
 hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st);
 hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const float* logits,
                            const int32_t* idx, const float* w, const float* dw, float* d_logits,

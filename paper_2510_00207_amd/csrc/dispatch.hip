@@ -303,7 +303,7 @@ template <typename TE, bool GATE, int KM, bool ADD = false>  // KM >= k: per-tok
 __global__ __launch_bounds__(256) void combine_rows_kernel(
     const TE* __restrict__ src, const int32_t* __restrict__ slot, const float* __restrict__ w,
     TE* __restrict__ y, int T, int M, int k, const int32_t* __restrict__ gidx,
-    const float* __restrict__ gw, const float* __restrict__ gdw, const float* __restrict__ wgt) {
+    const float* __restrict__ gw, const float* __restrict__ gdw, const TE* __restrict__ wgt) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = threadIdx.x & 63;
@@ -337,7 +337,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
   for (int m0 = lane * 8; m0 < M; m0 += 64 * 8 * U) {
     decltype(raw8_load(src)) raw[U][KM];
     decltype(raw8_load(src)) yold[ADD ? U : 1];
-    Raw8f graw[GATE ? U : 1][GATE ? KM : 1];
+    decltype(raw8_load(src)) graw[GATE ? U : 1][GATE ? KM : 1];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int m = m0 + 64 * 8 * u < M ? m0 + 64 * 8 * u : m0;
@@ -554,7 +554,7 @@ hipError_t launch_dispatch_bwd_add(const Shape& s, const void* dx_disp, const in
 
 hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const int32_t* slot,
                                     const int32_t* idx, const float* w, const float* dw,
-                                    const float* wgt, void* dx, hipStream_t st) {
+                                    const void* wgt, void* dx, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
   const int blocks = (s.T + 3) / 4;
   return traced(FLOWMOE_K_COMBINE, st, [&] {
@@ -563,11 +563,11 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
       if (s.dtype == FLOWMOE_BF16)
         hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true, KMV>), dim3(blocks), dim3(256), 0, st,
                            (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx, s.T, s.M, s.k, idx, w,
-                           dw, wgt);
+                           dw, (const bf16_t*)wgt);
       else
         hipLaunchKernelGGL((combine_rows_kernel<float, true, KMV>), dim3(blocks), dim3(256), 0, st,
                            (const float*)dx_disp, slot, nullptr, (float*)dx, s.T, s.M, s.k, idx, w,
-                           dw, wgt);
+                           dw, (const float*)wgt);
     });
   });
 }

@@ -478,11 +478,11 @@ __device__ __forceinline__ void token_dl(const int32_t* __restrict__ idx, const 
 // 8 consecutive m of one expert as two 16-byte vectors
 template <typename TIn>
 __global__ __launch_bounds__(256) void transpose_wg_kernel(const TIn* __restrict__ wg,
-                                                           float* __restrict__ wgt, int M, int E) {
+                                                           TIn* __restrict__ wgt, int M, int E) {
   const long n = (long)M * E;
   for (long q = blockIdx.x * 256L + threadIdx.x; q < n; q += (long)gridDim.x * 256) {
     const int e = (int)(q / M), m = (int)(q % M);
-    wgt[q] = Elem<TIn>::load(wg + (long)m * E + e);
+    wgt[q] = wg[(long)m * E + e];
   }
 }
 
@@ -490,7 +490,7 @@ __global__ __launch_bounds__(256) void transpose_wg_kernel(const TIn* __restrict
 template <typename TIn>
 __global__ __launch_bounds__(256) void gate_bwd_dx_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
-    const float* __restrict__ wgt, TIn* __restrict__ dx, int T, int M, int k) {
+    const TIn* __restrict__ wgt, TIn* __restrict__ dx, int T, int M, int k) {
   const int lane = threadIdx.x & 63;
   const long t = blockIdx.x * 4L + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -501,7 +501,7 @@ __global__ __launch_bounds__(256) void gate_bwd_dx_kernel(
   for (int m = lane * 8; m < M; m += 64 * 8) {  // M is a multiple of 8
     // this step's dx and W_g^T rows loaded before the add and the store
     const auto xr = raw8_load(row + m);
-    Raw8f gr[kMaxK];
+    decltype(raw8_load(wgt)) gr[kMaxK];
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j)
       if (j < k) gr[j] = raw8_load(wgt + (long)ij[j] * M + m);
@@ -734,10 +734,10 @@ bool gate_dw_on_gemm(const Shape& s) {
 }
 
 // GEMM path: token splits of the dW_g GEMM (its pseudo-experts): about 256
-// blocks of 256 x 128 tiles, at least 128 tokens per split, at most 16 MB
+// blocks of 256 x 256 tiles, at least 128 tokens per split, at most 16 MB
 // of fp32 partials
 int gate_dw_splits(const Shape& s) {
-  const long mt = (s.M + 255) / 256, nt = (gate_dw_cols(s.E) + 127) / 128;
+  const long mt = (s.M + 255) / 256, nt = (gate_dw_cols(s.E) + 255) / 256;
   long sp = 256 / (mt * nt);
   const long by_tokens = s.T / 128, by_bytes = (16L << 20) / ((long)s.M * gate_dw_cols(s.E) * 4);
   if (sp > by_tokens) sp = by_tokens;
@@ -881,30 +881,29 @@ hipError_t launch_gate_dx_full(const Shape& s, void* ws, void* dx, bool add, hip
 }
 
 hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st) {
-  float* wgt = static_cast<float*>(ws);
   const long n = (long)s.M * s.E;
   const int nb = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
   return traced(FLOWMOE_K_GATE_BWD_WT, st, [&] {
     if (s.dtype == FLOWMOE_BF16)
       hipLaunchKernelGGL(transpose_wg_kernel<bf16_t>, dim3(nb), dim3(256), 0, st,
-                         (const bf16_t*)w_gate, wgt, s.M, s.E);
+                         (const bf16_t*)w_gate, static_cast<bf16_t*>(ws), s.M, s.E);
     else
       hipLaunchKernelGGL(transpose_wg_kernel<float>, dim3(nb), dim3(256), 0, st,
-                         (const float*)w_gate, wgt, s.M, s.E);
+                         (const float*)w_gate, static_cast<float*>(ws), s.M, s.E);
   });
 }
 
 hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, const float* dw,
-                          const float* wgt, void* dx, hipStream_t st) {
+                          const void* wgt, void* dx, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
   const int tb = (s.T + 3) / 4;
   return traced(FLOWMOE_K_GATE_BWD_TOKEN, st, [&] {
     if (s.dtype == FLOWMOE_BF16)
-      hipLaunchKernelGGL(gate_bwd_dx_kernel<bf16_t>, dim3(tb), dim3(256), 0, st, idx, w, dw, wgt,
-                         (bf16_t*)dx, s.T, s.M, s.k);
+      hipLaunchKernelGGL(gate_bwd_dx_kernel<bf16_t>, dim3(tb), dim3(256), 0, st, idx, w, dw,
+                         (const bf16_t*)wgt, (bf16_t*)dx, s.T, s.M, s.k);
     else
-      hipLaunchKernelGGL(gate_bwd_dx_kernel<float>, dim3(tb), dim3(256), 0, st, idx, w, dw, wgt,
-                         (float*)dx, s.T, s.M, s.k);
+      hipLaunchKernelGGL(gate_bwd_dx_kernel<float>, dim3(tb), dim3(256), 0, st, idx, w, dw,
+                         (const float*)wgt, (float*)dx, s.T, s.M, s.k);
   });
 }
 

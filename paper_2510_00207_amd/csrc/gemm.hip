@@ -1359,7 +1359,10 @@ hipError_t launch_gate_dw_gemm(const void* x, int T, int M, const void* d, int N
   p.ksplit = 1 << 30;
   p.nseg = 1;
   p.rows_cap = T;
-  return run_gemm_bf16<MODE_KSUM, false, false, EPI_GATE_DW>(FLOWMOE_K_GATE_BWD_DW, s2, p, st);
+  // 256 x 256 tiles whatever the grid: these launches are bound by reading
+  // x once, and the 8-wave tile's deeper ring (4 stages against 3) keeps
+  // more of it in flight (the narrow tile took 1.2-1.7x as long)
+  return launch_dma<MODE_KSUM, false, false, EPI_GATE_DW, false>(FLOWMOE_K_GATE_BWD_DW, s2, p, st);
 }
 
 hipError_t launch_gate_dx_gemm(const void* dlhl, int T, int K, const void* wstack, int M,
