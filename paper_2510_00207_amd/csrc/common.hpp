@@ -84,6 +84,45 @@ __device__ __forceinline__ Raw8b raw8_load(const bf16_t* p) {
 __device__ __forceinline__ Raw8f raw8_load(const float* p) {
   return Raw8f{*reinterpret_cast<const u32x4v_t*>(p), *reinterpret_cast<const u32x4v_t*>(p + 4)};
 }
+// NT: non-temporal access (streams larger than the 256 MB Infinity Cache,
+// whose lines would only evict data that is read again)
+template <bool NT>
+__device__ __forceinline__ u32x4v_t ld16(const u32x4v_t* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+template <bool NT>
+__device__ __forceinline__ void st16(u32x4v_t* p, const u32x4v_t& v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+template <bool NT>
+__device__ __forceinline__ Raw8b raw8_ld(const bf16_t* p) {
+  return Raw8b{ld16<NT>(reinterpret_cast<const u32x4v_t*>(p))};
+}
+template <bool NT>
+__device__ __forceinline__ Raw8f raw8_ld(const float* p) {
+  return Raw8f{ld16<NT>(reinterpret_cast<const u32x4v_t*>(p)),
+               ld16<NT>(reinterpret_cast<const u32x4v_t*>(p + 4))};
+}
+template <bool NT>
+__device__ __forceinline__ void store8_t(bf16_t* p, const float v[8]) {
+  u32x4v_t q;
+  q.x = pack_bf16x2(v[0], v[1]);
+  q.y = pack_bf16x2(v[2], v[3]);
+  q.z = pack_bf16x2(v[4], v[5]);
+  q.w = pack_bf16x2(v[6], v[7]);
+  st16<NT>(reinterpret_cast<u32x4v_t*>(p), q);
+}
+template <bool NT>
+__device__ __forceinline__ void store8_t(float* p, const float v[8]) {
+  st16<NT>(reinterpret_cast<u32x4v_t*>(p),
+           u32x4v_t{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                    __float_as_uint(v[3])});
+  st16<NT>(reinterpret_cast<u32x4v_t*>(p + 4),
+           u32x4v_t{__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]),
+                    __float_as_uint(v[7])});
+}
 __device__ __forceinline__ void raw8_f32(const Raw8b& r, float v[8]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {

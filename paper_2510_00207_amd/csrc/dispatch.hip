@@ -35,6 +35,16 @@ __host__ void with_kmax(int k, F&& f) {
   else f(KConst<8>{});
 }
 
+// f(true or false as a type): non-temporal row streams for bf16 calls that
+// move at least 256 MB (the Infinity Cache): there every line of the stream
+// is gone before it is read again, and caching it only evicts the rest
+template <typename F>
+__host__ void with_nt(const Shape& s, long rows, F&& f) {
+  const bool nt = s.dtype == FLOWMOE_BF16 && (long)(rows + s.T) * s.M * 2 >= (256L << 20);
+  if (nt) f(std::true_type{});
+  else f(std::false_type{});
+}
+
 constexpr int kScanThreads = 1024;
 constexpr int kScanWaves = kScanThreads / 64;
 constexpr int kScanUnroll = 8;  // chunk loads in flight per lane
@@ -211,6 +221,7 @@ __global__ __launch_bounds__(kScanThreads) void route_scan_kernel(
 
 // x_disp[r] = x[row_src[r] / k] or zeros; rows [0, offsets[E]) (packed) or
 // all rows (padded). One wave per row; each lane has 4 loads in flight.
+template <bool NT>
 __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4v_t* __restrict__ x,
                                                           const int32_t* __restrict__ row_src,
                                                           const int32_t* __restrict__ offsets,
@@ -230,15 +241,15 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4v_t* __rest
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int v = v0 + 64 * u;
-        t[u] = s[v < vecs ? v : v0];  // (every load issued, from in-bounds addresses)
+        t[u] = ld16<NT>(s + (v < vecs ? v : v0));  // (every load issued, from in-bounds addresses)
       }
 #pragma unroll
       for (int u = 0; u < U; ++u)
-        if (v0 + 64 * u < vecs) dst[v0 + 64 * u] = t[u];
+        if (v0 + 64 * u < vecs) st16<NT>(dst + v0 + 64 * u, t[u]);
     }
   } else {
     const u32x4v_t z = {0u, 0u, 0u, 0u};
-    for (int v = lane; v < vecs; v += 64) dst[v] = z;
+    for (int v = lane; v < vecs; v += 64) st16<NT>(dst + v, z);
   }
 }
 
@@ -246,7 +257,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4v_t* __rest
 // once (4 loads in flight per lane) and written to each of its rows. Padded
 // layout: blocks past the token blocks zero the rows past each expert's
 // count. (Rows of the packed layout past offsets[E] are not written.)
-template <int KM>  // KM >= k
+template <int KM, bool NT>  // KM >= k
 __global__ __launch_bounds__(256) void scatter_rows_kernel(
     const u32x4v_t* __restrict__ x, const int32_t* __restrict__ slot,
     const int32_t* __restrict__ counts, u32x4v_t* __restrict__ x_disp, int T, int k, int vecs,
@@ -259,7 +270,7 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(
     const int e = (int)(r / C), i = (int)(r % C);
     if (i < counts[e]) return;
     const u32x4v_t z = {0u, 0u, 0u, 0u};
-    for (int v = lane; v < vecs; v += 64) x_disp[r * vecs + v] = z;
+    for (int v = lane; v < vecs; v += 64) st16<NT>(x_disp + r * vecs + v, z);
     return;
   }
   const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -278,7 +289,7 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int v = v0 + 64 * u;
-      q[u] = src[v < vecs ? v : v0];  // (every load issued, from in-bounds addresses)
+      q[u] = ld16<NT>(src + (v < vecs ? v : v0));  // (every load issued, from in-bounds addresses)
     }
 #pragma unroll
     for (int j = 0; j < KM; ++j) {
@@ -286,7 +297,7 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(
       u32x4v_t* dst = x_disp + (long)sl[j] * vecs;
 #pragma unroll
       for (int u = 0; u < U; ++u)
-        if (v0 + 64 * u < vecs) dst[v0 + 64 * u] = q[u];
+        if (v0 + 64 * u < vecs) st16<NT>(dst + v0 + 64 * u, q[u]);
     }
   }
 }
@@ -299,7 +310,7 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(
 // with dl_t taken from the selection (gidx), its weights (gw) and their
 // gradients (gdw), and W_g^T given transposed in float (wgt, E x M).
 // ADD: y[t] += (the sum) instead of =, the old y loaded with the source rows.
-template <typename TE, bool GATE, int KM, bool ADD = false>  // KM >= k: per-token array size
+template <typename TE, bool GATE, int KM, bool ADD, bool NT>  // KM >= k: per-token array size
 __global__ __launch_bounds__(256) void combine_rows_kernel(
     const TE* __restrict__ src, const int32_t* __restrict__ slot, const float* __restrict__ w,
     TE* __restrict__ y, int T, int M, int k, const int32_t* __restrict__ gidx,
@@ -343,13 +354,13 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
       const int m = m0 + 64 * 8 * u < M ? m0 + 64 * 8 * u : m0;
 #pragma unroll
       for (int j = 0; j < KM; ++j)
-        if (j < k) raw[u][j] = raw8_load(src + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
+        if (j < k) raw[u][j] = raw8_ld<NT>(src + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
       if constexpr (GATE) {
 #pragma unroll
         for (int j = 0; j < KM; ++j)
           if (j < k) graw[u][j] = raw8_load(wgt + (long)ge[j] * M + m);
       }
-      if constexpr (ADD) yold[u] = raw8_load(y + (long)t * M + m);
+      if constexpr (ADD) yold[u] = raw8_ld<NT>(y + (long)t * M + m);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -383,13 +394,13 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc[q] += o[q];
       }
-      store8(y + (long)t * M + m, acc);
+      store8_t<NT>(y + (long)t * M + m, acc);
     }
   }
 }
 
 // combine backward, token part: dy_disp[slot] = w * dy[t], d_w = <dy[t], y_disp[slot]>
-template <typename TE, int KM>  // KM >= k: size of the per-token arrays
+template <typename TE, int KM, bool NT>  // KM >= k: size of the per-token arrays
 __global__ __launch_bounds__(256) void combine_bwd_kernel(
     const TE* __restrict__ dy, const TE* __restrict__ y_disp, const int32_t* __restrict__ slot,
     const float* __restrict__ w, const int32_t* __restrict__ counts, TE* __restrict__ dy_disp,
@@ -402,7 +413,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
     const int e = (int)(r / C), i = (int)(r % C);
     if (i < counts[e]) return;
     const float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int m = lane * 8; m < M; m += 64 * 8) store8(dy_disp + r * M + m, z);
+    for (int m = lane * 8; m < M; m += 64 * 8) store8_t<NT>(dy_disp + r * M + m, z);
     return;
   }
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -424,10 +435,10 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int m = m0 + 64 * 8 * u < M ? m0 + 64 * 8 * u : m0;
-      graw[u] = raw8_load(dy + (long)t * M + m);
+      graw[u] = raw8_ld<NT>(dy + (long)t * M + m);
 #pragma unroll
       for (int j = 0; j < KM; ++j)
-        if (j < k) raw[u][j] = raw8_load(y_disp + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
+        if (j < k) raw[u][j] = raw8_ld<NT>(y_disp + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -445,7 +456,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
             dot[j] += g[q] * v[q];
             o[q] = wt[j] * g[q];
           }
-          store8(dy_disp + (long)sl[j] * M + m, o);
+          store8_t<NT>(dy_disp + (long)sl[j] * M + m, o);
         }
       }
     }
@@ -489,9 +500,11 @@ hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, in
   if (s.k == 1) {  // one row per token: walk the rows
     const long blocks = (s.rows + 3) / 4;
     return traced(FLOWMOE_K_GATHER, st, [&] {
-      hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
-                         (const u32x4v_t*)x, row_src, offsets, (u32x4v_t*)x_disp, s.E, s.k, vecs,
-                         s.rows, padded);
+      with_nt(s, s.rows, [&](auto ntc) {
+        hipLaunchKernelGGL((gather_rows_kernel<decltype(ntc)::value>), dim3((unsigned)blocks),
+                           dim3(256), 0, st, (const u32x4v_t*)x, row_src, offsets,
+                           (u32x4v_t*)x_disp, s.E, s.k, vecs, s.rows, padded);
+      });
     });
   }
   // k >= 2: walk the tokens, each x row read once for its k rows
@@ -502,9 +515,11 @@ hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, in
   return traced(FLOWMOE_K_GATHER, st, [&] {
     with_kmax(s.k, [&](auto kc) {
       constexpr int KMV = decltype(kc)::value;
-      hipLaunchKernelGGL((scatter_rows_kernel<KMV>), dim3((unsigned)blocks), dim3(256), 0, st,
-                         (const u32x4v_t*)x, slot, counts, (u32x4v_t*)x_disp, s.T, s.k, vecs, s.E,
-                         s.C, token_blocks);
+      with_nt(s, s.rows, [&](auto ntc) {
+        hipLaunchKernelGGL((scatter_rows_kernel<KMV, decltype(ntc)::value>), dim3((unsigned)blocks),
+                           dim3(256), 0, st, (const u32x4v_t*)x, slot, counts, (u32x4v_t*)x_disp,
+                           s.T, s.k, vecs, s.E, s.C, token_blocks);
+      });
     });
   });
 }
@@ -517,13 +532,15 @@ hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slo
     with_kmax(s.k, [&](auto kc) {
       constexpr int KMV = decltype(kc)::value;
       if (s.dtype == FLOWMOE_BF16)
-        hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV>), dim3(blocks), dim3(256), 0, st,
-                           (const bf16_t*)y_disp, slot, w, (bf16_t*)y, s.T, s.M, s.k, nullptr,
-                           nullptr, nullptr, nullptr);
+        with_nt(s, s.rows, [&](auto ntc) {
+          hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV, false, decltype(ntc)::value>),
+                             dim3(blocks), dim3(256), 0, st, (const bf16_t*)y_disp, slot, w,
+                             (bf16_t*)y, s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+        });
       else
-        hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV>), dim3(blocks), dim3(256), 0, st,
-                           (const float*)y_disp, slot, w, (float*)y, s.T, s.M, s.k, nullptr,
-                           nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV, false, false>), dim3(blocks),
+                           dim3(256), 0, st, (const float*)y_disp, slot, w, (float*)y, s.T, s.M,
+                           s.k, nullptr, nullptr, nullptr, nullptr);
     });
   });
 }
@@ -541,11 +558,13 @@ hipError_t launch_dispatch_bwd_add(const Shape& s, const void* dx_disp, const in
     with_kmax(s.k, [&](auto kc) {
       constexpr int KMV = decltype(kc)::value;
       if (s.dtype == FLOWMOE_BF16)
-        hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV, true>), dim3(blocks),
-                           dim3(256), 0, st, (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx,
-                           s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+        with_nt(s, s.rows, [&](auto ntc) {
+          hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV, true, decltype(ntc)::value>),
+                             dim3(blocks), dim3(256), 0, st, (const bf16_t*)dx_disp, slot, nullptr,
+                             (bf16_t*)dx, s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+        });
       else
-        hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV, true>), dim3(blocks),
+        hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV, true, false>), dim3(blocks),
                            dim3(256), 0, st, (const float*)dx_disp, slot, nullptr, (float*)dx,
                            s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
     });
@@ -561,13 +580,15 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
     with_kmax(s.k, [&](auto kc) {
       constexpr int KMV = decltype(kc)::value;
       if (s.dtype == FLOWMOE_BF16)
-        hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true, KMV>), dim3(blocks), dim3(256), 0, st,
-                           (const bf16_t*)dx_disp, slot, nullptr, (bf16_t*)dx, s.T, s.M, s.k, idx, w,
-                           dw, (const bf16_t*)wgt);
+        with_nt(s, s.rows, [&](auto ntc) {
+          hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true, KMV, false, decltype(ntc)::value>),
+                             dim3(blocks), dim3(256), 0, st, (const bf16_t*)dx_disp, slot, nullptr,
+                             (bf16_t*)dx, s.T, s.M, s.k, idx, w, dw, (const bf16_t*)wgt);
+        });
       else
-        hipLaunchKernelGGL((combine_rows_kernel<float, true, KMV>), dim3(blocks), dim3(256), 0, st,
-                           (const float*)dx_disp, slot, nullptr, (float*)dx, s.T, s.M, s.k, idx, w,
-                           dw, (const float*)wgt);
+        hipLaunchKernelGGL((combine_rows_kernel<float, true, KMV, false, false>), dim3(blocks),
+                           dim3(256), 0, st, (const float*)dx_disp, slot, nullptr, (float*)dx,
+                           s.T, s.M, s.k, idx, w, dw, (const float*)wgt);
     });
   });
 }
@@ -584,12 +605,15 @@ hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp
     with_kmax(s.k, [&](auto kc) {
       constexpr int KMV = decltype(kc)::value;
       if (s.dtype == FLOWMOE_BF16)
-        hipLaunchKernelGGL((combine_bwd_kernel<bf16_t, KMV>), dim3((unsigned)blocks), dim3(256), 0, st,
-                           (const bf16_t*)dy, (const bf16_t*)y_disp, slot, w, counts,
-                           (bf16_t*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
+        with_nt(s, 2 * s.rows, [&](auto ntc) {
+          hipLaunchKernelGGL((combine_bwd_kernel<bf16_t, KMV, decltype(ntc)::value>),
+                             dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t*)dy,
+                             (const bf16_t*)y_disp, slot, w, counts, (bf16_t*)dy_disp, dw, s.T, s.M,
+                             s.k, s.E, s.C, token_blocks);
+        });
       else
-        hipLaunchKernelGGL((combine_bwd_kernel<float, KMV>), dim3((unsigned)blocks), dim3(256), 0, st,
-                           (const float*)dy, (const float*)y_disp, slot, w, counts,
+        hipLaunchKernelGGL((combine_bwd_kernel<float, KMV, false>), dim3((unsigned)blocks),
+                           dim3(256), 0, st, (const float*)dy, (const float*)y_disp, slot, w, counts,
                            (float*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
     });
   });
