@@ -203,6 +203,22 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return x * q + (x < rem ? x : rem) + i;
 }
 
+// Weight-gradient tile vbid (after xcd_remap, so that each XCD takes a
+// contiguous range): expert e, then groups of 4 m tiles that walk the mtn x
+// ntn grid m tile fastest. The 32 tiles that an XCD runs at once are 4 m x 8
+// n tiles sharing 12 operand panels through its L2 (a walk along n alone
+// shares 33: 1 A and 32 B panels); on the large layer's weight gradients
+// that walk fetched ~12x their operands' bytes from HBM.
+__device__ __forceinline__ void ksum_tile(int vbid, int mtn, int ntn, int& e, int& mt, int& nt) {
+  constexpr int G = 4;
+  e = vbid / (mtn * ntn);
+  const int rem = vbid - e * (mtn * ntn);
+  const int g = rem / (G * ntn), rg = rem - g * (G * ntn);
+  const int gm = min(G, mtn - g * G);  // m tiles in this group
+  nt = rg / gm;
+  mt = g * G + (rg - nt * gm);
+}
+
 // Epilogue shared by the bf16 kernels: the accumulators of wave (wm, wn)
 // of the tile (each WM x WN, acc[i][j][4*g + q] = C[row wm*WM + i*32 + lane%32]
 // [col wn*WN + j*32 + 8*g + 4*(lane/32) + q]) to global memory, staged
@@ -444,11 +460,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
     cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
     row0 = p.offsets[e] + mt * BM;  // first global row of this tile
   } else {
-    const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
-    e = vbid / (mtn * ntn);
-    const int rem = vbid % (mtn * ntn);
-    mt = rem / ntn;
-    nt = rem % ntn;
+    ksum_tile(vbid, (p.Mdim + BM - 1) / BM, (p.N + BN - 1) / BN, e, mt, nt);
     cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
     row0 = p.offsets[e];
   }
@@ -769,11 +781,7 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
     cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
     row0 = p.offsets[e] + mt * BM;
   } else {
-    const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
-    e = vbid / (mtn * ntn);
-    const int rem = vbid % (mtn * ntn);
-    mt = rem / ntn;
-    nt = rem % ntn;
+    ksum_tile(vbid, (p.Mdim + BM - 1) / BM, (p.N + BN - 1) / BN, e, mt, nt);
     cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
     row0 = p.offsets[e];
   }
