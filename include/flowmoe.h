@@ -246,10 +246,10 @@ enum {
   FLOWMOE_K_WGRAD2 = 10,         /* grouped GEMM dW2 = A^T dY */
   FLOWMOE_K_WGRAD1 = 11,         /* grouped GEMM [dW1 | dW3] = X^T dH */
   FLOWMOE_K_DGRAD2 = 12,         /* grouped GEMM dX = dH W1^T (+ dH3 W3^T) */
-  FLOWMOE_K_GATE_BWD_WT = 13,    /* W_g transpose (float, E x M) for the dx term */
+  FLOWMOE_K_GATE_BWD_WT = 13,    /* stacked W_g^T of the full softmax gate's dense dx term */
   FLOWMOE_K_GATE_BWD_TOKEN = 14, /* dx += d_logits W_g^T (flowmoe_gate_topk_bwd with dx) */
   FLOWMOE_K_GATE_BWD_DW = 15,    /* d_logits, and dW_g / db split-T partials */
-  FLOWMOE_K_GATE_BWD_REDUCE = 16 /* dW_g / db reduction over splits */
+  FLOWMOE_K_GATE_BWD_REDUCE = 16 /* dW_g / db reduction over splits (+ W_g^T for the dx term) */
 };
 
 /* Start tracing on the calling host thread: every later kernel launch whose

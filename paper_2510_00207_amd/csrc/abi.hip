@@ -636,20 +636,21 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     sc.signal(evC[r], s_comm);
   }
   // gate parameter gradients of AT_R..AT_1, summed over chunks in that order;
-  // W_g^T for the dx term first (the gate workspace keeps it at its front).
+  // W_g^T for the dx term (the gate workspace keeps it at its front) comes
+  // with the first chunk's dW_g reduce.
   // The full softmax gate's d_logits is dense: its dx term is a GEMM over
   // all E experts, run per chunk right after that chunk's d_logits (whose
   // bf16 copy the next chunk's overwrites) and stored into dx, to which D_r
   // then adds the experts' part
   const bool full = s.gate == FLOWMOE_GATE_FULL;
-  if (s.T > 0)
-    sc.run(full ? launch_gate_wstack(s, b->w_gate, ws_gate, s_comm)
-                : launch_gate_wt(s, b->w_gate, ws_gate, s_comm));
+  // (the sparse gate's W_g^T comes from the first chunk's dW_g reduce launch)
+  if (s.T > 0 && full) sc.run(launch_gate_wstack(s, b->w_gate, ws_gate, s_comm));
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);
     sc.mark(3, r, 0, s_comm);
     sc.run(launch_gate_dw(s, c.x, c.logits, c.idx, c.w, c.dw, c.dl, b->dw_gate, b->dbias,
-                          r != R - 1, ws_gate, s_comm));
+                          r != R - 1, ws_gate, s_comm,
+                          (r == R - 1 && !full && s.T > 0) ? b->w_gate : nullptr));
     if (full) sc.run(launch_gate_dx_full(s, ws_gate, c.dx, false, s_comm));
     sc.mark(3, r, 1, s_comm);
   }

@@ -203,14 +203,13 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
 size_t gate_bwd_ws_bytes(const Shape& s);
 inline const void* gate_ws_wgt(const void* ws) { return ws; }
 // logits: needed by the full softmax gate (nullable otherwise)
+// w_gate (nullable): the reduce launch also writes W_g^T at the front of ws
 hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, const int32_t* idx,
                           const float* w, const float* dw, float* d_logits, float* dw_gate,
-                          float* dbias, int accumulate, void* ws, hipStream_t st);
+                          float* dbias, int accumulate, void* ws, hipStream_t st,
+                          const void* w_gate = nullptr);
 hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, const float* dw,
                           const void* wgt, void* dx, hipStream_t st);
-// W_g (M x E) -> W_g^T (E x M, both in the layer dtype: an exact copy) at the
-// front of the gate workspace
-hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st);
 hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, const float* logits,
                            const int32_t* idx, const float* w, const float* dw, float* d_logits,
                            float* dw_gate, float* dbias, void* dx, int accumulate, void* ws,

@@ -474,19 +474,8 @@ __device__ __forceinline__ void token_dl(const int32_t* __restrict__ idx, const 
   for (int j = 0; j < kMaxK; ++j) dl[j] = (j < k) ? wj[j] * (dwj[j] - s) : 0.f;
 }
 
-// W_g (M x E, layer dtype) -> W_g^T (E x M, float), so that the dx term reads
-// 8 consecutive m of one expert as two 16-byte vectors
-template <typename TIn>
-__global__ __launch_bounds__(256) void transpose_wg_kernel(const TIn* __restrict__ wg,
-                                                           TIn* __restrict__ wgt, int M, int E) {
-  const long n = (long)M * E;
-  for (long q = blockIdx.x * 256L + threadIdx.x; q < n; q += (long)gridDim.x * 256) {
-    const int e = (int)(q / M), m = (int)(q % M);
-    wgt[q] = wg[(long)m * E + e];
-  }
-}
-
-// dx[t] += dl_t W_g^T, one wave per token
+// dx[t] += dl_t W_g^T, one wave per token (W_g^T: E x M in the layer dtype,
+// so that each selected expert's 8 consecutive m are one 16-byte load)
 template <typename TIn>
 __global__ __launch_bounds__(256) void gate_bwd_dx_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
@@ -692,10 +681,24 @@ __global__ __launch_bounds__(256) void gate_wstack_kernel(const bf16_t* __restri
 // dW_g[m][e] = sum over splits of P[s][m][e] (split order; rows of pitch
 // ldp), plus the same sum over column lo_off + e when lo_off >= 0 (the lo
 // halves of the bf16 path); db = sum over the SB rows of Pb
+// Blocks past the reduction's (wt_block and on, when wg is given) copy W_g
+// (M x E) to W_g^T (E x M) in the layer dtype for the dx term: one launch
+// less than a kernel of its own.
 __global__ __launch_bounds__(256) void gate_bwd_dw_reduce_kernel(
     const float* __restrict__ P, const float* __restrict__ Pb, float* __restrict__ dw_gate,
-    float* __restrict__ dbias, int M, int E, int S, int ldp, int lo_off, int SB, int accumulate) {
+    float* __restrict__ dbias, int M, int E, int S, int ldp, int lo_off, int SB, int accumulate,
+    const void* __restrict__ wg, void* __restrict__ wgt, int wt_block, int bf) {
   const long n = (long)M * E;
+  if (wg != nullptr && (int)blockIdx.x >= wt_block) {
+    const long r = ((long)blockIdx.x - wt_block) * 256 + threadIdx.x;
+    if (r >= n) return;
+    const long e = r / M, m = r % M;
+    if (bf)
+      static_cast<bf16_t*>(wgt)[r] = static_cast<const bf16_t*>(wg)[m * E + e];
+    else
+      static_cast<float*>(wgt)[r] = static_cast<const float*>(wg)[m * E + e];
+    return;
+  }
   const long q = blockIdx.x * 256L + threadIdx.x;
   if (q >= n + E) return;
   if (q < n) {
@@ -880,19 +883,6 @@ hipError_t launch_gate_dx_full(const Shape& s, void* ws, void* dx, bool add, hip
                              gate_dw_splits(s), dx, add, st);
 }
 
-hipError_t launch_gate_wt(const Shape& s, const void* w_gate, void* ws, hipStream_t st) {
-  const long n = (long)s.M * s.E;
-  const int nb = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
-  return traced(FLOWMOE_K_GATE_BWD_WT, st, [&] {
-    if (s.dtype == FLOWMOE_BF16)
-      hipLaunchKernelGGL(transpose_wg_kernel<bf16_t>, dim3(nb), dim3(256), 0, st,
-                         (const bf16_t*)w_gate, static_cast<bf16_t*>(ws), s.M, s.E);
-    else
-      hipLaunchKernelGGL(transpose_wg_kernel<float>, dim3(nb), dim3(256), 0, st,
-                         (const float*)w_gate, static_cast<float*>(ws), s.M, s.E);
-  });
-}
-
 hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, const float* dw,
                           const void* wgt, void* dx, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
@@ -909,17 +899,21 @@ hipError_t launch_gate_dx(const Shape& s, const int32_t* idx, const float* w, co
 
 hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, const int32_t* idx,
                           const float* w, const float* dw, float* d_logits, float* dw_gate,
-                          float* dbias, int accumulate, void* ws, hipStream_t st) {
+                          float* dbias, int accumulate, void* ws, hipStream_t st,
+                          const void* w_gate) {
   const GateWs g = gate_ws(s, ws);
   const bool bf = s.dtype == FLOWMOE_BF16;
   const long n = (long)s.M * s.E + s.E;
   const int nred = (int)((n + 255) / 256);
+  // with w_gate, the reduce launch also writes W_g^T at the front of ws
+  const int ntr = w_gate != nullptr ? (int)(((long)s.M * s.E + 255) / 256) : 0;
   if (s.T == 0) {
     // with no tokens the gradient is zero: a reduce over zero splits writes it
-    if (accumulate) return hipSuccess;
+    if (accumulate && ntr == 0) return hipSuccess;
     return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
-      hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred), dim3(256), 0, st, g.P, g.Pb,
-                         dw_gate, dbias, s.M, s.E, 0, s.E, -1, 0, 0);
+      hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(accumulate ? ntr : nred + ntr), dim3(256),
+                         0, st, g.P, g.Pb, dw_gate, dbias, s.M, s.E, 0, s.E, -1, 0, 0, w_gate, ws,
+                         accumulate ? 0 : nred, (int)bf);
     });
   }
   if (gate_dw_on_gemm(s)) {
@@ -938,8 +932,9 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, co
     e = launch_gate_dw_gemm(x, s.T, s.M, g.dlhl, N, g.counts, g.offsets, S, g.P, st);
     if (e != hipSuccess) return e;
     return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
-      hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred), dim3(256), 0, st, g.P, g.Pb,
-                         dw_gate, dbias, s.M, s.E, S, N, N / 2, nb, accumulate);
+      hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred + ntr), dim3(256), 0, st, g.P, g.Pb,
+                         dw_gate, dbias, s.M, s.E, S, N, N / 2, nb, accumulate, w_gate, ws, nred,
+                         (int)bf);
     });
   }
   const int S = gate_splits(s);
@@ -967,8 +962,8 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, co
   });
   if (e != hipSuccess) return e;
   return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
-    hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred), dim3(256), 0, st, g.P, g.Pb, dw_gate,
-                       dbias, s.M, s.E, S, s.E, -1, S, accumulate);
+    hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred + ntr), dim3(256), 0, st, g.P, g.Pb,
+                       dw_gate, dbias, s.M, s.E, S, s.E, -1, S, accumulate, w_gate, ws, nred, (int)bf);
   });
 }
 
@@ -976,16 +971,17 @@ hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, co
                            const int32_t* idx, const float* w, const float* dw, float* d_logits,
                            float* dw_gate, float* dbias, void* dx, int accumulate, void* ws,
                            hipStream_t st) {
+  const bool full = s.gate == FLOWMOE_GATE_FULL;
+  // the sparse dx term reads W_g^T, which the dW_g reduce launch writes
+  const bool wt = dx != nullptr && s.T > 0 && !full;
   hipError_t e = launch_gate_dw(s, x, logits, idx, w, dw, d_logits, dw_gate, dbias, accumulate, ws,
-                                st);
+                                st, wt ? w_gate : nullptr);
   if (e != hipSuccess || dx == nullptr || s.T == 0) return e;
-  if (s.gate == FLOWMOE_GATE_FULL) {  // dense d_logits: dx += [hi | lo] [W_g^T ; W_g^T]
+  if (full) {  // dense d_logits: dx += [hi | lo] [W_g^T ; W_g^T]
     e = launch_gate_wstack(s, w_gate, ws, st);
     if (e != hipSuccess) return e;
     return launch_gate_dx_full(s, ws, dx, true, st);
   }
-  e = launch_gate_wt(s, w_gate, ws, st);
-  if (e != hipSuccess) return e;
   return launch_gate_dx(s, idx, w, dw, gate_ws_wgt(ws), dx, st);
 }
 
