@@ -521,7 +521,12 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_kernel(
     float* __restrict__ Pb, int T, int M, int E, int k, int tokens_per_split) {
   constexpr int TL = 32 / EG;
   constexpr int NE = 8 * EG;  // experts covered by the block
-  __shared__ float red[TL][64 + 1][NE];
+  // partial tiles by token lane: row i of the 8 x 8 tile of column group mg
+  // at red[tl * RS + (i * 8 + mg) * NE + e], so that the 8 lanes of one tl
+  // (mg = 0..7) write 8 consecutive runs of NE floats, and the lanes of
+  // successive tl start 4 banks apart; the bias row at i = 8, mg = 0
+  constexpr int RS = 9 * 8 * NE + 4;
+  __shared__ float red[TL * RS];
   const int tid = threadIdx.x;
   const int mg = tid & 7, eg = (tid >> 3) % EG, tl = tid / (8 * EG);
   const int m0 = blockIdx.x * 64 + mg * 8;
@@ -578,18 +583,20 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_kernel(
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) red[tl][mg * 8 + i][e0 + q] = acc[i][q];
+    for (int q = 0; q < 8; ++q) red[tl * RS + (i * 8 + mg) * NE + e0 + q] = acc[i][q];
   if (first_tile && mg == 0) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) red[tl][64][e0 + q] = accb[q];
+    for (int q = 0; q < 8; ++q) red[tl * RS + 64 * NE + e0 + q] = accb[q];
   }
   __syncthreads();
   const int rows = first_tile ? 65 : 64;
   for (int q = tid; q < rows * NE; q += 256) {
     const int mm = q / NE, e = q % NE;
     if (e >= E) continue;
+    // row mm = 8 mg + i of the m tile (mm = 64: the bias row)
+    const int at = (mm == 64 ? 64 : (mm & 7) * 8 + (mm >> 3)) * NE + e;
     float v = 0.f;
-    for (int l = 0; l < TL; ++l) v += red[l][mm][e];
+    for (int l = 0; l < TL; ++l) v += red[l * RS + at];
     if (mm == 64) {
       Pb[(long)s * E + e] = v;
     } else {
