@@ -72,7 +72,9 @@ def memory_bound(L, layer, cfg, torch, reps: int = 20, flush=None):
     timed steps, and small enough here to stay in the 256 MB Infinity Cache),
     against the algorithmic bytes of the step (kept rows A of the chunk):
       gate T*M*b; dispatch (scan + gather) (T + A)*M*b; combine (A + T)*M*b;
-      combine bwd (T + 2A)*M*b; dispatch bwd (A + T)*M*b; gate bwd T*M*b.
+      combine bwd (T + 2A)*M*b; dispatch bwd (A + T)*M*b; gate bwd T*M*b, except
+      for one selected expert under the renormalised gate, whose gradient is
+      exactly zero: then the d_logits and dW_g written, (T + M)*E*4.
     With a `flush` buffer (int64, >= 512 MiB) each step is also timed with
     cold caches (the *_flushed figures)."""
     s = layer.shape
@@ -85,6 +87,7 @@ def memory_bound(L, layer, cfg, torch, reps: int = 20, flush=None):
     dw, dl, slot = layer.d_topk_w[:T], layer.d_logits[:T], layer.slot[:T]
     cnt, off, rs, ld = layer.counts[0], layer.offsets[0], layer.row_src[0], layer.load[0]
     xd, yd, dyd, dxd = layer.x_disp[0], layer.y_disp[0], layer.dy_disp[0], layer.dx_disp[0]
+    zero_gate = k == 1 and cfg.gate != "full"
     steps = {
         "gate": (lambda: L.flowmoe_gate_topk(s, x, layer.w_gate, layer.bias, lg, idx, w, stream=st),
                  T * M * b),
@@ -100,7 +103,8 @@ def memory_bound(L, layer, cfg, torch, reps: int = 20, flush=None):
         "gate bwd (d_logits, dW_g)": (
             lambda: L.flowmoe_gate_topk_bwd(s, x, layer.w_gate, lg, idx, w, dw, dl, layer.dw_gate,
                                             layer.dbias, None, 0, layer.ws, layer.ws_bytes,
-                                            stream=st), T * M * b),
+                                            stream=st),
+            (T + M) * E * 4 if zero_gate else T * M * b),
     }
     out = {}
     flush_sum = torch.zeros((), dtype=torch.int64, device=x.device)

@@ -650,7 +650,8 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     sc.mark(3, r, 0, s_comm);
     sc.run(launch_gate_dw(s, c.x, c.logits, c.idx, c.w, c.dw, c.dl, b->dw_gate, b->dbias,
                           r != R - 1, ws_gate, s_comm,
-                          (r == R - 1 && !full && s.T > 0) ? b->w_gate : nullptr));
+                          (r == R - 1 && !full && s.T > 0 && !gate_grad_zero(s)) ? b->w_gate
+                                                                                : nullptr));
     if (full) sc.run(launch_gate_dx_full(s, ws_gate, c.dx, false, s_comm));
     sc.mark(3, r, 1, s_comm);
   }
@@ -675,9 +676,12 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     Chunk c = chunk_of(s, b, r);
     sc.wait(s_comm, evE[r]);
     sc.mark(2, r, 0, s_comm);
+    // (d_logits = 0 for one selected expert: the dispatch backward alone)
     sc.run(full ? launch_dispatch_bwd_add(s, c.dx_disp, c.slot, c.dx, s_comm)
-                : launch_dispatch_bwd_gate(s, c.dx_disp, c.slot, c.idx, c.w, c.dw,
-                                           gate_ws_wgt(ws_gate), c.dx, s_comm));
+           : gate_grad_zero(s)
+               ? launch_dispatch_bwd(s, c.dx_disp, c.slot, c.dx, s_comm)
+               : launch_dispatch_bwd_gate(s, c.dx_disp, c.slot, c.idx, c.w, c.dw,
+                                          gate_ws_wgt(ws_gate), c.dx, s_comm));
     sc.mark(2, r, 1, s_comm);
   }
   sc.signal(evEnd, s_comm);

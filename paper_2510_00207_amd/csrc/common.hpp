@@ -203,6 +203,11 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
 size_t gate_bwd_ws_bytes(const Shape& s);
 inline const void* gate_ws_wgt(const void* ws) { return ws; }
 // logits: needed by the full softmax gate (nullable otherwise)
+// One selected expert under the renormalised gate: its weight is exactly 1,
+// so d_logits = w (dw - w dw) is exactly zero, and with it dW_g, db and the
+// gate's share of dx; the gate backward then writes those zeros without
+// reading x (the full softmax gate's top-1 has a nonzero gradient).
+inline bool gate_grad_zero(const Shape& s) { return s.k == 1 && s.gate != FLOWMOE_GATE_FULL; }
 // w_gate (nullable): the reduce launch also writes W_g^T at the front of ws
 hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, const int32_t* idx,
                           const float* w, const float* dw, float* d_logits, float* dw_gate,

@@ -730,6 +730,10 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_reduce_kernel(
   }
 }
 
+__global__ __launch_bounds__(256) void zero_f32_kernel(float* __restrict__ p, long n) {
+  for (long q = blockIdx.x * 256L + threadIdx.x; q < n; q += (long)gridDim.x * 256) p[q] = 0.f;
+}
+
 int gate_eg(int E) { return E <= 8 ? 1 : E <= 16 ? 2 : E <= 32 ? 4 : 8; }
 
 // bf16 path: the GEMM's column count (hi and lo halves of E rounded up to 4)
@@ -914,8 +918,18 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, co
   const int nred = (int)((n + 255) / 256);
   // with w_gate, the reduce launch also writes W_g^T at the front of ws
   const int ntr = w_gate != nullptr ? (int)(((long)s.M * s.E + 255) / 256) : 0;
-  if (s.T == 0) {
-    // with no tokens the gradient is zero: a reduce over zero splits writes it
+  if (gate_grad_zero(s) && s.T > 0) {
+    // d_logits is exactly zero: nothing of x is read
+    const long nz = (long)s.T * s.E;
+    hipError_t e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
+      hipLaunchKernelGGL(zero_f32_kernel, dim3((unsigned)((nz + 255) / 256 < 1024 ? (nz + 255) / 256 : 1024)),
+                         dim3(256), 0, st, d_logits, nz);
+    });
+    if (e != hipSuccess) return e;
+  }
+  if (s.T == 0 || gate_grad_zero(s)) {
+    // with no tokens (or d_logits = 0) the gradient is zero: a reduce over
+    // zero splits writes it
     if (accumulate && ntr == 0) return hipSuccess;
     return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
       hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(accumulate ? ntr : nred + ntr), dim3(256),
@@ -979,7 +993,9 @@ hipError_t launch_gate_bwd(const Shape& s, const void* x, const void* w_gate, co
                            float* dw_gate, float* dbias, void* dx, int accumulate, void* ws,
                            hipStream_t st) {
   const bool full = s.gate == FLOWMOE_GATE_FULL;
-  // the sparse dx term reads W_g^T, which the dW_g reduce launch writes
+  // the sparse dx term reads W_g^T, which the dW_g reduce launch writes (with
+  // d_logits = 0 the term is zero: dx is left as it is)
+  if (gate_grad_zero(s)) dx = nullptr;
   const bool wt = dx != nullptr && s.T > 0 && !full;
   hipError_t e = launch_gate_dw(s, x, logits, idx, w, dw, d_logits, dw_gate, dbias, accumulate, ws,
                                 st, wt ? w_gate : nullptr);

@@ -483,6 +483,46 @@ def test_gate_bwd_shapes(T, M, E, k):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("M,E", [(1024, 16), (520, 64)])
+def test_gate_bwd_top1_is_exactly_zero(dtype, M, E):
+    """One selected expert under the renormalised gate: its weight is exactly
+    1, so d_logits = w (dw - w dw) = 0 exactly (Sec. 2.1's gate with a
+    single survivor), and so are dW_g, db and the dx term. The call writes
+    those zeros over garbage, leaves accumulated gradients as they were and
+    dx untouched, whichever dW_g path the shape would take; the oracle
+    agrees."""
+    need_gpu()
+    rng = np.random.default_rng(M + E)
+    d = dev()
+    T = 777
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x = torch.from_numpy(rng.standard_normal((T, M))).to(d).to(dt)
+    wg = torch.from_numpy(rng.standard_normal((M, E)) * 0.05).to(d).to(dt)
+    idx, w = oracle.topk_select(rng.standard_normal((T, E)), 1)
+    assert np.all(w == 1.0)
+    dtw = rng.standard_normal((T, 1))
+    t = lambda a, ty: torch.from_numpy(np.ascontiguousarray(a)).to(d).to(ty)
+    s = _shape(T, M, 8, E, 1, 0, dtype)
+    nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
+    ws = torch.empty(nws, dtype=torch.uint8, device=d)
+    for acc in (0, 1):
+        dlog = torch.full((T, E), 7.0, device=d)
+        dwg = torch.full((M, E), 3.0, device=d)
+        db = torch.full((E,), 3.0, device=d)
+        dx = torch.from_numpy(rng.standard_normal((T, M))).to(d).to(dt)
+        dx0 = dx.clone()
+        L.flowmoe_gate_topk_bwd(s, x, wg, None, t(idx, torch.int32), t(w, torch.float32),
+                                t(dtw, torch.float32), dlog, dwg, db, dx, acc, ws, nws)
+        torch.cuda.synchronize()
+        assert torch.all(dlog == 0)
+        want = 3.0 if acc else 0.0
+        assert torch.all(dwg == want) and torch.all(db == want)
+        assert torch.equal(dx, dx0)
+    g = oracle.gate_bwd(host(x), host(wg), idx, w, dtw)
+    assert np.all(g["d_logits"] == 0) and np.all(g["dw_gate"] == 0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
 def test_combine_and_backward_steps(dtype, layout):
     need_gpu()
