@@ -220,6 +220,9 @@ flowmoe_status_t flowmoe_dispatch_bwd(const flowmoe_shape_t* shape, const void* 
  * dbias = column sums of d_logits (E float, nullable). If dx is given,
  * dx += d_logits W_g^T (T x M layer dtype, read-modify-write). accumulate
  * != 0 adds dw_gate and dbias to the existing values (sum over chunks).
+ * With k = 1 under FLOWMOE_GATE_RENORM the single weight is exactly 1 and
+ * d_logits is exactly zero: the call writes the zeros (d_logits; dw_gate
+ * and dbias unless accumulating), leaves dx as it is and reads nothing of x.
  *   ws: flowmoe_workspace_bytes(shape, FLOWMOE_WS_GATE_BWD) bytes. */
 flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void* x,
                                        const void* w_gate, const float* logits,
