@@ -344,7 +344,9 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
     for (int j = 0; j < KM; ++j)
       if (j < k) gl[j] = gl[j] * (gdw[(long)t * k + j] - s);
   }
-  constexpr int U = sizeof(TE) == 2 ? 2 : 1;
+  // steps of 512 elements loaded together: 4 in the non-temporal (>= 256 MB)
+  // bf16 calls of tokens with at most two experts, else 2 (bf16) or 1
+  constexpr int U = sizeof(TE) == 2 ? ((NT && KM <= 2) ? 4 : 2) : 1;
   for (int m0 = lane * 8; m0 < M; m0 += 64 * 8 * U) {
     decltype(raw8_load(src)) raw[U][KM];
     decltype(raw8_load(src)) yold[ADD ? U : 1];
@@ -429,7 +431,9 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
     }
   }
   // dy and the k rows of y_disp of U steps loaded before any is used
-  constexpr int U = sizeof(TE) == 2 ? 2 : 1;
+  // steps of 512 elements loaded together: 4 in the non-temporal (>= 256 MB)
+  // bf16 calls of tokens with at most two experts, else 2 (bf16) or 1
+  constexpr int U = sizeof(TE) == 2 ? ((NT && KM <= 2) ? 4 : 2) : 1;
   for (int m0 = lane * 8; m0 < M; m0 += 64 * 8 * U) {
     decltype(raw8_load(dy)) graw[U], raw[U][KM];
 #pragma unroll
