@@ -5,15 +5,16 @@ capacity-bounded dispatch, grouped-GEMM experts, combine (forward), then
 combine backward, expert backward (dgrad + wgrad), dispatch backward and gate
 backward, through flowmoe_layer_fwd / flowmoe_layer_bwd on two HIP streams.
 
-Workload: the balanced MoE layer, T = 4096 tokens (8 x 512), M = 1024,
-H = 4096, E = 8, top-2, capacity factor 1.2, GELU experts, bf16 storage with
-fp32 accumulation, one chunk (R = 1), packed dispatch layout. Inputs are
-seeded synthetic tensors already resident in HBM.
+Workload (default): the large-expert MoE layer, one GPU's share of a
+Mixtral-shaped layer: T = 16384 tokens, M = 4096, H = 14336, E = 8 local
+experts, top-2, capacity factor 1.25, SwiGLU experts, bf16 storage with fp32
+accumulation, one chunk (R = 1), packed dispatch layout. Inputs are seeded
+synthetic tensors already resident in HBM.
 
 Prints one JSON line with tokens/s, the grouped-GEMM roofline (algorithmic
 FLOPs per launch over the average launch time, from HIP events recorded
 around every GEMM launch of the timed steps) and the fp64 CPU oracle timed on
-one full step of the same inputs.
+a bounded token sample of the same inputs (whole steps for the small layers).
 """
 from __future__ import annotations
 
@@ -29,7 +30,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-WORKLOAD = "balanced"
+WORKLOAD = "large"
 
 
 def parse():
@@ -38,7 +39,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=WORKLOAD,
-                    help="balanced (default) | skewed | large | fine | tiny")
+                    help="large (default) | balanced | skewed | fine | tiny")
     ap.add_argument("--layout", default="packed")
     ap.add_argument("--gate", default="renorm", choices=("renorm", "full"),
                     help="gate weights: softmax over the k selected (renorm) or the selected "
@@ -58,12 +59,55 @@ def parse():
     return ap.parse_args()
 
 
-def gemm_flops_per_launch(cfg, kept: int) -> float:
-    """Algorithmic FLOPs of one grouped-GEMM launch: every expert GEMM of the
-    layer multiplies the kept rows by an M x H (or H x M) weight, so each
-    launch does 2 * kept * M * H (SwiGLU's fused W1|W3 launch, its
-    [dW1 | dW3] launch and its K = 2H dgrad launch do twice that)."""
-    return 2.0 * kept * cfg.M * cfg.H
+def gemm_flops(cfg, kind: str, rows: float) -> float:
+    """Algorithmic FLOPs of one grouped-GEMM launch of `kind` over `rows` kept
+    rows: every expert GEMM multiplies those rows by an M x H (or H x M)
+    weight, 2 * rows * M * H; SwiGLU's fused W1|W3 forward, its [dW1 | dW3]
+    weight gradient and its K = 2H dgrad do twice that. The row-mode launches
+    (ffn1, ffn2, dgrad1, dgrad2) cover one chunk's rows; the two weight-gradient
+    launches reduce over the rows of all R chunks at once."""
+    two = 2.0 if cfg.act == "swiglu" else 1.0
+    mult = {"ffn1": two, "ffn2": 1.0, "dgrad1": 1.0, "dgrad2": two, "wgrad2": 1.0, "wgrad1": two}
+    return 2.0 * rows * cfg.M * cfg.H * mult[kind]
+
+
+def gemm_flops_per_step(cfg, kept: int) -> float:
+    """All expert-GEMM FLOPs of one fwd+bwd step: 12 M H (GELU) or 18 M H
+    (SwiGLU) per kept row."""
+    return (18.0 if cfg.act == "swiglu" else 12.0) * kept * cfg.M * cfg.H
+
+
+def oracle_sample_tokens(cfg, R: int) -> int:
+    """Tokens of the CPU oracle's sample: the whole batch when one fp64 step
+    is cheap, else the largest power-of-two number of tokens (a multiple of
+    R) whose expert FLOPs stay under 6e11, so that the sample takes seconds,
+    not minutes, of host time (the large layer's 1024 tokens took 191 s on
+    8 cores: its numpy backward runs near 35 GFLOP/s)."""
+    per_token = 2.0 * cfg.k * cfg.M * cfg.H * (9.0 if cfg.act == "swiglu" else 6.0)
+    t = cfg.T
+    while t > R and t * per_token > 6e11:
+        t //= 2
+    return max(R, (t // R) * R)
+
+
+def widen_f64(a):
+    """A stored tensor widened exactly to float64 (moe_inputs.as_f64), in
+    blocks on the host's cores (the large layer's weights are 1.4e9
+    elements)."""
+    import concurrent.futures as cf
+
+    import numpy as np
+    from moe_inputs import as_f64
+    flat = a.reshape(-1)
+    out = np.empty(flat.shape[0], dtype=np.float64)
+    blk = 1 << 24
+
+    def one(lo):
+        out[lo:lo + blk] = as_f64(flat[lo:lo + blk])
+
+    with cf.ThreadPoolExecutor(max(1, min(16, len(os.sched_getaffinity(0))))) as ex:
+        list(ex.map(one, range(0, flat.shape[0], blk)))
+    return out.reshape(a.shape)
 
 
 def memory_bound(L, layer, cfg, torch, reps: int = 20, flush=None):
@@ -216,7 +260,8 @@ def main():
     # events on its stream, for the per-launch durations (a timestamped event
     # around every launch adds ~2 us of idle per event to the step, so this
     # pass is kept out of the throughput)
-    gemm_per_step = 6 * R
+    # (per step: ffn1, ffn2, dgrad1, dgrad2 per chunk; wgrad1, wgrad2 once)
+    gemm_per_step = 4 * R + 2
     ev = EventArray(gemm_per_step * a.steps)
     L.flowmoe_trace_start(ev.ev, ev.kinds, ev.pairs, L.kind_mask(L.K_GEMM))
     torch.cuda.synchronize()
@@ -248,13 +293,27 @@ def main():
 
     ms_per_step = elapsed / a.steps * 1e3
     tokens_per_s = cfg.T * a.steps / elapsed
-    # each launch covers one chunk: average FLOPs per launch use kept / R rows
-    # (exact for the sum, as every chunk's six launches appear once per step)
-    fl = gemm_flops_per_launch(cfg, kept / R)
-    mult = {"ffn1": 2.0 if cfg.act == "swiglu" else 1.0, "ffn2": 1.0, "dgrad1": 1.0, "wgrad2": 1.0,
-            "wgrad1": 2.0 if cfg.act == "swiglu" else 1.0,
-            "dgrad2": 2.0 if cfg.act == "swiglu" else 1.0}
-    tot_flops = sum(fl * mult[k] for k in gemm_kinds)
+    # algorithmic FLOPs of the traced launches: each row-mode launch covers
+    # one chunk (its kept rows), each weight-gradient launch all R chunks;
+    # chunks are enqueued once per step in a fixed order, so the launches of
+    # one step come in the same order every step
+    chunk_kept = [int(v) for v in layer.counts.sum(dim=1).tolist()]
+    assert n == gemm_per_step * a.steps, (n, gemm_per_step, a.steps)
+    tot_flops = 0.0
+    for s0 in range(0, n, gemm_per_step):
+        seen = {}
+        for kd in gemm_kinds[s0:s0 + gemm_per_step]:
+            if kd.startswith("wgrad"):
+                tot_flops += gemm_flops(cfg, kd, kept)
+            else:
+                i = seen.get(kd, 0)
+                seen[kd] = i + 1
+                # forward kinds run chunks 0..R-1, backward kinds R-1..0
+                r = i if kd in ("ffn1", "ffn2") else R - 1 - i
+                tot_flops += gemm_flops(cfg, kd, chunk_kept[r])
+    step_flops = gemm_flops_per_step(cfg, kept)
+    assert abs(tot_flops - step_flops * a.steps) <= 1e-6 * step_flops * a.steps, (tot_flops, step_flops)
+    fl = tot_flops / max(1, n)
     tot_s = sum(gemm_ms) / 1e3
     avg_launch_ms = sum(gemm_ms) / max(1, len(gemm_ms))
     achieved_tflops = tot_flops / tot_s / 1e12 if tot_s > 0 else 0.0
@@ -291,24 +350,32 @@ def main():
     cpu = None
     if not a.no_cpu_baseline:
         import oracle
-        from moe_inputs import as_f64
         from threadpoolctl import threadpool_info
-        i64 = {k: (None if v is None else (v.astype(np.float64) if k == "bias" else as_f64(v)))
+        # a bounded sample of the same workload: the first Ts tokens, R
+        # chunks of Ts / R, the same weights and capacity factor (whole steps
+        # when they are cheap); weights widened to fp64 before the clock starts
+        Ts = oracle_sample_tokens(cfg, R)
+        i64 = {k: (None if v is None else (v.astype(np.float64) if k == "bias" else
+                                           widen_f64(v[:Ts] if k in ("x", "dy") else v)))
                for k, v in inp.items()}
-        # whole fwd+bwd steps of the same inputs, repeated until ~10 s of CPU work
+        del inp
         reps, c0 = 0, time.perf_counter()
         while True:
-            oracle.layer_fwd_bwd(i64, k=cfg.k, f=cfg.f, act=cfg.act, R=R, layout=a.layout)
+            oracle.layer_fwd_bwd(i64, k=cfg.k, f=cfg.f, act=cfg.act, R=R, layout=a.layout,
+                                 gate=cfg.gate)
             reps += 1
             if time.perf_counter() - c0 >= 10.0 or reps >= 20:
                 break
         c1 = time.perf_counter()
         threads = max([p.get("num_threads", 1) for p in threadpool_info()
                        if p.get("user_api") == "blas"] or [1])
-        cpu = {"value": round(cfg.T * reps / (c1 - c0), 2), "unit": "tokens/s", "cores": threads,
-               "kind": "oracle",
-               "sample": f"{reps} full fwd+bwd step(s) of the {cfg.name} workload ({cfg.T} tokens "
-                         f"each), numpy fp64, {c1 - c0:.1f} s"}
+        what = (f"{reps} full fwd+bwd step(s) of the {cfg.name} workload ({cfg.T} tokens each)"
+                if Ts == cfg.T else
+                f"{reps} fwd+bwd step(s) of the first {Ts} of the {cfg.name} workload's {cfg.T} "
+                f"tokens ({R} chunk(s), capacity from f = {cfg.f} at that size, all {cfg.E} "
+                f"experts' full weights)")
+        cpu = {"value": round(Ts * reps / (c1 - c0), 2), "unit": "tokens/s", "cores": threads,
+               "kind": "oracle", "sample": f"{what}, numpy fp64, {c1 - c0:.1f} s"}
 
     # the library's schedule: one chunk runs its forward on one stream, and its
     # backward on two only for layers whose expert GEMMs span many rounds
@@ -343,7 +410,7 @@ def main():
             "kept_rows": kept,
         },
         "roofline": {
-            "kernel": "grouped GEMM (gemm_dma_kernel, all 6 launches of a step)",
+            "kernel": f"grouped GEMM (gemm_dma_kernel, all {gemm_per_step} launches of a step)",
             "bound": "mfma",
             "achieved": round(achieved_tflops, 2),
             "peak": PEAK_BF16_TFLOPS,
@@ -352,6 +419,7 @@ def main():
             "traffic": traffic,
             "traffic_note": traffic_note,
             "flops_per_launch": fl,
+            "flops_per_step": step_flops,
             "avg_launch_us": round(avg_launch_ms * 1e3, 2),
             "launches": len(gemm_ms),
             "launch_timing": (f"HIP events around every GEMM launch of a second pass of the "

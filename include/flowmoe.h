@@ -92,10 +92,12 @@ const char* flowmoe_version(void);
 /* Message of the last non-OK status returned on this host thread ("" if none). */
 const char* flowmoe_last_error(void);
 
-/* Expert capacity C = ceil(f * k * T / E) (Sec. 2.1, C = f*k*B*N/E), with a
- * relative slack of 1e-9 so that products that are integers in decimal
- * arithmetic (e.g. f = 1.1) are not rounded up by binary rounding error.
- * Returns -1 for T < 0, E < 1, k < 1 or f <= 0. */
+/* Expert capacity C = ceil(f * k * T / E) (Sec. 2.1, C = f*k*B*N/E), computed
+ * exactly on the decimal value of f: the shortest decimal that reads back
+ * as f (1.1, not the binary value 1.10000000000000008882), so that products
+ * that are integers in decimal arithmetic are not rounded up by binary
+ * rounding error. Returns -1 for T < 0, E < 1, k < 1, f <= 0 or not finite,
+ * or a capacity above INT32_MAX. */
 int32_t flowmoe_capacity(int32_t T, int32_t E, int32_t k, double f);
 
 /* Rows of the dispatched buffers for `shape`: E*C (padded) or
@@ -281,6 +283,20 @@ enum { FLOWMOE_TILES_AUTO = 0, FLOWMOE_TILES_WIDE = 1, FLOWMOE_TILES_NARROW = 2 
  * (for tests and tuning). FLOWMOE_ERR_INVALID for another value. */
 flowmoe_status_t flowmoe_set_gemm_tiles(int32_t tiles);
 
+/* ---- row streams of the dispatch and combine kernels ----------------------- */
+
+/* How the row kernels (dispatch gather/scatter, combine, their backward and
+ * the dispatch backward) move bf16 rows. AUTO, the default: non-temporal
+ * loads and stores for calls that move at least 256 MB (more than the
+ * Infinity Cache holds, so caching the stream only evicts data that is read
+ * again), cached ones below. NT and CACHED force one kind for every bf16
+ * call; fp32 calls always go through the caches. Results are identical. */
+enum { FLOWMOE_ROWS_AUTO = 0, FLOWMOE_ROWS_NT = 1, FLOWMOE_ROWS_CACHED = 2 };
+
+/* Set the row-stream kind for launches enqueued after the call, process-wide
+ * (for tests and tuning). FLOWMOE_ERR_INVALID for another value. */
+flowmoe_status_t flowmoe_set_row_streams(int32_t mode);
+
 /* ---- the R-chunk two-stream layer (Sec. 3.2, Eqs. 3-6) -------------------- */
 
 /* Buffers of a whole layer over R chunks of shape->T tokens each. Per-token
@@ -356,9 +372,10 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
  * gradients). dW_g and db are summed over chunks in R..1 order.
  * bufs->h_save is consumed: each chunk's h_save is overwritten with its dH
  * (rows x H for GELU, rows x 2H = [dH1 | dH3] for SwiGLU).
- * trace (nullable): 8*R events as for the forward, task 0 = combine bwd,
- * 1 = experts bwd (chunk 1's span also covers the weight gradients),
- * 2 = dispatch bwd (+ gate dx term), 3 = gate parameter gradients.
+ * trace (nullable): 8*R + 2 events, the first 8*R as for the forward with
+ * task 0 = combine bwd, 1 = experts bwd (dH and dX of the chunk),
+ * 2 = dispatch bwd (+ gate dx term), 3 = gate parameter gradients; the last
+ * two (index 8*R, 8*R + 1) span the expert weight gradients.
  * With R = 1 the two streams are used only for large layers (capacity rows
  * x M x H >= 2.5e11), where the expert GEMMs span many rounds of the compute
  * units; smaller ones run everything on s_compute. */

@@ -86,6 +86,7 @@ def load():
         "flowmoe_trace_start": ([P, P, I32, ctypes.c_uint32], I32),
         "flowmoe_trace_stop": ([], I32),
         "flowmoe_set_gemm_tiles": ([I32], I32),
+        "flowmoe_set_row_streams": ([I32], I32),
         "flowmoe_layer_fwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
         "flowmoe_layer_bwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
     }
@@ -239,6 +240,15 @@ def flowmoe_set_gemm_tiles(tiles: str | int) -> None:
     _check(load().flowmoe_set_gemm_tiles(TILES[tiles] if isinstance(tiles, str) else tiles))
 
 
+ROW_STREAMS = {"auto": 0, "nt": 1, "cached": 2}
+
+
+def flowmoe_set_row_streams(mode: str | int) -> None:
+    """Row-stream kind of the dispatch/combine kernels for later launches:
+    "auto", "nt" (non-temporal) or "cached", or the FLOWMOE_ROWS_* value."""
+    _check(load().flowmoe_set_row_streams(ROW_STREAMS[mode] if isinstance(mode, str) else mode))
+
+
 # ---- R-chunk layer ---------------------------------------------------------------
 def layer_bufs(**tensors) -> LayerBufs:
     """LayerBufs from keyword tensors (names of the C struct fields)."""
@@ -262,6 +272,8 @@ def _events(trace):
 
 
 def flowmoe_layer_fwd(shape, R, bufs, s_compute=None, s_comm=None, trace=None):
+    if trace is not None and len(trace) < 8 * R:
+        raise ValueError(f"the forward trace takes 8 * R = {8 * R} events, got {len(trace)}")
     sc = _stream(s_compute)
     sm = sc if s_comm is None else _stream(s_comm)
     _check(load().flowmoe_layer_fwd(ctypes.byref(shape), R, ctypes.byref(bufs), sc, sm,
@@ -269,6 +281,9 @@ def flowmoe_layer_fwd(shape, R, bufs, s_compute=None, s_comm=None, trace=None):
 
 
 def flowmoe_layer_bwd(shape, R, bufs, s_compute=None, s_comm=None, trace=None):
+    if trace is not None and len(trace) < 8 * R + 2:
+        raise ValueError(f"the backward trace takes 8 * R + 2 = {8 * R + 2} events, "
+                         f"got {len(trace)}")
     sc = _stream(s_compute)
     sm = sc if s_comm is None else _stream(s_comm)
     _check(load().flowmoe_layer_bwd(ctypes.byref(shape), R, ctypes.byref(bufs), sc, sm,

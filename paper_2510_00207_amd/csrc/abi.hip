@@ -3,6 +3,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 
 #include <mutex>
 #include <vector>
@@ -190,16 +191,52 @@ flowmoe_status_t flowmoe_set_gemm_tiles(int32_t tiles) {
   return ok();
 }
 
-const char* flowmoe_version(void) { return "flowmoe 0.1.0 gfx950"; }
+flowmoe_status_t flowmoe_set_row_streams(int32_t mode) {
+  if (mode != FLOWMOE_ROWS_AUTO && mode != FLOWMOE_ROWS_NT && mode != FLOWMOE_ROWS_CACHED)
+    return fail(FLOWMOE_ERR_INVALID, "mode = %d is not a FLOWMOE_ROWS_* value", mode);
+  set_row_streams(mode);
+  return ok();
+}
+
+const char* flowmoe_version(void) { return "flowmoe 0.2.0 gfx950"; }
 
 const char* flowmoe_last_error(void) { return g_err; }
 
 int32_t flowmoe_capacity(int32_t T, int32_t E, int32_t k, double f) {
-  if (T < 0 || E < 1 || k < 1 || !(f > 0.0)) return -1;
-  const double v = f * (double)k * (double)T / (double)E;
-  const double c = ceil(v - 1e-9 * (v > 1.0 ? v : 1.0));
-  if (c > 2147483647.0) return -1;
-  return c < 0 ? 0 : (int32_t)c;
+  if (T < 0 || E < 1 || k < 1 || !(f > 0.0) || !isfinite(f)) return -1;
+  // f as the shortest decimal that reads back as f: D * 10^x with D an
+  // integer of p digits (printf rounds correctly; p = 17 always reads back)
+  char buf[40];
+  int p = 1;
+  for (; p < 17; ++p) {
+    snprintf(buf, sizeof(buf), "%.*e", p - 1, f);
+    if (strtod(buf, nullptr) == f) break;
+  }
+  snprintf(buf, sizeof(buf), "%.*e", p - 1, f);
+  unsigned long long D = 0;
+  const char* c = buf;
+  for (; *c != 'e'; ++c)
+    if (*c >= '0' && *c <= '9') D = D * 10 + (unsigned long long)(*c - '0');
+  const int x = atoi(c + 1) - (p - 1);
+  // C = ceil(D * 10^x * k * T / E) in 128-bit integers (D < 10^17, k * T < 2^62)
+  typedef unsigned __int128 u128;
+  const u128 kMax = ~(u128)0;
+  u128 num = (u128)D * (unsigned long long)k * (unsigned long long)T;
+  if (num == 0) return 0;
+  u128 den = (u128)(unsigned)E;
+  if (x >= 0) {
+    for (int i = 0; i < x; ++i) {
+      if (num > kMax / 10) return -1;  // far beyond any int32 capacity
+      num *= 10;
+    }
+  } else {
+    for (int i = 0; i < -x; ++i) {
+      if (den > num) return 1;  // 0 < value < 1
+      den *= 10;
+    }
+  }
+  const u128 c0 = num / den + (num % den != 0 ? 1 : 0);
+  return c0 > (u128)2147483647 ? -1 : (int32_t)c0;
 }
 
 int64_t flowmoe_rows_capacity(const flowmoe_shape_t* shape) {
@@ -665,12 +702,13 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     sc.mark(1, r, 0, s_compute);
     sc.run(launch_expert_ffn_dgrad(s, c.dy_disp, c.h_save, c.counts, c.offsets, b->w1, b->w3,
                                    b->w2, c.h_save, c.dx_disp, s_compute));
+    sc.mark(1, r, 1, s_compute);
     sc.signal(evE[r], s_compute);
-    if (r > 0) sc.mark(1, r, 1, s_compute);
   }
+  sc.mark(4, 0, 0, s_compute);  // (the trace's last pair: the weight gradients)
   sc.run(launch_expert_ffn_wgrad(s, R, b->dy_disp, b->x_disp, b->a_save, b->h_save, b->counts,
                                  b->offsets, b->dw1, b->dw3, b->dw2, 0, s_compute));
-  sc.mark(1, 0, 1, s_compute);
+  sc.mark(4, 0, 1, s_compute);
   // D_R..D_1 (dispatch backward, plus the gate's dx term) on the comm stream
   for (int r = R - 1; r >= 0; --r) {
     Chunk c = chunk_of(s, b, r);

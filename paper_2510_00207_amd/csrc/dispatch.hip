@@ -18,6 +18,8 @@
 //   than the recount, at 96 tiles 3x).
 // gather / combine / scatter kernels move whole rows with 16-byte vectors,
 //   one wave per row or token, accumulating in float in a fixed order.
+#include <atomic>
+
 #include "common.hpp"
 
 namespace flowmoe {
@@ -35,12 +37,19 @@ __host__ void with_kmax(int k, F&& f) {
   else f(KConst<8>{});
 }
 
+std::atomic<int> g_row_streams{FLOWMOE_ROWS_AUTO};
+
 // f(true or false as a type): non-temporal row streams for bf16 calls that
 // move at least 256 MB (the Infinity Cache): there every line of the stream
-// is gone before it is read again, and caching it only evicts the rest
+// is gone before it is read again, and caching it only evicts the rest.
+// flowmoe_set_row_streams can force either kind for bf16 calls (fp32 calls
+// always stream through the caches).
 template <typename F>
 __host__ void with_nt(const Shape& s, long rows, F&& f) {
-  const bool nt = s.dtype == FLOWMOE_BF16 && (long)(rows + s.T) * s.M * 2 >= (256L << 20);
+  const int mode = g_row_streams.load(std::memory_order_relaxed);
+  const bool big = (long)(rows + s.T) * s.M * 2 >= (256L << 20);
+  const bool nt = s.dtype == FLOWMOE_BF16 &&
+                  (mode == FLOWMOE_ROWS_NT || (mode == FLOWMOE_ROWS_AUTO && big));
   if (nt) f(std::true_type{});
   else f(std::false_type{});
 }
@@ -310,10 +319,13 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(
 // with dl_t taken from the selection (gidx), its weights (gw) and their
 // gradients (gdw), and W_g^T given transposed in float (wgt, E x M).
 // ADD: y[t] += (the sum) instead of =, the old y loaded with the source rows.
+// The source row of every slot j < kl is loaded, also of dropped ones (row 0,
+// value unused), so that all loads of a step are in flight together; kl = 0
+// when the call has no rows (C = 0: every slot dropped, src may be empty).
 template <typename TE, bool GATE, int KM, bool ADD, bool NT>  // KM >= k: per-token array size
 __global__ __launch_bounds__(256) void combine_rows_kernel(
     const TE* __restrict__ src, const int32_t* __restrict__ slot, const float* __restrict__ w,
-    TE* __restrict__ y, int T, int M, int k, const int32_t* __restrict__ gidx,
+    TE* __restrict__ y, int T, int M, int k, int kl, const int32_t* __restrict__ gidx,
     const float* __restrict__ gw, const float* __restrict__ gdw, const TE* __restrict__ wgt) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -356,7 +368,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
       const int m = m0 + 64 * 8 * u < M ? m0 + 64 * 8 * u : m0;
 #pragma unroll
       for (int j = 0; j < KM; ++j)
-        if (j < k) raw[u][j] = raw8_ld<NT>(src + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
+        if (j < kl) raw[u][j] = raw8_ld<NT>(src + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
       if constexpr (GATE) {
 #pragma unroll
         for (int j = 0; j < KM; ++j)
@@ -402,11 +414,12 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(
 }
 
 // combine backward, token part: dy_disp[slot] = w * dy[t], d_w = <dy[t], y_disp[slot]>
+// (kl as in combine_rows_kernel)
 template <typename TE, int KM, bool NT>  // KM >= k: size of the per-token arrays
 __global__ __launch_bounds__(256) void combine_bwd_kernel(
     const TE* __restrict__ dy, const TE* __restrict__ y_disp, const int32_t* __restrict__ slot,
     const float* __restrict__ w, const int32_t* __restrict__ counts, TE* __restrict__ dy_disp,
-    float* __restrict__ dw, int T, int M, int k, int E, int C, int token_blocks) {
+    float* __restrict__ dw, int T, int M, int k, int kl, int E, int C, int token_blocks) {
   const int lane = threadIdx.x & 63;
   if ((int)blockIdx.x >= token_blocks) {
     // padded layout: zero rows [e*C + counts[e], (e+1)*C)
@@ -442,7 +455,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
       graw[u] = raw8_ld<NT>(dy + (long)t * M + m);
 #pragma unroll
       for (int j = 0; j < KM; ++j)
-        if (j < k) raw[u][j] = raw8_ld<NT>(y_disp + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
+        if (j < kl) raw[u][j] = raw8_ld<NT>(y_disp + (long)(sl[j] >= 0 ? sl[j] : 0) * M + m);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -476,6 +489,8 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
 }
 
 }  // namespace
+
+void set_row_streams(int mode) { g_row_streams.store(mode, std::memory_order_relaxed); }
 
 size_t dispatch_ws_bytes(const Shape& s) {
   const long tiles = ((long)s.T * s.k + kScanThreads - 1) / kScanThreads;
@@ -531,6 +546,7 @@ hipError_t launch_dispatch(const Shape& s, const int32_t* idx, const void* x, in
 hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slot, const float* w,
                           void* y, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
+  const int kl = s.rows > 0 ? s.k : 0;  // no rows: no source loads
   const int blocks = (s.T + 3) / 4;
   return traced(FLOWMOE_K_COMBINE, st, [&] {
     with_kmax(s.k, [&](auto kc) {
@@ -539,12 +555,12 @@ hipError_t launch_combine(const Shape& s, const void* y_disp, const int32_t* slo
         with_nt(s, s.rows, [&](auto ntc) {
           hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV, false, decltype(ntc)::value>),
                              dim3(blocks), dim3(256), 0, st, (const bf16_t*)y_disp, slot, w,
-                             (bf16_t*)y, s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+                             (bf16_t*)y, s.T, s.M, s.k, kl, nullptr, nullptr, nullptr, nullptr);
         });
       else
         hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV, false, false>), dim3(blocks),
                            dim3(256), 0, st, (const float*)y_disp, slot, w, (float*)y, s.T, s.M,
-                           s.k, nullptr, nullptr, nullptr, nullptr);
+                           s.k, kl, nullptr, nullptr, nullptr, nullptr);
     });
   });
 }
@@ -557,6 +573,7 @@ hipError_t launch_dispatch_bwd(const Shape& s, const void* dx_disp, const int32_
 hipError_t launch_dispatch_bwd_add(const Shape& s, const void* dx_disp, const int32_t* slot,
                                    void* dx, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
+  const int kl = s.rows > 0 ? s.k : 0;  // no rows: no source loads
   const int blocks = (s.T + 3) / 4;
   return traced(FLOWMOE_K_COMBINE, st, [&] {
     with_kmax(s.k, [&](auto kc) {
@@ -565,12 +582,12 @@ hipError_t launch_dispatch_bwd_add(const Shape& s, const void* dx_disp, const in
         with_nt(s, s.rows, [&](auto ntc) {
           hipLaunchKernelGGL((combine_rows_kernel<bf16_t, false, KMV, true, decltype(ntc)::value>),
                              dim3(blocks), dim3(256), 0, st, (const bf16_t*)dx_disp, slot, nullptr,
-                             (bf16_t*)dx, s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+                             (bf16_t*)dx, s.T, s.M, s.k, kl, nullptr, nullptr, nullptr, nullptr);
         });
       else
         hipLaunchKernelGGL((combine_rows_kernel<float, false, KMV, true, false>), dim3(blocks),
                            dim3(256), 0, st, (const float*)dx_disp, slot, nullptr, (float*)dx,
-                           s.T, s.M, s.k, nullptr, nullptr, nullptr, nullptr);
+                           s.T, s.M, s.k, kl, nullptr, nullptr, nullptr, nullptr);
     });
   });
 }
@@ -579,6 +596,7 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
                                     const int32_t* idx, const float* w, const float* dw,
                                     const void* wgt, void* dx, hipStream_t st) {
   if (s.T == 0) return hipSuccess;
+  const int kl = s.rows > 0 ? s.k : 0;  // no rows: no source loads
   const int blocks = (s.T + 3) / 4;
   return traced(FLOWMOE_K_COMBINE, st, [&] {
     with_kmax(s.k, [&](auto kc) {
@@ -587,12 +605,12 @@ hipError_t launch_dispatch_bwd_gate(const Shape& s, const void* dx_disp, const i
         with_nt(s, s.rows, [&](auto ntc) {
           hipLaunchKernelGGL((combine_rows_kernel<bf16_t, true, KMV, false, decltype(ntc)::value>),
                              dim3(blocks), dim3(256), 0, st, (const bf16_t*)dx_disp, slot, nullptr,
-                             (bf16_t*)dx, s.T, s.M, s.k, idx, w, dw, (const bf16_t*)wgt);
+                             (bf16_t*)dx, s.T, s.M, s.k, kl, idx, w, dw, (const bf16_t*)wgt);
         });
       else
         hipLaunchKernelGGL((combine_rows_kernel<float, true, KMV, false, false>), dim3(blocks),
                            dim3(256), 0, st, (const float*)dx_disp, slot, nullptr, (float*)dx,
-                           s.T, s.M, s.k, idx, w, dw, (const float*)wgt);
+                           s.T, s.M, s.k, kl, idx, w, dw, (const float*)wgt);
     });
   });
 }
@@ -601,6 +619,7 @@ hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp
                               const int32_t* slot, const float* w, const int32_t* counts,
                               const int32_t* offsets, void* dy_disp, float* dw, hipStream_t st) {
   (void)offsets;
+  const int kl = s.rows > 0 ? s.k : 0;  // no rows: no source loads
   const int token_blocks = (s.T + 3) / 4;
   const long fill_blocks = (s.layout == FLOWMOE_PADDED) ? ((long)s.E * s.C + 3) / 4 : 0;
   const long blocks = token_blocks + fill_blocks;
@@ -613,12 +632,12 @@ hipError_t launch_combine_bwd(const Shape& s, const void* dy, const void* y_disp
           hipLaunchKernelGGL((combine_bwd_kernel<bf16_t, KMV, decltype(ntc)::value>),
                              dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t*)dy,
                              (const bf16_t*)y_disp, slot, w, counts, (bf16_t*)dy_disp, dw, s.T, s.M,
-                             s.k, s.E, s.C, token_blocks);
+                             s.k, kl, s.E, s.C, token_blocks);
         });
       else
         hipLaunchKernelGGL((combine_bwd_kernel<float, KMV, false>), dim3((unsigned)blocks),
                            dim3(256), 0, st, (const float*)dy, (const float*)y_disp, slot, w, counts,
-                           (float*)dy_disp, dw, s.T, s.M, s.k, s.E, s.C, token_blocks);
+                           (float*)dy_disp, dw, s.T, s.M, s.k, kl, s.E, s.C, token_blocks);
     });
   });
 }

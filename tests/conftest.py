@@ -27,3 +27,18 @@ def flowmoe_lib():
         from paper_2510_00207_amd import build
         build.build(verbose=False)
     return _lib.load()
+
+
+def pytest_sessionfinish(session, exitstatus):
+    """Write the error measures of every parity comparison of the session
+    (max-normalised and element-wise) to gpurun_out/parity_report.tsv."""
+    mod = sys.modules.get("gpu_helpers")
+    rep = getattr(mod, "REPORT", None) if mod is not None else None
+    if not rep:
+        return
+    out = os.path.join(ROOT, "gpurun_out")
+    os.makedirs(out, exist_ok=True)
+    with open(os.path.join(out, "parity_report.tsv"), "w") as f:
+        f.write("test\tquantity\tdtype\tmax_rel_err\telem_rel_err\n")
+        for test, what, dt, e1, e2 in rep:
+            f.write(f"{test}\t{what}\t{dt}\t{e1:.3e}\t{e2:.3e}\n")

@@ -188,3 +188,38 @@ def test_gemm_tiles_setting(flowmoe_lib):
     raw.flowmoe_set_gemm_tiles.argtypes = [ctypes.c_int32]
     assert raw.flowmoe_set_gemm_tiles(3) == L.ERR_INVALID
     assert raw.flowmoe_set_gemm_tiles(-1) == L.ERR_INVALID
+
+
+def test_capacity_exact_on_adversarial_factors(flowmoe_lib):
+    """C = ceil(f k T / E) on the decimal value of f, exactly as the oracle's
+    rational arithmetic: factors with many digits, factors just above and
+    below products that are integers, and large T (a double product with a
+    relative slack would round some of these the wrong way)."""
+    cases = [(1 << 20, 1, 1, 1.000000000001), (1 << 20, 1, 1, 0.999999999999),
+             (1 << 30, 1, 1, 1.0000000001), (1 << 30, 3, 1, 1.0000000001),
+             (4096, 8, 2, 1.2), (10, 1, 1, 1.1), (3, 1, 1, 0.1 + 0.2), (1 << 30, 1, 2, 0.5),
+             (100, 7, 3, 1.0 / 3.0), (2147483647, 64, 8, 0.123456789012345),
+             (2147483647, 1, 1, 1e-300), (12345, 17, 5, 123.456), (1, 64, 1, 5e-324)]
+    rng = __import__("numpy").random.default_rng(17)
+    for _ in range(300):
+        digits = int(rng.integers(1, 17))
+        f = float(f"{rng.integers(1, 10**digits)}e{int(rng.integers(-digits - 1, 2))}")
+        cases.append((int(rng.integers(0, 1 << 31)), int(rng.integers(1, 65)),
+                      int(rng.integers(1, 9)), f))
+    for T, E, k, f in cases:
+        want = oracle.capacity(T, E, k, f)
+        got = L.flowmoe_capacity(T, E, k, f)
+        assert got == (want if want <= 2**31 - 1 else -1), (T, E, k, f, got, want)
+    assert L.flowmoe_capacity(1 << 20, 1, 1, 1.000000000001) == (1 << 20) + 1
+    assert L.flowmoe_capacity(8, 1, 1, float("inf")) == -1
+    assert L.flowmoe_capacity(8, 1, 1, float("nan")) == -1
+    assert L.flowmoe_capacity(2147483647, 1, 8, 1.0) == -1  # above INT32_MAX
+
+
+def test_row_streams_setting(flowmoe_lib):
+    for m in ("nt", "cached", "auto"):
+        L.flowmoe_set_row_streams(m)
+    raw = ctypes.CDLL(L.LIB_PATH)
+    raw.flowmoe_set_row_streams.argtypes = [ctypes.c_int32]
+    assert raw.flowmoe_set_row_streams(3) == L.ERR_INVALID
+    assert raw.flowmoe_set_row_streams(-1) == L.ERR_INVALID

@@ -7,11 +7,16 @@ Checked against the fp64 oracle:
   * routing for every token and chunk, bit-exact: top-k indices from the
     GPU's fp32 logits, counts, offsets, slots, row sources, and the
     dispatched rows (bitwise copies of x);
-  * sampled tokens: y, dx, d_topk_w, d_logits, recomputed one token at a time
-    through oracle.expert_ffn / expert_ffn_bwd / gate_bwd on that token's
-    kept assignments;
-  * sampled entries of dW1, dW2 (and dW3): the sum over the expert's rows of
-    the oracle's per-row gradient for that one column;
+  * the oracle's own fp64 routing differs from the GPU's only on tokens with
+    a near-tie among their top k + 1 fp64 logits (a gap below 4 max|dl|);
+    the count is printed;
+  * sampled tokens: y, dx, d_topk_w, d_logits, and the rows of their kept
+    assignments in y_disp, dy_disp and dx_disp, recomputed one token at a
+    time through oracle.expert_ffn / combine_bwd / expert_ffn_bwd / gate_bwd
+    on that token's kept assignments;
+  * a sampled 32 x 32 block of dW1, dW2 (and dW3) of two experts: sums over
+    the expert's rows of the oracle's per-row gradients, the tolerance
+    scaled by the oracle block's largest entry;
   * dW_g and db: x^T d_logits and column sums of the GPU's own d_logits in
     fp64 (the reduction at full size; d_logits itself is sampled above).
 """
@@ -20,13 +25,13 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import assert_close, dev, host, load_layer, need_gpu
+from gpu_helpers import assert_close, dev, host, load_layer, near_tie_check, need_gpu
 from moe_inputs import as_f64, get_config, make_inputs
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 N_TOK = 24      # sampled tokens per workload
-N_W = 4         # sampled weight-gradient entries per tensor
+N_W = 32        # sampled rows and columns of the weight-gradient blocks
 
 
 def _w64(a, e):
@@ -74,6 +79,9 @@ def test_fullsize_parity(name):
     print(f"[fullsize] {name}: routing", flush=True)
     idx_ref, w_ref = oracle.topk_select(gl, k)
     assert np.array_equal(host(layer.topk_idx), idx_ref)
+    ndiff, nnear, bound = near_tie_check(own, gl, idx_ref, k)
+    print(f"[fullsize] {name}: own fp64 routing differs on {ndiff} token(s); {nnear} token(s) "
+          f"with a top-{k + 1} gap below {bound:.2e}", flush=True)
     np.testing.assert_allclose(host(layer.topk_w), w_ref, rtol=2e-6, atol=2e-7)
     C = oracle.capacity(Tr, E, k, cfg.f)
     assert layer.C == C
@@ -111,6 +119,13 @@ def test_fullsize_parity(name):
         for j in range(k):
             if slot_all[t, j] >= 0:
                 by_expert.setdefault(int(idx_ref[t, j]), []).append((i, j))
+    # the GPU's rows of every sampled kept assignment, in by_expert order
+    def rows_of(buf, items):
+        out = []
+        for i, j in items:
+            t = int(toks[i])
+            out.append(host(buf[t // Tr][int(slot_all[t, j])]))
+        return np.stack(out)
     for e, items in by_expert.items():
         W1, W2 = _w64(inp["w1"], e)[None], _w64(inp["w2"], e)[None]
         W3 = _w64(inp["w3"], e)[None] if cfg.act == "swiglu" else None
@@ -123,9 +138,13 @@ def test_fullsize_parity(name):
         for q, (i, j) in enumerate(items):
             y_ref[i] += wt[q] * sv["y_disp"][q]
             dw_ref[i, j] = float(dys[q] @ sv["y_disp"][q])
-        dxd, _, _, _ = oracle.expert_ffn_bwd(wt[:, None] * dys, Xs, sv, cnt, off, W1, W3, W2, cfg.act)
+        dyd, _ = oracle.combine_bwd(dys, sv["y_disp"], np.arange(n)[:, None], wt[:, None])
+        dxd, _, _, _ = oracle.expert_ffn_bwd(dyd, Xs, sv, cnt, off, W1, W3, W2, cfg.act)
         for q, (i, _) in enumerate(items):
             dxd_ref[i] += dxd[q]
+        assert_close(rows_of(layer.y_disp, items), sv["y_disp"], "bf16", f"{name} y_disp rows e={e}")
+        assert_close(rows_of(layer.dy_disp, items), dyd, "bf16", f"{name} dy_disp rows e={e}")
+        assert_close(rows_of(layer.dx_disp, items), dxd, "bf16", f"{name} dx_disp rows e={e}")
     g = oracle.gate_bwd(x64[toks], wg, idx_ref[toks], w_ref[toks], dw_ref)
     assert_close(y_gpu, y_ref, "bf16", f"{name} y (sampled)")
     assert_close(dtw_gpu, dw_ref, "bf16", f"{name} d_topk_w (sampled)")
@@ -158,8 +177,8 @@ def test_fullsize_parity(name):
         rows_t = np.array(rows_t)
         X = as_f64(x[rows_t])                                   # rows x M
         dY = np.array(rows_w)[:, None] * as_f64(dy_all[rows_t])  # rows x M (dy_disp)
-        hs = rng.choice(cfg.H, size=N_W, replace=False)
-        ms = rng.choice(M, size=N_W, replace=False)
+        hs = np.sort(rng.choice(cfg.H, size=N_W, replace=False))
+        ms = np.sort(rng.choice(M, size=N_W, replace=False))
         h1 = X @ W1e[:, hs]                                     # rows x N_W
         dA = dY @ W2e[hs, :].T                                  # rows x N_W
         if cfg.act == "gelu":
@@ -170,18 +189,13 @@ def test_fullsize_parity(name):
             a = oracle.silu(h1) * h3
             dH1 = dA * h3 * oracle.silu_grad(h1)
             dH3 = dA * oracle.silu(h1)
-        ref_w1 = np.array([X[:, ms[q]] @ dH1[:, q] for q in range(N_W)])
-        ref_w2 = np.array([a[:, q] @ dY[:, ms[q]] for q in range(N_W)])
-        got_w1 = host(layer.dw1[e][torch.from_numpy(ms).to(dev()), torch.from_numpy(hs).to(dev())])
-        got_w2 = host(layer.dw2[e][torch.from_numpy(hs).to(dev()), torch.from_numpy(ms).to(dev())])
-        # relative to the size of the whole gradient tensor of this expert
-        scale1 = float(torch.max(torch.abs(layer.dw1[e])).item())
-        scale2 = float(torch.max(torch.abs(layer.dw2[e])).item())
-        assert np.max(np.abs(got_w1 - ref_w1)) <= 2e-2 * scale1, (name, e, "dw1")
-        assert np.max(np.abs(got_w2 - ref_w2)) <= 2e-2 * scale2, (name, e, "dw2")
+        # blocks dW1[ms][:, hs] = X[:, ms]^T dH1 and dW2[hs][:, ms] = A^T dY[:, ms];
+        # the tolerance is relative to the oracle block's largest entry
+        hs_t, ms_t = torch.from_numpy(hs).to(dev()), torch.from_numpy(ms).to(dev())
+        blk = lambda w, r, c: host(w[e].index_select(0, r).index_select(1, c))
+        assert_close(blk(layer.dw1, ms_t, hs_t), X[:, ms].T @ dH1, "bf16", f"{name} dw1 block e={e}")
+        assert_close(blk(layer.dw2, hs_t, ms_t), a.T @ dY[:, ms], "bf16", f"{name} dw2 block e={e}")
         if cfg.act == "swiglu":
-            ref_w3 = np.array([X[:, ms[q]] @ dH3[:, q] for q in range(N_W)])
-            got_w3 = host(layer.dw3[e][torch.from_numpy(ms).to(dev()), torch.from_numpy(hs).to(dev())])
-            scale3 = float(torch.max(torch.abs(layer.dw3[e])).item())
-            assert np.max(np.abs(got_w3 - ref_w3)) <= 2e-2 * scale3, (name, e, "dw3")
+            assert_close(blk(layer.dw3, ms_t, hs_t), X[:, ms].T @ dH3, "bf16",
+                         f"{name} dw3 block e={e}")
     print(f"[fullsize] {name}: ok", flush=True)

@@ -8,8 +8,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import (assert_close, dev, f64_inputs, host, load_layer, need_gpu,
-                         oracle_for_layer)
+from gpu_helpers import (assert_close, dev, f64_inputs, host, load_layer, near_tie_check,
+                         need_gpu, oracle_for_layer)
 from moe_inputs import get_config, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -54,6 +54,10 @@ def check_against_oracle(cfg, layout, layer, inp, R):
     assert dl <= 1e-4 * np.max(np.abs(own)), f"logits off by {dl}"
     # routing is a function of the fp32 logits: bit-exact
     assert np.array_equal(host(layer.topk_idx), ref["topk_idx"])
+    # the oracle's own fp64 routing differs only on near-ties
+    ndiff, nnear, bound = near_tie_check(own, gl, host(layer.topk_idx), cfg.k)
+    print(f"[layer] own-logit routing: {ndiff} token(s) differ, {nnear} near-tie(s) "
+          f"below {bound:.2e}", flush=True)
     # (the full softmax gate divides by a sum over all E experts in fp32)
     wtol = dict(rtol=1e-5, atol=1e-7) if cfg.gate == "full" else dict(rtol=2e-6, atol=2e-7)
     np.testing.assert_allclose(host(layer.topk_w), ref["topk_w"], **wtol)

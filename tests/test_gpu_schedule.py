@@ -1,0 +1,103 @@
+"""The R-chunk two-stream schedule of flowmoe_layer_fwd / flowmoe_layer_bwd
+(Sec. 3.2, Eqs. 3-6), read from the timing events the layer records at the
+start and end of every task: the order of the tasks on each stream and the
+dependency constraints between the streams (Sec. 3.3, 6b-6c), and that
+tracing changes no result."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import dev, load_layer, need_gpu
+from moe_inputs import get_config, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+SLACK_MS = 1e-3  # timestamps of two streams compared to within 1 us
+
+FWD = {"G": 0, "D": 1, "E": 2, "C": 3}          # gate (AT), dispatch, experts, combine
+BWD = {"C": 0, "E": 1, "D": 2, "G": 3, "W": 4}  # combine bwd, experts bwd, dispatch bwd,
+                                                # gate parameter gradients, weight gradients
+
+
+def _spans(events, R, tasks, t0):
+    """(begin, end) in ms after t0 for every (task, chunk) of the trace."""
+    out = {}
+    for name, task in tasks.items():
+        for r in range(R if name != "W" else 1):
+            i = 2 * (task * R + r)
+            out[(name, r)] = (t0.elapsed_time(events[i]), t0.elapsed_time(events[i + 1]))
+    return out
+
+
+def _before(sp, a, b):
+    """task a ends before task b begins"""
+    assert sp[a][1] <= sp[b][0] + SLACK_MS, f"{a} ends at {sp[a][1]:.4f} ms after {b} begins at {sp[b][0]:.4f} ms"
+
+
+def _layer(cfg, R, inp):
+    from paper_2510_00207_amd.layer import MoELayer
+    layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
+                     dtype=cfg.dtype, device=dev())
+    load_layer(layer, inp)
+    return layer
+
+
+@pytest.mark.parametrize("name,R", [("fine", 4), ("balanced", 2), ("large", 3)])
+def test_layer_schedule_order_and_constraints(name, R):
+    need_gpu()
+    cfg = get_config(name, T=768 * R, M=512, H=256, R=R)
+    print(f"[schedule] {name} R={R}", flush=True)
+    inp = make_inputs(cfg)
+    sc, sm = torch.cuda.Stream(), torch.cuda.Stream()
+    ev = lambda n: [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    fwd_ev, bwd_ev, (t0,) = ev(8 * R), ev(8 * R + 2), ev(1)
+    traced = _layer(cfg, R, inp)
+    plain = _layer(cfg, R, inp)
+    with torch.cuda.stream(sc):
+        t0.record(sc)
+    traced.forward(sc, sm, trace=fwd_ev)
+    traced.backward(sc, sm, trace=bwd_ev)
+    plain.forward(sc, sm)
+    plain.backward(sc, sm)
+    torch.cuda.synchronize()
+    # forward (Eqs. 3-4): compute stream AT_1..AT_R then E_1..E_R, comm stream
+    # D_1..D_R then C_1..C_R; D_r after AT_r, E_r after D_r, C_r after E_r
+    f = _spans(fwd_ev, R, FWD, t0)
+    comp = [("G", r) for r in range(R)] + [("E", r) for r in range(R)]
+    comm = [("D", r) for r in range(R)] + [("C", r) for r in range(R)]
+    for seq in (comp, comm):
+        for a, b in zip(seq, seq[1:]):
+            _before(f, a, b)
+    for r in range(R):
+        _before(f, ("G", r), ("D", r))
+        _before(f, ("D", r), ("E", r))
+        _before(f, ("E", r), ("C", r))
+    # backward (Eqs. 5-6): comm stream C_R..C_1, the gate's parameter
+    # gradients AT_R..AT_1, then D_R..D_1; compute stream E_R..E_1 and the
+    # weight gradients; E_r after C_r (6b), D_r after E_r (6c)
+    b = _spans(bwd_ev, R, BWD, t0)
+    back = list(range(R - 1, -1, -1))
+    comm = [("C", r) for r in back] + [("G", r) for r in back] + [("D", r) for r in back]
+    comp = [("E", r) for r in back] + [("W", 0)]
+    for seq in (comm, comp):
+        for a, b_ in zip(seq, seq[1:]):
+            _before(b, a, b_)
+    for r in range(R):
+        _before(b, ("C", r), ("E", r))
+        _before(b, ("E", r), ("D", r))
+    for sp in (f, b):
+        for key, (s0, s1) in sp.items():
+            assert s0 <= s1 + SLACK_MS, key
+    # the forward is done before the backward starts (the call joins its streams)
+    assert max(e for _, e in f.values()) <= min(s for s, _ in b.values()) + SLACK_MS
+    # overlap: time during which both streams run a task, over the span
+    for label, sp, tasks_c in (("fwd", f, ("G", "E")), ("bwd", b, ("E", "W"))):
+        on_c = [v for k_, v in sp.items() if k_[0] in tasks_c]
+        on_m = [v for k_, v in sp.items() if k_[0] not in tasks_c]
+        both = sum(max(0.0, min(a1, b1) - max(a0, b0)) for a0, a1 in on_c for b0, b1 in on_m)
+        span = max(e for _, e in sp.values()) - min(s for s, _ in sp.values())
+        print(f"[schedule] {name} R={R} {label}: {span:.3f} ms, streams overlap "
+              f"{both:.3f} ms ({both / span:.1%})", flush=True)
+    # tracing records events only: the results are those of the plain run
+    for nm in ("y", "dx", "d_logits", "dw_gate", "dw1", "dw2", "x_disp", "dx_disp"):
+        assert torch.equal(getattr(traced, nm), getattr(plain, nm)), nm
