@@ -49,8 +49,15 @@ def test_layer_schedule_order_and_constraints(name, R):
     print(f"[schedule] {name} R={R}", flush=True)
     inp = make_inputs(cfg)
     sc, sm = torch.cuda.Stream(), torch.cuda.Stream()
-    ev = lambda n: [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    def ev(n):
+        # (torch creates an event's HIP handle at its first record)
+        out = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in out:
+            e.record(sc)
+        return out
+
     fwd_ev, bwd_ev, (t0,) = ev(8 * R), ev(8 * R + 2), ev(1)
+    torch.cuda.synchronize()
     traced = _layer(cfg, R, inp)
     plain = _layer(cfg, R, inp)
     with torch.cuda.stream(sc):
