@@ -60,6 +60,9 @@ def test_layer_schedule_order_and_constraints(name, R):
     torch.cuda.synchronize()
     traced = _layer(cfg, R, inp)
     plain = _layer(cfg, R, inp)
+    plain.forward(sc, sm)  # (warm-up: the first launches of a process load the code)
+    plain.backward(sc, sm)
+    torch.cuda.synchronize()
     with torch.cuda.stream(sc):
         t0.record(sc)
     traced.forward(sc, sm, trace=fwd_ev)
