@@ -233,6 +233,30 @@ flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void*
                                        float* dbias, void* dx, int32_t accumulate, void* ws,
                                        size_t ws_bytes, hipStream_t stream);
 
+/* ---- the gate backward without a workspace --------------------------------- */
+
+/* Bytes of device scratch the library holds for flowmoe_gate_topk_bwd_noalloc
+ * (32 MiB per GPU it runs on, from its load until the process ends). */
+#define FLOWMOE_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the gate
+ * backward of flowmoe_gate_topk_bwd, same arguments, same kernels and the
+ * same results, without the workspace arguments. Its scratch is the
+ * library's own static device array (FLOWMOE_NOALLOC_SCRATCH_BYTES per GPU);
+ * the call allocates nothing. A shape whose flowmoe_workspace_bytes(shape,
+ * FLOWMOE_WS_GATE_BWD) exceeds that size is rejected with
+ * FLOWMOE_ERR_WORKSPACE before anything is enqueued. Every call on one GPU
+ * shares that GPU's array: calls that may overlap on one GPU (on streams not
+ * ordered with each other, or from several host threads) race and must not
+ * be issued; calls in order on one stream are safe. */
+flowmoe_status_t flowmoe_gate_topk_bwd_noalloc(const flowmoe_shape_t* shape, const void* x,
+                                               const void* w_gate, const float* logits,
+                                               const int32_t* topk_idx, const float* topk_w,
+                                               const float* d_topk_w, float* d_logits,
+                                               float* dw_gate, float* dbias, void* dx,
+                                               int32_t accumulate, hipStream_t stream);
+
 /* ---- kernel tracing ------------------------------------------------------- */
 
 /* Kernel kinds (bit i of a trace mask selects kind i). */

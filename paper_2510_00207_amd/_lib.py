@@ -83,6 +83,7 @@ def load():
         "flowmoe_expert_ffn_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
         "flowmoe_dispatch_bwd": ([SP, P, P, P, P], I32),
         "flowmoe_gate_topk_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
+        "flowmoe_gate_topk_bwd_noalloc": ([SP, P, P, P, P, P, P, P, P, P, P, I32, P], I32),
         "flowmoe_trace_start": ([P, P, I32, ctypes.c_uint32], I32),
         "flowmoe_trace_stop": ([], I32),
         "flowmoe_set_gemm_tiles": ([I32], I32),
@@ -204,6 +205,18 @@ def flowmoe_gate_topk_bwd(shape, x, w_gate, logits, topk_idx, topk_w, d_topk_w, 
                                         ptr(topk_idx), ptr(topk_w), ptr(d_topk_w), ptr(d_logits),
                                         ptr(dw_gate), ptr(dbias), ptr(dx), int(accumulate), ptr(ws),
                                         ws_bytes, _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def flowmoe_gate_topk_bwd_noalloc(shape, x, w_gate, logits, topk_idx, topk_w, d_topk_w, d_logits,
+                                  dw_gate, dbias, dx, accumulate, stream=None):
+    _check(load().flowmoe_gate_topk_bwd_noalloc(ctypes.byref(shape), ptr(x), ptr(w_gate),
+                                                ptr(logits), ptr(topk_idx), ptr(topk_w),
+                                                ptr(d_topk_w), ptr(d_logits), ptr(dw_gate),
+                                                ptr(dbias), ptr(dx), int(accumulate),
+                                                _stream(stream)))
 
 
 # ---- kernel tracing --------------------------------------------------------------

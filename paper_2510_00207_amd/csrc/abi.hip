@@ -459,6 +459,83 @@ flowmoe_status_t flowmoe_gate_topk_bwd(const flowmoe_shape_t* shape, const void*
                     "flowmoe_gate_topk_bwd");
 }
 
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// the gate backward without a caller workspace
+// ---------------------------------------------------------------------------
+namespace {
+
+// The no-alloc gate backward's scratch: FLOWMOE_NOALLOC_SCRATCH_BYTES of
+// device memory that every GPU the library runs on holds from the module's
+// load until the process ends. Host code never uses this name as an address
+// (on the host it is a stand-in, not device memory): the device address
+// comes from hipGetSymbolAddress, once per device.
+__device__ __align__(256) char scratch[FLOWMOE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// device address of `scratch` on the current device
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+flowmoe_status_t flowmoe_gate_topk_bwd_noalloc(const flowmoe_shape_t* shape, const void* x,
+                                               const void* w_gate, const float* logits,
+                                               const int32_t* topk_idx, const float* topk_w,
+                                               const float* d_topk_w, float* d_logits,
+                                               float* dw_gate, float* dbias, void* dx,
+                                               int32_t accumulate, hipStream_t stream) {
+  Shape s;
+  flowmoe_status_t st = check_shape(shape, 0, &s);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE_T(w_gate, "w_gate");
+  REQUIRE(dw_gate, "dw_gate");
+  if (s.T > 0) {
+    REQUIRE_T(x, "x");
+    REQUIRE(topk_idx, "topk_idx");
+    REQUIRE(topk_w, "topk_w");
+    REQUIRE(d_topk_w, "d_topk_w");
+    REQUIRE(d_logits, "d_logits");
+    if (s.gate == FLOWMOE_GATE_FULL) REQUIRE(logits, "logits");
+  }
+  if (dx != nullptr && reinterpret_cast<uintptr_t>(dx) % 16 != 0)
+    return fail(FLOWMOE_ERR_INVALID, "dx is not 16-byte aligned");
+  const size_t need = gate_bwd_ws_bytes(s);
+  if (need > (size_t)FLOWMOE_NOALLOC_SCRATCH_BYTES)
+    return fail(FLOWMOE_ERR_WORKSPACE,
+                "flowmoe_gate_topk_bwd_noalloc: the shape needs %zu bytes of scratch, more than "
+                "the %zu the library holds; call flowmoe_gate_topk_bwd with a workspace",
+                need, (size_t)FLOWMOE_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  const hipError_t e = scratch_address(&ws);
+  if (e != hipSuccess) return hip_status(e, "flowmoe_gate_topk_bwd_noalloc: scratch address");
+  return hip_status(launch_gate_bwd(s, x, w_gate, logits, topk_idx, topk_w, d_topk_w, d_logits,
+                                    dw_gate, dbias, dx, accumulate != 0, ws, stream),
+                    "flowmoe_gate_topk_bwd_noalloc");
+}
+
+}  // extern "C"
+
 // ---------------------------------------------------------------------------
 // R-chunk layer
 // ---------------------------------------------------------------------------
@@ -531,6 +608,8 @@ flowmoe_status_t check_layer(const flowmoe_shape_t* shape, int32_t R, const flow
 }
 
 }  // namespace
+
+extern "C" {
 
 flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
                                    const flowmoe_layer_bufs_t* b, hipStream_t s_compute,
