@@ -219,6 +219,40 @@ __device__ __forceinline__ void ksum_tile(int vbid, int mtn, int ntn, int& e, in
   mt = g * G + (rg - nt * gm);
 }
 
+// Tile of dispatch position P (blocks go to the 8 XCDs round-robin: position
+// P runs on XCD P % 8, as its (P / 8)-th block) in an nrows x ncols grid of
+// output tiles walked in blocks of 16 x 16 tiles, row block by row block.
+// The 256 tiles of a full block are one round of all 256 CUs, and XCD x
+// takes its 4 x 8 sub-block (rows 4 (x % 4) .., columns 8 (x / 4) ..), m tile
+// fastest: inside an XCD the 32 tiles running together share 12 operand
+// panels through its L2 as before, and across XCDs every B panel is read by
+// four XCDs and every A panel by two at about the same time, so that the
+// Infinity Cache serves the repeats instead of HBM (with each XCD on a range
+// of its own, the XCDs stream eight different experts' weights at once).
+// Ragged blocks at the grid's edges walk their tiles m fastest. A full
+// block's sub-blocks need it to start at a multiple of 8: every block of
+// the grid does when the grid itself does.
+__device__ __forceinline__ void shared_block_tile(int P, int nrows, int ncols, int& mt, int& nt) {
+  constexpr int SB = 16;
+  const int rb = P / (SB * ncols);
+  const int r = min(SB, nrows - rb * SB);   // rows of this row block
+  const int Pr = P - rb * SB * ncols;       // position inside the row block
+  const int cb = Pr / (r * SB);
+  const int c = min(SB, ncols - cb * SB);   // columns of this block
+  const int j = Pr - cb * r * SB;           // position inside the r x c block
+  int lr, lc;
+  if (r == SB && c == SB) {
+    const int x = j & 7, s = j >> 3;
+    lr = (x & 3) * 4 + (s & 3);
+    lc = (x >> 2) * 8 + (s >> 2);
+  } else {
+    lr = j % r;
+    lc = j / r;
+  }
+  mt = rb * SB + lr;
+  nt = cb * SB + lc;
+}
+
 // Epilogue shared by the bf16 kernels: the accumulators of wave (wm, wn)
 // of the tile (each WM x WN, acc[i][j][4*g + q] = C[row wm*WM + i*32 + lane%32]
 // [col wn*WN + j*32 + 8*g + 4*(lane/32) + q]) to global memory, staged
@@ -607,10 +641,11 @@ struct IntC {
 // ones (an expert's short last tile, or padding only). Every XCD (blocks are
 // dispatched round-robin over the 8 XCDs) takes an equal share of each class
 // and runs its heavy tiles first, so that the light tiles make up the last,
-// partial round on every XCD instead of a full-cost round on some. Inside a
-// class, consecutive tiles walk kRowGroup row tiles x the column tiles, row
-// tiles fastest, so that the blocks running together on one XCD share A rows
-// and B columns through its L2. Returns false for a block with no tile.
+// partial round on every XCD instead of a full-cost round on some. The heavy
+// tiles (the experts' heavy row tiles one after the other x the column
+// tiles) are walked in shared 16 x 16 blocks (shared_block_tile); inside the
+// light class, consecutive tiles walk kRowGroup row tiles x the column
+// tiles, row tiles fastest. Returns false for a block with no tile.
 template <int BM>
 __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, int& e, int& mt,
                                                   int& nt, int& rows_e, int& cnt_e) {
@@ -635,23 +670,21 @@ __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, 
   const int H = HR * p.ntiles, L = LR * p.ntiles;
   const int hx = (H >> 3) + (x < (H & 7)), lx = (L >> 3) + (x < (L & 7));
   bool heavy;
-  int idx, nrows;
+  int ml;
   if (i < hx) {
     heavy = true;
-    idx = x * (H >> 3) + min(x, H & 7) + i;
-    nrows = HR;
+    shared_block_tile(i * 8 + x, HR, p.ntiles, ml, nt);  // (i * 8 + x < H)
   } else if (i < hx + lx) {
     heavy = false;
-    idx = x * (L >> 3) + min(x, L & 7) + (i - hx);
-    nrows = LR;
+    const int idx = x * (L >> 3) + min(x, L & 7) + (i - hx);
+    const int gsz = kRowGroup * p.ntiles;
+    const int g = idx / gsz, rg = idx - g * gsz;
+    const int gm = min(kRowGroup, LR - g * kRowGroup);  // row tiles in this group
+    nt = rg / gm;
+    ml = g * kRowGroup + (rg - nt * gm);
   } else {
     return false;
   }
-  const int gsz = kRowGroup * p.ntiles;
-  const int g = idx / gsz, rg = idx - g * gsz;
-  const int gm = min(kRowGroup, nrows - g * kRowGroup);  // row tiles in this group
-  nt = rg / gm;
-  const int ml = g * kRowGroup + (rg - nt * gm);
   int acc_t = 0;
   for (e = 0; e < p.E; ++e) {
     int c, r, te, he;
@@ -771,7 +804,6 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
-  const int vbid = xcd_remap(blockIdx.x, gridDim.x);
 
   // ---- which tile ----
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
@@ -781,7 +813,10 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
     cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
     row0 = p.offsets[e] + mt * BM;
   } else {
-    ksum_tile(vbid, (p.Mdim + BM - 1) / BM, (p.N + BN - 1) / BN, e, mt, nt);
+    // expert e's mtn x ntn tiles, walked in shared 16 x 16 blocks
+    const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
+    e = blockIdx.x / (mtn * ntn);
+    shared_block_tile(blockIdx.x - e * (mtn * ntn), mtn, ntn, mt, nt);
     cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
     row0 = p.offsets[e];
   }
