@@ -12,7 +12,8 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libflowmoe.so")
+# FLOWMOE_LIB names another build of the library (the host-sanitized one)
+LIB_PATH = os.environ.get("FLOWMOE_LIB") or os.path.join(_HERE, "libflowmoe.so")
 
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1

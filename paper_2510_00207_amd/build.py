@@ -76,8 +76,61 @@ def build(jobs: int | None = None, verbose: bool = True) -> str:
     return LIB
 
 
+# host-side sanitizers for the C ABI front end (argument validation, status
+# codes, capacity and workspace arithmetic, the event pool): each -fsanitize
+# applies to the host compilation only (-Xarch_host); the device code is built
+# as usual
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host",
+            "-fno-omit-frame-pointer"]
+SAN_DIR = os.path.join(BUILD, "sanitize")
+SAN_LIB = os.path.join(SAN_DIR, "libflowmoe_san.so")
+
+
+def asan_runtime() -> str:
+    """The clang ASan runtime that a process loading the sanitized library
+    must preload (its host executable is not instrumented)."""
+    llvm = os.path.join(os.path.dirname(os.path.dirname(hipcc())), "llvm", "lib", "clang")
+    for ver in sorted(os.listdir(llvm), reverse=True):
+        p = os.path.join(llvm, ver, "lib", "linux", "libclang_rt.asan-x86_64.so")
+        if os.path.exists(p):
+            return p
+    raise RuntimeError("clang ASan runtime not found")
+
+
+def build_sanitized(jobs: int | None = None, verbose: bool = True) -> str:
+    """libflowmoe_san.so: abi.hip's host code built with ASan and UBSan, the
+    other sources as usual, for host-only tests of the ABI front end."""
+    cc = hipcc()
+    os.makedirs(SAN_DIR, exist_ok=True)
+    srcs = sources()
+    objs = [os.path.join(SAN_DIR, os.path.basename(s)[:-4] + ".o") for s in srcs]
+
+    def compile_one(pair):
+        src, obj = pair
+        extra = SANITIZE if os.path.basename(src) == "abi.hip" else []
+        _run([cc, *HIPCC_FLAGS, *extra, "-c", src, "-o", obj])
+        if verbose:
+            print(f"[build] compiled {os.path.basename(src)}{' (sanitized)' if extra else ''}",
+                  flush=True)
+
+    with cf.ThreadPoolExecutor(jobs or min(8, len(srcs))) as ex:
+        list(ex.map(compile_one, zip(srcs, objs)))
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-Xarch_host",
+          "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-Xarch_host",
+          "-shared-libasan", "-o", SAN_LIB])
+    if verbose:
+        print(f"[build] linked {SAN_LIB}", flush=True)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=None)
+    ap.add_argument("--sanitize", action="store_true",
+                    help="build the host-sanitized library for the ABI tests instead")
     a = ap.parse_args()
-    build(a.jobs)
+    if a.sanitize:
+        build_sanitized(a.jobs)
+    else:
+        build(a.jobs)
