@@ -24,7 +24,9 @@ Recipe (all tensors row-major):
     (E x M x H); W2 ~ N(0, 0.02^2) (E x H x M); dy ~ N(0,1) (T x M);
   * the skewed workload adds a constant per-expert gate bias
     b_e = -1.2 * ln(rho_e), rho a seeded permutation of 1..E (log of a Zipf
-    pmf with s = 1.2, up to a shift), so expert loads are heavy-tailed.
+    pmf with s = 1.2, up to a shift), so expert loads are heavy-tailed;
+  * biased experts (expert_bias=True) add b1, b3 ~ N(0, 0.02^2) (E x H) and
+    b2 ~ N(0, 0.02^2) (E x M) in float32.
 
 bf16 tensors are held as numpy uint16 bit patterns; ``as_f64`` widens any
 stored tensor exactly to float64.
@@ -46,7 +48,8 @@ WEIGHT_STD = 0.02
 ZIPF_S = 1.2
 
 # tensor ids for the per-tensor streams
-_TID = {"x": 0, "w_gate": 1, "bias": 2, "w1": 3, "w3": 4, "w2": 5, "dy": 6}
+_TID = {"x": 0, "w_gate": 1, "bias": 2, "w1": 3, "w3": 4, "w2": 5, "dy": 6, "b1": 7, "b3": 8,
+        "b2": 9}
 _BLOCK = 1 << 22  # elements per independently seeded block
 
 
@@ -65,6 +68,7 @@ class MoEConfig:
     zipf_bias: bool = False
     seed: int = 0
     gate: str = "renorm"  # gate weights: "renorm" (softmax over the selection) | "full"
+    expert_bias: bool = False  # biased experts: b1, b3 (E x H), b2 (E x M), fp32
 
     def replace(self, **kw) -> "MoEConfig":
         return dataclasses.replace(self, **kw)
@@ -157,8 +161,10 @@ def make_inputs(cfg: MoEConfig, *, with_dy: bool = True, x_zero_rows=None) -> di
     """All layer inputs for ``cfg`` in storage form.
 
     Returns a dict with x (T,M), w_gate (M,E), bias (E,) float32 or None,
-    w1 (E,M,H), w3 (E,M,H) or None, w2 (E,H,M), dy (T,M). Storage arrays are
-    float32 for dtype 'f32' and uint16 bf16 bits for 'bf16'.
+    w1 (E,M,H), w3 (E,M,H) or None, w2 (E,H,M), dy (T,M), and the experts'
+    biases b1 (E,H), b3 (E,H), b2 (E,M) float32 (None unless
+    cfg.expert_bias; b3 only for SwiGLU). Storage arrays are float32 for
+    dtype 'f32' and uint16 bf16 bits for 'bf16'.
     ``x_zero_rows`` (iterable of token indices) zeroes those rows of x, which
     makes their gate logits all tie (edge-case inputs).
     """
@@ -176,6 +182,13 @@ def make_inputs(cfg: MoEConfig, *, with_dy: bool = True, x_zero_rows=None) -> di
                  if cfg.act == "swiglu" else None)
     out["w2"] = _normal(s, _TID["w2"], E * H * M, WEIGHT_STD, dt).reshape(E, H, M)
     out["dy"] = _normal(s, _TID["dy"], T * M, 1.0, dt).reshape(T, M) if with_dy else None
+    if cfg.expert_bias:  # fp32 like the gate bias
+        out["b1"] = _normal(s, _TID["b1"], E * H, WEIGHT_STD, "f32").reshape(E, H)
+        out["b3"] = (_normal(s, _TID["b3"], E * H, WEIGHT_STD, "f32").reshape(E, H)
+                     if cfg.act == "swiglu" else None)
+        out["b2"] = _normal(s, _TID["b2"], E * M, WEIGHT_STD, "f32").reshape(E, M)
+    else:
+        out["b1"] = out["b3"] = out["b2"] = None
     return out
 
 

@@ -16,6 +16,9 @@ Pins (what each function is checked against, in tests/test_oracle_pins.py):
   dispatch        exact copy (bitwise)
   expert_ffn(+bwd) dense torch-fp64 autograd formulation; central finite
                   differences; closed-form derivatives of GELU and SiLU
+  expert_bias_grads  the same autograd formulation and finite differences
+                  with biased experts; zero weights give y = b2 per kept
+                  assignment (closed form)
   combine(+bwd)   identity experts give (sum of kept w) * x; k = E with no
                   drops equals the dense softmax mixture of experts
   gate_bwd        torch autograd of the masked dense formulation; finite
@@ -28,6 +31,6 @@ no numeric output of an MoE layer.
 """
 from .moe_ref import (  # noqa: F401
     capacity, rows_capacity, gate_logits, topk_select, route, dispatch,
-    expert_ffn, combine, combine_bwd, expert_ffn_bwd, dispatch_bwd, gate_bwd,
+    expert_ffn, combine, combine_bwd, expert_ffn_bwd, expert_bias_grads, dispatch_bwd, gate_bwd,
     gelu, gelu_grad, silu, silu_grad, layer_chunk, layer_fwd_bwd,
 )

@@ -17,8 +17,10 @@ notes with its reason):
   * capacity priority: every first choice before any second choice, and
     ascending token order within a rank; weights are renormalised before the
     drop, so a token's kept weights may sum to less than one;
-  * experts have no biases; GELU is the exact erf form, SwiGLU is
-    silu(x W1) * (x W3) followed by W2;
+  * experts have no biases unless given (b1, b3 added to the first layer's
+    pre-activations, b2 to the second layer's output, the biased two-layer
+    experts that the parameter counts of Table 3 imply); GELU is the exact
+    erf form, SwiGLU is silu(x W1 + b1) * (x W3 + b3) followed by W2;
   * routing is piecewise constant: selection and dropping carry no gradient.
 """
 from __future__ import annotations
@@ -147,11 +149,12 @@ def silu_grad(z):
     return s * (1.0 + z * (1.0 - s))
 
 
-def expert_ffn(x_disp, counts, offsets, w1, w3, w2, act):
+def expert_ffn(x_disp, counts, offsets, w1, w3, w2, act, b1=None, b3=None, b2=None):
     """Step 7: each expert's two-layer FFN (Sec. 2.1: M x H then H x M) over
-    its rows [offsets[e], offsets[e] + counts[e]). Returns the pre-activations
-    h1 (and h3 for SwiGLU), the activation a that feeds W2, and y_disp.
-    Rows outside every expert's range stay zero."""
+    its rows [offsets[e], offsets[e] + counts[e]), with optional biases
+    (b1, b3: E x H on the first layer, b2: E x M on the second). Returns the
+    pre-activations h1 (and h3 for SwiGLU), the activation a that feeds W2,
+    and y_disp. Rows outside every expert's range stay zero."""
     rows, M = x_disp.shape
     H = w1.shape[2]
     h1 = np.zeros((rows, H))
@@ -164,12 +167,18 @@ def expert_ffn(x_disp, counts, offsets, w1, w3, w2, act):
             continue
         X = x_disp[lo:hi]
         h1[lo:hi] = X @ w1[e]
+        if b1 is not None:
+            h1[lo:hi] += b1[e]
         if act == "gelu":
             a[lo:hi] = gelu(h1[lo:hi])
         else:
             h3[lo:hi] = X @ w3[e]
+            if b3 is not None:
+                h3[lo:hi] += b3[e]
             a[lo:hi] = silu(h1[lo:hi]) * h3[lo:hi]
         y[lo:hi] = a[lo:hi] @ w2[e]
+        if b2 is not None:
+            y[lo:hi] += b2[e]
     return dict(h1=h1, h3=h3, a=a, y_disp=y)
 
 
@@ -240,6 +249,25 @@ def expert_ffn_bwd(dy_disp, x_disp, saved, counts, offsets, w1, w3, w2, act, ret
     return dx_disp, dw1, dw3, dw2
 
 
+def expert_bias_grads(dy_disp, dh, counts, offsets, act):
+    """Step 10's bias part: each bias gradient is the sum over the expert's
+    rows of the gradient of the pre-activation it is added to: db2_e = sum
+    of dY rows, db1_e = sum of dH1 rows (db3_e = sum of dH3 rows), with dH
+    as expert_ffn_bwd(..., return_dh=True) gives it."""
+    E = counts.shape[0]
+    M = dy_disp.shape[1]
+    H = dh.shape[1] if act == "gelu" else dh.shape[1] // 2
+    db1, db2 = np.zeros((E, H)), np.zeros((E, M))
+    db3 = np.zeros((E, H)) if act == "swiglu" else None
+    for e in range(E):
+        lo, hi = int(offsets[e]), int(offsets[e]) + int(counts[e])
+        db2[e] = dy_disp[lo:hi].sum(axis=0)
+        db1[e] = dh[lo:hi, :H].sum(axis=0)
+        if act == "swiglu":
+            db3[e] = dh[lo:hi, H:].sum(axis=0)
+    return db1, db3, db2
+
+
 def dispatch_bwd(dx_disp, slot):
     """Step 11: dx_t = sum over kept assignments of dx_disp[slot_tj]."""
     T, k = slot.shape
@@ -279,18 +307,18 @@ def gate_bwd(x, w_gate, topk_idx, w, dw, logits=None, gate="renorm"):
 # one chunk, and the chunked layer (Sec. 3.2 partition; App. H accumulation)
 # ---------------------------------------------------------------------------
 def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
-                logits_for_routing=None, gate="renorm"):
+                logits_for_routing=None, gate="renorm", b1=None, b3=None, b2=None):
     """Forward and backward of one chunk. ``logits_for_routing`` (the GPU's
     fp32 logits widened to fp64) replaces the oracle's own logits for
     selection and gate weights, so that floating-point parity is measured
-    on the same routing."""
+    on the same routing. b1, b3, b2: the experts' biases (or None)."""
     E = w_gate.shape[1]
     logits = gate_logits(x, w_gate, bias)
     lr = logits if logits_for_routing is None else logits_for_routing
     idx, w = topk_select(lr, k, gate)
     rt = route(idx, E, C, layout)
     x_disp = dispatch(x, rt["row_src"], k)
-    sv = expert_ffn(x_disp, rt["counts"], rt["offsets"], w1, w3, w2, act)
+    sv = expert_ffn(x_disp, rt["counts"], rt["offsets"], w1, w3, w2, act, b1, b3, b2)
     y = combine(sv["y_disp"], rt["slot"], w)
     out = dict(logits=logits, topk_idx=idx, topk_w=w, x_disp=x_disp, y=y, **rt, **sv)
     if dy is None:
@@ -303,6 +331,9 @@ def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
     out.update(dy_disp=dy_disp, d_topk_w=dw, dx_disp=dx_disp, dh=dh, dw1=dw1, dw3=dw3, dw2=dw2,
                d_logits=g["d_logits"], dw_gate=g["dw_gate"], dbias=g["dbias"],
                dx=dx + g["dx_gate"], dx_experts=dx)
+    if b1 is not None or b3 is not None or b2 is not None:
+        db1, db3, db2 = expert_bias_grads(dy_disp, dh, rt["counts"], rt["offsets"], act)
+        out.update(db1=db1, db3=db3, db2=db2)
     return out
 
 
@@ -311,7 +342,8 @@ def layer_fwd_bwd(inp, k, f, act, R=1, layout=PACKED, logits_for_routing=None,
     """The layer over T tokens split into R equal contiguous chunks, each an
     independent layer call with its own capacity; per-token outputs are
     concatenated and weight gradients summed over chunks. ``inp`` holds
-    float64 arrays x, w_gate, bias (or None), w1, w3 (or None), w2, dy."""
+    float64 arrays x, w_gate, bias (or None), w1, w3 (or None), w2, dy, and
+    optionally the experts' biases b1, b3, b2."""
     x = inp["x"]
     T = x.shape[0]
     if T % R:
@@ -326,12 +358,13 @@ def layer_fwd_bwd(inp, k, f, act, R=1, layout=PACKED, logits_for_routing=None,
         lr = None if logits_for_routing is None else logits_for_routing[sl]
         dy = None if inp.get("dy") is None else inp["dy"][sl]
         chunks.append(layer_chunk(x[sl], inp["w_gate"], inp.get("bias"), inp["w1"],
-                                  inp.get("w3"), inp["w2"], dy, k, C, act, layout, lr, gate))
+                                  inp.get("w3"), inp["w2"], dy, k, C, act, layout, lr, gate,
+                                  inp.get("b1"), inp.get("b3"), inp.get("b2")))
     res = dict(C=C, chunks=chunks)
     for key in ("logits", "topk_idx", "topk_w", "y", "dx", "d_topk_w", "d_logits"):
         if key in chunks[0]:
             res[key] = np.concatenate([c[key] for c in chunks], axis=0)
-    for key in ("dw1", "dw3", "dw2", "dw_gate", "dbias"):
+    for key in ("dw1", "dw3", "dw2", "dw_gate", "dbias", "db1", "db3", "db2"):
         if key in chunks[0] and chunks[0][key] is not None:
             res[key] = sum(c[key] for c in chunks)
     return res

@@ -253,6 +253,7 @@ def _torch_layer_grads(inp, k, C, act, gate="renorm"):
     t64 = lambda a: None if a is None else torch.tensor(a, dtype=torch.float64, requires_grad=True)
     x, wg, w1, w2 = t64(inp["x"]), t64(inp["w_gate"]), t64(inp["w1"]), t64(inp["w2"])
     w3 = t64(inp["w3"])
+    b1, b3, b2 = t64(inp.get("b1")), t64(inp.get("b3")), t64(inp.get("b2"))
     b = t64(inp["bias"]) if inp["bias"] is not None else None
     T, E = x.shape[0], wg.shape[1]
     l = x @ wg + (b if b is not None else 0)
@@ -272,12 +273,12 @@ def _torch_layer_grads(inp, k, C, act, gate="renorm"):
         g = torch.softmax(lm, dim=1) * keep
     y = torch.zeros_like(x)
     for e in range(E):
-        h1 = x @ w1[e]
+        h1 = x @ w1[e] + (b1[e] if b1 is not None else 0)
         if act == "gelu":
             a = torch.nn.functional.gelu(h1)
         else:
-            a = torch.nn.functional.silu(h1) * (x @ w3[e])
-        y = y + g[:, e:e + 1] * (a @ w2[e])
+            a = torch.nn.functional.silu(h1) * (x @ w3[e] + (b3[e] if b3 is not None else 0))
+        y = y + g[:, e:e + 1] * (a @ w2[e] + (b2[e] if b2 is not None else 0))
     dy = torch.tensor(inp["dy"], dtype=torch.float64)
     (y * dy).sum().backward()
     res = dict(y=y.detach().numpy(), dx=x.grad.numpy(), dw_gate=wg.grad.numpy(),
@@ -286,11 +287,14 @@ def _torch_layer_grads(inp, k, C, act, gate="renorm"):
         res["dw3"] = w3.grad.numpy()
     if b is not None:
         res["dbias"] = b.grad.numpy()
+    for name, p in (("db1", b1), ("db3", b3), ("db2", b2)):
+        if p is not None:
+            res[name] = p.grad.numpy()
     return res
 
 
-def _small_inputs(rng, T, M, H, E, act, bias=True):
-    return dict(
+def _small_inputs(rng, T, M, H, E, act, bias=True, expert_bias=False):
+    inp = dict(
         x=rng.standard_normal((T, M)),
         w_gate=rng.standard_normal((M, E)) * 0.3,
         bias=rng.standard_normal(E) * 0.2 if bias else None,
@@ -299,19 +303,64 @@ def _small_inputs(rng, T, M, H, E, act, bias=True):
         w2=rng.standard_normal((E, H, M)) * 0.3,
         dy=rng.standard_normal((T, M)),
     )
+    if expert_bias:
+        inp.update(b1=rng.standard_normal((E, H)) * 0.3,
+                   b3=rng.standard_normal((E, H)) * 0.3 if act == "swiglu" else None,
+                   b2=rng.standard_normal((E, M)) * 0.3)
+    return inp
 
 
+@pytest.mark.parametrize("expert_bias", [False, True])
 @pytest.mark.parametrize("gate", ["renorm", "full"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
 @pytest.mark.parametrize("f", [0.5, 1.0, 4.0])
-def test_layer_grads_match_torch_autograd(rng, act, layout, f, gate):
+def test_layer_grads_match_torch_autograd(rng, act, layout, f, gate, expert_bias):
     T, M, H, E, k = 24, 8, 12, 4, 2
-    inp = _small_inputs(rng, T, M, H, E, act)
+    inp = _small_inputs(rng, T, M, H, E, act, expert_bias=expert_bias)
     out = oracle.layer_fwd_bwd(inp, k=k, f=f, act=act, layout=layout, gate=gate)
     ref = _torch_layer_grads(inp, k, out["C"], act, gate)
+    assert ("db1" in ref) == expert_bias and ("db2" in out) == expert_bias
     for key in ref:
         np.testing.assert_allclose(out[key], ref[key], rtol=1e-11, atol=1e-12, err_msg=key)
+
+
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+def test_biased_experts_with_zero_weights(rng, act, layout):
+    """With every expert weight zero, FFN_e(x) = b2_e whatever the input (the
+    first layer's output is multiplied by W2 = 0), so y_t is the kept gate
+    weights times the chosen experts' b2 (Sec. 2.1 with constant experts);
+    db2_e = sum of w_tj dy_t over e's kept assignments, dW2_e = a^T dY with
+    a = act(b1_e) on every kept row, and dW1 = dW3 = db1 = db3 = 0 (dA = dY
+    W2^T = 0). Rows past an expert's count stay zero in the padded layout."""
+    T, M, H, E, k = 30, 6, 5, 4, 2
+    inp = _small_inputs(rng, T, M, H, E, act, expert_bias=True)
+    for w in ("w1", "w3", "w2"):
+        if inp[w] is not None:
+            inp[w] = np.zeros_like(inp[w])
+    out = oracle.layer_fwd_bwd(inp, k=k, f=0.75, act=act, layout=layout)
+    c = out["chunks"][0]
+    idx, w, slot = c["topk_idx"], c["topk_w"], c["slot"]
+    kept = slot >= 0
+    assert kept.any() and not kept.all()
+    y = np.zeros((T, M))
+    db2 = np.zeros((E, M))
+    for t in range(T):
+        for j in range(k):
+            if kept[t, j]:
+                y[t] += w[t, j] * inp["b2"][idx[t, j]]
+                db2[idx[t, j]] += w[t, j] * inp["dy"][t]
+    np.testing.assert_allclose(out["y"], y, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(out["db2"], db2, rtol=1e-13, atol=1e-14)
+    a = oracle.gelu(inp["b1"]) if act == "gelu" else oracle.silu(inp["b1"]) * inp["b3"]
+    np.testing.assert_allclose(out["dw2"], a[:, :, None] * db2[:, None, :], rtol=1e-12, atol=1e-14)
+    for name in ("dw1", "db1") + (("dw3", "db3") if act == "swiglu" else ()):
+        assert not out[name].any(), name
+    live = np.zeros(c["rows"], bool)
+    for e in range(E):
+        live[c["offsets"][e]:c["offsets"][e] + c["counts"][e]] = True
+    assert not c["y_disp"][~live].any() and not c["h1"][~live].any()
 
 
 def test_zero_capacity_leaves_only_gate_path(rng):
@@ -324,11 +373,12 @@ def test_zero_capacity_leaves_only_gate_path(rng):
     assert not out["dx"].any() and not out["dw_gate"].any()
 
 
+@pytest.mark.parametrize("expert_bias", [False, True])
 @pytest.mark.parametrize("gate", ["renorm", "full"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
-def test_layer_finite_differences(rng, act, gate):
+def test_layer_finite_differences(rng, act, gate, expert_bias):
     T, M, H, E, k = 10, 6, 5, 3, 2
-    inp = _small_inputs(rng, T, M, H, E, act)
+    inp = _small_inputs(rng, T, M, H, E, act, expert_bias=expert_bias)
     out = oracle.layer_fwd_bwd(inp, k=k, f=1.0, act=act, gate=gate)
     # routing must be locally constant for the check to hold
     l = out["logits"]
@@ -341,7 +391,10 @@ def test_layer_finite_differences(rng, act, gate):
 
     h = 1e-6
     names = ["x", "w_gate", "bias", "w1", "w2"] + (["w3"] if act == "swiglu" else [])
-    gname = {"x": "dx", "w_gate": "dw_gate", "bias": "dbias", "w1": "dw1", "w2": "dw2", "w3": "dw3"}
+    if expert_bias:
+        names += ["b1", "b2"] + (["b3"] if act == "swiglu" else [])
+    gname = {"x": "dx", "w_gate": "dw_gate", "bias": "dbias", "w1": "dw1", "w2": "dw2", "w3": "dw3",
+             "b1": "db1", "b2": "db2", "b3": "db3"}
     for name in names:
         a = inp[name]
         for flat in rng.choice(a.size, size=min(6, a.size), replace=False):
