@@ -160,18 +160,23 @@ flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* t
  * each expert's rows (counts and offsets as flowmoe_dispatch writes them;
  * they are device data, so they are not checked on the host, but a range
  * they would take past the rows buffers is cut there), as one grouped GEMM
- * per layer:
- *   GELU:   h = X W1_e,              a = gelu(h) (exact erf form)
- *   SwiGLU: h1 = X W1_e, h3 = X W3_e, a = silu(h1) * h3
- *   y_disp = a W2_e.
+ * per layer, with optional biases (the biased two-layer experts that the
+ * parameter counts of Table 3 imply):
+ *   GELU:   h = X W1_e + b1_e,                         a = gelu(h) (exact erf)
+ *   SwiGLU: h1 = X W1_e + b1_e, h3 = X W3_e + b3_e,    a = silu(h1) * h3
+ *   y_disp = a W2_e + b2_e.
  *   w1, w3   E x M x H layer dtype (w3 used only for SwiGLU, else nullable)
  *   w2       E x H x M layer dtype
+ *   b1, b3   E x H float, nullable (b3 used for SwiGLU only); b2 E x M
+ *            float, nullable; 16-byte aligned. Rows past an expert's count
+ *            (the padded layout) stay zero: no bias is added to them.
  *   h_save   rows x H (GELU) or rows x 2H ([h1 | h3], SwiGLU) (out)
  *   a_save   rows x H (out)  -- both kept for the backward
  *   y_disp   rows x M (out) */
 flowmoe_status_t flowmoe_expert_ffn(const flowmoe_shape_t* shape, const void* x_disp,
                                     const int32_t* counts, const int32_t* offsets,
                                     const void* w1, const void* w3, const void* w2,
+                                    const float* b1, const float* b3, const float* b2,
                                     void* h_save, void* a_save, void* y_disp,
                                     hipStream_t stream);
 
@@ -195,9 +200,14 @@ flowmoe_status_t flowmoe_combine_bwd(const flowmoe_shape_t* shape, const void* d
 /* Expert FFN backward: dA = dY W2_e^T, dW2_e = A^T dY; through the
  * activation (GELU: dH = dA * gelu'(h); SwiGLU: dH1 = dA * h3 * silu'(h1),
  * dH3 = dA * silu(h1)); dW1_e = X^T dH1, dW3_e = X^T dH3,
- * dX = dH1 W1_e^T (+ dH3 W3_e^T).
+ * dX = dH1 W1_e^T (+ dH3 W3_e^T); the biases' gradients are the column sums
+ * over expert e's rows: db2_e = sum dY, db1_e = sum dH1, db3_e = sum dH3.
  *   dw1, dw3 E x M x H float; dw2 E x H x M float. With accumulate != 0 the
- *   weight gradients are added to (sum over chunks, App. H), else written.
+ *   weight (and bias) gradients are added to (sum over chunks, App. H),
+ *   else written.
+ *   db1, db3 E x H float, db2 E x M float: each nullable (not computed),
+ *   16-byte aligned; they do not depend on whether the forward had biases
+ *   (h_save holds the biased pre-activations).
  *   dx_disp rows x M layer dtype (out).
  *   ws: flowmoe_workspace_bytes(shape, FLOWMOE_WS_FFN_BWD) bytes. */
 flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void* dy_disp,
@@ -205,8 +215,9 @@ flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void
                                         const void* a_save, const int32_t* counts,
                                         const int32_t* offsets, const void* w1,
                                         const void* w3, const void* w2, void* dx_disp,
-                                        float* dw1, float* dw3, float* dw2, int32_t accumulate,
-                                        void* ws, size_t ws_bytes, hipStream_t stream);
+                                        float* dw1, float* dw3, float* dw2, float* db1,
+                                        float* db3, float* db2, int32_t accumulate, void* ws,
+                                        size_t ws_bytes, hipStream_t stream);
 
 /* Dispatch backward: dx[t] = sum over kept j of dx_disp[slot[t][j]]
  * (zero for a token with no kept assignment). dx is T x M layer dtype. */
@@ -278,7 +289,8 @@ enum {
   FLOWMOE_K_GATE_BWD_WT = 13,    /* stacked W_g^T of the full softmax gate's dense dx term */
   FLOWMOE_K_GATE_BWD_TOKEN = 14, /* dx += d_logits W_g^T (flowmoe_gate_topk_bwd with dx) */
   FLOWMOE_K_GATE_BWD_DW = 15,    /* d_logits, and dW_g / db split-T partials */
-  FLOWMOE_K_GATE_BWD_REDUCE = 16 /* dW_g / db reduction over splits (+ W_g^T for the dx term) */
+  FLOWMOE_K_GATE_BWD_REDUCE = 16, /* dW_g / db reduction over splits (+ W_g^T for the dx term) */
+  FLOWMOE_K_BIAS_GRAD = 17        /* the experts' bias gradients (column sums of dY, dH) */
 };
 
 /* Start tracing on the calling host thread: every later kernel launch whose
@@ -333,6 +345,9 @@ typedef struct {
   const void* w1;     /* E x M x H */
   const void* w3;     /* E x M x H, SwiGLU only */
   const void* w2;     /* E x H x M */
+  const float* b1;    /* E x H, nullable: the experts' biases (flowmoe_expert_ffn) */
+  const float* b3;    /* E x H, nullable, SwiGLU only */
+  const float* b2;    /* E x M, nullable */
   /* forward */
   const void* x;      /* RT x M */
   float* logits;      /* RT x E */
@@ -360,6 +375,9 @@ typedef struct {
   float* dw1;         /* E x M x H, summed over chunks */
   float* dw3;         /* E x M x H, SwiGLU only */
   float* dw2;         /* E x H x M */
+  float* db1;         /* E x H, nullable: the experts' bias gradients, summed over chunks */
+  float* db3;         /* E x H, nullable, SwiGLU only */
+  float* db2;         /* E x M, nullable */
   /* scratch */
   void* ws;           /* flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
                          nullable in the forward, which uses it as the

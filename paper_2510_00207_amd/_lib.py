@@ -39,11 +39,11 @@ class Shape(ctypes.Structure):
 
 _VP = ctypes.c_void_p
 _LAYER_FIELDS = [
-    "w_gate", "bias", "w1", "w3", "w2",
+    "w_gate", "bias", "w1", "w3", "w2", "b1", "b3", "b2",
     "x", "logits", "topk_idx", "topk_w", "counts", "offsets", "slot", "row_src", "load",
     "x_disp", "h_save", "a_save", "y_disp", "y",
     "dy", "dy_disp", "d_topk_w", "dx_disp", "dx", "d_logits", "dw_gate", "dbias", "dw1", "dw3",
-    "dw2", "ws",
+    "dw2", "db1", "db3", "db2", "ws",
 ]
 
 
@@ -78,10 +78,11 @@ def load():
         "flowmoe_gate_topk": ([SP, P, P, P, P, P, P, P], I32),
         "flowmoe_route": ([SP, P, P, P, P], I32),
         "flowmoe_dispatch": ([SP, P, P, P, P, P, P, P, P, P, SZ, P], I32),
-        "flowmoe_expert_ffn": ([SP, P, P, P, P, P, P, P, P, P, P], I32),
+        "flowmoe_expert_ffn": ([SP, P, P, P, P, P, P, P, P, P, P, P, P, P], I32),
         "flowmoe_combine": ([SP, P, P, P, P, P], I32),
         "flowmoe_combine_bwd": ([SP, P, P, P, P, P, P, P, P, P], I32),
-        "flowmoe_expert_ffn_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
+        "flowmoe_expert_ffn_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, I32, P, SZ,
+                                    P], I32),
         "flowmoe_dispatch_bwd": ([SP, P, P, P, P], I32),
         "flowmoe_gate_topk_bwd": ([SP, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P], I32),
         "flowmoe_gate_topk_bwd_noalloc": ([SP, P, P, P, P, P, P, P, P, P, P, I32, P], I32),
@@ -167,10 +168,10 @@ def flowmoe_dispatch(shape, topk_idx, x, counts, offsets, slot, row_src, load_, 
 
 
 def flowmoe_expert_ffn(shape, x_disp, counts, offsets, w1, w3, w2, h_save, a_save, y_disp,
-                       stream=None):
+                       stream=None, b1=None, b3=None, b2=None):
     _check(load().flowmoe_expert_ffn(ctypes.byref(shape), ptr(x_disp), ptr(counts), ptr(offsets),
-                                     ptr(w1), ptr(w3), ptr(w2), ptr(h_save), ptr(a_save),
-                                     ptr(y_disp), _stream(stream)))
+                                     ptr(w1), ptr(w3), ptr(w2), ptr(b1), ptr(b3), ptr(b2),
+                                     ptr(h_save), ptr(a_save), ptr(y_disp), _stream(stream)))
 
 
 def flowmoe_combine(shape, y_disp, slot, topk_w, y, stream=None):
@@ -187,12 +188,13 @@ def flowmoe_combine_bwd(shape, dy, y_disp, slot, topk_w, counts, offsets, dy_dis
 
 
 def flowmoe_expert_ffn_bwd(shape, dy_disp, x_disp, h_save, a_save, counts, offsets, w1, w3, w2,
-                           dx_disp, dw1, dw3, dw2, accumulate, ws, ws_bytes, stream=None):
+                           dx_disp, dw1, dw3, dw2, accumulate, ws, ws_bytes, stream=None,
+                           db1=None, db3=None, db2=None):
     _check(load().flowmoe_expert_ffn_bwd(ctypes.byref(shape), ptr(dy_disp), ptr(x_disp),
                                          ptr(h_save), ptr(a_save), ptr(counts), ptr(offsets),
                                          ptr(w1), ptr(w3), ptr(w2), ptr(dx_disp), ptr(dw1),
-                                         ptr(dw3), ptr(dw2), int(accumulate), ptr(ws), ws_bytes,
-                                         _stream(stream)))
+                                         ptr(dw3), ptr(dw2), ptr(db1), ptr(db3), ptr(db2),
+                                         int(accumulate), ptr(ws), ws_bytes, _stream(stream)))
 
 
 def flowmoe_dispatch_bwd(shape, dx_disp, slot, dx, stream=None):
@@ -223,7 +225,7 @@ def flowmoe_gate_topk_bwd_noalloc(shape, x, w_gate, logits, topk_idx, topk_w, d_
 # ---- kernel tracing --------------------------------------------------------------
 K_NAMES = ["gate", "route", "scan", "gather", "ffn1", "ffn2", "swiglu_act", "combine",
            "combine_bwd", "dgrad1", "wgrad2", "wgrad1", "dgrad2", "gate_bwd_wt", "gate_bwd_token",
-           "gate_bwd_dw", "gate_bwd_reduce"]
+           "gate_bwd_dw", "gate_bwd_reduce", "bias_grad"]
 K = {n: i for i, n in enumerate(K_NAMES)}
 K_GEMM = ("ffn1", "ffn2", "dgrad1", "wgrad2", "wgrad1", "dgrad2")
 

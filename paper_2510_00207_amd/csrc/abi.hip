@@ -93,6 +93,18 @@ flowmoe_status_t check_shape(const flowmoe_shape_t* s, int need, Shape* out) {
   if (reinterpret_cast<uintptr_t>(p) % 16 != 0)                                 \
     return fail(FLOWMOE_ERR_INVALID, "%s is not 16-byte aligned", name)
 
+// the experts' biases (or their gradients, prefix "d"): each nullable, float,
+// 16-byte aligned (moved in 16-byte vectors); b3 is used with SwiGLU only
+flowmoe_status_t check_biases(const Shape& s, const float* b1, const float* b3, const float* b2,
+                              const char* prefix) {
+  const float* p[3] = {b1, s.act == FLOWMOE_SWIGLU ? b3 : nullptr, b2};
+  const char* n[3] = {"b1", "b3", "b2"};
+  for (int i = 0; i < 3; ++i)
+    if (p[i] != nullptr && reinterpret_cast<uintptr_t>(p[i]) % 16 != 0)
+      return fail(FLOWMOE_ERR_INVALID, "%s%s is not 16-byte aligned", prefix, n[i]);
+  return FLOWMOE_OK;
+}
+
 flowmoe_status_t check_ws(void* ws, size_t have, size_t need, const char* call) {
   if (need == 0) return FLOWMOE_OK;
   if (ws == nullptr || have < need)
@@ -322,6 +334,7 @@ flowmoe_status_t flowmoe_dispatch(const flowmoe_shape_t* shape, const int32_t* t
 flowmoe_status_t flowmoe_expert_ffn(const flowmoe_shape_t* shape, const void* x_disp,
                                     const int32_t* counts, const int32_t* offsets,
                                     const void* w1, const void* w3, const void* w2,
+                                    const float* b1, const float* b3, const float* b2,
                                     void* h_save, void* a_save, void* y_disp,
                                     hipStream_t stream) {
   Shape s;
@@ -332,14 +345,16 @@ flowmoe_status_t flowmoe_expert_ffn(const flowmoe_shape_t* shape, const void* x_
   REQUIRE_T(w1, "w1");
   REQUIRE_T(w2, "w2");
   if (s.act == FLOWMOE_SWIGLU) REQUIRE_T(w3, "w3");
+  st = check_biases(s, b1, b3, b2, "");
+  if (st != FLOWMOE_OK) return st;
   if (s.rows > 0) {
     REQUIRE_T(x_disp, "x_disp");
     REQUIRE_T(h_save, "h_save");
     REQUIRE_T(a_save, "a_save");
     REQUIRE_T(y_disp, "y_disp");
   }
-  return hip_status(launch_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save,
-                                      y_disp, stream),
+  return hip_status(launch_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, b1, b3, b2, h_save,
+                                      a_save, y_disp, stream),
                     "flowmoe_expert_ffn");
 }
 
@@ -387,8 +402,9 @@ flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void
                                         const void* a_save, const int32_t* counts,
                                         const int32_t* offsets, const void* w1,
                                         const void* w3, const void* w2, void* dx_disp,
-                                        float* dw1, float* dw3, float* dw2, int32_t accumulate,
-                                        void* ws, size_t ws_bytes, hipStream_t stream) {
+                                        float* dw1, float* dw3, float* dw2, float* db1,
+                                        float* db3, float* db2, int32_t accumulate, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
   Shape s;
   flowmoe_status_t st = check_shape(shape, NEED_H | NEED_C, &s);
   if (st != FLOWMOE_OK) return st;
@@ -409,11 +425,13 @@ flowmoe_status_t flowmoe_expert_ffn_bwd(const flowmoe_shape_t* shape, const void
     REQUIRE_T(a_save, "a_save");
     REQUIRE_T(dx_disp, "dx_disp");
   }
+  st = check_biases(s, db1, db3, db2, "d");
+  if (st != FLOWMOE_OK) return st;
   st = check_ws(ws, ws_bytes, ffn_bwd_ws_bytes(s), "flowmoe_expert_ffn_bwd");
   if (st != FLOWMOE_OK) return st;
   return hip_status(launch_expert_ffn_bwd(s, dy_disp, x_disp, h_save, a_save, counts, offsets, w1,
-                                          w3, w2, dx_disp, dw1, dw3, dw2, accumulate != 0, ws,
-                                          stream),
+                                          w3, w2, dx_disp, dw1, dw3, dw2, db1, db3, db2,
+                                          accumulate != 0, ws, stream),
                     "flowmoe_expert_ffn_bwd");
 }
 
@@ -623,6 +641,8 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
   REQUIRE(b->counts, "bufs->counts");
   REQUIRE(b->offsets, "bufs->offsets");
   if (s.act == FLOWMOE_SWIGLU) REQUIRE_T(b->w3, "bufs->w3");
+  st = check_biases(s, b->b1, b->b3, b->b2, "bufs->");
+  if (st != FLOWMOE_OK) return st;
   if (b->ws != nullptr) {  // optional here: the dispatch scan's tile histograms
     st = check_ws(b->ws, b->ws_bytes, dispatch_ws_bytes(s), "flowmoe_layer_fwd");
     if (st != FLOWMOE_OK) return st;
@@ -670,8 +690,8 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
     Chunk c = chunk_of(s, b, r);
     sc.wait(s_compute, evD[r]);
     sc.mark(2, r, 0, s_compute);
-    sc.run(launch_expert_ffn(s, c.x_disp, c.counts, c.offsets, b->w1, b->w3, b->w2, c.h_save,
-                             c.a_save, c.y_disp, s_compute));
+    sc.run(launch_expert_ffn(s, c.x_disp, c.counts, c.offsets, b->w1, b->w3, b->w2, b->b1, b->b3,
+                             b->b2, c.h_save, c.a_save, c.y_disp, s_compute));
     sc.mark(2, r, 1, s_compute);
     sc.signal(evF[r], s_compute);
   }
@@ -706,6 +726,8 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     REQUIRE_T(b->w3, "bufs->w3");
     REQUIRE(b->dw3, "bufs->dw3");
   }
+  st = check_biases(s, b->db1, b->db3, b->db2, "bufs->d");
+  if (st != FLOWMOE_OK) return st;
   if (s.T > 0) {
     REQUIRE_T(b->x, "bufs->x"); REQUIRE_T(b->dy, "bufs->dy"); REQUIRE(b->topk_idx, "bufs->topk_idx");
     REQUIRE(b->topk_w, "bufs->topk_w"); REQUIRE(b->slot, "bufs->slot");
@@ -786,7 +808,8 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
   }
   sc.mark(4, 0, 0, s_compute);  // (the trace's last pair: the weight gradients)
   sc.run(launch_expert_ffn_wgrad(s, R, b->dy_disp, b->x_disp, b->a_save, b->h_save, b->counts,
-                                 b->offsets, b->dw1, b->dw3, b->dw2, 0, s_compute));
+                                 b->offsets, b->dw1, b->dw3, b->dw2, b->db1, b->db3, b->db2, 0,
+                                 s_compute));
   sc.mark(4, 0, 1, s_compute);
   // D_R..D_1 (dispatch backward, plus the gate's dx term) on the comm stream
   for (int r = R - 1; r >= 0; --r) {

@@ -238,10 +238,11 @@ hipError_t launch_gate_dw_gemm(const void* x, int T, int M, const void* d, int N
 hipError_t launch_gate_dx_gemm(const void* dlhl, int T, int K, const void* wstack, int M,
                                const int32_t* counts, const int32_t* offsets, int S, void* dx,
                                bool add, hipStream_t st);
+// b1, b3 (E x H), b2 (E x M): float biases of the experts, each nullable
 hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* counts,
                              const int32_t* offsets, const void* w1, const void* w3,
-                             const void* w2, void* h_save, void* a_save, void* y_disp,
-                             hipStream_t st);
+                             const void* w2, const float* b1, const float* b3, const float* b2,
+                             void* h_save, void* a_save, void* y_disp, hipStream_t st);
 // input side of the expert backward of one chunk: dH (into dh, which may be
 // h_save itself: each element's pre-activation is read before its gradient
 // is written) and dX
@@ -250,16 +251,22 @@ hipError_t launch_expert_ffn_dgrad(const Shape& s, const void* dy_disp, const vo
                                    const void* w3, const void* w2, void* dh, void* dx_disp,
                                    hipStream_t st);
 // weight gradients summed over R chunks (chunk r's rows at r * rows of each
-// row buffer, its counts and offsets at r * E and r * (E + 1)), one GEMM each
+// row buffer, its counts and offsets at r * E and r * (E + 1)), one GEMM each,
+// and the bias gradients (db1, db3, db2 nullable) as column sums of dH / dY
 hipError_t launch_expert_ffn_wgrad(const Shape& s, int R, const void* dy_disp, const void* x_disp,
                                    const void* a_save, const void* dh, const int32_t* counts,
                                    const int32_t* offsets, float* dw1, float* dw3, float* dw2,
-                                   int accumulate, hipStream_t st);
+                                   float* db1, float* db3, float* db2, int accumulate,
+                                   hipStream_t st);
+hipError_t launch_expert_bias_grad(const Shape& s, int R, const void* dy_disp, const void* dh,
+                                   const int32_t* counts, const int32_t* offsets, float* db1,
+                                   float* db3, float* db2, int accumulate, hipStream_t st);
 hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void* x_disp,
                                  const void* h_save, const void* a_save, const int32_t* counts,
                                  const int32_t* offsets, const void* w1, const void* w3,
                                  const void* w2, void* dx_disp, float* dw1, float* dw3,
-                                 float* dw2, int accumulate, void* ws, hipStream_t st);
+                                 float* dw2, float* db1, float* db3, float* db2, int accumulate,
+                                 void* ws, hipStream_t st);
 
 // Kernel tracing (flowmoe_trace_start): record a begin/end event around a
 // launch when the kind is selected. Defined in abi.hip.

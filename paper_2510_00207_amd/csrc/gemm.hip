@@ -75,7 +75,21 @@ struct GemmParams {
   // rows of each row buffer (of each segment's): an expert's range
   // [offsets[e], offsets[e] + rows) is cut at it
   long rows_cap;
+  // forward epilogues: per-expert float biases added to the data rows' outputs
+  // (bias0 to C0's columns: b1 for h / h1, b2 for y; bias1: b3 for the dual
+  // forward's h3), bias0[e * bias_estride + column]; null: none
+  const float* bias0;
+  const float* bias1;
+  long bias_estride;
 };
+
+// v[q] += b[q] for 8 consecutive float biases
+__device__ __forceinline__ void add_bias8(float v[8], const float* b) {
+  const float4 lo = *reinterpret_cast<const float4*>(b);
+  const float4 hi = *reinterpret_cast<const float4*>(b + 4);
+  v[0] += lo.x; v[1] += lo.y; v[2] += lo.z; v[3] += lo.w;
+  v[4] += hi.x; v[5] += hi.y; v[6] += hi.z; v[7] += hi.w;
+}
 
 // counts and offsets are device data: a range that inconsistent ones would
 // take past the row buffers is cut there, not followed
@@ -339,6 +353,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
           float h1[8], h3[8], a[8];
           read8(rr, (jp * 64 + cin) >> 3, h1);
           read8(rr, (jp * 64 + 32 + cin) >> 3, h3);
+          if (data && p.bias0 != nullptr) add_bias8(h1, p.bias0 + (long)e * p.bias_estride + n);
+          if (data && p.bias1 != nullptr) add_bias8(h3, p.bias1 + (long)e * p.bias_estride + n);
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
             if (!data) h1[q] = h3[q] = 0.f;
@@ -412,6 +428,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
           if (!data) {
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[q] = 0.f;
+          }
+          if constexpr (EPI == EPI_STORE || EPI == EPI_GELU_FWD) {
+            if (data && p.bias0 != nullptr) add_bias8(v, p.bias0 + (long)e * p.bias_estride + n);
           }
           const long g = row0 + ti;
           if constexpr (EPI == EPI_STORE) {
@@ -1220,7 +1239,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
       if constexpr (MODE == MODE_ROWS) {
         const int li = mt * TB + ti;
         if (li >= rows_e) continue;
-        const float v = (li < cnt_e) ? acc[i][j] : 0.f;
+        float v = (li < cnt_e) ? acc[i][j] : 0.f;
+        if constexpr (EPI == EPI_STORE || EPI == EPI_GELU_FWD) {
+          if (li < cnt_e && p.bias0 != nullptr) v += p.bias0[(long)e * p.bias_estride + n];
+        }
         const long g = row0 + ti;
         if constexpr (EPI == EPI_STORE) {
           C0[g * p.ldc + p.coloff + n] = v;
@@ -1257,6 +1279,72 @@ __global__ void swiglu_act_f32_kernel(const float* __restrict__ h, float* __rest
     const int c = (int)(q % H);
     const float h1 = h[r * 2 * H + c], h3 = h[r * 2 * H + H + c];
     a[q] = h1 * sigmoid_f(h1) * h3;
+  }
+}
+
+// Bias gradients of the experts: per-expert column sums,
+// out[e][c] (+)= sum over expert e's rows r of src[r][c], over nseg row
+// segments (the chunks of a layer call: segment g's rows of expert e are
+// counts[g * E + e] rows from offsets[g * (E + 1) + e] of src + g * seg_stride)
+// in segment order; columns at or past nsplit go to out1[e][c - nsplit]
+// (SwiGLU's dH3 half), a null output is skipped. Block (512-column block,
+// expert): 64 lanes of 8 columns, wave w summing the rows w, w + 4, ... of
+// each segment in order (four rows in flight per lane), then the four
+// waves' sums added in wave order: deterministic.
+template <typename TE>
+__global__ __launch_bounds__(256) void bias_grad_kernel(
+    const TE* __restrict__ src, long ld, long seg_stride, const int32_t* __restrict__ counts,
+    const int32_t* __restrict__ offsets, int E, int nseg, long rows_cap, int ncols, int nsplit,
+    float* __restrict__ out0, float* __restrict__ out1, int accumulate) {
+  __shared__ float part[4][512];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int e = blockIdx.y;
+  const int c0 = blockIdx.x * 512 + lane * 8;  // ncols is a multiple of 8
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  auto add = [&](const auto& raw) {
+    float v[8];
+    raw8_f32(raw, v);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] += v[q];
+  };
+  if (c0 < ncols) {
+    for (int g = 0; g < nseg; ++g) {
+      const long off = offsets[g * (E + 1) + e];
+      const int n = clip_rows(off, counts[g * E + e], rows_cap);
+      const TE* base = src + g * seg_stride + off * ld + c0;
+      int r = w;
+      for (; r + 12 < n; r += 16) {
+        const auto a0 = raw8_load(base + (long)r * ld);
+        const auto a1 = raw8_load(base + (long)(r + 4) * ld);
+        const auto a2 = raw8_load(base + (long)(r + 8) * ld);
+        const auto a3 = raw8_load(base + (long)(r + 12) * ld);
+        add(a0);
+        add(a1);
+        add(a2);
+        add(a3);
+      }
+      for (; r < n; r += 4) add(raw8_load(base + (long)r * ld));
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) part[w][lane * 8 + q] = acc[q];
+  __syncthreads();
+  if (w == 0 && c0 < ncols) {
+    float* dst = c0 < nsplit ? out0 : out1;
+    if (dst == nullptr) return;
+    dst += c0 < nsplit ? (long)e * nsplit + c0 : (long)e * (ncols - nsplit) + (c0 - nsplit);
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      v[q] = ((part[0][lane * 8 + q] + part[1][lane * 8 + q]) + part[2][lane * 8 + q]) +
+             part[3][lane * 8 + q];
+    if (accumulate) {
+      float o[8];
+      load8(dst, o);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += o[q];
+    }
+    store8(dst, v);
   }
 }
 
@@ -1446,8 +1534,8 @@ size_t ffn_bwd_ws_bytes(const Shape& s) {
 
 hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* counts,
                              const int32_t* offsets, const void* w1, const void* w3,
-                             const void* w2, void* h_save, void* a_save, void* y_disp,
-                             hipStream_t st) {
+                             const void* w2, const float* b1, const float* b3, const float* b2,
+                             void* h_save, void* a_save, void* y_disp, hipStream_t st) {
   if (s.rows == 0) return hipSuccess;
   const bool swiglu = s.act == FLOWMOE_SWIGLU;
   const int H = s.H, M = s.M;
@@ -1465,6 +1553,9 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
   p.C1 = a_save;
   p.ldc = swiglu ? 2L * H : H;
   p.ldc1 = H;
+  p.bias0 = b1;
+  p.bias1 = swiglu ? b3 : nullptr;
+  p.bias_estride = H;
   if (s.dtype == FLOWMOE_BF16) {
     if (swiglu)
       FLOWMOE_TRY((run_gemm_bf16<MODE_ROWS, true, false, EPI_SWIGLU_FWD>(FLOWMOE_K_FFN1, s, p, st)));
@@ -1476,6 +1567,7 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
       FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN1, s, p, st)));
       p.B0 = w3;
       p.coloff = H;
+      p.bias0 = b3;
       FLOWMOE_TRY((run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN1, s, p, st)));
       FLOWMOE_TRY(traced(FLOWMOE_K_SWIGLU_ACT, st, [&] {
         hipLaunchKernelGGL(swiglu_act_f32_kernel, dim3(1024), dim3(256), 0, st,
@@ -1497,6 +1589,8 @@ hipError_t launch_expert_ffn(const Shape& s, const void* x_disp, const int32_t* 
   q.b_estride = (long)H * M;
   q.C0 = y_disp;
   q.ldc = M;
+  q.bias0 = b2;
+  q.bias_estride = M;
   if (s.dtype == FLOWMOE_BF16)
     return run_gemm_bf16<MODE_ROWS, true, false, EPI_STORE>(FLOWMOE_K_FFN2, s, q, st);
   return run_f32<MODE_ROWS, false, EPI_STORE>(FLOWMOE_K_FFN2, s, q, st);
@@ -1561,10 +1655,36 @@ hipError_t launch_expert_ffn_dgrad(const Shape& s, const void* dy_disp, const vo
   return hipSuccess;
 }
 
+hipError_t launch_expert_bias_grad(const Shape& s, int R, const void* dy_disp, const void* dh,
+                                   const int32_t* counts, const int32_t* offsets, float* db1,
+                                   float* db3, float* db2, int accumulate, hipStream_t st) {
+  const bool swiglu = s.act == FLOWMOE_SWIGLU;
+  const int H = s.H, M = s.M, HW = swiglu ? 2 * H : H;
+  const long rows = s.rows;
+  auto run = [&](const void* src, int ld, int ncols, int nsplit, float* o0, float* o1) {
+    return traced(FLOWMOE_K_BIAS_GRAD, st, [&] {
+      const dim3 grid((unsigned)((ncols + 511) / 512), (unsigned)s.E);
+      if (s.dtype == FLOWMOE_BF16)
+        hipLaunchKernelGGL(bias_grad_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)src,
+                           (long)ld, rows * ld, counts, offsets, s.E, R, rows, ncols, nsplit, o0, o1,
+                           accumulate);
+      else
+        hipLaunchKernelGGL(bias_grad_kernel<float>, grid, dim3(256), 0, st, (const float*)src,
+                           (long)ld, rows * ld, counts, offsets, s.E, R, rows, ncols, nsplit, o0, o1,
+                           accumulate);
+    });
+  };
+  if (db2 != nullptr) FLOWMOE_TRY(run(dy_disp, M, M, M, db2, nullptr));
+  if (db1 != nullptr || (swiglu && db3 != nullptr))
+    FLOWMOE_TRY(run(dh, HW, HW, H, db1, swiglu ? db3 : nullptr));
+  return hipSuccess;
+}
+
 hipError_t launch_expert_ffn_wgrad(const Shape& s, int R, const void* dy_disp, const void* x_disp,
                                    const void* a_save, const void* dh, const int32_t* counts,
                                    const int32_t* offsets, float* dw1, float* dw3, float* dw2,
-                                   int accumulate, hipStream_t st) {
+                                   float* db1, float* db3, float* db2, int accumulate,
+                                   hipStream_t st) {
   const bool swiglu = s.act == FLOWMOE_SWIGLU;
   const bool bf = s.dtype == FLOWMOE_BF16;
   const int H = s.H, M = s.M;
@@ -1614,19 +1734,22 @@ hipError_t launch_expert_ffn_wgrad(const Shape& s, int R, const void* dy_disp, c
     else
       FLOWMOE_TRY((run_f32<MODE_KSUM, false, EPI_WGRAD>(FLOWMOE_K_WGRAD1, s, p, st)));
   }
-  return hipSuccess;
+  // 3. the biases' gradients: column sums of dY and dH over each expert's rows
+  return launch_expert_bias_grad(s, R, dy_disp, dh, counts, offsets, db1, db3, db2, accumulate,
+                                 st);
 }
 
 hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void* x_disp,
                                  const void* h_save, const void* a_save, const int32_t* counts,
                                  const int32_t* offsets, const void* w1, const void* w3,
                                  const void* w2, void* dx_disp, float* dw1, float* dw3,
-                                 float* dw2, int accumulate, void* ws, hipStream_t st) {
+                                 float* dw2, float* db1, float* db3, float* db2, int accumulate,
+                                 void* ws, hipStream_t st) {
   // dH in the workspace (h_save is left as it is)
   FLOWMOE_TRY(launch_expert_ffn_dgrad(s, dy_disp, h_save, counts, offsets, w1, w3, w2, ws, dx_disp,
                                       st));
   return launch_expert_ffn_wgrad(s, 1, dy_disp, x_disp, a_save, ws, counts, offsets, dw1, dw3, dw2,
-                                 accumulate, st);
+                                 db1, db3, db2, accumulate, st);
 }
 
 }  // namespace flowmoe

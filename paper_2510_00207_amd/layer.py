@@ -16,15 +16,16 @@ _TORCH_DTYPE = {L.F32: torch.float32, L.BF16: torch.bfloat16}
 class MoELayer:
     """Buffers of a layer with T_total = R * T tokens.
 
-    Parameters and inputs (w_gate, bias, w1, w3, w2, x, dy) are attributes the
-    caller fills (or replaces with tensors of the same shape and dtype);
-    everything else is allocated here.
+    Parameters and inputs (w_gate, bias, w1, w3, w2, the experts' biases b1,
+    b3, b2 when expert_bias, x, dy) are attributes the caller fills (or
+    replaces with tensors of the same shape and dtype); everything else is
+    allocated here.
     """
 
     def __init__(self, *, T_total: int, M: int, H: int, E: int, k: int, R: int = 1,
                  f: float | None = None, C: int | None = None, act: str = "gelu",
                  dtype: str = "bf16", layout: str = "packed", bias: bool = False,
-                 gate: str = "renorm", device="cuda"):
+                 gate: str = "renorm", expert_bias: bool = False, device="cuda"):
         if T_total % R:
             raise ValueError("T_total must be a multiple of R")
         T = T_total // R
@@ -56,6 +57,10 @@ class MoELayer:
         self.w1 = z(E, M, H)
         self.w3 = z(E, M, H) if act == "swiglu" else None
         self.w2 = z(E, H, M)
+        sw = act == "swiglu"
+        self.b1 = z(E, H, dtype=f32) if expert_bias else None
+        self.b3 = z(E, H, dtype=f32) if expert_bias and sw else None
+        self.b2 = z(E, M, dtype=f32) if expert_bias else None
         # forward
         self.x = z(T_total, M)
         self.logits = z(T_total, E, dtype=f32)
@@ -83,6 +88,9 @@ class MoELayer:
         self.dw1 = z(E, M, H, dtype=f32)
         self.dw3 = z(E, M, H, dtype=f32) if act == "swiglu" else None
         self.dw2 = z(E, H, M, dtype=f32)
+        self.db1 = z(E, H, dtype=f32) if expert_bias else None
+        self.db3 = z(E, H, dtype=f32) if expert_bias and sw else None
+        self.db2 = z(E, M, dtype=f32) if expert_bias else None
         self.ws_bytes = L.flowmoe_workspace_bytes(self.shape, L.WS_LAYER_BWD)
         self.ws = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
 

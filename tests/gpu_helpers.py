@@ -83,10 +83,14 @@ def load_layer(layer, inp):
     layer.w2.copy_(to_torch(inp["w2"], d))
     if inp.get("dy") is not None:
         layer.dy.copy_(to_torch(inp["dy"], d))
+    for name in ("b1", "b3", "b2"):  # the experts' biases (fp32)
+        if inp.get(name) is not None:
+            getattr(layer, name).copy_(torch.from_numpy(inp[name]).to(d))
 
 
 def f64_inputs(inp):
-    return {k: (None if v is None else (v.astype(np.float64) if k == "bias" else as_f64(v)))
+    return {k: (None if v is None else (v.astype(np.float64) if v.dtype == np.float32 and
+                                        k in ("bias", "b1", "b3", "b2") else as_f64(v)))
             for k, v in inp.items()}
 
 

@@ -305,16 +305,19 @@ def gemm_tiles():
     L.flowmoe_set_gemm_tiles("auto")
 
 
+@pytest.mark.parametrize("biased", [False, True], ids=["nobias", "bias"])
 @pytest.mark.parametrize("MHT", [(200, 264, "auto"), (224, 288, "wide"), (224, 288, "narrow")],
                          ids=["staged", "streaming-wide", "streaming-narrow"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
-def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, gemm_tiles):
+def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, biased, gemm_tiles):
     """(200, 264): reductions not multiples of 32 (register-staged bf16 GEMM);
     (224, 288): multiples of 32 (LDS-streaming bf16 GEMM, 256 x 256 and
     256 x 128 tiles); all ragged. The counts give row tiles of every class:
-    empty, a few rows, under and over half a tile, full."""
+    empty, a few rows, under and over half a tile, full. Biased experts: b1
+    (b3) and b2 on the data rows only, and their gradients as per-expert
+    column sums."""
     need_gpu()
     rng = np.random.default_rng(3)
     E, k = 6, 1
@@ -326,9 +329,13 @@ def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, gemm_tiles):
     T = int(cnt.sum())
     idx = np.repeat(np.arange(E), cnt)[:, None]
     rt = oracle.route(idx, E, C, layout)
-    cfg = get_config("balanced", T=T, M=M, H=H, E=E, k=1, dtype=dtype, act=act, seed=11)
+    cfg = get_config("balanced", T=T, M=M, H=H, E=E, k=1, dtype=dtype, act=act, seed=11,
+                     expert_bias=biased)
     inp = make_inputs(cfg)
     d = dev()
+    bt = {kk: (None if inp[kk] is None else torch.from_numpy(inp[kk]).to(d))
+          for kk in ("b1", "b3", "b2")}
+    b64 = {kk: (None if inp[kk] is None else inp[kk].astype(np.float64)) for kk in ("b1", "b3", "b2")}
     xb = as_f64(inp["x"])
     x_disp64 = oracle.dispatch(xb, rt["row_src"], 1)
     rows = rt["rows"]
@@ -345,9 +352,10 @@ def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, gemm_tiles):
     y_disp = torch.full((rows, M), 5.0, dtype=td, device=d)
     s = _shape(T, M, H, E, 1, C, dtype, act, layout)
     assert L.flowmoe_rows_capacity(s) == rows
-    L.flowmoe_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save, y_disp)
+    L.flowmoe_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save, y_disp, **bt)
     w64 = {kk: (None if inp[kk] is None else as_f64(inp[kk])) for kk in ("w1", "w3", "w2")}
-    ref = oracle.expert_ffn(x_disp64, rt["counts"], rt["offsets"], w64["w1"], w64["w3"], w64["w2"], act)
+    ref = oracle.expert_ffn(x_disp64, rt["counts"], rt["offsets"], w64["w1"], w64["w3"], w64["w2"], act,
+                            **b64)
     # backward with a seeded upstream gradient on the live rows
     dy64 = rng.standard_normal((rows, M))
     live = np.zeros(rows, bool)
@@ -360,15 +368,27 @@ def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, gemm_tiles):
     dw1 = torch.full((E, M, H), 9.0, device=d)
     dw3 = torch.full((E, M, H), 9.0, device=d) if act == "swiglu" else None
     dw2 = torch.full((E, H, M), 9.0, device=d)
+    db = {"db1": torch.full((E, H), 9.0, device=d), "db2": torch.full((E, M), 9.0, device=d),
+          "db3": torch.full((E, H), 9.0, device=d) if act == "swiglu" else None}
+    if not biased:  # the bias gradients are optional outputs
+        db = {kk: None for kk in db}
     nws = L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD)
     ws = torch.empty(nws, dtype=torch.uint8, device=d)
     L.flowmoe_expert_ffn_bwd(s, dy_t, x_disp, h_save, a_save, counts, offsets, w1, w3, w2, dx_disp,
-                             dw1, dw3, dw2, 0, ws, nws)
+                             dw1, dw3, dw2, 0, ws, nws, **db)
     # accumulate = 1 adds a second identical gradient
     dw2b = dw2.clone()
+    db2b = None if db["db2"] is None else db["db2"].clone()
     torch.cuda.synchronize()
-    rdx, rdw1, rdw3, rdw2 = oracle.expert_ffn_bwd(dy64, x_disp64, ref, rt["counts"], rt["offsets"],
-                                                  w64["w1"], w64["w3"], w64["w2"], act)
+    rdx, rdw1, rdw3, rdw2, rdh = oracle.expert_ffn_bwd(dy64, x_disp64, ref, rt["counts"],
+                                                       rt["offsets"], w64["w1"], w64["w3"],
+                                                       w64["w2"], act, return_dh=True)
+    if biased:
+        rdb1, rdb3, rdb2 = oracle.expert_bias_grads(dy64, rdh, rt["counts"], rt["offsets"], act)
+        assert_close(host(db["db1"]), rdb1, dtype, "db1")
+        assert_close(host(db["db2"]), rdb2, dtype, "db2")
+        if act == "swiglu":
+            assert_close(host(db["db3"]), rdb3, dtype, "db3")
     nl = rows if layout == "padded" else int(rt["offsets"][-1])
     hw = ref["h1"] if act == "gelu" else np.concatenate([ref["h1"], ref["h3"]], axis=1)
     assert_close(host(h_save)[:nl], hw[:nl], dtype, "h_save")
@@ -382,9 +402,11 @@ def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, gemm_tiles):
     if act == "swiglu":
         assert_close(host(dw3), rdw3, dtype, "dw3")
     L.flowmoe_expert_ffn_bwd(s, dy_t, x_disp, h_save, a_save, counts, offsets, w1, w3, w2, dx_disp,
-                             dw1, dw3, dw2, 1, ws, nws)
+                             dw1, dw3, dw2, 1, ws, nws, **db)
     torch.cuda.synchronize()
     assert torch.equal(dw2, 2 * dw2b)
+    if biased:
+        assert torch.equal(db["db2"], 2 * db2b)
 
 
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])

@@ -33,7 +33,7 @@ def run_layer(cfg, layout, R=None, two_streams=True, inp=None):
     inp = make_inputs(cfg) if inp is None else inp
     layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
                      dtype=cfg.dtype, layout=layout, bias=cfg.zipf_bias, gate=cfg.gate,
-                     device=dev())
+                     expert_bias=cfg.expert_bias, device=dev())
     load_layer(layer, inp)
     sc = torch.cuda.current_stream()
     sm = torch.cuda.Stream() if two_streams else sc
@@ -88,6 +88,11 @@ def check_against_oracle(cfg, layout, layer, inp, R):
     assert_close(host(layer.dw2), ref["dw2"], dt, "dw2")
     if cfg.act == "swiglu":
         assert_close(host(layer.dw3), ref["dw3"], dt, "dw3")
+    if cfg.expert_bias:
+        assert_close(host(layer.db1), ref["db1"], dt, "db1")
+        assert_close(host(layer.db2), ref["db2"], dt, "db2")
+        if cfg.act == "swiglu":
+            assert_close(host(layer.db3), ref["db3"], dt, "db3")
     return ref
 
 
@@ -140,6 +145,28 @@ def test_layer_full_softmax_gate(name, R, layout):
     live = np.any(host(layer.d_topk_w) != 0.0, axis=1)
     assert live.any() and host(layer.dw_gate).any()
     assert np.all(host(layer.d_logits)[live] != 0.0)
+
+
+@pytest.mark.parametrize("name,R", [("tiny", 1), ("tiny", 2), ("balanced_s", 1), ("skewed_s", 1),
+                                    ("large_s", 2), ("fine_s", 4)])
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+def test_layer_biased_experts(name, R, layout):
+    """Biased two-layer experts (b1, b3 on the first layer, b2 on the second)
+    in the chunked layer: every output and gradient against the oracle, the
+    bias gradients summed over the chunks; rows past an expert's count in
+    the padded layout stay zero."""
+    need_gpu()
+    cfg = CASES[name].replace(expert_bias=True)
+    print(f"[layer] biased experts {name} {layout} R={R}", flush=True)
+    layer, inp = run_layer(cfg, layout, R=R)
+    ref = check_against_oracle(cfg, layout, layer, inp, R)
+    if layout == "padded":
+        for r, c in enumerate(ref["chunks"]):
+            live = np.zeros(c["rows"], bool)
+            for e in range(cfg.E):
+                live[c["offsets"][e]:c["offsets"][e] + c["counts"][e]] = True
+            assert not host(layer.y_disp[r])[~live].any(), f"y_disp padding of chunk {r}"
+            assert not host(layer.a_save[r])[~live].any(), f"a_save padding of chunk {r}"
 
 
 def test_two_streams_equal_one_stream_and_deterministic():
