@@ -45,6 +45,8 @@ def parse():
                     help="gate weights: softmax over the k selected (renorm) or the selected "
                          "experts' full-softmax probabilities (full, Switch-style)")
     ap.add_argument("--R", type=int, default=None, help="override the chunk count")
+    ap.add_argument("--expert-bias", action="store_true",
+                    help="biased experts (b1, b3 on the first layer, b2 on the second)")
     for dim, typ in (("T", int), ("M", int), ("H", int), ("E", int), ("k", int), ("f", float)):
         ap.add_argument(f"--{dim}", type=typ, default=None, help=f"override the workload's {dim}")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
@@ -88,6 +90,48 @@ def oracle_sample_tokens(cfg, R: int) -> int:
     while t > R and t * per_token > 6e11:
         t //= 2
     return max(R, (t // R) * R)
+
+
+def schedule_overlap(layer, R, sc, sm, torch):
+    """One untraced-throughput step with the layer's task events (the trace
+    of flowmoe_layer_fwd / flowmoe_layer_bwd: start and end of every task of
+    every chunk, on the stream it runs on): each pass's span, the time each
+    stream spends in its tasks, and the time both streams run a task at once
+    (the overlap the two-stream schedule of Eqs. 3-6 achieves on one GPU).
+    Forward: compute stream = gating, experts; comm stream = dispatch,
+    combine. Backward: compute stream = experts bwd and the weight
+    gradients; comm stream = combine bwd, gate gradients, dispatch bwd."""
+    def events(n):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in ev:  # (torch creates an event's handle at its first record)
+            e.record(sc)
+        return ev
+
+    fwd, bwd, (t0,) = events(8 * R), events(8 * R + 2), events(1)
+    torch.cuda.synchronize()
+    t0.record(sc)
+    layer.forward(sc, sm, trace=fwd)
+    layer.backward(sc, sm, trace=bwd)
+    torch.cuda.synchronize()
+    out = {}
+    for label, ev, comp in (("fwd", fwd, (0, 2)), ("bwd", bwd, (1, 4))):
+        spans = {}
+        for task in range(5 if label == "bwd" else 4):
+            for r in range(1 if task == 4 else R):
+                i = 2 * (task * R + r)
+                spans[(task, r)] = (t0.elapsed_time(ev[i]), t0.elapsed_time(ev[i + 1]))
+        c = [v for (task, _), v in spans.items() if task in comp]
+        m = [v for (task, _), v in spans.items() if task not in comp]
+        # the tasks of one stream never overlap each other (stream order)
+        both = sum(max(0.0, min(a1, b1) - max(a0, b0)) for a0, a1 in c for b0, b1 in m)
+        lo = min(a for a, _ in spans.values())
+        hi = max(b for _, b in spans.values())
+        busy_c = sum(b - a for a, b in c)
+        busy_m = sum(b - a for a, b in m)
+        out[label] = {"span_ms": round(hi - lo, 4), "compute_stream_ms": round(busy_c, 4),
+                      "comm_stream_ms": round(busy_m, 4), "overlap_ms": round(both, 4),
+                      "overlap_frac_of_comm": round(both / busy_m, 4) if busy_m > 0 else None}
+    return out
 
 
 def widen_f64(a):
@@ -214,17 +258,20 @@ def main():
     dev = torch.device("cuda:0")
 
     over = {d: getattr(a, d) for d in ("T", "M", "H", "E", "k", "f") if getattr(a, d) is not None}
-    cfg = get_config(a.workload, gate=a.gate, **over)
+    cfg = get_config(a.workload, gate=a.gate, expert_bias=a.expert_bias, **over)
     if over:  # another shape: named apart (no counter summary of the workload applies to it)
         cfg = cfg.replace(name=cfg.name + "(" + " ".join(f"{d}={v}" for d, v in over.items()) + ")")
     R = cfg.R if a.R is None else a.R
     inp = make_inputs(cfg)
     layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
                      dtype=cfg.dtype, layout=a.layout, bias=cfg.zipf_bias, gate=cfg.gate,
-                     device=dev)
+                     expert_bias=cfg.expert_bias, device=dev)
     for name in ("x", "w_gate", "w1", "w3", "w2", "dy"):
         if inp[name] is not None:
             getattr(layer, name).copy_(to_torch(inp[name], dev))
+    for name in ("b1", "b3", "b2"):  # the experts' biases (fp32)
+        if inp.get(name) is not None:
+            getattr(layer, name).copy_(torch.from_numpy(inp[name]).to(dev))
     if cfg.zipf_bias:
         layer.bias.copy_(torch.from_numpy(inp["bias"]).to(dev))
     bufs = layer.bufs()
@@ -290,6 +337,7 @@ def main():
         per_kernel.setdefault(nm, []).append(all_ev.elapsed_ms(i) * 1e3)
     all_ev.close()
     breakdown = {k: round(float(sum(v)), 2) for k, v in per_kernel.items()}  # us per step
+    sched = schedule_overlap(layer, R, sc, sm, torch)
 
     ms_per_step = elapsed / a.steps * 1e3
     tokens_per_s = cfg.T * a.steps / elapsed
@@ -404,9 +452,11 @@ def main():
             "workload": (f"{cfg.name} MoE layer: T={cfg.T} M={cfg.M} H={cfg.H} E={cfg.E} "
                          f"top-{cfg.k} f={cfg.f} {cfg.act} {cfg.dtype}, R={R}, {a.layout}, "
                          f"{streams}"
-                         f"{', full-softmax gate' if cfg.gate == 'full' else ''}"),
+                         f"{', full-softmax gate' if cfg.gate == 'full' else ''}"
+                         f"{', biased experts' if cfg.expert_bias else ''}"),
             "T": cfg.T, "M": cfg.M, "H": cfg.H, "E": cfg.E, "k": cfg.k, "f": cfg.f,
             "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "gate": cfg.gate, "tiles": a.tiles,
+            "expert_bias": cfg.expert_bias,
             "kept_rows": kept,
         },
         "roofline": {
@@ -431,6 +481,7 @@ def main():
         "step_ms_iqr": [round(q(25), 4), round(q(75), 4)],
         "memory_bound": mem,
         "kernel_us_per_step": breakdown,
+        "schedule": sched,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

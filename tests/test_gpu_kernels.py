@@ -504,6 +504,45 @@ def test_gate_bwd_shapes(T, M, E, k):
     assert_close(host(db), g["dbias"], "f32", "dbias")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("T,M,E,k", [(9000, 1000, 3, 2), (8200, 1032, 16, 4), (16400, 520, 12, 3),
+                                     (4100, 4104, 8, 2), (70000, 136, 5, 5)])
+def test_gate_bwd_long_inputs(T, M, E, k, dtype):
+    """The renormalised gate's backward for E <= 16 over more than 8 M
+    elements of x (bf16: dW_g on the GEMM path over token splits; fp32: the
+    register tiles), ragged column tiles and token splits; with the dx term
+    and accumulation."""
+    need_gpu()
+    rng = np.random.default_rng(T + M + E + k)
+    d = dev()
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x64 = host(torch.from_numpy(rng.standard_normal((T, M))).to(d).to(td))
+    wg64 = host(torch.from_numpy(rng.standard_normal((M, E)) * 0.05).to(d).to(td))
+    idx, w = oracle.topk_select(rng.standard_normal((T, E)), k)
+    dtw64 = rng.standard_normal((T, k))
+    t = lambda a, dt=td: torch.from_numpy(np.ascontiguousarray(a)).to(d).to(dt)
+    s = _shape(T, M, 8, E, k, 0, dtype)
+    dlog = torch.full((T, E), 7.0, device=d)
+    dwg = torch.full((M, E), 3.0, device=d)
+    db = torch.full((E,), 3.0, device=d)
+    dx0 = t(rng.standard_normal((T, M)))
+    dx = dx0.clone()
+    nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
+    ws = torch.empty(nws, dtype=torch.uint8, device=d)
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), None, t(idx, torch.int32), t(w, torch.float32),
+                            t(dtw64, torch.float32), dlog, dwg, db, dx, 0, ws, nws)
+    torch.cuda.synchronize()
+    g = oracle.gate_bwd(x64, wg64, idx, host(t(w, torch.float32)), host(t(dtw64, torch.float32)))
+    assert_close(host(dlog), g["d_logits"], "f32", "d_logits")
+    assert_close(host(dwg), g["dw_gate"], "f32", "dw_gate")
+    assert_close(host(db), g["dbias"], "f32", "dbias")
+    assert_close(host(dx), host(dx0) + g["dx_gate"], dtype, "dx + gate term")
+    L.flowmoe_gate_topk_bwd(s, t(x64), t(wg64), None, t(idx, torch.int32), t(w, torch.float32),
+                            t(dtw64, torch.float32), dlog, dwg, db, None, 1, ws, nws)
+    torch.cuda.synchronize()
+    assert_close(host(dwg), 2 * g["dw_gate"], "f32", "dw_gate accumulated")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("M,E", [(1024, 16), (520, 64)])
 def test_gate_bwd_top1_is_exactly_zero(dtype, M, E):
