@@ -235,17 +235,17 @@ __device__ __forceinline__ void ksum_tile(int vbid, int mtn, int ntn, int& e, in
 
 // Tile of dispatch position P (blocks go to the 8 XCDs round-robin: position
 // P runs on XCD P % 8, as its (P / 8)-th block) in an nrows x ncols grid of
-// output tiles walked in blocks of 16 x 16 tiles, row block by row block.
-// The 256 tiles of a full block are one round of all 256 CUs, and XCD x
-// takes its 4 x 8 sub-block (rows 4 (x % 4) .., columns 8 (x / 4) ..), m tile
-// fastest: inside an XCD the 32 tiles running together share 12 operand
-// panels through its L2 as before, and across XCDs every B panel is read by
-// four XCDs and every A panel by two at about the same time, so that the
-// Infinity Cache serves the repeats instead of HBM (with each XCD on a range
-// of its own, the XCDs stream eight different experts' weights at once).
-// Ragged blocks at the grid's edges walk their tiles m fastest. A full
-// block's sub-blocks need it to start at a multiple of 8: every block of
-// the grid does when the grid itself does.
+// output tiles walked in blocks of (at most) 16 x 16 tiles, row block by row
+// block. XCD x takes a sub-block of each block, m tile fastest: split 4 x 2
+// (rows (x % 4) r/4 .., columns (x / 4) c/2 ..) when the block's r rows and
+// c columns allow it, else 8 x 1 or 1 x 8, else the block is walked m tile
+// fastest. A full block's 256 tiles are one round of all 256 CUs: inside an
+// XCD the 32 tiles running together share 12 operand panels through its L2,
+// and across XCDs every B panel is read by four XCDs and every A panel by
+// two at about the same time, so that the Infinity Cache serves the
+// repeats instead of HBM (with each XCD on a range of its own, the XCDs
+// stream eight different experts' weights at once). Every block starts at a
+// multiple of 16, so its positions j have j % 8 == P % 8.
 __device__ __forceinline__ void shared_block_tile(int P, int nrows, int ncols, int& mt, int& nt) {
   constexpr int SB = 16;
   const int rb = P / (SB * ncols);
@@ -254,11 +254,13 @@ __device__ __forceinline__ void shared_block_tile(int P, int nrows, int ncols, i
   const int cb = Pr / (r * SB);
   const int c = min(SB, ncols - cb * SB);   // columns of this block
   const int j = Pr - cb * r * SB;           // position inside the r x c block
+  const int gr = (r % 4 == 0 && c % 2 == 0) ? 4 : (r % 8 == 0) ? 8 : (c % 8 == 0) ? 1 : 0;
   int lr, lc;
-  if (r == SB && c == SB) {
+  if (gr != 0) {
+    const int gc = 8 / gr, sr = r / gr, sc = c / gc;  // sub-block of sr x sc tiles per XCD
     const int x = j & 7, s = j >> 3;
-    lr = (x & 3) * 4 + (s & 3);
-    lc = (x >> 2) * 8 + (s >> 2);
+    lr = (x % gr) * sr + s % sr;
+    lc = (x / gr) * sc + s / sr;
   } else {
     lr = j % r;
     lc = j / r;
