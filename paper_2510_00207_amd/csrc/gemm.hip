@@ -83,13 +83,6 @@ struct GemmParams {
   long bias_estride;
 };
 
-// v[q] += b[q] for 8 consecutive float biases
-__device__ __forceinline__ void add_bias8(float v[8], const float* b) {
-  const float4 lo = *reinterpret_cast<const float4*>(b);
-  const float4 hi = *reinterpret_cast<const float4*>(b + 4);
-  v[0] += lo.x; v[1] += lo.y; v[2] += lo.z; v[3] += lo.w;
-  v[4] += hi.x; v[5] += hi.y; v[6] += hi.z; v[7] += hi.w;
-}
 
 // counts and offsets are device data: a range that inconsistent ones would
 // take past the row buffers is cut there, not followed
@@ -296,6 +289,34 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
     bf16_t* C1 = static_cast<bf16_t*>(p.C1);
     const bf16_t* aux = static_cast<const bf16_t*>(p.aux);
     auto sidx = [&](int r, int c4) { return r * WN + ((c4 ^ (r & (SCH - 1))) << 2); };
+    // forward biases: a lane's items all lie in one 8-column group (the item
+    // index is it * 64 + lane and 64 is a multiple of the groups per row), so
+    // its 8 (dual: 2 x 8) bias values are loaded once, before any store (a
+    // wait for a load issued after stores would wait for those stores too)
+    constexpr bool BIASED = MODE == MODE_ROWS && (EPI == EPI_STORE || EPI == EPI_GELU_FWD ||
+                                                  EPI == EPI_SWIGLU_FWD);
+    float bias0[8], bias1[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) bias0[q] = bias1[q] = 0.f;
+    if constexpr (BIASED) {
+      if (p.bias0 != nullptr || p.bias1 != nullptr) {
+        int n;
+        if constexpr (EPI == EPI_SWIGLU_FWD) {
+          constexpr int G8 = WN / 16;
+          static_assert(64 % G8 == 0, "one column group per lane");
+          const int c8 = lane % G8;
+          n = n0 + wn * (WN / 2) + (c8 >> 2) * 32 + (c8 & 3) * 8;
+        } else {
+          constexpr int G8 = WN / 8;
+          static_assert(64 % G8 == 0, "one column group per lane");
+          n = n0 + wn * WN + (lane % G8) * 8;
+        }
+        if (n < p.N) {
+          if (p.bias0 != nullptr) load8(p.bias0 + (long)e * p.bias_estride + n, bias0);
+          if (p.bias1 != nullptr) load8(p.bias1 + (long)e * p.bias_estride + n, bias1);
+        }
+      }
+    }
 #pragma unroll
     for (int hf = 0; hf < FM / 2; ++hf) {
       // activation-backward epilogues read the saved pre-activations: all of
@@ -355,8 +376,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
           float h1[8], h3[8], a[8];
           read8(rr, (jp * 64 + cin) >> 3, h1);
           read8(rr, (jp * 64 + 32 + cin) >> 3, h3);
-          if (data && p.bias0 != nullptr) add_bias8(h1, p.bias0 + (long)e * p.bias_estride + n);
-          if (data && p.bias1 != nullptr) add_bias8(h3, p.bias1 + (long)e * p.bias_estride + n);
+          if (data) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              h1[q] += bias0[q];
+              h3[q] += bias1[q];
+            }
+          }
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
             if (!data) h1[q] = h3[q] = 0.f;
@@ -432,7 +458,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
             for (int q = 0; q < 8; ++q) v[q] = 0.f;
           }
           if constexpr (EPI == EPI_STORE || EPI == EPI_GELU_FWD) {
-            if (data && p.bias0 != nullptr) add_bias8(v, p.bias0 + (long)e * p.bias_estride + n);
+            if (data) {
+#pragma unroll
+              for (int q = 0; q < 8; ++q) v[q] += bias0[q];
+            }
           }
           const long g = row0 + ti;
           if constexpr (EPI == EPI_STORE) {
