@@ -411,7 +411,10 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
  * layer needs, run once after E_1 as one GEMM per weight whose reduction
  * runs over the rows of chunks 1..R in that order (the same sums as R
  * per-chunk GEMMs, without R read-modify-write passes over the fp32
- * gradients). dW_g and db are summed over chunks in R..1 order.
+ * gradients); the experts' bias gradients (bufs->db1/db3/db2, column sums
+ * of dH and dY over the rows of every chunk) run after D_1 on the comm
+ * stream when both streams are in use, else after the weight gradients.
+ * dW_g and db are summed over chunks in R..1 order.
  * bufs->h_save is consumed: each chunk's h_save is overwritten with its dH
  * (rows x H for GELU, rows x 2H = [dH1 | dH3] for SwiGLU).
  * trace (nullable): 8*R + 2 events, the first 8*R as for the forward with

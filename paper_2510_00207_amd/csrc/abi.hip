@@ -807,8 +807,11 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     sc.signal(evE[r], s_compute);
   }
   sc.mark(4, 0, 0, s_compute);  // (the trace's last pair: the weight gradients)
+  // (with two streams the experts' bias gradients, which read dY and dH
+  // only, run on the comm stream after D_1, beside these GEMMs)
   sc.run(launch_expert_ffn_wgrad(s, R, b->dy_disp, b->x_disp, b->a_save, b->h_save, b->counts,
-                                 b->offsets, b->dw1, b->dw3, b->dw2, b->db1, b->db3, b->db2, 0,
+                                 b->offsets, b->dw1, b->dw3, b->dw2, sc.two ? nullptr : b->db1,
+                                 sc.two ? nullptr : b->db3, sc.two ? nullptr : b->db2, 0,
                                  s_compute));
   sc.mark(4, 0, 1, s_compute);
   // D_R..D_1 (dispatch backward, plus the gate's dx term) on the comm stream
@@ -824,6 +827,9 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
                                           gate_ws_wgt(ws_gate), c.dx, s_comm));
     sc.mark(2, r, 1, s_comm);
   }
+  if (sc.two)  // (after D_1, which waited for E_1: every chunk's dH and dY are final)
+    sc.run(launch_expert_bias_grad(s, R, b->dy_disp, b->h_save, b->counts, b->offsets, b->db1,
+                                   b->db3, b->db2, 0, s_comm));
   sc.signal(evEnd, s_comm);
   sc.wait(s_compute, evEnd);
   return hip_status(sc.err, "flowmoe_layer_bwd");
