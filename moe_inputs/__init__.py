@@ -26,7 +26,14 @@ Recipe (all tensors row-major):
     b_e = -1.2 * ln(rho_e), rho a seeded permutation of 1..E (log of a Zipf
     pmf with s = 1.2, up to a shift), so expert loads are heavy-tailed;
   * biased experts (expert_bias=True) add b1, b3 ~ N(0, 0.02^2) (E x H) and
-    b2 ~ N(0, 0.02^2) (E x M) in float32.
+    b2 ~ N(0, 0.02^2) (E x M) in float32;
+  * with the block's attention in AT_r (mha=True): the block input
+    mha_in ~ N(0,1) (T x M) in place of x as the layer's input, and
+    w_qkv ~ N(0, 0.02^2) (M x 3M, [W^Q | W^K | W^V]), w_o ~ N(0, 0.02^2)
+    (M x M); T/seq_len sequences of seq_len tokens, heads of width head_dim:
+      tiny 4 x 64, d 64 causal; balanced 8 x 512, d 64 bidirectional
+      (BERT-like); skewed 16 x 512, d 64 causal; large 4 x 4096, d 128 causal;
+      fine 4 x 4096 (one sequence per chunk), d 128 causal.
 
 bf16 tensors are held as numpy uint16 bit patterns; ``as_f64`` widens any
 stored tensor exactly to float64.
@@ -49,7 +56,7 @@ ZIPF_S = 1.2
 
 # tensor ids for the per-tensor streams
 _TID = {"x": 0, "w_gate": 1, "bias": 2, "w1": 3, "w3": 4, "w2": 5, "dy": 6, "b1": 7, "b3": 8,
-        "b2": 9}
+        "b2": 9, "mha_in": 10, "w_qkv": 11, "w_o": 12}
 _BLOCK = 1 << 22  # elements per independently seeded block
 
 
@@ -69,6 +76,10 @@ class MoEConfig:
     seed: int = 0
     gate: str = "renorm"  # gate weights: "renorm" (softmax over the selection) | "full"
     expert_bias: bool = False  # biased experts: b1, b3 (E x H), b2 (E x M), fp32
+    mha: bool = False     # AT_r includes the block's multi-head attention
+    seq_len: int = 0      # tokens per sequence (N of Sec. 2.1)
+    head_dim: int = 0     # width d of an attention head (heads = M / d)
+    causal: bool = True   # token i attends to tokens j <= i of its sequence
 
     def replace(self, **kw) -> "MoEConfig":
         return dataclasses.replace(self, **kw)
@@ -77,14 +88,22 @@ class MoEConfig:
     def T_chunk(self) -> int:
         return self.T // self.R
 
+    @property
+    def heads(self) -> int:
+        return self.M // self.head_dim if self.head_dim else 0
+
 
 CONFIGS = {
-    "tiny": MoEConfig("tiny", 256, 64, 128, 4, 2, 1.25, "gelu", "f32", seed=0),
-    "balanced": MoEConfig("balanced", 4096, 1024, 4096, 8, 2, 1.2, "gelu", "bf16", seed=1),
+    "tiny": MoEConfig("tiny", 256, 64, 128, 4, 2, 1.25, "gelu", "f32", seed=0,
+                      seq_len=64, head_dim=64),
+    "balanced": MoEConfig("balanced", 4096, 1024, 4096, 8, 2, 1.2, "gelu", "bf16", seed=1,
+                          seq_len=512, head_dim=64, causal=False),
     "skewed": MoEConfig("skewed", 8192, 1024, 4096, 16, 1, 1.0, "gelu", "bf16",
-                        zipf_bias=True, seed=2),
-    "large": MoEConfig("large", 16384, 4096, 14336, 8, 2, 1.25, "swiglu", "bf16", seed=3),
-    "fine": MoEConfig("fine", 16384, 2048, 1408, 64, 6, 1.5, "swiglu", "bf16", R=4, seed=4),
+                        zipf_bias=True, seed=2, seq_len=512, head_dim=64),
+    "large": MoEConfig("large", 16384, 4096, 14336, 8, 2, 1.25, "swiglu", "bf16", seed=3,
+                       seq_len=4096, head_dim=128),
+    "fine": MoEConfig("fine", 16384, 2048, 1408, 64, 6, 1.5, "swiglu", "bf16", R=4, seed=4,
+                      seq_len=4096, head_dim=128),
 }
 
 
@@ -163,7 +182,9 @@ def make_inputs(cfg: MoEConfig, *, with_dy: bool = True, x_zero_rows=None) -> di
     Returns a dict with x (T,M), w_gate (M,E), bias (E,) float32 or None,
     w1 (E,M,H), w3 (E,M,H) or None, w2 (E,H,M), dy (T,M), and the experts'
     biases b1 (E,H), b3 (E,H), b2 (E,M) float32 (None unless
-    cfg.expert_bias; b3 only for SwiGLU). Storage arrays are float32 for
+    cfg.expert_bias; b3 only for SwiGLU), and with cfg.mha the block input
+    mha_in (T,M) and the attention weights w_qkv (M,3M), w_o (M,M).
+    Storage arrays are float32 for
     dtype 'f32' and uint16 bf16 bits for 'bf16'.
     ``x_zero_rows`` (iterable of token indices) zeroes those rows of x, which
     makes their gate logits all tie (edge-case inputs).
@@ -182,6 +203,10 @@ def make_inputs(cfg: MoEConfig, *, with_dy: bool = True, x_zero_rows=None) -> di
                  if cfg.act == "swiglu" else None)
     out["w2"] = _normal(s, _TID["w2"], E * H * M, WEIGHT_STD, dt).reshape(E, H, M)
     out["dy"] = _normal(s, _TID["dy"], T * M, 1.0, dt).reshape(T, M) if with_dy else None
+    if cfg.mha:
+        out["mha_in"] = _normal(s, _TID["mha_in"], T * M, 1.0, dt).reshape(T, M)
+        out["w_qkv"] = _normal(s, _TID["w_qkv"], M * 3 * M, WEIGHT_STD, dt).reshape(M, 3 * M)
+        out["w_o"] = _normal(s, _TID["w_o"], M * M, WEIGHT_STD, dt).reshape(M, M)
     if cfg.expert_bias:  # fp32 like the gate bias
         out["b1"] = _normal(s, _TID["b1"], E * H, WEIGHT_STD, "f32").reshape(E, H)
         out["b3"] = (_normal(s, _TID["b3"], E * H, WEIGHT_STD, "f32").reshape(E, H)

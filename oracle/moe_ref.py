@@ -338,12 +338,26 @@ def layer_chunk(x, w_gate, bias, w1, w3, w2, dy, k, C, act, layout=PACKED,
 
 
 def layer_fwd_bwd(inp, k, f, act, R=1, layout=PACKED, logits_for_routing=None,
-                  C=None, gate="renorm"):
+                  C=None, gate="renorm", mha=None):
     """The layer over T tokens split into R equal contiguous chunks, each an
     independent layer call with its own capacity; per-token outputs are
     concatenated and weight gradients summed over chunks. ``inp`` holds
     float64 arrays x, w_gate, bias (or None), w1, w3 (or None), w2, dy, and
-    optionally the experts' biases b1, b3, b2."""
+    optionally the experts' biases b1, b3, b2.
+    ``mha`` (dict seq_len, heads, causal): AT_r is the chunk's multi-head
+    attention followed by the gate (Sec. 3.2); the MoE part's input x is
+    then the attention output I' of inp["mha_in"] under inp["w_qkv"] and
+    inp["w_o"], and the backward carries dx on through the attention to
+    d_in, dw_qkv and dw_o (summed over chunks)."""
+    if mha is not None:
+        from .mha_ref import mha_fwd
+        T = inp["mha_in"].shape[0]
+        if T % R:
+            raise ValueError("T must be a multiple of R")
+        Tr = T // R
+        fw = [mha_fwd(inp["mha_in"][r * Tr:(r + 1) * Tr], inp["w_qkv"], inp["w_o"],
+                      mha["seq_len"], mha["heads"], mha["causal"]) for r in range(R)]
+        inp = dict(inp, x=np.concatenate([m["out"] for m in fw], axis=0))
     x = inp["x"]
     T = x.shape[0]
     if T % R:
@@ -367,4 +381,18 @@ def layer_fwd_bwd(inp, k, f, act, R=1, layout=PACKED, logits_for_routing=None,
     for key in ("dw1", "dw3", "dw2", "dw_gate", "dbias", "db1", "db3", "db2"):
         if key in chunks[0] and chunks[0][key] is not None:
             res[key] = sum(c[key] for c in chunks)
+    if mha is not None:
+        from .mha_ref import mha_bwd
+        res["x"] = x
+        for key in ("qkv", "attn"):
+            res[key] = np.concatenate([m[key] for m in fw], axis=0)
+        res["lse"] = np.stack([m["lse"] for m in fw])  # R x heads x T_r
+        if "dx" in res:
+            bw = [mha_bwd(inp["mha_in"][r * Tr:(r + 1) * Tr], inp["w_qkv"], inp["w_o"], fw[r],
+                          chunks[r]["dx"], mha["seq_len"], mha["heads"], mha["causal"])
+                  for r in range(R)]
+            for key in ("d_attn", "d_qkv", "d_in"):
+                res[key] = np.concatenate([b[key] for b in bw], axis=0)
+            res["dw_qkv"] = sum(b["dw_qkv"] for b in bw)
+            res["dw_o"] = sum(b["dw_o"] for b in bw)
     return res

@@ -244,14 +244,19 @@ def test_k_equals_E_is_dense_softmax_mixture(rng, act):
 # ---------------------------------------------------------------------------
 # gradients: independent torch fp64 autograd of a dense masked formulation
 # ---------------------------------------------------------------------------
-def _torch_layer_grads(inp, k, C, act, gate="renorm"):
+def _torch_layer_grads(inp, k, C, act, gate="renorm", x=None):
     """Dense masked layer in torch fp64: the selection (torch.topk on
     continuous logits) and the keep mask (brute-force position count) are
     constants; y_t = sum_e keep_te * g_te * FFN_e(x_t) with g = softmax_S(l_t)
     (softmax over the selected logits) or, gate="full", softmax(l_t) over all
-    experts masked to the selection."""
+    experts masked to the selection. ``x``: a torch tensor to use as the
+    layer input (computed from other leaves; its gradient is kept)."""
     t64 = lambda a: None if a is None else torch.tensor(a, dtype=torch.float64, requires_grad=True)
-    x, wg, w1, w2 = t64(inp["x"]), t64(inp["w_gate"]), t64(inp["w1"]), t64(inp["w2"])
+    if x is None:
+        x = t64(inp["x"])
+    else:
+        x.retain_grad()
+    wg, w1, w2 = t64(inp["w_gate"]), t64(inp["w1"]), t64(inp["w2"])
     w3 = t64(inp["w3"])
     b1, b3, b2 = t64(inp.get("b1")), t64(inp.get("b3")), t64(inp.get("b2"))
     b = t64(inp["bias"]) if inp["bias"] is not None else None
