@@ -290,7 +290,14 @@ enum {
   FLOWMOE_K_GATE_BWD_TOKEN = 14, /* dx += d_logits W_g^T (flowmoe_gate_topk_bwd with dx) */
   FLOWMOE_K_GATE_BWD_DW = 15,    /* d_logits, and dW_g / db split-T partials */
   FLOWMOE_K_GATE_BWD_REDUCE = 16, /* dW_g / db reduction over splits (+ W_g^T for the dx term) */
-  FLOWMOE_K_BIAS_GRAD = 17        /* the experts' bias gradients (column sums of dY, dH) */
+  FLOWMOE_K_BIAS_GRAD = 17,       /* the experts' bias gradients (column sums of dY, dH) */
+  FLOWMOE_K_ATTN_QKV = 18,        /* attention: [Q | K | V] = I [W^Q | W^K | W^V] */
+  FLOWMOE_K_ATTN_FWD = 19,        /* attention: softmax(Q K^T / sqrt(d)) V per head */
+  FLOWMOE_K_ATTN_OUT = 20,        /* attention: I' = A W^O */
+  FLOWMOE_K_ATTN_DGRAD = 21,      /* attention: dA = dI' W^O^T, dI = d[Q|K|V] [W^Q|W^K|W^V]^T */
+  FLOWMOE_K_ATTN_BWD_DQ = 22,     /* attention backward: dQ and rowsum(dA * A) */
+  FLOWMOE_K_ATTN_BWD_DKDV = 23,   /* attention backward: dK, dV */
+  FLOWMOE_K_ATTN_WGRAD = 24       /* attention: dW^O, d[W^Q | W^K | W^V] */
 };
 
 /* Start tracing on the calling host thread: every later kernel launch whose
@@ -333,6 +340,62 @@ enum { FLOWMOE_ROWS_AUTO = 0, FLOWMOE_ROWS_NT = 1, FLOWMOE_ROWS_CACHED = 2 };
  * (for tests and tuning). FLOWMOE_ERR_INVALID for another value. */
 flowmoe_status_t flowmoe_set_row_streams(int32_t mode);
 
+/* ---- the attention part of AT_r (Sec. 2.1 MHA, Sec. 3.2 AT_r) ------------- */
+
+/* The block's multi-head attention. A call's shape->T tokens are
+ * T / seq_len whole sequences of seq_len tokens (N of Sec. 2.1) each, and
+ * M = heads * head_dim. Tensors are bf16 (shape->dtype must be
+ * FLOWMOE_BF16) and 16-byte aligned; lse and delta are float, 4-byte
+ * aligned. Only shape->T, shape->M and shape->dtype are used. */
+typedef struct {
+  int32_t seq_len;  /* tokens per sequence */
+  int32_t heads;
+  int32_t head_dim; /* 64 or 128 (else FLOWMOE_ERR_UNSUPPORTED) */
+  int32_t causal;   /* 1: token i attends to tokens j <= i of its sequence;
+                       0: to every token of its sequence */
+} flowmoe_mha_shape_t;
+
+/* Attention core (Sec. 2.1), per sequence and head h:
+ *   A_h = softmax(Q_h K_h^T / sqrt(head_dim)) V_h  (a row per query)
+ *   qkv   T x 3M (in): [Q | K | V], head h in columns h*head_dim .. of each
+ *   attn  T x M (out): the heads' A_h side by side (head h in its columns)
+ *   lse   heads x T float (out): the natural log of each row's softmax
+ *         denominator sum_j exp(s_ij), s = Q_h K_h^T / sqrt(head_dim) over
+ *         the row's visible tokens; the backward needs it
+ * Probabilities are rounded to bf16 before they multiply V; sums in float. */
+flowmoe_status_t flowmoe_attention_fwd(const flowmoe_shape_t* shape,
+                                       const flowmoe_mha_shape_t* mha, const void* qkv,
+                                       void* attn, float* lse, hipStream_t stream);
+
+/* Attention core backward: d_qkv (T x 3M, out) = the gradients of Q, K and V
+ * from d_attn (T x M, the gradient of attn) and the forward's qkv, attn and
+ * lse. delta (heads x T float, out): rowsum(d_attn_h * attn_h) per head and
+ * token, an intermediate of the softmax backward (written, then read). */
+flowmoe_status_t flowmoe_attention_bwd(const flowmoe_shape_t* shape,
+                                       const flowmoe_mha_shape_t* mha, const void* qkv,
+                                       const void* attn, const float* lse, const void* d_attn,
+                                       void* d_qkv, float* delta, hipStream_t stream);
+
+/* The block's MHA (Sec. 2.1): qkv = in [W^Q | W^K | W^V], the attention
+ * core, out = attn W^O (the I' that the gate and the experts consume).
+ *   in     T x M;  w_qkv M x 3M ([W^Q | W^K | W^V] side by side); w_o M x M
+ *   qkv    T x 3M, attn T x M, lse heads x T (out, kept for the backward)
+ *   out    T x M (out) */
+flowmoe_status_t flowmoe_mha_fwd(const flowmoe_shape_t* shape, const flowmoe_mha_shape_t* mha,
+                                 const void* in, const void* w_qkv, const void* w_o, void* qkv,
+                                 void* attn, float* lse, void* out, hipStream_t stream);
+
+/* MHA backward: d_attn = d_out W^O^T (T x M, out), the attention backward
+ * (d_qkv T x 3M and delta heads x T, out), d_in = d_qkv [W^Q|W^K|W^V]^T
+ * (T x M, out), dw_o = attn^T d_out (M x M float) and dw_qkv = in^T d_qkv
+ * (M x 3M float), overwritten or, with accumulate, added to. */
+flowmoe_status_t flowmoe_mha_bwd(const flowmoe_shape_t* shape, const flowmoe_mha_shape_t* mha,
+                                 const void* in, const void* w_qkv, const void* w_o,
+                                 const void* qkv, const void* attn, const float* lse,
+                                 const void* d_out, void* d_attn, void* d_qkv, float* delta,
+                                 void* d_in, float* dw_qkv, float* dw_o, int32_t accumulate,
+                                 hipStream_t stream);
+
 /* ---- the R-chunk two-stream layer (Sec. 3.2, Eqs. 3-6) -------------------- */
 
 /* Buffers of a whole layer over R chunks of shape->T tokens each. Per-token
@@ -349,7 +412,8 @@ typedef struct {
   const float* b3;    /* E x H, nullable, SwiGLU only */
   const float* b2;    /* E x M, nullable */
   /* forward */
-  const void* x;      /* RT x M */
+  void* x;            /* RT x M: the layer input; with `mha`, the attention
+                         output I' (written by the forward) */
   float* logits;      /* RT x E */
   int32_t* topk_idx;  /* RT x k */
   float* topk_w;      /* RT x k */
@@ -378,6 +442,22 @@ typedef struct {
   float* db1;         /* E x H, nullable: the experts' bias gradients, summed over chunks */
   float* db3;         /* E x H, nullable, SwiGLU only */
   float* db2;         /* E x M, nullable */
+  /* the attention part of AT_r (flowmoe_mha_fwd / _bwd per chunk); all
+     ignored when mha is null. Chunk r's sequences are its tokens, so
+     shape->T must be a whole number of sequences */
+  const flowmoe_mha_shape_t* mha;
+  const void* mha_in; /* RT x M: the block input I */
+  const void* w_qkv;  /* M x 3M */
+  const void* w_o;    /* M x M */
+  void* qkv;          /* RT x 3M (forward; kept for the backward) */
+  void* attn;         /* RT x M (forward; kept) */
+  float* lse;         /* R x heads x T (forward; kept) */
+  void* d_attn;       /* RT x M (backward) */
+  void* d_qkv;        /* RT x 3M (backward) */
+  float* delta;       /* R x heads x T (backward) */
+  void* d_in;         /* RT x M (backward): the block input's gradient */
+  float* dw_qkv;      /* M x 3M, summed over chunks */
+  float* dw_o;        /* M x M, summed over chunks */
   /* scratch */
   void* ws;           /* flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
                          nullable in the forward, which uses it as the
@@ -385,7 +465,8 @@ typedef struct {
   size_t ws_bytes;
 } flowmoe_layer_bufs_t;
 
-/* Forward of R chunks. Compute stream gets AT_1..AT_R (gating) then
+/* Forward of R chunks. Compute stream gets AT_1..AT_R (the chunk's
+ * attention when bufs->mha is set, then its gate) then
  * E_1..E_R (experts) (Eq. 3); comm stream gets D_1..D_R then C_1..C_R
  * (Eq. 4); events make D_r wait for AT_r, E_r for D_r and C_r for E_r.
  * The call first makes s_comm wait for work already on s_compute and ends by
@@ -393,8 +474,9 @@ typedef struct {
  * s_compute. s_comm may equal s_compute (serial schedule, same results); with
  * R = 1 there is nothing to overlap and everything runs on s_compute.
  * trace (nullable): 8*R events, recorded at start/end of each task, at index
- * 2*(task*R + r) (+1 for the end), task 0 = gate, 1 = dispatch,
- * 2 = experts, 3 = combine. The events must be created by the caller. */
+ * 2*(task*R + r) (+1 for the end), task 0 = AT_r (attention and gate),
+ * 1 = dispatch, 2 = experts, 3 = combine. The events must be created by the
+ * caller. */
 flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
                                    const flowmoe_layer_bufs_t* bufs, hipStream_t s_compute,
                                    hipStream_t s_comm, hipEvent_t* trace);
@@ -421,6 +503,13 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
  * task 0 = combine bwd, 1 = experts bwd (dH and dX of the chunk),
  * 2 = dispatch bwd (+ gate dx term), 3 = gate parameter gradients; the last
  * two (index 8*R, 8*R + 1) span the expert weight gradients.
+ * With bufs->mha, the attention part of AT_R..AT_1 runs on the compute
+ * stream after the expert weight gradients, chunk r's once D_r has made its
+ * dx final (constraint 6d): flowmoe_mha_bwd's data part, dx being the
+ * gradient of the attention output; then the attention's weight gradients
+ * over all chunks, one GEMM per weight (dW^O, dW_qkv). The trace then holds
+ * 10*R + 4 events: as above, then index 8*R + 2 + 2*r (+1) spanning chunk
+ * r's attention backward and 10*R + 2 (+1) its weight gradients.
  * With R = 1 the two streams are used only for large layers (capacity rows
  * x M x H >= 2.5e11), where the expert GEMMs span many rounds of the compute
  * units; smaller ones run everything on s_compute. */

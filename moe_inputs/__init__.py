@@ -48,7 +48,7 @@ import numpy as np
 
 __all__ = [
     "MoEConfig", "CONFIGS", "get_config", "make_inputs", "as_f64",
-    "bf16_round_bits", "bf16_bits_to_f32", "to_torch",
+    "bf16_round_bits", "bf16_bits_to_f32", "to_torch", "make_attention_inputs",
 ]
 
 WEIGHT_STD = 0.02
@@ -56,7 +56,7 @@ ZIPF_S = 1.2
 
 # tensor ids for the per-tensor streams
 _TID = {"x": 0, "w_gate": 1, "bias": 2, "w1": 3, "w3": 4, "w2": 5, "dy": 6, "b1": 7, "b3": 8,
-        "b2": 9, "mha_in": 10, "w_qkv": 11, "w_o": 12}
+        "b2": 9, "mha_in": 10, "w_qkv": 11, "w_o": 12, "qkv": 13, "d_attn": 14}
 _BLOCK = 1 << 22  # elements per independently seeded block
 
 
@@ -215,6 +215,13 @@ def make_inputs(cfg: MoEConfig, *, with_dy: bool = True, x_zero_rows=None) -> di
     else:
         out["b1"] = out["b3"] = out["b2"] = None
     return out
+
+
+def make_attention_inputs(seed: int, T: int, M: int) -> dict:
+    """Inputs of the attention core alone: qkv ~ N(0,1) (T x 3M, [Q | K | V])
+    and the gradient d_attn ~ N(0,1) (T x M), both bf16 bit patterns."""
+    return dict(qkv=_normal(seed, _TID["qkv"], T * 3 * M, 1.0, "bf16").reshape(T, 3 * M),
+                d_attn=_normal(seed, _TID["d_attn"], T * M, 1.0, "bf16").reshape(T, M))
 
 
 def to_torch(a: np.ndarray, device=None):

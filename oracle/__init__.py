@@ -26,7 +26,8 @@ Pins (what each function is checked against, in tests/test_oracle_pins.py):
   layer (chunked) concatenation of per-chunk calls; with no drops the weight
                   gradients equal the unchunked ones (microbatch equivalence,
                   App. H, Eqs. 19-23)
-  mha_fwd(+bwd)   (attention of AT_r) torch's fp64 scaled_dot_product_attention
+  attention(+bwd), mha_fwd(+bwd)
+                  (attention of AT_r) torch's fp64 scaled_dot_product_attention
                   and its autograd gradients; central finite differences;
                   closed forms: W^Q = 0 gives uniform weights (the mean, or
                   for causal attention the prefix mean, of V) and
@@ -41,4 +42,4 @@ from .moe_ref import (  # noqa: F401
     expert_ffn, combine, combine_bwd, expert_ffn_bwd, expert_bias_grads, dispatch_bwd, gate_bwd,
     gelu, gelu_grad, silu, silu_grad, layer_chunk, layer_fwd_bwd,
 )
-from .mha_ref import mha_fwd, mha_bwd  # noqa: F401
+from .mha_ref import attention, attention_bwd, mha_fwd, mha_bwd  # noqa: F401

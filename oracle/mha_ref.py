@@ -45,19 +45,15 @@ def _softmax_rows(s):
     return e / z, (m + np.log(z))[:, 0]
 
 
-def mha_fwd(inp, w_qkv, w_o, seq_len, heads, causal):
-    """Forward of one chunk's MHA (Sec. 2.1).
-
-    inp: T x M (T a multiple of seq_len: T / seq_len whole sequences),
-    w_qkv: M x 3M = [W^Q | W^K | W^V], w_o: M x M.
-    Returns qkv (T x 3M = [Q | K | V]), attn (T x M, the heads' outputs
-    concatenated, before W^O), lse (heads x T, log of each softmax
-    denominator with the row's scores), out = attn W^O (T x M)."""
-    T, M = inp.shape
+def attention(qkv, seq_len, heads, causal):
+    """The attention core per sequence and head: A_h = softmax(S) V_h with
+    s_ij = q_i . k_j / sqrt(d) over the visible tokens. qkv: T x 3M = [Q|K|V].
+    Returns attn (T x M, heads side by side) and lse (heads x T)."""
+    T, M3 = qkv.shape
+    M = M3 // 3
     if T % seq_len or M % heads:
         raise ValueError("T must hold whole sequences and M whole heads")
     d = M // heads
-    qkv = inp @ w_qkv
     attn = np.zeros((T, M))
     lse = np.zeros((heads, T))
     for b in range(T // seq_len):
@@ -69,20 +65,17 @@ def mha_fwd(inp, w_qkv, w_o, seq_len, heads, causal):
             p, l = _softmax_rows(_masked_scores(qkv[rows, cq], qkv[rows, ck], causal))
             attn[rows, cq] = p @ qkv[rows, cv]
             lse[h, rows] = l
-    return dict(qkv=qkv, attn=attn, lse=lse, out=attn @ w_o)
+    return attn, lse
 
 
-def mha_bwd(inp, w_qkv, w_o, saved, d_out, seq_len, heads, causal):
-    """Backward of mha_fwd by the chain rule, step by step: d_attn = d_out
-    W^O^T, dW^O = attn^T d_out; per sequence and head, with P the softmax
-    weights: dV = P^T dA, dP = dA V^T, dS = P * (dP - rowsum(P * dP))
-    (the softmax Jacobian), dQ = dS K / sqrt(d), dK = dS^T Q / sqrt(d); then
-    d_inp = d_qkv [W^Q | W^K | W^V]^T and dW_qkv = inp^T d_qkv.
-    Returns d_attn, d_qkv, d_in, dw_qkv, dw_o."""
-    T, M = inp.shape
+def attention_bwd(qkv, d_attn, seq_len, heads, causal):
+    """Gradient of attention() by the chain rule, per sequence and head, with
+    P the softmax weights: dV = P^T dA, dP = dA V^T, dS = P * (dP -
+    rowsum(P * dP)) (the softmax Jacobian), dQ = dS K / sqrt(d),
+    dK = dS^T Q / sqrt(d). Returns d_qkv (T x 3M)."""
+    T, M3 = qkv.shape
+    M = M3 // 3
     d = M // heads
-    qkv = saved["qkv"]
-    d_attn = d_out @ w_o.T
     d_qkv = np.zeros((T, 3 * M))
     for b in range(T // seq_len):
         rows = slice(b * seq_len, (b + 1) * seq_len)
@@ -98,5 +91,28 @@ def mha_bwd(inp, w_qkv, w_o, saved, d_out, seq_len, heads, causal):
             d_qkv[rows, cq] = ds @ k / np.sqrt(d)
             d_qkv[rows, ck] = ds.T @ q / np.sqrt(d)
             d_qkv[rows, cv] = p.T @ da
+    return d_qkv
+
+
+def mha_fwd(inp, w_qkv, w_o, seq_len, heads, causal):
+    """Forward of one chunk's MHA (Sec. 2.1).
+
+    inp: T x M (T a multiple of seq_len: T / seq_len whole sequences),
+    w_qkv: M x 3M = [W^Q | W^K | W^V], w_o: M x M.
+    Returns qkv (T x 3M = [Q | K | V]), attn (T x M, the heads' outputs
+    concatenated, before W^O), lse (heads x T, log of each softmax
+    denominator with the row's scores), out = attn W^O (T x M)."""
+    qkv = inp @ w_qkv
+    attn, lse = attention(qkv, seq_len, heads, causal)
+    return dict(qkv=qkv, attn=attn, lse=lse, out=attn @ w_o)
+
+
+def mha_bwd(inp, w_qkv, w_o, saved, d_out, seq_len, heads, causal):
+    """Backward of mha_fwd by the chain rule: d_attn = d_out W^O^T,
+    dW^O = attn^T d_out, the attention core's gradient d_qkv, then
+    d_inp = d_qkv [W^Q | W^K | W^V]^T and dW_qkv = inp^T d_qkv.
+    Returns d_attn, d_qkv, d_in, dw_qkv, dw_o."""
+    d_attn = d_out @ w_o.T
+    d_qkv = attention_bwd(saved["qkv"], d_attn, seq_len, heads, causal)
     return dict(d_attn=d_attn, d_qkv=d_qkv, d_in=d_qkv @ w_qkv.T, dw_qkv=inp.T @ d_qkv,
                 dw_o=saved["attn"].T @ d_out)

@@ -37,13 +37,19 @@ class Shape(ctypes.Structure):
                 for n in ("T", "M", "H", "E", "k", "C", "dtype", "act", "layout", "gate")]
 
 
+class MhaShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("seq_len", "heads", "head_dim", "causal")]
+
+
 _VP = ctypes.c_void_p
 _LAYER_FIELDS = [
     "w_gate", "bias", "w1", "w3", "w2", "b1", "b3", "b2",
     "x", "logits", "topk_idx", "topk_w", "counts", "offsets", "slot", "row_src", "load",
     "x_disp", "h_save", "a_save", "y_disp", "y",
     "dy", "dy_disp", "d_topk_w", "dx_disp", "dx", "d_logits", "dw_gate", "dbias", "dw1", "dw3",
-    "dw2", "db1", "db3", "db2", "ws",
+    "dw2", "db1", "db3", "db2",
+    "mha", "mha_in", "w_qkv", "w_o", "qkv", "attn", "lse", "d_attn", "d_qkv", "delta", "d_in",
+    "dw_qkv", "dw_o", "ws",
 ]
 
 
@@ -69,6 +75,7 @@ def load():
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, SZ = _VP, ctypes.c_int32, ctypes.c_size_t
     SP = ctypes.POINTER(Shape)
+    MP = ctypes.POINTER(MhaShape)
     sig = {
         "flowmoe_version": ([], ctypes.c_char_p),
         "flowmoe_last_error": ([], ctypes.c_char_p),
@@ -90,6 +97,10 @@ def load():
         "flowmoe_trace_stop": ([], I32),
         "flowmoe_set_gemm_tiles": ([I32], I32),
         "flowmoe_set_row_streams": ([I32], I32),
+        "flowmoe_attention_fwd": ([SP, MP, P, P, P, P], I32),
+        "flowmoe_attention_bwd": ([SP, MP, P, P, P, P, P, P, P], I32),
+        "flowmoe_mha_fwd": ([SP, MP, P, P, P, P, P, P, P, P], I32),
+        "flowmoe_mha_bwd": ([SP, MP] + [P] * 13 + [I32, P], I32),
         "flowmoe_layer_fwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
         "flowmoe_layer_bwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
     }
@@ -222,10 +233,41 @@ def flowmoe_gate_topk_bwd_noalloc(shape, x, w_gate, logits, topk_idx, topk_w, d_
                                                 _stream(stream)))
 
 
+# ---- the attention part of AT_r ----------------------------------------------------
+def make_mha_shape(seq_len, heads, head_dim, causal) -> MhaShape:
+    return MhaShape(seq_len, heads, head_dim, int(bool(causal)))
+
+
+def flowmoe_attention_fwd(shape, mha, qkv, attn, lse, stream=None):
+    _check(load().flowmoe_attention_fwd(ctypes.byref(shape), ctypes.byref(mha), ptr(qkv), ptr(attn),
+                                        ptr(lse), _stream(stream)))
+
+
+def flowmoe_attention_bwd(shape, mha, qkv, attn, lse, d_attn, d_qkv, delta, stream=None):
+    _check(load().flowmoe_attention_bwd(ctypes.byref(shape), ctypes.byref(mha), ptr(qkv), ptr(attn),
+                                        ptr(lse), ptr(d_attn), ptr(d_qkv), ptr(delta),
+                                        _stream(stream)))
+
+
+def flowmoe_mha_fwd(shape, mha, inp, w_qkv, w_o, qkv, attn, lse, out, stream=None):
+    _check(load().flowmoe_mha_fwd(ctypes.byref(shape), ctypes.byref(mha), ptr(inp), ptr(w_qkv),
+                                  ptr(w_o), ptr(qkv), ptr(attn), ptr(lse), ptr(out),
+                                  _stream(stream)))
+
+
+def flowmoe_mha_bwd(shape, mha, inp, w_qkv, w_o, qkv, attn, lse, d_out, d_attn, d_qkv, delta, d_in,
+                    dw_qkv, dw_o, accumulate, stream=None):
+    _check(load().flowmoe_mha_bwd(ctypes.byref(shape), ctypes.byref(mha), ptr(inp), ptr(w_qkv),
+                                  ptr(w_o), ptr(qkv), ptr(attn), ptr(lse), ptr(d_out), ptr(d_attn),
+                                  ptr(d_qkv), ptr(delta), ptr(d_in), ptr(dw_qkv), ptr(dw_o),
+                                  int(accumulate), _stream(stream)))
+
+
 # ---- kernel tracing --------------------------------------------------------------
 K_NAMES = ["gate", "route", "scan", "gather", "ffn1", "ffn2", "swiglu_act", "combine",
            "combine_bwd", "dgrad1", "wgrad2", "wgrad1", "dgrad2", "gate_bwd_wt", "gate_bwd_token",
-           "gate_bwd_dw", "gate_bwd_reduce", "bias_grad"]
+           "gate_bwd_dw", "gate_bwd_reduce", "bias_grad", "attn_qkv", "attn_fwd", "attn_out",
+           "attn_dgrad", "attn_bwd_dq", "attn_bwd_dkdv", "attn_wgrad"]
 K = {n: i for i, n in enumerate(K_NAMES)}
 K_GEMM = ("ffn1", "ffn2", "dgrad1", "wgrad2", "wgrad1", "dgrad2")
 
@@ -272,6 +314,9 @@ def layer_bufs(**tensors) -> LayerBufs:
     for name, t in tensors.items():
         if name == "ws_bytes":
             b.ws_bytes = int(t)
+        elif name == "mha":  # a MhaShape (or None), kept alive with the buffers
+            b._mha = t
+            b.mha = None if t is None else ctypes.addressof(t)
         elif name not in _LAYER_FIELDS:
             raise KeyError(name)
         else:
@@ -296,10 +341,15 @@ def flowmoe_layer_fwd(shape, R, bufs, s_compute=None, s_comm=None, trace=None):
                                     _events(trace)))
 
 
+def bwd_trace_len(R: int, mha: bool) -> int:
+    """Events of flowmoe_layer_bwd's trace: 8R + 2, or 10R + 4 with the attention."""
+    return 10 * R + 4 if mha else 8 * R + 2
+
+
 def flowmoe_layer_bwd(shape, R, bufs, s_compute=None, s_comm=None, trace=None):
-    if trace is not None and len(trace) < 8 * R + 2:
-        raise ValueError(f"the backward trace takes 8 * R + 2 = {8 * R + 2} events, "
-                         f"got {len(trace)}")
+    need = bwd_trace_len(R, bool(bufs.mha))
+    if trace is not None and len(trace) < need:
+        raise ValueError(f"the backward trace takes {need} events, got {len(trace)}")
     sc = _stream(s_compute)
     sm = sc if s_comm is None else _stream(s_comm)
     _check(load().flowmoe_layer_bwd(ctypes.byref(shape), R, ctypes.byref(bufs), sc, sm,

@@ -559,11 +559,139 @@ flowmoe_status_t flowmoe_gate_topk_bwd_noalloc(const flowmoe_shape_t* shape, con
 // ---------------------------------------------------------------------------
 namespace {
 
+// The attention of T tokens of width M: bf16, whole sequences, M = heads *
+// head_dim with head_dim 64 or 128
+flowmoe_status_t check_mha(const flowmoe_shape_t* s, const flowmoe_mha_shape_t* m, AttnShape* out) {
+  if (s == nullptr) return fail(FLOWMOE_ERR_INVALID, "shape is null");
+  if (m == nullptr) return fail(FLOWMOE_ERR_INVALID, "mha is null");
+  if (s->dtype != FLOWMOE_BF16)
+    return fail(FLOWMOE_ERR_UNSUPPORTED, "the attention runs in FLOWMOE_BF16 only");
+  if (s->T < 0) return fail(FLOWMOE_ERR_INVALID, "T = %d < 0", s->T);
+  if (m->head_dim != 64 && m->head_dim != 128)
+    return fail(FLOWMOE_ERR_UNSUPPORTED, "head_dim = %d is not 64 or 128", m->head_dim);
+  if (m->heads < 1 || (long)m->heads * m->head_dim != s->M)
+    return fail(FLOWMOE_ERR_INVALID, "heads * head_dim = %d * %d is not M = %d", m->heads,
+                m->head_dim, s->M);
+  if (m->seq_len < 1) return fail(FLOWMOE_ERR_INVALID, "seq_len = %d < 1", m->seq_len);
+  if (s->T % m->seq_len)
+    return fail(FLOWMOE_ERR_INVALID, "T = %d is not a whole number of sequences of %d tokens",
+                s->T, m->seq_len);
+  if (m->causal != 0 && m->causal != 1)
+    return fail(FLOWMOE_ERR_INVALID, "causal = %d is not 0 or 1", m->causal);
+  if ((long)s->T * 3 * s->M > (1L << 40) || s->T > (1 << 30))
+    return fail(FLOWMOE_ERR_UNSUPPORTED, "tensor too large");
+  if ((long)((m->seq_len + 127) / 128) * m->heads * (s->T / m->seq_len) > (1L << 31))
+    return fail(FLOWMOE_ERR_UNSUPPORTED, "too many attention tiles");
+  if (out) *out = AttnShape{m->seq_len, m->heads, m->head_dim, m->causal};
+  return FLOWMOE_OK;
+}
+
+#define REQUIRE_F(p, name)                                                     \
+  if ((p) == nullptr) return fail(FLOWMOE_ERR_INVALID, "%s is null", name);     \
+  if (reinterpret_cast<uintptr_t>(p) % 4 != 0)                                 \
+    return fail(FLOWMOE_ERR_INVALID, "%s is not 4-byte aligned", name)
+
+}  // namespace
+
+extern "C" {
+
+flowmoe_status_t flowmoe_attention_fwd(const flowmoe_shape_t* shape,
+                                       const flowmoe_mha_shape_t* mha, const void* qkv,
+                                       void* attn, float* lse, hipStream_t stream) {
+  AttnShape m;
+  flowmoe_status_t st = check_mha(shape, mha, &m);
+  if (st != FLOWMOE_OK) return st;
+  if (shape->T == 0) return ok();
+  REQUIRE_T(qkv, "qkv");
+  REQUIRE_T(attn, "attn");
+  REQUIRE_F(lse, "lse");
+  return hip_status(launch_attn_fwd(m, shape->T, shape->M, qkv, attn, lse, stream),
+                    "flowmoe_attention_fwd");
+}
+
+flowmoe_status_t flowmoe_attention_bwd(const flowmoe_shape_t* shape,
+                                       const flowmoe_mha_shape_t* mha, const void* qkv,
+                                       const void* attn, const float* lse, const void* d_attn,
+                                       void* d_qkv, float* delta, hipStream_t stream) {
+  AttnShape m;
+  flowmoe_status_t st = check_mha(shape, mha, &m);
+  if (st != FLOWMOE_OK) return st;
+  if (shape->T == 0) return ok();
+  REQUIRE_T(qkv, "qkv");
+  REQUIRE_T(attn, "attn");
+  REQUIRE_F(lse, "lse");
+  REQUIRE_T(d_attn, "d_attn");
+  REQUIRE_T(d_qkv, "d_qkv");
+  REQUIRE_F(delta, "delta");
+  return hip_status(launch_attn_bwd(m, shape->T, shape->M, qkv, attn, lse, d_attn, d_qkv, delta,
+                                    stream),
+                    "flowmoe_attention_bwd");
+}
+
+flowmoe_status_t flowmoe_mha_fwd(const flowmoe_shape_t* shape, const flowmoe_mha_shape_t* mha,
+                                 const void* in, const void* w_qkv, const void* w_o, void* qkv,
+                                 void* attn, float* lse, void* out, hipStream_t stream) {
+  AttnShape m;
+  flowmoe_status_t st = check_mha(shape, mha, &m);
+  if (st != FLOWMOE_OK) return st;
+  if (shape->T == 0) return ok();
+  REQUIRE_T(in, "in");
+  REQUIRE_T(w_qkv, "w_qkv");
+  REQUIRE_T(w_o, "w_o");
+  REQUIRE_T(qkv, "qkv");
+  REQUIRE_T(attn, "attn");
+  REQUIRE_F(lse, "lse");
+  REQUIRE_T(out, "out");
+  return hip_status(launch_mha_fwd(m, shape->T, shape->M, in, w_qkv, w_o, qkv, attn, lse, out,
+                                   stream),
+                    "flowmoe_mha_fwd");
+}
+
+flowmoe_status_t flowmoe_mha_bwd(const flowmoe_shape_t* shape, const flowmoe_mha_shape_t* mha,
+                                 const void* in, const void* w_qkv, const void* w_o,
+                                 const void* qkv, const void* attn, const float* lse,
+                                 const void* d_out, void* d_attn, void* d_qkv, float* delta,
+                                 void* d_in, float* dw_qkv, float* dw_o, int32_t accumulate,
+                                 hipStream_t stream) {
+  AttnShape m;
+  flowmoe_status_t st = check_mha(shape, mha, &m);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE_T(dw_qkv, "dw_qkv");
+  REQUIRE_T(dw_o, "dw_o");
+  if (shape->T > 0) {
+    REQUIRE_T(in, "in");
+    REQUIRE_T(w_qkv, "w_qkv");
+    REQUIRE_T(w_o, "w_o");
+    REQUIRE_T(qkv, "qkv");
+    REQUIRE_T(attn, "attn");
+    REQUIRE_F(lse, "lse");
+    REQUIRE_T(d_out, "d_out");
+    REQUIRE_T(d_attn, "d_attn");
+    REQUIRE_T(d_qkv, "d_qkv");
+    REQUIRE_F(delta, "delta");
+    REQUIRE_T(d_in, "d_in");
+  }
+  const int T = shape->T, M = shape->M;
+  hipError_t e = launch_mha_bwd_data(m, T, M, w_qkv, w_o, qkv, attn, lse, d_out, d_attn, d_qkv,
+                                     delta, d_in, stream);
+  if (e == hipSuccess)
+    e = launch_mha_wgrad(T, M, 1, in, attn, d_out, d_qkv, dw_qkv, dw_o, accumulate != 0, stream);
+  return hip_status(e, "flowmoe_mha_bwd");
+}
+
+}  // extern "C"
+
+namespace {
+
 struct Chunk {
   const char *x, *dy;
   float *logits, *w, *dw, *dl;
   int32_t *idx, *counts, *offsets, *slot, *row_src, *load;
   char *x_disp, *h_save, *a_save, *y_disp, *y, *dy_disp, *dx_disp, *dx;
+  // the attention part of AT_r (null without it); xw: x as written by it
+  const char* in;
+  char *xw, *qkv, *attn, *d_attn, *d_qkv, *d_in;
+  float *lse, *delta;
 };
 
 Chunk chunk_of(const Shape& s, const flowmoe_layer_bufs_t* b, int r) {
@@ -591,6 +719,16 @@ Chunk chunk_of(const Shape& s, const flowmoe_layer_bufs_t* b, int r) {
   c.dy_disp = mptr(b->dy_disp, r * rows * M * es);
   c.dx_disp = mptr(b->dx_disp, r * rows * M * es);
   c.dx = mptr(b->dx, r * T * M * es);
+  const long heads = b->mha ? b->mha->heads : 0;
+  c.in = b->mha_in ? cptr(b->mha_in, r * T * M * es) : nullptr;
+  c.xw = mptr(b->x, r * T * M * es);
+  c.qkv = mptr(b->qkv, r * T * 3 * M * es);
+  c.attn = mptr(b->attn, r * T * M * es);
+  c.d_attn = mptr(b->d_attn, r * T * M * es);
+  c.d_qkv = mptr(b->d_qkv, r * T * 3 * M * es);
+  c.d_in = mptr(b->d_in, r * T * M * es);
+  c.lse = b->lse ? b->lse + r * heads * T : nullptr;
+  c.delta = b->delta ? b->delta + r * heads * T : nullptr;
   return c;
 }
 
@@ -600,9 +738,9 @@ struct Sched {
   hipEvent_t* trace;
   int R;
   hipError_t err = hipSuccess;
-  void mark(int task, int r, int end, hipStream_t st) {
-    if (trace != nullptr && err == hipSuccess)
-      err = hipEventRecord(trace[2 * (task * R + r) + end], st);
+  void mark(int task, int r, int end, hipStream_t st) { mark_at(2 * (task * R + r) + end, st); }
+  void mark_at(int i, hipStream_t st) {
+    if (trace != nullptr && err == hipSuccess) err = hipEventRecord(trace[i], st);
   }
   void signal(hipEvent_t ev, hipStream_t st) {
     if (two && err == hipSuccess) err = hipEventRecord(ev, st);
@@ -625,6 +763,32 @@ flowmoe_status_t check_layer(const flowmoe_shape_t* shape, int32_t R, const flow
   return FLOWMOE_OK;
 }
 
+// the attention part of AT_r: shape and buffers (forward; backward adds its own)
+flowmoe_status_t check_layer_mha(const flowmoe_shape_t* shape, const flowmoe_layer_bufs_t* b,
+                                 bool bwd, AttnShape* m) {
+  flowmoe_status_t st = check_mha(shape, b->mha, m);
+  if (st != FLOWMOE_OK) return st;
+  REQUIRE_T(b->w_qkv, "bufs->w_qkv");
+  REQUIRE_T(b->w_o, "bufs->w_o");
+  if (bwd) {
+    REQUIRE_T(b->dw_qkv, "bufs->dw_qkv");
+    REQUIRE_T(b->dw_o, "bufs->dw_o");
+  }
+  if (shape->T > 0) {
+    REQUIRE_T(b->mha_in, "bufs->mha_in");
+    REQUIRE_T(b->qkv, "bufs->qkv");
+    REQUIRE_T(b->attn, "bufs->attn");
+    REQUIRE_F(b->lse, "bufs->lse");
+    if (bwd) {
+      REQUIRE_T(b->d_attn, "bufs->d_attn");
+      REQUIRE_T(b->d_qkv, "bufs->d_qkv");
+      REQUIRE_F(b->delta, "bufs->delta");
+      REQUIRE_T(b->d_in, "bufs->d_in");
+    }
+  }
+  return FLOWMOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -643,6 +807,11 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
   if (s.act == FLOWMOE_SWIGLU) REQUIRE_T(b->w3, "bufs->w3");
   st = check_biases(s, b->b1, b->b3, b->b2, "bufs->");
   if (st != FLOWMOE_OK) return st;
+  AttnShape am = {};
+  if (b->mha != nullptr) {
+    st = check_layer_mha(shape, b, false, &am);
+    if (st != FLOWMOE_OK) return st;
+  }
   if (b->ws != nullptr) {  // optional here: the dispatch scan's tile histograms
     st = check_ws(b->ws, b->ws_bytes, dispatch_ws_bytes(s), "flowmoe_layer_fwd");
     if (st != FLOWMOE_OK) return st;
@@ -667,10 +836,14 @@ flowmoe_status_t flowmoe_layer_fwd(const flowmoe_shape_t* shape, int32_t R,
   hipEvent_t *evG = ev, *evD = ev + R, *evF = ev + 2 * R, evStart = ev[3 * R], evEnd = ev[3 * R + 1];
   sc.signal(evStart, s_compute);
   sc.wait(s_comm, evStart);
-  // AT_1..AT_R on the compute stream (gating part of AT_r)
+  // AT_1..AT_R on the compute stream: the chunk's attention (which writes
+  // its x), then the gate
   for (int r = 0; r < R; ++r) {
     Chunk c = chunk_of(s, b, r);
     sc.mark(0, r, 0, s_compute);
+    if (b->mha != nullptr)
+      sc.run(launch_mha_fwd(am, s.T, s.M, c.in, b->w_qkv, b->w_o, c.qkv, c.attn, c.lse, c.xw,
+                            s_compute));
     sc.run(launch_gate_topk(s, c.x, b->w_gate, b->bias, c.logits, c.idx, c.w, s_compute));
     sc.mark(0, r, 1, s_compute);
     sc.signal(evG[r], s_compute);
@@ -728,6 +901,12 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
   }
   st = check_biases(s, b->db1, b->db3, b->db2, "bufs->d");
   if (st != FLOWMOE_OK) return st;
+  AttnShape am = {};
+  const bool mha = b->mha != nullptr;
+  if (mha) {
+    st = check_layer_mha(shape, b, true, &am);
+    if (st != FLOWMOE_OK) return st;
+  }
   if (s.T > 0) {
     REQUIRE_T(b->x, "bufs->x"); REQUIRE_T(b->dy, "bufs->dy"); REQUIRE(b->topk_idx, "bufs->topk_idx");
     REQUIRE(b->topk_w, "bufs->topk_w"); REQUIRE(b->slot, "bufs->slot");
@@ -753,9 +932,10 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
   if (R == 1 && (double)s.rows * s.M * s.H < 2.5e11) s_comm = s_compute;
   Sched sc{s_compute, s_comm, s_comm != s_compute, trace, R};
   hipEvent_t* ev = nullptr;
-  sc.run(get_events(3 * R + 2, &ev));
+  sc.run(get_events(4 * R + 2, &ev));
   if (sc.err != hipSuccess) return hip_status(sc.err, "flowmoe_layer_bwd events");
-  hipEvent_t *evC = ev, *evE = ev + R, evStart = ev[3 * R], evEnd = ev[3 * R + 1];
+  hipEvent_t *evC = ev, *evE = ev + R, *evD = ev + 3 * R + 2, evStart = ev[3 * R],
+             evEnd = ev[3 * R + 1];
   sc.signal(evStart, s_compute);
   sc.wait(s_comm, evStart);
   // The gate's own gradients (d_logits, dW_g, db) need only the combine
@@ -826,10 +1006,28 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
                : launch_dispatch_bwd_gate(s, c.dx_disp, c.slot, c.idx, c.w, c.dw,
                                           gate_ws_wgt(ws_gate), c.dx, s_comm));
     sc.mark(2, r, 1, s_comm);
+    if (mha) sc.signal(evD[r], s_comm);
   }
   if (sc.two)  // (after D_1, which waited for E_1: every chunk's dH and dY are final)
     sc.run(launch_expert_bias_grad(s, R, b->dy_disp, b->h_save, b->counts, b->offsets, b->db1,
                                    b->db3, b->db2, 0, s_comm));
+  // the attention part of AT_R..AT_1 on the compute stream, each after D_r
+  // has completed its x gradient (dx: the attention output's gradient),
+  // then its weight gradients over all chunks (one GEMM per weight)
+  if (mha) {
+    for (int r = R - 1; r >= 0; --r) {
+      Chunk c = chunk_of(s, b, r);
+      sc.wait(s_compute, evD[r]);
+      sc.mark_at(8 * R + 2 + 2 * r, s_compute);
+      sc.run(launch_mha_bwd_data(am, s.T, s.M, b->w_qkv, b->w_o, c.qkv, c.attn, c.lse, c.dx,
+                                 c.d_attn, c.d_qkv, c.delta, c.d_in, s_compute));
+      sc.mark_at(8 * R + 3 + 2 * r, s_compute);
+    }
+    sc.mark_at(10 * R + 2, s_compute);
+    sc.run(launch_mha_wgrad(s.T, s.M, R, b->mha_in, b->attn, b->dx, b->d_qkv, b->dw_qkv, b->dw_o,
+                            0, s_compute));
+    sc.mark_at(10 * R + 3, s_compute);
+  }
   sc.signal(evEnd, s_comm);
   sc.wait(s_compute, evEnd);
   return hip_status(sc.err, "flowmoe_layer_bwd");

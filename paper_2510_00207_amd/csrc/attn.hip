@@ -1,0 +1,583 @@
+// The multi-head attention of AT_r (Sec. 2.1): per sequence and head,
+// A = softmax(Q K^T / sqrt(d)) V with Q, K, V the head's columns of
+// I [W^Q | W^K | W^V], then I' = A W^O. The projections run on the grouped
+// GEMM as one dense expert; the attention runs in the kernels below, which
+// stream K and V tiles through LDS and never store the N x N scores.
+//
+// Forward (one block: 128 queries of one sequence and head, 4 waves of 32):
+// each wave computes S^T = K Q^T for a 64-key tile with
+// v_mfma_f32_32x32x16_bf16, so that a lane's accumulator column is one query
+// and the online-softmax statistics (running max and sum, base-2 exponents)
+// live in the lane pair (l, l + 32) that holds that query's 64 scores. The
+// bf16 probabilities P^T are then the second MFMA's column operand straight
+// from the registers, and O^T += V^T P^T takes V^T from LDS by transposing
+// reads (ds_read_b64_tr_b16). The log-sum-exp of each row is kept for the
+// backward.
+//
+// Backward (no atomics; every sum in a fixed order):
+//   dq kernel (blocks of 128 queries, loop over 64-key tiles): recomputes P
+//     from S and the log-sum-exp, dP^T = V dO^T, dS = P (dP - delta) with
+//     delta = rowsum(dO * O) (computed here and stored for the next kernel),
+//     dQ^T += K^T dS^T;
+//   dkdv kernel (blocks of 128 keys, loop over 32-query steps): S and dP with
+//     the key as the accumulator column, dV^T += dO^T P, dK^T += Q^T dS.
+#include <math.h>
+
+#include "common.hpp"
+
+namespace flowmoe {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+struct AttnArgs {
+  const bf16_t* qkv;  // T x 3M = [Q | K | V]; head h at columns h * D of each
+  const bf16_t* o;    // T x M: the heads' outputs (backward)
+  const bf16_t* d_o;  // T x M: their gradient (backward)
+  bf16_t* out;        // forward: T x M
+  bf16_t* d_qkv;      // backward: T x 3M
+  float* lse;         // heads x T: natural log-sum-exp of each row's scores
+  float* delta;       // heads x T: rowsum(dO * O) over the head's columns
+  int T, M, N, heads, nseq;
+  float c2;  // log2(e) / sqrt(D): a score times c2 is its base-2 exponent
+  float rs;  // 1 / sqrt(D)
+};
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ bf16x8 zero8() { return __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0}); }
+
+__device__ __forceinline__ floatx16 zero16() {
+  floatx16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.0f;
+  return z;
+}
+
+// LDS tiles hold rows of D bf16 (2D bytes); the 16-byte chunk c of row r
+// sits at chunk c ^ sw(r). For D = 128 (a row is one pass over the 64 banks)
+// sw is one-to-one on any 16 consecutive rows, so a row read (16 lanes on 16
+// rows, one chunk each) touches 16 distinct bank groups; sw / 2 takes 4
+// distinct values of one parity on 4 aligned rows, so a transposing read
+// (4 aligned rows x two adjacent 32-byte column pairs per 32 lanes) does too.
+// For D = 64 (two rows per pass) the same holds with the row parity as the
+// extra bank bit.
+template <int D>
+__device__ __forceinline__ int sw(int r) {
+  if constexpr (D == 128) return 4 * (r & 3) + ((r >> 2) & 3);
+  else return 4 * ((r >> 1) & 1) + 2 * ((r >> 2) & 1) + ((r >> 3) & 1);
+}
+template <int D>
+__device__ __forceinline__ int toff(int r, int c) {
+  return r * (2 * D) + ((c ^ sw<D>(r)) << 4);
+}
+
+// MFMA operand with d contiguous: lane l supplies row r (its l % 32 row of
+// the 32-row block) at d = 16 ks + 8 (l / 32) .. + 7
+template <int D>
+__device__ __forceinline__ bf16x8 frag_row(const char* t, int r, int ks, int h2) {
+  return *reinterpret_cast<const bf16x8*>(t + toff<D>(r, 2 * ks + h2));
+}
+
+// Transposed operand: lane l supplies column cb + l % 32 of the tile at the
+// 8 rows of its k-slots, slot 4 i + j (i = 0, 1; j = 0..3) being row
+// rb + 4 (l / 32) + 8 i + j. Each ds_read_b64_tr_b16 hands lane l' of a
+// 16-lane group element l' % 4 of the 4 values that lane 4 q + l' / 4
+// addressed, in slot q; lanes aimed at rows r0 + s / 4, columns c0 + 4 (s % 4)
+// give lane l' column c0 + l' at rows r0 .. r0 + 3.
+template <int D>
+__device__ __forceinline__ bf16x8 frag_tr(const char* t, int rb, int cb, int lane) {
+  const int G = lane >> 4, sl = lane & 15;
+  const int col = cb + (G & 1) * 16 + 4 * (sl & 3);
+  v4i16 v[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = rb + 4 * (G >> 1) + 8 * i + (sl >> 2);
+    v[i] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_v4i16_t*)(t + toff<D>(r, col >> 3) + ((col & 7) << 1)));
+  }
+  const short __attribute__((ext_vector_type(8))) s = {v[0][0], v[0][1], v[0][2], v[0][3],
+                                                       v[1][0], v[1][1], v[1][2], v[1][3]};
+  return __builtin_bit_cast(bf16x8, s);
+}
+
+// Rows 16 s .. 16 s + 15 of a 32 x 32 accumulator (lane l: column l % 32,
+// element 4 J + j = row 8 J + 4 (l / 32) + j) as an MFMA column operand in
+// frag_tr's slot order: slot 4 i + j <- element 8 s + 4 i + j.
+__device__ __forceinline__ bf16x8 pfrag(const floatx16& a, int s) {
+  bf16x8 r;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) r[t] = (__bf16)a[8 * s + t];
+  return r;
+}
+
+__device__ __forceinline__ floatx16 mfma(const bf16x8& a, const bf16x8& b, const floatx16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// store a 32-row block of a transposed accumulator (lane: column = token,
+// rows = d) as bf16 row segments dst[8 J + 4 (l / 32) .. + 3] * scale
+__device__ __forceinline__ void store_cols(bf16_t* dst, const floatx16& a, int h2, float scale) {
+#pragma unroll
+  for (int J = 0; J < 4; ++J) {
+    uint2 v;
+    v.x = pack_bf16x2(a[4 * J] * scale, a[4 * J + 1] * scale);
+    v.y = pack_bf16x2(a[4 * J + 2] * scale, a[4 * J + 3] * scale);
+    *reinterpret_cast<uint2*>(dst + 8 * J + 4 * h2) = v;
+  }
+}
+
+// 64-row K and V tiles of one (sequence, head), double-buffered through
+// registers: every thread moves D / 32 16-byte chunks of each per tile
+template <int D>
+struct KVTiles {
+  static constexpr int CPR = D / 8;             // 16-byte chunks per row
+  static constexpr int TB = 64 * D * 2;         // bytes of one tile
+  static constexpr int LD = 64 * CPR / 256;     // chunks per thread per tile
+  u32x4 rk[LD], rv[LD];
+  __device__ __forceinline__ void load(const bf16_t* Kg, const bf16_t* Vg, long ld, int key0, int N,
+                                       int tid) {
+#pragma unroll
+    for (int u = 0; u < LD; ++u) {
+      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, key = key0 + r;
+      if (key < N) {
+        rk[u] = *reinterpret_cast<const u32x4*>(Kg + key * ld + 8 * c);
+        rv[u] = *reinterpret_cast<const u32x4*>(Vg + key * ld + 8 * c);
+      } else {
+        rk[u] = u32x4{0, 0, 0, 0};
+        rv[u] = u32x4{0, 0, 0, 0};
+      }
+    }
+  }
+  __device__ __forceinline__ void store(char* tk, char* tv, int tid) {
+#pragma unroll
+    for (int u = 0; u < LD; ++u) {
+      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR;
+      *reinterpret_cast<u32x4*>(tk + toff<D>(r, c)) = rk[u];
+      *reinterpret_cast<u32x4*>(tv + toff<D>(r, c)) = rv[u];
+    }
+  }
+};
+
+// block -> (query or key tile, head, sequence); `rev`: tiles in descending
+// order (the causal forward's longest query tiles first)
+__device__ __forceinline__ void decode(const AttnArgs& a, bool rev, int& tile, int& hd, int& sq) {
+  const int per = a.heads * a.nseq, nt = (a.N + 127) / 128;
+  const int t = (int)(blockIdx.x / per), rest = (int)(blockIdx.x % per);
+  tile = rev ? nt - 1 - t : t;
+  hd = rest % a.heads;
+  sq = rest / a.heads;
+}
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
+  constexpr int KS = D / 16, DB = D / 32;
+  using Tiles = KVTiles<D>;
+  __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
+  int qt, hd, sq;
+  decode(a, CAUSAL, qt, hd, sq);
+  const long tok0 = (long)sq * a.N, ld = 3L * a.M;
+  const bf16_t* Qg = a.qkv + tok0 * ld + (long)hd * D;
+  const bf16_t* Kg = Qg + a.M;
+  const bf16_t* Vg = Qg + 2L * a.M;
+  const int q0 = qt * 128, qw = q0 + 32 * w + lq;
+
+  bf16x8 qf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+    qf[ks] = qw < a.N ? *reinterpret_cast<const bf16x8*>(Qg + qw * ld + 16 * ks + 8 * h2) : zero8();
+  floatx16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[db] = zero16();
+  float m = -INFINITY, l = 0.0f;
+
+  const int kend = CAUSAL ? min(a.N, q0 + 128) : a.N;
+  const int nk = (kend + 63) / 64;
+  Tiles tl;
+  tl.load(Kg, Vg, ld, 0, a.N, tid);
+  tl.store(lds, lds + Tiles::TB, tid);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt & 1;
+    if (kt + 1 < nk) tl.load(Kg, Vg, ld, (kt + 1) * 64, a.N, tid);
+    const char* tk = lds + st * 2 * Tiles::TB;
+    const char* tv = tk + Tiles::TB;
+    const int kb0 = kt * 64;
+    // (causal: a wave whose queries all precede the tile has nothing in it)
+    if (!CAUSAL || kb0 <= q0 + 32 * w + 31) {
+      floatx16 s[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        s[kb] = zero16();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) s[kb] = mfma(frag_row<D>(tk, 32 * kb + lq, ks, h2), qf[ks], s[kb]);
+      }
+      const bool edge = kb0 + 64 > a.N || (CAUSAL && kb0 + 63 > q0 + 32 * w);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float v = s[kb][r] * a.c2;
+          if (edge) {
+            const int key = kb0 + 32 * kb + 8 * (r >> 2) + 4 * h2 + (r & 3);
+            if (key >= a.N || (CAUSAL && key > qw)) v = -INFINITY;
+          }
+          s[kb][r] = v;
+          mx = fmaxf(mx, v);
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // every query sees key 0 in the first tile, so m is finite from then on
+      const float mn = fmaxf(m, mx);
+      const float al = exp2_fast(m - mn);
+      float rsum = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float pv = exp2_fast(s[kb][r] - mn);
+          s[kb][r] = pv;
+          rsum += pv;
+        }
+      }
+      rsum += __shfl_xor(rsum, 32);
+      l = l * al + rsum;
+      m = mn;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] *= al;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const bf16x8 pb = pfrag(s[kb], s2);
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+            o[db] = mfma(frag_tr<D>(tv, 32 * kb + 16 * s2, 32 * db, lane), pb, o[db]);
+        }
+      }
+    }
+    if (kt + 1 < nk) {
+      char* nk_ = lds + (st ^ 1) * 2 * Tiles::TB;
+      tl.store(nk_, nk_ + Tiles::TB, tid);
+    }
+    __syncthreads();
+  }
+  if (qw < a.N) {
+    const float inv = 1.0f / l;
+    bf16_t* Og = a.out + (tok0 + qw) * a.M + (long)hd * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) store_cols(Og + 32 * db, o[db], h2, inv);
+    if (h2 == 0) a.lse[(long)hd * a.T + tok0 + qw] = (m + log2f(l)) * kLn2;
+  }
+}
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(256, 1) void attn_dq_kernel(AttnArgs a) {
+  constexpr int KS = D / 16, DB = D / 32;
+  using Tiles = KVTiles<D>;
+  __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
+  int qt, hd, sq;
+  decode(a, CAUSAL, qt, hd, sq);
+  const long tok0 = (long)sq * a.N, ld = 3L * a.M;
+  const bf16_t* Qg = a.qkv + tok0 * ld + (long)hd * D;
+  const bf16_t* Kg = Qg + a.M;
+  const bf16_t* Vg = Qg + 2L * a.M;
+  const bf16_t* Gg = a.d_o + tok0 * a.M + (long)hd * D;
+  const bf16_t* Og = a.o + tok0 * a.M + (long)hd * D;
+  const int q0 = qt * 128, qw = q0 + 32 * w + lq;
+  const bool live = qw < a.N;
+
+  bf16x8 qf[KS], gf[KS];
+  float dl = 0.0f;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    qf[ks] = live ? *reinterpret_cast<const bf16x8*>(Qg + qw * ld + 16 * ks + 8 * h2) : zero8();
+    gf[ks] = live ? *reinterpret_cast<const bf16x8*>(Gg + (long)qw * a.M + 16 * ks + 8 * h2) : zero8();
+    const bf16x8 ov = live ? *reinterpret_cast<const bf16x8*>(Og + (long)qw * a.M + 16 * ks + 8 * h2) : zero8();
+#pragma unroll
+    for (int t = 0; t < 8; ++t) dl += (float)gf[ks][t] * (float)ov[t];
+  }
+  dl += __shfl_xor(dl, 32);
+  const long srow = (long)hd * a.T + tok0 + qw;
+  if (live && h2 == 0) a.delta[srow] = dl;
+  const float l2 = live ? a.lse[srow] * kLog2e : 0.0f;
+  floatx16 dq[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) dq[db] = zero16();
+
+  const int kend = CAUSAL ? min(a.N, q0 + 128) : a.N;
+  const int nk = (kend + 63) / 64;
+  Tiles tl;
+  tl.load(Kg, Vg, ld, 0, a.N, tid);
+  tl.store(lds, lds + Tiles::TB, tid);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt & 1;
+    if (kt + 1 < nk) tl.load(Kg, Vg, ld, (kt + 1) * 64, a.N, tid);
+    const char* tk = lds + st * 2 * Tiles::TB;
+    const char* tv = tk + Tiles::TB;
+    const int kb0 = kt * 64;
+    if (!CAUSAL || kb0 <= q0 + 32 * w + 31) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        floatx16 s = zero16(), dp = zero16();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row<D>(tk, 32 * kb + lq, ks, h2), qf[ks], s);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) dp = mfma(frag_row<D>(tv, 32 * kb + lq, ks, h2), gf[ks], dp);
+        const bool edge = kb0 + 32 * kb + 32 > a.N || (CAUSAL && kb0 + 32 * kb + 31 > q0 + 32 * w);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pv = exp2_fast(s[r] * a.c2 - l2);
+          if (edge) {
+            const int key = kb0 + 32 * kb + 8 * (r >> 2) + 4 * h2 + (r & 3);
+            if (key >= a.N || (CAUSAL && key > qw)) pv = 0.0f;
+          }
+          s[r] = pv * (dp[r] - dl);  // dS^T
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const bf16x8 pb = pfrag(s, s2);
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+            dq[db] = mfma(frag_tr<D>(tk, 32 * kb + 16 * s2, 32 * db, lane), pb, dq[db]);
+        }
+      }
+    }
+    if (kt + 1 < nk) {
+      char* nk_ = lds + (st ^ 1) * 2 * Tiles::TB;
+      tl.store(nk_, nk_ + Tiles::TB, tid);
+    }
+    __syncthreads();
+  }
+  if (live) {
+    bf16_t* dst = a.d_qkv + (tok0 + qw) * ld + (long)hd * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) store_cols(dst + 32 * db, dq[db], h2, a.rs);
+  }
+}
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(256, 1) void attn_dkdv_kernel(AttnArgs a) {
+  constexpr int KS = D / 16, DB = D / 32, CPR = D / 8;
+  constexpr int TQ = 32 * D * 2;                // one 32-row tile
+  constexpr int STG = 2 * TQ + 256;             // Q, dO, then 32 lse2 and 32 delta
+  constexpr int LD = 32 * CPR / 256;            // chunks per thread per tile
+  __shared__ __attribute__((aligned(16))) char lds[2 * STG];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
+  int kt, hd, sq;
+  decode(a, false, kt, hd, sq);
+  const long tok0 = (long)sq * a.N, ld = 3L * a.M;
+  const bf16_t* Qg = a.qkv + tok0 * ld + (long)hd * D;
+  const bf16_t* Gg = a.d_o + tok0 * a.M + (long)hd * D;
+  const long srow0 = (long)hd * a.T + tok0;
+  const int k0 = kt * 128, kw = k0 + 32 * w + lq;
+  const bool live = kw < a.N;
+
+  bf16x8 kf[KS], vf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kf[ks] = live ? *reinterpret_cast<const bf16x8*>(Qg + a.M + kw * ld + 16 * ks + 8 * h2) : zero8();
+    vf[ks] = live ? *reinterpret_cast<const bf16x8*>(Qg + 2L * a.M + kw * ld + 16 * ks + 8 * h2) : zero8();
+  }
+  floatx16 dv[DB], dk[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    dv[db] = zero16();
+    dk[db] = zero16();
+  }
+  // query steps of 32: causal keys k0.. are seen by queries >= k0 only
+  const int qs0 = CAUSAL ? k0 : 0;
+  const int nqs = (a.N - qs0 + 31) / 32;
+  u32x4 rq[LD], rg[LD];
+  float rstat = 0.0f;
+  auto load = [&](int qb) {
+#pragma unroll
+    for (int u = 0; u < LD; ++u) {
+      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, q = qb + r;
+      if (q < a.N) {
+        rq[u] = *reinterpret_cast<const u32x4*>(Qg + q * ld + 8 * c);
+        rg[u] = *reinterpret_cast<const u32x4*>(Gg + (long)q * a.M + 8 * c);
+      } else {
+        rq[u] = u32x4{0, 0, 0, 0};
+        rg[u] = u32x4{0, 0, 0, 0};
+      }
+    }
+    if (tid < 64) {
+      const int q = qb + (tid & 31);
+      rstat = q < a.N ? (tid < 32 ? a.lse[srow0 + q] * kLog2e : a.delta[srow0 + q]) : 0.0f;
+    }
+  };
+  auto store = [&](char* stg) {
+#pragma unroll
+    for (int u = 0; u < LD; ++u) {
+      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR;
+      *reinterpret_cast<u32x4*>(stg + toff<D>(r, c)) = rq[u];
+      *reinterpret_cast<u32x4*>(stg + TQ + toff<D>(r, c)) = rg[u];
+    }
+    if (tid < 64) reinterpret_cast<float*>(stg + 2 * TQ)[tid] = rstat;
+  };
+  if (nqs > 0) {
+    load(qs0);
+    store(lds);
+  }
+  __syncthreads();
+  for (int it = 0; it < nqs; ++it) {
+    const int st = it & 1, qb = qs0 + 32 * it;
+    if (it + 1 < nqs) load(qb + 32);
+    const char* tq = lds + st * STG;
+    const char* tg = tq + TQ;
+    const float* l2 = reinterpret_cast<const float*>(tq + 2 * TQ);
+    const float* dls = l2 + 32;
+    if (!CAUSAL || qb + 31 >= k0 + 32 * w) {
+      floatx16 s = zero16(), dp = zero16();
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row<D>(tq, lq, ks, h2), kf[ks], s);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) dp = mfma(frag_row<D>(tg, lq, ks, h2), vf[ks], dp);
+      const bool edge = qb + 32 > a.N || (CAUSAL && k0 + 32 * w + 31 > qb);
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        const float4 lv = *reinterpret_cast<const float4*>(l2 + 8 * J + 4 * h2);
+        const float4 dv4 = *reinterpret_cast<const float4*>(dls + 8 * J + 4 * h2);
+        const float lr[4] = {lv.x, lv.y, lv.z, lv.w}, dr[4] = {dv4.x, dv4.y, dv4.z, dv4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = 4 * J + j;
+          float pv = exp2_fast(s[r] * a.c2 - lr[j]);
+          if (edge) {
+            const int q = qb + 8 * J + 4 * h2 + j;
+            if (q >= a.N || (CAUSAL && kw > q)) pv = 0.0f;
+          }
+          s[r] = pv;
+          dp[r] = pv * (dp[r] - dr[j]);  // dS
+        }
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const bf16x8 pb = pfrag(s, s2), pd = pfrag(dp, s2);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          dv[db] = mfma(frag_tr<D>(tg, 16 * s2, 32 * db, lane), pb, dv[db]);
+          dk[db] = mfma(frag_tr<D>(tq, 16 * s2, 32 * db, lane), pd, dk[db]);
+        }
+      }
+    }
+    if (it + 1 < nqs) store(lds + (st ^ 1) * STG);
+    __syncthreads();
+  }
+  if (live) {
+    bf16_t* dst = a.d_qkv + (tok0 + kw) * ld + (long)hd * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      store_cols(dst + a.M + 32 * db, dk[db], h2, a.rs);
+      store_cols(dst + 2L * a.M + 32 * db, dv[db], h2, 1.0f);
+    }
+  }
+}
+
+AttnArgs attn_args(const AttnShape& m, int T, int M) {
+  AttnArgs a = {};
+  a.T = T;
+  a.M = M;
+  a.N = m.N;
+  a.heads = m.heads;
+  a.nseq = m.N > 0 ? T / m.N : 0;
+  a.c2 = kLog2e / sqrtf((float)m.D);
+  a.rs = 1.0f / sqrtf((float)m.D);
+  return a;
+}
+
+unsigned attn_blocks(const AttnArgs& a) { return (unsigned)(((a.N + 127) / 128) * a.heads * a.nseq); }
+
+#define FLOWMOE_ATTN_LAUNCH(KERNEL, a, st)                                                     \
+  do {                                                                                          \
+    const dim3 g(attn_blocks(a)), b(256);                                                       \
+    if (m.D == 128) {                                                                           \
+      if (m.causal) hipLaunchKernelGGL((KERNEL<128, true>), g, b, 0, st, a);                    \
+      else hipLaunchKernelGGL((KERNEL<128, false>), g, b, 0, st, a);                            \
+    } else {                                                                                    \
+      if (m.causal) hipLaunchKernelGGL((KERNEL<64, true>), g, b, 0, st, a);                     \
+      else hipLaunchKernelGGL((KERNEL<64, false>), g, b, 0, st, a);                             \
+    }                                                                                           \
+  } while (0)
+
+}  // namespace
+
+hipError_t launch_attn_fwd(const AttnShape& m, int T, int M, const void* qkv, void* o, float* lse,
+                           hipStream_t st) {
+  AttnArgs a = attn_args(m, T, M);
+  if (attn_blocks(a) == 0) return hipSuccess;
+  a.qkv = static_cast<const bf16_t*>(qkv);
+  a.out = static_cast<bf16_t*>(o);
+  a.lse = lse;
+  return traced(FLOWMOE_K_ATTN_FWD, st, [&] { FLOWMOE_ATTN_LAUNCH(attn_fwd_kernel, a, st); });
+}
+
+hipError_t launch_attn_bwd(const AttnShape& m, int T, int M, const void* qkv, const void* o,
+                           const float* lse, const void* d_o, void* d_qkv, float* delta,
+                           hipStream_t st) {
+  AttnArgs a = attn_args(m, T, M);
+  if (attn_blocks(a) == 0) return hipSuccess;
+  a.qkv = static_cast<const bf16_t*>(qkv);
+  a.o = static_cast<const bf16_t*>(o);
+  a.d_o = static_cast<const bf16_t*>(d_o);
+  a.d_qkv = static_cast<bf16_t*>(d_qkv);
+  a.lse = const_cast<float*>(lse);
+  a.delta = delta;
+  hipError_t e = traced(FLOWMOE_K_ATTN_BWD_DQ, st, [&] { FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st); });
+  if (e != hipSuccess) return e;
+  return traced(FLOWMOE_K_ATTN_BWD_DKDV, st, [&] { FLOWMOE_ATTN_LAUNCH(attn_dkdv_kernel, a, st); });
+}
+
+hipError_t launch_mha_fwd(const AttnShape& m, int T, int M, const void* in, const void* w_qkv,
+                          const void* w_o, void* qkv, void* attn, float* lse, void* out,
+                          hipStream_t st) {
+  if (T == 0) return hipSuccess;
+  hipError_t e = launch_dense_gemm(FLOWMOE_K_ATTN_QKV, T, in, M, M, w_qkv, 3L * M, false, 3 * M,
+                                   qkv, 3L * M, st);
+  if (e != hipSuccess) return e;
+  e = launch_attn_fwd(m, T, M, qkv, attn, lse, st);
+  if (e != hipSuccess) return e;
+  return launch_dense_gemm(FLOWMOE_K_ATTN_OUT, T, attn, M, M, w_o, M, false, M, out, M, st);
+}
+
+hipError_t launch_mha_bwd_data(const AttnShape& m, int T, int M, const void* w_qkv,
+                               const void* w_o, const void* qkv, const void* attn,
+                               const float* lse, const void* d_out, void* d_attn, void* d_qkv,
+                               float* delta, void* d_in, hipStream_t st) {
+  if (T == 0) return hipSuccess;
+  // d_attn = d_out W^O^T: B[k][n] = W^O[n][k] (K-contiguous)
+  hipError_t e = launch_dense_gemm(FLOWMOE_K_ATTN_DGRAD, T, d_out, M, M, w_o, M, true, M, d_attn,
+                                   M, st);
+  if (e != hipSuccess) return e;
+  e = launch_attn_bwd(m, T, M, qkv, attn, lse, d_attn, d_qkv, delta, st);
+  if (e != hipSuccess) return e;
+  // d_in = d_qkv [W^Q | W^K | W^V]^T: B[k][n] = W_qkv[n][k] (K-contiguous)
+  return launch_dense_gemm(FLOWMOE_K_ATTN_DGRAD, T, d_qkv, 3L * M, 3 * M, w_qkv, 3L * M, true, M,
+                           d_in, M, st);
+}
+
+hipError_t launch_mha_wgrad(int T, int M, int R, const void* in, const void* attn,
+                            const void* d_out, const void* d_qkv, float* dw_qkv, float* dw_o,
+                            int accumulate, hipStream_t st) {
+  // dW^O = attn^T d_out and dW_qkv = in^T d_qkv, each summed over the R
+  // chunks' rows in chunk order
+  hipError_t e = launch_dense_wgrad(FLOWMOE_K_ATTN_WGRAD, T, R, attn, M, (long)T * M, M, d_out, M,
+                                    (long)T * M, M, dw_o, M, accumulate, st);
+  if (e != hipSuccess) return e;
+  return launch_dense_wgrad(FLOWMOE_K_ATTN_WGRAD, T, R, in, M, (long)T * M, M, d_qkv, 3L * M,
+                            (long)T * 3 * M, 3 * M, dw_qkv, 3L * M, accumulate, st);
+}
+
+}  // namespace flowmoe

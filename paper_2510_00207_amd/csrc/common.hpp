@@ -268,6 +268,43 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
                                  float* dw2, float* db1, float* db3, float* db2, int accumulate,
                                  void* ws, hipStream_t st);
 
+// Dense GEMMs on the grouped GEMM (one expert of `rows` rows, bf16):
+// C (rows x N, bf16, ldc) = A (rows x K, lda) B (K x N) with B[k][n] at
+// B + n * ldb + k (b_kc) or B + k * ldb + n
+hipError_t launch_dense_gemm(int kind, long rows, const void* A, long lda, int K, const void* B,
+                             long ldb, bool b_kc, int N, void* C, long ldc, hipStream_t st);
+// C (Mdim x N, fp32, ldc) = (or +=) the sum over nseg segments g, in order,
+// of A_g^T B_g (A_g = A + g * a_sstride: rows x Mdim; B_g: rows x N)
+hipError_t launch_dense_wgrad(int kind, long rows, int nseg, const void* A, long lda,
+                              long a_sstride, int Mdim, const void* B, long ldb, long b_sstride,
+                              int N, float* C, long ldc, int accumulate, hipStream_t st);
+
+// The attention of AT_r: T tokens = T / N sequences of N tokens, `heads`
+// heads of width D (64 or 128), M = heads * D, bf16
+struct AttnShape {
+  int N, heads, D, causal;
+};
+hipError_t launch_attn_fwd(const AttnShape& m, int T, int M, const void* qkv, void* o, float* lse,
+                           hipStream_t st);
+hipError_t launch_attn_bwd(const AttnShape& m, int T, int M, const void* qkv, const void* o,
+                           const float* lse, const void* d_o, void* d_qkv, float* delta,
+                           hipStream_t st);
+// projections + attention: qkv = in W_qkv, attention -> attn, out = attn W_o
+hipError_t launch_mha_fwd(const AttnShape& m, int T, int M, const void* in, const void* w_qkv,
+                          const void* w_o, void* qkv, void* attn, float* lse, void* out,
+                          hipStream_t st);
+// input side of the backward: d_attn = d_out W_o^T, the attention backward
+// (d_qkv, delta), d_in = d_qkv W_qkv^T
+hipError_t launch_mha_bwd_data(const AttnShape& m, int T, int M, const void* w_qkv,
+                               const void* w_o, const void* qkv, const void* attn,
+                               const float* lse, const void* d_out, void* d_attn, void* d_qkv,
+                               float* delta, void* d_in, hipStream_t st);
+// weight gradients over R chunks of T rows: dW_o = sum attn^T d_out,
+// dW_qkv = sum in^T d_qkv
+hipError_t launch_mha_wgrad(int T, int M, int R, const void* in, const void* attn,
+                            const void* d_out, const void* d_qkv, float* dw_qkv, float* dw_o,
+                            int accumulate, hipStream_t st);
+
 // Kernel tracing (flowmoe_trace_start): record a begin/end event around a
 // launch when the kind is selected. Defined in abi.hip.
 hipError_t trace_mark(int kind, bool end, hipStream_t st);

@@ -91,6 +91,16 @@ __device__ __forceinline__ int clip_rows(long off, int n, long cap) {
   return (int)min((long)n, cap - off);
 }
 
+// Expert e's rows in segment g: counts[g * E + e] rows from row
+// offsets[g * (E + 1) + e]. A dense launch (counts null, E = 1: the
+// attention's projections) has rows_cap rows from row 0 in every segment.
+__device__ __forceinline__ int seg_count(const GemmParams& p, int g, int e) {
+  return p.counts ? p.counts[g * p.E + e] : (int)p.rows_cap;
+}
+__device__ __forceinline__ int seg_offset(const GemmParams& p, int g, int e) {
+  return p.counts ? p.offsets[g * (p.E + 1) + e] : 0;
+}
+
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------
@@ -528,7 +538,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
     int acc_t = 0;
     mt = -1;
     for (e = 0; e < p.E; ++e) {
-      const int c = p.counts[e];
+      const int c = seg_count(p, 0, e);
       const int r = p.padC ? p.padC : c;
       const int te = (r + BM - 1) / BM;
       if (ml < acc_t + te) {
@@ -540,13 +550,13 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p) {
       acc_t += te;
     }
     if (mt < 0) return;
-    rows_e = clip_rows(p.offsets[e], rows_e, p.rows_cap);
-    cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
-    row0 = p.offsets[e] + mt * BM;  // first global row of this tile
+    rows_e = clip_rows(seg_offset(p, 0, e), rows_e, p.rows_cap);
+    cnt_e = clip_rows(seg_offset(p, 0, e), cnt_e, p.rows_cap);
+    row0 = seg_offset(p, 0, e) + mt * BM;  // first global row of this tile
   } else {
     ksum_tile(vbid, (p.Mdim + BM - 1) / BM, (p.N + BN - 1) / BN, e, mt, nt);
-    cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
-    row0 = p.offsets[e];
+    cnt_e = clip_rows(seg_offset(p, 0, e), seg_count(p, 0, e), p.rows_cap);
+    row0 = seg_offset(p, 0, e);
   }
   constexpr int NCOLS = (EPI == EPI_SWIGLU_FWD) ? BN / 2 : BN;  // distinct output columns per tile
   const int n0 = nt * NCOLS;
@@ -702,7 +712,7 @@ __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, 
   // the experts' counts in one vector load (lane x: expert x, E <= 64), then
   // walked in scalar registers (no memory round trip per expert)
   const int lane = threadIdx.x & 63;
-  const int cvec = lane < p.E ? p.counts[lane] : 0;
+  const int cvec = lane < p.E ? seg_count(p, 0, lane) : 0;
   auto tiles = [&](int x, int& c, int& r, int& te, int& he) {
     c = __builtin_amdgcn_readlane(cvec, x);
     r = p.padC ? p.padC : c;
@@ -859,16 +869,16 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
   if constexpr (MODE == MODE_ROWS) {
     if (!row_tile_of_block<BM>(p, blockIdx.x, e, mt, nt, rows_e, cnt_e)) return;
-    rows_e = clip_rows(p.offsets[e], rows_e, p.rows_cap);
-    cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
-    row0 = p.offsets[e] + mt * BM;
+    rows_e = clip_rows(seg_offset(p, 0, e), rows_e, p.rows_cap);
+    cnt_e = clip_rows(seg_offset(p, 0, e), cnt_e, p.rows_cap);
+    row0 = seg_offset(p, 0, e) + mt * BM;
   } else {
     // expert e's mtn x ntn tiles, walked in shared 16 x 16 blocks
     const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
     e = blockIdx.x / (mtn * ntn);
     shared_block_tile(blockIdx.x - e * (mtn * ntn), mtn, ntn, mt, nt);
-    cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
-    row0 = p.offsets[e];
+    cnt_e = clip_rows(seg_offset(p, 0, e), seg_count(p, 0, e), p.rows_cap);
+    row0 = seg_offset(p, 0, e);
   }
   constexpr int NCOLS = DUAL ? BN / 2 : BN;
   const int n0 = nt * NCOLS;
@@ -946,8 +956,8 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   // g-th chunk's buffers (same per-lane offsets and k steps)
   auto bind_segment = [&](int g) {
     if constexpr (MODE == MODE_KSUM) {
-      row0 = p.offsets[g * (p.E + 1) + e];
-      cnt_e = clip_rows(row0, p.counts[g * p.E + e], p.rows_cap);
+      row0 = seg_offset(p, g, e);
+      cnt_e = clip_rows(row0, seg_count(p, g, e), p.rows_cap);
       const bf16_t* Ag = A + g * p.a_sstride;
       const bf16_t* Bg = B0 + g * p.b_sstride;
       const int m0 = mt * BM;
@@ -1175,7 +1185,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
     int acc_t = 0;
     mt = -1;
     for (e = 0; e < p.E; ++e) {
-      const int c = p.counts[e];
+      const int c = seg_count(p, 0, e);
       const int r = p.padC ? p.padC : c;
       const int te = (r + TB - 1) / TB;
       if (ml < acc_t + te) {
@@ -1187,17 +1197,17 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
       acc_t += te;
     }
     if (mt < 0) return;
-    rows_e = clip_rows(p.offsets[e], rows_e, p.rows_cap);
-    cnt_e = clip_rows(p.offsets[e], cnt_e, p.rows_cap);
-    row0 = p.offsets[e] + mt * TB;
+    rows_e = clip_rows(seg_offset(p, 0, e), rows_e, p.rows_cap);
+    cnt_e = clip_rows(seg_offset(p, 0, e), cnt_e, p.rows_cap);
+    row0 = seg_offset(p, 0, e) + mt * TB;
   } else {
     const int mtn = (p.Mdim + TB - 1) / TB, ntn = (p.N + TB - 1) / TB;
     e = blockIdx.x / (mtn * ntn);
     const int rem = blockIdx.x % (mtn * ntn);
     mt = rem / ntn;
     nt = rem % ntn;
-    cnt_e = clip_rows(p.offsets[e], p.counts[e], p.rows_cap);
-    row0 = p.offsets[e];
+    cnt_e = clip_rows(seg_offset(p, 0, e), seg_count(p, 0, e), p.rows_cap);
+    row0 = seg_offset(p, 0, e);
   }
   const int n0 = nt * TB;
   const float* A = static_cast<const float*>(p.A);
@@ -1209,8 +1219,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
   const int nseg = (MODE == MODE_KSUM) ? p.nseg : 1;
   for (int g = 0; g < nseg; ++g) {
     if (g > 0) {
-      row0 = p.offsets[g * (p.E + 1) + e];
-      cnt_e = clip_rows(row0, p.counts[g * p.E + e], p.rows_cap);
+      row0 = seg_offset(p, g, e);
+      cnt_e = clip_rows(row0, seg_count(p, g, e), p.rows_cap);
       A = static_cast<const float*>(p.A) + g * p.a_sstride;
       B0 = static_cast<const float*>(p.B0) + g * p.b_sstride;
     }
@@ -1556,6 +1566,61 @@ hipError_t launch_gate_dx_gemm(const void* dlhl, int T, int K, const void* wstac
   if (add)
     return run_gemm_bf16<MODE_ROWS, true, false, EPI_ADD>(FLOWMOE_K_GATE_BWD_TOKEN, s2, p, st);
   return run_gemm_bf16<MODE_ROWS, true, false, EPI_STORE>(FLOWMOE_K_GATE_BWD_TOKEN, s2, p, st);
+}
+
+hipError_t launch_dense_gemm(int kind, long rows, const void* A, long lda, int K, const void* B,
+                             long ldb, bool b_kc, int N, void* C, long ldc, hipStream_t st) {
+  if (rows == 0 || N == 0) return hipSuccess;
+  Shape s2 = {};
+  s2.T = (int)rows;
+  s2.E = 1;
+  s2.rows = rows;
+  s2.layout = FLOWMOE_PACKED;
+  GemmParams p = {};
+  p.E = 1;  // (counts null: one expert of rows_cap rows)
+  p.A = A;
+  p.lda = lda;
+  p.K = K;
+  p.B0 = B;
+  p.ldb = ldb;
+  p.N = N;
+  p.C0 = C;
+  p.ldc = ldc;
+  p.ksplit = 1 << 30;
+  p.nsplit = 1 << 30;
+  p.nseg = 1;
+  p.rows_cap = rows;
+  if (b_kc) return run_gemm_bf16<MODE_ROWS, true, true, EPI_STORE>(kind, s2, p, st);
+  return run_gemm_bf16<MODE_ROWS, true, false, EPI_STORE>(kind, s2, p, st);
+}
+
+hipError_t launch_dense_wgrad(int kind, long rows, int nseg, const void* A, long lda,
+                              long a_sstride, int Mdim, const void* B, long ldb, long b_sstride,
+                              int N, float* C, long ldc, int accumulate, hipStream_t st) {
+  Shape s2 = {};
+  s2.T = (int)rows;
+  s2.E = 1;
+  s2.rows = rows;
+  s2.layout = FLOWMOE_PACKED;
+  GemmParams p = {};
+  p.E = 1;
+  p.A = A;
+  p.lda = lda;
+  p.Mdim = Mdim;
+  p.B0 = B;
+  p.ldb = ldb;
+  p.N = N;
+  p.C0 = C;
+  p.C1 = C;
+  p.ldc = ldc;
+  p.ksplit = 1 << 30;
+  p.nsplit = 1 << 30;
+  p.accumulate = accumulate;
+  p.nseg = nseg;
+  p.a_sstride = a_sstride;
+  p.b_sstride = b_sstride;
+  p.rows_cap = rows;
+  return run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(kind, s2, p, st);
 }
 
 size_t ffn_bwd_ws_bytes(const Shape& s) {

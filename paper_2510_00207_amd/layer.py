@@ -19,13 +19,16 @@ class MoELayer:
     Parameters and inputs (w_gate, bias, w1, w3, w2, the experts' biases b1,
     b3, b2 when expert_bias, x, dy) are attributes the caller fills (or
     replaces with tensors of the same shape and dtype); everything else is
-    allocated here.
+    allocated here. ``mha`` (dict seq_len, head_dim, causal): AT_r includes
+    the block's attention; then mha_in, w_qkv and w_o are the caller's inputs
+    and x is the attention output the forward writes.
     """
 
     def __init__(self, *, T_total: int, M: int, H: int, E: int, k: int, R: int = 1,
                  f: float | None = None, C: int | None = None, act: str = "gelu",
                  dtype: str = "bf16", layout: str = "packed", bias: bool = False,
-                 gate: str = "renorm", expert_bias: bool = False, device="cuda"):
+                 gate: str = "renorm", expert_bias: bool = False, mha: dict | None = None,
+                 device="cuda"):
         if T_total % R:
             raise ValueError("T_total must be a multiple of R")
         T = T_total // R
@@ -91,6 +94,28 @@ class MoELayer:
         self.db1 = z(E, H, dtype=f32) if expert_bias else None
         self.db3 = z(E, H, dtype=f32) if expert_bias and sw else None
         self.db2 = z(E, M, dtype=f32) if expert_bias else None
+        # the attention part of AT_r
+        if mha is not None:
+            hd = mha["head_dim"]
+            heads = M // hd
+            self.mha = L.make_mha_shape(mha["seq_len"], heads, hd, mha.get("causal", True))
+            self.mha_in = z(T_total, M)
+            self.w_qkv = z(M, 3 * M)
+            self.w_o = z(M, M)
+            self.qkv = z(T_total, 3 * M)
+            self.attn = z(T_total, M)
+            self.lse = z(R, heads, T, dtype=f32)
+            self.d_attn = z(T_total, M)
+            self.d_qkv = z(T_total, 3 * M)
+            self.delta = z(R, heads, T, dtype=f32)
+            self.d_in = z(T_total, M)
+            self.dw_qkv = z(M, 3 * M, dtype=f32)
+            self.dw_o = z(M, M, dtype=f32)
+        else:
+            self.mha = None
+            for n in ("mha_in", "w_qkv", "w_o", "qkv", "attn", "lse", "d_attn", "d_qkv", "delta",
+                      "d_in", "dw_qkv", "dw_o"):
+                setattr(self, n, None)
         self.ws_bytes = L.flowmoe_workspace_bytes(self.shape, L.WS_LAYER_BWD)
         self.ws = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
 

@@ -146,7 +146,8 @@ def test_dispatch_workspace_checked(flowmoe_lib):
     assert ei.value.status == L.ERR_WORKSPACE and "flowmoe_dispatch" in str(ei.value)
     b = L.LayerBufs()
     for name in L._LAYER_FIELDS:
-        setattr(b, name, FAKE)
+        if name != "mha":  # (a host struct: None = no attention)
+            setattr(b, name, FAKE)
     b.ws_bytes = need - 256
     with pytest.raises(L.FlowMoEError) as ei:
         L.flowmoe_layer_fwd(s, 1, b, s_compute=0, s_comm=0)
@@ -223,3 +224,64 @@ def test_row_streams_setting(flowmoe_lib):
     raw.flowmoe_set_row_streams.argtypes = [ctypes.c_int32]
     assert raw.flowmoe_set_row_streams(3) == L.ERR_INVALID
     assert raw.flowmoe_set_row_streams(-1) == L.ERR_INVALID
+
+
+# ---------------------------------------------------------------------------
+# the attention part of AT_r
+# ---------------------------------------------------------------------------
+def test_mha_validation(flowmoe_lib):
+    s = L.make_shape(1024, 1024, 64, 4, 2, 8, L.BF16)
+    m = L.make_mha_shape(512, 16, 64, True)
+    cases = [
+        (L.make_shape(1024, 1024, 64, 4, 2, 8, L.F32), m, L.ERR_UNSUPPORTED, "BF16"),
+        (s, L.make_mha_shape(512, 8, 96, True), L.ERR_UNSUPPORTED, "head_dim"),
+        (s, L.make_mha_shape(512, 8, 64, True), L.ERR_INVALID, "heads * head_dim"),
+        (s, L.make_mha_shape(384, 16, 64, True), L.ERR_INVALID, "whole number of sequences"),
+        (s, L.make_mha_shape(0, 16, 64, True), L.ERR_INVALID, "seq_len"),
+        (s, L.MhaShape(512, 16, 64, 2), L.ERR_INVALID, "causal"),
+    ]
+    for shape, mha, status, text in cases:
+        for call in (lambda: L.flowmoe_attention_fwd(shape, mha, FAKE, FAKE, FAKE, stream=0),
+                     lambda: L.flowmoe_mha_fwd(shape, mha, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                               stream=0),
+                     lambda: L.flowmoe_mha_bwd(shape, mha, *([FAKE] * 13), 0, stream=0)):
+            with pytest.raises(L.FlowMoEError) as ei:
+                call()
+            assert ei.value.status == status and text in str(ei.value), str(ei.value)
+    # null and misaligned tensors
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_attention_fwd(s, m, FAKE, None, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "attn is null" in str(ei.value)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_attention_bwd(s, m, FAKE, FAKE, FAKE + 2, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "lse is not 4-byte aligned" in str(ei.value)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_mha_fwd(s, m, FAKE, FAKE + 8, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == L.ERR_INVALID and "w_qkv is not 16-byte aligned" in str(ei.value)
+    # no tokens: nothing to do, no tensor needed (the backward's weight gradients still are)
+    s0 = L.make_shape(0, 1024, 64, 4, 2, 8, L.BF16)
+    L.flowmoe_attention_fwd(s0, m, None, None, None, stream=0)
+    L.flowmoe_mha_fwd(s0, m, None, None, None, None, None, None, None, stream=0)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_mha_bwd(s0, m, *([None] * 13), 0, stream=0)
+    assert "dw_qkv is null" in str(ei.value)
+
+
+def test_layer_mha_validation(flowmoe_lib):
+    # the layer's chunk must hold whole sequences; its attention buffers are checked
+    s = L.make_shape(768, 256, 64, 4, 2, 8, L.BF16)
+    base = {n: FAKE for n in L._LAYER_FIELDS if n not in ("mha", "bias", "load", "w3", "dw3", "b1",
+                                                             "b3", "b2", "db1", "db3", "db2", "dbias")}
+    need = L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD)
+    b = L.layer_bufs(ws_bytes=need, mha=L.make_mha_shape(512, 4, 64, True), **base)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_layer_fwd(s, 2, b, s_compute=0, s_comm=0)
+    assert "whole number of sequences" in str(ei.value)
+    bad = dict(base, delta=None)
+    b = L.layer_bufs(ws_bytes=need, mha=L.make_mha_shape(256, 4, 64, True), **bad)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_layer_bwd(s, 2, b, s_compute=0, s_comm=0)
+    assert "bufs->delta is null" in str(ei.value)
+    with pytest.raises(ValueError):  # the binding checks the trace length first
+        L.flowmoe_layer_bwd(s, 2, b, s_compute=0, s_comm=0, trace=[0] * (8 * 2 + 2))
+    assert L.bwd_trace_len(2, True) == 24 and L.bwd_trace_len(2, False) == 18
