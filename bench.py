@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--R", type=int, default=None, help="override the chunk count")
     ap.add_argument("--expert-bias", action="store_true",
                     help="biased experts (b1, b3 on the first layer, b2 on the second)")
+    ap.add_argument("--mha", action="store_true",
+                    help="AT_r includes the block's multi-head attention (the workload's "
+                         "sequences and heads): one step is attention + MoE layer, fwd + bwd")
     for dim, typ in (("T", int), ("M", int), ("H", int), ("E", int), ("k", int), ("f", float)):
         ap.add_argument(f"--{dim}", type=typ, default=None, help=f"override the workload's {dim}")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
@@ -79,6 +82,22 @@ def gemm_flops_per_step(cfg, kept: int) -> float:
     return (18.0 if cfg.act == "swiglu" else 12.0) * kept * cfg.M * cfg.H
 
 
+def attention_flops(cfg, R: int) -> dict:
+    """Algorithmic FLOPs of the attention part of one step (all R chunks):
+    the core per (sequence, head) is 2 d FLOPs per visible (query, key) pair
+    for each of Q K^T and P V forward, and for each of the backward's five
+    products (S recomputed, dP, dV, dK, dQ): N^2 pairs, or N (N + 1) / 2 when
+    causal; the projections: [Q|K|V] = I W_qkv (2 T M 3M), I' = A W^O
+    (2 T M^2), their two dgrads and two weight gradients (the same again
+    each)."""
+    T, M, N, d = cfg.T, cfg.M, cfg.seq_len, cfg.head_dim
+    pairs = N * (N + 1) / 2 if cfg.causal else float(N * N)
+    units = pairs * d * 2.0 * cfg.heads * (T // N)
+    proj = 2.0 * T * M * 4 * M
+    return {"core_fwd": 2 * units, "core_bwd": 5 * units, "proj_fwd": proj,
+            "proj_dgrad": proj, "proj_wgrad": proj}
+
+
 def oracle_sample_tokens(cfg, R: int) -> int:
     """Tokens of the CPU oracle's sample: the whole batch when one fp64 step
     is cheap, else the largest power-of-two number of tokens (a multiple of
@@ -92,7 +111,7 @@ def oracle_sample_tokens(cfg, R: int) -> int:
     return max(R, (t // R) * R)
 
 
-def schedule_overlap(layer, R, sc, sm, torch):
+def schedule_overlap(layer, R, sc, sm, torch, mha=False):
     """One untraced-throughput step with the layer's task events (the trace
     of flowmoe_layer_fwd / flowmoe_layer_bwd: start and end of every task of
     every chunk, on the stream it runs on): each pass's span, the time each
@@ -100,14 +119,17 @@ def schedule_overlap(layer, R, sc, sm, torch):
     (the overlap the two-stream schedule of Eqs. 3-6 achieves on one GPU).
     Forward: compute stream = gating, experts; comm stream = dispatch,
     combine. Backward: compute stream = experts bwd and the weight
-    gradients; comm stream = combine bwd, gate gradients, dispatch bwd."""
+    gradients (and with the attention, its backward per chunk and its
+    weight gradients); comm stream = combine bwd, gate gradients, dispatch
+    bwd."""
+    from paper_2510_00207_amd import _lib as L
     def events(n):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
         for e in ev:  # (torch creates an event's handle at its first record)
             e.record(sc)
         return ev
 
-    fwd, bwd, (t0,) = events(8 * R), events(8 * R + 2), events(1)
+    fwd, bwd, (t0,) = events(8 * R), events(L.bwd_trace_len(R, mha)), events(1)
     torch.cuda.synchronize()
     t0.record(sc)
     layer.forward(sc, sm, trace=fwd)
@@ -120,6 +142,12 @@ def schedule_overlap(layer, R, sc, sm, torch):
             for r in range(1 if task == 4 else R):
                 i = 2 * (task * R + r)
                 spans[(task, r)] = (t0.elapsed_time(ev[i]), t0.elapsed_time(ev[i + 1]))
+        if label == "bwd" and mha:  # (task 5: attention backward per chunk, 6: its wgrad)
+            for r in range(R):
+                i = 8 * R + 2 + 2 * r
+                spans[(5, r)] = (t0.elapsed_time(ev[i]), t0.elapsed_time(ev[i + 1]))
+            spans[(6, 0)] = (t0.elapsed_time(ev[10 * R + 2]), t0.elapsed_time(ev[10 * R + 3]))
+            comp = comp + (5, 6)
         c = [v for (task, _), v in spans.items() if task in comp]
         m = [v for (task, _), v in spans.items() if task not in comp]
         # the tasks of one stream never overlap each other (stream order)
@@ -258,15 +286,18 @@ def main():
     dev = torch.device("cuda:0")
 
     over = {d: getattr(a, d) for d in ("T", "M", "H", "E", "k", "f") if getattr(a, d) is not None}
-    cfg = get_config(a.workload, gate=a.gate, expert_bias=a.expert_bias, **over)
+    cfg = get_config(a.workload, gate=a.gate, expert_bias=a.expert_bias, mha=a.mha, **over)
     if over:  # another shape: named apart (no counter summary of the workload applies to it)
         cfg = cfg.replace(name=cfg.name + "(" + " ".join(f"{d}={v}" for d, v in over.items()) + ")")
     R = cfg.R if a.R is None else a.R
     inp = make_inputs(cfg)
     layer = MoELayer(T_total=cfg.T, M=cfg.M, H=cfg.H, E=cfg.E, k=cfg.k, R=R, f=cfg.f, act=cfg.act,
                      dtype=cfg.dtype, layout=a.layout, bias=cfg.zipf_bias, gate=cfg.gate,
-                     expert_bias=cfg.expert_bias, device=dev)
-    for name in ("x", "w_gate", "w1", "w3", "w2", "dy"):
+                     expert_bias=cfg.expert_bias,
+                     mha=(dict(seq_len=cfg.seq_len, head_dim=cfg.head_dim, causal=cfg.causal)
+                          if cfg.mha else None), device=dev)
+    for name in ("x", "w_gate", "w1", "w3", "w2", "dy") + (("mha_in", "w_qkv", "w_o")
+                                                           if cfg.mha else ()):
         if inp[name] is not None:
             getattr(layer, name).copy_(to_torch(inp[name], dev))
     for name in ("b1", "b3", "b2"):  # the experts' biases (fp32)
@@ -337,7 +368,43 @@ def main():
         per_kernel.setdefault(nm, []).append(all_ev.elapsed_ms(i) * 1e3)
     all_ev.close()
     breakdown = {k: round(float(sum(v)), 2) for k, v in per_kernel.items()}  # us per step
-    sched = schedule_overlap(layer, R, sc, sm, torch)
+    sched = schedule_overlap(layer, R, sc, sm, torch, cfg.mha)
+
+    # the attention of AT_r: its kernels' durations over the K steps (HIP
+    # events around each launch, a pass of its own) against their
+    # algorithmic FLOPs
+    attention = None
+    if cfg.mha:
+        akinds = ("attn_fwd", "attn_bwd_dq", "attn_bwd_dkdv", "attn_qkv", "attn_out",
+                  "attn_dgrad", "attn_wgrad")
+        aev = EventArray((7 * R + 2) * a.steps)
+        L.flowmoe_trace_start(aev.ev, aev.kinds, aev.pairs, L.kind_mask(akinds))
+        for i in range(a.steps):
+            step()
+        torch.cuda.synchronize()
+        na = L.flowmoe_trace_stop()
+        per = {}
+        for i in range(na):
+            per.setdefault(L.K_NAMES[aev.kinds[i]], []).append(aev.elapsed_ms(i))
+        aev.close()
+        af = attention_flops(cfg, R)
+        ms = lambda *ks: sum(sum(per.get(k_, [])) for k_ in ks) / a.steps  # ms per step
+        def rate(flops, t_ms):
+            tf = flops / (t_ms * 1e-3) / 1e12 if t_ms > 0 else 0.0
+            return {"ms_per_step": round(t_ms, 4), "TFLOPs": round(tf, 1),
+                    "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+        attention = {
+            "shape": (f"{cfg.T // cfg.seq_len} sequences x {cfg.seq_len} tokens, {cfg.heads} "
+                      f"heads of {cfg.head_dim}, {'causal' if cfg.causal else 'bidirectional'}"),
+            "flops_per_step": af,
+            "core_fwd": rate(af["core_fwd"], ms("attn_fwd")),
+            "core_bwd": rate(af["core_bwd"], ms("attn_bwd_dq", "attn_bwd_dkdv")),
+            "core_bwd_dq_ms": round(ms("attn_bwd_dq"), 4),
+            "core_bwd_dkdv_ms": round(ms("attn_bwd_dkdv"), 4),
+            "projections": rate(af["proj_fwd"] + af["proj_dgrad"] + af["proj_wgrad"],
+                                ms("attn_qkv", "attn_out", "attn_dgrad", "attn_wgrad")),
+            "launch_timing": "HIP events around every attention launch of a separate pass",
+        }
 
     ms_per_step = elapsed / a.steps * 1e3
     tokens_per_s = cfg.T * a.steps / elapsed
@@ -396,7 +463,7 @@ def main():
             traffic_note = "kernel changed since the PMC summary was taken"
 
     cpu = None
-    if not a.no_cpu_baseline:
+    if not a.no_cpu_baseline and not cfg.mha:  # (the headline line is the MoE layer's)
         import oracle
         from threadpoolctl import threadpool_info
         # a bounded sample of the same workload: the first Ts tokens, R
@@ -453,7 +520,8 @@ def main():
                          f"top-{cfg.k} f={cfg.f} {cfg.act} {cfg.dtype}, R={R}, {a.layout}, "
                          f"{streams}"
                          f"{', full-softmax gate' if cfg.gate == 'full' else ''}"
-                         f"{', biased experts' if cfg.expert_bias else ''}"),
+                         f"{', biased experts' if cfg.expert_bias else ''}"
+                         f"{'; AT_r with attention: ' + attention['shape'] if attention else ''}"),
             "T": cfg.T, "M": cfg.M, "H": cfg.H, "E": cfg.E, "k": cfg.k, "f": cfg.f,
             "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "gate": cfg.gate, "tiles": a.tiles,
             "expert_bias": cfg.expert_bias,
@@ -482,6 +550,7 @@ def main():
         "memory_bound": mem,
         "kernel_us_per_step": breakdown,
         "schedule": sched,
+        "attention": attention,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -81,7 +81,9 @@ enum {
   FLOWMOE_WS_DISPATCH = 0,
   FLOWMOE_WS_FFN_BWD = 1,
   FLOWMOE_WS_GATE_BWD = 2,
-  FLOWMOE_WS_LAYER_BWD = 3
+  FLOWMOE_WS_LAYER_BWD = 3,
+  FLOWMOE_WS_MHA_BWD = 4,      /* flowmoe_mha_bwd (depends on shape->M only) */
+  FLOWMOE_WS_LAYER_BWD_MHA = 5 /* flowmoe_layer_bwd with bufs->mha set */
 };
 
 /* ---- utilities ---------------------------------------------------------- */
@@ -388,13 +390,17 @@ flowmoe_status_t flowmoe_mha_fwd(const flowmoe_shape_t* shape, const flowmoe_mha
 /* MHA backward: d_attn = d_out W^O^T (T x M, out), the attention backward
  * (d_qkv T x 3M and delta heads x T, out), d_in = d_qkv [W^Q|W^K|W^V]^T
  * (T x M, out), dw_o = attn^T d_out (M x M float) and dw_qkv = in^T d_qkv
- * (M x 3M float), overwritten or, with accumulate, added to. */
+ * (M x 3M float), overwritten or, with accumulate, added to.
+ * ws: flowmoe_workspace_bytes(shape, FLOWMOE_WS_MHA_BWD) bytes (nullable
+ * when that is 0): when the weight gradients have few output tiles for the
+ * compute units (M <= 1024), their token rows are split into partial sums
+ * there, which are then added in split order. */
 flowmoe_status_t flowmoe_mha_bwd(const flowmoe_shape_t* shape, const flowmoe_mha_shape_t* mha,
                                  const void* in, const void* w_qkv, const void* w_o,
                                  const void* qkv, const void* attn, const float* lse,
                                  const void* d_out, void* d_attn, void* d_qkv, float* delta,
                                  void* d_in, float* dw_qkv, float* dw_o, int32_t accumulate,
-                                 hipStream_t stream);
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---- the R-chunk two-stream layer (Sec. 3.2, Eqs. 3-6) -------------------- */
 
@@ -459,7 +465,8 @@ typedef struct {
   float* dw_qkv;      /* M x 3M, summed over chunks */
   float* dw_o;        /* M x M, summed over chunks */
   /* scratch */
-  void* ws;           /* flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
+  void* ws;           /* flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD), or
+                         FLOWMOE_WS_LAYER_BWD_MHA with mha;
                          nullable in the forward, which uses it as the
                          dispatch workspace of each chunk in turn */
   size_t ws_bytes;

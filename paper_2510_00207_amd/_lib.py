@@ -20,7 +20,7 @@ F32, BF16 = 0, 1
 GELU, SWIGLU = 0, 1
 PACKED, PADDED = 0, 1
 GATE_RENORM, GATE_FULL = 0, 1
-WS_DISPATCH, WS_FFN_BWD, WS_GATE_BWD, WS_LAYER_BWD = 0, 1, 2, 3
+WS_DISPATCH, WS_FFN_BWD, WS_GATE_BWD, WS_LAYER_BWD, WS_MHA_BWD, WS_LAYER_BWD_MHA = 0, 1, 2, 3, 4, 5
 
 _STATUS = {1: "FLOWMOE_ERR_INVALID", 2: "FLOWMOE_ERR_UNSUPPORTED", 3: "FLOWMOE_ERR_HIP",
            4: "FLOWMOE_ERR_WORKSPACE"}
@@ -100,7 +100,7 @@ def load():
         "flowmoe_attention_fwd": ([SP, MP, P, P, P, P], I32),
         "flowmoe_attention_bwd": ([SP, MP, P, P, P, P, P, P, P], I32),
         "flowmoe_mha_fwd": ([SP, MP, P, P, P, P, P, P, P, P], I32),
-        "flowmoe_mha_bwd": ([SP, MP] + [P] * 13 + [I32, P], I32),
+        "flowmoe_mha_bwd": ([SP, MP] + [P] * 13 + [I32, P, SZ, P], I32),
         "flowmoe_layer_fwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
         "flowmoe_layer_bwd": ([SP, I32, ctypes.POINTER(LayerBufs), P, P, P], I32),
     }
@@ -256,11 +256,11 @@ def flowmoe_mha_fwd(shape, mha, inp, w_qkv, w_o, qkv, attn, lse, out, stream=Non
 
 
 def flowmoe_mha_bwd(shape, mha, inp, w_qkv, w_o, qkv, attn, lse, d_out, d_attn, d_qkv, delta, d_in,
-                    dw_qkv, dw_o, accumulate, stream=None):
+                    dw_qkv, dw_o, accumulate, ws=None, ws_bytes=0, stream=None):
     _check(load().flowmoe_mha_bwd(ctypes.byref(shape), ctypes.byref(mha), ptr(inp), ptr(w_qkv),
                                   ptr(w_o), ptr(qkv), ptr(attn), ptr(lse), ptr(d_out), ptr(d_attn),
                                   ptr(d_qkv), ptr(delta), ptr(d_in), ptr(dw_qkv), ptr(dw_o),
-                                  int(accumulate), _stream(stream)))
+                                  int(accumulate), ptr(ws), int(ws_bytes), _stream(stream)))
 
 
 # ---- kernel tracing --------------------------------------------------------------

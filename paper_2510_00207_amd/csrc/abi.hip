@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -269,6 +270,11 @@ size_t flowmoe_workspace_bytes(const flowmoe_shape_t* shape, int32_t kind) {
     case FLOWMOE_WS_LAYER_BWD: {  // the backward's gate partials; the forward's scan histograms
       const size_t bwd = gate_bwd_ws_bytes(s), fwd = dispatch_ws_bytes(s);
       return bwd > fwd ? bwd : fwd;
+    }
+    case FLOWMOE_WS_MHA_BWD: return mha_wgrad_ws_bytes(s.M);
+    case FLOWMOE_WS_LAYER_BWD_MHA: {  // (the attention's weight gradients run last)
+      const size_t bwd = gate_bwd_ws_bytes(s), fwd = dispatch_ws_bytes(s);
+      return std::max(std::max(bwd, fwd), mha_wgrad_ws_bytes(s.M));
     }
     default: return 0;
   }
@@ -652,7 +658,7 @@ flowmoe_status_t flowmoe_mha_bwd(const flowmoe_shape_t* shape, const flowmoe_mha
                                  const void* qkv, const void* attn, const float* lse,
                                  const void* d_out, void* d_attn, void* d_qkv, float* delta,
                                  void* d_in, float* dw_qkv, float* dw_o, int32_t accumulate,
-                                 hipStream_t stream) {
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
   AttnShape m;
   flowmoe_status_t st = check_mha(shape, mha, &m);
   if (st != FLOWMOE_OK) return st;
@@ -671,11 +677,14 @@ flowmoe_status_t flowmoe_mha_bwd(const flowmoe_shape_t* shape, const flowmoe_mha
     REQUIRE_F(delta, "delta");
     REQUIRE_T(d_in, "d_in");
   }
+  st = check_ws(ws, ws_bytes, mha_wgrad_ws_bytes(shape->M), "flowmoe_mha_bwd");
+  if (st != FLOWMOE_OK) return st;
   const int T = shape->T, M = shape->M;
   hipError_t e = launch_mha_bwd_data(m, T, M, w_qkv, w_o, qkv, attn, lse, d_out, d_attn, d_qkv,
                                      delta, d_in, stream);
   if (e == hipSuccess)
-    e = launch_mha_wgrad(T, M, 1, in, attn, d_out, d_qkv, dw_qkv, dw_o, accumulate != 0, stream);
+    e = launch_mha_wgrad(T, M, 1, in, attn, d_out, d_qkv, dw_qkv, dw_o, accumulate != 0, ws,
+                         stream);
   return hip_status(e, "flowmoe_mha_bwd");
 }
 
@@ -919,7 +928,8 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     REQUIRE_T(b->a_save, "bufs->a_save"); REQUIRE_T(b->y_disp, "bufs->y_disp");
     REQUIRE_T(b->dy_disp, "bufs->dy_disp"); REQUIRE_T(b->dx_disp, "bufs->dx_disp");
   }
-  const size_t need = flowmoe_workspace_bytes(shape, FLOWMOE_WS_LAYER_BWD);
+  const size_t need =
+      flowmoe_workspace_bytes(shape, mha ? FLOWMOE_WS_LAYER_BWD_MHA : FLOWMOE_WS_LAYER_BWD);
   st = check_ws(b->ws, b->ws_bytes, need, "flowmoe_layer_bwd");
   if (st != FLOWMOE_OK) return st;
   // One chunk: the gate's parameter gradients and the dispatch backward can
@@ -1025,7 +1035,7 @@ flowmoe_status_t flowmoe_layer_bwd(const flowmoe_shape_t* shape, int32_t R,
     }
     sc.mark_at(10 * R + 2, s_compute);
     sc.run(launch_mha_wgrad(s.T, s.M, R, b->mha_in, b->attn, b->dx, b->d_qkv, b->dw_qkv, b->dw_o,
-                            0, s_compute));
+                            0, b->ws, s_compute));
     sc.mark_at(10 * R + 3, s_compute);
   }
   sc.signal(evEnd, s_comm);

@@ -221,39 +221,49 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
         for (int ks = 0; ks < KS; ++ks) s[kb] = mfma(frag_row<D>(tk, 32 * kb + lq, ks, h2), qf[ks], s[kb]);
       }
       const bool edge = kb0 + 64 > a.N || (CAUSAL && kb0 + 63 > q0 + 32 * w);
+      if (edge) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kb0 + 32 * kb + 8 * (r >> 2) + 4 * h2 + (r & 3);
+            if (key >= a.N || (CAUSAL && key > qw)) s[kb][r] = -INFINITY;
+          }
+        }
+      }
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float v = s[kb][r] * a.c2;
-          if (edge) {
-            const int key = kb0 + 32 * kb + 8 * (r >> 2) + 4 * h2 + (r & 3);
-            if (key >= a.N || (CAUSAL && key > qw)) v = -INFINITY;
-          }
-          s[kb][r] = v;
-          mx = fmaxf(mx, v);
-        }
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      // every query sees key 0 in the first tile, so m is finite from then on
-      const float mn = fmaxf(m, mx);
-      const float al = exp2_fast(m - mn);
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * a.c2;
+      // The reference m of the exponents moves only when a score exceeds it
+      // by more than 2^8 (then the sum and the accumulators are rescaled):
+      // probabilities up to 256 stay exact in float and in bf16's exponent
+      // range, and the final lse = m + log2(l) is the same. Every query sees
+      // key 0 in the first tile, so m is finite from then on.
+      const bool up = mx > m + 8.0f;
+      if (__any(up)) {
+        const float mn = up ? mx : m;
+        const float al = exp2_fast(m - mn);
+        l *= al;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db] *= al;
+        m = mn;
+      }
       float rsum = 0.0f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float pv = exp2_fast(s[kb][r] - mn);
+          const float pv = exp2_fast(fmaf(s[kb][r], a.c2, -m));
           s[kb][r] = pv;
           rsum += pv;
         }
       }
       rsum += __shfl_xor(rsum, 32);
-      l = l * al + rsum;
-      m = mn;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[db] *= al;
+      l += rsum;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -570,14 +580,16 @@ hipError_t launch_mha_bwd_data(const AttnShape& m, int T, int M, const void* w_q
 
 hipError_t launch_mha_wgrad(int T, int M, int R, const void* in, const void* attn,
                             const void* d_out, const void* d_qkv, float* dw_qkv, float* dw_o,
-                            int accumulate, hipStream_t st) {
+                            int accumulate, void* ws, hipStream_t st) {
   // dW^O = attn^T d_out and dW_qkv = in^T d_qkv, each summed over the R
-  // chunks' rows in chunk order
+  // chunks' rows in chunk order (through partial sums in ws when their
+  // output tiles are too few for the CUs)
+  float* part = static_cast<float*>(ws);
   hipError_t e = launch_dense_wgrad(FLOWMOE_K_ATTN_WGRAD, T, R, attn, M, (long)T * M, M, d_out, M,
-                                    (long)T * M, M, dw_o, M, accumulate, st);
+                                    (long)T * M, M, dw_o, M, accumulate, part, st);
   if (e != hipSuccess) return e;
   return launch_dense_wgrad(FLOWMOE_K_ATTN_WGRAD, T, R, in, M, (long)T * M, M, d_qkv, 3L * M,
-                            (long)T * 3 * M, 3 * M, dw_qkv, 3L * M, accumulate, st);
+                            (long)T * 3 * M, 3 * M, dw_qkv, 3L * M, accumulate, part, st);
 }
 
 }  // namespace flowmoe

@@ -274,10 +274,17 @@ hipError_t launch_expert_ffn_bwd(const Shape& s, const void* dy_disp, const void
 hipError_t launch_dense_gemm(int kind, long rows, const void* A, long lda, int K, const void* B,
                              long ldb, bool b_kc, int N, void* C, long ldc, hipStream_t st);
 // C (Mdim x N, fp32, ldc) = (or +=) the sum over nseg segments g, in order,
-// of A_g^T B_g (A_g = A + g * a_sstride: rows x Mdim; B_g: rows x N)
+// of A_g^T B_g (A_g = A + g * a_sstride: rows x Mdim; B_g: rows x N). With
+// `part` (mha_wgrad_ws_bytes, ldc = N), a launch with few output tiles splits
+// every segment's rows into partial sums there, added in order afterwards.
 hipError_t launch_dense_wgrad(int kind, long rows, int nseg, const void* A, long lda,
                               long a_sstride, int Mdim, const void* B, long ldb, long b_sstride,
-                              int N, float* C, long ldc, int accumulate, hipStream_t st);
+                              int N, float* C, long ldc, int accumulate, float* part,
+                              hipStream_t st);
+// row splits of such a launch (1: none), and the partial-sum bytes the
+// attention's two weight gradients (M x 3M, M x M) need at width M
+int dense_wgrad_splits(int Mdim, int N, long rows);
+size_t mha_wgrad_ws_bytes(int M);
 
 // The attention of AT_r: T tokens = T / N sequences of N tokens, `heads`
 // heads of width D (64 or 128), M = heads * D, bf16
@@ -301,9 +308,10 @@ hipError_t launch_mha_bwd_data(const AttnShape& m, int T, int M, const void* w_q
                                float* delta, void* d_in, hipStream_t st);
 // weight gradients over R chunks of T rows: dW_o = sum attn^T d_out,
 // dW_qkv = sum in^T d_qkv
+// (ws: mha_wgrad_ws_bytes(M) of scratch for the partial sums, or null)
 hipError_t launch_mha_wgrad(int T, int M, int R, const void* in, const void* attn,
                             const void* d_out, const void* d_qkv, float* dw_qkv, float* dw_o,
-                            int accumulate, hipStream_t st);
+                            int accumulate, void* ws, hipStream_t st);
 
 // Kernel tracing (flowmoe_trace_start): record a begin/end event around a
 // launch when the kind is selected. Defined in abi.hip.

@@ -19,6 +19,7 @@
 // same modes and epilogues.
 #include <math.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "common.hpp"
@@ -92,13 +93,16 @@ __device__ __forceinline__ int clip_rows(long off, int n, long cap) {
 }
 
 // Expert e's rows in segment g: counts[g * E + e] rows from row
-// offsets[g * (E + 1) + e]. A dense launch (counts null, E = 1: the
-// attention's projections) has rows_cap rows from row 0 in every segment.
-__device__ __forceinline__ int seg_count(const GemmParams& p, int g, int e) {
-  return p.counts ? p.counts[g * p.E + e] : (int)p.rows_cap;
-}
+// offsets[g * (E + 1) + e]. A dense launch (counts null: the attention's
+// projections) splits the rows_cap rows of every segment into E equal
+// parts, part e being rows [e rows_cap / E, (e + 1) rows_cap / E) (E = 1:
+// all of them; E > 1: the token splits of a weight gradient).
 __device__ __forceinline__ int seg_offset(const GemmParams& p, int g, int e) {
-  return p.counts ? p.offsets[g * (p.E + 1) + e] : 0;
+  return p.counts ? p.offsets[g * (p.E + 1) + e] : (int)(p.rows_cap * e / p.E);
+}
+__device__ __forceinline__ int seg_count(const GemmParams& p, int g, int e) {
+  return p.counts ? p.counts[g * p.E + e]
+                  : (int)(p.rows_cap * (e + 1) / p.E - p.rows_cap * e / p.E);
 }
 
 // ---------------------------------------------------------------------------
@@ -1332,6 +1336,23 @@ __global__ void swiglu_act_f32_kernel(const float* __restrict__ h, float* __rest
 // expert): 64 lanes of 8 columns, wave w summing the rows w, w + 4, ... of
 // each segment in order (four rows in flight per lane), then the four
 // waves' sums added in wave order: deterministic.
+// C (+)= the S partial sums of P (S x n4 float4), added in split order
+__global__ __launch_bounds__(256) void sum_splits_kernel(const float4* __restrict__ P, int S,
+                                                         long n4, float4* __restrict__ C,
+                                                         int accumulate) {
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+    float4 a = accumulate ? C[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int s = 0; s < S; ++s) {
+      const float4 v = P[s * n4 + i];
+      a.x += v.x;
+      a.y += v.y;
+      a.z += v.z;
+      a.w += v.w;
+    }
+    C[i] = a;
+  }
+}
+
 template <typename TE>
 __global__ __launch_bounds__(256) void bias_grad_kernel(
     const TE* __restrict__ src, long ld, long seg_stride, const int32_t* __restrict__ counts,
@@ -1594,33 +1615,59 @@ hipError_t launch_dense_gemm(int kind, long rows, const void* A, long lda, int K
   return run_gemm_bf16<MODE_ROWS, true, false, EPI_STORE>(kind, s2, p, st);
 }
 
+int dense_wgrad_splits(int Mdim, int N, long rows) {
+  const long tiles = (long)((Mdim + 255) / 256) * ((N + 255) / 256);
+  const long s = std::min<long>(8, (kCUs + tiles - 1) / tiles);
+  return (int)std::max<long>(1, std::min<long>(s, rows / 512));
+}
+
+size_t mha_wgrad_ws_bytes(int M) {
+  const long big = 1L << 40;  // (any number of rows)
+  const int s3 = dense_wgrad_splits(M, 3 * M, big), s1 = dense_wgrad_splits(M, M, big);
+  const size_t b3 = s3 > 1 ? (size_t)s3 * M * 3 * M * 4 : 0, b1 = s1 > 1 ? (size_t)s1 * M * M * 4 : 0;
+  return align256(std::max(b3, b1));
+}
+
 hipError_t launch_dense_wgrad(int kind, long rows, int nseg, const void* A, long lda,
                               long a_sstride, int Mdim, const void* B, long ldb, long b_sstride,
-                              int N, float* C, long ldc, int accumulate, hipStream_t st) {
+                              int N, float* C, long ldc, int accumulate, float* part,
+                              hipStream_t st) {
+  // few output tiles for the CUs: the rows of every segment are split S ways
+  // into partial sums in `part` (S x Mdim x N), which a reduction adds in
+  // split order (deterministic)
+  const int S = part ? dense_wgrad_splits(Mdim, N, rows * nseg) : 1;
   Shape s2 = {};
   s2.T = (int)rows;
-  s2.E = 1;
+  s2.E = S;
   s2.rows = rows;
   s2.layout = FLOWMOE_PACKED;
   GemmParams p = {};
-  p.E = 1;
+  p.E = S;
   p.A = A;
   p.lda = lda;
   p.Mdim = Mdim;
   p.B0 = B;
   p.ldb = ldb;
   p.N = N;
-  p.C0 = C;
-  p.C1 = C;
-  p.ldc = ldc;
+  p.C0 = S > 1 ? part : C;
+  p.C1 = p.C0;
+  p.ldc = S > 1 ? N : ldc;
+  p.c_estride = (long)Mdim * N;
   p.ksplit = 1 << 30;
   p.nsplit = 1 << 30;
-  p.accumulate = accumulate;
+  p.accumulate = S > 1 ? 0 : accumulate;
   p.nseg = nseg;
   p.a_sstride = a_sstride;
   p.b_sstride = b_sstride;
   p.rows_cap = rows;
-  return run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(kind, s2, p, st);
+  FLOWMOE_TRY((run_gemm_bf16<MODE_KSUM, false, false, EPI_WGRAD>(kind, s2, p, st)));
+  if (S == 1) return hipSuccess;
+  const long n4 = (long)Mdim * N / 4;  // (ldc == N here)
+  return traced(kind, st, [&] {
+    hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)std::min<long>(2048, (n4 + 255) / 256)),
+                       dim3(256), 0, st, reinterpret_cast<const float4*>(part), S, n4,
+                       reinterpret_cast<float4*>(C), accumulate);
+  });
 }
 
 size_t ffn_bwd_ws_bytes(const Shape& s) {

@@ -116,7 +116,8 @@ class MoELayer:
             for n in ("mha_in", "w_qkv", "w_o", "qkv", "attn", "lse", "d_attn", "d_qkv", "delta",
                       "d_in", "dw_qkv", "dw_o"):
                 setattr(self, n, None)
-        self.ws_bytes = L.flowmoe_workspace_bytes(self.shape, L.WS_LAYER_BWD)
+        self.ws_bytes = L.flowmoe_workspace_bytes(
+            self.shape, L.WS_LAYER_BWD_MHA if mha is not None else L.WS_LAYER_BWD)
         self.ws = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
 
     @property

@@ -267,12 +267,29 @@ def test_mha_validation(flowmoe_lib):
     assert "dw_qkv is null" in str(ei.value)
 
 
+def test_mha_workspace(flowmoe_lib):
+    # the attention's weight gradients split their token rows into partial
+    # sums when their 256 x 256 output tiles are too few for the 256 CUs:
+    # M = 1024: dW_qkv has 4 x 12 tiles -> 6 splits of 1024 x 3072 floats
+    # (dW_o: 4 x 4 -> 8 splits, fewer bytes); M = 4096 needs no split
+    m = L.make_mha_shape(512, 16, 64, True)
+    for M, need in ((1024, 6 * 1024 * 3072 * 4), (2048, 2 * 2048 * 6144 * 4), (4096, 0)):
+        s = L.make_shape(1024, M, 64, 4, 2, 8, L.BF16)
+        assert L.flowmoe_workspace_bytes(s, L.WS_MHA_BWD) == need, M
+        assert L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD_MHA) >= max(
+            need, L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD))
+    s = L.make_shape(1024, 1024, 64, 4, 2, 8, L.BF16)
+    with pytest.raises(L.FlowMoEError) as ei:
+        L.flowmoe_mha_bwd(s, m, *([FAKE] * 13), 0, FAKE, 6 * 1024 * 3072 * 4 - 1, stream=0)
+    assert ei.value.status == L.ERR_WORKSPACE and "flowmoe_mha_bwd" in str(ei.value)
+
+
 def test_layer_mha_validation(flowmoe_lib):
     # the layer's chunk must hold whole sequences; its attention buffers are checked
     s = L.make_shape(768, 256, 64, 4, 2, 8, L.BF16)
     base = {n: FAKE for n in L._LAYER_FIELDS if n not in ("mha", "bias", "load", "w3", "dw3", "b1",
                                                              "b3", "b2", "db1", "db3", "db2", "dbias")}
-    need = L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD)
+    need = L.flowmoe_workspace_bytes(s, L.WS_LAYER_BWD_MHA)
     b = L.layer_bufs(ws_bytes=need, mha=L.make_mha_shape(512, 4, 64, True), **base)
     with pytest.raises(L.FlowMoEError) as ei:
         L.flowmoe_layer_fwd(s, 2, b, s_compute=0, s_comm=0)

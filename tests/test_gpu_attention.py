@@ -116,6 +116,8 @@ MHA_CASES = {
     # the large layer's causal d = 128 heads, several tiles with ragged tails
     "balanced_s": get_config("balanced", T=640, M=256, mha=True, seq_len=320),
     "large_s": get_config("large", T=768, M=512, mha=True, seq_len=384),
+    # 2048 rows of width 256: the weight gradients split their rows 4 ways
+    "split_s": get_config("skewed", T=2048, M=256, mha=True, seq_len=256),
 }
 
 
@@ -141,12 +143,14 @@ def test_mha_fwd_bwd(name):
     t = {k: to_torch(inp[k], d) for k in ("mha_in", "w_qkv", "w_o", "dy")}
     s = L.make_shape(T, M, 64, 1, 1, 0, L.BF16)
     m = L.make_mha_shape(cfg.seq_len, heads, cfg.head_dim, cfg.causal)
+    wsb = L.flowmoe_workspace_bytes(s, L.WS_MHA_BWD)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=d)
     L.flowmoe_mha_fwd(s, m, t["mha_in"], t["w_qkv"], t["w_o"], b["qkv"], b["attn"], b["lse"],
                       b["out"])
     # d_out: the generator's dy stands in for the gradient of I'
     L.flowmoe_mha_bwd(s, m, t["mha_in"], t["w_qkv"], t["w_o"], b["qkv"], b["attn"], b["lse"],
                       t["dy"], b["d_attn"], b["d_qkv"], b["delta"], b["d_in"], b["dw_qkv"],
-                      b["dw_o"], 0)
+                      b["dw_o"], 0, ws, wsb)
     torch.cuda.synchronize()
     i64 = {k: as_f64(inp[k]) for k in ("mha_in", "w_qkv", "w_o", "dy")}
     f = oracle.mha_fwd(i64["mha_in"], i64["w_qkv"], i64["w_o"], cfg.seq_len, heads, cfg.causal)
@@ -161,7 +165,7 @@ def test_mha_fwd_bwd(name):
     dwq, dwo = b["dw_qkv"].clone(), b["dw_o"].clone()
     L.flowmoe_mha_bwd(s, m, t["mha_in"], t["w_qkv"], t["w_o"], b["qkv"], b["attn"], b["lse"],
                       t["dy"], b["d_attn"], b["d_qkv"], b["delta"], b["d_in"], b["dw_qkv"],
-                      b["dw_o"], 1)
+                      b["dw_o"], 1, ws, wsb)
     torch.cuda.synchronize()
     assert torch.allclose(b["dw_qkv"], 2 * dwq, rtol=1e-6, atol=1e-6)
     assert torch.allclose(b["dw_o"], 2 * dwo, rtol=1e-6, atol=1e-6)
