@@ -15,7 +15,7 @@
 // backward.
 //
 // Backward (no atomics; every sum in a fixed order):
-//   dq kernel (blocks of 128 queries, loop over 64-key tiles): recomputes P
+//   dq kernel (blocks of 128 queries, loop over 32-key tiles): recomputes P
 //     from S and the log-sum-exp, dP^T = V dO^T, dS = P (dP - delta) with
 //     delta = rowsum(dO * O) (computed here and stored for the next kernel),
 //     dQ^T += K^T dS^T;
@@ -134,13 +134,13 @@ __device__ __forceinline__ void store_cols(bf16_t* dst, const floatx16& a, int h
   }
 }
 
-// 64-row K and V tiles of one (sequence, head), double-buffered through
-// registers: every thread moves D / 32 16-byte chunks of each per tile
-template <int D>
+// ROWS-row K and V tiles of one (sequence, head), double-buffered through
+// registers: every thread moves ROWS * D / 2048 16-byte chunks of each per tile
+template <int D, int ROWS = 64>
 struct KVTiles {
   static constexpr int CPR = D / 8;             // 16-byte chunks per row
-  static constexpr int TB = 64 * D * 2;         // bytes of one tile
-  static constexpr int LD = 64 * CPR / 256;     // chunks per thread per tile
+  static constexpr int TB = ROWS * D * 2;       // bytes of one tile
+  static constexpr int LD = ROWS * CPR / 256;   // chunks per thread per tile
   u32x4 rk[LD], rv[LD];
   __device__ __forceinline__ void load(const bf16_t* Kg, const bf16_t* Vg, long ld, int key0, int N,
                                        int tid) {
@@ -291,10 +291,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 }
 
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(256, 1) void attn_dq_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
-  using Tiles = KVTiles<D>;
-  __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB];
+  constexpr int CPR = D / 8;
+  using Tiles = KVTiles<D, 32>;
+  // 32-key K/V stages, then the dO rows of the block's 128 queries (read
+  // from LDS each tile rather than held in registers): 64 KB of LDS at
+  // D = 128, so two blocks share a CU, and the kernel fits in the 256 VGPRs
+  // that leaves without moving values through the AGPRs every step
+  __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB + 128 * D * 2];
+  char* const gt = lds + 2 * 2 * Tiles::TB;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
   int qt, hd, sq;
   decode(a, CAUSAL, qt, hd, sq);
@@ -307,15 +313,21 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(AttnArgs a) {
   const int q0 = qt * 128, qw = q0 + 32 * w + lq;
   const bool live = qw < a.N;
 
-  bf16x8 qf[KS], gf[KS];
+#pragma unroll
+  for (int u = 0; u < 128 * CPR / 256; ++u) {
+    const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, q = q0 + r;
+    *reinterpret_cast<u32x4*>(gt + toff<D>(r, c)) =
+        q < a.N ? *reinterpret_cast<const u32x4*>(Gg + (long)q * a.M + 8 * c) : u32x4{0, 0, 0, 0};
+  }
+  bf16x8 qf[KS];
   float dl = 0.0f;
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     qf[ks] = live ? *reinterpret_cast<const bf16x8*>(Qg + qw * ld + 16 * ks + 8 * h2) : zero8();
-    gf[ks] = live ? *reinterpret_cast<const bf16x8*>(Gg + (long)qw * a.M + 16 * ks + 8 * h2) : zero8();
+    const bf16x8 gv = live ? *reinterpret_cast<const bf16x8*>(Gg + (long)qw * a.M + 16 * ks + 8 * h2) : zero8();
     const bf16x8 ov = live ? *reinterpret_cast<const bf16x8*>(Og + (long)qw * a.M + 16 * ks + 8 * h2) : zero8();
 #pragma unroll
-    for (int t = 0; t < 8; ++t) dl += (float)gf[ks][t] * (float)ov[t];
+    for (int t = 0; t < 8; ++t) dl += (float)gv[t] * (float)ov[t];
   }
   dl += __shfl_xor(dl, 32);
   const long srow = (long)hd * a.T + tok0 + qw;
@@ -326,42 +338,40 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(AttnArgs a) {
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
 
   const int kend = CAUSAL ? min(a.N, q0 + 128) : a.N;
-  const int nk = (kend + 63) / 64;
+  const int nk = (kend + 31) / 32;
   Tiles tl;
   tl.load(Kg, Vg, ld, 0, a.N, tid);
   tl.store(lds, lds + Tiles::TB, tid);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int st = kt & 1;
-    if (kt + 1 < nk) tl.load(Kg, Vg, ld, (kt + 1) * 64, a.N, tid);
+    if (kt + 1 < nk) tl.load(Kg, Vg, ld, (kt + 1) * 32, a.N, tid);
     const char* tk = lds + st * 2 * Tiles::TB;
     const char* tv = tk + Tiles::TB;
-    const int kb0 = kt * 64;
+    const int kb0 = kt * 32;
     if (!CAUSAL || kb0 <= q0 + 32 * w + 31) {
+      floatx16 s = zero16(), dp = zero16();
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        floatx16 s = zero16(), dp = zero16();
+      for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row<D>(tk, lq, ks, h2), qf[ks], s);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row<D>(tk, 32 * kb + lq, ks, h2), qf[ks], s);
+      for (int ks = 0; ks < KS; ++ks)
+        dp = mfma(frag_row<D>(tv, lq, ks, h2), frag_row<D>(gt, 32 * w + lq, ks, h2), dp);
+      const bool edge = kb0 + 32 > a.N || (CAUSAL && kb0 + 31 > q0 + 32 * w);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) dp = mfma(frag_row<D>(tv, 32 * kb + lq, ks, h2), gf[ks], dp);
-        const bool edge = kb0 + 32 * kb + 32 > a.N || (CAUSAL && kb0 + 32 * kb + 31 > q0 + 32 * w);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float pv = exp2_fast(s[r] * a.c2 - l2);
-          if (edge) {
-            const int key = kb0 + 32 * kb + 8 * (r >> 2) + 4 * h2 + (r & 3);
-            if (key >= a.N || (CAUSAL && key > qw)) pv = 0.0f;
-          }
-          s[r] = pv * (dp[r] - dl);  // dS^T
+      for (int r = 0; r < 16; ++r) {
+        float pv = exp2_fast(s[r] * a.c2 - l2);
+        if (edge) {
+          const int key = kb0 + 8 * (r >> 2) + 4 * h2 + (r & 3);
+          if (key >= a.N || (CAUSAL && key > qw)) pv = 0.0f;
         }
+        s[r] = pv * (dp[r] - dl);  // dS^T
+      }
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const bf16x8 pb = pfrag(s, s2);
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const bf16x8 pb = pfrag(s, s2);
 #pragma unroll
-          for (int db = 0; db < DB; ++db)
-            dq[db] = mfma(frag_tr<D>(tk, 32 * kb + 16 * s2, 32 * db, lane), pb, dq[db]);
-        }
+        for (int db = 0; db < DB; ++db)
+          dq[db] = mfma(frag_tr<D>(tk, 16 * s2, 32 * db, lane), pb, dq[db]);
       }
     }
     if (kt + 1 < nk) {
@@ -378,12 +388,16 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(AttnArgs a) {
 }
 
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(256, 1) void attn_dkdv_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a) {
   constexpr int KS = D / 16, DB = D / 32, CPR = D / 8;
   constexpr int TQ = 32 * D * 2;                // one 32-row tile
   constexpr int STG = 2 * TQ + 256;             // Q, dO, then 32 lse2 and 32 delta
   constexpr int LD = 32 * CPR / 256;            // chunks per thread per tile
-  __shared__ __attribute__((aligned(16))) char lds[2 * STG];
+  // two query stages, then the V rows of the block's 128 keys (read from
+  // LDS each step rather than held in registers: the kernel then fits in the
+  // 256 VGPRs without moving values through the AGPRs every step)
+  __shared__ __attribute__((aligned(16))) char lds[2 * STG + 128 * D * 2];
+  char* const vt = lds + 2 * STG;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
   int kt, hd, sq;
   decode(a, false, kt, hd, sq);
@@ -394,11 +408,16 @@ __global__ __launch_bounds__(256, 1) void attn_dkdv_kernel(AttnArgs a) {
   const int k0 = kt * 128, kw = k0 + 32 * w + lq;
   const bool live = kw < a.N;
 
-  bf16x8 kf[KS], vf[KS];
+  bf16x8 kf[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
+  for (int ks = 0; ks < KS; ++ks)
     kf[ks] = live ? *reinterpret_cast<const bf16x8*>(Qg + a.M + kw * ld + 16 * ks + 8 * h2) : zero8();
-    vf[ks] = live ? *reinterpret_cast<const bf16x8*>(Qg + 2L * a.M + kw * ld + 16 * ks + 8 * h2) : zero8();
+#pragma unroll
+  for (int u = 0; u < 128 * CPR / 256; ++u) {
+    const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, key = k0 + r;
+    *reinterpret_cast<u32x4*>(vt + toff<D>(r, c)) =
+        key < a.N ? *reinterpret_cast<const u32x4*>(Qg + 2L * a.M + key * ld + 8 * c)
+                  : u32x4{0, 0, 0, 0};
   }
   floatx16 dv[DB], dk[DB];
 #pragma unroll
@@ -454,7 +473,8 @@ __global__ __launch_bounds__(256, 1) void attn_dkdv_kernel(AttnArgs a) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row<D>(tq, lq, ks, h2), kf[ks], s);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) dp = mfma(frag_row<D>(tg, lq, ks, h2), vf[ks], dp);
+      for (int ks = 0; ks < KS; ++ks)
+        dp = mfma(frag_row<D>(tg, lq, ks, h2), frag_row<D>(vt, 32 * w + lq, ks, h2), dp);
       const bool edge = qb + 32 > a.N || (CAUSAL && k0 + 32 * w + 31 > qb);
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
