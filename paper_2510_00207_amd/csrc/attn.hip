@@ -136,17 +136,17 @@ __device__ __forceinline__ void store_cols(bf16_t* dst, const floatx16& a, int h
 
 // ROWS-row K and V tiles of one (sequence, head), double-buffered through
 // registers: every thread moves ROWS * D / 2048 16-byte chunks of each per tile
-template <int D, int ROWS = 64>
+template <int D, int ROWS = 64, int NT = 256>
 struct KVTiles {
   static constexpr int CPR = D / 8;             // 16-byte chunks per row
   static constexpr int TB = ROWS * D * 2;       // bytes of one tile
-  static constexpr int LD = ROWS * CPR / 256;   // chunks per thread per tile
+  static constexpr int LD = ROWS * CPR / NT;    // chunks per thread per tile
   u32x4 rk[LD], rv[LD];
   __device__ __forceinline__ void load(const bf16_t* Kg, const bf16_t* Vg, long ld, int key0, int N,
                                        int tid) {
 #pragma unroll
     for (int u = 0; u < LD; ++u) {
-      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, key = key0 + r;
+      const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR, key = key0 + r;
       if (key < N) {
         rk[u] = *reinterpret_cast<const u32x4*>(Kg + key * ld + 8 * c);
         rv[u] = *reinterpret_cast<const u32x4*>(Vg + key * ld + 8 * c);
@@ -159,7 +159,7 @@ struct KVTiles {
   __device__ __forceinline__ void store(char* tk, char* tv, int tid) {
 #pragma unroll
     for (int u = 0; u < LD; ++u) {
-      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR;
+      const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR;
       *reinterpret_cast<u32x4*>(tk + toff<D>(r, c)) = rk[u];
       *reinterpret_cast<u32x4*>(tv + toff<D>(r, c)) = rv[u];
     }
@@ -168,27 +168,32 @@ struct KVTiles {
 
 // block -> (query or key tile, head, sequence); `rev`: tiles in descending
 // order (the causal forward's longest query tiles first)
-__device__ __forceinline__ void decode(const AttnArgs& a, bool rev, int& tile, int& hd, int& sq) {
-  const int per = a.heads * a.nseq, nt = (a.N + 127) / 128;
+__device__ __forceinline__ void decode(const AttnArgs& a, bool rev, int& tile, int& hd, int& sq,
+                                       int rows = 128) {
+  const int per = a.heads * a.nseq, nt = (a.N + rows - 1) / rows;
   const int t = (int)(blockIdx.x / per), rest = (int)(blockIdx.x % per);
   tile = rev ? nt - 1 - t : t;
   hd = rest % a.heads;
   sq = rest / a.heads;
 }
 
-template <int D, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
-  constexpr int KS = D / 16, DB = D / 32;
-  using Tiles = KVTiles<D>;
+// NW waves (of 32 queries each) per forward block: every K/V tile that a
+// block stages in LDS serves 32 NW queries (8 waves halve the staging
+// traffic per MFMA of 4; the launch picks 4 when 8 would leave fewer than
+// two blocks per CU)
+template <int D, bool CAUSAL, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(AttnArgs a) {
+  constexpr int KS = D / 16, DB = D / 32, QB = 32 * NW;
+  using Tiles = KVTiles<D, 64, 64 * NW>;
   __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
   int qt, hd, sq;
-  decode(a, CAUSAL, qt, hd, sq);
+  decode(a, CAUSAL, qt, hd, sq, QB);
   const long tok0 = (long)sq * a.N, ld = 3L * a.M;
   const bf16_t* Qg = a.qkv + tok0 * ld + (long)hd * D;
   const bf16_t* Kg = Qg + a.M;
   const bf16_t* Vg = Qg + 2L * a.M;
-  const int q0 = qt * 128, qw = q0 + 32 * w + lq;
+  const int q0 = qt * QB, qw = q0 + 32 * w + lq;
 
   bf16x8 qf[KS];
 #pragma unroll
@@ -199,7 +204,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
   for (int db = 0; db < DB; ++db) o[db] = zero16();
   float m = -INFINITY, l = 0.0f;
 
-  const int kend = CAUSAL ? min(a.N, q0 + 128) : a.N;
+  const int kend = CAUSAL ? min(a.N, q0 + QB) : a.N;
   const int nk = (kend + 63) / 64;
   Tiles tl;
   tl.load(Kg, Vg, ld, 0, a.N, tid);
@@ -528,17 +533,19 @@ AttnArgs attn_args(const AttnShape& m, int T, int M) {
   return a;
 }
 
-unsigned attn_blocks(const AttnArgs& a) { return (unsigned)(((a.N + 127) / 128) * a.heads * a.nseq); }
+unsigned attn_blocks(const AttnArgs& a, int rows = 128) {
+  return (unsigned)(((a.N + rows - 1) / rows) * a.heads * a.nseq);
+}
 
-#define FLOWMOE_ATTN_LAUNCH(KERNEL, a, st)                                                     \
+#define FLOWMOE_ATTN_LAUNCH(KERNEL, a, st, ROWS, THREADS, ...)                                 \
   do {                                                                                          \
-    const dim3 g(attn_blocks(a)), b(256);                                                       \
+    const dim3 g(attn_blocks(a, ROWS)), b(THREADS);                                             \
     if (m.D == 128) {                                                                           \
-      if (m.causal) hipLaunchKernelGGL((KERNEL<128, true>), g, b, 0, st, a);                    \
-      else hipLaunchKernelGGL((KERNEL<128, false>), g, b, 0, st, a);                            \
+      if (m.causal) hipLaunchKernelGGL((KERNEL<128, true, ##__VA_ARGS__>), g, b, 0, st, a);     \
+      else hipLaunchKernelGGL((KERNEL<128, false, ##__VA_ARGS__>), g, b, 0, st, a);             \
     } else {                                                                                    \
-      if (m.causal) hipLaunchKernelGGL((KERNEL<64, true>), g, b, 0, st, a);                     \
-      else hipLaunchKernelGGL((KERNEL<64, false>), g, b, 0, st, a);                             \
+      if (m.causal) hipLaunchKernelGGL((KERNEL<64, true, ##__VA_ARGS__>), g, b, 0, st, a);      \
+      else hipLaunchKernelGGL((KERNEL<64, false, ##__VA_ARGS__>), g, b, 0, st, a);              \
     }                                                                                           \
   } while (0)
 
@@ -551,7 +558,11 @@ hipError_t launch_attn_fwd(const AttnShape& m, int T, int M, const void* qkv, vo
   a.qkv = static_cast<const bf16_t*>(qkv);
   a.out = static_cast<bf16_t*>(o);
   a.lse = lse;
-  return traced(FLOWMOE_K_ATTN_FWD, st, [&] { FLOWMOE_ATTN_LAUNCH(attn_fwd_kernel, a, st); });
+  const bool wide = attn_blocks(a, 256) >= 2u * 256u;
+  return traced(FLOWMOE_K_ATTN_FWD, st, [&] {
+    if (wide) FLOWMOE_ATTN_LAUNCH(attn_fwd_kernel, a, st, 256, 512, 8);
+    else FLOWMOE_ATTN_LAUNCH(attn_fwd_kernel, a, st, 128, 256, 4);
+  });
 }
 
 hipError_t launch_attn_bwd(const AttnShape& m, int T, int M, const void* qkv, const void* o,
@@ -565,9 +576,11 @@ hipError_t launch_attn_bwd(const AttnShape& m, int T, int M, const void* qkv, co
   a.d_qkv = static_cast<bf16_t*>(d_qkv);
   a.lse = const_cast<float*>(lse);
   a.delta = delta;
-  hipError_t e = traced(FLOWMOE_K_ATTN_BWD_DQ, st, [&] { FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st); });
+  hipError_t e = traced(FLOWMOE_K_ATTN_BWD_DQ, st,
+                        [&] { FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st, 128, 256); });
   if (e != hipSuccess) return e;
-  return traced(FLOWMOE_K_ATTN_BWD_DKDV, st, [&] { FLOWMOE_ATTN_LAUNCH(attn_dkdv_kernel, a, st); });
+  return traced(FLOWMOE_K_ATTN_BWD_DKDV, st,
+                [&] { FLOWMOE_ATTN_LAUNCH(attn_dkdv_kernel, a, st, 128, 256); });
 }
 
 hipError_t launch_mha_fwd(const AttnShape& m, int T, int M, const void* in, const void* w_qkv,

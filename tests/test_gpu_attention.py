@@ -51,6 +51,10 @@ CORE_CASES = [
     (1, 64, 4, 64, True),
     (1, 1000, 1, 128, True),   # 8 query blocks, 16 key tiles, the last ragged
     (2, 97, 3, 64, False),
+    # grids of at least 512 blocks of 256 queries: the 8-wave forward blocks,
+    # with ragged tails
+    (4, 700, 48, 64, True),
+    (2, 520, 96, 128, False),
 ]
 
 
