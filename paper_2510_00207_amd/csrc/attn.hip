@@ -140,14 +140,15 @@ template <int D, int ROWS = 64, int NT = 256>
 struct KVTiles {
   static constexpr int CPR = D / 8;             // 16-byte chunks per row
   static constexpr int TB = ROWS * D * 2;       // bytes of one tile
-  static constexpr int LD = ROWS * CPR / NT;    // chunks per thread per tile
+  static constexpr int TOT = ROWS * CPR;        // chunks per tile
+  static constexpr int LD = (TOT + NT - 1) / NT; // chunks per thread per tile
   u32x4 rk[LD], rv[LD];
   __device__ __forceinline__ void load(const bf16_t* Kg, const bf16_t* Vg, long ld, int key0, int N,
                                        int tid) {
 #pragma unroll
     for (int u = 0; u < LD; ++u) {
       const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR, key = key0 + r;
-      if (key < N) {
+      if (key < N && idx < TOT) {
         rk[u] = *reinterpret_cast<const u32x4*>(Kg + key * ld + 8 * c);
         rv[u] = *reinterpret_cast<const u32x4*>(Vg + key * ld + 8 * c);
       } else {
@@ -160,8 +161,10 @@ struct KVTiles {
 #pragma unroll
     for (int u = 0; u < LD; ++u) {
       const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR;
-      *reinterpret_cast<u32x4*>(tk + toff<D>(r, c)) = rk[u];
-      *reinterpret_cast<u32x4*>(tv + toff<D>(r, c)) = rv[u];
+      if (TOT % NT == 0 || idx < TOT) {
+        *reinterpret_cast<u32x4*>(tk + toff<D>(r, c)) = rk[u];
+        *reinterpret_cast<u32x4*>(tv + toff<D>(r, c)) = rv[u];
+      }
     }
   }
 };
@@ -295,32 +298,32 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(AttnArgs a) {
   }
 }
 
-template <int D, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a) {
-  constexpr int KS = D / 16, DB = D / 32;
+template <int D, bool CAUSAL, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dq_kernel(AttnArgs a) {
+  constexpr int KS = D / 16, DB = D / 32, QB = 32 * NW, NT = 64 * NW;
   constexpr int CPR = D / 8;
-  using Tiles = KVTiles<D, 32>;
+  using Tiles = KVTiles<D, 32, NT>;
   // 32-key K/V stages, then the dO rows of the block's 128 queries (read
   // from LDS each tile rather than held in registers): 64 KB of LDS at
   // D = 128, so two blocks share a CU, and the kernel fits in the 256 VGPRs
   // that leaves without moving values through the AGPRs every step
-  __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB + 128 * D * 2];
+  __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB + QB * D * 2];
   char* const gt = lds + 2 * 2 * Tiles::TB;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
   int qt, hd, sq;
-  decode(a, CAUSAL, qt, hd, sq);
+  decode(a, CAUSAL, qt, hd, sq, QB);
   const long tok0 = (long)sq * a.N, ld = 3L * a.M;
   const bf16_t* Qg = a.qkv + tok0 * ld + (long)hd * D;
   const bf16_t* Kg = Qg + a.M;
   const bf16_t* Vg = Qg + 2L * a.M;
   const bf16_t* Gg = a.d_o + tok0 * a.M + (long)hd * D;
   const bf16_t* Og = a.o + tok0 * a.M + (long)hd * D;
-  const int q0 = qt * 128, qw = q0 + 32 * w + lq;
+  const int q0 = qt * QB, qw = q0 + 32 * w + lq;
   const bool live = qw < a.N;
 
 #pragma unroll
-  for (int u = 0; u < 128 * CPR / 256; ++u) {
-    const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, q = q0 + r;
+  for (int u = 0; u < QB * CPR / NT; ++u) {
+    const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR, q = q0 + r;
     *reinterpret_cast<u32x4*>(gt + toff<D>(r, c)) =
         q < a.N ? *reinterpret_cast<const u32x4*>(Gg + (long)q * a.M + 8 * c) : u32x4{0, 0, 0, 0};
   }
@@ -342,7 +345,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
 
-  const int kend = CAUSAL ? min(a.N, q0 + 128) : a.N;
+  const int kend = CAUSAL ? min(a.N, q0 + QB) : a.N;
   const int nk = (kend + 31) / 32;
   Tiles tl;
   tl.load(Kg, Vg, ld, 0, a.N, tid);
@@ -392,25 +395,26 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a) {
   }
 }
 
-template <int D, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a) {
-  constexpr int KS = D / 16, DB = D / 32, CPR = D / 8;
+template <int D, bool CAUSAL, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dkdv_kernel(AttnArgs a) {
+  constexpr int KS = D / 16, DB = D / 32, CPR = D / 8, KB = 32 * NW, NT = 64 * NW;
   constexpr int TQ = 32 * D * 2;                // one 32-row tile
   constexpr int STG = 2 * TQ + 256;             // Q, dO, then 32 lse2 and 32 delta
-  constexpr int LD = 32 * CPR / 256;            // chunks per thread per tile
+  constexpr int TOT = 32 * CPR;                 // chunks per 32-row tile
+  constexpr int LD = (TOT + NT - 1) / NT;       // chunks per thread per tile
   // two query stages, then the V rows of the block's 128 keys (read from
   // LDS each step rather than held in registers: the kernel then fits in the
   // 256 VGPRs without moving values through the AGPRs every step)
-  __shared__ __attribute__((aligned(16))) char lds[2 * STG + 128 * D * 2];
+  __shared__ __attribute__((aligned(16))) char lds[2 * STG + KB * D * 2];
   char* const vt = lds + 2 * STG;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
   int kt, hd, sq;
-  decode(a, false, kt, hd, sq);
+  decode(a, false, kt, hd, sq, KB);
   const long tok0 = (long)sq * a.N, ld = 3L * a.M;
   const bf16_t* Qg = a.qkv + tok0 * ld + (long)hd * D;
   const bf16_t* Gg = a.d_o + tok0 * a.M + (long)hd * D;
   const long srow0 = (long)hd * a.T + tok0;
-  const int k0 = kt * 128, kw = k0 + 32 * w + lq;
+  const int k0 = kt * KB, kw = k0 + 32 * w + lq;
   const bool live = kw < a.N;
 
   bf16x8 kf[KS];
@@ -418,8 +422,8 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a) {
   for (int ks = 0; ks < KS; ++ks)
     kf[ks] = live ? *reinterpret_cast<const bf16x8*>(Qg + a.M + kw * ld + 16 * ks + 8 * h2) : zero8();
 #pragma unroll
-  for (int u = 0; u < 128 * CPR / 256; ++u) {
-    const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, key = k0 + r;
+  for (int u = 0; u < KB * CPR / NT; ++u) {
+    const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR, key = k0 + r;
     *reinterpret_cast<u32x4*>(vt + toff<D>(r, c)) =
         key < a.N ? *reinterpret_cast<const u32x4*>(Qg + 2L * a.M + key * ld + 8 * c)
                   : u32x4{0, 0, 0, 0};
@@ -438,8 +442,8 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a) {
   auto load = [&](int qb) {
 #pragma unroll
     for (int u = 0; u < LD; ++u) {
-      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR, q = qb + r;
-      if (q < a.N) {
+      const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR, q = qb + r;
+      if (q < a.N && idx < TOT) {
         rq[u] = *reinterpret_cast<const u32x4*>(Qg + q * ld + 8 * c);
         rg[u] = *reinterpret_cast<const u32x4*>(Gg + (long)q * a.M + 8 * c);
       } else {
@@ -455,7 +459,8 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a) {
   auto store = [&](char* stg) {
 #pragma unroll
     for (int u = 0; u < LD; ++u) {
-      const int idx = tid + 256 * u, r = idx / CPR, c = idx % CPR;
+      const int idx = tid + NT * u, r = idx / CPR, c = idx % CPR;
+      if (TOT % NT != 0 && idx >= TOT) continue;
       *reinterpret_cast<u32x4*>(stg + toff<D>(r, c)) = rq[u];
       *reinterpret_cast<u32x4*>(stg + TQ + toff<D>(r, c)) = rg[u];
     }
@@ -576,11 +581,18 @@ hipError_t launch_attn_bwd(const AttnShape& m, int T, int M, const void* qkv, co
   a.d_qkv = static_cast<bf16_t*>(d_qkv);
   a.lse = const_cast<float*>(lse);
   a.delta = delta;
-  hipError_t e = traced(FLOWMOE_K_ATTN_BWD_DQ, st,
-                        [&] { FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st, 128, 256); });
+  // 8-wave blocks (256 queries, or keys) when that grid still gives two
+  // blocks per CU: each staged tile then serves twice the MFMA work
+  const bool wide = attn_blocks(a, 256) >= 2u * 256u;
+  hipError_t e = traced(FLOWMOE_K_ATTN_BWD_DQ, st, [&] {
+    if (wide) FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st, 256, 512, 8);
+    else FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st, 128, 256, 4);
+  });
   if (e != hipSuccess) return e;
-  return traced(FLOWMOE_K_ATTN_BWD_DKDV, st,
-                [&] { FLOWMOE_ATTN_LAUNCH(attn_dkdv_kernel, a, st, 128, 256); });
+  return traced(FLOWMOE_K_ATTN_BWD_DKDV, st, [&] {
+    if (wide) FLOWMOE_ATTN_LAUNCH(attn_dkdv_kernel, a, st, 256, 512, 8);
+    else FLOWMOE_ATTN_LAUNCH(attn_dkdv_kernel, a, st, 128, 256, 4);
+  });
 }
 
 hipError_t launch_mha_fwd(const AttnShape& m, int T, int M, const void* in, const void* w_qkv,
