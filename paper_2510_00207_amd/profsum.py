@@ -12,7 +12,8 @@
         source, so a later kernel change is detected and the figure dropped.
 
     python -m paper_2510_00207_amd.profsum mfma DIR --out FILE.md --command "..."
-        MFMA busy share of the expert GEMMs from one PMC pass with
+        MFMA busy share of the expert GEMMs (or of the kernels whose names
+        match --match) from one PMC pass with
         SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE: GRBM_GUI_ACTIVE is summed
         over the 8 XCDs, so a dispatch's cycles are GRBM_GUI_ACTIVE / 8 and its
         MFMA busy share is SQ_VALU_MFMA_BUSY_CYCLES / (cycles * 1024 SIMDs);
@@ -133,8 +134,9 @@ def cmd_mfma(a) -> None:
         c["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
         c[r["Counter_Name"]] = c.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
     agg = collections.defaultdict(lambda: [0, 0.0, 0.0, 0.0])  # launches, busy, cycles, ns
+    pick = (lambda nm: re.search(a.match, nm)) if a.match else expert_gemm
     for c in per.values():
-        if not expert_gemm(c["name"]) or "SQ_VALU_MFMA_BUSY_CYCLES" not in c:
+        if not pick(c["name"]) or "SQ_VALU_MFMA_BUSY_CYCLES" not in c:
             continue
         g = agg[c["name"]]
         g[0] += 1
@@ -154,7 +156,8 @@ def cmd_mfma(a) -> None:
         lines.append(f"| `{nm}` | {n} | {ns / n / 1e3:.1f} | {cyc / ns:.2f} | "
                      f"{busy / (cyc * 1024):.3f} |")
     if tc > 0:
-        lines += ["", f"All expert GEMM launches together: MFMA busy {tb / (tc * 1024):.3f}."]
+        what = "matching" if a.match else "expert GEMM"
+        lines += ["", f"All {what} launches together: MFMA busy {tb / (tc * 1024):.3f}."]
     if a.note:
         lines += ["", a.note]
     open(a.out, "w").write("\n".join(lines) + "\n")
@@ -183,6 +186,8 @@ def main() -> None:
     m.add_argument("--title", default="MFMA busy share of the expert GEMMs")
     m.add_argument("--command", required=True)
     m.add_argument("--note", default="")
+    m.add_argument("--match", default="",
+                   help="regex over kernel names (default: the expert GEMMs)")
     a = ap.parse_args()
     {"trace": cmd_trace, "traffic": cmd_traffic, "mfma": cmd_mfma}[a.cmd](a)
 
