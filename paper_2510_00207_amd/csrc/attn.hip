@@ -52,6 +52,14 @@ struct AttnArgs {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// the LDS stage of a double-buffered loop as a compile-time constant: the
+// loops run their steps in pairs (stage 0, stage 1), so every LDS address of
+// a step is a register base plus an immediate offset
+template <int S>
+struct Stage {
+  static constexpr int value = S;
+};
+
 __device__ __forceinline__ bf16x8 zero8() { return __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0}); }
 
 __device__ __forceinline__ floatx16 zero16() {
@@ -106,6 +114,41 @@ __device__ __forceinline__ bf16x8 frag_tr(const char* t, int rb, int cb, int lan
   const short __attribute__((ext_vector_type(8))) s = {v[0][0], v[0][1], v[0][2], v[0][3],
                                                        v[1][0], v[1][1], v[1][2], v[1][3]};
   return __builtin_bit_cast(bf16x8, s);
+}
+
+// The swizzle lets a lane's fragment addresses be formed from three per-lane
+// bases: a row read of row r0 + lq (r0 a multiple of 32) at k step ks is at
+// r0 * 2D + (row_base ^ 32 ks), and a transposing read at rows rb (a
+// multiple of 16) and columns cb (a multiple of 32) at
+// rb * 2D + (tr_base_i ^ 2 cb) for its two halves i. The loops rebuild the
+// XORs in every step from bases they mark as changed (opaque()): the
+// compiler would otherwise keep every combination live across the loop and,
+// short of registers, spill them and reload one before each LDS read.
+template <int D>
+__device__ __forceinline__ int row_base(int lq, int h2) {
+  return toff<D>(lq, h2);
+}
+template <int D>
+__device__ __forceinline__ int tr_base(int lane, int i) {
+  const int G = lane >> 4, sl = lane & 15;
+  const int col = (G & 1) * 16 + 4 * (sl & 3);
+  const int r = 4 * (G >> 1) + 8 * i + (sl >> 2);
+  return toff<D>(r, col >> 3) + ((col & 7) << 1);
+}
+template <int D>
+__device__ __forceinline__ bf16x8 frag_row_x(const char* t, int base, int r0, int ks) {
+  return *reinterpret_cast<const bf16x8*>(t + r0 * 2 * D + (base ^ (ks << 5)));
+}
+template <int D>
+__device__ __forceinline__ bf16x8 frag_tr_x(const char* t, int b0, int b1, int rb, int cb) {
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(t + rb * 2 * D + (b0 ^ (2 * cb))));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(t + rb * 2 * D + (b1 ^ (2 * cb))));
+  const short __attribute__((ext_vector_type(8))) s = {lo[0], lo[1], lo[2], lo[3],
+                                                       hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, s);
+}
+__device__ __forceinline__ void opaque(int& a, int& b, int& c) {
+  asm volatile("" : "+v"(a), "+v"(b), "+v"(c));
 }
 
 // Rows 16 s .. 16 s + 15 of a 32 x 32 accumulator (lane l: column l % 32,
@@ -213,8 +256,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(AttnArgs a) {
   tl.load(Kg, Vg, ld, 0, a.N, tid);
   tl.store(lds, lds + Tiles::TB, tid);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & 1;
+  int rbase = row_base<D>(lq, h2), tb0 = tr_base<D>(lane, 0), tb1 = tr_base<D>(lane, 1);
+  auto step = [&](const int kt, auto stc) {
+    constexpr int st = decltype(stc)::value;
+    opaque(rbase, tb0, tb1);
     if (kt + 1 < nk) tl.load(Kg, Vg, ld, (kt + 1) * 64, a.N, tid);
     const char* tk = lds + st * 2 * Tiles::TB;
     const char* tv = tk + Tiles::TB;
@@ -226,7 +271,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(AttnArgs a) {
       for (int kb = 0; kb < 2; ++kb) {
         s[kb] = zero16();
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) s[kb] = mfma(frag_row<D>(tk, 32 * kb + lq, ks, h2), qf[ks], s[kb]);
+        for (int ks = 0; ks < KS; ++ks) s[kb] = mfma(frag_row_x<D>(tk, rbase, 32 * kb, ks), qf[ks], s[kb]);
       }
       const bool edge = kb0 + 64 > a.N || (CAUSAL && kb0 + 63 > q0 + 32 * w);
       if (edge) {
@@ -279,7 +324,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(AttnArgs a) {
           const bf16x8 pb = pfrag(s[kb], s2);
 #pragma unroll
           for (int db = 0; db < DB; ++db)
-            o[db] = mfma(frag_tr<D>(tv, 32 * kb + 16 * s2, 32 * db, lane), pb, o[db]);
+            o[db] = mfma(frag_tr_x<D>(tv, tb0, tb1, 32 * kb + 16 * s2, 32 * db), pb, o[db]);
         }
       }
     }
@@ -288,6 +333,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(AttnArgs a) {
       tl.store(nk_, nk_ + Tiles::TB, tid);
     }
     __syncthreads();
+    };
+  for (int kt = 0; kt < nk; kt += 2) {
+    step(kt, Stage<0>{});
+    if (kt + 1 < nk) step(kt + 1, Stage<1>{});
   }
   if (qw < a.N) {
     const float inv = 1.0f / l;
@@ -351,8 +400,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dq_kernel(AttnArgs a) {
   tl.load(Kg, Vg, ld, 0, a.N, tid);
   tl.store(lds, lds + Tiles::TB, tid);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & 1;
+  int rbase = row_base<D>(lq, h2), tb0 = tr_base<D>(lane, 0), tb1 = tr_base<D>(lane, 1);
+  auto step = [&](const int kt, auto stc) {
+    constexpr int st = decltype(stc)::value;
+    opaque(rbase, tb0, tb1);
     if (kt + 1 < nk) tl.load(Kg, Vg, ld, (kt + 1) * 32, a.N, tid);
     const char* tk = lds + st * 2 * Tiles::TB;
     const char* tv = tk + Tiles::TB;
@@ -360,10 +411,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dq_kernel(AttnArgs a) {
     if (!CAUSAL || kb0 <= q0 + 32 * w + 31) {
       floatx16 s = zero16(), dp = zero16();
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row<D>(tk, lq, ks, h2), qf[ks], s);
+      for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row_x<D>(tk, rbase, 0, ks), qf[ks], s);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        dp = mfma(frag_row<D>(tv, lq, ks, h2), frag_row<D>(gt, 32 * w + lq, ks, h2), dp);
+        dp = mfma(frag_row_x<D>(tv, rbase, 0, ks), frag_row_x<D>(gt, rbase, 32 * w, ks), dp);
       const bool edge = kb0 + 32 > a.N || (CAUSAL && kb0 + 31 > q0 + 32 * w);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -379,7 +430,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dq_kernel(AttnArgs a) {
         const bf16x8 pb = pfrag(s, s2);
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          dq[db] = mfma(frag_tr<D>(tk, 16 * s2, 32 * db, lane), pb, dq[db]);
+          dq[db] = mfma(frag_tr_x<D>(tk, tb0, tb1, 16 * s2, 32 * db), pb, dq[db]);
       }
     }
     if (kt + 1 < nk) {
@@ -387,6 +438,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dq_kernel(AttnArgs a) {
       tl.store(nk_, nk_ + Tiles::TB, tid);
     }
     __syncthreads();
+    };
+  for (int kt = 0; kt < nk; kt += 2) {
+    step(kt, Stage<0>{});
+    if (kt + 1 < nk) step(kt + 1, Stage<1>{});
   }
   if (live) {
     bf16_t* dst = a.d_qkv + (tok0 + qw) * ld + (long)hd * D;
@@ -471,8 +526,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dkdv_kernel(AttnArgs a) 
     store(lds);
   }
   __syncthreads();
-  for (int it = 0; it < nqs; ++it) {
-    const int st = it & 1, qb = qs0 + 32 * it;
+  int rbase = row_base<D>(lq, h2), tb0 = tr_base<D>(lane, 0), tb1 = tr_base<D>(lane, 1);
+  auto step = [&](const int it, auto stc) {
+    constexpr int st = decltype(stc)::value;
+    opaque(rbase, tb0, tb1);
+    const int qb = qs0 + 32 * it;
     if (it + 1 < nqs) load(qb + 32);
     const char* tq = lds + st * STG;
     const char* tg = tq + TQ;
@@ -481,10 +539,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dkdv_kernel(AttnArgs a) 
     if (!CAUSAL || qb + 31 >= k0 + 32 * w) {
       floatx16 s = zero16(), dp = zero16();
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row<D>(tq, lq, ks, h2), kf[ks], s);
+      for (int ks = 0; ks < KS; ++ks) s = mfma(frag_row_x<D>(tq, rbase, 0, ks), kf[ks], s);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        dp = mfma(frag_row<D>(tg, lq, ks, h2), frag_row<D>(vt, 32 * w + lq, ks, h2), dp);
+        dp = mfma(frag_row_x<D>(tg, rbase, 0, ks), frag_row_x<D>(vt, rbase, 32 * w, ks), dp);
       const bool edge = qb + 32 > a.N || (CAUSAL && k0 + 32 * w + 31 > qb);
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
@@ -508,13 +566,17 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dkdv_kernel(AttnArgs a) 
         const bf16x8 pb = pfrag(s, s2), pd = pfrag(dp, s2);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          dv[db] = mfma(frag_tr<D>(tg, 16 * s2, 32 * db, lane), pb, dv[db]);
-          dk[db] = mfma(frag_tr<D>(tq, 16 * s2, 32 * db, lane), pd, dk[db]);
+          dv[db] = mfma(frag_tr_x<D>(tg, tb0, tb1, 16 * s2, 32 * db), pb, dv[db]);
+          dk[db] = mfma(frag_tr_x<D>(tq, tb0, tb1, 16 * s2, 32 * db), pd, dk[db]);
         }
       }
     }
     if (it + 1 < nqs) store(lds + (st ^ 1) * STG);
     __syncthreads();
+    };
+  for (int it = 0; it < nqs; it += 2) {
+    step(it, Stage<0>{});
+    if (it + 1 < nqs) step(it + 1, Stage<1>{});
   }
   if (live) {
     bf16_t* dst = a.d_qkv + (tok0 + kw) * ld + (long)hd * D;
