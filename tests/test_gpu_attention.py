@@ -315,3 +315,48 @@ def test_layer_with_attention_schedule():
         assert t(fwd_ev[2 * r + 1]) <= t(fwd_ev[2 * (R + r)]) + slack
     for nm in ("y", "x", "d_in", "dw_qkv", "dw_o", "dw1", "dw_gate"):
         assert torch.equal(getattr(traced, nm), getattr(plain, nm)), nm
+
+
+def test_layer_with_attention_deterministic_and_graph_replays():
+    """The layer with the attention in AT_r (R = 2): two streams equal one
+    stream bit for bit, two runs are bit-identical, and a fwd+bwd step
+    captured in a HIP graph replays bit-identical to the eager step, replay
+    after replay, with the outputs clobbered eagerly in between."""
+    need_gpu()
+    cfg = LAYER_CASES["fine_s"]
+    R = 2
+    inp = make_inputs(cfg)
+    names = ("x", "qkv", "attn", "lse", "logits", "topk_idx", "y", "dx", "d_attn", "d_qkv",
+             "delta", "d_in", "dw_qkv", "dw_o", "dw_gate", "dw1", "dw3", "dw2")
+
+    def run(two):
+        lay = _mha_layer(cfg, R, inp)
+        sc = torch.cuda.current_stream()
+        sm = torch.cuda.Stream() if two else sc
+        lay.forward(sc, sm)
+        lay.backward(sc, sm)
+        torch.cuda.synchronize()
+        return lay
+
+    a, b, c = run(True), run(False), run(True)
+    for nm in names:
+        assert torch.equal(getattr(a, nm), getattr(b, nm)), f"{nm}: two streams differ from one"
+        assert torch.equal(getattr(a, nm), getattr(c, nm)), f"{nm}: not deterministic"
+    layer = _mha_layer(cfg, R, inp)
+    bufs = layer.bufs()
+    gs, sm = torch.cuda.Stream(), torch.cuda.Stream()
+    layer.forward(gs, sm, bufs=bufs)  # (one-time set-up outside the capture)
+    layer.backward(gs, sm, bufs=bufs)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=gs):
+        layer.forward(gs, sm, bufs=bufs)
+        layer.backward(gs, sm, bufs=bufs)
+    for rep in range(3):
+        for nm in names:
+            getattr(layer, nm).fill_(7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for nm in names:
+            assert torch.equal(getattr(layer, nm), getattr(a, nm)), f"replay {rep}: {nm}"
