@@ -102,10 +102,10 @@ __device__ __forceinline__ void topk_write(float logit, int e, bool valid, int E
 
 // Top-k of one token's E logits by P consecutive lanes (P a power of two
 // <= 64). Lane p keeps the KM largest keys of logits p, p + P, ... in order
-// (an insertion without branches); then log2(P) exchanges with lane p ^ m
-// merge two sorted lists: the larger of a[j] and b[KM - 1 - j] for every j
-// gives the KM largest of both as a bitonic sequence, which half-cleaners
-// sort. Every lane ends with the same list; lane p == 0 writes.
+// (an insertion without branches); then log2(P) exchanges with a lane of
+// the other half of ever wider lane groups (lane_partner below) merge two
+// sorted lists (topk_merge). Every lane ends with the same list; lane p == 0
+// writes.
 template <int KM>
 __device__ __forceinline__ void topk_insert(uint64_t key, uint64_t (&tk)[KM]) {
   bool b[KM];
@@ -117,38 +117,140 @@ __device__ __forceinline__ void topk_insert(uint64_t key, uint64_t (&tk)[KM]) {
   tk[0] = b[0] ? key : tk[0];
 }
 
+// Exchange with a lane of the other half of an aligned group of 2 M lanes
+// (M < 16: DPP moves inside a row, no LDS round trip: M = 1 and 2 swap
+// neighbours and pairs of a quad, M = 4 and 8 mirror the halves of a row;
+// wider: lane ^ M). After exchanges M = 1, 2, ..., P / 2 of lists that are
+// merged (or values that are combined) at each step, every lane of an
+// aligned P-lane group holds the result of the whole group. All lanes of
+// the group must be active.
+template <int M>
+__device__ __forceinline__ uint32_t lane_partner(uint32_t v) {
+  if constexpr (M == 1) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+  else if constexpr (M == 2) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
+  else if constexpr (M == 4) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, false);
+  else if constexpr (M == 8) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, false);
+  else return __shfl_xor(v, M);
+}
+template <int M>
+__device__ __forceinline__ uint64_t key_partner(uint64_t key) {
+  const uint32_t lo = lane_partner<M>((uint32_t)key), hi = lane_partner<M>((uint32_t)(key >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+template <int M>
+__device__ __forceinline__ float sum_partner(float z) {
+  return z + __uint_as_float(lane_partner<M>(__float_as_uint(z)));
+}
+
+// one merge step: the partner's sorted list b, the larger of a[j] and
+// b[KM - 1 - j] for every j (the KM largest of both as a bitonic
+// sequence), then half-cleaners sort it
+template <int KM, int M>
+__device__ __forceinline__ void topk_merge(uint64_t (&tk)[KM]) {
+  uint64_t o[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) o[j] = key_partner<M>(tk[j]);
+#pragma unroll
+  for (int j = 0; j < KM; ++j) tk[j] = tk[j] > o[KM - 1 - j] ? tk[j] : o[KM - 1 - j];
+#pragma unroll
+  for (int d = KM / 2; d >= 1; d >>= 1)
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+      if ((j & d) == 0) {
+        const uint64_t a = tk[j], b = tk[j + d];
+        const bool up = a > b;  // (one compare for both selects)
+        tk[j] = up ? a : b;
+        tk[j + d] = up ? b : a;
+      }
+}
+
 template <int KM, int P>
 __device__ __forceinline__ void topk_lanes(const float* logit, int E, int k, int p, bool full,
                                            int32_t* idx_out, float* w_out) {
+  constexpr int NV = kMaxE / P;  // logits per lane at most
+  float v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = p + i * P < E ? logit[p + i * P] : 0.f;  // reads first
   uint64_t tk[KM];
 #pragma unroll
   for (int j = 0; j < KM; ++j) tk[j] = 0ull;
-  for (int e = p; e < E; e += P) topk_insert<KM>(sel_key(logit[e], e), tk);
 #pragma unroll
-  for (int m = 1; m < P; m <<= 1) {
-    uint64_t o[KM];
-#pragma unroll
-    for (int j = 0; j < KM; ++j) o[j] = shfl_xor_key(tk[j], m);
-#pragma unroll
-    for (int j = 0; j < KM; ++j) tk[j] = tk[j] > o[KM - 1 - j] ? tk[j] : o[KM - 1 - j];
-#pragma unroll
-    for (int d = KM / 2; d >= 1; d >>= 1)
-#pragma unroll
-      for (int j = 0; j < KM; ++j)
-        if ((j & d) == 0) {
-          const uint64_t hi = tk[j] > tk[j + d] ? tk[j] : tk[j + d];
-          const uint64_t lo = tk[j] > tk[j + d] ? tk[j + d] : tk[j];
-          tk[j] = hi;
-          tk[j + d] = lo;
-        }
-  }
+  for (int i = 0; i < NV; ++i)
+    if (p + i * P < E) topk_insert<KM>(sel_key(v[i], p + i * P), tk);
+  if constexpr (P > 1) topk_merge<KM, 1>(tk);
+  if constexpr (P > 2) topk_merge<KM, 2>(tk);
+  if constexpr (P > 4) topk_merge<KM, 4>(tk);
+  if constexpr (P > 8) topk_merge<KM, 8>(tk);
+  if constexpr (P > 16) topk_merge<KM, 16>(tk);
+  if constexpr (P > 32) topk_merge<KM, 32>(tk);
   float z = -1.f;
-  if (full) {  // the full softmax's sum: each lane its logits, then a butterfly
+  if (full) {  // the full softmax's sum: each lane its logits, then the exchanges
     const float v0 = key_value(tk[0]);
     z = 0.f;
-    for (int e = p; e < E; e += P) z += expf(logit[e] - v0);
 #pragma unroll
-    for (int m = 1; m < P; m <<= 1) z += __shfl_xor(z, m);
+    for (int i = 0; i < NV; ++i)
+      if (p + i * P < E) z += expf(v[i] - v0);
+    if constexpr (P > 1) z = sum_partner<1>(z);
+    if constexpr (P > 2) z = sum_partner<2>(z);
+    if constexpr (P > 4) z = sum_partner<4>(z);
+    if constexpr (P > 8) z = sum_partner<8>(z);
+    if constexpr (P > 16) z = sum_partner<16>(z);
+    if constexpr (P > 32) z = sum_partner<32>(z);
+  }
+  if (p == 0) topk_store<KM>(tk, k, z, idx_out, w_out);
+}
+
+// Top-k of one token's E logits by P >= 8 consecutive lanes (at most 8
+// logits per lane), the same selection as topk_lanes in fewer steps: each
+// lane sorts its own keys; then k rounds take the largest head over the
+// group (the exchanges of lane_partner) and the one lane holding that key
+// (keys are distinct) drops it. Lane p == 0 writes.
+template <int KM, int P>
+__device__ __forceinline__ void topk_extract(const float* logit, int E, int k, int p, bool full,
+                                             int32_t* idx_out, float* w_out) {
+  static_assert(P >= 8, "at most 8 logits per lane");
+  constexpr int NV = kMaxE / P;
+  float v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = p + i * P < E ? logit[p + i * P] : 0.f;  // reads first
+  uint64_t own[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) own[i] = 0ull;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (p + i * P < E) topk_insert<NV>(sel_key(v[i], p + i * P), own);
+  uint64_t tk[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    uint64_t best = own[0];
+    if (j < k) {  // (uniform; k <= E, so best is a real key)
+      uint64_t o;
+      o = key_partner<1>(best), best = o > best ? o : best;
+      o = key_partner<2>(best), best = o > best ? o : best;
+      o = key_partner<4>(best), best = o > best ? o : best;
+      if constexpr (P > 8) o = key_partner<8>(best), best = o > best ? o : best;
+      if constexpr (P > 16) o = key_partner<16>(best), best = o > best ? o : best;
+      if constexpr (P > 32) o = key_partner<32>(best), best = o > best ? o : best;
+      const bool pop = own[0] == best;
+#pragma unroll
+      for (int i = 0; i + 1 < NV; ++i) own[i] = pop ? own[i + 1] : own[i];
+      own[NV - 1] = pop ? 0ull : own[NV - 1];
+    }
+    tk[j] = best;  // (rounds past k are never stored)
+  }
+  float z = -1.f;
+  if (full) {  // the full softmax's sum: each lane its logits, then the exchanges
+    const float v0 = key_value(tk[0]);
+    z = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (p + i * P < E) z += expf(v[i] - v0);
+    z = sum_partner<1>(z);
+    z = sum_partner<2>(z);
+    z = sum_partner<4>(z);
+    if constexpr (P > 8) z = sum_partner<8>(z);
+    if constexpr (P > 16) z = sum_partner<16>(z);
+    if constexpr (P > 32) z = sum_partner<32>(z);
   }
   if (p == 0) topk_store<KM>(tk, k, z, idx_out, w_out);
 }
@@ -208,45 +310,49 @@ __global__ __launch_bounds__(kGateThreads) void gate_topk_kernel(
   }
 }
 
-// bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16). A block of 4 waves owns TGB
+// bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16). A block of NW waves owns TGB
 // groups of 16 tokens; the reduction over M is split between the waves: wave
-// w takes the 32-deep k steps s = w, w + 4, ... and needs only those steps'
+// w takes the 32-deep k steps s = w, w + NW, ... and needs only those steps'
 // W_g rows, so each wave streams on its own, with no block barrier until the
 // partial sums meet. Per step a lane loads 16 bytes of x for each token group
 // (8 consecutive k of one token: the A fragment as it lies in memory) and up
 // to NB 16-byte units of the step's 32 W_g rows; a ring of D steps of these
-// loads stays in flight in registers. The W_g rows of the next step go to
-// the wave's own LDS slice (two slices, alternating), from which each lane
-// gathers its B fragments (8 consecutive k of one expert) with 2-byte reads.
-// Every load is issued from a clamped in-bounds address and its value
-// zeroed when out of range (rows past M, tokens past T, steps past the
-// wave's last), so the ring never leaves registers. The four partial logit
-// tiles are summed in LDS in wave order (deterministic), the bias added, and
-// each token's top-k taken by a segment of EP lanes (E <= 16) or by P = 256 /
-// (16 TGB) lanes per token (wider gates).
+// loads stays in flight in registers, and no load is issued for a step past
+// the wave's last. A step's W_g rows go to the wave's own LDS slice (two
+// slices, alternating) one step ahead; each B fragment (8 consecutive k of
+// one expert) comes back as two transposing reads (ds_read_b64_tr_b16),
+// issued before the next step's rows are written, so that the MFMAs wait
+// for those reads only. Loads use clamped in-bounds addresses; rows past M
+// are staged as zeros and the slice columns past E are zeroed once, so the
+// accumulator columns past E hold zeros and are never written. The NW
+// partial logit tiles are summed in LDS in wave order (deterministic), the
+// bias added, and each token's top-k taken by a segment of EP lanes (E <=
+// 16) or by P = 256 / (16 TGB) lanes per token (wider gates) on the block's
+// first 256 lanes.
 constexpr int kGateTok = 16;  // tokens per group
 constexpr int kGateDepth = 4; // k steps of loads in flight per wave
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef short gv4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) gv4i16_t lds_gv4i16_t;
 
-
-// NB 16-expert column blocks (E <= 16 NB), TGB token groups per block, VEC:
-// E a multiple of 8 (W_g rows are whole 16-byte units)
-template <int NB, int TGB, bool VEC>
-__global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
+// NB 16-expert column blocks (E <= 16 NB), TGB token groups per block, NW
+// waves, VEC: E a multiple of 8 (W_g rows are whole 16-byte units)
+template <int NB, int TGB, int NW, bool VEC>
+__global__ __launch_bounds__(64 * NW) void gate_topk_mfma_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg, const float* __restrict__ bias,
     float* __restrict__ logits, int32_t* __restrict__ idx, float* __restrict__ w, int T, int M,
     int E, int k, int EP, int full) {
   constexpr int TB = kGateTok * TGB;           // tokens per block
   constexpr int PW = NB * 16 + 1;              // partial-tile row pitch (floats)
-  constexpr int PART_BYTES = 4 * TB * PW * 4;  // the four waves' partial tiles
-  // W_g slice: 32 rows at a pitch of 16 NB + 8 bf16, so a B fragment's eight
-  // rows are immediate offsets from one address and the lanes of the four k
-  // groups (rows 8 apart) fall on two bank sets instead of one
+  constexpr int PART_BYTES = NW * TB * PW * 4; // the waves' partial tiles
+  // W_g slice: 32 rows at a pitch of 16 NB + 8 bf16 (a multiple of 16
+  // bytes, so every transposing read is 8-byte aligned; the 16 spare bytes
+  // shift successive rows by 4 banks)
   constexpr int PITCH = 16 * NB + 8;
   constexpr int SLICE = 32 * PITCH + 8;  // bf16 per slice (+ a 16-byte slot for unused lanes)
-  constexpr int SLICE_BYTES = 4 * 2 * SLICE * 2;    // two slices per wave
+  constexpr int SLICE_BYTES = NW * 2 * SLICE * 2;  // two slices per wave
   constexpr int SMEM = PART_BYTES > SLICE_BYTES ? PART_BYTES : SLICE_BYTES;
   constexpr int D = kGateDepth;
   constexpr int WU = NB;  // 16-byte W_g units per lane per step: 32 rows * E / 8 <= 64 NB
@@ -259,17 +365,29 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
   const int t0 = blockIdx.x * TB;
   const int kq = (lane >> 4) * 8;  // k offset of this lane inside a step
   const bf16_t* xrow[TGB];
-  bool arow_ok[TGB];
 #pragma unroll
   for (int g = 0; g < TGB; ++g) {
     const int arow = t0 + g * kGateTok + (lane & 15);  // token whose A row this lane feeds
-    arow_ok[g] = arow < T;
-    xrow[g] = x + (long)(arow_ok[g] ? arow : 0) * M;
+    xrow[g] = x + (long)(arow < T ? arow : 0) * M;
   }
-  const int S = (M + 31) / 32;                       // k steps
-  const int nj = S > wave ? (S - wave + 3) / 4 : 0;  // this wave's steps: s = wave + 4 j
-  const int UR = E / 8;                              // 16-byte units per W_g row
-  const int n16 = 32 * UR;                           // units per step
+  const int S = (M + 31) / 32;                          // k steps
+  const int nj = S > wave ? (S - wave + NW - 1) / NW : 0;  // this wave's steps: s = wave + NW j
+  const int UR = E / 8;                                 // 16-byte units per W_g row
+  const int n16 = 32 * UR;                              // units per step
+  // transposing reads: in each 16-lane group q (= lane / 16) lane l aims at
+  // slice row 8 q + l / 4 (+ 4 for the second read), columns 4 (l % 4) .. + 3
+  // of a column block, and receives the group's 8 consecutive rows (k) of
+  // column l of the block: its B fragment, in the x fragment's k order
+  const int tr_off = ((8 * (lane >> 4) + ((lane & 15) >> 2)) * PITCH + 4 * (lane & 3)) * 2;
+
+  // columns past E of both slices: zero (the staging never writes them)
+  if (E < 16 * NB) {
+    const int pad = 16 * NB - E;
+    for (int q = lane; q < 64 * pad; q += 64) {
+      const int rr = q / pad, c = E + (q - rr * pad);
+      slices[(rr >> 5) * SLICE + (rr & 31) * PITCH + c] = (bf16_t)0;
+    }
+  }
 
   floatx4_t acc[TGB][NB];
 #pragma unroll
@@ -278,100 +396,106 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
     for (int nb = 0; nb < NB; ++nb) acc[g][nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
   u32x4_t xr[D][TGB], wr[D][WU];
-  // The wave's j-th step is s = wave + 4 ((j + rot) mod nj): blocks start at
-  // different k steps, so they do not all read the same W_g rows at once (on
-  // 16384 tokens at E = 8 that hot spot made the gate 1.5x slower). Steps
-  // past nj are dead.
+  // The wave's j-th step is s = wave + NW ((j + rot) mod nj): blocks start
+  // at different k steps, so they do not all read the same W_g rows at once
+  // (on 16384 tokens at E = 8 that hot spot made the gate 1.5x slower).
   const int rot = nj > 0 ? (int)(blockIdx.x % (unsigned)nj) : 0;
   auto step_of = [&](int j) {
     const int jj = j + rot;
-    return wave + 4 * (jj < nj ? jj : jj - nj);
+    return wave + NW * (jj < nj ? jj : jj - nj);
   };
-  // rows of W_g in the wave's step j: 0 past the last step
-  auto step_rows = [&](int j) { return j < nj ? min(32, M - step_of(j) * 32) : 0; };
-  // loads of step j into ring slot d. No value is masked here (a select
-  // would wait for the load): x of tokens past T only reaches logits that
-  // are not written, x past M meets W_g rows that are zero in LDS, and the
-  // W_g units past the step's rows are zeroed when staged.
+  // loads of step j into ring slot d; a step past the wave's last loads the
+  // last one's addresses again (L2 hits, never used), so that every step
+  // issues the same loads and the compiler's load counting stays exact. No
+  // value is masked here (a select would wait for the load): x of tokens
+  // past T only reaches logits that are not written, x past M meets W_g
+  // rows that are zero in LDS, and the W_g units past the step's rows are
+  // zeroed when staged.
   auto issue = [&](int d, int j) __attribute__((always_inline)) {
-    const int s = step_of(j);
+    const int s = step_of(j < nj ? j : nj - 1);
     const int kk = s * 32 + kq;
-    const int ko = (j < nj && kk < M) ? kk : 0;
+    const int ko = kk < M ? kk : 0;
 #pragma unroll
     for (int g = 0; g < TGB; ++g) xr[d][g] = *reinterpret_cast<const u32x4_t*>(xrow[g] + ko);
     // rows [32 s, 32 s + 32) of W_g are one contiguous range of 32 E values
     // (16-byte aligned: 64 E bytes per step)
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(wg + (j < nj ? (long)s * 32 * E : 0));
-    const int units = step_rows(j) * E / 8;  // whole 16-byte units inside W_g
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(wg + (long)s * 32 * E);
+    const int units = min(32, M - s * 32) * UR;  // whole 16-byte units inside W_g
 #pragma unroll
     for (int u = 0; u < WU; ++u) {
       const int q = lane + 64 * u;
       wr[d][u] = src[q < units ? q : 0];
     }
   };
-  // W_g rows of step j into slice b (rows past M zero; columns past E are
-  // never read)
+  // W_g rows of step j (< nj) into slice b (rows past M zero; columns past
+  // E keep their zeros)
   auto stage = [&](int d, int j, int b) __attribute__((always_inline)) {
     bf16_t* dst = slices + b * SLICE;
+    const int s = step_of(j);
+    const int rows = min(32, M - s * 32);
     if constexpr (VEC) {
-      const int units = step_rows(j) * UR;
+      const int units = rows * UR;
 #pragma unroll
       for (int u = 0; u < WU; ++u) {
         const int q = lane + 64 * u;
         const int r = q / UR, cu = q - r * UR;
         // (lanes past the slice's units write the spare slot: no branch)
-        *reinterpret_cast<u32x4_t*>(dst + (q < n16 ? r * PITCH + cu * 8 : 32 * PITCH)) =
-            q < units ? wr[d][u] : u32x4_t{0u, 0u, 0u, 0u};
+        bf16_t* p = dst + (q < n16 ? r * PITCH + cu * 8 : 32 * PITCH);
+        if (rows == 32)  // (uniform: every step but a last partial one)
+          *reinterpret_cast<u32x4_t*>(p) = wr[d][u];
+        else
+          *reinterpret_cast<u32x4_t*>(p) = q < units ? wr[d][u] : u32x4_t{0u, 0u, 0u, 0u};
       }
     } else {  // element by element (E not a multiple of 8)
-      const int s = step_of(j);
       for (int q = lane; q < 32 * E; q += 64) {
         const int r = q / E, e = q - r * E;
         const int row = s * 32 + r;
-        dst[r * PITCH + e] = (j < nj && row < M) ? wg[(long)row * E + e] : (bf16_t)0;
+        dst[r * PITCH + e] = row < M ? wg[(long)row * E + e] : (bf16_t)0;
       }
     }
   };
   // (the LDS operations of one wave complete in order; the fence keeps the
-  // compiler from moving a slice's reads above other lanes' writes to it,
-  // or its next writes above the reads)
+  // compiler from moving a slice's reads below the next writes to it, or
+  // the writes above the reads)
   auto lds_fence = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   };
 
+  if (nj > 0) {  // (uniform)
 #pragma unroll
-  for (int d = 0; d < D; ++d) issue(d, d);
-  stage(0, 0, 0);
-  lds_fence();
-  // (steps past the wave's last, up to a multiple of D, add exact zeros:
-  // their W_g rows are staged as zeros and their x loads read real x)
+    for (int d = 0; d < D; ++d) issue(d, d);
+    stage(0, 0, 0);
+    lds_fence();
+  }
   for (int j0 = 0; j0 < nj; j0 += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int j = j0 + d;
-      {
-        // next step's W_g rows into the other slice
-        stage((d + 1) % D, j + 1, (d + 1) & 1);
-        const bf16_t* sb = slices + (d & 1) * SLICE;
+      if (j < nj) {  // (uniform)
+        const char* sb = reinterpret_cast<const char*>(slices + (d & 1) * SLICE) + tr_off;
+        bf16x8_t bfr[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          const int e = nb * 16 + (lane & 15);
-          const bf16_t* bp = sb + kq * PITCH + e;
-          uint32_t u[4];
+          const gv4i16_t lo =
+              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_gv4i16_t*)(sb + 32 * nb));
+          const gv4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_gv4i16_t*)(sb + 32 * nb + 8 * PITCH));
+          const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3],
+                                                               hi[0], hi[1], hi[2], hi[3]};
+          bfr[nb] = __builtin_bit_cast(bf16x8_t, v);
+        }
+        lds_fence();
+        // next step's W_g rows into the other slice
+        if (j + 1 < nj) stage((d + 1) % D, j + 1, (d + 1) & 1);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const uint32_t lo = bp[(2 * q) * PITCH], hi = bp[(2 * q + 1) * PITCH];
-            u[q] = e < E ? lo | (hi << 16) : 0u;  // columns past E were never written
-          }
-          const bf16x8_t bfr = __builtin_bit_cast(bf16x8_t, make_uint4(u[0], u[1], u[2], u[3]));
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
           for (int g = 0; g < TGB; ++g)
             acc[g][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, xr[d][g]), bfr, acc[g][nb], 0, 0, 0);
-        }
-        issue(d, j + D);
-        lds_fence();
+                __builtin_bit_cast(bf16x8_t, xr[d][g]), bfr[nb], acc[g][nb], 0, 0, 0);
       }
+      issue(d, j + D);
+      lds_fence();
     }
   }
   // the slices overlap other waves' partial tiles
@@ -385,34 +509,40 @@ __global__ __launch_bounds__(256) void gate_topk_mfma_kernel(
       for (int r = 0; r < 4; ++r)
         part[wave][g * kGateTok + (lane >> 4) * 4 + r][nb * 16 + (lane & 15)] = acc[g][nb][r];
   __syncthreads();
-  // sum the four partial tiles in wave order; bias; logits out
-  for (int q = tid; q < TB * E; q += 256) {
+  // sum the partial tiles in wave order; bias; logits out
+  for (int q = tid; q < TB * E; q += 64 * NW) {
     const int tt = q / E, e = q % E;
-    float l = part[0][tt][e] + part[1][tt][e];
-    l += part[2][tt][e];
-    l += part[3][tt][e];
+    float l = part[0][tt][e];
+#pragma unroll
+    for (int v = 1; v < NW; ++v) l += part[v][tt][e];
     if (bias != nullptr) l += bias[e];
     part[0][tt][e] = l;
     if (t0 + tt < T) logits[(long)(t0 + tt) * E + e] = l;
   }
   __syncthreads();
   if (E > 16) {
-    // top-k: the block's 256 lanes, P per token, logits read from LDS
+    // top-k: the block's first 256 lanes, P per token, logits read from LDS
     constexpr int P = 256 / TB;
     const int tt = tid / P, p = tid % P, t = t0 + tt;
-    if (t < T) {  // (whole P-lane groups: T bounds tokens, P divides 64)
+    if (tid < 256 && t < T) {  // (whole P-lane groups: T bounds tokens, P divides 64)
       int32_t* io = idx + (long)t * k;
       float* wo = w + (long)t * k;
-      if (k <= 2) topk_lanes<2, P>(part[0][tt], E, k, p, full, io, wo);
-      else if (k <= 4) topk_lanes<4, P>(part[0][tt], E, k, p, full, io, wo);
-      else topk_lanes<8, P>(part[0][tt], E, k, p, full, io, wo);
+      if constexpr (P >= 8) {
+        if (k <= 2) topk_extract<2, P>(part[0][tt], E, k, p, full, io, wo);
+        else if (k <= 4) topk_extract<4, P>(part[0][tt], E, k, p, full, io, wo);
+        else topk_extract<8, P>(part[0][tt], E, k, p, full, io, wo);
+      } else {
+        if (k <= 2) topk_lanes<2, P>(part[0][tt], E, k, p, full, io, wo);
+        else if (k <= 4) topk_lanes<4, P>(part[0][tt], E, k, p, full, io, wo);
+        else topk_lanes<8, P>(part[0][tt], E, k, p, full, io, wo);
+      }
     }
   } else {
     // top-k: segments of EP <= 16 lanes, one token per segment per round
     const int G = 64 / EP;
     const int seg = lane / EP, e = lane % EP;
     const bool evalid = e < E;
-    for (int i = wave * G + seg; i < TB; i += 4 * G) {
+    for (int i = wave * G + seg; i < TB; i += NW * G) {
       const int t = t0 + i;
       if (t >= T) break;  // uniform across the segment
       const float l = evalid ? part[0][i][e] : 0.f;
@@ -431,6 +561,13 @@ inline int gate_groups_per_block(int T, int E) {
   if (groups >= 1024) return 4;
   if (groups >= 512) return 2;
   return 1;
+}
+
+// waves per block: wide gates with blocks of one token group split M
+// eight ways
+inline int gate_waves(int T, int E, int tgb) {
+  (void)T;
+  return tgb == 1 && E > 16 ? 8 : 4;
 }
 
 __global__ __launch_bounds__(kGateThreads) void route_kernel(const float* __restrict__ logits,
@@ -782,24 +919,27 @@ hipError_t launch_gate_topk(const Shape& s, const void* x, const void* w_gate, c
     const int NB = (s.E + 15) / 16;
     const int TGB = gate_groups_per_block(s.T, s.E);
     const int blocks = (s.T + kGateTok * TGB - 1) / (kGateTok * TGB);
+    const int NW = gate_waves(s.T, s.E, TGB);
     return traced(FLOWMOE_K_GATE, st, [&] {
-#define FLOWMOE_GATE_KERNEL(NBV, TGBV, VECV)                                                      \
-  hipLaunchKernelGGL((gate_topk_mfma_kernel<NBV, TGBV, VECV>), dim3(blocks), dim3(256), 0, st,    \
-                     (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T, s.M, s.E, \
-                     s.k, EP, full)
-#define FLOWMOE_GATE_LAUNCH(NBV, TGBV)                              \
-  do {                                                              \
-    if (s.E % 8 == 0) FLOWMOE_GATE_KERNEL(NBV, TGBV, true);        \
-    else FLOWMOE_GATE_KERNEL(NBV, TGBV, false);                    \
+#define FLOWMOE_GATE_KERNEL(NBV, TGBV, NWV, VECV)                                                 \
+  hipLaunchKernelGGL((gate_topk_mfma_kernel<NBV, TGBV, NWV, VECV>), dim3(blocks), dim3(64 * NWV), \
+                     0, st, (const bf16_t*)x, (const bf16_t*)w_gate, bias, logits, idx, w, s.T,   \
+                     s.M, s.E, s.k, EP, full)
+#define FLOWMOE_GATE_LAUNCH(NBV, TGBV, NWV)                          \
+  do {                                                               \
+    if (s.E % 8 == 0) FLOWMOE_GATE_KERNEL(NBV, TGBV, NWV, true);    \
+    else FLOWMOE_GATE_KERNEL(NBV, TGBV, NWV, false);                \
   } while (0)
-#define FLOWMOE_GATE_NB(TGBV)                  \
-  if (NB == 1) FLOWMOE_GATE_LAUNCH(1, TGBV);   \
-  else if (NB == 2) FLOWMOE_GATE_LAUNCH(2, TGBV); \
-  else if (NB == 3) FLOWMOE_GATE_LAUNCH(3, TGBV); \
-  else FLOWMOE_GATE_LAUNCH(4, TGBV);
-      if (TGB == 1) { FLOWMOE_GATE_NB(1) }
-      else if (TGB == 2) { FLOWMOE_GATE_NB(2) }
-      else { FLOWMOE_GATE_NB(4) }
+#define FLOWMOE_GATE_NB(TGBV, NWV)                     \
+  if (NB == 1) FLOWMOE_GATE_LAUNCH(1, TGBV, NWV);      \
+  else if (NB == 2) FLOWMOE_GATE_LAUNCH(2, TGBV, NWV); \
+  else if (NB == 3) FLOWMOE_GATE_LAUNCH(3, TGBV, NWV); \
+  else FLOWMOE_GATE_LAUNCH(4, TGBV, NWV);
+      if (TGB == 1) {
+        if (NW == 8) { FLOWMOE_GATE_NB(1, 8) }
+        else { FLOWMOE_GATE_NB(1, 4) }
+      } else if (TGB == 2) { FLOWMOE_GATE_NB(2, 4) }
+      else { FLOWMOE_GATE_NB(4, 4) }
 #undef FLOWMOE_GATE_NB
 #undef FLOWMOE_GATE_LAUNCH
 #undef FLOWMOE_GATE_KERNEL

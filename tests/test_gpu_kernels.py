@@ -46,11 +46,14 @@ def test_gate_topk(E, k, dtype):
     assert np.allclose(gl[0], host(bias))
 
 
-@pytest.mark.parametrize("T,M,E,k", [(77, 520, 64, 6), (130, 1000, 33, 3), (40, 4104, 8, 2)])
+@pytest.mark.parametrize("T,M,E,k", [(77, 520, 64, 6), (130, 1000, 33, 3), (40, 4104, 8, 2),
+                                   (200, 2056, 64, 6), (300, 1096, 8, 2)])
 def test_gate_topk_chunked_weights(T, M, E, k):
     """W_g taller than one LDS chunk of the bf16 gate (32 KB of rows at a pitch
     of 16 * ceil(E / 16) + 8: 224 rows at E = 64, 288 at E = 33 (copied
-    element by element), 672 at E = 8), with a ragged last chunk."""
+    element by element), 672 at E = 8), with a ragged last chunk; M = 2056
+    and 1096: 65 and 35 k steps of 32 over the waves of one-group blocks,
+    the last step 8 rows deep."""
     need_gpu()
     cfg = get_config("balanced", T=T, M=M, H=8, E=E, k=k, dtype="bf16", seed=M + E)
     inp = make_inputs(cfg, with_dy=False)
