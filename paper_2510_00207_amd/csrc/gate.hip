@@ -744,23 +744,23 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_kernel(
 }
 
 // bf16 layers: d_logits of 64 tokens per block, written as float (the
-// output) and as a bf16 pair hi + lo per value (hi = bf16(dl), lo =
-// bf16(dl - hi): about 16 significant bits) in rows [hi(E4) | lo(E4)] for
-// the dW_g GEMM; db partials per block (token order); block 0 also writes
-// the row counts and offsets of the GEMM's token splits.
+// output) and, for the full softmax gate's GEMM path, as a bf16 pair hi + lo
+// per value (hi = bf16(dl), lo = bf16(dl - hi): about 16 significant bits)
+// in rows [hi(E4) | lo(E4)]; db partials per block (token order); block 0
+// also writes the row counts and offsets of that GEMM's token splits.
 constexpr int kDlTok = 64;
-__global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
-    const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
-    const float* __restrict__ logits, float* __restrict__ d_logits, bf16_t* __restrict__ dlhl,
-    float* __restrict__ Pb, int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int T,
-    int E, int E4, int k, int S, int tps, int full) {
-  // dense tile of the block's d_logits rows (odd pitch: column sums and row
+__device__ __forceinline__ void dl_rows(
+    int blk, float (*tile)[kMaxE + 1], const int32_t* __restrict__ idx,
+    const float* __restrict__ w, const float* __restrict__ dw, const float* __restrict__ logits,
+    float* __restrict__ d_logits, bf16_t* __restrict__ dlhl, float* __restrict__ Pb,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int T, int E, int E4, int k,
+    int S, int tps, int full) {
+  // (dense tile of the block's d_logits rows; odd pitch: column sums and row
   // writes both spread over the banks)
-  __shared__ float tile[kDlTok][kMaxE + 1];
   const int tid = threadIdx.x;
-  const long t0 = (long)blockIdx.x * kDlTok;
+  const long t0 = (long)blk * kDlTok;
   for (int q = tid; q < kDlTok * (kMaxE + 1); q += 256) (&tile[0][0])[q] = 0.f;
-  if (blockIdx.x == 0 && tid < S) {
+  if (counts != nullptr && blk == 0 && tid < S) {
     const long r0 = (long)tid * tps;
     counts[tid] = (int32_t)(r0 < T ? min((long)tps, T - r0) : 0);
     offsets[tid] = (int32_t)(r0 < T ? r0 : T);
@@ -798,14 +798,233 @@ __global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
     if (t >= T) break;
     const float v = tile[tt][e];
     if (e < E) d_logits[t * E + e] = v;
-    const bf16_t hi = f32_to_bf16(v);
-    dlhl[t * 2 * E4 + e] = hi;
-    dlhl[t * 2 * E4 + E4 + e] = f32_to_bf16(v - bf16_to_f32(hi));
+    if (dlhl != nullptr) {
+      const bf16_t hi = f32_to_bf16(v);
+      dlhl[t * 2 * E4 + e] = hi;
+      dlhl[t * 2 * E4 + E4 + e] = f32_to_bf16(v - bf16_to_f32(hi));
+    }
   }
   if (tid < E) {
     float v = 0.f;
     for (int tt = 0; tt < kDlTok; ++tt) v += tile[tt][tid];  // rows past T are zero
-    Pb[(long)blockIdx.x * E + tid] = v;
+    Pb[(long)blk * E + tid] = v;
+  }
+}
+
+__global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ w, const float* __restrict__ dw,
+    const float* __restrict__ logits, float* __restrict__ d_logits, bf16_t* __restrict__ dlhl,
+    float* __restrict__ Pb, int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int T,
+    int E, int E4, int k, int S, int tps, int full) {
+  __shared__ float tile[kDlTok][kMaxE + 1];
+  dl_rows(blockIdx.x, tile, idx, w, dw, logits, d_logits, dlhl, Pb, counts, offsets, T, E, E4, k,
+          S, tps, full);
+}
+
+// dW_g of the renormalised bf16 gate on MFMA (v_mfma_f32_16x16x32_bf16),
+// one launch with the d_logits rows. Blocks [0, ndl) are dl_rows blocks
+// (d_logits, db partials per 64 tokens). Each other block takes MT columns
+// m0 .. m0 + MT - 1 of x (rows of dW_g) over one token split [tb, te) and
+// computes, in chunks of 64 tokens,
+//   Q[r][m] = sum over the chunk's tokens t of D[r][t] x[t][m],
+// where row r = 2 e + h of D holds the bf16 part hi (h = 0) or the rest lo
+// (h = 1) of d_logits[t][e] (hi = bf16(dl), lo = bf16(dl - hi): about 16
+// significant bits; zero for experts a token did not select), and finally
+// P[split][m][e] = Q[2 e][m] + Q[2 e + 1][m], summed over the splits in
+// order by the reduce launch. Per chunk: every thread computes the d_logits
+// of its token's selection (4 threads a token, two entries each, the sum s
+// over the k entries in entry order as token_dl takes it, the entries
+// gathered from the quad by DPP) and stores its part of the x tile (loaded
+// kDwDepth chunks ahead in registers); a barrier; it writes its entries
+// into D and clears the previous chunk's from the other D buffer (both D
+// buffers start zero, so only entries are ever written); a barrier; each
+// wave multiplies its row tiles of D (A operand, 16-byte row reads: 8
+// consecutive tokens of one row) by its 16 columns of the x tile (B
+// operand, two transposing reads: 8 consecutive tokens of one column). D and
+// the x tile are double-buffered, so one chunk's writes never meet the
+// previous chunk's reads. Every load is issued unconditionally from a
+// clamped address (tokens past the split: its first token, whose entries
+// are not used; columns past M: column 0, whose results are not written).
+constexpr int kDwTok = 64;    // tokens per chunk
+constexpr int kDwDepth = 4;   // chunks of loads in flight
+constexpr int kDwDPitch = 72; // bf16 per row of D (64 tokens + 8: 16-byte aligned rows, 4 banks apart)
+
+template <int S_>
+__device__ __forceinline__ float quad_bcast(float v) {  // lane S_ of each quad
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), S_ * 0x55, 0xF, 0xF, false));
+}
+
+// NR 16-row tiles of D (2 E <= 16 NR); kDwCols columns of x per block, each
+// wave one 16-column tile and every row tile (32 columns, each wave half of
+// the row tiles, measured 5-10% slower at E = 64)
+constexpr int kDwCols = 64;
+template <int NR>
+__global__ __launch_bounds__(256) void gate_dw_mfma_kernel(
+    const bf16_t* __restrict__ x, const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const float* __restrict__ dw, float* __restrict__ d_logits, float* __restrict__ P,
+    float* __restrict__ Pb, int T, int M, int E, int k, int tps, int mtiles, int ndl) {
+  constexpr int MT = kDwCols;
+  constexpr int XP = MT + 8;                // bf16 per x tile row
+  constexpr int XT = kDwTok * XP;           // bf16 per x tile
+  constexpr int DT = 16 * NR * kDwDPitch;   // bf16 per D tile
+  constexpr int XPT = MT / 32;              // 16-byte x pieces per thread and chunk
+  constexpr int CPR = MT / 8;               // 16-byte pieces per token row
+  constexpr int CT = MT / 16;               // column tiles
+  constexpr int WG = 4 / CT;                // wave groups over the row tiles
+  constexpr int RT = NR / WG;               // row tiles per wave
+  static_assert(RT >= 1 && RT * WG == NR, "row tiles split evenly over the wave groups");
+  constexpr int DW_BYTES = 2 * (XT + DT) * 2;
+  constexpr int DL_BYTES = kDlTok * (kMaxE + 1) * 4;
+  constexpr int D = kDwDepth;
+  typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+  __shared__ __attribute__((aligned(16))) char smem[DW_BYTES > DL_BYTES ? DW_BYTES : DL_BYTES];
+  if ((int)blockIdx.x < ndl) {  // (uniform)
+    dl_rows(blockIdx.x, reinterpret_cast<float(*)[kMaxE + 1]>(smem), idx, w, dw, nullptr, d_logits,
+            nullptr, Pb, nullptr, nullptr, T, E, E, k, 0, 0, 0);
+    return;
+  }
+  const int blk = blockIdx.x - ndl;
+  const int mt = blk % mtiles, sp = blk / mtiles;
+  const int m0 = mt * MT;
+  const int tb = sp * tps, te = min(T, tb + tps);  // (tb < T: every split holds tokens)
+  const int nch = (te - tb + kDwTok - 1) / kDwTok;
+  bf16_t* xt = reinterpret_cast<bf16_t*>(smem);  // [2][kDwTok][XP]: tokens x columns
+  bf16_t* dt = xt + 2 * XT;                      // [2][16 NR][kDwDPitch]: rows r x tokens
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ct = wave % CT, rg = wave / CT;
+  // x: XPT 16-byte pieces a thread, tokens tid / CPR + (256 / CPR) h of the
+  // chunk, columns m0 + xc .. + 7
+  const int xc = 8 * (tid % CPR);
+  const int xm = m0 + xc < M ? m0 + xc : 0;
+  // selection: token st of the chunk, entries q and q + 4
+  const int st = tid >> 2, q = tid & 3;
+  const int ja = q < k ? q : 0, jb = q + 4 < k ? q + 4 : 0;
+
+  u32x4_t xr[D][XPT];
+  int32_t ir[D][2];
+  float wr[D][2], dr[D][2];
+  auto issue = [&](int d, int c) __attribute__((always_inline)) {
+    const int tc = tb + (c < nch ? c : nch - 1) * kDwTok;
+#pragma unroll
+    for (int h = 0; h < XPT; ++h) {
+      const int t = tc + tid / CPR + (256 / CPR) * h;
+      xr[d][h] = *reinterpret_cast<const u32x4_t*>(x + (long)(t < te ? t : tb) * M + xm);
+    }
+    const int t = tc + st;
+    const long r = (long)(t < te ? t : tb) * k;
+    ir[d][0] = idx[r + ja];
+    ir[d][1] = idx[r + jb];
+    wr[d][0] = w[r + ja];
+    wr[d][1] = w[r + jb];
+    dr[d][0] = dw[r + ja];
+    dr[d][1] = dw[r + jb];
+  };
+
+  // both D buffers zero
+  for (int u = tid; u < 2 * DT / 8; u += 256)
+    reinterpret_cast<u32x4_t*>(dt)[u] = u32x4_t{0u, 0u, 0u, 0u};
+  floatx4_t acc[RT];
+#pragma unroll
+  for (int i = 0; i < RT; ++i) acc[i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  // transposing reads of the x tile: lane l aims at token 8 (l / 16) + (l %
+  // 16) / 4 (+ 4 for the second read) of a 32-token step, columns 16 ct +
+  // 4 (l % 4) .. + 3, and receives 8 consecutive tokens of column 16 ct + l % 16
+  const int tr_off = ((8 * (lane >> 4) + ((lane & 15) >> 2)) * XP + 16 * ct + 4 * (lane & 3)) * 2;
+  // row reads of D: row l % 16 of a tile, tokens 8 (l / 16) .. + 7 of a step
+  const int a_off = (((16 * RT * rg) + (lane & 15)) * kDwDPitch + 8 * (lane >> 4)) * 2;
+  // D positions this thread wrote for the previous chunk (-1: none)
+  int pa = -1, pb = -1;
+
+  // chunk c from ring slot d
+  auto chunk = [&](int d, int c) __attribute__((always_inline)) {
+    bf16_t* xb = xt + (c & 1) * XT;
+    bf16_t* db = dt + (c & 1) * DT;
+    // d_logits of this thread's two entries, as token_dl computes them
+    float wv[kMaxK], dv[kMaxK];
+    wv[0] = quad_bcast<0>(wr[d][0]), dv[0] = quad_bcast<0>(dr[d][0]);
+    wv[1] = quad_bcast<1>(wr[d][0]), dv[1] = quad_bcast<1>(dr[d][0]);
+    wv[2] = quad_bcast<2>(wr[d][0]), dv[2] = quad_bcast<2>(dr[d][0]);
+    wv[3] = quad_bcast<3>(wr[d][0]), dv[3] = quad_bcast<3>(dr[d][0]);
+    wv[4] = quad_bcast<0>(wr[d][1]), dv[4] = quad_bcast<0>(dr[d][1]);
+    wv[5] = quad_bcast<1>(wr[d][1]), dv[5] = quad_bcast<1>(dr[d][1]);
+    wv[6] = quad_bcast<2>(wr[d][1]), dv[6] = quad_bcast<2>(dr[d][1]);
+    wv[7] = quad_bcast<3>(wr[d][1]), dv[7] = quad_bcast<3>(dr[d][1]);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+      if (j < k) s += wv[j] * dv[j];
+    const float dla = wr[d][0] * (dr[d][0] - s), dlb = wr[d][1] * (dr[d][1] - s);
+    const bool live = tb + c * kDwTok + st < te;
+    const int ea = ir[d][0], eb = ir[d][1];
+    const int na = live && q < k && ea >= 0 && ea < E ? 2 * ea * kDwDPitch + st : -1;
+    const int nb = live && q + 4 < k && eb >= 0 && eb < E ? 2 * eb * kDwDPitch + st : -1;
+#pragma unroll
+    for (int h = 0; h < XPT; ++h)
+      *reinterpret_cast<u32x4_t*>(xb + (tid / CPR + (256 / CPR) * h) * XP + xc) = xr[d][h];
+    __syncthreads();
+    // the previous chunk's entries out of the other D buffer, this chunk's
+    // in (a token's selected experts are distinct)
+    bf16_t* dp = dt + ((c + 1) & 1) * DT;
+    if (pa >= 0) dp[pa] = dp[pa + kDwDPitch] = (bf16_t)0;
+    if (pb >= 0) dp[pb] = dp[pb + kDwDPitch] = (bf16_t)0;
+    if (na >= 0) {
+      const bf16_t hi = f32_to_bf16(dla);
+      db[na] = hi;
+      db[na + kDwDPitch] = f32_to_bf16(dla - bf16_to_f32(hi));
+    }
+    if (nb >= 0) {
+      const bf16_t hi = f32_to_bf16(dlb);
+      db[nb] = hi;
+      db[nb + kDwDPitch] = f32_to_bf16(dlb - bf16_to_f32(hi));
+    }
+    pa = na, pb = nb;
+    __syncthreads();
+    const char* xbc = reinterpret_cast<const char*>(xb);
+    const char* dbc = reinterpret_cast<const char*>(db);
+#pragma unroll
+    for (int ks = 0; ks < kDwTok / 32; ++ks) {
+      const char* bp = xbc + tr_off + ks * 32 * XP * 2;
+      const gv4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_gv4i16_t*)bp);
+      const gv4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_gv4i16_t*)(bp + 8 * XP));
+      const short __attribute__((ext_vector_type(8))) bv = {lo[0], lo[1], lo[2], lo[3],
+                                                            hi[0], hi[1], hi[2], hi[3]};
+      const bf16x8_t bfr = __builtin_bit_cast(bf16x8_t, bv);
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        const bf16x8_t afr = *reinterpret_cast<const bf16x8_t*>(
+            dbc + a_off + (16 * i * kDwDPitch + 32 * ks) * 2);
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr, acc[i], 0, 0, 0);
+      }
+    }
+  };
+
+#pragma unroll
+  for (int d = 0; d < D; ++d) issue(d, d);
+  // whole rounds of D chunks without branches (the compiler's load counting
+  // stays exact), each chunk's slot reloaded D chunks ahead; then the last
+  // chunks, nothing more to load
+  int c0 = 0;
+  for (; c0 + D <= nch; c0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      chunk(d, c0 + d);
+      issue(d, c0 + d + D);
+    }
+  }
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+    if (c0 + d < nch) chunk(d, c0 + d);  // (uniform)
+  // acc[i][j]: Q row 16 (RT rg + i) + 4 (lane / 16) + j, column m0 + 16 ct + lane % 16
+  const int m = m0 + 16 * ct + (lane & 15);
+  if (m < M) {
+    float* pr = P + ((long)sp * M + m) * E;
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int i2 = 0; i2 < 2; ++i2) {
+        const int e = 8 * (RT * rg + i) + 2 * (lane >> 4) + i2;
+        if (e < E) pr[e] = acc[i][2 * i2] + acc[i][2 * i2 + 1];
+      }
   }
 }
 
@@ -824,10 +1043,13 @@ __global__ __launch_bounds__(256) void gate_wstack_kernel(const bf16_t* __restri
 
 // dW_g[m][e] = sum over splits of P[s][m][e] (split order; rows of pitch
 // ldp), plus the same sum over column lo_off + e when lo_off >= 0 (the lo
-// halves of the bf16 path); db = sum over the SB rows of Pb
-// Blocks past the reduction's (wt_block and on, when wg is given) copy W_g
-// (M x E) to W_g^T (E x M) in the layer dtype for the dx term: one launch
-// less than a kernel of its own.
+// halves of the bf16 path), one thread an element, in blocks [0, nw) (nw =
+// ceil(M E / 256)); db[e] = sum over the SB rows of Pb, block nw + e: each
+// thread the rows i, i + 256, ... in order, then a fixed pairwise tree (a
+// lone thread's serial sum over thousands of rows took tens of us).
+// Blocks past the reduction's (wt_block = nw + E and on, when wg is given)
+// copy W_g (M x E) to W_g^T (E x M) in the layer dtype for the dx term: one
+// launch less than a kernel of its own.
 __global__ __launch_bounds__(256) void gate_bwd_dw_reduce_kernel(
     const float* __restrict__ P, const float* __restrict__ Pb, float* __restrict__ dw_gate,
     float* __restrict__ dbias, int M, int E, int S, int ldp, int lo_off, int SB, int accumulate,
@@ -843,8 +1065,24 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_reduce_kernel(
       static_cast<float*>(wgt)[r] = static_cast<const float*>(wg)[m * E + e];
     return;
   }
+  const int nw = (int)((n + 255) / 256);
+  if ((int)blockIdx.x >= nw) {
+    const int e = (int)blockIdx.x - nw;
+    if (e >= E || dbias == nullptr) return;  // (uniform)
+    __shared__ float red[256];
+    const int tid = threadIdx.x;
+    float v = 0.f;
+    for (int s = tid; s < SB; s += 256) v += Pb[(long)s * E + e];
+    red[tid] = v;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+      if (tid < off) red[tid] += red[tid + off];
+      __syncthreads();
+    }
+    if (tid == 0) dbias[e] = accumulate ? dbias[e] + red[0] : red[0];
+    return;
+  }
   const long q = blockIdx.x * 256L + threadIdx.x;
-  if (q >= n + E) return;
   if (q < n) {
     const long m = q / E, e = q % E;
     const long stride = (long)M * ldp;
@@ -859,11 +1097,6 @@ __global__ __launch_bounds__(256) void gate_bwd_dw_reduce_kernel(
       v += vl;
     }
     dw_gate[q] = accumulate ? dw_gate[q] + v : v;
-  } else if (q < n + E && dbias != nullptr) {
-    const int e = (int)(q - n);
-    float v = 0.f;
-    for (int s = 0; s < SB; ++s) v += Pb[(long)s * E + e];
-    dbias[e] = accumulate ? dbias[e] + v : v;
   }
 }
 
@@ -876,12 +1109,31 @@ int gate_eg(int E) { return E <= 8 ? 1 : E <= 16 ? 2 : E <= 32 ? 4 : 8; }
 // bf16 path: the GEMM's column count (hi and lo halves of E rounded up to 4)
 int gate_dw_cols(int E) { return 2 * ((E + 3) / 4 * 4); }
 
-// bf16 gates with E <= 16 over at most 8 M elements of x take the
-// register-tile kernel (one launch and a reduce; at these sizes launch
-// latency dominates); the others d_logits, then dW_g as a GEMM
-bool gate_dw_on_gemm(const Shape& s) {
-  if (s.gate == FLOWMOE_GATE_FULL) return true;  // (bf16 only: dense d_logits for the dx GEMM)
-  return s.dtype == FLOWMOE_BF16 && (s.E > 16 || (long)s.T * s.M > (8L << 20));
+// dW_g paths: the renormalised bf16 gate takes the MFMA kernel (d_logits
+// rows and dW_g partials in one launch, then the reduce); the full softmax
+// gate d_logits, then dW_g as a GEMM (its hi/lo rows also feed the dense dx
+// GEMM); fp32 gates the register-tile kernel
+bool gate_dw_on_mfma(const Shape& s) {
+  return s.dtype == FLOWMOE_BF16 && s.gate != FLOWMOE_GATE_FULL;
+}
+bool gate_dw_on_gemm(const Shape& s) { return s.gate == FLOWMOE_GATE_FULL; }
+
+// MFMA path: token splits (multiples of 64 tokens): about two blocks per
+// CU over the 64-column tiles, partials (splits x M x E floats) at most a
+// quarter of x's bytes
+int gate_dwm_tps(const Shape& s) {
+  const long mtiles = (s.M + kDwCols - 1) / kDwCols;
+  long sp = (512 + mtiles - 1) / mtiles;
+  const long by_bytes = s.T / (8L * s.E), by_chunks = (s.T + kDwTok - 1) / kDwTok;
+  if (sp > by_bytes) sp = by_bytes;
+  if (sp > by_chunks) sp = by_chunks;
+  if (sp < 1) sp = 1;
+  const long tps = (s.T + sp - 1) / sp;
+  return (int)((tps + kDwTok - 1) / kDwTok * kDwTok);
+}
+int gate_dwm_splits(const Shape& s) {
+  const int tps = gate_dwm_tps(s);
+  return s.T > 0 ? (s.T + tps - 1) / tps : 1;
 }
 
 // GEMM path: token splits of the dW_g GEMM (its pseudo-experts): about 256
@@ -971,8 +1223,9 @@ hipError_t launch_route(const Shape& s, const float* logits, int32_t* idx, float
 }
 
 // workspace: [W_g^T (E x M float) | P | Pb | GEMM path: dl hi/lo (T x N bf16),
-// split counts and offsets (S int32 each)]; register-tile path: P (S x M x E),
-// Pb (S x E); GEMM path: P (S x M x N, N = gate_dw_cols(E)), Pb (ceil(T/64) x E)
+// split counts and offsets (S int32 each)]; MFMA path: P (S x M x E), Pb
+// (ceil(T/64) x E); register-tile path: P (S x M x E), Pb (S x E); GEMM path:
+// P (S x M x N, N = gate_dw_cols(E)), Pb (ceil(T/64) x E)
 size_t gate_wt_bytes(const Shape& s) { return align256((size_t)s.M * s.E * sizeof(float)); }
 
 namespace {
@@ -994,7 +1247,12 @@ GateWs gate_ws(const Shape& s, void* ws) {
     off += align256(n);
     return p;
   };
-  if (gate_dw_on_gemm(s)) {
+  if (gate_dw_on_mfma(s)) {
+    const int S = gate_dwm_splits(s);
+    const long nb = (s.T + kDlTok - 1) / kDlTok;
+    g.P = reinterpret_cast<float*>(take((size_t)S * s.M * s.E * sizeof(float)));
+    g.Pb = reinterpret_cast<float*>(take((size_t)(nb > 0 ? nb : 1) * s.E * sizeof(float)));
+  } else if (gate_dw_on_gemm(s)) {
     const int S = gate_dw_splits(s), N = gate_dw_cols(s.E);
     const long nb = (s.T + kDlTok - 1) / kDlTok;
     g.P = reinterpret_cast<float*>(take((size_t)S * s.M * N * sizeof(float)));
@@ -1054,8 +1312,8 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, co
                           const void* w_gate) {
   const GateWs g = gate_ws(s, ws);
   const bool bf = s.dtype == FLOWMOE_BF16;
-  const long n = (long)s.M * s.E + s.E;
-  const int nred = (int)((n + 255) / 256);
+  // reduce blocks: dW_g elements, then one block per db entry
+  const int nred = (int)(((long)s.M * s.E + 255) / 256) + s.E;
   // with w_gate, the reduce launch also writes W_g^T at the front of ws
   const int ntr = w_gate != nullptr ? (int)(((long)s.M * s.E + 255) / 256) : 0;
   if (gate_grad_zero(s) && s.T > 0) {
@@ -1075,6 +1333,29 @@ hipError_t launch_gate_dw(const Shape& s, const void* x, const float* logits, co
       hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(accumulate ? ntr : nred + ntr), dim3(256),
                          0, st, g.P, g.Pb, dw_gate, dbias, s.M, s.E, 0, s.E, -1, 0, 0, w_gate, ws,
                          accumulate ? 0 : nred, (int)bf);
+    });
+  }
+  if (gate_dw_on_mfma(s)) {
+    const int tps = gate_dwm_tps(s), S = gate_dwm_splits(s);
+    const int mtiles = (s.M + kDwCols - 1) / kDwCols;
+    const int ndl = (s.T + kDlTok - 1) / kDlTok;
+    const int nr = (2 * s.E + 15) / 16;
+    const dim3 grid(ndl + mtiles * S);
+    hipError_t e = traced(FLOWMOE_K_GATE_BWD_DW, st, [&] {
+#define FLOWMOE_DWM_LAUNCH(NRV)                                                                   \
+  hipLaunchKernelGGL(gate_dw_mfma_kernel<NRV>, grid, dim3(256), 0, st, (const bf16_t*)x, idx, w,   \
+                     dw, d_logits, g.P, g.Pb, s.T, s.M, s.E, s.k, tps, mtiles, ndl)
+      if (nr <= 1) FLOWMOE_DWM_LAUNCH(1);
+      else if (nr <= 2) FLOWMOE_DWM_LAUNCH(2);
+      else if (nr <= 4) FLOWMOE_DWM_LAUNCH(4);
+      else FLOWMOE_DWM_LAUNCH(8);
+#undef FLOWMOE_DWM_LAUNCH
+    });
+    if (e != hipSuccess) return e;
+    return traced(FLOWMOE_K_GATE_BWD_REDUCE, st, [&] {
+      hipLaunchKernelGGL(gate_bwd_dw_reduce_kernel, dim3(nred + ntr), dim3(256), 0, st, g.P, g.Pb,
+                         dw_gate, dbias, s.M, s.E, S, s.E, -1, ndl, accumulate, w_gate, ws, nred,
+                         (int)bf);
     });
   }
   if (gate_dw_on_gemm(s)) {

@@ -41,8 +41,8 @@ def _outputs(T, M, E, dx0):
 
 @pytest.mark.parametrize("gate", ["renorm", "full"])
 @pytest.mark.parametrize("big,small", [
-    ((3000, 1024, 64, 6), (1100, 520, 64, 4)),   # dW_g on the GEMM path (E > 16)
-    ((2000, 1024, 8, 2), (700, 264, 4, 2)),     # register tiles (renorm) / GEMM path (full)
+    ((3000, 1024, 64, 6), (1100, 520, 64, 4)),   # dW_g: MFMA kernel (renorm) / GEMM path (full)
+    ((2000, 1024, 8, 2), (700, 264, 4, 2)),     # the same at E <= 16
 ])
 def test_gate_bwd_noalloc_matches_workspace_call(gate, big, small):
     need_gpu()
@@ -72,7 +72,7 @@ def test_gate_bwd_noalloc_matches_workspace_call(gate, big, small):
 def test_gate_bwd_noalloc_rejects_shapes_beyond_its_scratch():
     """A shape whose workspace exceeds the static scratch is an error raised
     before anything is enqueued (pointers are never dereferenced)."""
-    s = L.make_shape(1 << 20, 8192, 8, 64, 2, 0, L.BF16)
+    s = L.make_shape(1 << 20, 1 << 17, 8, 64, 2, 0, L.BF16)
     assert L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD) > L.NOALLOC_SCRATCH_BYTES
     fake = 0x10000
     with pytest.raises(L.FlowMoEError) as ei:
