@@ -932,11 +932,14 @@ __global__ __launch_bounds__(256) void gate_dw_mfma_kernel(
   const int tr_off = ((8 * (lane >> 4) + ((lane & 15) >> 2)) * XP + 16 * ct + 4 * (lane & 3)) * 2;
   // row reads of D: row l % 16 of a tile, tokens 8 (l / 16) .. + 7 of a step
   const int a_off = (((16 * RT * rg) + (lane & 15)) * kDwDPitch + 8 * (lane >> 4)) * 2;
-  // D positions this thread wrote for the previous chunk (-1: none)
-  int pa = -1, pb = -1;
+  // D positions this thread wrote in each buffer for its last chunk there (-1: none)
+  int pa0 = -1, pb0 = -1, pa1 = -1, pb1 = -1;
 
-  // chunk c from ring slot d
-  auto chunk = [&](int d, int c) __attribute__((always_inline)) {
+  // chunk c's x tile and D entries from ring slot d into buffers c & 1,
+  // after clearing chunk c - 2's entries there (the same token columns:
+  // only this thread's quad writes them, clears before sets in program
+  // order; a token's selected experts are distinct)
+  auto build = [&](int d, int c) __attribute__((always_inline)) {
     bf16_t* xb = xt + (c & 1) * XT;
     bf16_t* db = dt + (c & 1) * DT;
     // d_logits of this thread's two entries, as token_dl computes them
@@ -961,12 +964,10 @@ __global__ __launch_bounds__(256) void gate_dw_mfma_kernel(
 #pragma unroll
     for (int h = 0; h < XPT; ++h)
       *reinterpret_cast<u32x4_t*>(xb + (tid / CPR + (256 / CPR) * h) * XP + xc) = xr[d][h];
-    __syncthreads();
-    // the previous chunk's entries out of the other D buffer, this chunk's
-    // in (a token's selected experts are distinct)
-    bf16_t* dp = dt + ((c + 1) & 1) * DT;
-    if (pa >= 0) dp[pa] = dp[pa + kDwDPitch] = (bf16_t)0;
-    if (pb >= 0) dp[pb] = dp[pb + kDwDPitch] = (bf16_t)0;
+    int& qa = (c & 1) ? pa1 : pa0;
+    int& qb = (c & 1) ? pb1 : pb0;
+    if (qa >= 0) db[qa] = db[qa + kDwDPitch] = (bf16_t)0;
+    if (qb >= 0) db[qb] = db[qb + kDwDPitch] = (bf16_t)0;
     if (na >= 0) {
       const bf16_t hi = f32_to_bf16(dla);
       db[na] = hi;
@@ -977,10 +978,12 @@ __global__ __launch_bounds__(256) void gate_dw_mfma_kernel(
       db[nb] = hi;
       db[nb + kDwDPitch] = f32_to_bf16(dlb - bf16_to_f32(hi));
     }
-    pa = na, pb = nb;
-    __syncthreads();
-    const char* xbc = reinterpret_cast<const char*>(xb);
-    const char* dbc = reinterpret_cast<const char*>(db);
+    qa = na, qb = nb;
+  };
+  // chunk c: D times the x tile from buffers c & 1
+  auto multiply = [&](int c) __attribute__((always_inline)) {
+    const char* xbc = reinterpret_cast<const char*>(xt + (c & 1) * XT);
+    const char* dbc = reinterpret_cast<const char*>(dt + (c & 1) * DT);
 #pragma unroll
     for (int ks = 0; ks < kDwTok / 32; ++ks) {
       const char* bp = xbc + tr_off + ks * 32 * XP * 2;
@@ -998,33 +1001,63 @@ __global__ __launch_bounds__(256) void gate_dw_mfma_kernel(
     }
   };
 
+  // One barrier a chunk: iteration c multiplies chunk c, builds chunk c + 1
+  // into the other buffers (last read by chunk c - 1, which every wave
+  // finished before the previous barrier) and reloads that ring slot D
+  // chunks ahead. Whole rounds of D chunks run without branches (the
+  // compiler's load counting stays exact); the last chunks after the loop
+  // load nothing more.
 #pragma unroll
   for (int d = 0; d < D; ++d) issue(d, d);
-  // whole rounds of D chunks without branches (the compiler's load counting
-  // stays exact), each chunk's slot reloaded D chunks ahead; then the last
-  // chunks, nothing more to load
+  build(0, 0);
+  issue(0, D);
+  __syncthreads();
   int c0 = 0;
-  for (; c0 + D <= nch; c0 += D) {
+  for (; c0 + D < nch; c0 += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
-      chunk(d, c0 + d);
-      issue(d, c0 + d + D);
+      multiply(c0 + d);
+      build((d + 1) % D, c0 + d + 1);
+      issue((d + 1) % D, c0 + d + 1 + D);
+      __syncthreads();
     }
   }
 #pragma unroll
-  for (int d = 0; d < D; ++d)
-    if (c0 + d < nch) chunk(d, c0 + d);  // (uniform)
-  // acc[i][j]: Q row 16 (RT rg + i) + 4 (lane / 16) + j, column m0 + 16 ct + lane % 16
-  const int m = m0 + 16 * ct + (lane & 15);
-  if (m < M) {
-    float* pr = P + ((long)sp * M + m) * E;
+  for (int d = 0; d < D; ++d) {
+    if (c0 + d < nch) {  // (uniform)
+      multiply(c0 + d);
+      if (c0 + d + 1 < nch) build((d + 1) % D, c0 + d + 1);
+      __syncthreads();
+    }
+  }
+  // acc[i][j]: Q row 16 (RT rg + i) + 4 (lane / 16) + j, column m0 + 16 ct + lane % 16.
+  // The block's partial rows P[split][m0 .. m0 + MT)[0 .. E) are one
+  // contiguous range: staged in LDS (free after the loop's last barrier),
+  // then written as whole 16-byte pieces (4-byte scattered stores of the
+  // accumulators took 3 of the 16 us of a 4096-token chunk at E = 64).
+  constexpr int PP = kMaxE + 4;  // staging row pitch (floats)
+  static_assert(MT * PP * 4 <= DW_BYTES, "the staging fits the block's LDS");
+  float* pt = reinterpret_cast<float*>(smem);
 #pragma unroll
-    for (int i = 0; i < RT; ++i)
+  for (int i = 0; i < RT; ++i)
 #pragma unroll
-      for (int i2 = 0; i2 < 2; ++i2) {
-        const int e = 8 * (RT * rg + i) + 2 * (lane >> 4) + i2;
-        if (e < E) pr[e] = acc[i][2 * i2] + acc[i][2 * i2 + 1];
-      }
+    for (int i2 = 0; i2 < 2; ++i2) {
+      const int e = 8 * (RT * rg + i) + 2 * (lane >> 4) + i2;
+      if (e < E) pt[(16 * ct + (lane & 15)) * PP + e] = acc[i][2 * i2] + acc[i][2 * i2 + 1];
+    }
+  __syncthreads();
+  const int rows = min(MT, M - m0), n = rows * E;
+  float* pr = P + ((long)sp * M + m0) * E;
+  if (E % 4 == 0) {
+    for (int q4 = 4 * tid; q4 < n; q4 += 4 * 256) {
+      const int r = q4 / E, e = q4 - r * E;
+      *reinterpret_cast<float4*>(pr + q4) = *reinterpret_cast<const float4*>(pt + r * PP + e);
+    }
+  } else {
+    for (int q1 = tid; q1 < n; q1 += 256) {
+      const int r = q1 / E;
+      pr[q1] = pt[r * PP + (q1 - r * E)];
+    }
   }
 }
 
