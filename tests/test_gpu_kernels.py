@@ -478,14 +478,15 @@ def test_gemm_tile_shapes_agree(act, layout, gemm_tiles):
 @pytest.mark.parametrize("T,M,E,k", [(3000, 520, 64, 6), (2000, 520, 20, 4), (9000, 1000, 3, 2),
                                      (1000, 264, 3, 2), (777, 1024, 16, 1), (40, 136, 8, 2),
                                      (4097, 2056, 64, 6), (1345, 200, 40, 8), (37, 72, 24, 3),
-                                     (8193, 1024, 8, 2)])
+                                     (8193, 1024, 8, 2), (100, 64, 2, 2), (300, 8, 4, 2)])
 def test_gate_bwd_shapes(T, M, E, k):
     """bf16 gate backward on the MFMA dW_g kernel (d_logits rows and dW_g
     partials in one launch, then the reduce): several token splits of whole
     64-token chunks and a ragged last chunk, 64-column x tiles with a ragged
     last one, fewer tokens than one chunk, E not a multiple of 4 and every
     row-tile count (2 E rounded up to 16, 32, 64, 128 rows of the hi/lo
-    matrix), k from 1 to 8: d_logits, dW_g and db against the oracle within
+    matrix), k from 1 to 8, the narrowest gates (E = k = 2) and rows of x
+    (M = 8, one short column tile): d_logits, dW_g and db against the oracle within
     the fp32 bound (the kernel multiplies a hi + lo bf16 pair per d_logits
     value: about 16 significant bits)."""
     need_gpu()
