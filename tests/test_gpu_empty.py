@@ -1,0 +1,103 @@
+"""Degenerate inputs on the GPU: no tokens (T = 0) through every step of the
+layer, forward and backward, and the attention of AT_r. Nothing that does not
+exist is read (the token tensors are null); what a step defines for an empty
+input is written: per-expert counts and offsets of zero (Sec. 2.1's dispatch
+of no assignment), and gradients that are sums over no tokens, exactly zero
+unless the call accumulates into them."""
+from __future__ import annotations
+
+import pytest
+import torch
+
+from gpu_helpers import dev, need_gpu
+from paper_2510_00207_amd import _lib as L
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+def test_no_tokens_through_every_step(layout, act):
+    need_gpu()
+    d = dev()
+    T, M, H, E, k, C = 0, 64, 128, 4, 2, 8
+    s = L.make_shape(T, M, H, E, k, C, L.BF16, L.SWIGLU if act == "swiglu" else L.GELU,
+                     L.PADDED if layout == "padded" else L.PACKED)
+    rows = L.flowmoe_rows_capacity(s)
+    bf = lambda *shape: torch.randn(*shape, device=d).to(torch.bfloat16)
+    w_gate = bf(M, E)
+    w1, w2 = bf(E, M, H), bf(E, H, M)
+    w3 = bf(E, M, H) if act == "swiglu" else None
+
+    # forward: gate, routing and dispatch, experts, combine
+    L.flowmoe_gate_topk(s, None, w_gate, None, None, None, None)
+    L.flowmoe_route(s, None, None, None)
+    counts = torch.full((E,), 7, dtype=torch.int32, device=d)
+    offsets = torch.full((E + 1,), 7, dtype=torch.int32, device=d)
+    x_disp = bf(max(rows, 1), M)
+    row_src = torch.full((max(rows, 1),), 7, dtype=torch.int32, device=d)
+    L.flowmoe_dispatch(s, None, None, counts, offsets, None, row_src if rows else None, None,
+                       x_disp if rows else None)
+    torch.cuda.synchronize()
+    assert counts.eq(0).all(), counts
+    if layout == "packed":
+        assert offsets.eq(0).all(), offsets
+    else:  # padded: expert e's rows start at e C whatever its count
+        assert offsets.tolist() == [e * C for e in range(E + 1)], offsets
+    h_save = bf(max(rows, 1), (2 if act == "swiglu" else 1) * H)
+    a_save = bf(max(rows, 1), H)
+    y_disp = bf(max(rows, 1), M)
+    L.flowmoe_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save, y_disp)
+    L.flowmoe_combine(s, y_disp, None, None, None)
+
+    # backward: combine, experts (weight gradients: sums over no rows), dispatch, gate
+    L.flowmoe_combine_bwd(s, None, y_disp, None, None, counts, offsets, y_disp, None)
+    dw1 = torch.full((E, M, H), 3.0, device=d)
+    dw2 = torch.full((E, H, M), 3.0, device=d)
+    dw3 = torch.full((E, M, H), 3.0, device=d) if act == "swiglu" else None
+    nws = L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=d)
+    dx_disp = bf(max(rows, 1), M)
+    for acc in (1, 0):
+        L.flowmoe_expert_ffn_bwd(s, y_disp, x_disp, h_save, a_save, counts, offsets, w1, w3, w2,
+                                 dx_disp, dw1, dw3, dw2, acc, ws, nws)
+        torch.cuda.synchronize()
+        want = 3.0 if acc else 0.0
+        for g in (dw1, dw2) + ((dw3,) if dw3 is not None else ()):
+            assert g.eq(want).all(), (acc, float(g.abs().max()))
+    L.flowmoe_dispatch_bwd(s, dx_disp, None, None)
+    dw_gate = torch.full((M, E), 3.0, device=d)
+    dbias = torch.full((E,), 3.0, device=d)
+    nws = L.flowmoe_workspace_bytes(s, L.WS_GATE_BWD)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=d)
+    for acc in (1, 0):
+        L.flowmoe_gate_topk_bwd(s, None, w_gate, None, None, None, None, None, dw_gate, dbias,
+                                None, acc, ws, nws)
+        torch.cuda.synchronize()
+        want = 3.0 if acc else 0.0
+        assert dw_gate.eq(want).all() and dbias.eq(want).all(), acc
+
+
+def test_no_tokens_through_the_attention():
+    """The attention core and the MHA of AT_r with no tokens: nothing to do
+    but the backward's weight gradients, which are sums over no tokens."""
+    need_gpu()
+    d = dev()
+    M = 128
+    s = L.make_shape(0, M, 64, 1, 1, 0, L.BF16)
+    m = L.make_mha_shape(64, 2, 64, True)
+    L.flowmoe_attention_fwd(s, m, None, None, None)
+    L.flowmoe_attention_bwd(s, m, None, None, None, None, None, None)
+    w_qkv = torch.randn(M, 3 * M, device=d).to(torch.bfloat16)
+    w_o = torch.randn(M, M, device=d).to(torch.bfloat16)
+    L.flowmoe_mha_fwd(s, m, None, w_qkv, w_o, None, None, None, None)
+    dw_qkv = torch.full((M, 3 * M), 3.0, device=d)
+    dw_o = torch.full((M, M), 3.0, device=d)
+    nws = L.flowmoe_workspace_bytes(s, L.WS_MHA_BWD)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=d)
+    for acc in (1, 0):
+        L.flowmoe_mha_bwd(s, m, None, w_qkv, w_o, None, None, None, None, None, None, None,
+                          None, dw_qkv, dw_o, acc, ws=ws, ws_bytes=nws)
+        torch.cuda.synchronize()
+        want = 3.0 if acc else 0.0
+        assert dw_qkv.eq(want).all() and dw_o.eq(want).all(), acc
