@@ -101,3 +101,24 @@ def test_no_tokens_through_the_attention():
         torch.cuda.synchronize()
         want = 3.0 if acc else 0.0
         assert dw_qkv.eq(want).all() and dw_o.eq(want).all(), acc
+
+
+@pytest.mark.parametrize("mha", [False, True])
+@pytest.mark.parametrize("R", [1, 2])
+def test_layer_with_no_tokens(R, mha):
+    """The layer driver's R-chunk schedule over no tokens: every task has
+    nothing to do, and the parameter gradients (sums over the chunks' tokens)
+    are written as zeros."""
+    need_gpu()
+    from paper_2510_00207_amd.layer import MoELayer
+    layer = MoELayer(T_total=0, M=128, H=256, E=4, k=2, R=R, C=8, act="swiglu", bias=True,
+                     mha=dict(seq_len=64, head_dim=64, causal=True) if mha else None)
+    names = ["dw_gate", "dbias", "dw1", "dw3", "dw2"] + (["dw_qkv", "dw_o"] if mha else [])
+    for n in names:
+        getattr(layer, n).fill_(3.0)
+    layer.forward()
+    layer.backward()
+    torch.cuda.synchronize()
+    for n in names:
+        assert getattr(layer, n).eq(0).all(), n
+    assert layer.counts.eq(0).all()
