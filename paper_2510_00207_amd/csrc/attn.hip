@@ -46,6 +46,7 @@ struct AttnArgs {
   float* lse;         // heads x T: natural log-sum-exp of each row's scores
   float* delta;       // heads x T: rowsum(dO * O) over the head's columns
   int T, M, N, heads, nseq;
+  int pair;  // causal grid of one round of resident blocks: pair long and short tiles (decode)
   float c2;  // log2(e) / sqrt(D): a score times c2 is its base-2 exponent
   float rs;  // 1 / sqrt(D)
 };
@@ -212,13 +213,21 @@ struct KVTiles {
   }
 };
 
-// block -> (query or key tile, head, sequence); `rev`: tiles in descending
-// order (the causal forward's longest query tiles first)
+// block -> (query or key tile, head, sequence). Blocks are dispatched in
+// order; u = blockIdx / (heads x sequences) ranks the tiles by their causal
+// work, longest first (`rev`: tiles in descending order, the query tiles of
+// the forward and of dQ; else ascending, the key tiles of dK/dV). With
+// `a.pair` (every block resident at once, two to a CU: the second half of
+// the grid lands on the CUs of the first half) the second half runs the
+// shortest tiles first, so that a CU's two blocks have complementary work
+// (ranks u and nt - 1 - u) instead of ranks u and u + nt / 2.
 __device__ __forceinline__ void decode(const AttnArgs& a, bool rev, int& tile, int& hd, int& sq,
                                        int rows = 128) {
   const int per = a.heads * a.nseq, nt = (a.N + rows - 1) / rows;
-  const int t = (int)(blockIdx.x / per), rest = (int)(blockIdx.x % per);
-  tile = rev ? nt - 1 - t : t;
+  const int u = (int)(blockIdx.x / per), rest = (int)(blockIdx.x % per);
+  const int h = (nt + 1) / 2;
+  const int r = a.pair && u >= h ? nt - 1 - (u - h) : u;  // rank in work order
+  tile = rev ? nt - 1 - r : r;
   hd = rest % a.heads;
   sq = rest / a.heads;
 }
@@ -604,6 +613,13 @@ unsigned attn_blocks(const AttnArgs& a, int rows = 128) {
   return (unsigned)(((a.N + rows - 1) / rows) * a.heads * a.nseq);
 }
 
+// pair long and short causal tiles (decode) when the 4-wave grid (two
+// blocks per CU) is resident all at once: then the makespan is a CU's two
+// blocks together, not the longest-first order's
+int attn_pair(const AttnShape& m, const AttnArgs& a, bool wide) {
+  return m.causal && !wide && attn_blocks(a, 128) <= 2u * 256u ? 1 : 0;
+}
+
 #define FLOWMOE_ATTN_LAUNCH(KERNEL, a, st, ROWS, THREADS, ...)                                 \
   do {                                                                                          \
     const dim3 g(attn_blocks(a, ROWS)), b(THREADS);                                             \
@@ -626,6 +642,7 @@ hipError_t launch_attn_fwd(const AttnShape& m, int T, int M, const void* qkv, vo
   a.out = static_cast<bf16_t*>(o);
   a.lse = lse;
   const bool wide = attn_blocks(a, 256) >= 2u * 256u;
+  a.pair = attn_pair(m, a, wide);
   return traced(FLOWMOE_K_ATTN_FWD, st, [&] {
     if (wide) FLOWMOE_ATTN_LAUNCH(attn_fwd_kernel, a, st, 256, 512, 8);
     else FLOWMOE_ATTN_LAUNCH(attn_fwd_kernel, a, st, 128, 256, 4);
@@ -646,6 +663,7 @@ hipError_t launch_attn_bwd(const AttnShape& m, int T, int M, const void* qkv, co
   // 8-wave blocks (256 queries, or keys) when that grid still gives two
   // blocks per CU: each staged tile then serves twice the MFMA work
   const bool wide = attn_blocks(a, 256) >= 2u * 256u;
+  a.pair = attn_pair(m, a, wide);
   hipError_t e = traced(FLOWMOE_K_ATTN_BWD_DQ, st, [&] {
     if (wide) FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st, 256, 512, 8);
     else FLOWMOE_ATTN_LAUNCH(attn_dq_kernel, a, st, 128, 256, 4);
