@@ -831,20 +831,22 @@ __global__ __launch_bounds__(256) void gate_bwd_dl_kernel(
 // (h = 1) of d_logits[t][e] (hi = bf16(dl), lo = bf16(dl - hi): about 16
 // significant bits; zero for experts a token did not select), and finally
 // P[split][m][e] = Q[2 e][m] + Q[2 e + 1][m], summed over the splits in
-// order by the reduce launch. Per chunk: every thread computes the d_logits
-// of its token's selection (4 threads a token, two entries each, the sum s
-// over the k entries in entry order as token_dl takes it, the entries
-// gathered from the quad by DPP) and stores its part of the x tile (loaded
-// kDwDepth chunks ahead in registers); a barrier; it writes its entries
-// into D and clears the previous chunk's from the other D buffer (both D
-// buffers start zero, so only entries are ever written); a barrier; each
-// wave multiplies its row tiles of D (A operand, 16-byte row reads: 8
-// consecutive tokens of one row) by its 16 columns of the x tile (B
-// operand, two transposing reads: 8 consecutive tokens of one column). D and
-// the x tile are double-buffered, so one chunk's writes never meet the
-// previous chunk's reads. Every load is issued unconditionally from a
-// clamped address (tokens past the split: its first token, whose entries
-// are not used; columns past M: column 0, whose results are not written).
+// order by the reduce launch. Building a chunk: every thread computes the
+// d_logits of its token's selection (4 threads a token, two entries each,
+// the sum s over the k entries in entry order as token_dl takes it, the
+// entries gathered from the quad by DPP), stores its part of the x tile
+// (loaded kDwDepth chunks ahead in registers), clears the entries it wrote
+// two chunks earlier into the same D buffer and writes its new ones (both
+// D buffers start zero, so only entries are ever written). Multiplying a
+// chunk: each wave takes its row tiles of D (A operand, 16-byte row reads:
+// 8 consecutive tokens of one row) times its 16 columns of the x tile (B
+// operand, two transposing reads: 8 consecutive tokens of one column). D
+// and the x tile are double-buffered; each step multiplies chunk c and
+// builds chunk c + 1, then meets the block at one barrier. Every load is
+// issued unconditionally from a clamped address (tokens past the split: its
+// first token, whose entries are not used; columns past M: column 0, whose
+// results are not written). The block's partial rows go out through LDS as
+// one contiguous range.
 constexpr int kDwTok = 64;    // tokens per chunk
 constexpr int kDwDepth = 4;   // chunks of loads in flight
 constexpr int kDwDPitch = 72; // bf16 per row of D (64 tokens + 8: 16-byte aligned rows, 4 banks apart)
