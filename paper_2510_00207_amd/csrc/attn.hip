@@ -88,34 +88,17 @@ __device__ __forceinline__ int toff(int r, int c) {
   return r * (2 * D) + ((c ^ sw<D>(r)) << 4);
 }
 
-// MFMA operand with d contiguous: lane l supplies row r (its l % 32 row of
-// the 32-row block) at d = 16 ks + 8 (l / 32) .. + 7
-template <int D>
-__device__ __forceinline__ bf16x8 frag_row(const char* t, int r, int ks, int h2) {
-  return *reinterpret_cast<const bf16x8*>(t + toff<D>(r, 2 * ks + h2));
-}
-
-// Transposed operand: lane l supplies column cb + l % 32 of the tile at the
-// 8 rows of its k-slots, slot 4 i + j (i = 0, 1; j = 0..3) being row
-// rb + 4 (l / 32) + 8 i + j. Each ds_read_b64_tr_b16 hands lane l' of a
-// 16-lane group element l' % 4 of the 4 values that lane 4 q + l' / 4
-// addressed, in slot q; lanes aimed at rows r0 + s / 4, columns c0 + 4 (s % 4)
-// give lane l' column c0 + l' at rows r0 .. r0 + 3.
-template <int D>
-__device__ __forceinline__ bf16x8 frag_tr(const char* t, int rb, int cb, int lane) {
-  const int G = lane >> 4, sl = lane & 15;
-  const int col = cb + (G & 1) * 16 + 4 * (sl & 3);
-  v4i16 v[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = rb + 4 * (G >> 1) + 8 * i + (sl >> 2);
-    v[i] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4i16_t*)(t + toff<D>(r, col >> 3) + ((col & 7) << 1)));
-  }
-  const short __attribute__((ext_vector_type(8))) s = {v[0][0], v[0][1], v[0][2], v[0][3],
-                                                       v[1][0], v[1][1], v[1][2], v[1][3]};
-  return __builtin_bit_cast(bf16x8, s);
-}
+// Two MFMA operand forms are read from these tiles:
+//   row operand (d contiguous): lane l supplies row r0 + l % 32 of a 32-row
+//     block at d = 16 ks + 8 (l / 32) .. + 7, one 16-byte read of chunk
+//     2 ks + l / 32 (row_base, frag_row_x);
+//   transposed operand: lane l supplies column cb + l % 32 of the tile at
+//     the 8 rows of its k-slots, slot 4 i + j (i = 0, 1; j = 0..3) being row
+//     rb + 4 (l / 32) + 8 i + j, as two transposing reads (tr_base,
+//     frag_tr_x). Each ds_read_b64_tr_b16 hands lane l' of a 16-lane group
+//     element l' % 4 of the 4 values that lane 4 q + l' / 4 addressed, in
+//     slot q; lanes aimed at rows r0 + s / 4, columns c0 + 4 (s % 4) give
+//     lane l' column c0 + l' at rows r0 .. r0 + 3.
 
 // The swizzle lets a lane's fragment addresses be formed from three per-lane
 // bases: a row read of row r0 + lq (r0 a multiple of 32) at k step ks is at
@@ -154,7 +137,7 @@ __device__ __forceinline__ void opaque(int& a, int& b, int& c) {
 
 // Rows 16 s .. 16 s + 15 of a 32 x 32 accumulator (lane l: column l % 32,
 // element 4 J + j = row 8 J + 4 (l / 32) + j) as an MFMA column operand in
-// frag_tr's slot order: slot 4 i + j <- element 8 s + 4 i + j.
+// the transposed operand's slot order: slot 4 i + j <- element 8 s + 4 i + j.
 __device__ __forceinline__ bf16x8 pfrag(const floatx16& a, int s) {
   bf16x8 r;
 #pragma unroll
