@@ -266,7 +266,7 @@ def main():
     a = parse()
     if a.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {a.gpus}); the multi-GPU expert-parallel "
-              "path is not part of this build", file=sys.stderr)
+              "path (all-to-all over RCCL) is not implemented", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

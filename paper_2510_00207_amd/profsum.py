@@ -56,7 +56,7 @@ def short_name(name: str) -> str:
 
 def cmd_trace(a) -> None:
     rows = list(csv.DictReader(open(os.path.join(a.dir, "run_kernel_stats.csv"))))
-    lines = [f"# {a.title}", "", "Command (repo root on the GPU box, MI355X):", "",
+    lines = [f"# {a.title}", "", "Command (run from the repository root on one MI355X):", "",
              f"    {a.command}", "",
              "| kernel | calls | avg us | min us | max us | total ms |",
              "|---|---|---|---|---|---|"]
@@ -111,7 +111,7 @@ def cmd_traffic(a) -> None:
            "gemm_bytes_per_launch": tot / max(1, n), "gemm_launches": n, "kernels": kernels}
     json.dump(res, open(a.out, "w"), indent=1)
     if a.md:
-        lines = [f"# {a.title}", "", "Commands (repo root on the GPU box, MI355X), one pass per counter:", "",
+        lines = [f"# {a.title}", "", "Commands (run from the repository root on one MI355X), one pass per counter:", "",
                  f"    {a.command}", "",
                  f"Calibration: the {a.probe_mib} MiB copy probe read FETCH_SIZE x{f_scale:.3f} and "
                  f"WRITE_SIZE x{w_scale:.3f} of its true bytes; the figures below are scaled by those "
@@ -143,7 +143,7 @@ def cmd_mfma(a) -> None:
         g[1] += c["SQ_VALU_MFMA_BUSY_CYCLES"]
         g[2] += c["GRBM_GUI_ACTIVE"] / 8.0
         g[3] += c["ns"]
-    lines = [f"# {a.title}", "", "Command (repo root on the GPU box, MI355X):", "",
+    lines = [f"# {a.title}", "", "Command (run from the repository root on one MI355X):", "",
              f"    {a.command}", "",
              "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cycles x 1024 SIMDs), cycles = "
              "GRBM_GUI_ACTIVE / 8 (the counter is summed over the 8 XCDs); clock = cycles / "
