@@ -31,12 +31,14 @@ def flowmoe_lib():
 
 def pytest_sessionfinish(session, exitstatus):
     """Write the error measures of every parity comparison of the session
-    (max-normalised and element-wise) to gpurun_out/parity_report.tsv."""
+    (max-normalised and element-wise) to parity_report.tsv in the output
+    folder (FLOWMOE_REPORT_DIR, default: the folder that a remote run copies
+    back)."""
     mod = sys.modules.get("gpu_helpers")
     rep = getattr(mod, "REPORT", None) if mod is not None else None
     if not rep:
         return
-    out = os.path.join(ROOT, "gpurun_out")
+    out = os.environ.get("FLOWMOE_REPORT_DIR") or os.path.join(ROOT, "gpurun_out")
     os.makedirs(out, exist_ok=True)
     with open(os.path.join(out, "parity_report.tsv"), "w") as f:
         f.write("test\tquantity\tdtype\tmax_rel_err\telem_rel_err\n")
