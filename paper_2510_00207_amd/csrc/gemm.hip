@@ -700,6 +700,17 @@ struct IntC {
   static constexpr int value = V;
 };
 
+// inclusive prefix sum of v over the lanes of a wave
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(v, d, 64);
+    if (lane >= d) v += u;
+  }
+  return v;
+}
+
 // Row-mode tile of the streaming kernel for block `bid`. The row tiles fall
 // in two classes: heavy ones (at least half a tile of live rows) and light
 // ones (an expert's short last tile, or padding only). Every XCD (blocks are
@@ -712,24 +723,21 @@ struct IntC {
 // tiles, row tiles fastest. Returns false for a block with no tile.
 template <int BM>
 __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, int& e, int& mt,
-                                                  int& nt, int& rows_e, int& cnt_e) {
-  // the experts' counts in one vector load (lane x: expert x, E <= 64), then
-  // walked in scalar registers (no memory round trip per expert)
+                                                  int& nt, int& rows_e, int& cnt_e, int& off_e) {
+  // lane x holds expert x (E <= 64): its count and first row are loaded
+  // together (one memory round trip), its tile counts per class summed over
+  // the lanes by a prefix scan, and the block's expert found by a ballot
+  // (a walk over the experts in scalar registers cost ~0.15 us per expert)
   const int lane = threadIdx.x & 63;
-  const int cvec = lane < p.E ? seg_count(p, 0, lane) : 0;
-  auto tiles = [&](int x, int& c, int& r, int& te, int& he) {
-    c = __builtin_amdgcn_readlane(cvec, x);
-    r = p.padC ? p.padC : c;
-    te = (r + BM - 1) / BM;
-    he = min(te, (c + BM / 2) / BM);
-  };
-  int HR = 0, LR = 0;  // heavy / light row tiles
-  for (int x = 0; x < p.E; ++x) {
-    int c, r, te, he;
-    tiles(x, c, r, te, he);
-    HR += he;
-    LR += te - he;
-  }
+  const bool live = lane < p.E;
+  const int c = live ? seg_count(p, 0, lane) : 0;
+  const int o = live ? seg_offset(p, 0, lane) : 0;
+  const int r = live ? (p.padC ? p.padC : c) : 0;
+  const int te = (r + BM - 1) / BM;
+  const int he = min(te, (c + BM / 2) / BM);  // heavy row tiles of this expert
+  const int le = te - he;                     // light ones
+  const int hin = wave_incl_scan(he), lin = wave_incl_scan(le);
+  const int HR = __builtin_amdgcn_readlane(hin, 63), LR = __builtin_amdgcn_readlane(lin, 63);
   const int x = bid & 7, i = bid >> 3;
   const int H = HR * p.ntiles, L = LR * p.ntiles;
   const int hx = (H >> 3) + (x < (H & 7)), lx = (L >> 3) + (x < (L & 7));
@@ -749,20 +757,18 @@ __device__ __forceinline__ bool row_tile_of_block(const GemmParams& p, int bid, 
   } else {
     return false;
   }
-  int acc_t = 0;
-  for (e = 0; e < p.E; ++e) {
-    int c, r, te, he;
-    tiles(e, c, r, te, he);
-    const int ce = heavy ? he : te - he;
-    if (ml < acc_t + ce) {
-      mt = (heavy ? 0 : he) + (ml - acc_t);
-      rows_e = r;
-      cnt_e = c;
-      return true;
-    }
-    acc_t += ce;
-  }
-  return false;
+  // the expert whose range of class tiles holds ml: the one lane with
+  // (inclusive sum - own count) <= ml < inclusive sum
+  const int inc = heavy ? hin : lin, own = heavy ? he : le;
+  const uint64_t hit = __ballot(live && ml < inc && ml >= inc - own);
+  if (hit == 0) return false;
+  e = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(hit));
+  mt = (heavy ? 0 : __builtin_amdgcn_readlane(he, e)) + ml -
+       (__builtin_amdgcn_readlane(inc, e) - __builtin_amdgcn_readlane(own, e));
+  rows_e = __builtin_amdgcn_readlane(r, e);
+  cnt_e = __builtin_amdgcn_readlane(c, e);
+  off_e = __builtin_amdgcn_readlane(o, e);
+  return true;
 }
 
 // grid of the streaming kernel in row mode: ceil(tiles / 8) + 1 blocks per
@@ -872,10 +878,11 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   // ---- which tile ----
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
   if constexpr (MODE == MODE_ROWS) {
-    if (!row_tile_of_block<BM>(p, blockIdx.x, e, mt, nt, rows_e, cnt_e)) return;
-    rows_e = clip_rows(seg_offset(p, 0, e), rows_e, p.rows_cap);
-    cnt_e = clip_rows(seg_offset(p, 0, e), cnt_e, p.rows_cap);
-    row0 = seg_offset(p, 0, e) + mt * BM;
+    int off_e = 0;
+    if (!row_tile_of_block<BM>(p, blockIdx.x, e, mt, nt, rows_e, cnt_e, off_e)) return;
+    rows_e = clip_rows(off_e, rows_e, p.rows_cap);
+    cnt_e = clip_rows(off_e, cnt_e, p.rows_cap);
+    row0 = off_e + mt * BM;
   } else {
     // expert e's mtn x ntn tiles, walked in shared 16 x 16 blocks
     const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
