@@ -877,6 +877,7 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
 
   // ---- which tile ----
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
+  int seg_o = 0, seg_c = 0;  // KSUM: segment ranges, one lane per segment
   if constexpr (MODE == MODE_ROWS) {
     int off_e = 0;
     if (!row_tile_of_block<BM>(p, blockIdx.x, e, mt, nt, rows_e, cnt_e, off_e)) return;
@@ -888,8 +889,13 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
     const int mtn = (p.Mdim + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
     e = blockIdx.x / (mtn * ntn);
     shared_block_tile(blockIdx.x - e * (mtn * ntn), mtn, ntn, mt, nt);
-    cnt_e = clip_rows(seg_offset(p, 0, e), seg_count(p, 0, e), p.rows_cap);
-    row0 = seg_offset(p, 0, e);
+    // lane g holds segment g's first row and count of this expert (g < 64):
+    // every segment's range in one memory round trip
+    const int g = lane;
+    seg_o = g < p.nseg ? seg_offset(p, g, e) : 0;
+    seg_c = g < p.nseg ? seg_count(p, g, e) : 0;
+    row0 = __builtin_amdgcn_readlane(seg_o, 0);
+    cnt_e = clip_rows(row0, __builtin_amdgcn_readlane(seg_c, 0), p.rows_cap);
   }
   constexpr int NCOLS = DUAL ? BN / 2 : BN;
   const int n0 = nt * NCOLS;
@@ -967,8 +973,9 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   // g-th chunk's buffers (same per-lane offsets and k steps)
   auto bind_segment = [&](int g) {
     if constexpr (MODE == MODE_KSUM) {
-      row0 = seg_offset(p, g, e);
-      cnt_e = clip_rows(row0, seg_count(p, g, e), p.rows_cap);
+      row0 = g < 64 ? __builtin_amdgcn_readlane(seg_o, g) : seg_offset(p, g, e);
+      cnt_e = clip_rows(row0, g < 64 ? __builtin_amdgcn_readlane(seg_c, g) : seg_count(p, g, e),
+                        p.rows_cap);
       const bf16_t* Ag = A + g * p.a_sstride;
       const bf16_t* Bg = B0 + g * p.b_sstride;
       const int m0 = mt * BM;
