@@ -141,14 +141,18 @@ __device__ __forceinline__ void raw8_f32(const Raw8f& r, float v[8]) {
 // activations (fp32). erf follows Abramowitz & Stegun 7.1.26,
 // erf(x) = 1 - (a1 t + ... + a5 t^5) exp(-x^2), t = 1 / (1 + p x), x >= 0,
 // absolute error <= 1.5e-7; its exp(-x^2) term is also phi(z) * sqrt(2 pi)
-// for x = z / sqrt(2), which the GELU derivative reuses.
+// for x = z / sqrt(2), which the GELU derivative reuses. Reciprocals use the
+// hardware's v_rcp_f32 (1 ulp), not a correctly rounded division: the
+// epilogues evaluate these per output element, and the division sequence
+// (about ten instructions each) made them a large share of a tile's time.
+__device__ __forceinline__ float rcp_f(float x) { return __builtin_amdgcn_rcpf(x); }
 struct ErfParts {
   float erf;   // erf(z / sqrt(2))
   float gexp;  // exp(-z^2 / 2)
 };
 __device__ __forceinline__ ErfParts erf_parts(float z) {
   const float x = fabsf(z) * 0.70710678118654752f;
-  const float t = __frcp_rn(1.0f + 0.3275911f * x);
+  const float t = rcp_f(1.0f + 0.3275911f * x);
   const float poly =
       t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
   const float g = __expf(-x * x);
@@ -162,7 +166,7 @@ __device__ __forceinline__ float gelu_grad_f(float z) {
   const ErfParts e = erf_parts(z);
   return 0.5f * (1.0f + e.erf) + z * 0.39894228040143268f * e.gexp;
 }
-__device__ __forceinline__ float sigmoid_f(float z) { return __frcp_rn(1.0f + __expf(-z)); }
+__device__ __forceinline__ float sigmoid_f(float z) { return rcp_f(1.0f + __expf(-z)); }
 
 // ---------------------------------------------------------------------------
 // host side
