@@ -328,6 +328,22 @@ enum { FLOWMOE_TILES_AUTO = 0, FLOWMOE_TILES_WIDE = 1, FLOWMOE_TILES_NARROW = 2 
  * (for tests and tuning). FLOWMOE_ERR_INVALID for another value. */
 flowmoe_status_t flowmoe_set_gemm_tiles(int32_t tiles);
 
+/* Order of the row-mode tiles of the bf16 grouped GEMM. An expert's row
+ * tiles are heavy (at least half of 256 rows live) or light (its short last
+ * tile). SPLIT runs every heavy tile before any light one (the light tiles
+ * fill the last round of the compute units); JOINED walks an expert's light
+ * tiles with its heavy ones, so that a light tile reads its weight panels
+ * while the heavy tiles of the same expert have them in the L2 / Infinity
+ * Cache. AUTO, the default: JOINED when the launch's expert weights exceed
+ * the 256 MB Infinity Cache and the experts average at most eight row tiles
+ * (rows capacity <= 2048 E), else SPLIT. Every output is computed by the
+ * same tile code in the same k order: results are bit-identical. */
+enum { FLOWMOE_TILE_ORDER_AUTO = 0, FLOWMOE_TILE_ORDER_SPLIT = 1, FLOWMOE_TILE_ORDER_JOINED = 2 };
+
+/* Set the tile order for launches enqueued after the call, process-wide (for
+ * tests and tuning). FLOWMOE_ERR_INVALID for another value. */
+flowmoe_status_t flowmoe_set_tile_order(int32_t order);
+
 /* ---- row streams of the dispatch and combine kernels ----------------------- */
 
 /* How the row kernels (dispatch gather/scatter, combine, their backward and

@@ -97,6 +97,7 @@ def load():
         "flowmoe_trace_stop": ([], I32),
         "flowmoe_set_gemm_tiles": ([I32], I32),
         "flowmoe_set_row_streams": ([I32], I32),
+        "flowmoe_set_tile_order": ([I32], I32),
         "flowmoe_attention_fwd": ([SP, MP, P, P, P, P], I32),
         "flowmoe_attention_bwd": ([SP, MP, P, P, P, P, P, P, P], I32),
         "flowmoe_mha_fwd": ([SP, MP, P, P, P, P, P, P, P, P], I32),
@@ -296,6 +297,16 @@ def flowmoe_set_gemm_tiles(tiles: str | int) -> None:
     """Grouped-GEMM tile shape for later launches: "auto", "wide" (256 x 256)
     or "narrow" (256 x 128), or the FLOWMOE_TILES_* value."""
     _check(load().flowmoe_set_gemm_tiles(TILES[tiles] if isinstance(tiles, str) else tiles))
+
+
+TILE_ORDERS = {"auto": 0, "split": 1, "joined": 2}
+
+
+def flowmoe_set_tile_order(order: str | int) -> None:
+    """Row-mode tile order of the grouped GEMM for later launches: "auto",
+    "split" (light tiles after every heavy one) or "joined" (an expert's
+    light tiles with its heavy ones), or the FLOWMOE_TILE_ORDER_* value."""
+    _check(load().flowmoe_set_tile_order(TILE_ORDERS[order] if isinstance(order, str) else order))
 
 
 ROW_STREAMS = {"auto": 0, "nt": 1, "cached": 2}

@@ -204,6 +204,14 @@ flowmoe_status_t flowmoe_set_gemm_tiles(int32_t tiles) {
   return ok();
 }
 
+flowmoe_status_t flowmoe_set_tile_order(int32_t order) {
+  if (order != FLOWMOE_TILE_ORDER_AUTO && order != FLOWMOE_TILE_ORDER_SPLIT &&
+      order != FLOWMOE_TILE_ORDER_JOINED)
+    return fail(FLOWMOE_ERR_INVALID, "order = %d is not a FLOWMOE_TILE_ORDER_* value", order);
+  set_tile_order(order);
+  return ok();
+}
+
 flowmoe_status_t flowmoe_set_row_streams(int32_t mode) {
   if (mode != FLOWMOE_ROWS_AUTO && mode != FLOWMOE_ROWS_NT && mode != FLOWMOE_ROWS_CACHED)
     return fail(FLOWMOE_ERR_INVALID, "mode = %d is not a FLOWMOE_ROWS_* value", mode);

@@ -230,6 +230,7 @@ hipError_t launch_gate_wstack(const Shape& s, const void* w_gate, void* ws, hipS
 hipError_t launch_gate_dx_full(const Shape& s, void* ws, void* dx, bool add, hipStream_t st);
 size_t ffn_bwd_ws_bytes(const Shape& s);
 void set_gemm_tiles(int tiles);  // FLOWMOE_TILES_*, validated by the caller
+void set_tile_order(int order);  // FLOWMOE_TILE_ORDER_*, validated by the caller
 void set_row_streams(int mode);  // FLOWMOE_ROWS_*, validated by the caller
 // dW_g partials of the bf16 gate backward: P[s] = X_s^T D_s (fp32, M x N)
 // over token split s (rows offsets[s] .. + counts[s] of x (T x M, bf16) and

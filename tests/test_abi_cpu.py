@@ -191,6 +191,15 @@ def test_gemm_tiles_setting(flowmoe_lib):
     assert raw.flowmoe_set_gemm_tiles(-1) == L.ERR_INVALID
 
 
+def test_tile_order_setting(flowmoe_lib):
+    for o in ("joined", "split", "auto"):
+        L.flowmoe_set_tile_order(o)
+    raw = ctypes.CDLL(L.LIB_PATH)
+    raw.flowmoe_set_tile_order.argtypes = [ctypes.c_int32]
+    assert raw.flowmoe_set_tile_order(3) == L.ERR_INVALID
+    assert raw.flowmoe_set_tile_order(-1) == L.ERR_INVALID
+
+
 def test_capacity_exact_on_adversarial_factors(flowmoe_lib):
     """C = ceil(f k T / E) on the decimal value of f, exactly as the oracle's
     rational arithmetic: factors with many digits, factors just above and

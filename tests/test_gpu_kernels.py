@@ -308,6 +308,13 @@ def gemm_tiles():
     L.flowmoe_set_gemm_tiles("auto")
 
 
+@pytest.fixture
+def tile_order():
+    """Set the grouped-GEMM row-tile order for one test; back to "auto" after it."""
+    yield L.flowmoe_set_tile_order
+    L.flowmoe_set_tile_order("auto")
+
+
 @pytest.mark.parametrize("biased", [False, True], ids=["nobias", "bias"])
 @pytest.mark.parametrize("MHT", [(200, 264, "auto"), (224, 288, "wide"), (224, 288, "narrow")],
                          ids=["staged", "streaming-wide", "streaming-narrow"])
@@ -414,11 +421,13 @@ def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, biased, gemm_tiles):
 
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
-def test_gemm_tile_shapes_agree(act, layout, gemm_tiles):
-    """256 x 256 and 256 x 128 tiles over several row and column tiles with
-    ragged edges and light last row tiles: both match the oracle, and as
-    both accumulate every output in the same k order, their outputs are
-    bit-identical."""
+def test_gemm_tile_shapes_agree(act, layout, gemm_tiles, tile_order):
+    """256 x 256 and 256 x 128 tiles, each in the split and the joined
+    row-tile order, over several row and column tiles with ragged edges,
+    light last row tiles (one live row, four live rows) and an empty
+    expert: all match the oracle, and as every output is accumulated in the
+    same k order whatever the tile's shape or place in the walk, their
+    outputs are bit-identical."""
     need_gpu()
     rng = np.random.default_rng(21)
     E, M, H = 4, 512, 800
@@ -444,8 +453,10 @@ def test_gemm_tile_shapes_agree(act, layout, gemm_tiles):
     HW = 2 * H if act == "swiglu" else H
     nws = L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD)
     out = {}
-    for tiles in ("wide", "narrow"):
+    for tiles, order in (("wide", "split"), ("narrow", "split"), ("wide", "joined"),
+                         ("narrow", "joined")):
         gemm_tiles(tiles)
+        tile_order(order)
         h = torch.full((rows, HW), 5.0, dtype=bf, device=d)
         a = torch.full((rows, H), 5.0, dtype=bf, device=d)
         y = torch.full((rows, M), 5.0, dtype=bf, device=d)
@@ -458,21 +469,23 @@ def test_gemm_tile_shapes_agree(act, layout, gemm_tiles):
         L.flowmoe_expert_ffn_bwd(s, dy, x_disp, h, a, counts, offsets, w1, w3, w2, dx, dw1, dw3, dw2,
                                  0, ws, nws)
         torch.cuda.synchronize()
-        out[tiles] = [t for t in (h, a, y, dx, dw1, dw3, dw2) if t is not None]
-        if tiles == "wide":
+        out[(tiles, order)] = [t for t in (h, a, y, dx, dw1, dw3, dw2) if t is not None]
+        if (tiles, order) == ("wide", "split"):
             x64, dy64 = host(x_disp), host(dy)
             w64 = [None if w is None else host(w) for w in (w1, w3, w2)]
             ref = oracle.expert_ffn(x64, rt["counts"], rt["offsets"], *w64, act)
             rdx, rdw1, rdw3, rdw2 = oracle.expert_ffn_bwd(dy64, x64, ref, rt["counts"], rt["offsets"],
                                                           *w64, act)
         nl = rows if layout == "padded" else int(rt["offsets"][-1])
-        assert_close(host(y)[:nl], ref["y_disp"][:nl], "bf16", f"{tiles} y")
-        assert_close(host(dx)[:nl], rdx[:nl], "bf16", f"{tiles} dx")
-        assert_close(host(dw1), rdw1, "bf16", f"{tiles} dw1")
-        assert_close(host(dw2), rdw2, "bf16", f"{tiles} dw2")
+        assert_close(host(y)[:nl], ref["y_disp"][:nl], "bf16", f"{tiles} {order} y")
+        assert_close(host(dx)[:nl], rdx[:nl], "bf16", f"{tiles} {order} dx")
+        assert_close(host(dw1), rdw1, "bf16", f"{tiles} {order} dw1")
+        assert_close(host(dw2), rdw2, "bf16", f"{tiles} {order} dw2")
     names = [n for n in ("h", "a", "y", "dx", "dw1", "dw3", "dw2") if n != "dw3" or act == "swiglu"]
-    for name, p, q in zip(names, out["wide"], out["narrow"]):
-        assert torch.equal(p, q), name
+    first = out[("wide", "split")]
+    for key, got in out.items():
+        for name, p, q in zip(names, first, got):
+            assert torch.equal(p, q), (key, name)
 
 
 @pytest.mark.parametrize("T,M,E,k", [(3000, 520, 64, 6), (2000, 520, 20, 4), (9000, 1000, 3, 2),
