@@ -11,6 +11,7 @@ import oracle
 from gpu_helpers import (assert_close, dev, f64_inputs, host, load_layer, near_tie_check,
                          need_gpu, oracle_for_layer)
 from moe_inputs import get_config, make_inputs
+from paper_2510_00207_amd import _lib as L
 
 pytestmark = pytest.mark.gpu
 
@@ -113,6 +114,32 @@ def test_layer_chunks(R):
     print(f"[layer] chunks R={R}", flush=True)
     layer, inp = run_layer(cfg, "packed", R=R)
     check_against_oracle(cfg, "packed", layer, inp, R)
+
+
+@pytest.mark.parametrize("order", ["split", "joined"])
+@pytest.mark.parametrize("name,R", [("fine_s", 4), ("balanced_m", 1)])
+@pytest.mark.parametrize("layout", ["packed", "padded"])
+def test_layer_tile_orders(name, R, layout, order):
+    """The layer with the grouped GEMM's row tiles in either order (the
+    light tiles after every heavy one, or walked with their expert's heavy
+    ones): every step matches the oracle, and the two orders give
+    bit-identical results. fine_s has only light row tiles per chunk
+    (~24 rows per expert), balanced_m experts of ~512 rows with and
+    without a short third tile."""
+    need_gpu()
+    cfg = CASES[name] if name in CASES else get_config("balanced", T=2048, M=256, H=416)
+    print(f"[layer] tile order {order} {name} {layout} R={R}", flush=True)
+    try:
+        L.flowmoe_set_tile_order(order)
+        layer, inp = run_layer(cfg, layout, R=R)
+        check_against_oracle(cfg, layout, layer, inp, R)
+        other = "joined" if order == "split" else "split"
+        L.flowmoe_set_tile_order(other)
+        layer2, _ = run_layer(cfg, layout, R=R)
+    finally:
+        L.flowmoe_set_tile_order("auto")
+    for nm in ("y", "dx", "dw_gate", "dw1", "dw2", "x_disp", "dx_disp"):
+        assert torch.equal(getattr(layer, nm), getattr(layer2, nm)), nm
 
 
 @pytest.mark.parametrize("R", [2, 4])
