@@ -411,16 +411,20 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
           store8(C1 + g * p.ldc1 + n, a);
         }
       } else if constexpr (MODE == MODE_KSUM) {  // fp32 weight gradient, C0 | C1 split at nsplit
-        constexpr int G8 = WN / 8;
-        constexpr int PER = 64 * G8 / 64;
-        constexpr int PB = PER >= 4 ? 4 : PER;  // items per batch of accumulation loads
+        // 16-byte items of 4 columns, WN / 4 to a staged row: a row's WN * 4
+        // bytes are written by consecutive lanes, so every store instruction
+        // writes whole 128-byte lines (of 64 / (WN / 4) rows); items of 8
+        // columns had left a 16-byte gap between the lanes of each store
+        constexpr int G4 = WN / 4;
+        constexpr int PER = 64 * G4 / 64;
+        constexpr int PB = PER >= 8 ? 8 : PER;  // items per batch of accumulation loads
         float* D0 = static_cast<float*>(p.C0);
         float* D1 = static_cast<float*>(p.C1);
         auto dst_of = [&](int it, bool& ok) {
           const int item = it * 64 + lane;
-          const int rr = item / G8, c8 = item % G8;
+          const int rr = item / G4, c4 = item % G4;
           const int m = mt * BM + wm * WM + hf * 64 + rr;
-          const int n = n0 + wn * WN + c8 * 8;
+          const int n = n0 + wn * WN + c4 * 4;
           ok = m < p.Mdim && n < p.N;  // N and nsplit are multiples of 8
           return (n < p.nsplit) ? D0 + (long)e * p.c_estride + (long)m * p.ldc + n
                                 : D1 + (long)e * p.c_estride + (long)m * p.ldc + (n - p.nsplit);
@@ -429,13 +433,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
         for (int b0 = 0; b0 < PER; b0 += PB) {
           // accumulation: the batch's old values are all loaded before any
           // store (from clamped addresses), one memory round trip per batch
-          Raw8f old[PB];
+          float4 old[PB];
           if (p.accumulate) {
 #pragma unroll
             for (int i = 0; i < PB; ++i) {
               bool ok;
               float* d = dst_of(b0 + i, ok);
-              old[i] = raw8_load(ok ? d : D0);
+              old[i] = *reinterpret_cast<const float4*>(ok ? d : D0);
             }
           }
 #pragma unroll
@@ -445,15 +449,14 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, floatx16 (&ac
             float* dst = dst_of(it, ok);
             if (!ok) continue;
             const int item = it * 64 + lane;
-            float v[8];
-            read8(item / G8, item % G8, v);
+            float4 v = *reinterpret_cast<const float4*>(stage + sidx(item / G4, item % G4));
             if (p.accumulate) {
-              float o[8];
-              raw8_f32(old[i], o);
-#pragma unroll
-              for (int q = 0; q < 8; ++q) v[q] += o[q];
+              v.x += old[i].x;
+              v.y += old[i].y;
+              v.z += old[i].z;
+              v.w += old[i].w;
             }
-            store8(dst, v);
+            *reinterpret_cast<float4*>(dst) = v;
           }
         }
       } else {
