@@ -116,6 +116,18 @@ def test_layer_chunks(R):
     check_against_oracle(cfg, "packed", layer, inp, R)
 
 
+def test_layer_many_chunks():
+    """R = 70 chunks of 16 tokens: the weight-gradient GEMMs reduce over 70
+    row segments per expert (the first 64 segments' ranges are loaded up
+    front, one lane each, the later ones one by one), every step against
+    the oracle."""
+    need_gpu()
+    cfg = get_config("balanced", T=70 * 16, M=128, H=96)
+    print("[layer] many chunks R=70", flush=True)
+    layer, inp = run_layer(cfg, "packed", R=70)
+    check_against_oracle(cfg, "packed", layer, inp, 70)
+
+
 @pytest.mark.parametrize("order", ["split", "joined"])
 @pytest.mark.parametrize("name,R", [("fine_s", 4), ("balanced_m", 1)])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
