@@ -53,6 +53,9 @@ def parse():
     for dim, typ in (("T", int), ("M", int), ("H", int), ("E", int), ("k", int), ("f", float)):
         ap.add_argument(f"--{dim}", type=typ, default=None, help=f"override the workload's {dim}")
     ap.add_argument("--one-stream", action="store_true", help="serial schedule on one stream")
+    ap.add_argument("--tile-order", default="auto", choices=("auto", "split", "joined"),
+                    help="grouped-GEMM row-tile order (light tiles after every heavy one, or "
+                         "walked with their expert's heavy ones)")
     ap.add_argument("--tiles", default="auto", choices=("auto", "wide", "narrow"),
                     help="grouped-GEMM tile shape")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -282,6 +285,7 @@ def main():
         build.build(verbose=False)
     L.load()
     L.flowmoe_set_gemm_tiles(a.tiles)
+    L.flowmoe_set_tile_order(a.tile_order)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
 
@@ -524,6 +528,7 @@ def main():
                          f"{'; AT_r with attention: ' + attention['shape'] if attention else ''}"),
             "T": cfg.T, "M": cfg.M, "H": cfg.H, "E": cfg.E, "k": cfg.k, "f": cfg.f,
             "C": layer.C, "R": R, "act": cfg.act, "layout": a.layout, "gate": cfg.gate, "tiles": a.tiles,
+            "tile_order": a.tile_order,
             "expert_bias": cfg.expert_bias,
             "kept_rows": kept,
         },
