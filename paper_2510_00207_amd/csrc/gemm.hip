@@ -802,12 +802,12 @@ __device__ __forceinline__ u32x4 make_rsrc(const void* base, long bytes) {
 }
 
 // One wave: 64 x 16 bytes from the buffer (per-lane byte offset voff) into
-// the 1 KB LDS block at lds_block, lane-ordered. Issued as inline assembly so
+// the 1 KB LDS block at LDS byte address m0v (wave-uniform, computed in
+// scalar registers: a vector-to-scalar move per load had put a dependent
+// chain in front of every load), lane-ordered. Issued as inline assembly so
 // that the compiler does not pair it with the LDS reads of other stages: the
 // kernel orders them itself with s_waitcnt vmcnt and barriers.
-__device__ __forceinline__ void dma16(u32x4 d, char* lds_block, unsigned voff) {
-  const unsigned m0v =
-      __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_void_t*)lds_block);
+__device__ __forceinline__ void dma16(u32x4 d, unsigned m0v, unsigned voff) {
   // the descriptor is wave-uniform; say so, so that it sits in scalar registers
   d.x = __builtin_amdgcn_readfirstlane(d.x);
   d.y = __builtin_amdgcn_readfirstlane(d.y);
@@ -881,6 +881,10 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
+  // the LDS-DMA destinations in scalar registers: the ring's LDS address and
+  // the wave index (both wave-uniform)
+  const unsigned lds0 = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_void_t*)smem);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
 
   // ---- which tile ----
   int e = 0, mt = 0, nt = 0, row0 = 0, rows_e = 0, cnt_e = 0;
@@ -996,23 +1000,23 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
   // Loads of k-tile kt into stage `stage`, in two parts: part 0 takes this
   // wave's first ceil(n / 2) of its n blocks of each operand, part 1 the rest.
   auto issue_part = [&](int kt, int stage, int q) {
-    char* sa = smem + stage * STB;
-    char* sb = sa + A_BYTES;
+    const unsigned sa = lds0 + (unsigned)(stage * STB), sb = sa + A_BYTES;
     const unsigned ka = (unsigned)kt * (unsigned)a_kstep;
     constexpr int HA = (BPA + 1) / 2, HB = (BPB + 1) / 2;
 #pragma unroll
-    for (int i = q ? HA : 0; i < (q ? BPA : HA); ++i) dma16(ra, sa + (wave + NW * i) * 1024, aoff[i] + ka);
+    for (int i = q ? HA : 0; i < (q ? BPA : HA); ++i) dma16(ra, sa + (wave_s + NW * i) * 1024, aoff[i] + ka);
 #pragma unroll
     for (int i = q ? HB : 0; i < (q ? BPB : HB); ++i) {
       if constexpr (B_KC) {
         const int k0 = kt * DBK;
         const bool second = k0 >= p.ksplit;
         const unsigned kb = (unsigned)((second ? k0 - p.ksplit : k0) * 2);
-        dma16(second ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
+        dma16(second ? rb1 : rb0, sb + (wave_s + NW * i) * 1024, boff[i] + kb);
       } else {
         const unsigned kb = (unsigned)kt * (unsigned)b_kstep;
-        // blocks 8..15 (i >= 1, as wave < NW = 8 in the wide tile) hold the W3 panel
-        dma16((DUAL && i >= 1) ? rb1 : rb0, sb + (wave + NW * i) * 1024, boff[i] + kb);
+        // blocks 8..15 hold the W3 panel
+        const int blk = wave_s + NW * i;
+        dma16((DUAL && blk >= 8) ? rb1 : rb0, sb + blk * 1024, boff[i] + kb);
       }
     }
   };
