@@ -1144,27 +1144,38 @@ __global__ __launch_bounds__(NARROW ? 256 : 512, 2) void gemm_dma_kernel(GemmPar
     // second half of iteration kt (its stage was freed by that iteration's
     // barrier), the second in the first half of iteration kt + 1, both before
     // the wait that needs them (iteration kt + NST - 1).
-    for (int kt = 0; kt + 1 < nk; ++kt) {
+    // Iteration kt of the ring. In the steady state (1 <= kt < nk - NST)
+    // every load exists and the wait always leaves the loads of NST - 2
+    // tiles in flight: that instance has no branches (a branch per
+    // iteration for the wait's count and the loads' bounds cost ~2% on the
+    // large layer).
+    auto iter = [&](int kt, auto steady_c) {
+      constexpr bool S = decltype(steady_c)::value == 1;
       const int stage = kt % NST;
       // step 1 of tile kt is read while step 0 runs; second part of tile kt + NST - 1
       half_step(
           0, [&] { read_frags(stage, 1, 1); },
           [&] {
             const int tl = kt + NST - 1;
-            if (tl >= NST && tl < nk) issue_part(tl, tl % NST, 1);
+            if (S || (tl >= NST && tl < nk)) issue_part(tl, tl % NST, 1);
           });
       // this wave's reads of tile kt are done (lgkmcnt 0) and its loads of
       // tile kt + 1 have landed; after the barrier every wave's have
-      wait_tile(kt + 1, NST - 2);
+      if constexpr (S) wait_vm_lgkm0<(NST - 2) * LPT>();
+      else wait_tile(kt + 1, NST - 2);
       barrier();
       // step 0 of tile kt + 1 is read while step 1 of tile kt runs; first part
       // of tile kt + NST into the stage tile kt leaves
       half_step(
           1, [&] { read_frags((kt + 1) % NST, 0, 0); },
           [&] {
-            if (kt + NST < nk) issue_part(kt + NST, stage, 0);
+            if (S || kt + NST < nk) issue_part(kt + NST, stage, 0);
           });
-    }
+    };
+    int kt = 0;
+    if (nk > 1) iter(kt++, IntC<0>{});
+    for (; kt + NST < nk; ++kt) iter(kt, IntC<1>{});
+    for (; kt + 1 < nk; ++kt) iter(kt, IntC<0>{});
     if (nk > 0) {
       read_frags((nk - 1) % NST, 1, 1);
       mfma_rows(0, 0, FML);
