@@ -419,6 +419,66 @@ def test_expert_ffn_fwd_bwd(dtype, act, layout, MHT, biased, gemm_tiles):
         assert torch.equal(db["db2"], 2 * db2b)
 
 
+@pytest.mark.parametrize("M", [32, 64, 96, 160, 192])
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+def test_expert_ffn_ring_depths(act, M, gemm_tiles):
+    """Short reductions on the LDS-streaming GEMM (wide 256 x 256 tiles, a
+    4-stage ring of 32-deep k-tiles): K = M of the first GEMM and of the
+    input-gradient GEMM gives 1, 2, 3, 5 and 6 k-tiles, K = H = 96 and
+    2H = 192 give 3 and 6, and the weight gradients reduce over expert row
+    counts of 1 to 6 k-tiles (ragged ones among them): every prologue-only,
+    partly steady and steady ring walk, each against the oracle."""
+    need_gpu()
+    gemm_tiles("wide")
+    rng = np.random.default_rng(17)
+    E, H = 5, 96
+    cnt = np.array([32, 64, 95, 150, 192])
+    C = int(cnt.max())
+    T = int(cnt.sum())
+    idx = np.repeat(np.arange(E), cnt)[:, None]
+    rt = oracle.route(idx, E, C, "packed")
+    cfg = get_config("balanced", T=T, M=M, H=H, E=E, k=1, dtype="bf16", act=act, seed=23)
+    inp = make_inputs(cfg)
+    d = dev()
+    x_disp64 = oracle.dispatch(as_f64(inp["x"]), rt["row_src"], 1)
+    rows = rt["rows"]
+    x_disp = torch.from_numpy(x_disp64).to(d).to(torch.bfloat16)
+    counts = torch.from_numpy(rt["counts"].astype(np.int32)).to(d)
+    offsets = torch.from_numpy(rt["offsets"].astype(np.int32)).to(d)
+    w1, w2 = to_torch(inp["w1"], d), to_torch(inp["w2"], d)
+    w3 = to_torch(inp["w3"], d) if act == "swiglu" else None
+    HW = 2 * H if act == "swiglu" else H
+    h_save = torch.full((rows, HW), 5.0, dtype=torch.bfloat16, device=d)
+    a_save = torch.full((rows, H), 5.0, dtype=torch.bfloat16, device=d)
+    y_disp = torch.full((rows, M), 5.0, dtype=torch.bfloat16, device=d)
+    s = _shape(T, M, H, E, 1, C, "bf16", act, "packed")
+    L.flowmoe_expert_ffn(s, x_disp, counts, offsets, w1, w3, w2, h_save, a_save, y_disp)
+    w64 = {kk: (None if inp[kk] is None else as_f64(inp[kk])) for kk in ("w1", "w3", "w2")}
+    ref = oracle.expert_ffn(x_disp64, rt["counts"], rt["offsets"], w64["w1"], w64["w3"], w64["w2"], act)
+    dy_t = torch.from_numpy(rng.standard_normal((rows, M))).to(d).to(torch.bfloat16)
+    dy64 = host(dy_t)
+    dx_disp = torch.full((rows, M), 5.0, dtype=torch.bfloat16, device=d)
+    dw1 = torch.full((E, M, H), 9.0, device=d)
+    dw3 = torch.full((E, M, H), 9.0, device=d) if act == "swiglu" else None
+    dw2 = torch.full((E, H, M), 9.0, device=d)
+    nws = L.flowmoe_workspace_bytes(s, L.WS_FFN_BWD)
+    ws = torch.empty(max(1, nws), dtype=torch.uint8, device=d)
+    L.flowmoe_expert_ffn_bwd(s, dy_t, x_disp, h_save, a_save, counts, offsets, w1, w3, w2, dx_disp,
+                             dw1, dw3, dw2, 0, ws, nws)
+    torch.cuda.synchronize()
+    rdx, rdw1, rdw3, rdw2 = oracle.expert_ffn_bwd(dy64, x_disp64, ref, rt["counts"], rt["offsets"],
+                                                  w64["w1"], w64["w3"], w64["w2"], act)
+    hw = ref["h1"] if act == "gelu" else np.concatenate([ref["h1"], ref["h3"]], axis=1)
+    assert_close(host(h_save), hw, "bf16", "h_save")
+    assert_close(host(a_save), ref["a"], "bf16", "a_save")
+    assert_close(host(y_disp), ref["y_disp"], "bf16", "y_disp")
+    assert_close(host(dx_disp), rdx, "bf16", "dx_disp")
+    assert_close(host(dw1), rdw1, "bf16", "dw1")
+    assert_close(host(dw2), rdw2, "bf16", "dw2")
+    if act == "swiglu":
+        assert_close(host(dw3), rdw3, "bf16", "dw3")
+
+
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("layout", ["packed", "padded"])
 def test_gemm_tile_shapes_agree(act, layout, gemm_tiles, tile_order):
