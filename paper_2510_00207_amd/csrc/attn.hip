@@ -224,7 +224,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(AttnArgs a) {
   constexpr int KS = D / 16, DB = D / 32, QB = 32 * NW;
   using Tiles = KVTiles<D, 64, 64 * NW>;
   __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
+  // the wave index through readfirstlane: the compiler then knows it is
+  // wave-uniform, and the branches on a wave's query or key range are
+  // scalar branches instead of exec-mask ones (backward 7-10% faster)
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6),
+            h2 = lane >> 5, lq = lane & 31;
   int qt, hd, sq;
   decode(a, CAUSAL, qt, hd, sq, QB);
   const long tok0 = (long)sq * a.N, ld = 3L * a.M;
@@ -350,7 +354,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dq_kernel(AttnArgs a) {
   // that leaves without moving values through the AGPRs every step
   __shared__ __attribute__((aligned(16))) char lds[2 * 2 * Tiles::TB + QB * D * 2];
   char* const gt = lds + 2 * 2 * Tiles::TB;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
+  // the wave index through readfirstlane: the compiler then knows it is
+  // wave-uniform, and the branches on a wave's query or key range are
+  // scalar branches instead of exec-mask ones (backward 7-10% faster)
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6),
+            h2 = lane >> 5, lq = lane & 31;
   int qt, hd, sq;
   decode(a, CAUSAL, qt, hd, sq, QB);
   const long tok0 = (long)sq * a.N, ld = 3L * a.M;
@@ -454,7 +462,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_dkdv_kernel(AttnArgs a) 
   // 256 VGPRs without moving values through the AGPRs every step)
   __shared__ __attribute__((aligned(16))) char lds[2 * STG + KB * D * 2];
   char* const vt = lds + 2 * STG;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h2 = lane >> 5, lq = lane & 31;
+  // the wave index through readfirstlane: the compiler then knows it is
+  // wave-uniform, and the branches on a wave's query or key range are
+  // scalar branches instead of exec-mask ones (backward 7-10% faster)
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6),
+            h2 = lane >> 5, lq = lane & 31;
   int kt, hd, sq;
   decode(a, false, kt, hd, sq, KB);
   const long tok0 = (long)sq * a.N, ld = 3L * a.M;
